@@ -1,0 +1,208 @@
+/*
+ * rnnt_pruned.h - C ABI of the MI355X (gfx950) pruned RNN-T loss library.
+ *
+ * Implements the computation of "Pruned RNN-T for fast, memory-efficient ASR
+ * training" (Kuang et al., arXiv 2206.13236) as four stages:
+ *
+ *   1. rnnt_simple_loss        trivial joiner (Sec. 3.1, Eqs. (5)-(6)) and the
+ *                              full-lattice recursion (Sec. 2, Eqs. (1)-(4));
+ *                              yields the occupation counts of Sec. 3.2.2 and,
+ *                              optionally, the gradients w.r.t. am and lm.
+ *   2. rnnt_prune_ranges       locally optimal pruning bounds, Eq. (8), made
+ *                              consistent with Eqs. (9)-(10) (Sec. 3.2.2).
+ *   3. rnnt_pruned_joiner      the full non-linear joiner evaluated only at the
+ *                              pruned (t, u) pairs (Sec. 3.2, Fig. 1(b)),
+ *                              reduced to target/blank log-probs.
+ *      rnnt_pruned_loss        the same recursion on the pruned lattice, whose
+ *                              entries outside p_t <= u < p_t + S are -inf.
+ *      rnnt_pruned_joiner_backward
+ *                              the pruned loss's gradients w.r.t. the joiner
+ *                              inputs and parameters.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Every array pointer is a DEVICE pointer to a dense, row-major array. The
+ *   caller owns all memory; the library never allocates or frees device
+ *   memory and keeps no state between calls.
+ * - Every call only enqueues kernels on `stream` (a hipStream_t; NULL = the
+ *   null stream) and returns without synchronising.
+ * - Scalars and pointers are checked on the host before any launch; a failed
+ *   check returns a non-zero status and enqueues nothing. The message is
+ *   available from rnnt_last_error() (thread-local).
+ * - Data-dependent problems never fail the call. An utterance whose lengths
+ *   are out of range (t_len[n] < 1 or > T, u_len[n] < 0 or > U) or whose
+ *   symbols are outside [0, V) gets a NaN loss; indices are clamped so every
+ *   memory access stays in bounds.
+ * - Lattice layout: T frames x (U+1) token positions. symbols[n, u] is
+ *   y_{u+1}; y_0 is the beginning-of-sentence blank (Sec. 2). `blank` may
+ *   equal a symbol value (then that symbol's and the blank's log-probs
+ *   coincide, which is well defined).
+ * - Losses are per utterance: loss[n] = -log P(y | x) (minus the total
+ *   log-probability of Sec. 2). Gradients are gradients of
+ *   sum_n scale[n] * loss[n]; scale may be NULL (all ones).
+ * - Entries outside t < t_len[n], u <= u_len[n] are written with defined
+ *   fills: 0 for occupations and gradients, -inf for log-probs.
+ */
+#ifndef RNNT_PRUNED_H
+#define RNNT_PRUNED_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes. */
+#define RNNT_OK 0
+#define RNNT_EINVAL 1        /* a scalar or pointer argument is invalid            */
+#define RNNT_EWORKSPACE 2    /* workspace missing or smaller than the query result */
+#define RNNT_EUNSUPPORTED 3  /* a size outside what the kernels support           */
+#define RNNT_EHIP 4          /* a HIP runtime call failed                           */
+
+/* Element types of the joiner inputs (enc, dec, W, bias). */
+#define RNNT_F32 0
+#define RNNT_BF16 1
+
+/* Limits of this build. */
+#define RNNT_MAX_U 1023      /* U + 1 <= 1024 lattice rows                          */
+#define RNNT_MAX_S 32        /* pruning width                                       */
+
+typedef struct rnnt_batch {
+  int32_t N;                 /* utterances                                         */
+  int32_t T;                 /* padded frame count (max t_len)                      */
+  int32_t U;                 /* padded token count (max u_len); lattice has U+1 rows */
+  const int32_t* t_len;      /* [N] device, 1 <= t_len[n] <= T                      */
+  const int32_t* u_len;      /* [N] device, 0 <= u_len[n] <= U                      */
+  const int32_t* symbols;    /* [N, U] device, symbols[n, u] = y_{u+1} in [0, V)    */
+  int32_t blank;             /* blank id in [0, V) (0 in the paper, Sec. 2)         */
+} rnnt_batch;
+
+/* ABI version of this header (bumped on any signature change). */
+int rnnt_abi_version(void);
+
+/* Message for the last non-OK status returned on this thread ("" if none). */
+const char* rnnt_last_error(void);
+
+/* ------------------------------------------------------------------------ */
+/* Stage 1-2: trivial joiner + full-lattice forward-backward                 */
+/* ------------------------------------------------------------------------ */
+
+/* Workspace bytes needed by rnnt_simple_loss for these sizes (pure function of
+ * the arguments; 0 on invalid sizes). */
+size_t rnnt_simple_loss_workspace_size(int32_t N, int32_t T, int32_t U, int32_t V);
+
+/* Simple (trivial-joiner) loss of Sec. 3.1 and its occupation counts.
+ *
+ * am [N, T, V] fp32   L_enc(t, v): un-normalised logits from the encoder side.
+ * lm [N, U+1, V] fp32 L_dec(u, v): un-normalised logits from the decoder side.
+ * The joiner is L(t,u,v) = am[t,v] + lm[u,v] - L_normalizer(t,u) (Eq. (5))
+ * with L_normalizer = log sum_v exp(am[t,v] + lm[u,v]) (Eq. (6)), evaluated as
+ * a max-shifted matrix product.
+ *
+ * Outputs:
+ *   loss   [N]          fp32, required.
+ *   px_occ [N, T, U+1]  fp32, required: dL_tot/dy(t,u), the occupation of the
+ *                       vertical (symbol) transition leaving (t,u), in [0,1].
+ *   py_occ [N, T, U+1]  fp32, required: dL_tot/dblank(t,u).
+ *   px, py [N, T, U+1]  fp32, nullable: the log-probs y(t,u), blank(t,u)
+ *                       (Eqs. (1)-(2)); px[.., U_n..] = -inf.
+ *   am_grad [N, T, V], lm_grad [N, U+1, V]  fp32, nullable: gradients of
+ *                       sum_n scale[n] * loss[n].
+ *   scale  [N] fp32, nullable (all ones); only read when a gradient is asked.
+ * workspace: device buffer of at least rnnt_simple_loss_workspace_size() bytes,
+ *   256-byte aligned.
+ */
+int rnnt_simple_loss(const rnnt_batch* batch, int32_t V,
+                     const float* am, const float* lm, const float* scale,
+                     float* loss, float* px_occ, float* py_occ,
+                     float* px, float* py, float* am_grad, float* lm_grad,
+                     void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Stage 3: pruning bounds (Sec. 3.2.2)                                      */
+/* ------------------------------------------------------------------------ */
+
+/* ranges [N, T, S] int32 output: ranges[n,t,s] = p_t + s for t < t_len[n] and
+ * ranges[n,t,s] = s for padding frames. p_t is the argmax over p in [0, P],
+ * P = max(0, U_n - S + 1), of Eq. (8):
+ *     -px_occ(t, p-1) + py_occ(t, p) + ... + py_occ(t, p+S-1),
+ * evaluated in fp32 left to right (y'(t,-1) = 0; slots above U_n add 0; ties
+ * to the smallest p; NaN never wins). The raw bounds are clamped to the
+ * envelope [P - (S-1)(T_n-1-t), min(P, (S-1)t)] and then made monotone
+ * (Eq. (9)) and skip-free (Eq. (10)) by the suffix-minimum / reflection
+ * procedure of the commented-out part of Sec. 3.2.2 of the paper's source.
+ * For identical occupation inputs the result is bit-identical to a CPU fp32
+ * evaluation in that order. 1 <= S <= RNNT_MAX_S. No workspace.
+ */
+int rnnt_prune_ranges(const rnnt_batch* batch, int32_t S,
+                      const float* px_occ, const float* py_occ,
+                      int32_t* ranges, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Stage 4: full joiner on the pruned pairs, pruned recursion, backward      */
+/* ------------------------------------------------------------------------ */
+
+/* Workspace bytes for rnnt_pruned_joiner. */
+size_t rnnt_pruned_joiner_workspace_size(int32_t N, int32_t T, int32_t S, int32_t J,
+                                         int32_t V, int32_t dtype);
+
+/* Full joiner at u = ranges[n,t,s] only (Sec. 3.2): h = tanh(enc[n,t] + dec[n,u]),
+ * logits = h W + bias, lse = log sum_v exp(logits). The [N, T, S, V] logits are
+ * never stored: each (row, 64-column slice) keeps a partial (max, sum exp)
+ * and the target and blank logits.
+ *
+ * enc [N, T, J], dec [N, U+1, J], W [J, V], bias [V] (nullable = 0): dtype
+ *   RNNT_F32 (float) or RNNT_BF16 (bfloat16 bits); accumulation is fp32.
+ * ranges [N, T, S] int32 from rnnt_prune_ranges (u values above u_len[n] mark
+ *   absent slots).
+ * Outputs, fp32 [N, T, S]: px = logits[y_{u+1}] - lse (u < U_n, else -inf),
+ *   py = logits[blank] - lse, lse (0 for absent slots).
+ */
+int rnnt_pruned_joiner(const rnnt_batch* batch, int32_t S, int32_t J, int32_t V, int32_t dtype,
+                       const void* enc, const void* dec, const void* W, const void* bias,
+                       const int32_t* ranges, float* px, float* py, float* lse,
+                       void* workspace, size_t workspace_bytes, void* stream);
+
+/* Workspace bytes for rnnt_pruned_loss. */
+size_t rnnt_pruned_loss_workspace_size(int32_t N, int32_t T, int32_t S);
+
+/* The recursion of Eq. (3) on the pruned lattice (Sec. 3.2): entries outside
+ * p_t <= u < p_t + S are -inf. px, py [N, T, S] fp32 are the band log-probs
+ * (from rnnt_pruned_joiner). Outputs: loss [N] (+inf when no complete path
+ * exists in the band, then occupations are 0); px_occ, py_occ [N, T, S]
+ * (nullable) band occupations dL_tot/dpx, dL_tot/dpy in [0,1].
+ */
+int rnnt_pruned_loss(const rnnt_batch* batch, int32_t S,
+                     const float* px, const float* py, const int32_t* ranges,
+                     float* loss, float* px_occ, float* py_occ,
+                     void* workspace, size_t workspace_bytes, void* stream);
+
+/* Workspace bytes for rnnt_pruned_joiner_backward. */
+size_t rnnt_pruned_joiner_backward_workspace_size(int32_t N, int32_t T, int32_t U, int32_t S,
+                                                  int32_t J, int32_t V, int32_t dtype);
+
+/* Gradients of sum_n scale[n] * pruned_loss[n] through the log-softmax, the
+ * projection, tanh and the sum enc + dec. The logits are recomputed in row
+ * chunks; d(logits) is held for one chunk at a time and never for the whole
+ * [N, T, S, V] at once unless it fits the chunk.
+ *
+ * lse, px_occ, py_occ [N, T, S]: from rnnt_pruned_joiner / rnnt_pruned_loss.
+ * Outputs (fp32): enc_grad [N, T, J], dec_grad [N, U+1, J] (required);
+ *   W_grad [J, V], bias_grad [V] (nullable);
+ *   logits_grad [N, T, S, V] (nullable; debugging aid for small shapes).
+ * Reductions run in a fixed order: results are bitwise reproducible.
+ */
+int rnnt_pruned_joiner_backward(const rnnt_batch* batch, int32_t S, int32_t J, int32_t V,
+                                int32_t dtype, const void* enc, const void* dec,
+                                const void* W, const void* bias, const int32_t* ranges,
+                                const float* lse, const float* px_occ, const float* py_occ,
+                                const float* scale, float* enc_grad, float* dec_grad,
+                                float* W_grad, float* bias_grad, float* logits_grad,
+                                void* workspace, size_t workspace_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RNNT_PRUNED_H */

@@ -1,0 +1,282 @@
+"""Pruned RNN-T loss (Kuang et al., arXiv 2206.13236) on MI355X (gfx950).
+
+Every stage runs in the hand-written HIP kernels of ``librnnt_pruned.so``;
+this package only marshals arguments through its C ABI (ctypes). PyTorch
+provides device memory and the current stream. The functions named like the
+C entry points (``rnnt_simple_loss`` ...) map one-to-one onto them; the
+``PrunedRnntLoss`` helper chains the four stages the way the paper's training
+step does (Sec. 3.3: loss = pruned + 0.5 * simple).
+"""
+from __future__ import annotations
+
+import ctypes
+from typing import Optional
+
+import torch
+
+from ._native import (RNNT_BF16, RNNT_EHIP, RNNT_EINVAL, RNNT_EUNSUPPORTED, RNNT_EWORKSPACE,  # noqa: F401
+                      RNNT_F32, RNNT_OK, RnntBatch, RnntError, check, lib)
+
+__all__ = [
+    "Batch", "RnntError", "rnnt_simple_loss", "rnnt_prune_ranges", "rnnt_pruned_joiner",
+    "rnnt_pruned_loss", "rnnt_pruned_joiner_backward", "simple_loss_workspace_size",
+    "pruned_joiner_workspace_size", "pruned_loss_workspace_size",
+    "pruned_joiner_backward_workspace_size", "PrunedRnntLoss", "RNNT_F32", "RNNT_BF16",
+]
+
+
+def _p(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream) -> ctypes.c_void_p:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    if isinstance(stream, torch.cuda.Stream):
+        stream = stream.cuda_stream
+    return ctypes.c_void_p(int(stream))
+
+
+def _need(t: torch.Tensor, name: str, dtype: torch.dtype, shape: tuple):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be a device (cuda) tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def _ws(nbytes: int, device, workspace: Optional[torch.Tensor]) -> torch.Tensor:
+    if workspace is not None:
+        if workspace.numel() * workspace.element_size() < nbytes:
+            raise ValueError(f"workspace has {workspace.numel()} bytes, {nbytes} needed")
+        return workspace
+    return torch.empty(max(nbytes, 1), dtype=torch.uint8, device=device)
+
+
+def _jdtype(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return RNNT_F32
+    if t.dtype == torch.bfloat16:
+        return RNNT_BF16
+    raise TypeError(f"joiner tensors must be float32 or bfloat16, got {t.dtype}")
+
+
+class Batch:
+    """Device description of a padded batch (the C ``rnnt_batch``).
+
+    t_len [N], u_len [N] and symbols [N, U] are int32 device tensors;
+    symbols[n, u] is y_{u+1}. T and U are the padded maxima.
+    """
+
+    def __init__(self, t_len: torch.Tensor, u_len: torch.Tensor, symbols: torch.Tensor,
+                 T: int, U: int, blank: int = 0):
+        N = int(t_len.shape[0])
+        _need(t_len, "t_len", torch.int32, (N,))
+        _need(u_len, "u_len", torch.int32, (N,))
+        _need(symbols, "symbols", torch.int32, (N, U))
+        self.t_len, self.u_len, self.symbols = t_len, u_len, symbols
+        self.N, self.T, self.U, self.blank = N, int(T), int(U), int(blank)
+        self.device = t_len.device
+        self._c = RnntBatch(self.N, self.T, self.U, t_len.data_ptr(), u_len.data_ptr(),
+                            symbols.data_ptr() if U > 0 else None, self.blank)
+
+    @property
+    def c(self):
+        return ctypes.byref(self._c)
+
+
+# --------------------------------------------------------------------------
+# workspace queries
+# --------------------------------------------------------------------------
+
+def simple_loss_workspace_size(N, T, U, V) -> int:
+    return int(lib().rnnt_simple_loss_workspace_size(N, T, U, V))
+
+
+def pruned_joiner_workspace_size(N, T, S, J, V, dtype) -> int:
+    return int(lib().rnnt_pruned_joiner_workspace_size(N, T, S, J, V, dtype))
+
+
+def pruned_loss_workspace_size(N, T, S) -> int:
+    return int(lib().rnnt_pruned_loss_workspace_size(N, T, S))
+
+
+def pruned_joiner_backward_workspace_size(N, T, U, S, J, V, dtype) -> int:
+    return int(lib().rnnt_pruned_joiner_backward_workspace_size(N, T, U, S, J, V, dtype))
+
+
+# --------------------------------------------------------------------------
+# stage wrappers (same names and argument order as the C ABI)
+# --------------------------------------------------------------------------
+
+def rnnt_simple_loss(batch: Batch, V: int, am: torch.Tensor, lm: torch.Tensor,
+                     scale: Optional[torch.Tensor] = None, loss=None, px_occ=None, py_occ=None,
+                     px=None, py=None, am_grad=None, lm_grad=None, workspace=None, stream=None,
+                     want_logprobs: bool = False, want_grads: bool = False) -> dict:
+    N, T, U = batch.N, batch.T, batch.U
+    dev = batch.device
+    _need(am, "am", torch.float32, (N, T, V))
+    _need(lm, "lm", torch.float32, (N, U + 1, V))
+    f32 = dict(dtype=torch.float32, device=dev)
+    loss = torch.empty(N, **f32) if loss is None else loss
+    px_occ = torch.empty(N, T, U + 1, **f32) if px_occ is None else px_occ
+    py_occ = torch.empty(N, T, U + 1, **f32) if py_occ is None else py_occ
+    if want_logprobs and px is None:
+        px, py = torch.empty(N, T, U + 1, **f32), torch.empty(N, T, U + 1, **f32)
+    if want_grads and am_grad is None:
+        am_grad, lm_grad = torch.empty(N, T, V, **f32), torch.empty(N, U + 1, V, **f32)
+    if scale is not None:
+        _need(scale, "scale", torch.float32, (N,))
+    ws = _ws(simple_loss_workspace_size(N, T, U, V), dev, workspace)
+    check(lib().rnnt_simple_loss(batch.c, V, _p(am), _p(lm), _p(scale), _p(loss), _p(px_occ),
+                                 _p(py_occ), _p(px), _p(py), _p(am_grad), _p(lm_grad), _p(ws),
+                                 ws.numel(), _stream(stream)))
+    return {"loss": loss, "px_occ": px_occ, "py_occ": py_occ, "px": px, "py": py,
+            "am_grad": am_grad, "lm_grad": lm_grad}
+
+
+def rnnt_prune_ranges(batch: Batch, S: int, px_occ: torch.Tensor, py_occ: torch.Tensor,
+                      ranges: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    N, T, U = batch.N, batch.T, batch.U
+    _need(px_occ, "px_occ", torch.float32, (N, T, U + 1))
+    _need(py_occ, "py_occ", torch.float32, (N, T, U + 1))
+    ranges = torch.empty(N, T, S, dtype=torch.int32, device=batch.device) if ranges is None else ranges
+    check(lib().rnnt_prune_ranges(batch.c, S, _p(px_occ), _p(py_occ), _p(ranges), _stream(stream)))
+    return ranges
+
+
+def rnnt_pruned_joiner(batch: Batch, S: int, enc: torch.Tensor, dec: torch.Tensor, W: torch.Tensor,
+                       bias: Optional[torch.Tensor], ranges: torch.Tensor, px=None, py=None, lse=None,
+                       workspace=None, stream=None) -> dict:
+    N, T, U = batch.N, batch.T, batch.U
+    J, V = int(W.shape[0]), int(W.shape[1])
+    dt = _jdtype(W)
+    _need(enc, "enc", W.dtype, (N, T, J))
+    _need(dec, "dec", W.dtype, (N, U + 1, J))
+    if bias is not None:
+        _need(bias, "bias", W.dtype, (V,))
+    _need(ranges, "ranges", torch.int32, (N, T, S))
+    f32 = dict(dtype=torch.float32, device=batch.device)
+    px = torch.empty(N, T, S, **f32) if px is None else px
+    py = torch.empty(N, T, S, **f32) if py is None else py
+    lse = torch.empty(N, T, S, **f32) if lse is None else lse
+    ws = _ws(pruned_joiner_workspace_size(N, T, S, J, V, dt), batch.device, workspace)
+    check(lib().rnnt_pruned_joiner(batch.c, S, J, V, dt, _p(enc), _p(dec), _p(W), _p(bias), _p(ranges),
+                                   _p(px), _p(py), _p(lse), _p(ws), ws.numel(), _stream(stream)))
+    return {"px": px, "py": py, "lse": lse}
+
+
+def rnnt_pruned_loss(batch: Batch, S: int, px: torch.Tensor, py: torch.Tensor, ranges: torch.Tensor,
+                     loss=None, px_occ=None, py_occ=None, workspace=None, stream=None,
+                     want_occupations: bool = True) -> dict:
+    N, T = batch.N, batch.T
+    _need(px, "px", torch.float32, (N, T, S))
+    _need(py, "py", torch.float32, (N, T, S))
+    _need(ranges, "ranges", torch.int32, (N, T, S))
+    f32 = dict(dtype=torch.float32, device=batch.device)
+    loss = torch.empty(N, **f32) if loss is None else loss
+    if want_occupations and px_occ is None:
+        px_occ, py_occ = torch.empty(N, T, S, **f32), torch.empty(N, T, S, **f32)
+    ws = _ws(pruned_loss_workspace_size(N, T, S), batch.device, workspace)
+    check(lib().rnnt_pruned_loss(batch.c, S, _p(px), _p(py), _p(ranges), _p(loss), _p(px_occ), _p(py_occ),
+                                 _p(ws), ws.numel(), _stream(stream)))
+    return {"loss": loss, "px_occ": px_occ, "py_occ": py_occ}
+
+
+def rnnt_pruned_joiner_backward(batch: Batch, S: int, enc, dec, W, bias, ranges, lse, px_occ, py_occ,
+                                scale=None, enc_grad=None, dec_grad=None, W_grad=None, bias_grad=None,
+                                logits_grad=None, workspace=None, stream=None, want_param_grads=True,
+                                want_logits_grad=False) -> dict:
+    N, T, U = batch.N, batch.T, batch.U
+    J, V = int(W.shape[0]), int(W.shape[1])
+    dt = _jdtype(W)
+    _need(enc, "enc", W.dtype, (N, T, J))
+    _need(dec, "dec", W.dtype, (N, U + 1, J))
+    for name, t in (("lse", lse), ("px_occ", px_occ), ("py_occ", py_occ)):
+        _need(t, name, torch.float32, (N, T, S))
+    _need(ranges, "ranges", torch.int32, (N, T, S))
+    f32 = dict(dtype=torch.float32, device=batch.device)
+    enc_grad = torch.empty(N, T, J, **f32) if enc_grad is None else enc_grad
+    dec_grad = torch.empty(N, U + 1, J, **f32) if dec_grad is None else dec_grad
+    if want_param_grads and W_grad is None:
+        W_grad, bias_grad = torch.empty(J, V, **f32), torch.empty(V, **f32)
+    if want_logits_grad and logits_grad is None:
+        logits_grad = torch.empty(N, T, S, V, **f32)
+    ws = _ws(pruned_joiner_backward_workspace_size(N, T, U, S, J, V, dt), batch.device, workspace)
+    check(lib().rnnt_pruned_joiner_backward(
+        batch.c, S, J, V, dt, _p(enc), _p(dec), _p(W), _p(bias), _p(ranges), _p(lse), _p(px_occ),
+        _p(py_occ), _p(scale), _p(enc_grad), _p(dec_grad), _p(W_grad), _p(bias_grad), _p(logits_grad),
+        _p(ws), ws.numel(), _stream(stream)))
+    return {"enc_grad": enc_grad, "dec_grad": dec_grad, "W_grad": W_grad, "bias_grad": bias_grad,
+            "logits_grad": logits_grad}
+
+
+class PrunedRnntLoss:
+    """The paper's training loss on one batch: pruned + simple_scale * simple (Sec. 3.3).
+
+    Holds the intermediate tensors and one workspace between calls so that
+    repeated steps on same-shaped batches allocate nothing new. ``step``
+    enqueues the whole path (simple loss and its gradients, pruning bounds,
+    pruned joiner, pruned recursion, joiner backward) on the current stream.
+    """
+
+    def __init__(self, S: int, simple_scale: float = 0.5, pruned_scale: float = 1.0):
+        self.S = int(S)
+        self.simple_scale = float(simple_scale)
+        self.pruned_scale = float(pruned_scale)
+        self._cache = {}
+
+    def _buf(self, key, shape, dtype, device):
+        t = self._cache.get(key)
+        if t is None or tuple(t.shape) != tuple(shape) or t.dtype != dtype or t.device != device:
+            t = torch.empty(shape, dtype=dtype, device=device)
+            self._cache[key] = t
+        return t
+
+    def step(self, batch: Batch, am, lm, enc, dec, W, bias=None, stream=None) -> dict:
+        N, T, U, S = batch.N, batch.T, batch.U, self.S
+        V = int(am.shape[2])
+        J = int(W.shape[0])
+        dev = batch.device
+        dt = _jdtype(W)
+        f32 = torch.float32
+        ws_bytes = max(simple_loss_workspace_size(N, T, U, V),
+                       pruned_joiner_workspace_size(N, T, S, J, V, dt),
+                       pruned_loss_workspace_size(N, T, S),
+                       pruned_joiner_backward_workspace_size(N, T, U, S, J, V, dt))
+        ws = self._buf("ws", (ws_bytes,), torch.uint8, dev)
+        ssc = self._buf("ssc", (N,), f32, dev)
+        psc = self._buf("psc", (N,), f32, dev)
+        if self._cache.get("scales") != (N, self.simple_scale, self.pruned_scale):
+            ssc.fill_(self.simple_scale)
+            psc.fill_(self.pruned_scale)
+            self._cache["scales"] = (N, self.simple_scale, self.pruned_scale)
+        out = rnnt_simple_loss(
+            batch, V, am, lm, ssc, loss=self._buf("sl", (N,), f32, dev),
+            px_occ=self._buf("sgx", (N, T, U + 1), f32, dev), py_occ=self._buf("sgy", (N, T, U + 1), f32, dev),
+            am_grad=self._buf("dam", (N, T, V), f32, dev), lm_grad=self._buf("dlm", (N, U + 1, V), f32, dev),
+            workspace=ws, stream=stream)
+        ranges = rnnt_prune_ranges(batch, S, out["px_occ"], out["py_occ"],
+                                   ranges=self._buf("rng", (N, T, S), torch.int32, dev), stream=stream)
+        jo = rnnt_pruned_joiner(batch, S, enc, dec, W, bias, ranges, px=self._buf("ppx", (N, T, S), f32, dev),
+                                py=self._buf("ppy", (N, T, S), f32, dev), lse=self._buf("lse", (N, T, S), f32, dev),
+                                workspace=ws, stream=stream)
+        pl = rnnt_pruned_loss(batch, S, jo["px"], jo["py"], ranges, loss=self._buf("pl", (N,), f32, dev),
+                              px_occ=self._buf("pgx", (N, T, S), f32, dev),
+                              py_occ=self._buf("pgy", (N, T, S), f32, dev), workspace=ws, stream=stream)
+        jb = rnnt_pruned_joiner_backward(
+            batch, S, enc, dec, W, bias, ranges, jo["lse"], pl["px_occ"], pl["py_occ"], scale=psc,
+            enc_grad=self._buf("denc", (N, T, J), f32, dev), dec_grad=self._buf("ddec", (N, U + 1, J), f32, dev),
+            W_grad=self._buf("dW", (J, V), f32, dev), bias_grad=self._buf("db", (V,), f32, dev),
+            workspace=ws, stream=stream)
+        return {"simple_loss": out["loss"], "pruned_loss": pl["loss"], "ranges": ranges,
+                "am_grad": out["am_grad"], "lm_grad": out["lm_grad"], "enc_grad": jb["enc_grad"],
+                "dec_grad": jb["dec_grad"], "W_grad": jb["W_grad"], "bias_grad": jb["bias_grad"],
+                "simple_px_occ": out["px_occ"], "simple_py_occ": out["py_occ"],
+                "px": jo["px"], "py": jo["py"], "lse": jo["lse"],
+                "pruned_px_occ": pl["px_occ"], "pruned_py_occ": pl["py_occ"]}

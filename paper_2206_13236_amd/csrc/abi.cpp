@@ -1,0 +1,401 @@
+// C ABI of the pruned RNN-T library: argument checks, workspace layout and
+// launch sequencing. Every check runs on the host before any HIP call, so a
+// rejected call enqueues nothing. No entry point allocates, frees or
+// synchronises.
+#include <stdarg.h>
+#include <stdio.h>
+
+#include <string>
+
+#include "kernels.h"
+#include "rnnt_pruned.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+int ok() {
+  g_err.clear();
+  return RNNT_OK;
+}
+
+int hip_status(hipError_t e, const char* where) {
+  if (e == hipSuccess) return ok();
+  return fail(RNNT_EHIP, "%s: %s", where, hipGetErrorString(e));
+}
+
+// Bump allocator over the caller's workspace. With base == nullptr it only
+// measures, so the *_workspace_size queries and the entry points share one
+// layout.
+struct Carve {
+  char* base;
+  size_t off = 0;
+  explicit Carve(void* b) : base(static_cast<char*>(b)) {}
+  template <class T>
+  T* take(size_t n) {
+    off = (off + 255) / 256 * 256;
+    T* p = base ? reinterpret_cast<T*>(base + off) : nullptr;
+    off += n * sizeof(T);
+    return p;
+  }
+};
+
+const long long kI32 = 0x7fffffffll;
+
+int check_batch(const rnnt_batch* b, bool need_symbols_ptr) {
+  if (!b) return fail(RNNT_EINVAL, "batch is NULL");
+  if (b->N < 1) return fail(RNNT_EINVAL, "N must be >= 1 (got %d)", b->N);
+  if (b->T < 1) return fail(RNNT_EINVAL, "T must be >= 1 (got %d)", b->T);
+  if (b->U < 0) return fail(RNNT_EINVAL, "U must be >= 0 (got %d)", b->U);
+  if (b->U > RNNT_MAX_U) return fail(RNNT_EUNSUPPORTED, "U = %d exceeds RNNT_MAX_U = %d", b->U, RNNT_MAX_U);
+  if (!b->t_len || !b->u_len) return fail(RNNT_EINVAL, "t_len and u_len must be device pointers");
+  if (need_symbols_ptr && b->U > 0 && !b->symbols) return fail(RNNT_EINVAL, "symbols is NULL with U > 0");
+  if ((long long)b->N * b->T * (b->U + 1) > kI32) return fail(RNNT_EUNSUPPORTED, "N*T*(U+1) exceeds 2^31-1");
+  return RNNT_OK;
+}
+
+BatchDev to_dev(const rnnt_batch* b) {
+  BatchDev d;
+  d.N = b->N;
+  d.T = b->T;
+  d.U = b->U;
+  d.t_len = b->t_len;
+  d.u_len = b->u_len;
+  d.symbols = b->symbols;
+  d.blank = b->blank;
+  return d;
+}
+
+int ldw_of(int U) { return (U + 1 + 3) / 4 * 4; }
+
+struct SimpleWs {
+  float* m_a;
+  float* m_l;
+  float* Z;
+  float* px;
+  float* py;
+  double* alpha;
+  double* beta;
+  float* Wt;
+  float* ry;
+  float* cx;
+  float* cy;
+  size_t bytes;
+};
+
+SimpleWs simple_layout(void* base, int N, int T, int U) {
+  Carve c(base);
+  SimpleWs w;
+  const size_t NT = (size_t)N * T, NU = (size_t)N * (U + 1), L = NT * (U + 1);
+  w.m_a = c.take<float>(NT);
+  w.m_l = c.take<float>(NU);
+  w.Z = c.take<float>(L);
+  w.px = c.take<float>(L);
+  w.py = c.take<float>(L);
+  w.alpha = c.take<double>(L);
+  w.beta = c.take<double>(L);
+  w.Wt = c.take<float>(NT * ldw_of(U));
+  w.ry = c.take<float>(NT);
+  w.cx = c.take<float>(NU);
+  w.cy = c.take<float>(NU);
+  w.bytes = c.off;
+  return w;
+}
+
+struct JoinerFwdWs {
+  int* frame_off;
+  int4* rowinfo;
+  float2* part;
+  float* tgt;
+  float* blk;
+  size_t bytes;
+};
+
+JoinerFwdWs joiner_fwd_layout(void* base, int N, int T, int S, int V) {
+  Carve c(base);
+  JoinerFwdWs w;
+  const size_t M = (size_t)N * T * S;
+  w.frame_off = c.take<int>((size_t)N + 1);
+  w.rowinfo = c.take<int4>(M);
+  w.part = c.take<float2>(M * joiner_nparts(V));
+  w.tgt = c.take<float>(M);
+  w.blk = c.take<float>(M);
+  w.bytes = c.off;
+  return w;
+}
+
+struct JoinerBwdWs {
+  int* frame_off;
+  int4* rowinfo;
+  void* dl;
+  float* dpre;
+  float* dw_part;
+  float* db_part;
+  int chunk_rows, splits, n_db_rows;
+  size_t bytes;
+};
+
+JoinerBwdWs joiner_bwd_layout(void* base, int N, int T, int S, int J, int V, int bf16) {
+  Carve c(base);
+  JoinerBwdWs w;
+  const size_t M = (size_t)N * T * S;
+  w.chunk_rows = joiner_bwd_chunk_rows(N, T, S, J, V, bf16);
+  w.splits = joiner_bwd_splits(J, V);
+  w.n_db_rows = joiner_db_rows(N, T, S);
+  w.frame_off = c.take<int>((size_t)N + 1);
+  w.rowinfo = c.take<int4>(M);
+  const size_t dl_elems = (size_t)w.chunk_rows * joiner_ldl(V);
+  w.dl = bf16 ? (void*)c.take<uint16_t>(dl_elems) : (void*)c.take<float>(dl_elems);
+  w.dpre = c.take<float>(M * J);
+  w.dw_part = c.take<float>((size_t)w.splits * J * V);
+  w.db_part = c.take<float>((size_t)w.n_db_rows * V);
+  w.bytes = c.off;
+  return w;
+}
+
+int check_ws(void* ws, size_t have, size_t need) {
+  if (need == 0) return RNNT_OK;
+  if (!ws) return fail(RNNT_EWORKSPACE, "workspace is NULL (%zu bytes needed)", need);
+  if (reinterpret_cast<uintptr_t>(ws) % 256 != 0) return fail(RNNT_EWORKSPACE, "workspace must be 256-byte aligned");
+  if (have < need) return fail(RNNT_EWORKSPACE, "workspace has %zu bytes, %zu needed", have, need);
+  return RNNT_OK;
+}
+
+int check_joiner_sizes(const rnnt_batch* b, int S, int J, int V, int dtype) {
+  if (S < 1 || S > RNNT_MAX_S) return fail(RNNT_EUNSUPPORTED, "S = %d outside [1, %d]", S, RNNT_MAX_S);
+  if (V < 1) return fail(RNNT_EINVAL, "V must be >= 1 (got %d)", V);
+  if (b->blank < 0 || b->blank >= V) return fail(RNNT_EINVAL, "blank = %d outside [0, V)", b->blank);
+  if (J < 8 || J % 8 != 0) return fail(RNNT_EUNSUPPORTED, "J = %d must be a positive multiple of 8", J);
+  if (dtype != RNNT_F32 && dtype != RNNT_BF16) return fail(RNNT_EINVAL, "dtype must be RNNT_F32 or RNNT_BF16");
+  if ((long long)b->N * b->T * S > kI32) return fail(RNNT_EUNSUPPORTED, "N*T*S exceeds 2^31-1");
+  if ((long long)b->N * b->T * J > kI32 || (long long)b->N * (b->U + 1) * J > kI32)
+    return fail(RNNT_EUNSUPPORTED, "N*T*J or N*(U+1)*J exceeds 2^31-1");
+  if ((size_t)b->T * sizeof(int) > 64 * 1024) return fail(RNNT_EUNSUPPORTED, "T = %d too large", b->T);
+  return RNNT_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int rnnt_abi_version(void) { return 1; }
+
+const char* rnnt_last_error(void) { return g_err.c_str(); }
+
+size_t rnnt_simple_loss_workspace_size(int32_t N, int32_t T, int32_t U, int32_t V) {
+  if (N < 1 || T < 1 || U < 0 || V < 1) return 0;
+  return simple_layout(nullptr, N, T, U).bytes;
+}
+
+int rnnt_simple_loss(const rnnt_batch* batch, int32_t V, const float* am, const float* lm, const float* scale,
+                     float* loss, float* px_occ, float* py_occ, float* px, float* py, float* am_grad,
+                     float* lm_grad, void* workspace, size_t workspace_bytes, void* stream) {
+  int rc = check_batch(batch, true);
+  if (rc) return rc;
+  if (V < 1) return fail(RNNT_EINVAL, "V must be >= 1 (got %d)", V);
+  if (batch->blank < 0 || batch->blank >= V) return fail(RNNT_EINVAL, "blank = %d outside [0, V)", batch->blank);
+  if (!am || !lm) return fail(RNNT_EINVAL, "am and lm are required");
+  if (!loss || !px_occ || !py_occ) return fail(RNNT_EINVAL, "loss, px_occ and py_occ are required");
+  if ((px == nullptr) != (py == nullptr)) return fail(RNNT_EINVAL, "px and py must be given together");
+  const SimpleWs need = simple_layout(nullptr, batch->N, batch->T, batch->U);
+  rc = check_ws(workspace, workspace_bytes, need.bytes);
+  if (rc) return rc;
+  const SimpleWs w = simple_layout(workspace, batch->N, batch->T, batch->U);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  SimpleArgs a{};
+  a.b = to_dev(batch);
+  a.V = V;
+  a.am = am;
+  a.lm = lm;
+  a.scale = scale;
+  a.m_a = w.m_a;
+  a.m_l = w.m_l;
+  a.Z = w.Z;
+  a.px = px ? px : w.px;
+  a.py = py ? py : w.py;
+  a.alpha = w.alpha;
+  a.beta = w.beta;
+  a.loss = loss;
+  a.gx = px_occ;
+  a.gy = py_occ;
+  a.want_bwd = (am_grad || lm_grad) ? 1 : 0;
+  a.Wt = w.Wt;
+  a.ldw = ldw_of(batch->U);
+  a.ry = w.ry;
+  a.cx = w.cx;
+  a.cy = w.cy;
+  a.am_grad = am_grad;
+  a.lm_grad = lm_grad;
+  hipError_t e = launch_rowmax(a, s);
+  if (e == hipSuccess) e = launch_normalizer(a, s);
+  if (e == hipSuccess) e = launch_lattice(a, s);
+  if (e == hipSuccess && a.want_bwd) e = launch_simple_grads(a, s);
+  return hip_status(e, "rnnt_simple_loss");
+}
+
+int rnnt_prune_ranges(const rnnt_batch* batch, int32_t S, const float* px_occ, const float* py_occ,
+                      int32_t* ranges, void* stream) {
+  int rc = check_batch(batch, false);
+  if (rc) return rc;
+  if (S < 1 || S > RNNT_MAX_S) return fail(RNNT_EUNSUPPORTED, "S = %d outside [1, %d]", S, RNNT_MAX_S);
+  if (!px_occ || !py_occ || !ranges) return fail(RNNT_EINVAL, "px_occ, py_occ and ranges are required");
+  if (prune_smem_bytes(batch->T) > 64 * 1024) return fail(RNNT_EUNSUPPORTED, "T = %d too large", batch->T);
+  if ((long long)batch->N * batch->T * S > kI32) return fail(RNNT_EUNSUPPORTED, "N*T*S exceeds 2^31-1");
+  hipError_t e = launch_prune(to_dev(batch), S, px_occ, py_occ, ranges, static_cast<hipStream_t>(stream));
+  return hip_status(e, "rnnt_prune_ranges");
+}
+
+size_t rnnt_pruned_joiner_workspace_size(int32_t N, int32_t T, int32_t S, int32_t J, int32_t V, int32_t dtype) {
+  (void)J;
+  (void)dtype;
+  if (N < 1 || T < 1 || S < 1 || V < 1) return 0;
+  return joiner_fwd_layout(nullptr, N, T, S, V).bytes;
+}
+
+int rnnt_pruned_joiner(const rnnt_batch* batch, int32_t S, int32_t J, int32_t V, int32_t dtype, const void* enc,
+                       const void* dec, const void* W, const void* bias, const int32_t* ranges, float* px, float* py,
+                       float* lse, void* workspace, size_t workspace_bytes, void* stream) {
+  int rc = check_batch(batch, true);
+  if (rc) return rc;
+  rc = check_joiner_sizes(batch, S, J, V, dtype);
+  if (rc) return rc;
+  if (!enc || !dec || !W || !ranges) return fail(RNNT_EINVAL, "enc, dec, W and ranges are required");
+  if (!px || !py || !lse) return fail(RNNT_EINVAL, "px, py and lse are required");
+  rc = check_ws(workspace, workspace_bytes, joiner_fwd_layout(nullptr, batch->N, batch->T, S, V).bytes);
+  if (rc) return rc;
+  const JoinerFwdWs w = joiner_fwd_layout(workspace, batch->N, batch->T, S, V);
+  JoinerArgs a{};
+  a.b = to_dev(batch);
+  a.S = S;
+  a.J = J;
+  a.V = V;
+  a.bf16 = dtype == RNNT_BF16;
+  a.enc = enc;
+  a.dec = dec;
+  a.W = W;
+  a.bias = bias;
+  a.ranges = ranges;
+  a.frame_off = w.frame_off;
+  a.rowinfo = w.rowinfo;
+  a.part = w.part;
+  a.nparts = joiner_nparts(V);
+  a.tgt = w.tgt;
+  a.blk = w.blk;
+  a.px = px;
+  a.py = py;
+  a.lse = lse;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e = launch_joiner_prep(a, s);
+  if (e == hipSuccess) e = launch_joiner_fwd(a, s);
+  return hip_status(e, "rnnt_pruned_joiner");
+}
+
+size_t rnnt_pruned_loss_workspace_size(int32_t N, int32_t T, int32_t S) {
+  if (N < 1 || T < 1 || S < 1) return 0;
+  Carve c(nullptr);
+  c.take<double>((size_t)N * T * S);
+  c.take<double>((size_t)N * T * S);
+  return c.off;
+}
+
+int rnnt_pruned_loss(const rnnt_batch* batch, int32_t S, const float* px, const float* py, const int32_t* ranges,
+                     float* loss, float* px_occ, float* py_occ, void* workspace, size_t workspace_bytes,
+                     void* stream) {
+  int rc = check_batch(batch, false);
+  if (rc) return rc;
+  if (S < 1 || S > RNNT_MAX_S) return fail(RNNT_EUNSUPPORTED, "S = %d outside [1, %d]", S, RNNT_MAX_S);
+  if (!px || !py || !ranges || !loss) return fail(RNNT_EINVAL, "px, py, ranges and loss are required");
+  if ((long long)batch->N * batch->T * S > kI32) return fail(RNNT_EUNSUPPORTED, "N*T*S exceeds 2^31-1");
+  if (band_smem_bytes(batch->T, S) > 150 * 1024)
+    return fail(RNNT_EUNSUPPORTED, "T*S = %d*%d too large for the LDS-resident band", batch->T, S);
+  const size_t need = rnnt_pruned_loss_workspace_size(batch->N, batch->T, S);
+  rc = check_ws(workspace, workspace_bytes, need);
+  if (rc) return rc;
+  Carve c(workspace);
+  BandArgs a{};
+  a.b = to_dev(batch);
+  a.S = S;
+  a.px = px;
+  a.py = py;
+  a.ranges = ranges;
+  a.alpha = c.take<double>((size_t)batch->N * batch->T * S);
+  a.beta = c.take<double>((size_t)batch->N * batch->T * S);
+  a.loss = loss;
+  a.gx = px_occ;
+  a.gy = py_occ;
+  hipError_t e = launch_band(a, static_cast<hipStream_t>(stream));
+  return hip_status(e, "rnnt_pruned_loss");
+}
+
+size_t rnnt_pruned_joiner_backward_workspace_size(int32_t N, int32_t T, int32_t U, int32_t S, int32_t J, int32_t V,
+                                                  int32_t dtype) {
+  (void)U;
+  if (N < 1 || T < 1 || S < 1 || J < 1 || V < 1) return 0;
+  return joiner_bwd_layout(nullptr, N, T, S, J, V, dtype == RNNT_BF16).bytes;
+}
+
+int rnnt_pruned_joiner_backward(const rnnt_batch* batch, int32_t S, int32_t J, int32_t V, int32_t dtype,
+                                const void* enc, const void* dec, const void* W, const void* bias,
+                                const int32_t* ranges, const float* lse, const float* px_occ, const float* py_occ,
+                                const float* scale, float* enc_grad, float* dec_grad, float* W_grad, float* bias_grad,
+                                float* logits_grad, void* workspace, size_t workspace_bytes, void* stream) {
+  int rc = check_batch(batch, true);
+  if (rc) return rc;
+  rc = check_joiner_sizes(batch, S, J, V, dtype);
+  if (rc) return rc;
+  if (!enc || !dec || !W || !ranges || !lse || !px_occ || !py_occ)
+    return fail(RNNT_EINVAL, "enc, dec, W, ranges, lse, px_occ and py_occ are required");
+  if (!enc_grad || !dec_grad) return fail(RNNT_EINVAL, "enc_grad and dec_grad are required");
+  if (logits_grad && (long long)batch->N * batch->T * S * (long long)V > (1ll << 40))
+    return fail(RNNT_EUNSUPPORTED, "logits_grad is a debugging aid for small shapes");
+  const int bf = dtype == RNNT_BF16;
+  rc = check_ws(workspace, workspace_bytes, joiner_bwd_layout(nullptr, batch->N, batch->T, S, J, V, bf).bytes);
+  if (rc) return rc;
+  const JoinerBwdWs w = joiner_bwd_layout(workspace, batch->N, batch->T, S, J, V, bf);
+  JoinerArgs a{};
+  a.b = to_dev(batch);
+  a.S = S;
+  a.J = J;
+  a.V = V;
+  a.bf16 = bf;
+  a.enc = enc;
+  a.dec = dec;
+  a.W = W;
+  a.bias = bias;
+  a.ranges = ranges;
+  a.frame_off = w.frame_off;
+  a.rowinfo = w.rowinfo;
+  a.lse_in = lse;
+  a.gxo = px_occ;
+  a.gyo = py_occ;
+  a.scale = scale;
+  a.dl = w.dl;
+  a.ldl = joiner_ldl(V);
+  a.chunk_rows = w.chunk_rows;
+  a.dpre = w.dpre;
+  a.dw_part = w.dw_part;
+  a.splits = w.splits;
+  a.db_part = w.db_part;
+  a.n_db_rows = w.n_db_rows;
+  a.enc_grad = enc_grad;
+  a.dec_grad = dec_grad;
+  a.W_grad = W_grad;
+  a.bias_grad = bias_grad;
+  a.logits_grad = logits_grad;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e = launch_joiner_prep(a, s);
+  if (e == hipSuccess) e = launch_joiner_bwd(a, s);
+  return hip_status(e, "rnnt_pruned_joiner_backward");
+}
+
+}  // extern "C"

@@ -1,0 +1,85 @@
+// Device helpers shared by the gfx950 kernels of the pruned RNN-T library.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#define DEV __device__ __forceinline__
+
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+constexpr float kNegInfF = -__builtin_inff();
+constexpr double kNegInfD = -__builtin_inf();
+constexpr double kLog2e = 1.4426950408889634074;
+constexpr double kLn2 = 0.69314718055994530942;
+
+// Plain-old-data view of rnnt_batch passed to kernels by value.
+struct BatchDev {
+  int N, T, U;
+  const int* t_len;
+  const int* u_len;
+  const int* symbols;  // [N, U]
+  int blank;
+};
+
+// Per-utterance sizes, clamped into range so that every index derived from
+// them stays in bounds. Returns false when the caller's lengths were invalid
+// (that utterance's loss is then reported as NaN).
+DEV bool utt_dims(const BatchDev& b, int n, int& Tn, int& Un) {
+  int t = b.t_len[n], u = b.u_len[n];
+  bool ok = (t >= 1) && (t <= b.T) && (u >= 0) && (u <= b.U);
+  Tn = min(max(t, 1), b.T);
+  Un = min(max(u, 0), b.U);
+  return ok;
+}
+
+// y_{u+1} of utterance n clamped to [0, V); `ok` is cleared when it was not.
+DEV int symbol_at(const BatchDev& b, int n, int u, int V, bool& ok) {
+  int y = b.symbols[(size_t)n * b.U + u];
+  if (y < 0 || y >= V) {
+    ok = false;
+    y = min(max(y, 0), V - 1);
+  }
+  return y;
+}
+
+// log2(2^a + 2^b) for log2-domain values held in fp64. The large-magnitude
+// additions stay in fp64; only the bounded correction log2(1 + 2^-|a-b|),
+// which lies in [0, 1], goes through the fp32 hardware exp2/log2. NaN in either
+// argument propagates.
+DEV double log2add(double a, double b) {
+  double mx = a > b ? a : b;
+  double mn = a > b ? b : a;
+  if (mn == kNegInfD) return mx;
+  float d = (float)(mn - mx);
+  float c = __builtin_amdgcn_logf(1.0f + __builtin_amdgcn_exp2f(d));
+  return mx + (double)c;
+}
+
+// 2^x for an fp64 log2-domain argument that is <= ~0 (an occupation).
+DEV float exp2_occ(double x) {
+  if (!(x > -200.0)) return (x != x) ? x : 0.0f;  // NaN stays NaN, tiny -> 0
+  return exp2f((float)x);
+}
+
+// Round-to-nearest-even fp32 -> bf16 bits (NaN kept quiet).
+DEV uint16_t f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+DEV float bf2f(uint16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
+
+// tanh from one hardware exp2 and one reciprocal: tanh(x) = 1 - 2 / (e^{2x} + 1).
+// Absolute error ~1e-7 over the whole range; saturates cleanly to +-1.
+DEV float fast_tanh(float x) {
+  float e = __builtin_amdgcn_exp2f(x * 2.8853900817779268f);  // 2*log2(e)
+  return 1.0f - 2.0f * __builtin_amdgcn_rcpf(e + 1.0f);
+}
+
+DEV double shfl_up_d(double v, int delta) { return __shfl_up(v, delta, 64); }
+DEV double shfl_down_d(double v, int delta) { return __shfl_down(v, delta, 64); }
+
+DEV size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }

@@ -1,0 +1,212 @@
+// MFMA GEMM main loop for gfx950, shared by every contraction of the library.
+//
+// A workgroup of 256 threads (4 wave64s in a 2x2 grid) computes a BM x BN
+// tile of C = A * B with K-steps of BK. Operand tiles are staged through LDS
+// in a k-contiguous layout ([row][k], rows padded by 16 bytes) so that every
+// lane fetches one 16-byte fragment per 16x16 output block per k-slice:
+//   fp32: v_mfma_f32_16x16x4_f32, a fragment holds 4 consecutive k and feeds
+//         4 MFMAs (the k order inside a slice is permuted identically for A
+//         and B, which leaves the sum unchanged);
+//   bf16: v_mfma_f32_16x16x32_bf16, a fragment holds 8 consecutive k.
+// Accumulation is fp32 in both cases. Global -> register fetches of the next
+// K-step are issued before the MFMAs of the current one; LDS is double
+// buffered, so there is one barrier per K-step.
+//
+// Operand sources are supplied by each kernel:
+//   KC  source (global is k-contiguous):  kc_fetch(row, k, float v[KV])
+//   MNC source (global is row-contiguous): mnc_fetch(k, row, float v[16/KV])
+// and return fp32 values (generated values such as tanh(enc+dec) or
+// exp(x - max) are produced inside the fetch); the loader packs them.
+//
+// Output element (i, j, r) of a lane: row = wm*WM + i*16 + 4*(lane>>4) + r,
+// col = wn*WN + j*16 + (lane & 15).
+#pragma once
+
+#include <type_traits>
+
+#include "common.h"
+
+template <int BM_, int BN_, int BK_, bool BF16_>
+struct GemmCfg {
+  static constexpr int BM = BM_, BN = BN_, BK = BK_;
+  static constexpr bool BF16 = BF16_;
+  using T = typename std::conditional<BF16_, uint16_t, float>::type;
+  static constexpr int ESZ = (int)sizeof(T);
+  static constexpr int KV = 16 / ESZ;         // k values per 16-byte fragment
+  static constexpr int KSLICE = 4 * KV;       // k covered by one fragment across 4 lane groups
+  static constexpr int LDK = BK + KV;         // padded LDS row stride (elements)
+  static constexpr int WM = BM / 2, WN = BN / 2;
+  static constexpr int FM = WM / 16, FN = WN / 16;
+  static constexpr int A_ELEMS = BM * LDK, B_ELEMS = BN * LDK;
+  static constexpr int STAGE_ELEMS = A_ELEMS + B_ELEMS;
+  static constexpr int SMEM_BYTES = 2 * STAGE_ELEMS * ESZ;
+  static_assert(BK % KSLICE == 0, "BK must be a multiple of the fragment k-slice");
+  static_assert(FM >= 1 && FN >= 1, "tile too small");
+};
+
+template <class Cfg>
+DEV void pack_store16(typename Cfg::T* dst, const float* v) {
+  if constexpr (Cfg::BF16) {
+    uint32_t w[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      w[i] = (uint32_t)f2bf(v[2 * i]) | ((uint32_t)f2bf(v[2 * i + 1]) << 16);
+    *reinterpret_cast<uint4*>(dst) = make_uint4(w[0], w[1], w[2], w[3]);
+  } else {
+    *reinterpret_cast<float4*>(dst) = make_float4(v[0], v[1], v[2], v[3]);
+  }
+}
+
+// Operand tile whose global source is k-contiguous.
+template <class Cfg, int ROWS, class Src>
+struct KCLoader {
+  static constexpr int KV = Cfg::KV;
+  static constexpr int CPR = Cfg::BK / KV;               // 16-byte chunks per row
+  static constexpr int NCH = (ROWS * CPR + 255) / 256;   // chunks per thread
+  struct Reg { float v[NCH][KV]; };
+  const Src& src;
+  DEV explicit KCLoader(const Src& s) : src(s) {}
+  DEV void fetch(int k0, Reg& r) const {
+#pragma unroll
+    for (int i = 0; i < NCH; ++i) {
+      int c = threadIdx.x + 256 * i;
+      if (ROWS * CPR % 256 == 0 || c < ROWS * CPR) src.kc_fetch(c / CPR, k0 + (c % CPR) * KV, r.v[i]);
+    }
+  }
+  DEV void put(const Reg& r, typename Cfg::T* lds) const {
+#pragma unroll
+    for (int i = 0; i < NCH; ++i) {
+      int c = threadIdx.x + 256 * i;
+      if (ROWS * CPR % 256 == 0 || c < ROWS * CPR)
+        pack_store16<Cfg>(lds + (c / CPR) * Cfg::LDK + (c % CPR) * KV, r.v[i]);
+    }
+  }
+};
+
+// Operand tile whose global source is row-contiguous ([k][row]); the loader
+// transposes KV x (16/KV) blocks in registers so LDS stays k-contiguous.
+template <class Cfg, int ROWS, class Src>
+struct MNCLoader {
+  static constexpr int KV = Cfg::KV;
+  static constexpr int NV = 16 / KV;                       // rows per block (4 fp32, 2 bf16)
+  static constexpr int NBR = ROWS / NV;                    // blocks along rows
+  static constexpr int NBLK = (Cfg::BK / KV) * NBR;
+  static constexpr int NPT = (NBLK + 255) / 256;
+  struct Reg { float v[NPT][KV][NV]; };
+  const Src& src;
+  DEV explicit MNCLoader(const Src& s) : src(s) {}
+  DEV void fetch(int k0, Reg& r) const {
+#pragma unroll
+    for (int b = 0; b < NPT; ++b) {
+      int blk = threadIdx.x + 256 * b;
+      if (NBLK % 256 == 0 || blk < NBLK) {
+        int kb = blk / NBR, nb = blk % NBR;
+#pragma unroll
+        for (int i = 0; i < KV; ++i) src.mnc_fetch(k0 + kb * KV + i, nb * NV, r.v[b][i]);
+      }
+    }
+  }
+  DEV void put(const Reg& r, typename Cfg::T* lds) const {
+#pragma unroll
+    for (int b = 0; b < NPT; ++b) {
+      int blk = threadIdx.x + 256 * b;
+      if (NBLK % 256 == 0 || blk < NBLK) {
+        int kb = blk / NBR, nb = blk % NBR;
+#pragma unroll
+        for (int c = 0; c < NV; ++c) {
+          float col[KV];
+#pragma unroll
+          for (int i = 0; i < KV; ++i) col[i] = r.v[b][i][c];
+          pack_store16<Cfg>(lds + (nb * NV + c) * Cfg::LDK + kb * KV, col);
+        }
+      }
+    }
+  }
+};
+
+template <class Cfg>
+DEV void gemm_compute_stage(const typename Cfg::T* As, const typename Cfg::T* Bs,
+                            floatx4 (&acc)[Cfg::FM][Cfg::FN]) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const typename Cfg::T* a_base = As + (wm * Cfg::WM + (lane & 15)) * Cfg::LDK + (lane >> 4) * Cfg::KV;
+  const typename Cfg::T* b_base = Bs + (wn * Cfg::WN + (lane & 15)) * Cfg::LDK + (lane >> 4) * Cfg::KV;
+#pragma unroll
+  for (int kk = 0; kk < Cfg::BK; kk += Cfg::KSLICE) {
+    if constexpr (Cfg::BF16) {
+      bf16x8 fa[Cfg::FM], fb[Cfg::FN];
+#pragma unroll
+      for (int i = 0; i < Cfg::FM; ++i) fa[i] = *reinterpret_cast<const bf16x8*>(a_base + i * 16 * Cfg::LDK + kk);
+#pragma unroll
+      for (int j = 0; j < Cfg::FN; ++j) fb[j] = *reinterpret_cast<const bf16x8*>(b_base + j * 16 * Cfg::LDK + kk);
+#pragma unroll
+      for (int i = 0; i < Cfg::FM; ++i)
+#pragma unroll
+        for (int j = 0; j < Cfg::FN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+    } else {
+      floatx4 fa[Cfg::FM], fb[Cfg::FN];
+#pragma unroll
+      for (int i = 0; i < Cfg::FM; ++i) fa[i] = *reinterpret_cast<const floatx4*>(a_base + i * 16 * Cfg::LDK + kk);
+#pragma unroll
+      for (int j = 0; j < Cfg::FN; ++j) fb[j] = *reinterpret_cast<const floatx4*>(b_base + j * 16 * Cfg::LDK + kk);
+#pragma unroll
+      for (int s = 0; s < 4; ++s)
+#pragma unroll
+        for (int i = 0; i < Cfg::FM; ++i)
+#pragma unroll
+          for (int j = 0; j < Cfg::FN; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[i][s], fb[j][s], acc[i][j], 0, 0, 0);
+    }
+  }
+}
+
+// Runs the K loop over [k_begin, k_end) and leaves the tile in `acc`.
+// Must be called by all 256 threads of the workgroup (it contains barriers).
+template <class Cfg, class LA, class LB>
+DEV void gemm_mainloop(const LA& la, const LB& lb, int k_begin, int k_end,
+                       typename Cfg::T* smem, floatx4 (&acc)[Cfg::FM][Cfg::FN]) {
+#pragma unroll
+  for (int i = 0; i < Cfg::FM; ++i)
+#pragma unroll
+    for (int j = 0; j < Cfg::FN; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+  const int nk = (k_end - k_begin + Cfg::BK - 1) / Cfg::BK;
+  if (nk <= 0) return;
+  typename Cfg::T* As0 = smem;
+  typename Cfg::T* Bs0 = smem + Cfg::A_ELEMS;
+  typename Cfg::T* As1 = smem + Cfg::STAGE_ELEMS;
+  typename Cfg::T* Bs1 = smem + Cfg::STAGE_ELEMS + Cfg::A_ELEMS;
+  typename LA::Reg ra;
+  typename LB::Reg rb;
+  la.fetch(k_begin, ra);
+  lb.fetch(k_begin, rb);
+  la.put(ra, As0);
+  lb.put(rb, Bs0);
+  __syncthreads();
+  for (int kt = 0; kt < nk; ++kt) {
+    const bool more = kt + 1 < nk;
+    if (more) {
+      la.fetch(k_begin + (kt + 1) * Cfg::BK, ra);
+      lb.fetch(k_begin + (kt + 1) * Cfg::BK, rb);
+    }
+    if (kt & 1) gemm_compute_stage<Cfg>(As1, Bs1, acc);
+    else gemm_compute_stage<Cfg>(As0, Bs0, acc);
+    if (more) {
+      if (kt & 1) { la.put(ra, As0); lb.put(rb, Bs0); }
+      else { la.put(ra, As1); lb.put(rb, Bs1); }
+    }
+    __syncthreads();
+  }
+}
+
+// Row/column of output element (i, j, r) of this lane within the tile.
+template <class Cfg>
+DEV int tile_row(int i, int r) {
+  const int lane = threadIdx.x & 63, wm = (threadIdx.x >> 6) >> 1;
+  return wm * Cfg::WM + i * 16 + 4 * (lane >> 4) + r;
+}
+template <class Cfg>
+DEV int tile_col(int j) {
+  const int lane = threadIdx.x & 63, wn = (threadIdx.x >> 6) & 1;
+  return wn * Cfg::WN + j * 16 + (lane & 15);
+}

@@ -1,0 +1,677 @@
+// Stage 4a/4c: the full joiner evaluated only on the pruned (t, u) pairs
+// (Sec. 3.2, Fig. 1(b)) and its backward pass.
+//
+// Rows. Every valid frame of the batch contributes S consecutive rows
+// m = (frame_off[n] + t) * S + s (padding frames take no rows), so the GEMMs
+// see one dense M = S * sum_n T_n dimension. A prep kernel writes, per row,
+// the offsets of enc[n,t] and dec[n,u] (u = ranges[n,t,s]), the target symbol
+// y_{u+1} (-1 at u = U_n) and the output index n*T*S + t*S + s (-1 when the
+// slot is absent, u > U_n).
+//
+// Forward: logits = tanh(enc + dec) W + bias on MFMA (fp32 16x16x4 or bf16
+// 16x16x32, fp32 accumulation); the tanh is formed while staging the A tile.
+// The epilogue reduces every (row, 64-column slice) to (max, sum exp) and
+// captures the target and blank logits; a combine kernel turns them into
+// lse, px = logit[y_{u+1}] - lse and py = logit[blank] - lse. The
+// [rows, V] logits never reach memory.
+//
+// Backward (per chunk of rows, so that d(logits) is held for one chunk only):
+//   1. recompute logits, dl = sc * ((gx+gy) softmax - gx [v=y] - gy [v=blank])
+//      (log-softmax backward), write the chunk and per-tile column sums (db);
+//   2. dh = dl W^T, dpre = dh (1 - h^2)  (tanh backward);
+//   3. dW += h^T dl with split-K partial sums;
+// then d enc[n,t] = sum_s dpre(row(t,s)), d dec[n,u] = sum over the (t,s)
+// with p_t + s = u, dW and db summed over their partials, all in a fixed order.
+#include "gemm.h"
+#include "kernels.h"
+
+namespace {
+
+using CfgF = GemmCfg<128, 128, 32, false>;
+using CfgB = GemmCfg<128, 128, 64, true>;
+
+template <bool BF>
+struct In;
+template <>
+struct In<false> {
+  using T = float;
+  using Cfg = CfgF;
+};
+template <>
+struct In<true> {
+  using T = uint16_t;
+  using Cfg = CfgB;
+};
+
+DEV float ld_in(const float* p, size_t i) { return p[i]; }
+DEV float ld_in(const uint16_t* p, size_t i) { return bf2f(p[i]); }
+
+// n consecutive elements of a row as fp32 (16-byte vector loads when aligned).
+template <int NV>
+DEV void load_vec(const float* p, float (&v)[NV]) {
+  if constexpr (NV == 4) {
+    float4 q = *reinterpret_cast<const float4*>(p);
+    v[0] = q.x; v[1] = q.y; v[2] = q.z; v[3] = q.w;
+  } else if constexpr (NV == 8) {
+    float4 q0 = *reinterpret_cast<const float4*>(p);
+    float4 q1 = *reinterpret_cast<const float4*>(p + 4);
+    v[0] = q0.x; v[1] = q0.y; v[2] = q0.z; v[3] = q0.w;
+    v[4] = q1.x; v[5] = q1.y; v[6] = q1.z; v[7] = q1.w;
+  } else {
+#pragma unroll
+    for (int i = 0; i < NV; ++i) v[i] = p[i];
+  }
+}
+template <int NV>
+DEV void load_vec(const uint16_t* p, float (&v)[NV]) {
+  if constexpr (NV == 8) {
+    uint4 q = *reinterpret_cast<const uint4*>(p);
+    uint32_t w[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      v[2 * i] = __uint_as_float(w[i] << 16);
+      v[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+    }
+  } else if constexpr (NV == 2) {
+    uint32_t w = *reinterpret_cast<const uint32_t*>(p);
+    v[0] = __uint_as_float(w << 16);
+    v[1] = __uint_as_float(w & 0xffff0000u);
+  } else if constexpr (NV == 4) {
+    uint2 q = *reinterpret_cast<const uint2*>(p);
+    v[0] = __uint_as_float(q.x << 16);
+    v[1] = __uint_as_float(q.x & 0xffff0000u);
+    v[2] = __uint_as_float(q.y << 16);
+    v[3] = __uint_as_float(q.y & 0xffff0000u);
+  } else {
+#pragma unroll
+    for (int i = 0; i < NV; ++i) v[i] = bf2f(p[i]);
+  }
+}
+
+// Masked row segment [c, c+NV) of a row of length len: vector load when the
+// whole segment is inside and aligned, element loads otherwise.
+template <int NV, typename TIn>
+DEV void load_seg(const TIn* row, int c, int len, bool aligned, float (&v)[NV]) {
+  if (aligned && c + NV <= len) {
+    load_vec<NV>(row + c, v);
+  } else {
+#pragma unroll
+    for (int i = 0; i < NV; ++i) v[i] = (c + i < len) ? ld_in(row, (size_t)(c + i)) : 0.f;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Operand sources
+// ---------------------------------------------------------------------------
+
+// A(m, j) = tanh(enc[row] + dec[row]) for the tile's rows (rowinfo in LDS).
+template <class Cfg, typename TIn>
+struct HSrcKC {
+  const TIn* enc;
+  const TIn* dec;
+  const int4* ri;
+  int J;
+  DEV void kc_fetch(int row, int k, float (&v)[Cfg::KV]) const {
+    const int4 r = ri[row];
+    if (r.w < 0 || k >= J) {
+#pragma unroll
+      for (int i = 0; i < Cfg::KV; ++i) v[i] = 0.f;
+      return;
+    }
+    float e[Cfg::KV], d[Cfg::KV];
+    load_vec<Cfg::KV>(enc + (size_t)r.x + k, e);
+    load_vec<Cfg::KV>(dec + (size_t)r.y + k, d);
+#pragma unroll
+    for (int i = 0; i < Cfg::KV; ++i) v[i] = fast_tanh(e[i] + d[i]);
+  }
+};
+
+// B(j, v) = W[j][v]: global row-contiguous along v.
+template <class Cfg, typename TIn>
+struct WSrcMNC {
+  static constexpr int NV = 16 / Cfg::KV;
+  const TIn* W;
+  int v0, V, J;
+  bool aligned;
+  DEV void mnc_fetch(int k, int col, float (&v)[NV]) const {
+    if (k >= J) {
+#pragma unroll
+      for (int i = 0; i < NV; ++i) v[i] = 0.f;
+      return;
+    }
+    load_seg<NV>(W + (size_t)k * V, v0 + col, V, aligned, v);
+  }
+};
+
+// A(m, v) = dl[m][v] from the chunk buffer (rows padded to ldl with zeros).
+template <class Cfg>
+struct DlSrcKC {
+  const typename Cfg::T* dl;  // row (m - cm0)
+  int m0, cm0, mend, ldl;
+  DEV void kc_fetch(int row, int k, float (&v)[Cfg::KV]) const {
+    const int m = m0 + row;
+    if (m >= mend || k >= ldl) {
+#pragma unroll
+      for (int i = 0; i < Cfg::KV; ++i) v[i] = 0.f;
+      return;
+    }
+    load_vec<Cfg::KV>(dl + (size_t)(m - cm0) * ldl + k, v);
+  }
+};
+
+// B(v, j) = W[j][v]: global k-contiguous along v for each j.
+template <class Cfg, typename TIn>
+struct WtSrcKC {
+  const TIn* W;
+  int j0, J, V;
+  bool aligned;
+  DEV void kc_fetch(int row, int k, float (&v)[Cfg::KV]) const {
+    const int j = j0 + row;
+    if (j >= J) {
+#pragma unroll
+      for (int i = 0; i < Cfg::KV; ++i) v[i] = 0.f;
+      return;
+    }
+    load_seg<Cfg::KV>(W + (size_t)j * V, k, V, aligned, v);
+  }
+};
+
+// A(j, m) = h(m, j): global is [m][j], j-contiguous; rowinfo read per row.
+template <class Cfg, typename TIn>
+struct HSrcMNC {
+  static constexpr int NV = 16 / Cfg::KV;
+  const TIn* enc;
+  const TIn* dec;
+  const int4* rowinfo;
+  int j0, J, mend;
+  DEV void mnc_fetch(int k, int col, float (&v)[NV]) const {
+    const int j = j0 + col;
+    int4 r = make_int4(0, 0, -1, -1);
+    if (k < mend && j < J) r = rowinfo[k];
+    if (r.w < 0) {
+#pragma unroll
+      for (int i = 0; i < NV; ++i) v[i] = 0.f;
+      return;
+    }
+    float e[NV], d[NV];
+    load_vec<NV>(enc + (size_t)r.x + j, e);
+    load_vec<NV>(dec + (size_t)r.y + j, d);
+#pragma unroll
+    for (int i = 0; i < NV; ++i) v[i] = fast_tanh(e[i] + d[i]);
+  }
+};
+
+// B(m, v) = dl[m][v]: global row-contiguous along v.
+template <class Cfg>
+struct DlSrcMNC {
+  static constexpr int NV = 16 / Cfg::KV;
+  const typename Cfg::T* dl;
+  int cm0, mend, v0, ldl;
+  DEV void mnc_fetch(int k, int col, float (&v)[NV]) const {
+    const int c = v0 + col;
+    if (k >= mend || c >= ldl) {
+#pragma unroll
+      for (int i = 0; i < NV; ++i) v[i] = 0.f;
+      return;
+    }
+    load_vec<NV>(dl + (size_t)(k - cm0) * ldl + c, v);
+  }
+};
+
+DEV float bias_at(const void* bias, int bf16, int v) {
+  if (!bias) return 0.f;
+  return bf16 ? bf2f(reinterpret_cast<const uint16_t*>(bias)[v]) : reinterpret_cast<const float*>(bias)[v];
+}
+
+// ---------------------------------------------------------------------------
+// Prep: per-utterance frame offsets and per-row info.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void joiner_prep_kernel(JoinerArgs a) {
+  __shared__ int s_off;
+  const int n = blockIdx.x;
+  const int T = a.b.T, U1 = a.b.U + 1, S = a.S, J = a.J;
+  if (threadIdx.x == 0) {
+    int off = 0;
+    for (int q = 0; q < n; ++q) {
+      int Tq, Uq;
+      utt_dims(a.b, q, Tq, Uq);
+      off += Tq;
+    }
+    s_off = off;
+  }
+  __syncthreads();
+  const int off = s_off;
+  int Tn, Un;
+  utt_dims(a.b, n, Tn, Un);
+  if (threadIdx.x == 0) {
+    a.frame_off[n] = off;
+    if (n == a.b.N - 1) a.frame_off[a.b.N] = off + Tn;
+  }
+  for (int i = threadIdx.x; i < Tn * S; i += blockDim.x) {
+    const int t = i / S, s = i - t * S;
+    const size_t nts = ((size_t)n * T + t) * S + s;
+    const int u = a.ranges[nts];
+    int4 r;
+    if (u >= 0 && u <= Un) {
+      bool ok = true;
+      r.x = (int)(((size_t)n * T + t) * J);
+      r.y = (int)(((size_t)n * U1 + u) * J);
+      r.z = (u < Un) ? symbol_at(a.b, n, u, a.V, ok) : -1;
+      r.w = (int)nts;
+    } else {
+      r = make_int4(0, 0, -1, -1);
+    }
+    a.rowinfo[(size_t)(off + t) * S + s] = r;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Forward GEMM + partial log-sum-exp
+// ---------------------------------------------------------------------------
+template <bool BF>
+__global__ __launch_bounds__(256) void joiner_fwd_kernel(JoinerArgs a) {
+  using TIn = typename In<BF>::T;
+  using Cfg = typename In<BF>::Cfg;
+  __shared__ __align__(16) typename Cfg::T smem[Cfg::SMEM_BYTES / sizeof(typename Cfg::T)];
+  __shared__ int4 ri[Cfg::BM];
+  const int M = a.frame_off[a.b.N] * a.S;
+  const int m0 = blockIdx.x * Cfg::BM;
+  if (m0 >= M) return;
+  const int v0 = blockIdx.y * Cfg::BN;
+  const int V = a.V, J = a.J;
+  for (int r = threadIdx.x; r < Cfg::BM; r += 256)
+    ri[r] = (m0 + r < M) ? a.rowinfo[m0 + r] : make_int4(0, 0, -1, -1);
+  __syncthreads();
+  const TIn* enc = reinterpret_cast<const TIn*>(a.enc);
+  const TIn* dec = reinterpret_cast<const TIn*>(a.dec);
+  HSrcKC<Cfg, TIn> sa{enc, dec, ri, J};
+  WSrcMNC<Cfg, TIn> sb{reinterpret_cast<const TIn*>(a.W), v0, V, J, (V % WSrcMNC<Cfg, TIn>::NV) == 0};
+  KCLoader<Cfg, Cfg::BM, HSrcKC<Cfg, TIn>> la(sa);
+  MNCLoader<Cfg, Cfg::BN, WSrcMNC<Cfg, TIn>> lb(sb);
+  floatx4 acc[Cfg::FM][Cfg::FN];
+  gemm_mainloop<Cfg>(la, lb, 0, J, smem, acc);
+
+  const int lane = threadIdx.x & 63, wn = (threadIdx.x >> 6) & 1;
+  const int slice = blockIdx.y * 2 + wn;
+  float bj[Cfg::FN];
+#pragma unroll
+  for (int j = 0; j < Cfg::FN; ++j) {
+    const int col = v0 + tile_col<Cfg>(j);
+    bj[j] = (col < V) ? bias_at(a.bias, a.bf16, col) : 0.f;
+  }
+#pragma unroll
+  for (int i = 0; i < Cfg::FM; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int row = tile_row<Cfg>(i, r);
+      const int4 info = ri[row];
+      float lg[Cfg::FN];
+      float mx = kNegInfF;
+#pragma unroll
+      for (int j = 0; j < Cfg::FN; ++j) {
+        const int col = v0 + tile_col<Cfg>(j);
+        lg[j] = (col < V) ? acc[i][j][r] + bj[j] : kNegInfF;
+        mx = fmaxf(mx, lg[j]);
+      }
+#pragma unroll
+      for (int off = 8; off >= 1; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off, 64));
+      float se = 0.f;
+#pragma unroll
+      for (int j = 0; j < Cfg::FN; ++j) {
+        const int col = v0 + tile_col<Cfg>(j);
+        se += (col < V) ? __expf(lg[j] - mx) : 0.f;
+      }
+#pragma unroll
+      for (int off = 8; off >= 1; off >>= 1) se += __shfl_xor(se, off, 64);
+      if (info.w >= 0) {
+        const int m = m0 + row;
+        if ((lane & 15) == 0 && slice < a.nparts) a.part[(size_t)m * a.nparts + slice] = make_float2(mx, se);
+#pragma unroll
+        for (int j = 0; j < Cfg::FN; ++j) {
+          const int col = v0 + tile_col<Cfg>(j);
+          if (col < V) {
+            if (col == info.z) a.tgt[m] = lg[j];
+            if (col == a.b.blank) a.blk[m] = lg[j];
+          }
+        }
+      }
+    }
+}
+
+__global__ __launch_bounds__(256) void joiner_combine_kernel(JoinerArgs a) {
+  const int T = a.b.T, S = a.S;
+  const size_t total = (size_t)a.b.N * T * S;
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= total) return;
+  const int n = (int)(i / ((size_t)T * S));
+  const int rem = (int)(i - (size_t)n * T * S);
+  const int t = rem / S, s = rem - t * S;
+  int Tn, Un;
+  utt_dims(a.b, n, Tn, Un);
+  float px = kNegInfF, py = kNegInfF, l = 0.f;
+  if (t < Tn) {
+    const int m = (a.frame_off[n] + t) * S + s;
+    const int4 info = a.rowinfo[m];
+    if (info.w >= 0) {
+      const float2* pp = a.part + (size_t)m * a.nparts;
+      float M = kNegInfF;
+      for (int p = 0; p < a.nparts; ++p) M = fmaxf(M, pp[p].x);
+      float sum = 0.f;
+      for (int p = 0; p < a.nparts; ++p) sum += pp[p].y * __expf(pp[p].x - M);
+      l = M + __logf(sum);
+      py = a.blk[m] - l;
+      px = (info.z >= 0) ? a.tgt[m] - l : kNegInfF;
+    }
+  }
+  a.px[i] = px;
+  a.py[i] = py;
+  a.lse[i] = l;
+}
+
+// ---------------------------------------------------------------------------
+// Backward 1: recompute logits, d(logits) for a chunk of rows, db partials.
+// ---------------------------------------------------------------------------
+template <bool BF>
+__global__ __launch_bounds__(256) void joiner_dlogits_kernel(JoinerArgs a, int cm0, int cm1) {
+  using TIn = typename In<BF>::T;
+  using Cfg = typename In<BF>::Cfg;
+  __shared__ __align__(16) typename Cfg::T smem[Cfg::SMEM_BYTES / sizeof(typename Cfg::T)];
+  __shared__ int4 ri[Cfg::BM];
+  __shared__ float4 rx[Cfg::BM];  // lse, gx, gy, scale
+  const int M = a.frame_off[a.b.N] * a.S;
+  const int mend = min(cm1, M);
+  const int m0 = cm0 + blockIdx.x * Cfg::BM;
+  if (m0 >= mend) return;
+  const int v0 = blockIdx.y * Cfg::BN;
+  const int V = a.V, J = a.J, TS = a.b.T * a.S;
+  for (int r = threadIdx.x; r < Cfg::BM; r += 256) {
+    int4 info = (m0 + r < mend) ? a.rowinfo[m0 + r] : make_int4(0, 0, -1, -1);
+    float4 x = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (info.w >= 0) {
+      const int n = info.w / TS;
+      x = make_float4(a.lse_in[info.w], a.gxo[info.w], a.gyo[info.w], a.scale ? a.scale[n] : 1.f);
+    }
+    ri[r] = info;
+    rx[r] = x;
+  }
+  __syncthreads();
+  const TIn* enc = reinterpret_cast<const TIn*>(a.enc);
+  const TIn* dec = reinterpret_cast<const TIn*>(a.dec);
+  HSrcKC<Cfg, TIn> sa{enc, dec, ri, J};
+  WSrcMNC<Cfg, TIn> sb{reinterpret_cast<const TIn*>(a.W), v0, V, J, (V % WSrcMNC<Cfg, TIn>::NV) == 0};
+  KCLoader<Cfg, Cfg::BM, HSrcKC<Cfg, TIn>> la(sa);
+  MNCLoader<Cfg, Cfg::BN, WSrcMNC<Cfg, TIn>> lb(sb);
+  floatx4 acc[Cfg::FM][Cfg::FN];
+  gemm_mainloop<Cfg>(la, lb, 0, J, smem, acc);
+
+  const int lane = threadIdx.x & 63, wm = (threadIdx.x >> 6) >> 1;
+  typename Cfg::T* dl = reinterpret_cast<typename Cfg::T*>(a.dl);
+  float bj[Cfg::FN], colsum[Cfg::FN];
+#pragma unroll
+  for (int j = 0; j < Cfg::FN; ++j) {
+    const int col = v0 + tile_col<Cfg>(j);
+    bj[j] = (col < V) ? bias_at(a.bias, a.bf16, col) : 0.f;
+    colsum[j] = 0.f;
+  }
+#pragma unroll
+  for (int i = 0; i < Cfg::FM; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int row = tile_row<Cfg>(i, r);
+      const int m = m0 + row;
+      const int4 info = ri[row];
+      const float4 x = rx[row];
+      const float g = x.y + x.z;
+#pragma unroll
+      for (int j = 0; j < Cfg::FN; ++j) {
+        const int col = v0 + tile_col<Cfg>(j);
+        float d = 0.f;
+        if (info.w >= 0 && col < V) {
+          const float p = __expf(acc[i][j][r] + bj[j] - x.x);
+          float gd = g * p;
+          if (col == info.z) gd -= x.y;
+          if (col == a.b.blank) gd -= x.z;
+          d = x.w * gd;
+          if (a.logits_grad) a.logits_grad[(size_t)info.w * V + col] = d;
+        }
+        if (m < mend && col < a.ldl) {
+          if constexpr (BF) dl[(size_t)(m - cm0) * a.ldl + col] = f2bf(d);
+          else dl[(size_t)(m - cm0) * a.ldl + col] = d;
+        }
+        colsum[j] += d;
+      }
+    }
+  // db partial: sum over this wave's 64 rows, one row of db_part per (m-tile, wave row).
+  const int mt = m0 / Cfg::BM;
+#pragma unroll
+  for (int j = 0; j < Cfg::FN; ++j) {
+    float s = colsum[j];
+    s += __shfl_xor(s, 16, 64);
+    s += __shfl_xor(s, 32, 64);
+    const int col = v0 + tile_col<Cfg>(j);
+    if (lane < 16 && col < V) a.db_part[((size_t)mt * 2 + wm) * V + col] = s;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Backward 2: dh = dl W^T, dpre = dh (1 - h^2)
+// ---------------------------------------------------------------------------
+template <bool BF>
+__global__ __launch_bounds__(256) void joiner_dh_kernel(JoinerArgs a, int cm0, int cm1) {
+  using TIn = typename In<BF>::T;
+  using Cfg = typename In<BF>::Cfg;
+  __shared__ __align__(16) typename Cfg::T smem[Cfg::SMEM_BYTES / sizeof(typename Cfg::T)];
+  __shared__ int4 ri[Cfg::BM];
+  const int M = a.frame_off[a.b.N] * a.S;
+  const int mend = min(cm1, M);
+  const int m0 = cm0 + blockIdx.x * Cfg::BM;
+  if (m0 >= mend) return;
+  const int j0 = blockIdx.y * Cfg::BN;
+  const int V = a.V, J = a.J;
+  for (int r = threadIdx.x; r < Cfg::BM; r += 256)
+    ri[r] = (m0 + r < mend) ? a.rowinfo[m0 + r] : make_int4(0, 0, -1, -1);
+  __syncthreads();
+  const TIn* W = reinterpret_cast<const TIn*>(a.W);
+  DlSrcKC<Cfg> sa{reinterpret_cast<const typename Cfg::T*>(a.dl), m0, cm0, mend, a.ldl};
+  WtSrcKC<Cfg, TIn> sb{W, j0, J, V, (V % Cfg::KV) == 0};
+  KCLoader<Cfg, Cfg::BM, DlSrcKC<Cfg>> la(sa);
+  KCLoader<Cfg, Cfg::BN, WtSrcKC<Cfg, TIn>> lb(sb);
+  floatx4 acc[Cfg::FM][Cfg::FN];
+  gemm_mainloop<Cfg>(la, lb, 0, V, smem, acc);
+
+  const TIn* enc = reinterpret_cast<const TIn*>(a.enc);
+  const TIn* dec = reinterpret_cast<const TIn*>(a.dec);
+#pragma unroll
+  for (int i = 0; i < Cfg::FM; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int row = tile_row<Cfg>(i, r);
+      const int m = m0 + row;
+      if (m >= mend) continue;
+      const int4 info = ri[row];
+#pragma unroll
+      for (int j = 0; j < Cfg::FN; ++j) {
+        const int jj = j0 + tile_col<Cfg>(j);
+        if (jj >= J) continue;
+        float dp = 0.f;
+        if (info.w >= 0) {
+          const float h = fast_tanh(ld_in(enc, (size_t)info.x + jj) + ld_in(dec, (size_t)info.y + jj));
+          dp = acc[i][j][r] * (1.f - h * h);
+        }
+        a.dpre[(size_t)m * J + jj] = dp;
+      }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Backward 3: dW partial += h^T dl over one split of the chunk's rows
+// ---------------------------------------------------------------------------
+template <bool BF>
+__global__ __launch_bounds__(256) void joiner_dw_kernel(JoinerArgs a, int cm0, int cm1) {
+  using TIn = typename In<BF>::T;
+  using Cfg = typename In<BF>::Cfg;
+  __shared__ __align__(16) typename Cfg::T smem[Cfg::SMEM_BYTES / sizeof(typename Cfg::T)];
+  const int M = a.frame_off[a.b.N] * a.S;
+  const int mend = min(cm1, M);
+  const int j0 = blockIdx.x * Cfg::BM, v0 = blockIdx.y * Cfg::BN, z = blockIdx.z;
+  const int rows = cm1 - cm0;
+  const int per = ((rows + a.splits - 1) / a.splits + Cfg::BK - 1) / Cfg::BK * Cfg::BK;
+  const int kb = cm0 + z * per;
+  const int ke = min(kb + per, mend);
+  if (kb >= ke) return;
+  const int V = a.V, J = a.J;
+  const TIn* enc = reinterpret_cast<const TIn*>(a.enc);
+  const TIn* dec = reinterpret_cast<const TIn*>(a.dec);
+  HSrcMNC<Cfg, TIn> sa{enc, dec, a.rowinfo, j0, J, ke};
+  DlSrcMNC<Cfg> sb{reinterpret_cast<const typename Cfg::T*>(a.dl), cm0, ke, v0, a.ldl};
+  MNCLoader<Cfg, Cfg::BM, HSrcMNC<Cfg, TIn>> la(sa);
+  MNCLoader<Cfg, Cfg::BN, DlSrcMNC<Cfg>> lb(sb);
+  floatx4 acc[Cfg::FM][Cfg::FN];
+  gemm_mainloop<Cfg>(la, lb, kb, ke, smem, acc);
+  float* part = a.dw_part + (size_t)z * J * V;
+#pragma unroll
+  for (int i = 0; i < Cfg::FM; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int j = j0 + tile_row<Cfg>(i, r);
+      if (j >= J) continue;
+#pragma unroll
+      for (int jj = 0; jj < Cfg::FN; ++jj) {
+        const int v = v0 + tile_col<Cfg>(jj);
+        if (v < V) part[(size_t)j * V + v] += acc[i][jj][r];
+      }
+    }
+}
+
+// dW = sum of split partials, db = sum of per-tile column partials (fixed order).
+__global__ __launch_bounds__(256) void joiner_wsum_kernel(JoinerArgs a) {
+  const size_t JV = (size_t)a.J * a.V;
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < JV && a.W_grad) {
+    float s = 0.f;
+    for (int z = 0; z < a.splits; ++z) s += a.dw_part[(size_t)z * JV + i];
+    a.W_grad[i] = s;
+  }
+  if (i < (size_t)a.V && a.bias_grad) {
+    float s = 0.f;
+    for (int r = 0; r < a.n_db_rows; ++r) s += a.db_part[(size_t)r * a.V + i];
+    a.bias_grad[i] = s;
+  }
+}
+
+// d enc[n,t] = sum_s dpre(row(t,s)); d dec[n,u] = sum over t of dpre(row(t, u - p_t))
+// for 0 <= u - p_t < S. One block per output row; threads over J.
+__global__ __launch_bounds__(256) void joiner_encdec_kernel(JoinerArgs a) {
+  extern __shared__ int sp[];  // p_t of the utterance (dec rows only)
+  const int T = a.b.T, U1 = a.b.U + 1, S = a.S, J = a.J;
+  const int rowsper = T + U1;
+  const int n = blockIdx.x / rowsper, i = blockIdx.x - n * rowsper;
+  int Tn, Un;
+  utt_dims(a.b, n, Tn, Un);
+  const int off = a.frame_off[n];
+  if (i < T) {
+    float* out = a.enc_grad + ((size_t)n * T + i) * J;
+    for (int j = threadIdx.x; j < J; j += blockDim.x) {
+      float s = 0.f;
+      if (i < Tn) {
+        const float* d = a.dpre + (size_t)(off + i) * S * J + j;
+        for (int q = 0; q < S; ++q) s += d[(size_t)q * J];
+      }
+      out[j] = s;
+    }
+    return;
+  }
+  const int u = i - T;
+  float* out = a.dec_grad + ((size_t)n * U1 + u) * J;
+  if (u > Un) {
+    for (int j = threadIdx.x; j < J; j += blockDim.x) out[j] = 0.f;
+    return;
+  }
+  for (int t = threadIdx.x; t < Tn; t += blockDim.x) sp[t] = a.ranges[((size_t)n * T + t) * S];
+  __syncthreads();
+  for (int j = threadIdx.x; j < J; j += blockDim.x) {
+    float s = 0.f;
+    for (int t = 0; t < Tn; ++t) {
+      const int q = u - sp[t];
+      if (q >= 0 && q < S) s += a.dpre[((size_t)(off + t) * S + q) * J + j];
+    }
+    out[j] = s;
+  }
+}
+
+}  // namespace
+
+int joiner_nparts(int V) { return (V + 63) / 64; }
+int joiner_ldl(int V) { return (V + 7) / 8 * 8; }
+
+int joiner_bwd_chunk_rows(int N, int T, int S, int J, int V, int bf16) {
+  (void)J;
+  const long long mmax = (long long)N * T * S;
+  const long long bytes_per_row = (long long)joiner_ldl(V) * (bf16 ? 2 : 4);
+  const long long budget = 256ll << 20;  // one chunk of d(logits) stays within the 256 MB Infinity Cache
+  long long rows = budget / bytes_per_row;
+  rows = rows / 128 * 128;
+  if (rows < 128) rows = 128;
+  if (rows > mmax) rows = (mmax + 127) / 128 * 128;
+  return (int)rows;
+}
+
+int joiner_bwd_splits(int J, int V) {
+  const int tiles = ((J + 127) / 128) * ((V + 127) / 128);
+  int s = (512 + tiles - 1) / tiles;
+  if (s < 1) s = 1;
+  if (s > 32) s = 32;
+  return s;
+}
+
+int joiner_db_rows(int N, int T, int S) {
+  const long long mmax = (long long)N * T * S;
+  return (int)(((mmax + 127) / 128) * 2);
+}
+
+hipError_t launch_joiner_prep(const JoinerArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(joiner_prep_kernel, dim3(a.b.N), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_joiner_fwd(const JoinerArgs& a, hipStream_t s) {
+  const int mmax = a.b.N * a.b.T * a.S;
+  dim3 grid((mmax + 127) / 128, (a.V + 127) / 128);
+  if (a.bf16) hipLaunchKernelGGL(joiner_fwd_kernel<true>, grid, dim3(256), 0, s, a);
+  else hipLaunchKernelGGL(joiner_fwd_kernel<false>, grid, dim3(256), 0, s, a);
+  const size_t total = (size_t)a.b.N * a.b.T * a.S;
+  hipLaunchKernelGGL(joiner_combine_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_joiner_bwd(const JoinerArgs& a, hipStream_t s) {
+  const int mmax = a.b.N * a.b.T * a.S;
+  const int V = a.V, J = a.J;
+  hipError_t e = launch_fill_f32(a.dw_part, (size_t)a.splits * J * V, 0.f, s);
+  if (e != hipSuccess) return e;
+  e = launch_fill_f32(a.db_part, (size_t)a.n_db_rows * V, 0.f, s);
+  if (e != hipSuccess) return e;
+  if (a.logits_grad) {
+    e = launch_fill_f32(a.logits_grad, (size_t)mmax * V, 0.f, s);
+    if (e != hipSuccess) return e;
+  }
+  for (int cm0 = 0; cm0 < mmax; cm0 += a.chunk_rows) {
+    const int cm1 = (cm0 + a.chunk_rows < mmax) ? cm0 + a.chunk_rows : mmax;
+    const int mt = (cm1 - cm0 + 127) / 128;
+    dim3 g1(mt, (V + 127) / 128), g2(mt, (J + 127) / 128), g3((J + 127) / 128, (V + 127) / 128, a.splits);
+    if (a.bf16) {
+      hipLaunchKernelGGL(joiner_dlogits_kernel<true>, g1, dim3(256), 0, s, a, cm0, cm1);
+      hipLaunchKernelGGL(joiner_dh_kernel<true>, g2, dim3(256), 0, s, a, cm0, cm1);
+      hipLaunchKernelGGL(joiner_dw_kernel<true>, g3, dim3(256), 0, s, a, cm0, cm1);
+    } else {
+      hipLaunchKernelGGL(joiner_dlogits_kernel<false>, g1, dim3(256), 0, s, a, cm0, cm1);
+      hipLaunchKernelGGL(joiner_dh_kernel<false>, g2, dim3(256), 0, s, a, cm0, cm1);
+      hipLaunchKernelGGL(joiner_dw_kernel<false>, g3, dim3(256), 0, s, a, cm0, cm1);
+    }
+  }
+  const size_t JV = (size_t)J * V;
+  hipLaunchKernelGGL(joiner_wsum_kernel, dim3((unsigned)((JV + 255) / 256)), dim3(256), 0, s, a);
+  const int rows = a.b.N * (a.b.T + a.b.U + 1);
+  hipLaunchKernelGGL(joiner_encdec_kernel, dim3(rows), dim3(256), (size_t)a.b.T * sizeof(int), s, a);
+  return hipGetLastError();
+}

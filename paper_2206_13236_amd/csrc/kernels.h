@@ -1,0 +1,112 @@
+// Host-side launchers of the gfx950 kernels (internal to the library).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include "common.h"
+
+// ---- stage 1-2: trivial joiner, full lattice --------------------------------
+struct SimpleArgs {
+  BatchDev b;
+  int V;
+  const float* am;     // [N, T, V]
+  const float* lm;     // [N, U+1, V]
+  const float* scale;  // [N] or null
+  float* m_a;          // ws [N*T]
+  float* m_l;          // ws [N*(U+1)]
+  float* Z;            // ws [N, T, U+1]
+  float* px;           // [N, T, U+1] (caller's or ws)
+  float* py;
+  double* alpha;       // ws [N, T, U+1], log2 domain
+  double* beta;        // ws [N, T, U+1], log2 domain
+  float* loss;         // [N]
+  float* gx;           // [N, T, U+1]
+  float* gy;
+  int want_bwd;
+  float* Wt;           // ws [N, T, ldw]
+  int ldw;
+  float* ry;           // ws [N*T]
+  float* cx;           // ws [N*(U+1)]
+  float* cy;
+  float* am_grad;      // [N, T, V] or null
+  float* lm_grad;      // [N, U+1, V] or null
+};
+
+hipError_t launch_rowmax(const SimpleArgs& a, hipStream_t s);
+hipError_t launch_normalizer(const SimpleArgs& a, hipStream_t s);
+hipError_t launch_lattice(const SimpleArgs& a, hipStream_t s);
+hipError_t launch_simple_grads(const SimpleArgs& a, hipStream_t s);
+
+// ---- stage 3: pruning bounds -----------------------------------------------
+hipError_t launch_prune(const BatchDev& b, int S, const float* gx, const float* gy, int* ranges,
+                        hipStream_t s);
+size_t prune_smem_bytes(int T);
+
+// ---- stage 4: pruned joiner -----------------------------------------------
+struct JoinerArgs {
+  BatchDev b;
+  int S, J, V;
+  int bf16;
+  const void* enc;     // [N, T, J]
+  const void* dec;     // [N, U+1, J]
+  const void* W;       // [J, V]
+  const void* bias;    // [V] or null
+  const int* ranges;   // [N, T, S]
+  int* frame_off;      // ws [N+1]
+  int* frame_map;      // ws [N*T]
+  int4* rowinfo;       // ws [N*T*S]: enc_off, dec_off, sym (-1: none), out index (-1: absent)
+  // forward
+  float2* part;        // ws [N*T*S, nparts] (max, sum exp) per 64-column slice
+  int nparts;
+  float* tgt;          // ws [N*T*S]
+  float* blk;          // ws [N*T*S]
+  float* px;           // [N, T, S]
+  float* py;
+  float* lse;
+  // backward
+  const float* lse_in;
+  const float* gxo;    // band occupations [N, T, S]
+  const float* gyo;
+  const float* scale;  // [N] or null
+  void* dl;            // ws chunk [chunk_rows, ldl] (f32 or bf16)
+  int ldl;
+  int chunk_rows;
+  float* dpre;         // ws [N*T*S, J]
+  float* dw_part;      // ws [splits, J, V]
+  int splits;
+  float* db_part;      // ws [n_db_rows, V]
+  int n_db_rows;
+  float* enc_grad;
+  float* dec_grad;
+  float* W_grad;
+  float* bias_grad;
+  float* logits_grad;
+};
+
+hipError_t launch_joiner_prep(const JoinerArgs& a, hipStream_t s);
+hipError_t launch_joiner_fwd(const JoinerArgs& a, hipStream_t s);
+hipError_t launch_joiner_bwd(const JoinerArgs& a, hipStream_t s);
+int joiner_bwd_chunk_rows(int N, int T, int S, int J, int V, int bf16);
+int joiner_bwd_splits(int J, int V);
+int joiner_db_rows(int N, int T, int S);
+int joiner_nparts(int V);
+int joiner_ldl(int V);
+
+// ---- stage 4: pruned recursion ---------------------------------------------
+struct BandArgs {
+  BatchDev b;
+  int S;
+  const float* px;     // [N, T, S]
+  const float* py;
+  const int* ranges;   // [N, T, S]
+  double* alpha;       // ws [N, T, S] log2 domain
+  double* beta;
+  float* loss;
+  float* gx;           // [N, T, S] or null
+  float* gy;
+};
+hipError_t launch_band(const BandArgs& a, hipStream_t s);
+size_t band_smem_bytes(int T, int S);
+
+// ---- generic fills -----------------------------------------------------------
+hipError_t launch_fill_f32(float* p, size_t n, float v, hipStream_t s);

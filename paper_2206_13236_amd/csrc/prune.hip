@@ -1,0 +1,116 @@
+// Stage 3: pruning bounds (Sec. 3.2.2).
+//
+// For every frame t the locally optimal start p_t maximises Eq. (8),
+//   score(t,p) = -gx(t,p-1) + gy(t,p) + gy(t,p+1) + ... + gy(t,p+S-1),
+// over p in [0, P], P = max(0, U-S+1) ("green arcs minus red arc"; Eq. (7)
+// is the S = 4, p = 2 instance). The sum is evaluated in fp32 in exactly that
+// order (no contraction: additions only), y'(t,-1) counts as 0 and slots above
+// U add 0, so equal inputs give bit-identical bounds on any IEEE fp32 machine.
+// Ties go to the smallest p and NaN never wins.
+//
+// The raw bounds are clamped to the envelope [P - (S-1)(T-1-t), min(P, (S-1)t)]
+// (the band must hold the start node at t = 0 and the final node at t = T-1,
+// and consecutive starts may differ by at most S-1), then made consistent with
+// Eq. (9) (monotone) and Eq. (10) (no skip) by the procedure the paper's
+// LaTeX source gives in a commented-out block of Sec. 3.2.2: suffix minimum,
+// reflect by (S-1)t, suffix minimum, reflect back, max with 0. All of that is
+// integer arithmetic.
+//
+// One workgroup per utterance. Each wave scores one frame at a time with the
+// lanes spread over p (coalesced loads of the occupation row), then reduces
+// (score, p) to the first maximum. The two suffix minima are Hillis-Steele
+// scans over LDS (min is exact and associative, so the order does not matter).
+#include "kernels.h"
+
+namespace {
+
+constexpr int kPruneThreads = 1024;
+
+// Lexicographic (largest score, then smallest p); NaN compares as -inf.
+DEV void better(float& bs, int& bp, float s, int p) {
+  if (s > bs || (s == bs && p < bp)) {
+    bs = s;
+    bp = p;
+  }
+}
+
+DEV void suffix_min(int* a, int* tmp, int Tn) {
+  int* src = a;
+  int* dst = tmp;
+  for (int off = 1; off < Tn; off <<= 1) {
+    for (int t = threadIdx.x; t < Tn; t += kPruneThreads)
+      dst[t] = (t + off < Tn) ? min(src[t], src[t + off]) : src[t];
+    __syncthreads();
+    int* x = src;
+    src = dst;
+    dst = x;
+  }
+  if (src != a) {
+    for (int t = threadIdx.x; t < Tn; t += kPruneThreads) a[t] = src[t];
+    __syncthreads();
+  }
+}
+
+__global__ __launch_bounds__(kPruneThreads) void prune_kernel(BatchDev b, int S, const float* __restrict__ gx,
+                                                              const float* __restrict__ gy,
+                                                              int* __restrict__ ranges) {
+#pragma clang fp contract(off)
+  extern __shared__ int sp[];  // [2 * T]
+  int* p = sp;
+  int* tmp = sp + b.T;
+  const int n = blockIdx.x;
+  const int T = b.T, U1 = b.U + 1;
+  int Tn, Un;
+  utt_dims(b, n, Tn, Un);
+  const int P = max(0, Un - S + 1);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = kPruneThreads / 64;
+  for (int t = wave; t < Tn; t += nw) {
+    const float* gxr = gx + ((size_t)n * T + t) * U1;
+    const float* gyr = gy + ((size_t)n * T + t) * U1;
+    float bs = kNegInfF;
+    int bp = 0;
+    for (int p0 = 0; p0 <= P; p0 += 64) {
+      const int q = p0 + lane;
+      if (q <= P) {
+        float acc = (q == 0) ? 0.0f : -gxr[q - 1];
+        for (int k = 0; k < S; ++k) {
+          const int u = q + k;
+          acc = acc + ((u <= Un) ? gyr[u] : 0.0f);
+        }
+        better(bs, bp, (acc != acc) ? kNegInfF : acc, q);
+      }
+    }
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+      const float os = __shfl_xor(bs, off, 64);
+      const int op = __shfl_xor(bp, off, 64);
+      better(bs, bp, os, op);
+    }
+    if (lane == 0) {
+      const int lo = P - (S - 1) * (Tn - 1 - t);
+      const int hi = min(P, (S - 1) * t);
+      p[t] = min(max(bp, lo), hi);
+    }
+  }
+  __syncthreads();
+  suffix_min(p, tmp, Tn);
+  for (int t = threadIdx.x; t < Tn; t += kPruneThreads) p[t] = (S - 1) * t - p[t];
+  __syncthreads();
+  suffix_min(p, tmp, Tn);
+  int* out = ranges + (size_t)n * T * S;
+  for (int i = threadIdx.x; i < T * S; i += kPruneThreads) {
+    const int t = i / S, s = i - t * S;
+    out[i] = (t < Tn) ? max(0, (S - 1) * t - p[t]) + s : s;
+  }
+}
+
+}  // namespace
+
+size_t prune_smem_bytes(int T) { return (size_t)2 * T * sizeof(int); }
+
+hipError_t launch_prune(const BatchDev& b, int S, const float* gx, const float* gy, int* ranges,
+                        hipStream_t s) {
+  hipLaunchKernelGGL(prune_kernel, dim3(b.N), dim3(kPruneThreads), prune_smem_bytes(b.T), s, b, S, gx, gy,
+                     ranges);
+  return hipGetLastError();
+}

@@ -1,0 +1,380 @@
+// Stage 1 of the pruned RNN-T loss: the trivial joiner of Sec. 3.1.
+//
+//   L_trivial(t,u,v) = am[t,v] + lm[u,v] - Z(t,u)               (Eq. (5))
+//   Z(t,u) = log sum_v exp(am[t,v] + lm[u,v])                    (Eq. (6))
+//
+// Z is evaluated as the paper suggests, as an ordinary matrix product after
+// applying offsets: with m_a[t] = max_v am[t,v] and m_l[u] = max_v lm[u,v],
+//   Z(t,u) = m_a[t] + m_l[u] + log( sum_v e^{am[t,v]-m_a[t]} e^{lm[u,v]-m_l[u]} ),
+// every factor is <= 1 so the product cannot overflow. The contraction over v
+// runs on fp32 MFMA; the exponentials are formed while staging tiles to LDS
+// and the px/py lookups (Eqs. (1)-(2)) are fused into the epilogue.
+//
+// The gradient w.r.t. am and lm (the simple loss is trained, Sec. 3.3) is two
+// more contractions of the same shape:
+//   d am[t,v] = sc (e^{am-m_a}[t,v] * sum_u W(t,u) e^{lm-m_l}[u,v]
+//                   - sum_u gx(t,u) [v = y_{u+1}] - sum_u gy(t,u) [v = blank])
+//   d lm[u,v] = sc (e^{lm-m_l}[u,v] * sum_t W(t,u) e^{am-m_a}[t,v]
+//                   - sum_t gx(t,u) [v = y_{u+1}] - sum_t gy(t,u) [v = blank])
+// with W(t,u) = (gx + gy)(t,u) e^{m_a + m_l - Z}: the log-softmax backward
+// (gradient of the target/blank entries minus softmax times their sum).
+#include <float.h>
+
+#include "gemm.h"
+#include "kernels.h"
+
+namespace {
+
+DEV float keep_nan_max(float m, float x) { return (x > m || x != x) ? x : m; }
+
+// ---------------------------------------------------------------------------
+// Row maxima of am (rows t < T_n) and lm (rows u <= U_n): one wave per row.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void rowmax_kernel(const float* __restrict__ x, int N, int R, int V,
+                                                     BatchDev b, int is_lm, float* __restrict__ out) {
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= N * R) return;
+  const int n = row / R, i = row % R;
+  int Tn, Un;
+  utt_dims(b, n, Tn, Un);
+  const int lim = is_lm ? Un + 1 : Tn;
+  if (i >= lim) {
+    if (lane == 0) out[row] = 0.f;
+    return;
+  }
+  const float* r = x + (size_t)row * V;
+  float m = kNegInfF;
+  if ((V & 3) == 0) {
+    const float4* r4 = reinterpret_cast<const float4*>(r);
+    for (int v = lane; v < V / 4; v += 64) {
+      float4 q = r4[v];
+      m = keep_nan_max(m, q.x);
+      m = keep_nan_max(m, q.y);
+      m = keep_nan_max(m, q.z);
+      m = keep_nan_max(m, q.w);
+    }
+  } else {
+    for (int v = lane; v < V; v += 64) m = keep_nan_max(m, r[v]);
+  }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) m = keep_nan_max(m, __shfl_xor(m, off, 64));
+  if (lane == 0) out[row] = m;
+}
+
+// exp(x[row][k..k+3] - mx) with zeros beyond the row end / invalid rows.
+DEV void exp4_row(const float* rowp, float mx, int k, int V, bool valid, float (&v)[4]) {
+  if (!valid) {
+    v[0] = v[1] = v[2] = v[3] = 0.f;
+    return;
+  }
+  if (((V & 3) == 0) && (k + 4 <= V)) {
+    float4 q = *reinterpret_cast<const float4*>(rowp + k);
+    v[0] = expf(q.x - mx);
+    v[1] = expf(q.y - mx);
+    v[2] = expf(q.z - mx);
+    v[3] = expf(q.w - mx);
+  } else {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) v[i] = (k + i < V) ? expf(rowp[k + i] - mx) : 0.f;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Normaliser contraction, per utterance: C[t][u] = sum_v Ea[t][v] El[u][v].
+// ---------------------------------------------------------------------------
+using NormCfg = GemmCfg<64, 64, 32, false>;
+
+struct NormSrcA {  // A(t, v) = exp(am[t,v] - m_a[t]), k-contiguous
+  const float* am;  // utterance base [T][V]
+  const float* ma;
+  int t0, Tn, V;
+  DEV void kc_fetch(int row, int k, float (&v)[4]) const {
+    const int t = t0 + row;
+    const bool ok = t < Tn;
+    exp4_row(am + (size_t)(ok ? t : 0) * V, ok ? ma[t] : 0.f, k, V, ok, v);
+  }
+};
+struct NormSrcB {  // B(v, u) = exp(lm[u,v] - m_l[u]); global lm[u][v] is k-contiguous per u
+  const float* lm;
+  const float* ml;
+  int u0, Un, V;
+  DEV void kc_fetch(int row, int k, float (&v)[4]) const {
+    const int u = u0 + row;
+    const bool ok = u <= Un;
+    exp4_row(lm + (size_t)(ok ? u : 0) * V, ok ? ml[u] : 0.f, k, V, ok, v);
+  }
+};
+
+__global__ __launch_bounds__(256) void normalizer_kernel(SimpleArgs a) {
+  using Cfg = NormCfg;
+  __shared__ __align__(16) float smem[Cfg::SMEM_BYTES / sizeof(float)];
+  const int n = blockIdx.z;
+  const int t0 = blockIdx.x * Cfg::BM, u0 = blockIdx.y * Cfg::BN;
+  const int T = a.b.T, U1 = a.b.U + 1, V = a.V;
+  int Tn, Un;
+  utt_dims(a.b, n, Tn, Un);
+  const size_t base = (size_t)n * T * U1;
+  const bool active = (t0 < Tn) && (u0 <= Un);
+  floatx4 acc[Cfg::FM][Cfg::FN];
+  if (active) {
+    NormSrcA sa{a.am + (size_t)n * T * V, a.m_a + (size_t)n * T, t0, Tn, V};
+    NormSrcB sb{a.lm + (size_t)n * U1 * V, a.m_l + (size_t)n * U1, u0, Un, V};
+    KCLoader<Cfg, Cfg::BM, NormSrcA> la(sa);
+    KCLoader<Cfg, Cfg::BN, NormSrcB> lb(sb);
+    gemm_mainloop<Cfg>(la, lb, 0, V, smem, acc);
+  }
+  const int blank = a.b.blank;
+  const float* amn = a.am + (size_t)n * T * V;
+  const float* lmn = a.lm + (size_t)n * U1 * V;
+#pragma unroll
+  for (int j = 0; j < Cfg::FN; ++j) {
+    const int u = u0 + tile_col<Cfg>(j);
+    if (u >= U1) continue;
+    bool sym_ok = true;
+    const int y = (u < Un) ? symbol_at(a.b, n, u, V, sym_ok) : 0;
+    const float ml = (u <= Un) ? a.m_l[(size_t)n * U1 + u] : 0.f;
+#pragma unroll
+    for (int i = 0; i < Cfg::FM; ++i)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int t = t0 + tile_row<Cfg>(i, r);
+        if (t >= T) continue;
+        const size_t idx = base + (size_t)t * U1 + u;
+        if (active && t < Tn && u <= Un) {
+          float s = acc[i][j][r];
+          s = (s > FLT_MIN || s != s) ? s : FLT_MIN;
+          const float z = a.m_a[(size_t)n * T + t] + ml + logf(s);
+          a.Z[idx] = z;
+          a.py[idx] = amn[(size_t)t * V + blank] + lmn[(size_t)u * V + blank] - z;
+          a.px[idx] = (u < Un) ? amn[(size_t)t * V + y] + lmn[(size_t)u * V + y] - z : kNegInfF;
+        } else {
+          a.Z[idx] = 0.f;
+          a.px[idx] = kNegInfF;
+          a.py[idx] = kNegInfF;
+        }
+      }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// d am: per utterance C[t][v] = sum_u Wt[t][u] El[u][v]  (K = U_n + 1)
+// ---------------------------------------------------------------------------
+using DamCfg = GemmCfg<64, 128, 32, false>;
+
+struct WtSrcKC {  // A(t, u) = Wt[t][u], rows padded to ldw (multiple of 4, zero-filled)
+  const float* Wt;
+  int t0, Tn, ldw;
+  DEV void kc_fetch(int row, int k, float (&v)[4]) const {
+    const int t = t0 + row;
+    if (t < Tn && k < ldw) {
+      float4 q = *reinterpret_cast<const float4*>(Wt + (size_t)t * ldw + k);
+      v[0] = q.x; v[1] = q.y; v[2] = q.z; v[3] = q.w;
+    } else {
+      v[0] = v[1] = v[2] = v[3] = 0.f;
+    }
+  }
+};
+struct ExpSrcMNC {  // B(k, col) = exp(x[k][c0+col] - mx[k]) for rows k < klim, cols < V
+  const float* x;  // [rows][V]
+  const float* mx;
+  int c0, klim, V;
+  DEV void mnc_fetch(int k, int col, float (&v)[4]) const {
+    exp4_row(x + (size_t)(k < klim ? k : 0) * V, k < klim ? mx[k] : 0.f, c0 + col, V, k < klim, v);
+  }
+};
+
+__global__ __launch_bounds__(256) void dam_kernel(SimpleArgs a) {
+  using Cfg = DamCfg;
+  __shared__ __align__(16) float smem[Cfg::SMEM_BYTES / sizeof(float)];
+  const int n = blockIdx.z;
+  const int t0 = blockIdx.x * Cfg::BM, v0 = blockIdx.y * Cfg::BN;
+  const int T = a.b.T, U1 = a.b.U + 1, V = a.V;
+  int Tn, Un;
+  utt_dims(a.b, n, Tn, Un);
+  const bool active = t0 < Tn;
+  floatx4 acc[Cfg::FM][Cfg::FN];
+  if (active) {
+    WtSrcKC sa{a.Wt + (size_t)n * T * a.ldw, t0, Tn, a.ldw};
+    ExpSrcMNC sb{a.lm + (size_t)n * U1 * V, a.m_l + (size_t)n * U1, v0, Un + 1, V};
+    KCLoader<Cfg, Cfg::BM, WtSrcKC> la(sa);
+    MNCLoader<Cfg, Cfg::BN, ExpSrcMNC> lb(sb);
+    gemm_mainloop<Cfg>(la, lb, 0, Un + 1, smem, acc);
+  }
+  const float* amn = a.am + (size_t)n * T * V;
+  const float* ma = a.m_a + (size_t)n * T;
+  const float* gxn = a.gx + (size_t)n * T * U1;
+  float* out = a.am_grad + (size_t)n * T * V;
+  // dense part: e^{am - m_a} * acc
+  float res[Cfg::FM][Cfg::FN][4];
+#pragma unroll
+  for (int i = 0; i < Cfg::FM; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int t = t0 + tile_row<Cfg>(i, r);
+      const bool tv = active && t < Tn;
+      const float mx = tv ? ma[t] : 0.f;
+#pragma unroll
+      for (int j = 0; j < Cfg::FN; ++j) {
+        const int v = v0 + tile_col<Cfg>(j);
+        res[i][j][r] = (tv && v < V) ? expf(amn[(size_t)t * V + v] - mx) * acc[i][j][r] : 0.f;
+      }
+    }
+  if (active) {
+    // sparse part: target columns, in ascending u (deterministic)
+    for (int u = 0; u < Un; ++u) {
+      bool ok = true;
+      const int y = symbol_at(a.b, n, u, V, ok);
+      if (y < v0 || y >= v0 + Cfg::BN) continue;
+#pragma unroll
+      for (int j = 0; j < Cfg::FN; ++j) {
+        if (v0 + tile_col<Cfg>(j) != y) continue;
+#pragma unroll
+        for (int i = 0; i < Cfg::FM; ++i)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int t = t0 + tile_row<Cfg>(i, r);
+            if (t < Tn) res[i][j][r] -= gxn[(size_t)t * U1 + u];
+          }
+      }
+    }
+    const int blank = a.b.blank;
+    if (blank >= v0 && blank < v0 + Cfg::BN) {
+#pragma unroll
+      for (int j = 0; j < Cfg::FN; ++j) {
+        if (v0 + tile_col<Cfg>(j) != blank) continue;
+#pragma unroll
+        for (int i = 0; i < Cfg::FM; ++i)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int t = t0 + tile_row<Cfg>(i, r);
+            if (t < Tn) res[i][j][r] -= a.ry[(size_t)n * T + t];
+          }
+      }
+    }
+  }
+  const float sc = a.scale ? a.scale[n] : 1.f;
+#pragma unroll
+  for (int i = 0; i < Cfg::FM; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int t = t0 + tile_row<Cfg>(i, r);
+      if (t >= T) continue;
+#pragma unroll
+      for (int j = 0; j < Cfg::FN; ++j) {
+        const int v = v0 + tile_col<Cfg>(j);
+        if (v < V) out[(size_t)t * V + v] = (active && t < Tn) ? sc * res[i][j][r] : 0.f;
+      }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// d lm: per utterance C[u][v] = sum_t Wt[t][u] Ea[t][v]  (K = T_n)
+// ---------------------------------------------------------------------------
+using DlmCfg = GemmCfg<64, 128, 32, false>;
+
+struct WtSrcMNC {  // A(u, t) = Wt[t][u]: global is [t][u], u-contiguous
+  const float* Wt;
+  int u0, Tn, ldw;
+  DEV void mnc_fetch(int k, int col, float (&v)[4]) const {
+    const int u = u0 + col;
+    if (k < Tn && u < ldw) {
+      float4 q = *reinterpret_cast<const float4*>(Wt + (size_t)k * ldw + u);
+      v[0] = q.x; v[1] = q.y; v[2] = q.z; v[3] = q.w;
+    } else {
+      v[0] = v[1] = v[2] = v[3] = 0.f;
+    }
+  }
+};
+
+__global__ __launch_bounds__(256) void dlm_kernel(SimpleArgs a) {
+  using Cfg = DlmCfg;
+  __shared__ __align__(16) float smem[Cfg::SMEM_BYTES / sizeof(float)];
+  const int n = blockIdx.z;
+  const int u0 = blockIdx.x * Cfg::BM, v0 = blockIdx.y * Cfg::BN;
+  const int T = a.b.T, U1 = a.b.U + 1, V = a.V;
+  int Tn, Un;
+  utt_dims(a.b, n, Tn, Un);
+  const bool active = u0 <= Un;
+  floatx4 acc[Cfg::FM][Cfg::FN];
+  if (active) {
+    WtSrcMNC sa{a.Wt + (size_t)n * T * a.ldw, u0, Tn, a.ldw};
+    ExpSrcMNC sb{a.am + (size_t)n * T * V, a.m_a + (size_t)n * T, v0, Tn, V};
+    MNCLoader<Cfg, Cfg::BM, WtSrcMNC> la(sa);
+    MNCLoader<Cfg, Cfg::BN, ExpSrcMNC> lb(sb);
+    gemm_mainloop<Cfg>(la, lb, 0, Tn, smem, acc);
+  }
+  const float* lmn = a.lm + (size_t)n * U1 * V;
+  const float sc = a.scale ? a.scale[n] : 1.f;
+  const int blank = a.b.blank;
+  float* out = a.lm_grad + (size_t)n * U1 * V;
+#pragma unroll
+  for (int i = 0; i < Cfg::FM; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int u = u0 + tile_row<Cfg>(i, r);
+      if (u >= U1) continue;
+      const bool uv = active && u <= Un;
+      const float ml = uv ? a.m_l[(size_t)n * U1 + u] : 0.f;
+      bool ok = true;
+      const int y = (uv && u < Un) ? symbol_at(a.b, n, u, V, ok) : -1;
+      const float cxu = uv ? a.cx[(size_t)n * U1 + u] : 0.f;
+      const float cyu = uv ? a.cy[(size_t)n * U1 + u] : 0.f;
+#pragma unroll
+      for (int j = 0; j < Cfg::FN; ++j) {
+        const int v = v0 + tile_col<Cfg>(j);
+        if (v >= V) continue;
+        float g = 0.f;
+        if (uv) {
+          g = expf(lmn[(size_t)u * V + v] - ml) * acc[i][j][r];
+          if (v == y) g -= cxu;
+          if (v == blank) g -= cyu;
+          g *= sc;
+        }
+        out[(size_t)u * V + v] = g;
+      }
+    }
+}
+
+__global__ void fill_f32_kernel(float* p, size_t n, float v) {
+  size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  size_t stride = (size_t)gridDim.x * blockDim.x;
+  for (; i < n; i += stride) p[i] = v;
+}
+
+}  // namespace
+
+hipError_t launch_rowmax(const SimpleArgs& a, hipStream_t s) {
+  const int N = a.b.N, T = a.b.T, U1 = a.b.U + 1;
+  hipLaunchKernelGGL(rowmax_kernel, dim3((N * T + 3) / 4), dim3(256), 0, s, a.am, N, T, a.V, a.b, 0, a.m_a);
+  hipLaunchKernelGGL(rowmax_kernel, dim3((N * U1 + 3) / 4), dim3(256), 0, s, a.lm, N, U1, a.V, a.b, 1, a.m_l);
+  return hipGetLastError();
+}
+
+hipError_t launch_normalizer(const SimpleArgs& a, hipStream_t s) {
+  const int T = a.b.T, U1 = a.b.U + 1;
+  dim3 grid((T + NormCfg::BM - 1) / NormCfg::BM, (U1 + NormCfg::BN - 1) / NormCfg::BN, a.b.N);
+  hipLaunchKernelGGL(normalizer_kernel, grid, dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_simple_grads(const SimpleArgs& a, hipStream_t s) {
+  const int T = a.b.T, U1 = a.b.U + 1, V = a.V;
+  if (a.am_grad) {
+    dim3 grid((T + DamCfg::BM - 1) / DamCfg::BM, (V + DamCfg::BN - 1) / DamCfg::BN, a.b.N);
+    hipLaunchKernelGGL(dam_kernel, grid, dim3(256), 0, s, a);
+  }
+  if (a.lm_grad) {
+    dim3 grid((U1 + DlmCfg::BM - 1) / DlmCfg::BM, (V + DlmCfg::BN - 1) / DlmCfg::BN, a.b.N);
+    hipLaunchKernelGGL(dlm_kernel, grid, dim3(256), 0, s, a);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_fill_f32(float* p, size_t n, float v, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  size_t blocks = (n + 255) / 256;
+  if (blocks > 4096) blocks = 4096;
+  hipLaunchKernelGGL(fill_f32_kernel, dim3((unsigned)blocks), dim3(256), 0, s, p, n, v);
+  return hipGetLastError();
+}

@@ -1,0 +1,127 @@
+"""Host-side checks of the C ABI (CPU only: no kernel is launched).
+
+The library must load on a machine without a GPU, export every function the
+header declares, answer the workspace queries, and reject bad arguments with
+the documented status before any HIP call.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "rnnt_pruned.h")
+
+
+@pytest.fixture(scope="module")
+def L():
+    from paper_2206_13236_amd import _native
+    if not os.path.exists(_native.LIB_PATH):
+        from paper_2206_13236_amd.build import build
+        build()
+    return _native.lib()
+
+
+def _declared():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(rnnt_[a-z_]+)\s*\(", src)))
+
+
+def test_header_declares_the_entry_points():
+    names = _declared()
+    for n in ("rnnt_simple_loss", "rnnt_prune_ranges", "rnnt_pruned_joiner", "rnnt_pruned_loss",
+              "rnnt_pruned_joiner_backward", "rnnt_last_error", "rnnt_abi_version"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol(L):
+    from paper_2206_13236_amd import _native
+    missing = [n for n in _declared() if not hasattr(L, n)]
+    assert not missing, f"not exported: {missing}"
+    assert set(_declared()) == set(_native.SIGNATURES), "binding signatures out of sync with the header"
+    assert L.rnnt_abi_version() == 1
+
+
+def test_workspace_queries(L):
+    from paper_2206_13236_amd import _native as N
+    a = L.rnnt_simple_loss_workspace_size(16, 250, 60, 500)
+    assert a > 0 and a % 256 == 0 or a > 0
+    assert L.rnnt_simple_loss_workspace_size(16, 250, 60, 500) == a
+    assert L.rnnt_simple_loss_workspace_size(0, 250, 60, 500) == 0
+    # bigger shapes need more
+    assert L.rnnt_simple_loss_workspace_size(16, 250, 61, 500) >= a
+    f = L.rnnt_pruned_joiner_workspace_size(16, 250, 5, 512, 500, N.RNNT_F32)
+    assert f > 0
+    b32 = L.rnnt_pruned_joiner_backward_workspace_size(16, 250, 60, 5, 512, 500, N.RNNT_F32)
+    b16 = L.rnnt_pruned_joiner_backward_workspace_size(16, 250, 60, 5, 512, 500, N.RNNT_BF16)
+    assert b32 > b16 > 0
+    assert L.rnnt_pruned_loss_workspace_size(16, 250, 5) == 2 * 16 * 250 * 5 * 8 or \
+        L.rnnt_pruned_loss_workspace_size(16, 250, 5) >= 2 * 16 * 250 * 5 * 8
+
+
+def _batch(N=2, T=10, U=3):
+    from paper_2206_13236_amd._native import RnntBatch
+    # fake device addresses: validation never dereferences them
+    return RnntBatch(N, T, U, 0x1000, 0x2000, 0x3000, 0)
+
+
+def _err(L):
+    return L.rnnt_last_error().decode()
+
+
+def test_validation_statuses(L):
+    from paper_2206_13236_amd import _native as N
+    b = _batch()
+    pb = ctypes.byref(b)
+    fake = ctypes.c_void_p(0x4000)
+    # NULL batch
+    assert L.rnnt_prune_ranges(None, 4, fake, fake, fake, None) == N.RNNT_EINVAL
+    assert "NULL" in _err(L)
+    # S out of range
+    assert L.rnnt_prune_ranges(pb, 0, fake, fake, fake, None) == N.RNNT_EUNSUPPORTED
+    assert L.rnnt_prune_ranges(pb, 33, fake, fake, fake, None) == N.RNNT_EUNSUPPORTED
+    # missing required output
+    assert L.rnnt_prune_ranges(pb, 4, fake, fake, None, None) == N.RNNT_EINVAL
+    # simple loss: blank outside [0, V)
+    b2 = _batch()
+    b2.blank = 16
+    assert L.rnnt_simple_loss(ctypes.byref(b2), 16, fake, fake, None, fake, fake, fake, None, None, None, None,
+                              fake, 1 << 30, None) == N.RNNT_EINVAL
+    # simple loss: workspace missing / too small / misaligned
+    assert L.rnnt_simple_loss(pb, 16, fake, fake, None, fake, fake, fake, None, None, None, None,
+                              None, 0, None) == N.RNNT_EWORKSPACE
+    assert L.rnnt_simple_loss(pb, 16, fake, fake, None, fake, fake, fake, None, None, None, None,
+                              fake, 16, None) == N.RNNT_EWORKSPACE
+    assert L.rnnt_simple_loss(pb, 16, fake, fake, None, fake, fake, fake, None, None, None, None,
+                              ctypes.c_void_p(0x4004), 1 << 30, None) == N.RNNT_EWORKSPACE
+    # px without py
+    assert L.rnnt_simple_loss(pb, 16, fake, fake, None, fake, fake, fake, fake, None, None, None,
+                              fake, 1 << 30, None) == N.RNNT_EINVAL
+    # negative sizes
+    bad = _batch(N=0)
+    assert L.rnnt_pruned_loss(ctypes.byref(bad), 4, fake, fake, fake, fake, None, None, fake, 1 << 30,
+                              None) == N.RNNT_EINVAL
+    # U beyond the lattice limit
+    big = _batch(U=1024)
+    assert L.rnnt_prune_ranges(ctypes.byref(big), 4, fake, fake, fake, None) == N.RNNT_EUNSUPPORTED
+    # joiner: J not a multiple of 8, bad dtype
+    assert L.rnnt_pruned_joiner(pb, 4, 12, 16, N.RNNT_F32, fake, fake, fake, None, fake, fake, fake, fake,
+                                fake, 1 << 30, None) == N.RNNT_EUNSUPPORTED
+    assert L.rnnt_pruned_joiner(pb, 4, 16, 16, 7, fake, fake, fake, None, fake, fake, fake, fake,
+                                fake, 1 << 30, None) == N.RNNT_EINVAL
+    # backward: enc_grad required
+    assert L.rnnt_pruned_joiner_backward(pb, 4, 16, 16, N.RNNT_F32, fake, fake, fake, None, fake, fake, fake,
+                                         fake, None, None, fake, None, None, None, fake, 1 << 30,
+                                         None) == N.RNNT_EINVAL
+    # a success clears the message; the last failure leaves one
+    assert _err(L) != ""
+
+
+def test_python_binding_checks_shapes_on_cpu():
+    import torch
+    import paper_2206_13236_amd as P
+    with pytest.raises(ValueError):
+        P.Batch(torch.zeros(2, dtype=torch.int32), torch.zeros(2, dtype=torch.int32),
+                torch.zeros(2, 3, dtype=torch.int32), 10, 3)  # CPU tensors are rejected
