@@ -1,0 +1,181 @@
+#!/usr/bin/env python
+"""Throughput of the pruned RNN-T loss (forward + backward) on one MI355X.
+
+One step is the whole path on one batch resident in HBM:
+  trivial joiner + full-lattice forward/backward + d am, d lm (simple loss,
+  scaled 0.5 as in Sec. 3.3), pruning bounds, the full joiner on the pruned
+  (t, u) pairs, the pruned recursion, and the joiner backward to d enc, d dec,
+  dW, db.
+The workload is the BPE-sized batch (N=16, T ~ U[150,250], U ~ U[20,60],
+V=500, S=5, J=512, fp32), synthetic and seeded; frames = sum of valid T_n.
+
+Prints one JSON line: frames/s, peak HBM bytes, the roofline of the dominant
+contraction (HIP events recorded by the library on the launch stream during
+the timed steps) and the CPU oracle's throughput on the host cores.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_TFLOPS = {"f32": 157.3, "bf16": 2516.6}  # MI355X dense MFMA
+PEAK_HBM_GBS = 8000.0
+
+WORKLOAD_TEXT = {
+    "bpe": "bpe: N=16, T~U[150,250], U~U[20,60], V=500, S=5, J=512, fp32 joiner",
+    "long": "long: N=32, T~U[300,500], U~U[50,100], V=500, S=5, J=512, bf16 joiner",
+    "largev": "largev: N=16, T~U[200,300], U~U[40,80], V=5000 (Zipf 1.1 symbols), S=5, J=512, fp32 joiner",
+    "stress": "stress: N=8, T~U[800,1000], U~U[200,300] (25% U=T/3), V=8000, S=10, J=768, bf16 joiner",
+}
+
+
+def _cpu_baseline(b, S, budget_s: float) -> dict:
+    """The CPU oracle (as is) on the first utterances of the same batch, one thread."""
+    import numpy as np
+    from threadpoolctl import threadpool_limits
+
+    import oracle as O
+    frames = 0
+    done = 0
+    t0 = time.perf_counter()
+    with threadpool_limits(1):
+        for n in range(b.N):
+            sl = slice(n, n + 1)
+            s1 = O.simple_stage(b.am[sl], b.lm[sl], b.symbols[sl], b.t_len[sl], b.u_len[sl], b.wl.blank,
+                                scale=np.full(1, 0.5))
+            r = O.prune_ranges(s1["gx"], s1["gy"], b.t_len[sl], b.u_len[sl], S)
+            O.pruned_stage(b.enc[sl], b.dec[sl], b.W, b.bias, r, b.symbols[sl], b.t_len[sl], b.u_len[sl],
+                           b.wl.blank)
+            frames += int(b.t_len[n])
+            done += 1
+            if time.perf_counter() - t0 > budget_s:
+                break
+    dt = time.perf_counter() - t0
+    return {"value": round(frames / dt, 2), "unit": "frames/s", "cores": 1, "kind": "oracle",
+            "sample": f"{done} of {b.N} utterances of the same batch ({frames} frames), full oracle path "
+                      f"(trivial joiner, lattice, am/lm grads, bounds, pruned joiner, pruned lattice, joiner grads), "
+                      f"fp64 NumPy, 1 thread, {dt:.1f} s"}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="bpe", choices=sorted(WORKLOAD_TEXT))
+    ap.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of oracle work for cpu_baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path (the loss is per-utterance; "
+              "data-parallel sharding over utterances is described in DESIGN.md). Run with --gpus 1.",
+              file=sys.stderr)
+        return 2
+
+    import ctypes
+
+    import numpy as np
+    import torch
+
+    import paper_2206_13236_amd as P
+    from paper_2206_13236_amd import _native
+    from workloads import make_batch
+
+    assert torch.cuda.is_available(), "bench.py needs a ROCm GPU"
+    dev = torch.device("cuda:0")
+    b = make_batch(args.workload, seed=0)
+    bf = b.wl.joiner_dtype == "bf16"
+    S, J, V = b.wl.S, b.wl.J, b.V
+    frames = b.frames
+    M = S * frames
+
+    f32 = lambda a: torch.from_numpy(np.ascontiguousarray(a, np.float32)).to(dev)
+    i32 = lambda a: torch.from_numpy(np.ascontiguousarray(a, np.int32)).to(dev)
+    jt = (lambda a: f32(a).to(torch.bfloat16)) if bf else f32
+    torch.cuda.reset_peak_memory_stats(dev)
+    base_mem = torch.cuda.memory_allocated(dev)
+    batch = P.Batch(i32(b.t_len), i32(b.u_len), i32(b.symbols), b.T, b.U, b.wl.blank)
+    am, lm = f32(b.am), f32(b.lm)
+    enc, dec, W, bias = jt(b.enc), jt(b.dec), jt(b.W), jt(b.bias)
+    inputs_mem = torch.cuda.memory_allocated(dev) - base_mem
+    step = P.PrunedRnntLoss(S, simple_scale=0.5)
+
+    for _ in range(args.warmup):
+        step.step(batch, am, lm, enc, dec, W, bias)
+    torch.cuda.synchronize()
+    L = _native.lib()
+    L.rnnt_profile_reset()
+    L.rnnt_profile_enable(1)
+    stream = torch.cuda.current_stream()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        step.step(batch, am, lm, enc, dec, W, bias)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    L.rnnt_profile_enable(0)
+    ms_total = ev0.elapsed_time(ev1)
+    ms_step = ms_total / args.steps
+    peak = torch.cuda.max_memory_allocated(dev) - base_mem
+
+    # per-kernel times from the library's events
+    buf = ctypes.create_string_buffer(4096)
+    L.rnnt_profile_names(buf, 4096)
+    kernels = {}
+    for name in [x for x in buf.value.decode().split(",") if x]:
+        n = ctypes.c_int32()
+        tot = ctypes.c_double()
+        _native.check(L.rnnt_profile_query(name.encode(), ctypes.byref(n), ctypes.byref(tot)))
+        kernels[name] = {"launches": n.value, "avg_us": round(1000 * tot.value / max(n.value, 1), 2),
+                         "us_per_step": round(1000 * tot.value / args.steps, 2)}
+    L.rnnt_profile_reset()
+    # the dominant contraction: joiner GEMMs with algorithmic work 2*M*J*V each
+    # (the backward's logits recompute is overhead, not work, and is excluded)
+    work = {"joiner_fwd": 2.0 * M * J * V, "joiner_dh": 2.0 * M * J * V, "joiner_dw": 2.0 * M * J * V}
+    dom = max((k for k in work if k in kernels), key=lambda k: kernels[k]["us_per_step"])
+    per_launch_flops = work[dom] / (kernels[dom]["launches"] / args.steps)
+    achieved = per_launch_flops / (kernels[dom]["avg_us"] * 1e-6) / 1e12
+    dt = "bf16" if bf else "f32"
+    roofline = {"kernel": dom, "bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_TFLOPS[dt],
+                "unit": "TFLOP/s", "frac": round(achieved / PEAK_TFLOPS[dt], 4), "traffic": None,
+                "algorithmic_flops_per_launch": per_launch_flops, "avg_launch_us": kernels[dom]["avg_us"]}
+
+    cpu = None if args.no_cpu_baseline else _cpu_baseline(b, S, args.cpu_budget)
+    line = {
+        "metric": "pruned RNN-T loss fwd+bwd frames/sec at V=500,S=5; peak HBM bytes",
+        "value": round(frames * args.steps / (ms_total / 1000.0), 1),
+        "unit": "frames/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32" if not bf else "bf16",
+        "data": "synthetic",
+        "config": {"workload": WORKLOAD_TEXT[args.workload], "frames_per_step": frames, "rows_M": M,
+                   "N": b.N, "T": b.T, "U": b.U, "V": V, "S": S, "J": J, "seed": 0},
+        "peak_hbm_bytes": int(peak),
+        "peak_hbm_bytes_excl_inputs": int(peak - inputs_mem),
+        "wall_s_timed": round(wall, 3),
+        "roofline": roofline,
+        "kernels": kernels,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

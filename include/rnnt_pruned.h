@@ -201,6 +201,26 @@ int rnnt_pruned_joiner_backward(const rnnt_batch* batch, int32_t S, int32_t J, i
                                 float* W_grad, float* bias_grad, float* logits_grad,
                                 void* workspace, size_t workspace_bytes, void* stream);
 
+/* ------------------------------------------------------------------------ */
+/* Kernel timing (opt-in; for benchmarks and profiling)                      */
+/* ------------------------------------------------------------------------ */
+
+/* Enable (on != 0) or disable recording of per-kernel HIP events. While
+ * enabled, every kernel launch of the library is bracketed by two events
+ * recorded on its stream, under a fixed kernel name ("joiner_fwd",
+ * "joiner_dlogits", "joiner_dh", "joiner_dw", "lattice", "band", ...). */
+int rnnt_profile_enable(int on);
+
+/* Forget all records (waits for the recorded events to complete). */
+int rnnt_profile_reset(void);
+
+/* Number of recorded launches of kernel `name` and their summed duration in
+ * milliseconds. Synchronises on the recorded events. */
+int rnnt_profile_query(const char* name, int32_t* launches, double* total_ms);
+
+/* Comma-separated names of the kernels recorded so far, into buf[cap]. */
+int rnnt_profile_names(char* buf, size_t cap);
+
 #ifdef __cplusplus
 }
 #endif

@@ -56,6 +56,10 @@ SIGNATURES = {
                                               c_void_p, c_void_p, c_void_p, c_void_p,
                                               c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
                                               c_void_p, c_size_t, c_void_p]),
+    "rnnt_profile_enable": (c_int32, [c_int32]),
+    "rnnt_profile_reset": (c_int32, []),
+    "rnnt_profile_query": (c_int32, [c_char_p, POINTER(c_int32), POINTER(ctypes.c_double)]),
+    "rnnt_profile_names": (c_int32, [c_char_p, c_size_t]),
 }
 
 _lib = None

@@ -19,6 +19,7 @@
 // log2 domain, fp64 accumulators, fp32 exp2/log2 only for LogAdd's bounded
 // correction term.
 #include "kernels.h"
+#include "prof.h"
 
 namespace {
 
@@ -184,6 +185,9 @@ hipError_t launch_band(const BandArgs& a, hipStream_t s) {
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)sm);
     if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL(band_kernel, dim3(a.b.N), dim3(kBandThreads), sm, s, a);
+  {
+    RNNT_PROF(s, "band");
+    hipLaunchKernelGGL(band_kernel, dim3(a.b.N), dim3(kBandThreads), sm, s, a);
+  }
   return hipGetLastError();
 }

@@ -24,6 +24,7 @@
 // with p_t + s = u, dW and db summed over their partials, all in a fixed order.
 #include "gemm.h"
 #include "kernels.h"
+#include "prof.h"
 
 namespace {
 
@@ -630,17 +631,26 @@ int joiner_db_rows(int N, int T, int S) {
 }
 
 hipError_t launch_joiner_prep(const JoinerArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(joiner_prep_kernel, dim3(a.b.N), dim3(256), 0, s, a);
+  {
+    RNNT_PROF(s, "joiner_prep");
+    hipLaunchKernelGGL(joiner_prep_kernel, dim3(a.b.N), dim3(256), 0, s, a);
+  }
   return hipGetLastError();
 }
 
 hipError_t launch_joiner_fwd(const JoinerArgs& a, hipStream_t s) {
   const int mmax = a.b.N * a.b.T * a.S;
   dim3 grid((mmax + 127) / 128, (a.V + 127) / 128);
-  if (a.bf16) hipLaunchKernelGGL(joiner_fwd_kernel<true>, grid, dim3(256), 0, s, a);
+  {
+    RNNT_PROF(s, "joiner_fwd");
+    if (a.bf16) hipLaunchKernelGGL(joiner_fwd_kernel<true>, grid, dim3(256), 0, s, a);
   else hipLaunchKernelGGL(joiner_fwd_kernel<false>, grid, dim3(256), 0, s, a);
+  }
   const size_t total = (size_t)a.b.N * a.b.T * a.S;
-  hipLaunchKernelGGL(joiner_combine_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, a);
+  {
+    RNNT_PROF(s, "joiner_combine");
+    hipLaunchKernelGGL(joiner_combine_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, a);
+  }
   return hipGetLastError();
 }
 
@@ -660,18 +670,42 @@ hipError_t launch_joiner_bwd(const JoinerArgs& a, hipStream_t s) {
     const int mt = (cm1 - cm0 + 127) / 128;
     dim3 g1(mt, (V + 127) / 128), g2(mt, (J + 127) / 128), g3((J + 127) / 128, (V + 127) / 128, a.splits);
     if (a.bf16) {
-      hipLaunchKernelGGL(joiner_dlogits_kernel<true>, g1, dim3(256), 0, s, a, cm0, cm1);
-      hipLaunchKernelGGL(joiner_dh_kernel<true>, g2, dim3(256), 0, s, a, cm0, cm1);
-      hipLaunchKernelGGL(joiner_dw_kernel<true>, g3, dim3(256), 0, s, a, cm0, cm1);
+      {
+        RNNT_PROF(s, "joiner_dlogits");
+        hipLaunchKernelGGL(joiner_dlogits_kernel<true>, g1, dim3(256), 0, s, a, cm0, cm1);
+      }
+      {
+        RNNT_PROF(s, "joiner_dh");
+        hipLaunchKernelGGL(joiner_dh_kernel<true>, g2, dim3(256), 0, s, a, cm0, cm1);
+      }
+      {
+        RNNT_PROF(s, "joiner_dw");
+        hipLaunchKernelGGL(joiner_dw_kernel<true>, g3, dim3(256), 0, s, a, cm0, cm1);
+      }
     } else {
-      hipLaunchKernelGGL(joiner_dlogits_kernel<false>, g1, dim3(256), 0, s, a, cm0, cm1);
-      hipLaunchKernelGGL(joiner_dh_kernel<false>, g2, dim3(256), 0, s, a, cm0, cm1);
-      hipLaunchKernelGGL(joiner_dw_kernel<false>, g3, dim3(256), 0, s, a, cm0, cm1);
+      {
+        RNNT_PROF(s, "joiner_dlogits");
+        hipLaunchKernelGGL(joiner_dlogits_kernel<false>, g1, dim3(256), 0, s, a, cm0, cm1);
+      }
+      {
+        RNNT_PROF(s, "joiner_dh");
+        hipLaunchKernelGGL(joiner_dh_kernel<false>, g2, dim3(256), 0, s, a, cm0, cm1);
+      }
+      {
+        RNNT_PROF(s, "joiner_dw");
+        hipLaunchKernelGGL(joiner_dw_kernel<false>, g3, dim3(256), 0, s, a, cm0, cm1);
+      }
     }
   }
   const size_t JV = (size_t)J * V;
-  hipLaunchKernelGGL(joiner_wsum_kernel, dim3((unsigned)((JV + 255) / 256)), dim3(256), 0, s, a);
+  {
+    RNNT_PROF(s, "joiner_wsum");
+    hipLaunchKernelGGL(joiner_wsum_kernel, dim3((unsigned)((JV + 255) / 256)), dim3(256), 0, s, a);
+  }
   const int rows = a.b.N * (a.b.T + a.b.U + 1);
-  hipLaunchKernelGGL(joiner_encdec_kernel, dim3(rows), dim3(256), (size_t)a.b.T * sizeof(int), s, a);
+  {
+    RNNT_PROF(s, "joiner_encdec");
+    hipLaunchKernelGGL(joiner_encdec_kernel, dim3(rows), dim3(256), (size_t)a.b.T * sizeof(int), s, a);
+  }
   return hipGetLastError();
 }

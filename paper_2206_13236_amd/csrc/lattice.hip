@@ -16,6 +16,7 @@
 // only the bounded correction term of LogAdd goes through fp32 exp2/log2
 // (see log2add). alpha and beta are stored in fp64.
 #include "kernels.h"
+#include "prof.h"
 
 namespace {
 
@@ -226,6 +227,7 @@ hipError_t launch_lattice(const SimpleArgs& a, hipStream_t s) {
   const int U1 = a.b.U + 1;
   const int need = (U1 + 63) / 64;
   dim3 grid(a.b.N), block(kLatThreads);
+  RNNT_PROF(s, "lattice");
   if (need <= 1) hipLaunchKernelGGL((lattice_kernel<1, 8>), grid, block, 0, s, a);
   else if (need <= 2) hipLaunchKernelGGL((lattice_kernel<2, 8>), grid, block, 0, s, a);
   else if (need <= 4) hipLaunchKernelGGL((lattice_kernel<4, 4>), grid, block, 0, s, a);

@@ -21,6 +21,7 @@
 // (score, p) to the first maximum. The two suffix minima are Hillis-Steele
 // scans over LDS (min is exact and associative, so the order does not matter).
 #include "kernels.h"
+#include "prof.h"
 
 namespace {
 
@@ -110,7 +111,10 @@ size_t prune_smem_bytes(int T) { return (size_t)2 * T * sizeof(int); }
 
 hipError_t launch_prune(const BatchDev& b, int S, const float* gx, const float* gy, int* ranges,
                         hipStream_t s) {
-  hipLaunchKernelGGL(prune_kernel, dim3(b.N), dim3(kPruneThreads), prune_smem_bytes(b.T), s, b, S, gx, gy,
+  {
+    RNNT_PROF(s, "prune");
+    hipLaunchKernelGGL(prune_kernel, dim3(b.N), dim3(kPruneThreads), prune_smem_bytes(b.T), s, b, S, gx, gy,
                      ranges);
+  }
   return hipGetLastError();
 }

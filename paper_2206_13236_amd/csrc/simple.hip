@@ -22,6 +22,7 @@
 
 #include "gemm.h"
 #include "kernels.h"
+#include "prof.h"
 
 namespace {
 
@@ -346,15 +347,24 @@ __global__ void fill_f32_kernel(float* p, size_t n, float v) {
 
 hipError_t launch_rowmax(const SimpleArgs& a, hipStream_t s) {
   const int N = a.b.N, T = a.b.T, U1 = a.b.U + 1;
-  hipLaunchKernelGGL(rowmax_kernel, dim3((N * T + 3) / 4), dim3(256), 0, s, a.am, N, T, a.V, a.b, 0, a.m_a);
-  hipLaunchKernelGGL(rowmax_kernel, dim3((N * U1 + 3) / 4), dim3(256), 0, s, a.lm, N, U1, a.V, a.b, 1, a.m_l);
+  {
+    RNNT_PROF(s, "rowmax");
+    hipLaunchKernelGGL(rowmax_kernel, dim3((N * T + 3) / 4), dim3(256), 0, s, a.am, N, T, a.V, a.b, 0, a.m_a);
+  }
+  {
+    RNNT_PROF(s, "rowmax");
+    hipLaunchKernelGGL(rowmax_kernel, dim3((N * U1 + 3) / 4), dim3(256), 0, s, a.lm, N, U1, a.V, a.b, 1, a.m_l);
+  }
   return hipGetLastError();
 }
 
 hipError_t launch_normalizer(const SimpleArgs& a, hipStream_t s) {
   const int T = a.b.T, U1 = a.b.U + 1;
   dim3 grid((T + NormCfg::BM - 1) / NormCfg::BM, (U1 + NormCfg::BN - 1) / NormCfg::BN, a.b.N);
-  hipLaunchKernelGGL(normalizer_kernel, grid, dim3(256), 0, s, a);
+  {
+    RNNT_PROF(s, "normalizer");
+    hipLaunchKernelGGL(normalizer_kernel, grid, dim3(256), 0, s, a);
+  }
   return hipGetLastError();
 }
 
@@ -362,11 +372,17 @@ hipError_t launch_simple_grads(const SimpleArgs& a, hipStream_t s) {
   const int T = a.b.T, U1 = a.b.U + 1, V = a.V;
   if (a.am_grad) {
     dim3 grid((T + DamCfg::BM - 1) / DamCfg::BM, (V + DamCfg::BN - 1) / DamCfg::BN, a.b.N);
-    hipLaunchKernelGGL(dam_kernel, grid, dim3(256), 0, s, a);
+    {
+      RNNT_PROF(s, "simple_dam");
+      hipLaunchKernelGGL(dam_kernel, grid, dim3(256), 0, s, a);
+    }
   }
   if (a.lm_grad) {
     dim3 grid((U1 + DlmCfg::BM - 1) / DlmCfg::BM, (V + DlmCfg::BN - 1) / DlmCfg::BN, a.b.N);
-    hipLaunchKernelGGL(dlm_kernel, grid, dim3(256), 0, s, a);
+    {
+      RNNT_PROF(s, "simple_dlm");
+      hipLaunchKernelGGL(dlm_kernel, grid, dim3(256), 0, s, a);
+    }
   }
   return hipGetLastError();
 }
@@ -375,6 +391,9 @@ hipError_t launch_fill_f32(float* p, size_t n, float v, hipStream_t s) {
   if (n == 0) return hipSuccess;
   size_t blocks = (n + 255) / 256;
   if (blocks > 4096) blocks = 4096;
-  hipLaunchKernelGGL(fill_f32_kernel, dim3((unsigned)blocks), dim3(256), 0, s, p, n, v);
+  {
+    RNNT_PROF(s, "fill");
+    hipLaunchKernelGGL(fill_f32_kernel, dim3((unsigned)blocks), dim3(256), 0, s, p, n, v);
+  }
   return hipGetLastError();
 }

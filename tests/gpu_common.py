@@ -50,7 +50,8 @@ def assert_close(name, got, ref, atol=0.0, rtol=0.0, mask=None):
         got = np.where(mask, got, 0.0)
         ref = np.where(mask, ref, 0.0)
     both_inf = np.isinf(got) & np.isinf(ref) & (np.sign(got) == np.sign(ref))
-    diff = np.where(both_inf, 0.0, np.abs(got - ref))
+    with np.errstate(invalid="ignore"):
+        diff = np.where(both_inf, 0.0, np.abs(got - ref))
     tol = atol + rtol * np.where(np.isinf(ref), 0.0, np.abs(ref))
     bad = ~(diff <= tol)
     if bad.any():
