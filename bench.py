@@ -90,6 +90,9 @@ def main() -> int:
 
     assert torch.cuda.is_available(), "bench.py needs a ROCm GPU"
     dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    torch.zeros(1, device=dev)
+    torch.cuda.synchronize()
     b = make_batch(args.workload, seed=0)
     bf = b.wl.joiner_dtype == "bf16"
     S, J, V = b.wl.S, b.wl.J, b.V

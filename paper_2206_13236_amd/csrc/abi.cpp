@@ -86,10 +86,11 @@ struct SimpleWs {
   float* py;
   double* alpha;
   double* beta;
+  double* Ldiag;
   float* Wt;
-  float* ry;
-  float* cx;
-  float* cy;
+  double* ry;
+  double* cx;
+  double* cy;
   size_t bytes;
 };
 
@@ -104,10 +105,11 @@ SimpleWs simple_layout(void* base, int N, int T, int U) {
   w.py = c.take<float>(L);
   w.alpha = c.take<double>(L);
   w.beta = c.take<double>(L);
-  w.Wt = c.take<float>(NT * ldw_of(U));
-  w.ry = c.take<float>(NT);
-  w.cx = c.take<float>(NU);
-  w.cy = c.take<float>(NU);
+  w.Ldiag = c.take<double>((size_t)N * (T + U + 1));
+  w.Wt =c.take<float>(NT * ldw_of(U));
+  w.ry = c.take<double>(NT);
+  w.cx = c.take<double>(NU);
+  w.cy = c.take<double>(NU);
   w.bytes = c.off;
   return w;
 }
@@ -225,6 +227,7 @@ int rnnt_simple_loss(const rnnt_batch* batch, int32_t V, const float* am, const 
   a.py = py ? py : w.py;
   a.alpha = w.alpha;
   a.beta = w.beta;
+  a.Ldiag = w.Ldiag;
   a.loss = loss;
   a.gx = px_occ;
   a.gy = py_occ;
@@ -316,7 +319,7 @@ int rnnt_pruned_loss(const rnnt_batch* batch, int32_t S, const float* px, const 
   if (S < 1 || S > RNNT_MAX_S) return fail(RNNT_EUNSUPPORTED, "S = %d outside [1, %d]", S, RNNT_MAX_S);
   if (!px || !py || !ranges || !loss) return fail(RNNT_EINVAL, "px, py, ranges and loss are required");
   if ((long long)batch->N * batch->T * S > kI32) return fail(RNNT_EUNSUPPORTED, "N*T*S exceeds 2^31-1");
-  if (band_smem_bytes(batch->T, S) > 150 * 1024)
+  if (band_smem_bytes(batch->T, batch->U, S) > 150 * 1024)
     return fail(RNNT_EUNSUPPORTED, "T*S = %d*%d too large for the LDS-resident band", batch->T, S);
   const size_t need = rnnt_pruned_loss_workspace_size(batch->N, batch->T, S);
   rc = check_ws(workspace, workspace_bytes, need);

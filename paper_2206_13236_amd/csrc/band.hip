@@ -148,6 +148,41 @@ __global__ __launch_bounds__(kBandThreads) void band_kernel(BandArgs a) {
   if (threadIdx.x == 0) a.loss[n] = (L2 == L2) ? (float)(-L2 * kLn2) : __builtin_nanf("");
   if (!a.gx && !a.gy) return;
   const bool live = (L2 == L2) && (L2 != kNegInfD);
+  // Per-anti-diagonal normalisers (every complete path crosses diagonal
+  // d = t + u at exactly one band node): the occupations of the edges leaving
+  // diagonal d are normalised by that diagonal's own total, which cancels the
+  // common part of the rounding accumulated by alpha and beta.
+  double* Ld = reinterpret_cast<double*>(sm + (size_t)2 * T * S + T + (T & 1));
+  const int D = Tn + Un;
+  if (live) {
+    for (int d = threadIdx.x; d < D; d += kBandThreads) {
+      // last frame whose band starts at or before d (e_t = t + p_t is increasing)
+      int lo = 0, hi = Tn - 1;
+      while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (mid + P[mid] <= d) lo = mid;
+        else hi = mid - 1;
+      }
+      double mx = kNegInfD;
+      for (int t = lo; t >= 0 && d - (t + P[t]) < S; --t) {
+        const int s = d - (t + P[t]);
+        if (s >= 0 && P[t] + s <= Un) {
+          const double x = alpha[(size_t)t * S + s] + beta[(size_t)t * S + s];
+          mx = x > mx ? x : mx;
+        }
+      }
+      double sum = 0.0;
+      for (int t = lo; t >= 0 && d - (t + P[t]) < S; --t) {
+        const int s = d - (t + P[t]);
+        if (s >= 0 && P[t] + s <= Un) {
+          const double x = alpha[(size_t)t * S + s] + beta[(size_t)t * S + s];
+          if (x != kNegInfD) sum += (double)exp2f((float)(x - mx));
+        }
+      }
+      Ld[d] = mx + log2(sum);
+    }
+  }
+  __syncthreads();
   for (int i = threadIdx.x; i < T * S; i += kBandThreads) {
     const int t = i / S, s = i - t * S;
     float gxv = 0.f, gyv = 0.f;
@@ -156,8 +191,9 @@ __global__ __launch_bounds__(kBandThreads) void band_kernel(BandArgs a) {
       const int u = p + s;
       if (u <= Un) {
         const double al = alpha[i];
+        const double Lt = Ld[t + u];
         if (s + 1 < S && u + 1 <= Un)
-          gxv = exp2_occ(al + (double)v.X[i] * kLog2e + beta[i + 1] - L2);
+          gxv = exp2_occ(al + (double)v.X[i] * kLog2e + beta[i + 1] - Lt);
         double nb;
         if (t + 1 < Tn) {
           const int s2 = u - v.P[t + 1];
@@ -165,7 +201,7 @@ __global__ __launch_bounds__(kBandThreads) void band_kernel(BandArgs a) {
         } else {
           nb = (u == Un) ? 0.0 : kNegInfD;
         }
-        gyv = exp2_occ(al + (double)v.Y[i] * kLog2e + nb - L2);
+        gyv = exp2_occ(al + (double)v.Y[i] * kLog2e + nb - Lt);
       }
     }
     if (a.gx) a.gx[base + i] = gxv;
@@ -175,10 +211,13 @@ __global__ __launch_bounds__(kBandThreads) void band_kernel(BandArgs a) {
 
 }  // namespace
 
-size_t band_smem_bytes(int T, int S) { return (size_t)T * S * 2 * sizeof(float) + (size_t)T * sizeof(int); }
+// px, py [T*S] floats, p_t [T] ints (padded to 8 bytes), per-diagonal totals [T+U+1] doubles
+size_t band_smem_bytes(int T, int U, int S) {
+  return (size_t)T * S * 2 * sizeof(float) + (size_t)(T + (T & 1)) * sizeof(int) + (size_t)(T + U + 1) * sizeof(double);
+}
 
 hipError_t launch_band(const BandArgs& a, hipStream_t s) {
-  const size_t sm = band_smem_bytes(a.b.T, a.S);
+  const size_t sm = band_smem_bytes(a.b.T, a.b.U, a.S);
   if (sm > 150 * 1024) return hipErrorInvalidValue;
   if (sm > 64 * 1024) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(band_kernel),

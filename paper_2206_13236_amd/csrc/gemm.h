@@ -12,11 +12,15 @@
 // K-step are issued before the MFMAs of the current one; LDS is double
 // buffered, so there is one barrier per K-step.
 //
-// Operand sources are supplied by each kernel:
-//   KC  source (global is k-contiguous):  kc_fetch(row, k, float v[KV])
-//   MNC source (global is row-contiguous): mnc_fetch(k, row, float v[16/KV])
-// and return fp32 values (generated values such as tanh(enc+dec) or
-// exp(x - max) are produced inside the fetch); the loader packs them.
+// Operand sources are supplied by each kernel, in two halves so that global
+// loads for the next K-step stay in flight while the current one computes:
+//   KC  source (global is k-contiguous):
+//     kc_load(row, k, Raw&)            issue the loads only
+//     kc_finish(const Raw&, v[KV])     turn them into KV fp32 values
+//   MNC source (global is row-contiguous): mnc_load(k, row, Raw&) and
+//     mnc_finish(const Raw&, v[16/KV]).
+// Generated operands (tanh(enc+dec), exp(x - max)) are formed in *_finish,
+// which runs after the MFMAs of the current K-step; the loader packs them.
 //
 // Output element (i, j, r) of a lane: row = wm*WM + i*16 + 4*(lane>>4) + r,
 // col = wn*WN + j*16 + (lane & 15).
@@ -44,6 +48,19 @@ struct GemmCfg {
   static_assert(FM >= 1 && FN >= 1, "tile too small");
 };
 
+// Raw operand registers of a source whose values need no transform.
+template <int N>
+struct RawF {
+  float v[N];
+};
+
+// Raw registers of an exp(x - m) source: the loaded values and the row max.
+template <int N>
+struct RawExp {
+  float x[N];
+  float m;
+};
+
 template <class Cfg>
 DEV void pack_store16(typename Cfg::T* dst, const float* v) {
   if constexpr (Cfg::BF16) {
@@ -63,22 +80,25 @@ struct KCLoader {
   static constexpr int KV = Cfg::KV;
   static constexpr int CPR = Cfg::BK / KV;               // 16-byte chunks per row
   static constexpr int NCH = (ROWS * CPR + 255) / 256;   // chunks per thread
-  struct Reg { float v[NCH][KV]; };
+  struct Reg { typename Src::Raw v[NCH]; };
   const Src& src;
   DEV explicit KCLoader(const Src& s) : src(s) {}
   DEV void fetch(int k0, Reg& r) const {
 #pragma unroll
     for (int i = 0; i < NCH; ++i) {
       int c = threadIdx.x + 256 * i;
-      if (ROWS * CPR % 256 == 0 || c < ROWS * CPR) src.kc_fetch(c / CPR, k0 + (c % CPR) * KV, r.v[i]);
+      if (ROWS * CPR % 256 == 0 || c < ROWS * CPR) src.kc_load(c / CPR, k0 + (c % CPR) * KV, r.v[i]);
     }
   }
   DEV void put(const Reg& r, typename Cfg::T* lds) const {
 #pragma unroll
     for (int i = 0; i < NCH; ++i) {
       int c = threadIdx.x + 256 * i;
-      if (ROWS * CPR % 256 == 0 || c < ROWS * CPR)
-        pack_store16<Cfg>(lds + (c / CPR) * Cfg::LDK + (c % CPR) * KV, r.v[i]);
+      if (ROWS * CPR % 256 == 0 || c < ROWS * CPR) {
+        float v[KV];
+        src.kc_finish(r.v[i], v);
+        pack_store16<Cfg>(lds + (c / CPR) * Cfg::LDK + (c % CPR) * KV, v);
+      }
     }
   }
 };
@@ -92,7 +112,7 @@ struct MNCLoader {
   static constexpr int NBR = ROWS / NV;                    // blocks along rows
   static constexpr int NBLK = (Cfg::BK / KV) * NBR;
   static constexpr int NPT = (NBLK + 255) / 256;
-  struct Reg { float v[NPT][KV][NV]; };
+  struct Reg { typename Src::Raw v[NPT][KV]; };
   const Src& src;
   DEV explicit MNCLoader(const Src& s) : src(s) {}
   DEV void fetch(int k0, Reg& r) const {
@@ -102,7 +122,7 @@ struct MNCLoader {
       if (NBLK % 256 == 0 || blk < NBLK) {
         int kb = blk / NBR, nb = blk % NBR;
 #pragma unroll
-        for (int i = 0; i < KV; ++i) src.mnc_fetch(k0 + kb * KV + i, nb * NV, r.v[b][i]);
+        for (int i = 0; i < KV; ++i) src.mnc_load(k0 + kb * KV + i, nb * NV, r.v[b][i]);
       }
     }
   }
@@ -112,11 +132,14 @@ struct MNCLoader {
       int blk = threadIdx.x + 256 * b;
       if (NBLK % 256 == 0 || blk < NBLK) {
         int kb = blk / NBR, nb = blk % NBR;
+        float m[KV][NV];
+#pragma unroll
+        for (int i = 0; i < KV; ++i) src.mnc_finish(r.v[b][i], m[i]);
 #pragma unroll
         for (int c = 0; c < NV; ++c) {
           float col[KV];
 #pragma unroll
-          for (int i = 0; i < KV; ++i) col[i] = r.v[b][i][c];
+          for (int i = 0; i < KV; ++i) col[i] = m[i][c];
           pack_store16<Cfg>(lds + (nb * NV + c) * Cfg::LDK + kb * KV, col);
         }
       }

@@ -102,121 +102,179 @@ DEV void load_seg(const TIn* row, int c, int len, bool aligned, float (&v)[NV]) 
 }
 
 // ---------------------------------------------------------------------------
+// Raw operand registers: N elements of TIn kept as 32-bit words until the
+// loader's finish step, so that no conversion waits on an in-flight load.
+// ---------------------------------------------------------------------------
+template <typename TIn, int N>
+struct RawVec {
+  static constexpr int W = (N * (int)sizeof(TIn) + 3) / 4;
+  uint32_t w[W];
+};
+
+template <typename TIn, int N>
+DEV void raw_load(const TIn* p, bool full, bool valid, int count, RawVec<TIn, N>& r) {
+  // full: the N elements at p are in range and aligned for one vector load;
+  // otherwise the first `count` elements are loaded one by one (0 beyond).
+  if (!valid) {
+#pragma unroll
+    for (int i = 0; i < RawVec<TIn, N>::W; ++i) r.w[i] = 0u;
+    return;
+  }
+  if (full) {
+    if constexpr (RawVec<TIn, N>::W == 4) {
+      uint4 q = *reinterpret_cast<const uint4*>(p);
+      r.w[0] = q.x; r.w[1] = q.y; r.w[2] = q.z; r.w[3] = q.w;
+    } else if constexpr (RawVec<TIn, N>::W == 2) {
+      uint2 q = *reinterpret_cast<const uint2*>(p);
+      r.w[0] = q.x; r.w[1] = q.y;
+    } else if constexpr (RawVec<TIn, N>::W == 1) {
+      r.w[0] = *reinterpret_cast<const uint32_t*>(p);
+    } else {
+#pragma unroll
+      for (int i = 0; i < RawVec<TIn, N>::W; ++i) r.w[i] = reinterpret_cast<const uint32_t*>(p)[i];
+    }
+    return;
+  }
+  if constexpr (sizeof(TIn) == 4) {
+#pragma unroll
+    for (int i = 0; i < N; ++i) r.w[i] = (i < count) ? __float_as_uint(p[i]) : 0u;
+  } else {
+#pragma unroll
+    for (int i = 0; i < RawVec<TIn, N>::W; ++i) {
+      const uint32_t lo = (2 * i < count) ? (uint32_t)p[2 * i] : 0u;
+      const uint32_t hi = (2 * i + 1 < count) ? (uint32_t)p[2 * i + 1] : 0u;
+      r.w[i] = lo | (hi << 16);
+    }
+  }
+}
+
+template <typename TIn, int N>
+DEV void raw_to_float(const RawVec<TIn, N>& r, float (&v)[N]) {
+  if constexpr (sizeof(TIn) == 4) {
+#pragma unroll
+    for (int i = 0; i < N; ++i) v[i] = __uint_as_float(r.w[i]);
+  } else {
+#pragma unroll
+    for (int i = 0; i < N / 2; ++i) {
+      v[2 * i] = __uint_as_float(r.w[i] << 16);
+      v[2 * i + 1] = __uint_as_float(r.w[i] & 0xffff0000u);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Operand sources
 // ---------------------------------------------------------------------------
+
+// h = tanh(enc + dec) from two raw segments.
+template <typename TIn, int N>
+struct RawH {
+  RawVec<TIn, N> e, d;
+};
+template <typename TIn, int N>
+DEV void finish_h(const RawH<TIn, N>& r, float (&v)[N]) {
+  float e[N], d[N];
+  raw_to_float(r.e, e);
+  raw_to_float(r.d, d);
+#pragma unroll
+  for (int i = 0; i < N; ++i) v[i] = fast_tanh(e[i] + d[i]);
+}
 
 // A(m, j) = tanh(enc[row] + dec[row]) for the tile's rows (rowinfo in LDS).
 template <class Cfg, typename TIn>
 struct HSrcKC {
+  using Raw = RawH<TIn, Cfg::KV>;
   const TIn* enc;
   const TIn* dec;
   const int4* ri;
   int J;
-  DEV void kc_fetch(int row, int k, float (&v)[Cfg::KV]) const {
-    const int4 r = ri[row];
-    if (r.w < 0 || k >= J) {
-#pragma unroll
-      for (int i = 0; i < Cfg::KV; ++i) v[i] = 0.f;
-      return;
-    }
-    float e[Cfg::KV], d[Cfg::KV];
-    load_vec<Cfg::KV>(enc + (size_t)r.x + k, e);
-    load_vec<Cfg::KV>(dec + (size_t)r.y + k, d);
-#pragma unroll
-    for (int i = 0; i < Cfg::KV; ++i) v[i] = fast_tanh(e[i] + d[i]);
+  DEV void kc_load(int row, int k, Raw& r) const {
+    const int4 q = ri[row];
+    const bool ok = q.w >= 0 && k < J;
+    raw_load(enc + (ok ? (size_t)q.x + k : 0), true, ok, Cfg::KV, r.e);
+    raw_load(dec + (ok ? (size_t)q.y + k : 0), true, ok, Cfg::KV, r.d);
   }
+  DEV void kc_finish(const Raw& r, float (&v)[Cfg::KV]) const { finish_h(r, v); }
 };
 
 // B(j, v) = W[j][v]: global row-contiguous along v.
 template <class Cfg, typename TIn>
 struct WSrcMNC {
   static constexpr int NV = 16 / Cfg::KV;
+  using Raw = RawVec<TIn, NV>;
   const TIn* W;
   int v0, V, J;
   bool aligned;
-  DEV void mnc_fetch(int k, int col, float (&v)[NV]) const {
-    if (k >= J) {
-#pragma unroll
-      for (int i = 0; i < NV; ++i) v[i] = 0.f;
-      return;
-    }
-    load_seg<NV>(W + (size_t)k * V, v0 + col, V, aligned, v);
+  DEV void mnc_load(int k, int col, Raw& r) const {
+    const int c = v0 + col;
+    const bool ok = k < J && c < V;
+    raw_load(W + (ok ? (size_t)k * V + c : 0), aligned && c + NV <= V, ok, V - c, r);
   }
+  DEV void mnc_finish(const Raw& r, float (&v)[NV]) const { raw_to_float(r, v); }
 };
 
 // A(m, v) = dl[m][v] from the chunk buffer (rows padded to ldl with zeros).
 template <class Cfg>
 struct DlSrcKC {
+  using Raw = RawVec<typename Cfg::T, Cfg::KV>;
   const typename Cfg::T* dl;  // row (m - cm0)
   int m0, cm0, mend, ldl;
-  DEV void kc_fetch(int row, int k, float (&v)[Cfg::KV]) const {
+  DEV void kc_load(int row, int k, Raw& r) const {
     const int m = m0 + row;
-    if (m >= mend || k >= ldl) {
-#pragma unroll
-      for (int i = 0; i < Cfg::KV; ++i) v[i] = 0.f;
-      return;
-    }
-    load_vec<Cfg::KV>(dl + (size_t)(m - cm0) * ldl + k, v);
+    const bool ok = m < mend && k < ldl;
+    raw_load(dl + (ok ? (size_t)(m - cm0) * ldl + k : 0), true, ok, Cfg::KV, r);
   }
+  DEV void kc_finish(const Raw& r, float (&v)[Cfg::KV]) const { raw_to_float(r, v); }
 };
 
 // B(v, j) = W[j][v]: global k-contiguous along v for each j.
 template <class Cfg, typename TIn>
 struct WtSrcKC {
+  using Raw = RawVec<TIn, Cfg::KV>;
   const TIn* W;
   int j0, J, V;
   bool aligned;
-  DEV void kc_fetch(int row, int k, float (&v)[Cfg::KV]) const {
+  DEV void kc_load(int row, int k, Raw& r) const {
     const int j = j0 + row;
-    if (j >= J) {
-#pragma unroll
-      for (int i = 0; i < Cfg::KV; ++i) v[i] = 0.f;
-      return;
-    }
-    load_seg<Cfg::KV>(W + (size_t)j * V, k, V, aligned, v);
+    const bool ok = j < J && k < V;
+    raw_load(W + (ok ? (size_t)j * V + k : 0), aligned && k + Cfg::KV <= V, ok, V - k, r);
   }
+  DEV void kc_finish(const Raw& r, float (&v)[Cfg::KV]) const { raw_to_float(r, v); }
 };
 
 // A(j, m) = h(m, j): global is [m][j], j-contiguous; rowinfo read per row.
 template <class Cfg, typename TIn>
 struct HSrcMNC {
   static constexpr int NV = 16 / Cfg::KV;
+  using Raw = RawH<TIn, NV>;
   const TIn* enc;
   const TIn* dec;
   const int4* rowinfo;
   int j0, J, mend;
-  DEV void mnc_fetch(int k, int col, float (&v)[NV]) const {
+  DEV void mnc_load(int k, int col, Raw& r) const {
     const int j = j0 + col;
-    int4 r = make_int4(0, 0, -1, -1);
-    if (k < mend && j < J) r = rowinfo[k];
-    if (r.w < 0) {
-#pragma unroll
-      for (int i = 0; i < NV; ++i) v[i] = 0.f;
-      return;
-    }
-    float e[NV], d[NV];
-    load_vec<NV>(enc + (size_t)r.x + j, e);
-    load_vec<NV>(dec + (size_t)r.y + j, d);
-#pragma unroll
-    for (int i = 0; i < NV; ++i) v[i] = fast_tanh(e[i] + d[i]);
+    int4 q = make_int4(0, 0, -1, -1);
+    if (k < mend && j < J) q = rowinfo[k];
+    const bool ok = q.w >= 0;
+    raw_load(enc + (ok ? (size_t)q.x + j : 0), true, ok, NV, r.e);
+    raw_load(dec + (ok ? (size_t)q.y + j : 0), true, ok, NV, r.d);
   }
+  DEV void mnc_finish(const Raw& r, float (&v)[NV]) const { finish_h(r, v); }
 };
 
 // B(m, v) = dl[m][v]: global row-contiguous along v.
 template <class Cfg>
 struct DlSrcMNC {
   static constexpr int NV = 16 / Cfg::KV;
+  using Raw = RawVec<typename Cfg::T, NV>;
   const typename Cfg::T* dl;
   int cm0, mend, v0, ldl;
-  DEV void mnc_fetch(int k, int col, float (&v)[NV]) const {
+  DEV void mnc_load(int k, int col, Raw& r) const {
     const int c = v0 + col;
-    if (k >= mend || c >= ldl) {
-#pragma unroll
-      for (int i = 0; i < NV; ++i) v[i] = 0.f;
-      return;
-    }
-    load_vec<NV>(dl + (size_t)(k - cm0) * ldl + c, v);
+    const bool ok = k < mend && c < ldl;
+    raw_load(dl + (ok ? (size_t)(k - cm0) * ldl + c : 0), true, ok, NV, r);
   }
+  DEV void mnc_finish(const Raw& r, float (&v)[NV]) const { raw_to_float(r, v); }
 };
 
 DEV float bias_at(const void* bias, int bf16, int v) {
@@ -508,7 +566,7 @@ __global__ __launch_bounds__(256) void joiner_dh_kernel(JoinerArgs a, int cm0, i
 // Backward 3: dW partial += h^T dl over one split of the chunk's rows
 // ---------------------------------------------------------------------------
 template <bool BF>
-__global__ __launch_bounds__(256) void joiner_dw_kernel(JoinerArgs a, int cm0, int cm1) {
+__global__ __launch_bounds__(256) void joiner_dw_kernel(JoinerArgs a, int cm0, int cm1, int first) {
   using TIn = typename In<BF>::T;
   using Cfg = typename In<BF>::Cfg;
   __shared__ __align__(16) typename Cfg::T smem[Cfg::SMEM_BYTES / sizeof(typename Cfg::T)];
@@ -519,8 +577,18 @@ __global__ __launch_bounds__(256) void joiner_dw_kernel(JoinerArgs a, int cm0, i
   const int per = ((rows + a.splits - 1) / a.splits + Cfg::BK - 1) / Cfg::BK * Cfg::BK;
   const int kb = cm0 + z * per;
   const int ke = min(kb + per, mend);
-  if (kb >= ke) return;
   const int V = a.V, J = a.J;
+  float* part = a.dw_part + (size_t)z * J * V;
+  if (kb >= ke) {
+    // no rows for this split: the first chunk still defines the partial
+    if (first) {
+      for (int e = threadIdx.x; e < Cfg::BM * Cfg::BN; e += 256) {
+        const int j = j0 + e / Cfg::BN, v = v0 + e % Cfg::BN;
+        if (j < J && v < V) part[(size_t)j * V + v] = 0.f;
+      }
+    }
+    return;
+  }
   const TIn* enc = reinterpret_cast<const TIn*>(a.enc);
   const TIn* dec = reinterpret_cast<const TIn*>(a.dec);
   HSrcMNC<Cfg, TIn> sa{enc, dec, a.rowinfo, j0, J, ke};
@@ -529,7 +597,6 @@ __global__ __launch_bounds__(256) void joiner_dw_kernel(JoinerArgs a, int cm0, i
   MNCLoader<Cfg, Cfg::BN, DlSrcMNC<Cfg>> lb(sb);
   floatx4 acc[Cfg::FM][Cfg::FN];
   gemm_mainloop<Cfg>(la, lb, kb, ke, smem, acc);
-  float* part = a.dw_part + (size_t)z * J * V;
 #pragma unroll
   for (int i = 0; i < Cfg::FM; ++i)
 #pragma unroll
@@ -539,24 +606,44 @@ __global__ __launch_bounds__(256) void joiner_dw_kernel(JoinerArgs a, int cm0, i
 #pragma unroll
       for (int jj = 0; jj < Cfg::FN; ++jj) {
         const int v = v0 + tile_col<Cfg>(jj);
-        if (v < V) part[(size_t)j * V + v] += acc[i][jj][r];
+        if (v < V) {
+          float* q = part + (size_t)j * V + v;
+          *q = first ? acc[i][jj][r] : *q + acc[i][jj][r];
+        }
       }
     }
 }
 
-// dW = sum of split partials, db = sum of per-tile column partials (fixed order).
+// dW = sum of the split partials, in split order.
 __global__ __launch_bounds__(256) void joiner_wsum_kernel(JoinerArgs a) {
   const size_t JV = (size_t)a.J * a.V;
   const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < JV && a.W_grad) {
-    float s = 0.f;
-    for (int z = 0; z < a.splits; ++z) s += a.dw_part[(size_t)z * JV + i];
-    a.W_grad[i] = s;
+  if (i >= JV) return;
+  float s = 0.f;
+#pragma unroll 8
+  for (int z = 0; z < a.splits; ++z) s += a.dw_part[(size_t)z * JV + i];
+  a.W_grad[i] = s;
+}
+
+// db = sum of the per-(row tile, wave) column partials written by the
+// d(logits) kernel: 16 interleaved parts per column, then the parts in order.
+__global__ __launch_bounds__(1024) void joiner_dbsum_kernel(JoinerArgs a) {
+  __shared__ float red[16][64];
+  const int c = threadIdx.x & 63, part = threadIdx.x >> 6;
+  const int v = blockIdx.x * 64 + c;
+  const int M = a.frame_off[a.b.N] * a.S;
+  const int rows = 2 * ((M + 127) / 128);
+  float s = 0.f;
+  if (v < a.V) {
+#pragma unroll 4
+    for (int r = part; r < rows; r += 16) s += a.db_part[(size_t)r * a.V + v];
   }
-  if (i < (size_t)a.V && a.bias_grad) {
-    float s = 0.f;
-    for (int r = 0; r < a.n_db_rows; ++r) s += a.db_part[(size_t)r * a.V + i];
-    a.bias_grad[i] = s;
+  red[part][c] = s;
+  __syncthreads();
+  if (part == 0 && v < a.V) {
+    float t = 0.f;
+    for (int q = 0; q < 16; ++q) t += red[q][c];
+    a.bias_grad[v] = t;
   }
 }
 
@@ -590,12 +677,25 @@ __global__ __launch_bounds__(256) void joiner_encdec_kernel(JoinerArgs a) {
   }
   for (int t = threadIdx.x; t < Tn; t += blockDim.x) sp[t] = a.ranges[((size_t)n * T + t) * S];
   __syncthreads();
+  // p_t is non-decreasing (Eq. (9)), so the frames whose band holds u form
+  // the interval [first t with p_t > u - S, first t with p_t > u).
+  int lo = 0, hi = Tn;
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    if (sp[mid] > u - S) hi = mid;
+    else lo = mid + 1;
+  }
+  const int t0 = lo;
+  hi = Tn;
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    if (sp[mid] > u) hi = mid;
+    else lo = mid + 1;
+  }
+  const int t1 = lo;
   for (int j = threadIdx.x; j < J; j += blockDim.x) {
     float s = 0.f;
-    for (int t = 0; t < Tn; ++t) {
-      const int q = u - sp[t];
-      if (q >= 0 && q < S) s += a.dpre[((size_t)(off + t) * S + q) * J + j];
-    }
+    for (int t = t0; t < t1; ++t) s += a.dpre[((size_t)(off + t) * S + (u - sp[t])) * J + j];
     out[j] = s;
   }
 }
@@ -657,10 +757,7 @@ hipError_t launch_joiner_fwd(const JoinerArgs& a, hipStream_t s) {
 hipError_t launch_joiner_bwd(const JoinerArgs& a, hipStream_t s) {
   const int mmax = a.b.N * a.b.T * a.S;
   const int V = a.V, J = a.J;
-  hipError_t e = launch_fill_f32(a.dw_part, (size_t)a.splits * J * V, 0.f, s);
-  if (e != hipSuccess) return e;
-  e = launch_fill_f32(a.db_part, (size_t)a.n_db_rows * V, 0.f, s);
-  if (e != hipSuccess) return e;
+  hipError_t e = hipSuccess;
   if (a.logits_grad) {
     e = launch_fill_f32(a.logits_grad, (size_t)mmax * V, 0.f, s);
     if (e != hipSuccess) return e;
@@ -680,7 +777,7 @@ hipError_t launch_joiner_bwd(const JoinerArgs& a, hipStream_t s) {
       }
       {
         RNNT_PROF(s, "joiner_dw");
-        hipLaunchKernelGGL(joiner_dw_kernel<true>, g3, dim3(256), 0, s, a, cm0, cm1);
+        hipLaunchKernelGGL(joiner_dw_kernel<true>, g3, dim3(256), 0, s, a, cm0, cm1, cm0 == 0);
       }
     } else {
       {
@@ -693,14 +790,18 @@ hipError_t launch_joiner_bwd(const JoinerArgs& a, hipStream_t s) {
       }
       {
         RNNT_PROF(s, "joiner_dw");
-        hipLaunchKernelGGL(joiner_dw_kernel<false>, g3, dim3(256), 0, s, a, cm0, cm1);
+        hipLaunchKernelGGL(joiner_dw_kernel<false>, g3, dim3(256), 0, s, a, cm0, cm1, cm0 == 0);
       }
     }
   }
   const size_t JV = (size_t)J * V;
-  {
+  if (a.W_grad) {
     RNNT_PROF(s, "joiner_wsum");
     hipLaunchKernelGGL(joiner_wsum_kernel, dim3((unsigned)((JV + 255) / 256)), dim3(256), 0, s, a);
+  }
+  if (a.bias_grad) {
+    RNNT_PROF(s, "joiner_dbsum");
+    hipLaunchKernelGGL(joiner_dbsum_kernel, dim3((unsigned)((V + 63) / 64)), dim3(1024), 0, s, a);
   }
   const int rows = a.b.N * (a.b.T + a.b.U + 1);
   {

@@ -19,15 +19,16 @@ struct SimpleArgs {
   float* py;
   double* alpha;       // ws [N, T, U+1], log2 domain
   double* beta;        // ws [N, T, U+1], log2 domain
+  double* Ldiag;       // ws [N, T+U+1]: per-anti-diagonal total log2-prob
   float* loss;         // [N]
   float* gx;           // [N, T, U+1]
   float* gy;
   int want_bwd;
   float* Wt;           // ws [N, T, ldw]
   int ldw;
-  float* ry;           // ws [N*T]
-  float* cx;           // ws [N*(U+1)]
-  float* cy;
+  double* ry;          // ws [N*T]      row sums of gy (fp64)
+  double* cx;          // ws [N*(U+1)]  column sums of gx (fp64)
+  double* cy;          //               column sums of gy
   float* am_grad;      // [N, T, V] or null
   float* lm_grad;      // [N, U+1, V] or null
 };
@@ -106,7 +107,7 @@ struct BandArgs {
   float* gy;
 };
 hipError_t launch_band(const BandArgs& a, hipStream_t s);
-size_t band_smem_bytes(int T, int S);
+size_t band_smem_bytes(int T, int U, int S);
 
 // ---- generic fills -----------------------------------------------------------
 hipError_t launch_fill_f32(float* p, size_t n, float v, hipStream_t s);

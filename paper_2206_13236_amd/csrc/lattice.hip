@@ -122,7 +122,7 @@ DEV void beta_pass(const float* __restrict__ px, const float* __restrict__ py, d
 
 template <int R, int P>
 __global__ __launch_bounds__(kLatThreads) void lattice_kernel(SimpleArgs a) {
-  __shared__ float red[2 * kLatThreads];
+  __shared__ double red[2 * kLatThreads];
   __shared__ double sL;
   const int n = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -150,74 +150,103 @@ __global__ __launch_bounds__(kLatThreads) void lattice_kernel(SimpleArgs a) {
   const bool live = (L2 == L2) && (L2 != kNegInfD);
   if (tid == 0) a.loss[n] = (L2 == L2) ? (float)(-L2 * kLn2) : __builtin_nanf("");
 
+  // Every complete path crosses each anti-diagonal d = t + u at exactly one
+  // node, so L = log2 sum_{t+u=d} 2^(alpha + beta) for every d. Normalising
+  // the occupations of the edges leaving diagonal d by that diagonal's own
+  // sum cancels the rounding that alpha and beta accumulate along their
+  // chains (their common part), which otherwise scales all occupations alike.
+  double* Ld = a.Ldiag + (size_t)n * (T + U1);
+  const int D = Tn + Un;
+  if (live) {
+    for (int d = wave; d < D; d += kLatThreads / 64) {
+      double v[R];
+      double mx = kNegInfD;
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        const int u = lane * R + r, t = d - u;
+        const bool on = (t >= 0) && (t < Tn) && (u <= Un);
+        const size_t i = on ? (size_t)t * U1 + u : 0;
+        v[r] = on ? alpha[i] + beta[i] : kNegInfD;
+        mx = v[r] > mx ? v[r] : mx;
+      }
+#pragma unroll
+      for (int off = 32; off >= 1; off >>= 1) {
+        const double o = __shfl_xor(mx, off, 64);
+        mx = o > mx ? o : mx;
+      }
+      double s = 0.0;
+#pragma unroll
+      for (int r = 0; r < R; ++r) s += (v[r] != kNegInfD) ? (double)exp2f((float)(v[r] - mx)) : 0.0;
+#pragma unroll
+      for (int off = 32; off >= 1; off >>= 1) s += __shfl_xor(s, off, 64);
+      if (lane == 0) Ld[d] = mx + log2(s);
+    }
+  }
+  __syncthreads();
+
   const float* ma = a.m_a + (size_t)n * T;
   const float* ml = a.m_l + (size_t)n * U1;
   float* gx = a.gx + base;
   float* gy = a.gy + base;
   float* Wt = a.want_bwd ? a.Wt + (size_t)n * T * a.ldw : nullptr;
-  for (int idx = tid; idx < T * U1; idx += kLatThreads) {
-    const int t = idx / U1, u = idx - t * U1;
-    float gxv = 0.f, gyv = 0.f;
-    if (live && t < Tn && u <= Un) {
-      const double al = alpha[idx];
-      if (u < Un) gxv = exp2_occ(al + (double)px[idx] * kLog2e + beta[idx + 1] - L2);
-      const double nb = (t + 1 < Tn) ? beta[idx + U1] : (u == Un ? 0.0 : kNegInfD);
-      gyv = exp2_occ(al + (double)py[idx] * kLog2e + nb - L2);
+  // Occupations, one frame per wave and lanes across u (coalesced). The row
+  // sums of gy (blank column of d am) are wave reductions; the column sums of
+  // gx and gy (target and blank columns of d lm) stay in fp64 registers per
+  // lane and are added across waves in a fixed order.
+  constexpr int NW = kLatThreads / 64;
+  double cxa[R], cya[R];
+#pragma unroll
+  for (int c = 0; c < R; ++c) cxa[c] = cya[c] = 0.0;
+  for (int t = wave; t < T; t += NW) {
+    double rs = 0.0;
+    const bool trow = live && t < Tn;
+    const float mat = trow ? ma[t] : 0.f;
+#pragma unroll
+    for (int c = 0; c < R; ++c) {
+      const int u = c * 64 + lane;
+      if (u >= U1) continue;
+      const size_t idx = (size_t)t * U1 + u;
+      float gxv = 0.f, gyv = 0.f;
+      const bool on = trow && u <= Un;
+      if (on) {
+        const double al = alpha[idx];
+        const double Lt = Ld[t + u];
+        if (u < Un) gxv = exp2_occ(al + (double)px[idx] * kLog2e + beta[idx + 1] - Lt);
+        const double nb = (t + 1 < Tn) ? beta[idx + U1] : (u == Un ? 0.0 : kNegInfD);
+        gyv = exp2_occ(al + (double)py[idx] * kLog2e + nb - Lt);
+      }
+      gx[idx] = gxv;
+      gy[idx] = gyv;
+      if (Wt) {
+        Wt[(size_t)t * a.ldw + u] = on ? (gxv + gyv) * expf(mat + ml[u] - a.Z[base + idx]) : 0.f;
+        rs += (double)gyv;
+        cxa[c] += (double)gxv;
+        cya[c] += (double)gyv;
+      }
     }
-    gx[idx] = gxv;
-    gy[idx] = gyv;
     if (Wt) {
-      float w = 0.f;
-      if (live && t < Tn && u <= Un) w = (gxv + gyv) * expf(ma[t] + ml[u] - a.Z[base + idx]);
-      Wt[(size_t)t * a.ldw + u] = w;
-    }
-  }
-  if (Wt && a.ldw > U1) {
-    const int padw = a.ldw - U1;
-    for (int idx = tid; idx < T * padw; idx += kLatThreads) {
-      const int t = idx / padw, u = U1 + (idx - t * padw);
-      Wt[(size_t)t * a.ldw + u] = 0.f;
+      if (lane < a.ldw - U1) Wt[(size_t)t * a.ldw + U1 + lane] = 0.f;
+#pragma unroll
+      for (int off = 32; off >= 1; off >>= 1) rs += __shfl_xor(rs, off, 64);
+      if (lane == 0) a.ry[(size_t)n * T + t] = rs;
     }
   }
   if (!a.want_bwd) return;
-  __syncthreads();
-  // Row sums ry[t] = sum_u gy(t,u) (blank column of d am): one thread per row.
-  for (int t = tid; t < T; t += kLatThreads) {
-    float s = 0.f;
-    if (t < Tn) {
-      const float* row = gy + (size_t)t * U1;
-#pragma unroll 4
-      for (int u = 0; u <= Un; ++u) s += row[u];
-    }
-    a.ry[(size_t)n * T + t] = s;
-  }
-  // Column sums cx[u] = sum_t gx(t,u), cy[u] = sum_t gy(t,u): `parts` threads
-  // per column sum interleaved frames, then the parts are added in order.
-  const int Uc = Un + 1;
-  const int parts = max(1, kLatThreads / Uc);
-  {
-    const int u = tid % Uc, part = tid / Uc;
-    if (part < parts && tid < parts * Uc) {
-      float sx = 0.f, sy = 0.f;
-      for (int t = part; t < Tn; t += parts) {
-        sx += gx[(size_t)t * U1 + u];
-        sy += gy[(size_t)t * U1 + u];
+  for (int c = 0; c < R; ++c) {
+    red[wave * 64 + lane] = cxa[c];
+    red[kLatThreads + wave * 64 + lane] = cya[c];
+    __syncthreads();
+    const int u = c * 64 + tid;
+    if (tid < 64 && u < U1) {
+      double sx = 0.0, sy = 0.0;
+      for (int w = 0; w < NW; ++w) {
+        sx += red[w * 64 + tid];
+        sy += red[kLatThreads + w * 64 + tid];
       }
-      red[part * Uc + u] = sx;
-      red[kLatThreads + part * Uc + u] = sy;
+      a.cx[(size_t)n * U1 + u] = sx;
+      a.cy[(size_t)n * U1 + u] = sy;
     }
-  }
-  __syncthreads();
-  for (int u = tid; u < U1; u += kLatThreads) {
-    float sx = 0.f, sy = 0.f;
-    if (u <= Un && Uc <= kLatThreads) {
-      for (int p = 0; p < parts; ++p) {
-        sx += red[p * Uc + u];
-        sy += red[kLatThreads + p * Uc + u];
-      }
-    }
-    a.cx[(size_t)n * U1 + u] = sx;
-    a.cy[(size_t)n * U1 + u] = sy;
+    __syncthreads();
   }
 }
 

@@ -63,22 +63,40 @@ __global__ __launch_bounds__(256) void rowmax_kernel(const float* __restrict__ x
   if (lane == 0) out[row] = m;
 }
 
-// exp(x[row][k..k+3] - mx) with zeros beyond the row end / invalid rows.
-DEV void exp4_row(const float* rowp, float mx, int k, int V, bool valid, float (&v)[4]) {
-  if (!valid) {
-    v[0] = v[1] = v[2] = v[3] = 0.f;
-    return;
-  }
-  if (((V & 3) == 0) && (k + 4 <= V)) {
+// Loads x[row][k..k+3] and the row max for exp(x - max); positions beyond the
+// row end or of an invalid row load -inf, whose exponential is 0.
+DEV void load_exp4(const float* x, const float* mx, int row, int k, int V, bool valid, RawExp<4>& r) {
+  r.m = valid ? mx[row] : 0.f;
+  const float* rowp = x + (size_t)(valid ? row : 0) * V;
+  if (valid && ((V & 3) == 0) && (k + 4 <= V)) {
     float4 q = *reinterpret_cast<const float4*>(rowp + k);
-    v[0] = expf(q.x - mx);
-    v[1] = expf(q.y - mx);
-    v[2] = expf(q.z - mx);
-    v[3] = expf(q.w - mx);
+    r.x[0] = q.x;
+    r.x[1] = q.y;
+    r.x[2] = q.z;
+    r.x[3] = q.w;
   } else {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) v[i] = (k + i < V) ? expf(rowp[k + i] - mx) : 0.f;
+    for (int i = 0; i < 4; ++i) r.x[i] = (valid && k + i < V) ? rowp[k + i] : kNegInfF;
   }
+}
+DEV void finish_exp4(const RawExp<4>& r, float (&v)[4]) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) v[i] = expf(r.x[i] - r.m);
+}
+DEV void load_plain4(const float* p, bool valid, RawF<4>& r) {
+  if (valid) {
+    float4 q = *reinterpret_cast<const float4*>(p);
+    r.v[0] = q.x;
+    r.v[1] = q.y;
+    r.v[2] = q.z;
+    r.v[3] = q.w;
+  } else {
+    r.v[0] = r.v[1] = r.v[2] = r.v[3] = 0.f;
+  }
+}
+DEV void finish_plain4(const RawF<4>& r, float (&v)[4]) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) v[i] = r.v[i];
 }
 
 // ---------------------------------------------------------------------------
@@ -86,25 +104,13 @@ DEV void exp4_row(const float* rowp, float mx, int k, int V, bool valid, float (
 // ---------------------------------------------------------------------------
 using NormCfg = GemmCfg<64, 64, 32, false>;
 
-struct NormSrcA {  // A(t, v) = exp(am[t,v] - m_a[t]), k-contiguous
-  const float* am;  // utterance base [T][V]
-  const float* ma;
-  int t0, Tn, V;
-  DEV void kc_fetch(int row, int k, float (&v)[4]) const {
-    const int t = t0 + row;
-    const bool ok = t < Tn;
-    exp4_row(am + (size_t)(ok ? t : 0) * V, ok ? ma[t] : 0.f, k, V, ok, v);
-  }
-};
-struct NormSrcB {  // B(v, u) = exp(lm[u,v] - m_l[u]); global lm[u][v] is k-contiguous per u
-  const float* lm;
-  const float* ml;
-  int u0, Un, V;
-  DEV void kc_fetch(int row, int k, float (&v)[4]) const {
-    const int u = u0 + row;
-    const bool ok = u <= Un;
-    exp4_row(lm + (size_t)(ok ? u : 0) * V, ok ? ml[u] : 0.f, k, V, ok, v);
-  }
+struct ExpRowsKC {  // rows r0 + row of x[.][V], value exp(x - max[row]); rows < lim
+  using Raw = RawExp<4>;
+  const float* x;
+  const float* mx;
+  int r0, lim, V;
+  DEV void kc_load(int row, int k, Raw& r) const { load_exp4(x, mx, r0 + row, k, V, r0 + row < lim, r); }
+  DEV void kc_finish(const Raw& r, float (&v)[4]) const { finish_exp4(r, v); }
 };
 
 __global__ __launch_bounds__(256) void normalizer_kernel(SimpleArgs a) {
@@ -119,10 +125,10 @@ __global__ __launch_bounds__(256) void normalizer_kernel(SimpleArgs a) {
   const bool active = (t0 < Tn) && (u0 <= Un);
   floatx4 acc[Cfg::FM][Cfg::FN];
   if (active) {
-    NormSrcA sa{a.am + (size_t)n * T * V, a.m_a + (size_t)n * T, t0, Tn, V};
-    NormSrcB sb{a.lm + (size_t)n * U1 * V, a.m_l + (size_t)n * U1, u0, Un, V};
-    KCLoader<Cfg, Cfg::BM, NormSrcA> la(sa);
-    KCLoader<Cfg, Cfg::BN, NormSrcB> lb(sb);
+    ExpRowsKC sa{a.am + (size_t)n * T * V, a.m_a + (size_t)n * T, t0, Tn, V};
+    ExpRowsKC sb{a.lm + (size_t)n * U1 * V, a.m_l + (size_t)n * U1, u0, Un + 1, V};
+    KCLoader<Cfg, Cfg::BM, ExpRowsKC> la(sa);
+    KCLoader<Cfg, Cfg::BN, ExpRowsKC> lb(sb);
     gemm_mainloop<Cfg>(la, lb, 0, V, smem, acc);
   }
   const int blank = a.b.blank;
@@ -164,25 +170,23 @@ __global__ __launch_bounds__(256) void normalizer_kernel(SimpleArgs a) {
 using DamCfg = GemmCfg<64, 128, 32, false>;
 
 struct WtSrcKC {  // A(t, u) = Wt[t][u], rows padded to ldw (multiple of 4, zero-filled)
+  using Raw = RawF<4>;
   const float* Wt;
   int t0, Tn, ldw;
-  DEV void kc_fetch(int row, int k, float (&v)[4]) const {
+  DEV void kc_load(int row, int k, Raw& r) const {
     const int t = t0 + row;
-    if (t < Tn && k < ldw) {
-      float4 q = *reinterpret_cast<const float4*>(Wt + (size_t)t * ldw + k);
-      v[0] = q.x; v[1] = q.y; v[2] = q.z; v[3] = q.w;
-    } else {
-      v[0] = v[1] = v[2] = v[3] = 0.f;
-    }
+    const bool ok = t < Tn && k < ldw;
+    load_plain4(Wt + (ok ? (size_t)t * ldw + k : 0), ok, r);
   }
+  DEV void kc_finish(const Raw& r, float (&v)[4]) const { finish_plain4(r, v); }
 };
 struct ExpSrcMNC {  // B(k, col) = exp(x[k][c0+col] - mx[k]) for rows k < klim, cols < V
+  using Raw = RawExp<4>;
   const float* x;  // [rows][V]
   const float* mx;
   int c0, klim, V;
-  DEV void mnc_fetch(int k, int col, float (&v)[4]) const {
-    exp4_row(x + (size_t)(k < klim ? k : 0) * V, k < klim ? mx[k] : 0.f, c0 + col, V, k < klim, v);
-  }
+  DEV void mnc_load(int k, int col, Raw& r) const { load_exp4(x, mx, k, c0 + col, V, k < klim, r); }
+  DEV void mnc_finish(const Raw& r, float (&v)[4]) const { finish_exp4(r, v); }
 };
 
 __global__ __launch_bounds__(256) void dam_kernel(SimpleArgs a) {
@@ -249,7 +253,7 @@ __global__ __launch_bounds__(256) void dam_kernel(SimpleArgs a) {
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
             const int t = t0 + tile_row<Cfg>(i, r);
-            if (t < Tn) res[i][j][r] -= a.ry[(size_t)n * T + t];
+            if (t < Tn) res[i][j][r] = (float)((double)res[i][j][r] - a.ry[(size_t)n * T + t]);
           }
       }
     }
@@ -275,17 +279,15 @@ __global__ __launch_bounds__(256) void dam_kernel(SimpleArgs a) {
 using DlmCfg = GemmCfg<64, 128, 32, false>;
 
 struct WtSrcMNC {  // A(u, t) = Wt[t][u]: global is [t][u], u-contiguous
+  using Raw = RawF<4>;
   const float* Wt;
   int u0, Tn, ldw;
-  DEV void mnc_fetch(int k, int col, float (&v)[4]) const {
+  DEV void mnc_load(int k, int col, Raw& r) const {
     const int u = u0 + col;
-    if (k < Tn && u < ldw) {
-      float4 q = *reinterpret_cast<const float4*>(Wt + (size_t)k * ldw + u);
-      v[0] = q.x; v[1] = q.y; v[2] = q.z; v[3] = q.w;
-    } else {
-      v[0] = v[1] = v[2] = v[3] = 0.f;
-    }
+    const bool ok = k < Tn && u < ldw;
+    load_plain4(Wt + (ok ? (size_t)k * ldw + u : 0), ok, r);
   }
+  DEV void mnc_finish(const Raw& r, float (&v)[4]) const { finish_plain4(r, v); }
 };
 
 __global__ __launch_bounds__(256) void dlm_kernel(SimpleArgs a) {
@@ -319,18 +321,20 @@ __global__ __launch_bounds__(256) void dlm_kernel(SimpleArgs a) {
       const float ml = uv ? a.m_l[(size_t)n * U1 + u] : 0.f;
       bool ok = true;
       const int y = (uv && u < Un) ? symbol_at(a.b, n, u, V, ok) : -1;
-      const float cxu = uv ? a.cx[(size_t)n * U1 + u] : 0.f;
-      const float cyu = uv ? a.cy[(size_t)n * U1 + u] : 0.f;
+      const double cxu = uv ? a.cx[(size_t)n * U1 + u] : 0.0;
+      const double cyu = uv ? a.cy[(size_t)n * U1 + u] : 0.0;
 #pragma unroll
       for (int j = 0; j < Cfg::FN; ++j) {
         const int v = v0 + tile_col<Cfg>(j);
         if (v >= V) continue;
         float g = 0.f;
         if (uv) {
-          g = expf(lmn[(size_t)u * V + v] - ml) * acc[i][j][r];
-          if (v == y) g -= cxu;
-          if (v == blank) g -= cyu;
-          g *= sc;
+          // the target/blank columns collect a sum over all frames: combine in
+          // fp64 and round once
+          double gd = (double)(expf(lmn[(size_t)u * V + v] - ml) * acc[i][j][r]);
+          if (v == y) gd -= cxu;
+          if (v == blank) gd -= cyu;
+          g = (float)(sc * gd);
         }
         out[(size_t)u * V + v] = g;
       }
