@@ -86,11 +86,12 @@ struct SimpleWs {
   float* py;
   double* alpha;
   double* beta;
-  double* Ldiag;
+  double* Lutt;
+  double* dummy;
   float* Wt;
   double* ry;
-  double* cx;
-  double* cy;
+  double* cpx;
+  double* cpy;
   size_t bytes;
 };
 
@@ -105,11 +106,12 @@ SimpleWs simple_layout(void* base, int N, int T, int U) {
   w.py = c.take<float>(L);
   w.alpha = c.take<double>(L);
   w.beta = c.take<double>(L);
-  w.Ldiag = c.take<double>((size_t)N * (T + U + 1));
+  w.Lutt = c.take<double>((size_t)N);
+  w.dummy = c.take<double>((size_t)N * 2 * 1024);
   w.Wt =c.take<float>(NT * ldw_of(U));
   w.ry = c.take<double>(NT);
-  w.cx = c.take<double>(NU);
-  w.cy = c.take<double>(NU);
+  w.cpx = c.take<double>((size_t)N * lattice_colblocks(T) * (U + 1));
+  w.cpy = c.take<double>((size_t)N * lattice_colblocks(T) * (U + 1));
   w.bytes = c.off;
   return w;
 }
@@ -227,7 +229,8 @@ int rnnt_simple_loss(const rnnt_batch* batch, int32_t V, const float* am, const 
   a.py = py ? py : w.py;
   a.alpha = w.alpha;
   a.beta = w.beta;
-  a.Ldiag = w.Ldiag;
+  a.Lutt = w.Lutt;
+  a.dummy = w.dummy;
   a.loss = loss;
   a.gx = px_occ;
   a.gy = py_occ;
@@ -235,8 +238,9 @@ int rnnt_simple_loss(const rnnt_batch* batch, int32_t V, const float* am, const 
   a.Wt = w.Wt;
   a.ldw = ldw_of(batch->U);
   a.ry = w.ry;
-  a.cx = w.cx;
-  a.cy = w.cy;
+  a.cpx = w.cpx;
+  a.cpy = w.cpy;
+  a.ncolblk = lattice_colblocks(batch->T);
   a.am_grad = am_grad;
   a.lm_grad = lm_grad;
   hipError_t e = launch_rowmax(a, s);
@@ -308,6 +312,8 @@ size_t rnnt_pruned_loss_workspace_size(int32_t N, int32_t T, int32_t S) {
   Carve c(nullptr);
   c.take<double>((size_t)N * T * S);
   c.take<double>((size_t)N * T * S);
+  c.take<double>((size_t)N);
+  c.take<double>((size_t)N * 2 * 64);
   return c.off;
 }
 
@@ -333,6 +339,8 @@ int rnnt_pruned_loss(const rnnt_batch* batch, int32_t S, const float* px, const 
   a.ranges = ranges;
   a.alpha = c.take<double>((size_t)batch->N * batch->T * S);
   a.beta = c.take<double>((size_t)batch->N * batch->T * S);
+  a.Lutt = c.take<double>((size_t)batch->N);
+  a.dummy = c.take<double>((size_t)batch->N * 2 * 64);
   a.loss = loss;
   a.gx = px_occ;
   a.gy = py_occ;

@@ -2,111 +2,131 @@
 // Fig. 1(b)): only nodes p_t <= u < p_t + S (and u <= U) exist; every
 // transition into any other node is -inf. Loss and band occupations.
 //
-// Anti-diagonal schedule. Band node (t, s) (u = p_t + s) lies on diagonal
-// d = t + u = e_t + s with e_t = t + p_t strictly increasing in t. Its
-// vertical predecessor (t, s-1) is on diagonal d-1 of the same frame and its
-// horizontal predecessor (t-1, u) is on diagonal d-1 of frame t-1. So a wave
-// can advance the whole band one diagonal per step: lane l handles the frames
-// t = l, l+64, l+128, ... in turn (a frame is active for at most S <= 32
-// consecutive diagonals, so a lane is always free when its next frame
-// starts), keeps its own vertical carry in a register and receives the
-// horizontal value from lane l-1 by one rotate. The sequential depth is
-// T + U diagonals instead of T * S slot updates.
+// band_fb_kernel, anti-diagonal schedule. Band node (t, s) (u = p_t + s) lies
+// on diagonal d = t + u = e_t + s with e_t = t + p_t strictly increasing in t.
+// Its vertical predecessor (t, s-1) is on diagonal d-1 of the same frame and
+// its horizontal predecessor (t-1, u) is on diagonal d-1 of frame t-1. So a
+// wave advances the whole band one diagonal per step: lane l handles the
+// frames t = l, l+64, l+128, ... in turn (a frame is active for at most
+// S <= 32 consecutive diagonals, so a lane is always free when its next frame
+// starts), keeps its vertical carry in a register and receives the horizontal
+// value from lane l-1 by one DPP wave rotate. The sequential depth is T + U
+// diagonals instead of T * S slot updates. Wave 0 runs alpha and wave 1 beta
+// concurrently; band log-probs and bounds are staged in LDS and each lane
+// prefetches its next node's values one step ahead.
 //
-// Wave 0 runs the forward (alpha) pass and wave 1 the backward (beta) pass
-// concurrently; then all waves form the occupations. Band log-probs and the
-// bounds are staged in LDS first. Same precision scheme as the full lattice:
-// log2 domain, fp64 accumulators, fp32 exp2/log2 only for LogAdd's bounded
-// correction term.
+// band_occ_kernel: one wave per frame of the batch, lanes over the S slots.
+// Every complete path leaves frame t through exactly one blank edge, so the
+// frame's own log-sum of alpha + blank + beta(next) equals the total; the
+// occupations of frame t are normalised by it (cancelling the rounding the
+// alpha and beta chains accumulate in common).
+//
+// Same precision scheme as the full lattice: log2 domain, fp64 accumulators,
+// fp32 exp2/log2 only for LogAdd's bounded correction term.
 #include "kernels.h"
 #include "prof.h"
 
 namespace {
 
-constexpr int kBandThreads = 256;
+constexpr int kBandThreads = 128;
 
 struct BandView {
-  const float* X;  // px [T*S] of the utterance (LDS or global)
+  const float* X;  // px [T*S] of the utterance (LDS)
   const float* Y;  // py
   const int* P;    // p_t [T]
   int Tn, Un, S;
 };
 
+// Start diagonal e = t + p_t and number of present slots of frame t (e huge
+// and no slots outside [0, Tn)); the LDS read is unconditional.
 DEV void band_frame(const BandView& v, int t, int& e, int& ns) {
-  if (t >= 0 && t < v.Tn) {
-    const int p = v.P[t];
-    e = t + p;
-    ns = min(v.S, v.Un - p + 1);
-  } else {
-    e = 1 << 30;
-    ns = 0;
-  }
+  const bool in = (t >= 0) && (t < v.Tn);
+  const int p = v.P[in ? t : 0];
+  e = in ? t + p : (1 << 30);
+  ns = in ? min(v.S, v.Un - p + 1) : 0;
 }
 
-DEV void band_alpha(const BandView& v, double* __restrict__ alpha, int lane) {
-  const int D = v.Tn + v.Un;
+// The step loops below are branch-free: frame switches are selects, the
+// geometry of the lane's following frame is re-read from LDS every step (and
+// only used at the next switch), the values of the next node are prefetched
+// every step, and lanes without a node store into a per-lane dummy slot.
+// Divergent branches with LDS reads would make every step wait for them.
+DEV void band_alpha(const BandView& v, double* __restrict__ alpha, double* __restrict__ dummy, int lane) {
+  const int D = v.Tn + v.Un, S = v.S;
   int t = lane, e, ns;
   band_frame(v, t, e, ns);
+  int tn = t + 64, en, nsn;
+  band_frame(v, tn, en, nsn);
   double hout = kNegInfD, vout = kNegInfD;
-  const int src = (lane + 63) & 63;
+  int kn = (t < v.Tn) ? t * S : 0;  // the next node this lane will process
+  float xn = v.X[kn], yn = v.Y[kn];
   for (int d = 0; d < D; ++d) {
-    double hin = __shfl(hout, src, 64);
-    int s = d - e;
-    if (s >= ns && t < v.Tn) {
-      t += 64;
-      band_frame(v, t, e, ns);
-      s = d - e;
-    }
-    double nh = kNegInfD, nv = kNegInfD;
-    if (s >= 0 && s < ns) {
-      const int k = t * v.S + s;
-      const double x2 = (double)v.X[k] * kLog2e;
-      const double y2 = (double)v.Y[k] * kLog2e;
-      if (t == 0) hin = kNegInfD;
-      const double vin = (s == 0) ? kNegInfD : vout;
-      const double al = (d == 0) ? 0.0 : log2add(hin, vin);
-      alpha[k] = al;
-      nh = al + y2;
-      nv = al + x2;
-    }
-    hout = nh;
-    vout = nv;
+    const double hin0 = dpp_move_d<kDppWaveRor1>(hout, kNegInfD);
+    const bool adv = (d - e >= ns) && (t < v.Tn);
+    t = adv ? tn : t;
+    e = adv ? en : e;
+    ns = adv ? nsn : ns;
+    tn = t + 64;
+    band_frame(v, tn, en, nsn);
+    const int s = d - e;
+    const bool act = (s >= 0) && (s < ns);
+    const int k = act ? t * S + s : 0;
+    const double x2 = (double)xn * kLog2e;
+    const double y2 = (double)yn * kLog2e;
+    const double hin = (t == 0) ? kNegInfD : hin0;
+    const double vin = (s == 0) ? kNegInfD : vout;
+    const double al = (d == 0) ? 0.0 : log2add(hin, vin);
+    double* dst = act ? alpha + k : dummy + lane;
+    *dst = al;
+    hout = act ? al + y2 : kNegInfD;
+    vout = act ? al + x2 : kNegInfD;
+    // next node: (t, s+1) while the frame lasts, else the first node of frame t+64
+    kn = act ? ((s + 1 < ns) ? k + 1 : (tn < v.Tn ? tn * S : 0)) : kn;
+    xn = v.X[kn];
+    yn = v.Y[kn];
   }
 }
 
-DEV void band_beta(const BandView& v, double* __restrict__ beta, int lane) {
-  const int D = v.Tn + v.Un;
+DEV void band_beta(const BandView& v, double* __restrict__ beta, double* __restrict__ dummy, int lane) {
+  const int D = v.Tn + v.Un, S = v.S;
   // this lane's frames in descending order: the largest t = lane (mod 64) below Tn
   int t = (lane < v.Tn) ? lane + 64 * ((v.Tn - 1 - lane) / 64) : -1;
   int e, ns;
   band_frame(v, t, e, ns);
+  int tn = t - 64, en, nsn;
+  band_frame(v, tn, en, nsn);
   double bout = kNegInfD;
-  const int src = (lane + 1) & 63;
+  int kn = (t >= 0) ? t * S + ns - 1 : 0;  // the next node this lane will process
+  float xn = v.X[kn], yn = v.Y[kn];
   for (int d = D - 1; d >= 0; --d) {
-    double hin = __shfl(bout, src, 64);
-    int s = d - e;
-    if (s < 0 && t >= 0) {
-      t -= 64;
-      band_frame(v, t, e, ns);
-      s = d - e;
-    }
-    double nb = kNegInfD;
-    if (t >= 0 && s >= 0 && s < ns) {
-      const int k = t * v.S + s;
-      const double x2 = (double)v.X[k] * kLog2e;
-      const double y2 = (double)v.Y[k] * kLog2e;
-      if (t == v.Tn - 1) hin = (v.P[t] + s == v.Un) ? 0.0 : kNegInfD;
-      const double vin = (s + 1 < ns) ? bout : kNegInfD;
-      nb = log2add(y2 + hin, x2 + vin);
-      beta[k] = nb;
-    }
-    bout = nb;
+    const double hin0 = dpp_move_d<kDppWaveRol1>(bout, kNegInfD);
+    const bool adv = (d - e < 0) && (t >= 0);
+    t = adv ? tn : t;
+    e = adv ? en : e;
+    ns = adv ? nsn : ns;
+    tn = t - 64;
+    band_frame(v, tn, en, nsn);
+    const int s = d - e;
+    const bool act = (t >= 0) && (s >= 0) && (s < ns);
+    const int k = act ? t * S + s : 0;
+    const double x2 = (double)xn * kLog2e;
+    const double y2 = (double)yn * kLog2e;
+    // the successor of the last frame's final node is the end (beta = 0)
+    const double hin = (t == v.Tn - 1) ? ((e - t + s == v.Un) ? 0.0 : kNegInfD) : hin0;
+    const double vin = (s + 1 < ns) ? bout : kNegInfD;
+    const double be = log2add(y2 + hin, x2 + vin);
+    double* dst = act ? beta + k : dummy + lane;
+    *dst = be;
+    bout = act ? be : kNegInfD;
+    // next node: (t, s-1) while the frame lasts, else the top node of frame t-64
+    kn = act ? ((s > 0) ? k - 1 : (tn >= 0 ? tn * S + nsn - 1 : 0)) : kn;
+    xn = v.X[kn];
+    yn = v.Y[kn];
   }
 }
 
-__global__ __launch_bounds__(kBandThreads) void band_kernel(BandArgs a) {
+__global__ __launch_bounds__(kBandThreads) void band_fb_kernel(BandArgs a) {
   extern __shared__ __align__(16) float sm[];
-  __shared__ double sL;
   const int n = blockIdx.x;
   const int T = a.b.T, S = a.S;
   int Tn, Un;
@@ -133,100 +153,85 @@ __global__ __launch_bounds__(kBandThreads) void band_kernel(BandArgs a) {
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   double* alpha = a.alpha + base;
   double* beta = a.beta + base;
-  if (wave == 0) band_alpha(v, alpha, lane);
-  else if (wave == 1) band_beta(v, beta, lane);
+  double* dummy = a.dummy + ((size_t)n * 2 + wave) * 64;
+  if (wave == 0) band_alpha(v, alpha, dummy, lane);
+  else band_beta(v, beta, dummy, lane);
   __syncthreads();
   if (threadIdx.x == 0) {
-    const int pl = v.P[Tn - 1];
-    const int se = Un - pl;
+    const int se = Un - P[Tn - 1];
     double L = kNegInfD;
-    if (se >= 0 && se < S) L = alpha[(size_t)(Tn - 1) * S + se] + (double)v.Y[(Tn - 1) * S + se] * kLog2e;
-    sL = ok ? L : __builtin_nan("");
+    if (se >= 0 && se < S) L = alpha[(size_t)(Tn - 1) * S + se] + (double)Y[(Tn - 1) * S + se] * kLog2e;
+    const double L2 = ok ? L : __builtin_nan("");
+    a.Lutt[n] = L2;
+    a.loss[n] = (L2 == L2) ? (float)(-L2 * kLn2) : __builtin_nanf("");
   }
-  __syncthreads();
-  const double L2 = sL;
-  if (threadIdx.x == 0) a.loss[n] = (L2 == L2) ? (float)(-L2 * kLn2) : __builtin_nanf("");
-  if (!a.gx && !a.gy) return;
-  const bool live = (L2 == L2) && (L2 != kNegInfD);
-  // Per-anti-diagonal normalisers (every complete path crosses diagonal
-  // d = t + u at exactly one band node): the occupations of the edges leaving
-  // diagonal d are normalised by that diagonal's own total, which cancels the
-  // common part of the rounding accumulated by alpha and beta.
-  double* Ld = reinterpret_cast<double*>(sm + (size_t)2 * T * S + T + (T & 1));
-  const int D = Tn + Un;
-  if (live) {
-    for (int d = threadIdx.x; d < D; d += kBandThreads) {
-      // last frame whose band starts at or before d (e_t = t + p_t is increasing)
-      int lo = 0, hi = Tn - 1;
-      while (lo < hi) {
-        const int mid = (lo + hi + 1) >> 1;
-        if (mid + P[mid] <= d) lo = mid;
-        else hi = mid - 1;
+}
+
+__global__ __launch_bounds__(256) void band_occ_kernel(BandArgs a) {
+  const int T = a.b.T, S = a.S;
+  const int lane = threadIdx.x & 63;
+  const int f = blockIdx.x * 4 + (threadIdx.x >> 6);  // frame over N*T
+  if (f >= a.b.N * T) return;
+  const int n = f / T, t = f - n * T;
+  int Tn, Un;
+  utt_dims(a.b, n, Tn, Un);
+  const double Lu = a.Lutt[n];
+  const bool live = (Lu == Lu) && (Lu != kNegInfD) && t < Tn;
+  const int s = lane;
+  double ey = kNegInfD, ex = kNegInfD;
+  if (live && s < S) {
+    const int p = min(max(a.ranges[(size_t)f * S], 0), Un);
+    const int u = p + s;
+    if (u <= Un) {
+      const size_t k = (size_t)f * S + s;
+      const double al = a.alpha[k];
+      double nb;
+      if (t + 1 < Tn) {
+        const int pn = min(max(a.ranges[(size_t)(f + 1) * S], 0), Un);
+        const int s2 = u - pn;
+        nb = (s2 >= 0 && s2 < S) ? a.beta[(size_t)(f + 1) * S + s2] : kNegInfD;
+      } else {
+        nb = (u == Un) ? 0.0 : kNegInfD;
       }
-      double mx = kNegInfD;
-      for (int t = lo; t >= 0 && d - (t + P[t]) < S; --t) {
-        const int s = d - (t + P[t]);
-        if (s >= 0 && P[t] + s <= Un) {
-          const double x = alpha[(size_t)t * S + s] + beta[(size_t)t * S + s];
-          mx = x > mx ? x : mx;
-        }
-      }
-      double sum = 0.0;
-      for (int t = lo; t >= 0 && d - (t + P[t]) < S; --t) {
-        const int s = d - (t + P[t]);
-        if (s >= 0 && P[t] + s <= Un) {
-          const double x = alpha[(size_t)t * S + s] + beta[(size_t)t * S + s];
-          if (x != kNegInfD) sum += (double)exp2f((float)(x - mx));
-        }
-      }
-      Ld[d] = mx + log2(sum);
+      ey = al + (double)a.py[k] * kLog2e + nb;
+      if (s + 1 < S && u + 1 <= Un) ex = al + (double)a.px[k] * kLog2e + a.beta[k + 1];
     }
   }
-  __syncthreads();
-  for (int i = threadIdx.x; i < T * S; i += kBandThreads) {
-    const int t = i / S, s = i - t * S;
+  const double mx = wave_max_d(ey);
+  const double sum = wave_sum_d((ey != kNegInfD) ? (double)exp2f((float)(ey - mx)) : 0.0);
+  const double Lt = mx + log2(sum);
+  if (s < S) {
     float gxv = 0.f, gyv = 0.f;
-    if (live && t < Tn) {
-      const int p = v.P[t];
-      const int u = p + s;
-      if (u <= Un) {
-        const double al = alpha[i];
-        const double Lt = Ld[t + u];
-        if (s + 1 < S && u + 1 <= Un)
-          gxv = exp2_occ(al + (double)v.X[i] * kLog2e + beta[i + 1] - Lt);
-        double nb;
-        if (t + 1 < Tn) {
-          const int s2 = u - v.P[t + 1];
-          nb = (s2 >= 0 && s2 < S) ? beta[(size_t)(t + 1) * S + s2] : kNegInfD;
-        } else {
-          nb = (u == Un) ? 0.0 : kNegInfD;
-        }
-        gyv = exp2_occ(al + (double)v.Y[i] * kLog2e + nb - Lt);
-      }
-    }
-    if (a.gx) a.gx[base + i] = gxv;
-    if (a.gy) a.gy[base + i] = gyv;
+    if (live && ey != kNegInfD) gyv = exp2_occ(ey - Lt);
+    if (live && ex != kNegInfD) gxv = exp2_occ(ex - Lt);
+    if (a.gx) a.gx[(size_t)f * S + s] = gxv;
+    if (a.gy) a.gy[(size_t)f * S + s] = gyv;
   }
 }
 
 }  // namespace
 
-// px, py [T*S] floats, p_t [T] ints (padded to 8 bytes), per-diagonal totals [T+U+1] doubles
+// px, py [T*S] floats, p_t [T] ints
 size_t band_smem_bytes(int T, int U, int S) {
-  return (size_t)T * S * 2 * sizeof(float) + (size_t)(T + (T & 1)) * sizeof(int) + (size_t)(T + U + 1) * sizeof(double);
+  (void)U;
+  return (size_t)T * S * 2 * sizeof(float) + (size_t)T * sizeof(int);
 }
 
 hipError_t launch_band(const BandArgs& a, hipStream_t s) {
   const size_t sm = band_smem_bytes(a.b.T, a.b.U, a.S);
   if (sm > 150 * 1024) return hipErrorInvalidValue;
   if (sm > 64 * 1024) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(band_kernel),
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(band_fb_kernel),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)sm);
     if (e != hipSuccess) return e;
   }
   {
-    RNNT_PROF(s, "band");
-    hipLaunchKernelGGL(band_kernel, dim3(a.b.N), dim3(kBandThreads), sm, s, a);
+    RNNT_PROF(s, "band_fb");
+    hipLaunchKernelGGL(band_fb_kernel, dim3(a.b.N), dim3(kBandThreads), sm, s, a);
+  }
+  if (a.gx || a.gy) {
+    RNNT_PROF(s, "band_occ");
+    hipLaunchKernelGGL(band_occ_kernel, dim3((a.b.N * a.b.T + 3) / 4), dim3(256), 0, s, a);
   }
   return hipGetLastError();
 }

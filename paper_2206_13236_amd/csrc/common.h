@@ -82,4 +82,33 @@ DEV float fast_tanh(float x) {
 DEV double shfl_up_d(double v, int delta) { return __shfl_up(v, delta, 64); }
 DEV double shfl_down_d(double v, int delta) { return __shfl_down(v, delta, 64); }
 
+// Whole-wave DPP lane moves (GFX9 wave_shr/shl/ror/rol by one lane), for a
+// double held in two VGPRs. Lanes without a source keep `old`.
+constexpr int kDppWaveShl1 = 0x130;  // lane i <- lane i+1
+constexpr int kDppWaveRol1 = 0x134;  // lane i <- lane (i+1) mod 64
+constexpr int kDppWaveShr1 = 0x138;  // lane i <- lane i-1
+constexpr int kDppWaveRor1 = 0x13C;  // lane i <- lane (i-1) mod 64
+
+template <int CTRL>
+DEV double dpp_move_d(double v, double old) {
+  const int lo = __builtin_amdgcn_update_dpp(__double2loint(old), __double2loint(v), CTRL, 0xf, 0xf, false);
+  const int hi = __builtin_amdgcn_update_dpp(__double2hiint(old), __double2hiint(v), CTRL, 0xf, 0xf, false);
+  return __hiloint2double(hi, lo);
+}
+
+// Wave-wide max and sum of doubles (fixed butterfly order: deterministic).
+DEV double wave_max_d(double v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    const double o = __shfl_xor(v, off, 64);
+    v = o > v ? o : v;
+  }
+  return v;
+}
+DEV double wave_sum_d(double v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+
 DEV size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }

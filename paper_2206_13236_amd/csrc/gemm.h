@@ -1,6 +1,6 @@
 // MFMA GEMM main loop for gfx950, shared by every contraction of the library.
 //
-// A workgroup of 256 threads (4 wave64s in a 2x2 grid) computes a BM x BN
+// A workgroup of WGM x WGN wave64s (NT threads) computes a BM x BN
 // tile of C = A * B with K-steps of BK. Operand tiles are staged through LDS
 // in a k-contiguous layout ([row][k], rows padded by 16 bytes) so that every
 // lane fetches one 16-byte fragment per 16x16 output block per k-slice:
@@ -30,7 +30,7 @@
 
 #include "common.h"
 
-template <int BM_, int BN_, int BK_, bool BF16_>
+template <int BM_, int BN_, int BK_, bool BF16_, int WGM_ = 2, int WGN_ = 2>
 struct GemmCfg {
   static constexpr int BM = BM_, BN = BN_, BK = BK_;
   static constexpr bool BF16 = BF16_;
@@ -39,7 +39,9 @@ struct GemmCfg {
   static constexpr int KV = 16 / ESZ;         // k values per 16-byte fragment
   static constexpr int KSLICE = 4 * KV;       // k covered by one fragment across 4 lane groups
   static constexpr int LDK = BK + KV;         // padded LDS row stride (elements)
-  static constexpr int WM = BM / 2, WN = BN / 2;
+  static constexpr int WGM = WGM_, WGN = WGN_;       // wave grid
+  static constexpr int NT = 64 * WGM * WGN;          // threads per workgroup
+  static constexpr int WM = BM / WGM, WN = BN / WGN;  // wave tile
   static constexpr int FM = WM / 16, FN = WN / 16;
   static constexpr int A_ELEMS = BM * LDK, B_ELEMS = BN * LDK;
   static constexpr int STAGE_ELEMS = A_ELEMS + B_ELEMS;
@@ -79,22 +81,22 @@ template <class Cfg, int ROWS, class Src>
 struct KCLoader {
   static constexpr int KV = Cfg::KV;
   static constexpr int CPR = Cfg::BK / KV;               // 16-byte chunks per row
-  static constexpr int NCH = (ROWS * CPR + 255) / 256;   // chunks per thread
+  static constexpr int NCH = (ROWS * CPR + Cfg::NT - 1) / Cfg::NT;  // chunks per thread
   struct Reg { typename Src::Raw v[NCH]; };
   const Src& src;
   DEV explicit KCLoader(const Src& s) : src(s) {}
   DEV void fetch(int k0, Reg& r) const {
 #pragma unroll
     for (int i = 0; i < NCH; ++i) {
-      int c = threadIdx.x + 256 * i;
-      if (ROWS * CPR % 256 == 0 || c < ROWS * CPR) src.kc_load(c / CPR, k0 + (c % CPR) * KV, r.v[i]);
+      int c = threadIdx.x + Cfg::NT * i;
+      if (ROWS * CPR % Cfg::NT == 0 || c < ROWS * CPR) src.kc_load(c / CPR, k0 + (c % CPR) * KV, r.v[i]);
     }
   }
   DEV void put(const Reg& r, typename Cfg::T* lds) const {
 #pragma unroll
     for (int i = 0; i < NCH; ++i) {
-      int c = threadIdx.x + 256 * i;
-      if (ROWS * CPR % 256 == 0 || c < ROWS * CPR) {
+      int c = threadIdx.x + Cfg::NT * i;
+      if (ROWS * CPR % Cfg::NT == 0 || c < ROWS * CPR) {
         float v[KV];
         src.kc_finish(r.v[i], v);
         pack_store16<Cfg>(lds + (c / CPR) * Cfg::LDK + (c % CPR) * KV, v);
@@ -111,15 +113,15 @@ struct MNCLoader {
   static constexpr int NV = 16 / KV;                       // rows per block (4 fp32, 2 bf16)
   static constexpr int NBR = ROWS / NV;                    // blocks along rows
   static constexpr int NBLK = (Cfg::BK / KV) * NBR;
-  static constexpr int NPT = (NBLK + 255) / 256;
+  static constexpr int NPT = (NBLK + Cfg::NT - 1) / Cfg::NT;
   struct Reg { typename Src::Raw v[NPT][KV]; };
   const Src& src;
   DEV explicit MNCLoader(const Src& s) : src(s) {}
   DEV void fetch(int k0, Reg& r) const {
 #pragma unroll
     for (int b = 0; b < NPT; ++b) {
-      int blk = threadIdx.x + 256 * b;
-      if (NBLK % 256 == 0 || blk < NBLK) {
+      int blk = threadIdx.x + Cfg::NT * b;
+      if (NBLK % Cfg::NT == 0 || blk < NBLK) {
         int kb = blk / NBR, nb = blk % NBR;
 #pragma unroll
         for (int i = 0; i < KV; ++i) src.mnc_load(k0 + kb * KV + i, nb * NV, r.v[b][i]);
@@ -129,8 +131,8 @@ struct MNCLoader {
   DEV void put(const Reg& r, typename Cfg::T* lds) const {
 #pragma unroll
     for (int b = 0; b < NPT; ++b) {
-      int blk = threadIdx.x + 256 * b;
-      if (NBLK % 256 == 0 || blk < NBLK) {
+      int blk = threadIdx.x + Cfg::NT * b;
+      if (NBLK % Cfg::NT == 0 || blk < NBLK) {
         int kb = blk / NBR, nb = blk % NBR;
         float m[KV][NV];
 #pragma unroll
@@ -151,7 +153,7 @@ template <class Cfg>
 DEV void gemm_compute_stage(const typename Cfg::T* As, const typename Cfg::T* Bs,
                             floatx4 (&acc)[Cfg::FM][Cfg::FN]) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / Cfg::WGN, wn = wave % Cfg::WGN;
   const typename Cfg::T* a_base = As + (wm * Cfg::WM + (lane & 15)) * Cfg::LDK + (lane >> 4) * Cfg::KV;
   const typename Cfg::T* b_base = Bs + (wn * Cfg::WN + (lane & 15)) * Cfg::LDK + (lane >> 4) * Cfg::KV;
 #pragma unroll
@@ -185,7 +187,7 @@ DEV void gemm_compute_stage(const typename Cfg::T* As, const typename Cfg::T* Bs
 }
 
 // Runs the K loop over [k_begin, k_end) and leaves the tile in `acc`.
-// Must be called by all 256 threads of the workgroup (it contains barriers).
+// Must be called by all NT threads of the workgroup (it contains barriers).
 template <class Cfg, class LA, class LB>
 DEV void gemm_mainloop(const LA& la, const LB& lb, int k_begin, int k_end,
                        typename Cfg::T* smem, floatx4 (&acc)[Cfg::FM][Cfg::FN]) {
@@ -225,11 +227,11 @@ DEV void gemm_mainloop(const LA& la, const LB& lb, int k_begin, int k_end,
 // Row/column of output element (i, j, r) of this lane within the tile.
 template <class Cfg>
 DEV int tile_row(int i, int r) {
-  const int lane = threadIdx.x & 63, wm = (threadIdx.x >> 6) >> 1;
+  const int lane = threadIdx.x & 63, wm = (threadIdx.x >> 6) / Cfg::WGN;
   return wm * Cfg::WM + i * 16 + 4 * (lane >> 4) + r;
 }
 template <class Cfg>
 DEV int tile_col(int j) {
-  const int lane = threadIdx.x & 63, wn = (threadIdx.x >> 6) & 1;
+  const int lane = threadIdx.x & 63, wn = (threadIdx.x >> 6) % Cfg::WGN;
   return wn * Cfg::WN + j * 16 + (lane & 15);
 }

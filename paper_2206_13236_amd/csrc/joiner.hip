@@ -695,7 +695,16 @@ __global__ __launch_bounds__(256) void joiner_encdec_kernel(JoinerArgs a) {
   const int t1 = lo;
   for (int j = threadIdx.x; j < J; j += blockDim.x) {
     float s = 0.f;
-    for (int t = t0; t < t1; ++t) s += a.dpre[((size_t)(off + t) * S + (u - sp[t])) * J + j];
+    int t = t0;
+    // loads of 8 frames in flight, added in ascending t
+    for (; t + 8 <= t1; t += 8) {
+      float v[8];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) v[q] = a.dpre[((size_t)(off + t + q) * S + (u - sp[t + q])) * J + j];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) s += v[q];
+    }
+    for (; t < t1; ++t) s += a.dpre[((size_t)(off + t) * S + (u - sp[t])) * J + j];
     out[j] = s;
   }
 }

@@ -19,7 +19,8 @@ struct SimpleArgs {
   float* py;
   double* alpha;       // ws [N, T, U+1], log2 domain
   double* beta;        // ws [N, T, U+1], log2 domain
-  double* Ldiag;       // ws [N, T+U+1]: per-anti-diagonal total log2-prob
+  double* Lutt;        // ws [N]: total log2-prob (NaN for an invalid utterance)
+  double* dummy;       // ws [N, 2, 1024]: store target of lanes outside the lattice
   float* loss;         // [N]
   float* gx;           // [N, T, U+1]
   float* gy;
@@ -27,8 +28,9 @@ struct SimpleArgs {
   float* Wt;           // ws [N, T, ldw]
   int ldw;
   double* ry;          // ws [N*T]      row sums of gy (fp64)
-  double* cx;          // ws [N*(U+1)]  column sums of gx (fp64)
-  double* cy;          //               column sums of gy
+  double* cpx;         // ws [N, ncolblk, U+1]: column sums of gx over 16-frame blocks
+  double* cpy;         //                       same for gy
+  int ncolblk;
   float* am_grad;      // [N, T, V] or null
   float* lm_grad;      // [N, U+1, V] or null
 };
@@ -36,6 +38,7 @@ struct SimpleArgs {
 hipError_t launch_rowmax(const SimpleArgs& a, hipStream_t s);
 hipError_t launch_normalizer(const SimpleArgs& a, hipStream_t s);
 hipError_t launch_lattice(const SimpleArgs& a, hipStream_t s);
+int lattice_colblocks(int T);
 hipError_t launch_simple_grads(const SimpleArgs& a, hipStream_t s);
 
 // ---- stage 3: pruning bounds -----------------------------------------------
@@ -102,6 +105,8 @@ struct BandArgs {
   const int* ranges;   // [N, T, S]
   double* alpha;       // ws [N, T, S] log2 domain
   double* beta;
+  double* Lutt;        // ws [N]: total log2-prob (NaN for an invalid utterance)
+  double* dummy;       // ws [N, 2, 64]: store target of lanes without a node
   float* loss;
   float* gx;           // [N, T, S] or null
   float* gy;

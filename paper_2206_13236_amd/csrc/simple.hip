@@ -321,19 +321,27 @@ __global__ __launch_bounds__(256) void dlm_kernel(SimpleArgs a) {
       const float ml = uv ? a.m_l[(size_t)n * U1 + u] : 0.f;
       bool ok = true;
       const int y = (uv && u < Un) ? symbol_at(a.b, n, u, V, ok) : -1;
-      const double cxu = uv ? a.cx[(size_t)n * U1 + u] : 0.0;
-      const double cyu = uv ? a.cy[(size_t)n * U1 + u] : 0.0;
 #pragma unroll
       for (int j = 0; j < Cfg::FN; ++j) {
         const int v = v0 + tile_col<Cfg>(j);
         if (v >= V) continue;
         float g = 0.f;
         if (uv) {
-          // the target/blank columns collect a sum over all frames: combine in
-          // fp64 and round once
+          // The target and blank columns collect sum_t gx(t,u) and sum_t gy(t,u):
+          // added from the per-16-frame partials in fixed order, in fp64, and
+          // rounded once.
           double gd = (double)(expf(lmn[(size_t)u * V + v] - ml) * acc[i][j][r]);
-          if (v == y) gd -= cxu;
-          if (v == blank) gd -= cyu;
+          if (v == y || v == blank) {
+            double cx = 0.0, cy = 0.0;
+            const double* px_ = a.cpx + (size_t)n * a.ncolblk * U1 + u;
+            const double* py_ = a.cpy + (size_t)n * a.ncolblk * U1 + u;
+            for (int q = 0; q < a.ncolblk; ++q) {
+              cx += px_[(size_t)q * U1];
+              cy += py_[(size_t)q * U1];
+            }
+            if (v == y) gd -= cx;
+            if (v == blank) gd -= cy;
+          }
           g = (float)(sc * gd);
         }
         out[(size_t)u * V + v] = g;
