@@ -10,8 +10,10 @@ The workload is the BPE-sized batch (N=16, T ~ U[150,250], U ~ U[20,60],
 V=500, S=5, J=512, fp32), synthetic and seeded; frames = sum of valid T_n.
 
 Prints one JSON line: frames/s, peak HBM bytes, the roofline of the dominant
-contraction (HIP events recorded by the library on the launch stream during
-the timed steps) and the CPU oracle's throughput on the host cores.
+contraction (HIP events recorded by the library on the launch stream around
+that kernel only, during the timed steps), a per-kernel census from a short
+untimed pass with every launch bracketed, and the CPU oracle's throughput on
+the host cores.
 """
 from __future__ import annotations
 
@@ -114,7 +116,38 @@ def main() -> int:
         step.step(batch, am, lm, enc, dec, W, bias)
     torch.cuda.synchronize()
     L = _native.lib()
+
+    def kernel_table(nsteps):
+        buf = ctypes.create_string_buffer(4096)
+        L.rnnt_profile_names(buf, 4096)
+        out = {}
+        for name in [x for x in buf.value.decode().split(",") if x]:
+            n = ctypes.c_int32()
+            tot = ctypes.c_double()
+            _native.check(L.rnnt_profile_query(name.encode(), ctypes.byref(n), ctypes.byref(tot)))
+            out[name] = {"launches": n.value, "avg_us": round(1000 * tot.value / max(n.value, 1), 2),
+                         "us_per_step": round(1000 * tot.value / nsteps, 2)}
+        return out
+
+    # census: every kernel bracketed by events, outside the timed region (the
+    # event packets themselves cost ~5 us per launch)
+    census_steps = max(1, min(args.steps, 5))
     L.rnnt_profile_reset()
+    L.rnnt_profile_select(None)
+    L.rnnt_profile_enable(1)
+    for _ in range(census_steps):
+        step.step(batch, am, lm, enc, dec, W, bias)
+    torch.cuda.synchronize()
+    L.rnnt_profile_enable(0)
+    kernels = kernel_table(census_steps)
+    L.rnnt_profile_reset()
+    # the dominant contraction: joiner GEMMs with algorithmic work 2*M*J*V each
+    # (a recompute of the logits in the backward would be overhead, not work)
+    work = {"joiner_fwd": 2.0 * M * J * V, "joiner_dh": 2.0 * M * J * V, "joiner_dw": 2.0 * M * J * V}
+    dom = max((k for k in work if k in kernels), key=lambda k: kernels[k]["us_per_step"])
+
+    # timed region: events around the dominant kernel only
+    L.rnnt_profile_select(dom.encode())
     L.rnnt_profile_enable(1)
     stream = torch.cuda.current_stream()
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -131,27 +164,16 @@ def main() -> int:
     ms_step = ms_total / args.steps
     peak = torch.cuda.max_memory_allocated(dev) - base_mem
 
-    # per-kernel times from the library's events
-    buf = ctypes.create_string_buffer(4096)
-    L.rnnt_profile_names(buf, 4096)
-    kernels = {}
-    for name in [x for x in buf.value.decode().split(",") if x]:
-        n = ctypes.c_int32()
-        tot = ctypes.c_double()
-        _native.check(L.rnnt_profile_query(name.encode(), ctypes.byref(n), ctypes.byref(tot)))
-        kernels[name] = {"launches": n.value, "avg_us": round(1000 * tot.value / max(n.value, 1), 2),
-                         "us_per_step": round(1000 * tot.value / args.steps, 2)}
+    timed = kernel_table(args.steps)[dom]
     L.rnnt_profile_reset()
-    # the dominant contraction: joiner GEMMs with algorithmic work 2*M*J*V each
-    # (the backward's logits recompute is overhead, not work, and is excluded)
-    work = {"joiner_fwd": 2.0 * M * J * V, "joiner_dh": 2.0 * M * J * V, "joiner_dw": 2.0 * M * J * V}
-    dom = max((k for k in work if k in kernels), key=lambda k: kernels[k]["us_per_step"])
-    per_launch_flops = work[dom] / (kernels[dom]["launches"] / args.steps)
-    achieved = per_launch_flops / (kernels[dom]["avg_us"] * 1e-6) / 1e12
+    L.rnnt_profile_select(None)
+    per_launch_flops = work[dom] / (timed["launches"] / args.steps)
+    achieved = per_launch_flops / (timed["avg_us"] * 1e-6) / 1e12
     dt = "bf16" if bf else "f32"
     roofline = {"kernel": dom, "bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_TFLOPS[dt],
                 "unit": "TFLOP/s", "frac": round(achieved / PEAK_TFLOPS[dt], 4), "traffic": None,
-                "algorithmic_flops_per_launch": per_launch_flops, "avg_launch_us": kernels[dom]["avg_us"]}
+                "algorithmic_flops_per_launch": per_launch_flops, "avg_launch_us": timed["avg_us"],
+                "launches_timed": timed["launches"]}
 
     cpu = None if args.no_cpu_baseline else _cpu_baseline(b, S, args.cpu_budget)
     line = {
@@ -174,6 +196,7 @@ def main() -> int:
         "wall_s_timed": round(wall, 3),
         "roofline": roofline,
         "kernels": kernels,
+        "kernels_census_steps": census_steps,
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)

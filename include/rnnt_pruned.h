@@ -148,9 +148,9 @@ size_t rnnt_pruned_joiner_workspace_size(int32_t N, int32_t T, int32_t S, int32_
                                          int32_t V, int32_t dtype);
 
 /* Full joiner at u = ranges[n,t,s] only (Sec. 3.2): h = tanh(enc[n,t] + dec[n,u]),
- * logits = h W + bias, lse = log sum_v exp(logits). The [N, T, S, V] logits are
- * never stored: each (row, 64-column slice) keeps a partial (max, sum exp)
- * and the target and blank logits.
+ * logits = h W + bias, lse = log sum_v exp(logits). The log-softmax is reduced
+ * in the GEMM epilogue: each (row, 64-column slice) keeps a partial
+ * (max, sum exp) and the target and blank logits.
  *
  * enc [N, T, J], dec [N, U+1, J], W [J, V], bias [V] (nullable = 0): dtype
  *   RNNT_F32 (float) or RNNT_BF16 (bfloat16 bits); accumulation is fp32.
@@ -158,10 +158,15 @@ size_t rnnt_pruned_joiner_workspace_size(int32_t N, int32_t T, int32_t S, int32_
  *   absent slots).
  * Outputs, fp32 [N, T, S]: px = logits[y_{u+1}] - lse (u < U_n, else -inf),
  *   py = logits[blank] - lse, lse (0 for absent slots).
+ * logits [N, T, S, V] fp32 (nullable, caller-owned): when given, the logits
+ *   are stored as well (entries of absent slots and padding frames are left
+ *   untouched), so that rnnt_pruned_joiner_backward can stream them instead
+ *   of recomputing the projection. This is the [N, T, S, V] memory the
+ *   method's cost scales with (Sec. 3.2).
  */
 int rnnt_pruned_joiner(const rnnt_batch* batch, int32_t S, int32_t J, int32_t V, int32_t dtype,
                        const void* enc, const void* dec, const void* W, const void* bias,
-                       const int32_t* ranges, float* px, float* py, float* lse,
+                       const int32_t* ranges, float* px, float* py, float* lse, float* logits,
                        void* workspace, size_t workspace_bytes, void* stream);
 
 /* Workspace bytes for rnnt_pruned_loss. */
@@ -183,11 +188,13 @@ size_t rnnt_pruned_joiner_backward_workspace_size(int32_t N, int32_t T, int32_t 
                                                   int32_t J, int32_t V, int32_t dtype);
 
 /* Gradients of sum_n scale[n] * pruned_loss[n] through the log-softmax, the
- * projection, tanh and the sum enc + dec. The logits are recomputed in row
- * chunks; d(logits) is held for one chunk at a time and never for the whole
- * [N, T, S, V] at once unless it fits the chunk.
+ * projection, tanh and the sum enc + dec, in row chunks: d(logits) is held
+ * for one chunk at a time and never for the whole [N, T, S, V] at once
+ * unless it fits the chunk.
  *
  * lse, px_occ, py_occ [N, T, S]: from rnnt_pruned_joiner / rnnt_pruned_loss.
+ * logits [N, T, S, V] (nullable): the logits stored by rnnt_pruned_joiner
+ *   for the same inputs; when null they are recomputed (one more GEMM).
  * Outputs (fp32): enc_grad [N, T, J], dec_grad [N, U+1, J] (required);
  *   W_grad [J, V], bias_grad [V] (nullable);
  *   logits_grad [N, T, S, V] (nullable; debugging aid for small shapes).
@@ -196,7 +203,8 @@ size_t rnnt_pruned_joiner_backward_workspace_size(int32_t N, int32_t T, int32_t 
 int rnnt_pruned_joiner_backward(const rnnt_batch* batch, int32_t S, int32_t J, int32_t V,
                                 int32_t dtype, const void* enc, const void* dec,
                                 const void* W, const void* bias, const int32_t* ranges,
-                                const float* lse, const float* px_occ, const float* py_occ,
+                                const float* lse, const float* logits,
+                                const float* px_occ, const float* py_occ,
                                 const float* scale, float* enc_grad, float* dec_grad,
                                 float* W_grad, float* bias_grad, float* logits_grad,
                                 void* workspace, size_t workspace_bytes, void* stream);
@@ -210,6 +218,12 @@ int rnnt_pruned_joiner_backward(const rnnt_batch* batch, int32_t S, int32_t J, i
  * recorded on its stream, under a fixed kernel name ("joiner_fwd",
  * "joiner_dlogits", "joiner_dh", "joiner_dw", "lattice", "band", ...). */
 int rnnt_profile_enable(int on);
+
+/* Restrict recording to the kernels named in `names` (comma-separated, as in
+ * rnnt_profile_names); NULL or "" records every kernel again. Each recorded
+ * launch costs two event packets on its stream, so timing one kernel inside
+ * a throughput measurement should select just that kernel. */
+int rnnt_profile_select(const char* names);
 
 /* Forget all records (waits for the recorded events to complete). */
 int rnnt_profile_reset(void);

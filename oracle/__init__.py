@@ -25,6 +25,7 @@ from .rnnt import (  # noqa: F401
     adjust_pruning_bounds,
     prune_ranges,
     joiner_hidden,
+    pruned_joiner_logits,
     pruned_joiner_logprobs,
     pruned_loss,
     pruned_joiner_grad,

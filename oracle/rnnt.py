@@ -324,6 +324,23 @@ def _joiner_logits(enc, dec, W, bias, n, ts, us):
     return h, h @ np.asarray(W, np.float64) + np.asarray(bias, np.float64)
 
 
+def pruned_joiner_logits(enc, dec, W, bias, ranges, t_len, u_len):
+    """The (N, T, S, V) pruned logits of Sec. 3.2: tanh(enc[t] + dec[u]) W + b at u = ranges[n,t,s].
+
+    Absent slots (u > U_n) and frames t >= T_n are NaN.
+    """
+    N, T, S = ranges.shape
+    V = np.asarray(W).shape[1]
+    out = np.full((N, T, S, V), np.nan)
+    for n in range(N):
+        Tn, Un = int(t_len[n]), int(u_len[n])
+        u = np.asarray(ranges[n, :Tn], np.int64)
+        ts = np.repeat(np.arange(Tn)[:, None], S, axis=1)
+        _, lg = _joiner_logits(enc, dec, W, bias, n, ts, np.minimum(u, Un))
+        out[n, :Tn] = np.where((u <= Un)[..., None], lg, np.nan)
+    return out
+
+
 def pruned_joiner_logprobs(enc, dec, W, bias, ranges, symbols, t_len, u_len, blank=0,
                            t_chunk: int = 32):
     """Full joiner evaluated only at u = ranges[n,t,s] (Sec. 3.2, output (N,T,S,V)).

@@ -152,7 +152,7 @@ def rnnt_prune_ranges(batch: Batch, S: int, px_occ: torch.Tensor, py_occ: torch.
 
 def rnnt_pruned_joiner(batch: Batch, S: int, enc: torch.Tensor, dec: torch.Tensor, W: torch.Tensor,
                        bias: Optional[torch.Tensor], ranges: torch.Tensor, px=None, py=None, lse=None,
-                       workspace=None, stream=None) -> dict:
+                       logits=None, workspace=None, stream=None, keep_logits: bool = False) -> dict:
     N, T, U = batch.N, batch.T, batch.U
     J, V = int(W.shape[0]), int(W.shape[1])
     dt = _jdtype(W)
@@ -165,10 +165,14 @@ def rnnt_pruned_joiner(batch: Batch, S: int, enc: torch.Tensor, dec: torch.Tenso
     px = torch.empty(N, T, S, **f32) if px is None else px
     py = torch.empty(N, T, S, **f32) if py is None else py
     lse = torch.empty(N, T, S, **f32) if lse is None else lse
+    if keep_logits and logits is None:
+        logits = torch.empty(N, T, S, V, **f32)
+    if logits is not None:
+        _need(logits, "logits", torch.float32, (N, T, S, V))
     ws = _ws(pruned_joiner_workspace_size(N, T, S, J, V, dt), batch.device, workspace)
     check(lib().rnnt_pruned_joiner(batch.c, S, J, V, dt, _p(enc), _p(dec), _p(W), _p(bias), _p(ranges),
-                                   _p(px), _p(py), _p(lse), _p(ws), ws.numel(), _stream(stream)))
-    return {"px": px, "py": py, "lse": lse}
+                                   _p(px), _p(py), _p(lse), _p(logits), _p(ws), ws.numel(), _stream(stream)))
+    return {"px": px, "py": py, "lse": lse, "logits": logits}
 
 
 def rnnt_pruned_loss(batch: Batch, S: int, px: torch.Tensor, py: torch.Tensor, ranges: torch.Tensor,
@@ -191,7 +195,7 @@ def rnnt_pruned_loss(batch: Batch, S: int, px: torch.Tensor, py: torch.Tensor, r
 def rnnt_pruned_joiner_backward(batch: Batch, S: int, enc, dec, W, bias, ranges, lse, px_occ, py_occ,
                                 scale=None, enc_grad=None, dec_grad=None, W_grad=None, bias_grad=None,
                                 logits_grad=None, workspace=None, stream=None, want_param_grads=True,
-                                want_logits_grad=False) -> dict:
+                                want_logits_grad=False, logits=None) -> dict:
     N, T, U = batch.N, batch.T, batch.U
     J, V = int(W.shape[0]), int(W.shape[1])
     dt = _jdtype(W)
@@ -200,6 +204,8 @@ def rnnt_pruned_joiner_backward(batch: Batch, S: int, enc, dec, W, bias, ranges,
     for name, t in (("lse", lse), ("px_occ", px_occ), ("py_occ", py_occ)):
         _need(t, name, torch.float32, (N, T, S))
     _need(ranges, "ranges", torch.int32, (N, T, S))
+    if logits is not None:
+        _need(logits, "logits", torch.float32, (N, T, S, V))
     f32 = dict(dtype=torch.float32, device=batch.device)
     enc_grad = torch.empty(N, T, J, **f32) if enc_grad is None else enc_grad
     dec_grad = torch.empty(N, U + 1, J, **f32) if dec_grad is None else dec_grad
@@ -209,7 +215,7 @@ def rnnt_pruned_joiner_backward(batch: Batch, S: int, enc, dec, W, bias, ranges,
         logits_grad = torch.empty(N, T, S, V, **f32)
     ws = _ws(pruned_joiner_backward_workspace_size(N, T, U, S, J, V, dt), batch.device, workspace)
     check(lib().rnnt_pruned_joiner_backward(
-        batch.c, S, J, V, dt, _p(enc), _p(dec), _p(W), _p(bias), _p(ranges), _p(lse), _p(px_occ),
+        batch.c, S, J, V, dt, _p(enc), _p(dec), _p(W), _p(bias), _p(ranges), _p(lse), _p(logits), _p(px_occ),
         _p(py_occ), _p(scale), _p(enc_grad), _p(dec_grad), _p(W_grad), _p(bias_grad), _p(logits_grad),
         _p(ws), ws.numel(), _stream(stream)))
     return {"enc_grad": enc_grad, "dec_grad": dec_grad, "W_grad": W_grad, "bias_grad": bias_grad,
@@ -223,12 +229,17 @@ class PrunedRnntLoss:
     repeated steps on same-shaped batches allocate nothing new. ``step``
     enqueues the whole path (simple loss and its gradients, pruning bounds,
     pruned joiner, pruned recursion, joiner backward) on the current stream.
+    With ``keep_logits`` the pruned logits [N, T, S, V] are kept between the
+    joiner's forward and backward (the method's own memory footprint);
+    without it the backward recomputes them and holds one row chunk at a time.
     """
 
-    def __init__(self, S: int, simple_scale: float = 0.5, pruned_scale: float = 1.0):
+    def __init__(self, S: int, simple_scale: float = 0.5, pruned_scale: float = 1.0,
+                 keep_logits: bool = True):
         self.S = int(S)
         self.simple_scale = float(simple_scale)
         self.pruned_scale = float(pruned_scale)
+        self.keep_logits = bool(keep_logits)
         self._cache = {}
 
     def _buf(self, key, shape, dtype, device):
@@ -263,9 +274,10 @@ class PrunedRnntLoss:
             workspace=ws, stream=stream)
         ranges = rnnt_prune_ranges(batch, S, out["px_occ"], out["py_occ"],
                                    ranges=self._buf("rng", (N, T, S), torch.int32, dev), stream=stream)
+        logits = self._buf("logits", (N, T, S, V), f32, dev) if self.keep_logits else None
         jo = rnnt_pruned_joiner(batch, S, enc, dec, W, bias, ranges, px=self._buf("ppx", (N, T, S), f32, dev),
                                 py=self._buf("ppy", (N, T, S), f32, dev), lse=self._buf("lse", (N, T, S), f32, dev),
-                                workspace=ws, stream=stream)
+                                logits=logits, workspace=ws, stream=stream)
         pl = rnnt_pruned_loss(batch, S, jo["px"], jo["py"], ranges, loss=self._buf("pl", (N,), f32, dev),
                               px_occ=self._buf("pgx", (N, T, S), f32, dev),
                               py_occ=self._buf("pgy", (N, T, S), f32, dev), workspace=ws, stream=stream)
@@ -273,7 +285,7 @@ class PrunedRnntLoss:
             batch, S, enc, dec, W, bias, ranges, jo["lse"], pl["px_occ"], pl["py_occ"], scale=psc,
             enc_grad=self._buf("denc", (N, T, J), f32, dev), dec_grad=self._buf("ddec", (N, U + 1, J), f32, dev),
             W_grad=self._buf("dW", (J, V), f32, dev), bias_grad=self._buf("db", (V,), f32, dev),
-            workspace=ws, stream=stream)
+            workspace=ws, stream=stream, logits=logits)
         return {"simple_loss": out["loss"], "pruned_loss": pl["loss"], "ranges": ranges,
                 "am_grad": out["am_grad"], "lm_grad": out["lm_grad"], "enc_grad": jb["enc_grad"],
                 "dec_grad": jb["dec_grad"], "W_grad": jb["W_grad"], "bias_grad": jb["bias_grad"],

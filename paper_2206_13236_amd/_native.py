@@ -46,17 +46,19 @@ SIGNATURES = {
     "rnnt_pruned_joiner_workspace_size": (c_size_t, [c_int32] * 6),
     "rnnt_pruned_joiner": (c_int32, [POINTER(RnntBatch), c_int32, c_int32, c_int32, c_int32,
                                      c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
-                                     c_void_p, c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]),
+                                     c_void_p, c_void_p, c_void_p, c_void_p,
+                                     c_void_p, c_size_t, c_void_p]),
     "rnnt_pruned_loss_workspace_size": (c_size_t, [c_int32] * 3),
     "rnnt_pruned_loss": (c_int32, [POINTER(RnntBatch), c_int32, c_void_p, c_void_p, c_void_p,
                                    c_void_p, c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]),
     "rnnt_pruned_joiner_backward_workspace_size": (c_size_t, [c_int32] * 7),
     "rnnt_pruned_joiner_backward": (c_int32, [POINTER(RnntBatch), c_int32, c_int32, c_int32, c_int32,
                                               c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
-                                              c_void_p, c_void_p, c_void_p, c_void_p,
+                                              c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
                                               c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
                                               c_void_p, c_size_t, c_void_p]),
     "rnnt_profile_enable": (c_int32, [c_int32]),
+    "rnnt_profile_select": (c_int32, [c_char_p]),
     "rnnt_profile_reset": (c_int32, []),
     "rnnt_profile_query": (c_int32, [c_char_p, POINTER(c_int32), POINTER(ctypes.c_double)]),
     "rnnt_profile_names": (c_int32, [c_char_p, c_size_t]),

@@ -192,7 +192,7 @@ int check_joiner_sizes(const rnnt_batch* b, int S, int J, int V, int dtype) {
 
 extern "C" {
 
-int rnnt_abi_version(void) { return 1; }
+int rnnt_abi_version(void) { return 2; }
 
 const char* rnnt_last_error(void) { return g_err.c_str(); }
 
@@ -271,7 +271,7 @@ size_t rnnt_pruned_joiner_workspace_size(int32_t N, int32_t T, int32_t S, int32_
 
 int rnnt_pruned_joiner(const rnnt_batch* batch, int32_t S, int32_t J, int32_t V, int32_t dtype, const void* enc,
                        const void* dec, const void* W, const void* bias, const int32_t* ranges, float* px, float* py,
-                       float* lse, void* workspace, size_t workspace_bytes, void* stream) {
+                       float* lse, float* logits, void* workspace, size_t workspace_bytes, void* stream) {
   int rc = check_batch(batch, true);
   if (rc) return rc;
   rc = check_joiner_sizes(batch, S, J, V, dtype);
@@ -301,6 +301,7 @@ int rnnt_pruned_joiner(const rnnt_batch* batch, int32_t S, int32_t J, int32_t V,
   a.px = px;
   a.py = py;
   a.lse = lse;
+  a.logits = logits;
   hipStream_t s = static_cast<hipStream_t>(stream);
   hipError_t e = launch_joiner_prep(a, s);
   if (e == hipSuccess) e = launch_joiner_fwd(a, s);
@@ -357,7 +358,8 @@ size_t rnnt_pruned_joiner_backward_workspace_size(int32_t N, int32_t T, int32_t 
 
 int rnnt_pruned_joiner_backward(const rnnt_batch* batch, int32_t S, int32_t J, int32_t V, int32_t dtype,
                                 const void* enc, const void* dec, const void* W, const void* bias,
-                                const int32_t* ranges, const float* lse, const float* px_occ, const float* py_occ,
+                                const int32_t* ranges, const float* lse, const float* logits,
+                                const float* px_occ, const float* py_occ,
                                 const float* scale, float* enc_grad, float* dec_grad, float* W_grad, float* bias_grad,
                                 float* logits_grad, void* workspace, size_t workspace_bytes, void* stream) {
   int rc = check_batch(batch, true);
@@ -387,6 +389,7 @@ int rnnt_pruned_joiner_backward(const rnnt_batch* batch, int32_t S, int32_t J, i
   a.frame_off = w.frame_off;
   a.rowinfo = w.rowinfo;
   a.lse_in = lse;
+  a.logits_in = logits;
   a.gxo = px_occ;
   a.gyo = py_occ;
   a.scale = scale;

@@ -12,12 +12,15 @@
 // 16x16x32, fp32 accumulation); the tanh is formed while staging the A tile.
 // The epilogue reduces every (row, 64-column slice) to (max, sum exp) and
 // captures the target and blank logits; a combine kernel turns them into
-// lse, px = logit[y_{u+1}] - lse and py = logit[blank] - lse. The
-// [rows, V] logits never reach memory.
+// lse, px = logit[y_{u+1}] - lse and py = logit[blank] - lse. The logits
+// reach memory only when the caller asks for them ([N, T, S, V], the size
+// the method's memory scales with).
 //
 // Backward (per chunk of rows, so that d(logits) is held for one chunk only):
-//   1. recompute logits, dl = sc * ((gx+gy) softmax - gx [v=y] - gy [v=blank])
-//      (log-softmax backward), write the chunk and per-tile column sums (db);
+//   1. dl = sc * ((gx+gy) softmax - gx [v=y] - gy [v=blank]) (log-softmax
+//      backward) from the stored logits by a streaming kernel, or, without
+//      them, by recomputing the logits GEMM; write the chunk and column
+//      sums (db);
 //   2. dh = dl W^T, dpre = dh (1 - h^2)  (tanh backward);
 //   3. dW += h^T dl with split-K partial sums;
 // then d enc[n,t] = sum_s dpre(row(t,s)), d dec[n,u] = sum over the (t,s)
@@ -28,8 +31,14 @@
 
 namespace {
 
-using CfgF = GemmCfg<128, 128, 32, false>;
-using CfgB = GemmCfg<128, 128, 64, true>;
+// 8 waves in a 4 x 2 grid (32 x 64 wave tiles): about 100 registers per
+// lane, so two workgroups (four waves per SIMD) share a CU.
+constexpr int kGemmThreads = 512;
+using CfgF = GemmCfg<128, 128, 32, false, 4, 2>;
+using CfgB = GemmCfg<128, 128, 64, true, 4, 2>;
+static_assert(CfgF::NT == kGemmThreads && CfgB::NT == kGemmThreads, "joiner GEMM block size");
+static_assert(CfgF::WN == 64 && CfgB::WN == 64, "the forward's partial log-sum-exp slices are 64 columns");
+static_assert(CfgF::BM == CfgB::BM && CfgF::WGM == CfgB::WGM, "db partial rows per row tile");
 
 template <bool BF>
 struct In;
@@ -328,7 +337,7 @@ __global__ __launch_bounds__(256) void joiner_prep_kernel(JoinerArgs a) {
 // Forward GEMM + partial log-sum-exp
 // ---------------------------------------------------------------------------
 template <bool BF>
-__global__ __launch_bounds__(256) void joiner_fwd_kernel(JoinerArgs a) {
+__global__ __launch_bounds__(kGemmThreads) void joiner_fwd_kernel(JoinerArgs a) {
   using TIn = typename In<BF>::T;
   using Cfg = typename In<BF>::Cfg;
   __shared__ __align__(16) typename Cfg::T smem[Cfg::SMEM_BYTES / sizeof(typename Cfg::T)];
@@ -338,7 +347,7 @@ __global__ __launch_bounds__(256) void joiner_fwd_kernel(JoinerArgs a) {
   if (m0 >= M) return;
   const int v0 = blockIdx.y * Cfg::BN;
   const int V = a.V, J = a.J;
-  for (int r = threadIdx.x; r < Cfg::BM; r += 256)
+  for (int r = threadIdx.x; r < Cfg::BM; r += Cfg::NT)
     ri[r] = (m0 + r < M) ? a.rowinfo[m0 + r] : make_int4(0, 0, -1, -1);
   __syncthreads();
   const TIn* enc = reinterpret_cast<const TIn*>(a.enc);
@@ -350,8 +359,8 @@ __global__ __launch_bounds__(256) void joiner_fwd_kernel(JoinerArgs a) {
   floatx4 acc[Cfg::FM][Cfg::FN];
   gemm_mainloop<Cfg>(la, lb, 0, J, smem, acc);
 
-  const int lane = threadIdx.x & 63, wn = (threadIdx.x >> 6) & 1;
-  const int slice = blockIdx.y * 2 + wn;
+  const int lane = threadIdx.x & 63, wn = (threadIdx.x >> 6) % Cfg::WGN;
+  const int slice = blockIdx.y * Cfg::WGN + wn;
   float bj[Cfg::FN];
 #pragma unroll
   for (int j = 0; j < Cfg::FN; ++j) {
@@ -391,6 +400,7 @@ __global__ __launch_bounds__(256) void joiner_fwd_kernel(JoinerArgs a) {
           if (col < V) {
             if (col == info.z) a.tgt[m] = lg[j];
             if (col == a.b.blank) a.blk[m] = lg[j];
+            if (a.logits) a.logits[(size_t)info.w * V + col] = lg[j];
           }
         }
       }
@@ -431,7 +441,7 @@ __global__ __launch_bounds__(256) void joiner_combine_kernel(JoinerArgs a) {
 // Backward 1: recompute logits, d(logits) for a chunk of rows, db partials.
 // ---------------------------------------------------------------------------
 template <bool BF>
-__global__ __launch_bounds__(256) void joiner_dlogits_kernel(JoinerArgs a, int cm0, int cm1) {
+__global__ __launch_bounds__(kGemmThreads) void joiner_dlogits_kernel(JoinerArgs a, int cm0, int cm1) {
   using TIn = typename In<BF>::T;
   using Cfg = typename In<BF>::Cfg;
   __shared__ __align__(16) typename Cfg::T smem[Cfg::SMEM_BYTES / sizeof(typename Cfg::T)];
@@ -443,7 +453,7 @@ __global__ __launch_bounds__(256) void joiner_dlogits_kernel(JoinerArgs a, int c
   if (m0 >= mend) return;
   const int v0 = blockIdx.y * Cfg::BN;
   const int V = a.V, J = a.J, TS = a.b.T * a.S;
-  for (int r = threadIdx.x; r < Cfg::BM; r += 256) {
+  for (int r = threadIdx.x; r < Cfg::BM; r += Cfg::NT) {
     int4 info = (m0 + r < mend) ? a.rowinfo[m0 + r] : make_int4(0, 0, -1, -1);
     float4 x = make_float4(0.f, 0.f, 0.f, 0.f);
     if (info.w >= 0) {
@@ -463,7 +473,7 @@ __global__ __launch_bounds__(256) void joiner_dlogits_kernel(JoinerArgs a, int c
   floatx4 acc[Cfg::FM][Cfg::FN];
   gemm_mainloop<Cfg>(la, lb, 0, J, smem, acc);
 
-  const int lane = threadIdx.x & 63, wm = (threadIdx.x >> 6) >> 1;
+  const int lane = threadIdx.x & 63, wm = (threadIdx.x >> 6) / Cfg::WGN;
   typename Cfg::T* dl = reinterpret_cast<typename Cfg::T*>(a.dl);
   float bj[Cfg::FN], colsum[Cfg::FN];
 #pragma unroll
@@ -500,7 +510,7 @@ __global__ __launch_bounds__(256) void joiner_dlogits_kernel(JoinerArgs a, int c
         colsum[j] += d;
       }
     }
-  // db partial: sum over this wave's 64 rows, one row of db_part per (m-tile, wave row).
+  // db partial: sum over this wave's WM rows, one row of db_part per (m-tile, wave row).
   const int mt = m0 / Cfg::BM;
 #pragma unroll
   for (int j = 0; j < Cfg::FN; ++j) {
@@ -508,7 +518,118 @@ __global__ __launch_bounds__(256) void joiner_dlogits_kernel(JoinerArgs a, int c
     s += __shfl_xor(s, 16, 64);
     s += __shfl_xor(s, 32, 64);
     const int col = v0 + tile_col<Cfg>(j);
-    if (lane < 16 && col < V) a.db_part[((size_t)mt * 2 + wm) * V + col] = s;
+    if (lane < 16 && col < V) a.db_part[((size_t)mt * Cfg::WGM + wm) * V + col] = s;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Backward 1, stored logits: the same d(logits) streamed from the logits the
+// forward kept. One block per kDlRows rows of the chunk, threads over groups
+// of 4 columns (padding columns up to ldl get zeros), several rows per thread
+// with their loads issued together; the block's column sums are one db_part
+// row.
+// ---------------------------------------------------------------------------
+constexpr int kDlRows = 64;
+constexpr int kDlThreads = 512;
+
+template <bool BF>
+__global__ __launch_bounds__(kDlThreads) void joiner_dl_kernel(JoinerArgs a, int cm0, int cm1) {
+  __shared__ int4 ri[kDlRows];
+  __shared__ float4 rx[kDlRows];  // lse, gx, gy, scale
+  __shared__ float4 red[kDlThreads];
+  const int M = a.frame_off[a.b.N] * a.S;
+  const int mend = min(cm1, M);
+  const int m0 = cm0 + blockIdx.x * kDlRows;
+  if (m0 >= mend) return;
+  const int V = a.V, TS = a.b.T * a.S, ldl = a.ldl, blank = a.b.blank;
+  const int nrows = min(kDlRows, mend - m0);
+  if (threadIdx.x < kDlRows) {
+    const int r = threadIdx.x;
+    int4 info = (r < nrows) ? a.rowinfo[m0 + r] : make_int4(0, 0, -1, -1);
+    float4 x = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (info.w >= 0) {
+      const int n = info.w / TS;
+      x = make_float4(a.lse_in[info.w], a.gxo[info.w], a.gyo[info.w], a.scale ? a.scale[n] : 1.f);
+    }
+    ri[r] = info;
+    rx[r] = x;
+  }
+  __syncthreads();
+  const float* __restrict__ lg = a.logits_in;
+  typename In<BF>::Cfg::T* __restrict__ dl = reinterpret_cast<typename In<BF>::Cfg::T*>(a.dl);
+  const int ng = ldl / 4;
+  const int tpr = ng <= 64 ? 64 : (ng <= 128 ? 128 : (ng <= 256 ? 256 : kDlThreads));
+  const int nrg = kDlThreads / tpr, rg = threadIdx.x / tpr, ct = threadIdx.x - rg * tpr;
+  const bool vec = (V & 3) == 0;
+  for (int g0 = 0; g0 < ng; g0 += tpr) {
+    const int c = 4 * (g0 + ct);
+    const bool gok = g0 + ct < ng;
+    float cs[4] = {0.f, 0.f, 0.f, 0.f};
+    if (gok) {
+      for (int r0 = rg; r0 < nrows; r0 += 4 * nrg) {
+        float l[4][4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const int r = r0 + k * nrg;
+          const int4 info = ri[min(r, kDlRows - 1)];
+          const bool ok = r < nrows && info.w >= 0 && c < V;
+          const float* src = lg + (ok ? (size_t)info.w * V + c : 0);
+          if (ok && vec) {
+            const float4 q = *reinterpret_cast<const float4*>(src);
+            l[k][0] = q.x; l[k][1] = q.y; l[k][2] = q.z; l[k][3] = q.w;
+          } else {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) l[k][q] = (ok && c + q < V) ? src[q] : 0.f;
+          }
+        }
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const int r = r0 + k * nrg;
+          if (r >= nrows) break;
+          const int4 info = ri[r];
+          const float4 x = rx[r];
+          const float g = x.y + x.z;
+          float d[4];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const int col = c + q;
+            d[q] = 0.f;
+            if (info.w >= 0 && col < V) {
+              float gd = g * __expf(l[k][q] - x.x);
+              if (col == info.z) gd -= x.y;
+              if (col == blank) gd -= x.z;
+              d[q] = x.w * gd;
+              if (a.logits_grad) a.logits_grad[(size_t)info.w * V + col] = d[q];
+            }
+            cs[q] += d[q];
+          }
+          const size_t o = (size_t)(m0 + r - cm0) * ldl + c;
+          if constexpr (BF) {
+            *reinterpret_cast<uint2*>(dl + o) =
+                make_uint2((uint32_t)f2bf(d[0]) | ((uint32_t)f2bf(d[1]) << 16),
+                           (uint32_t)f2bf(d[2]) | ((uint32_t)f2bf(d[3]) << 16));
+          } else {
+            *reinterpret_cast<float4*>(dl + o) = make_float4(d[0], d[1], d[2], d[3]);
+          }
+        }
+      }
+    }
+    if (nrg > 1) {  // ng <= tpr here, so every thread runs this loop exactly once
+      red[threadIdx.x] = make_float4(cs[0], cs[1], cs[2], cs[3]);
+      __syncthreads();
+      if (rg == 0) {
+        for (int k = 1; k < nrg; ++k) {
+          const float4 o = red[k * tpr + ct];
+          cs[0] += o.x; cs[1] += o.y; cs[2] += o.z; cs[3] += o.w;
+        }
+      }
+    }
+    if (rg == 0 && gok) {
+      float* db = a.db_part + (size_t)(m0 / kDlRows) * V;
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        if (c + q < V) db[c + q] = cs[q];
+    }
   }
 }
 
@@ -516,7 +637,7 @@ __global__ __launch_bounds__(256) void joiner_dlogits_kernel(JoinerArgs a, int c
 // Backward 2: dh = dl W^T, dpre = dh (1 - h^2)
 // ---------------------------------------------------------------------------
 template <bool BF>
-__global__ __launch_bounds__(256) void joiner_dh_kernel(JoinerArgs a, int cm0, int cm1) {
+__global__ __launch_bounds__(kGemmThreads) void joiner_dh_kernel(JoinerArgs a, int cm0, int cm1) {
   using TIn = typename In<BF>::T;
   using Cfg = typename In<BF>::Cfg;
   __shared__ __align__(16) typename Cfg::T smem[Cfg::SMEM_BYTES / sizeof(typename Cfg::T)];
@@ -527,7 +648,7 @@ __global__ __launch_bounds__(256) void joiner_dh_kernel(JoinerArgs a, int cm0, i
   if (m0 >= mend) return;
   const int j0 = blockIdx.y * Cfg::BN;
   const int V = a.V, J = a.J;
-  for (int r = threadIdx.x; r < Cfg::BM; r += 256)
+  for (int r = threadIdx.x; r < Cfg::BM; r += Cfg::NT)
     ri[r] = (m0 + r < mend) ? a.rowinfo[m0 + r] : make_int4(0, 0, -1, -1);
   __syncthreads();
   const TIn* W = reinterpret_cast<const TIn*>(a.W);
@@ -566,7 +687,7 @@ __global__ __launch_bounds__(256) void joiner_dh_kernel(JoinerArgs a, int cm0, i
 // Backward 3: dW partial += h^T dl over one split of the chunk's rows
 // ---------------------------------------------------------------------------
 template <bool BF>
-__global__ __launch_bounds__(256) void joiner_dw_kernel(JoinerArgs a, int cm0, int cm1, int first) {
+__global__ __launch_bounds__(kGemmThreads) void joiner_dw_kernel(JoinerArgs a, int cm0, int cm1, int first) {
   using TIn = typename In<BF>::T;
   using Cfg = typename In<BF>::Cfg;
   __shared__ __align__(16) typename Cfg::T smem[Cfg::SMEM_BYTES / sizeof(typename Cfg::T)];
@@ -582,7 +703,7 @@ __global__ __launch_bounds__(256) void joiner_dw_kernel(JoinerArgs a, int cm0, i
   if (kb >= ke) {
     // no rows for this split: the first chunk still defines the partial
     if (first) {
-      for (int e = threadIdx.x; e < Cfg::BM * Cfg::BN; e += 256) {
+      for (int e = threadIdx.x; e < Cfg::BM * Cfg::BN; e += Cfg::NT) {
         const int j = j0 + e / Cfg::BN, v = v0 + e % Cfg::BN;
         if (j < J && v < V) part[(size_t)j * V + v] = 0.f;
       }
@@ -625,14 +746,15 @@ __global__ __launch_bounds__(256) void joiner_wsum_kernel(JoinerArgs a) {
   a.W_grad[i] = s;
 }
 
-// db = sum of the per-(row tile, wave) column partials written by the
-// d(logits) kernel: 16 interleaved parts per column, then the parts in order.
+// db = sum of the column partials written by the d(logits) kernel (one per
+// 64 rows streamed, one per wave row of a GEMM tile recomputed): 16
+// interleaved parts per column, then the parts in order.
 __global__ __launch_bounds__(1024) void joiner_dbsum_kernel(JoinerArgs a) {
   __shared__ float red[16][64];
   const int c = threadIdx.x & 63, part = threadIdx.x >> 6;
   const int v = blockIdx.x * 64 + c;
   const int M = a.frame_off[a.b.N] * a.S;
-  const int rows = 2 * ((M + 127) / 128);
+  const int rows = a.logits_in ? (M + kDlRows - 1) / kDlRows : CfgF::WGM * ((M + CfgF::BM - 1) / CfgF::BM);
   float s = 0.f;
   if (v < a.V) {
 #pragma unroll 4
@@ -736,7 +858,9 @@ int joiner_bwd_splits(int J, int V) {
 
 int joiner_db_rows(int N, int T, int S) {
   const long long mmax = (long long)N * T * S;
-  return (int)(((mmax + 127) / 128) * 2);
+  const long long streamed = (mmax + kDlRows - 1) / kDlRows;
+  const long long tiled = ((mmax + CfgF::BM - 1) / CfgF::BM) * CfgF::WGM;
+  return (int)(streamed > tiled ? streamed : tiled);
 }
 
 hipError_t launch_joiner_prep(const JoinerArgs& a, hipStream_t s) {
@@ -752,8 +876,8 @@ hipError_t launch_joiner_fwd(const JoinerArgs& a, hipStream_t s) {
   dim3 grid((mmax + 127) / 128, (a.V + 127) / 128);
   {
     RNNT_PROF(s, "joiner_fwd");
-    if (a.bf16) hipLaunchKernelGGL(joiner_fwd_kernel<true>, grid, dim3(256), 0, s, a);
-  else hipLaunchKernelGGL(joiner_fwd_kernel<false>, grid, dim3(256), 0, s, a);
+    if (a.bf16) hipLaunchKernelGGL(joiner_fwd_kernel<true>, grid, dim3(kGemmThreads), 0, s, a);
+  else hipLaunchKernelGGL(joiner_fwd_kernel<false>, grid, dim3(kGemmThreads), 0, s, a);
   }
   const size_t total = (size_t)a.b.N * a.b.T * a.S;
   {
@@ -775,31 +899,38 @@ hipError_t launch_joiner_bwd(const JoinerArgs& a, hipStream_t s) {
     const int cm1 = (cm0 + a.chunk_rows < mmax) ? cm0 + a.chunk_rows : mmax;
     const int mt = (cm1 - cm0 + 127) / 128;
     dim3 g1(mt, (V + 127) / 128), g2(mt, (J + 127) / 128), g3((J + 127) / 128, (V + 127) / 128, a.splits);
+    const dim3 gdl((cm1 - cm0 + kDlRows - 1) / kDlRows);
     if (a.bf16) {
-      {
+      if (a.logits_in) {
+        RNNT_PROF(s, "joiner_dl");
+        hipLaunchKernelGGL(joiner_dl_kernel<true>, gdl, dim3(kDlThreads), 0, s, a, cm0, cm1);
+      } else {
         RNNT_PROF(s, "joiner_dlogits");
-        hipLaunchKernelGGL(joiner_dlogits_kernel<true>, g1, dim3(256), 0, s, a, cm0, cm1);
+        hipLaunchKernelGGL(joiner_dlogits_kernel<true>, g1, dim3(kGemmThreads), 0, s, a, cm0, cm1);
       }
       {
         RNNT_PROF(s, "joiner_dh");
-        hipLaunchKernelGGL(joiner_dh_kernel<true>, g2, dim3(256), 0, s, a, cm0, cm1);
+        hipLaunchKernelGGL(joiner_dh_kernel<true>, g2, dim3(kGemmThreads), 0, s, a, cm0, cm1);
       }
       {
         RNNT_PROF(s, "joiner_dw");
-        hipLaunchKernelGGL(joiner_dw_kernel<true>, g3, dim3(256), 0, s, a, cm0, cm1, cm0 == 0);
+        hipLaunchKernelGGL(joiner_dw_kernel<true>, g3, dim3(kGemmThreads), 0, s, a, cm0, cm1, cm0 == 0);
       }
     } else {
-      {
+      if (a.logits_in) {
+        RNNT_PROF(s, "joiner_dl");
+        hipLaunchKernelGGL(joiner_dl_kernel<false>, gdl, dim3(kDlThreads), 0, s, a, cm0, cm1);
+      } else {
         RNNT_PROF(s, "joiner_dlogits");
-        hipLaunchKernelGGL(joiner_dlogits_kernel<false>, g1, dim3(256), 0, s, a, cm0, cm1);
+        hipLaunchKernelGGL(joiner_dlogits_kernel<false>, g1, dim3(kGemmThreads), 0, s, a, cm0, cm1);
       }
       {
         RNNT_PROF(s, "joiner_dh");
-        hipLaunchKernelGGL(joiner_dh_kernel<false>, g2, dim3(256), 0, s, a, cm0, cm1);
+        hipLaunchKernelGGL(joiner_dh_kernel<false>, g2, dim3(kGemmThreads), 0, s, a, cm0, cm1);
       }
       {
         RNNT_PROF(s, "joiner_dw");
-        hipLaunchKernelGGL(joiner_dw_kernel<false>, g3, dim3(256), 0, s, a, cm0, cm1, cm0 == 0);
+        hipLaunchKernelGGL(joiner_dw_kernel<false>, g3, dim3(kGemmThreads), 0, s, a, cm0, cm1, cm0 == 0);
       }
     }
   }

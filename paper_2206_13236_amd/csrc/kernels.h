@@ -67,8 +67,10 @@ struct JoinerArgs {
   float* px;           // [N, T, S]
   float* py;
   float* lse;
+  float* logits;       // [N, T, S, V] or null: the forward also stores the logits
   // backward
   const float* lse_in;
+  const float* logits_in;  // [N, T, S, V] or null: stored logits (else recomputed)
   const float* gxo;    // band occupations [N, T, S]
   const float* gyo;
   const float* scale;  // [N] or null

@@ -22,6 +22,14 @@ std::mutex g_mu;
 bool g_on = false;
 std::vector<Rec> g_recs;
 std::vector<hipEvent_t> g_pool;
+std::vector<std::string> g_sel;  // names to record; empty: all
+
+bool selected(const char* name) {
+  if (g_sel.empty()) return true;
+  for (auto& s : g_sel)
+    if (s == name) return true;
+  return false;
+}
 
 hipEvent_t get_event() {
   if (!g_pool.empty()) {
@@ -39,6 +47,7 @@ hipEvent_t get_event() {
 void prof_begin(hipStream_t s, const char* name) {
   if (!g_on) return;
   std::lock_guard<std::mutex> lk(g_mu);
+  if (!selected(name)) return;
   hipEvent_t a = get_event(), b = get_event();
   if (!a || !b) return;
   hipEventRecord(a, s);
@@ -62,6 +71,23 @@ extern "C" {
 int rnnt_profile_enable(int on) {
   std::lock_guard<std::mutex> lk(g_mu);
   g_on = on != 0;
+  return RNNT_OK;
+}
+
+int rnnt_profile_select(const char* names) {
+  std::lock_guard<std::mutex> lk(g_mu);
+  g_sel.clear();
+  if (!names) return RNNT_OK;
+  std::string cur;
+  for (const char* c = names;; ++c) {
+    if (*c == ',' || *c == 0) {
+      if (!cur.empty()) g_sel.push_back(cur);
+      cur.clear();
+      if (*c == 0) break;
+    } else {
+      cur += *c;
+    }
+  }
   return RNNT_OK;
 }
 

@@ -41,7 +41,7 @@ def test_library_exports_every_declared_symbol(L):
     missing = [n for n in _declared() if not hasattr(L, n)]
     assert not missing, f"not exported: {missing}"
     assert set(_declared()) == set(_native.SIGNATURES), "binding signatures out of sync with the header"
-    assert L.rnnt_abi_version() == 1
+    assert L.rnnt_abi_version() == 2
 
 
 def test_workspace_queries(L):
@@ -108,12 +108,12 @@ def test_validation_statuses(L):
     assert L.rnnt_prune_ranges(ctypes.byref(big), 4, fake, fake, fake, None) == N.RNNT_EUNSUPPORTED
     # joiner: J not a multiple of 8, bad dtype
     assert L.rnnt_pruned_joiner(pb, 4, 12, 16, N.RNNT_F32, fake, fake, fake, None, fake, fake, fake, fake,
-                                fake, 1 << 30, None) == N.RNNT_EUNSUPPORTED
+                                None, fake, 1 << 30, None) == N.RNNT_EUNSUPPORTED
     assert L.rnnt_pruned_joiner(pb, 4, 16, 16, 7, fake, fake, fake, None, fake, fake, fake, fake,
-                                fake, 1 << 30, None) == N.RNNT_EINVAL
+                                None, fake, 1 << 30, None) == N.RNNT_EINVAL
     # backward: enc_grad required
-    assert L.rnnt_pruned_joiner_backward(pb, 4, 16, 16, N.RNNT_F32, fake, fake, fake, None, fake, fake, fake,
-                                         fake, None, None, fake, None, None, None, fake, 1 << 30,
+    assert L.rnnt_pruned_joiner_backward(pb, 4, 16, 16, N.RNNT_F32, fake, fake, fake, None, fake, fake, None,
+                                         fake, fake, None, None, fake, None, None, None, fake, 1 << 30,
                                          None) == N.RNNT_EINVAL
     # a success clears the message; the last failure leaves one
     assert _err(L) != ""

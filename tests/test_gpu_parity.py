@@ -111,13 +111,17 @@ def test_pruned_joiner(name):
     say(f"[joiner] {name} bf16={bf}")
     batch = make_dev_batch(b)
     out = P.rnnt_pruned_joiner(batch, o["S"], dev_joiner(b.enc, bf), dev_joiner(b.dec, bf), dev_joiner(b.W, bf),
-                               dev_joiner(b.bias, bf), dev_i32(o["ranges"]))
+                               dev_joiner(b.bias, bf), dev_i32(o["ranges"]), keep_logits=True)
     torch.cuda.synchronize()
     st = o["st"]
     tol = 2e-2 if bf else 5e-5
     assert_close("px", host(out["px"]), st["px"], atol=tol)
     assert_close("py", host(out["py"]), st["py"], atol=tol)
     assert_close("lse", host(out["lse"]), st["lse"], atol=tol, rtol=tol)
+    # the stored logits at every present slot (absent slots are left untouched)
+    ref = O.pruned_joiner_logits(b.enc, b.dec, b.W, b.bias, o["ranges"], b.t_len, b.u_len)
+    present = ~np.isnan(ref[..., 0])
+    assert_close("logits", host(out["logits"])[present], ref[present], atol=tol)
 
 
 @pytest.mark.parametrize("name", list(CASES))
@@ -138,12 +142,13 @@ def test_pruned_loss(name):
     assert_close("py_occ", host(out["py_occ"]), gy_ref, atol=1e-4)
 
 
+@pytest.mark.parametrize("stored", [False, True], ids=["recompute", "stored_logits"])
 @pytest.mark.parametrize("name", list(CASES))
-def test_pruned_joiner_backward(name):
+def test_pruned_joiner_backward(name, stored):
     o = _oracle(name)
     b = o["b"]
     bf = b.wl.joiner_dtype == "bf16"
-    say(f"[joiner-bwd] {name} bf16={bf}")
+    say(f"[joiner-bwd] {name} bf16={bf} stored_logits={stored}")
     st = o["st"]
     lse32 = st["lse"].astype(np.float32)
     gx32, gy32 = st["gx"].astype(np.float32), st["gy"].astype(np.float32)
@@ -151,10 +156,16 @@ def test_pruned_joiner_backward(name):
                                gx32.astype(np.float64), gy32.astype(np.float64), scale=o["sc"],
                                want_logits_grad=(name == "tiny"))
     batch = make_dev_batch(b)
+    args = (dev_joiner(b.enc, bf), dev_joiner(b.dec, bf), dev_joiner(b.W, bf), dev_joiner(b.bias, bf))
+    rng = dev_i32(o["ranges"])
+    logits, lse = None, dev_f32(lse32)
+    if stored:
+        # the backward streams the logits the forward kept, with the forward's own lse
+        fw = P.rnnt_pruned_joiner(batch, o["S"], *args, rng, keep_logits=True)
+        logits, lse = fw["logits"], fw["lse"]
     out = P.rnnt_pruned_joiner_backward(
-        batch, o["S"], dev_joiner(b.enc, bf), dev_joiner(b.dec, bf), dev_joiner(b.W, bf), dev_joiner(b.bias, bf),
-        dev_i32(o["ranges"]), dev_f32(lse32), dev_f32(gx32), dev_f32(gy32), scale=dev_f32(o["sc"]),
-        want_logits_grad=(name == "tiny"))
+        batch, o["S"], *args, rng, lse, dev_f32(gx32), dev_f32(gy32), scale=dev_f32(o["sc"]),
+        want_logits_grad=(name == "tiny"), logits=logits)
     torch.cuda.synchronize()
     for k in ("enc_grad", "dec_grad"):
         assert_close(k, host(out[k]), ref[k], atol=grad_atol(ref[k], bf))

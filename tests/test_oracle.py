@@ -367,6 +367,43 @@ def test_pruned_joiner_logprobs_match_full_joiner_and_torch():
     assert abs(lse[0, 3, 1] - torch.logsumexp(lg, dim=-1).item()) < 1e-12
 
 
+def test_pruned_logits_special_cases():
+    # W = I, bias = 0: the logits are the hidden activations tanh(enc + dec[p_t + s]) themselves
+    rng = np.random.default_rng(11)
+    N, T, U, J, S = 2, 5, 3, 6, 3
+    enc = rng.standard_normal((N, T, J))
+    dec = rng.standard_normal((N, U + 1, J))
+    tl, ul = np.array([5, 3]), np.array([3, 2])
+    ranges = np.zeros((N, T, S), np.int32)
+    ranges[0] = (np.array([0, 0, 1, 1, 1])[:, None] + np.arange(S))
+    ranges[1] = (np.array([0, 0, 0, 0, 0])[:, None] + np.arange(S))
+    lg = O.pruned_joiner_logits(enc, dec, np.eye(J), np.zeros(J), ranges, tl, ul)
+    for n in range(N):
+        for t in range(T):
+            for s in range(S):
+                u = ranges[n, t, s]
+                if t >= tl[n] or u > ul[n]:
+                    assert np.all(np.isnan(lg[n, t, s]))
+                else:
+                    np.testing.assert_array_equal(lg[n, t, s], np.tanh(enc[n, t] + dec[n, u]))
+    # dec = -enc broadcast: h = 0 and every present logit row is the bias
+    dec2 = np.zeros((N, U + 1, J))
+    enc2 = np.zeros((N, T, J))
+    W = rng.standard_normal((J, 4))
+    bias = rng.standard_normal(4)
+    lg2 = O.pruned_joiner_logits(enc2, dec2, W, bias, ranges, tl, ul)
+    ok = ~np.isnan(lg2[..., 0])
+    np.testing.assert_array_equal(lg2[ok], np.broadcast_to(bias, lg2[ok].shape))
+    # the log-softmax of the logits gives the joiner's px/py
+    b = make_batch("tiny", seed=2)
+    r = np.tile(np.arange(b.wl.S, dtype=np.int32), (b.N, b.T, 1))
+    px, py, lse = O.pruned_joiner_logprobs(b.enc, b.dec, b.W, b.bias, r, b.symbols, b.t_len, b.u_len, 0)
+    lg3 = O.pruned_joiner_logits(b.enc, b.dec, b.W, b.bias, r, b.t_len, b.u_len)
+    from scipy.special import logsumexp
+    np.testing.assert_allclose(logsumexp(lg3, axis=-1), lse, rtol=1e-13)
+    np.testing.assert_allclose(lg3[..., 0] - lse, py, rtol=1e-13)
+
+
 def _total_pruned_loss(enc, dec, W, bias, ranges, sym, tl, ul, sc):
     px, py, _ = O.pruned_joiner_logprobs(enc, dec, W, bias, ranges, sym, tl, ul, 0)
     loss, _, _ = O.pruned_loss(px, py, ranges, tl, ul)
