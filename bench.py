@@ -73,6 +73,9 @@ def main() -> int:
     ap.add_argument("--workload", default="bpe", choices=sorted(WORKLOAD_TEXT))
     ap.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of oracle work for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-mib", type=int, default=0,
+                    help="before the census, run one device-to-device copy of this many MiB (a plain copy "
+                         "kernel of known size that scales rocprofv3's FETCH_SIZE / WRITE_SIZE)")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -128,6 +131,14 @@ def main() -> int:
             out[name] = {"launches": n.value, "avg_us": round(1000 * tot.value / max(n.value, 1), 2),
                          "us_per_step": round(1000 * tot.value / nsteps, 2)}
         return out
+
+    if args.copy_mib > 0:
+        src = torch.ones(args.copy_mib << 18, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     # census: every kernel bracketed by events, outside the timed region (the
     # event packets themselves cost ~5 us per launch)

@@ -182,8 +182,11 @@ int check_joiner_sizes(const rnnt_batch* b, int S, int J, int V, int dtype) {
   if (J < 8 || J % 8 != 0) return fail(RNNT_EUNSUPPORTED, "J = %d must be a positive multiple of 8", J);
   if (dtype != RNNT_F32 && dtype != RNNT_BF16) return fail(RNNT_EINVAL, "dtype must be RNNT_F32 or RNNT_BF16");
   if ((long long)b->N * b->T * S > kI32) return fail(RNNT_EUNSUPPORTED, "N*T*S exceeds 2^31-1");
-  if ((long long)b->N * b->T * J > kI32 || (long long)b->N * (b->U + 1) * J > kI32)
-    return fail(RNNT_EUNSUPPORTED, "N*T*J or N*(U+1)*J exceeds 2^31-1");
+  // operands are read through 32-bit buffer offsets: each array stays below 2^31 bytes
+  const long long esz = dtype == RNNT_BF16 ? 2 : 4;
+  if ((long long)b->N * b->T * J * esz > kI32 || (long long)b->N * (b->U + 1) * J * esz > kI32 ||
+      (long long)J * V * esz > kI32)
+    return fail(RNNT_EUNSUPPORTED, "enc, dec or W exceeds 2^31-1 bytes");
   if ((size_t)b->T * sizeof(int) > 64 * 1024) return fail(RNNT_EUNSUPPORTED, "T = %d too large", b->T);
   return RNNT_OK;
 }

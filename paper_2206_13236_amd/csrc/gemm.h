@@ -224,6 +224,23 @@ DEV void gemm_mainloop(const LA& la, const LB& lb, int k_begin, int k_end,
   }
 }
 
+// XCD-aware tile order. Workgroup w of a launch (x fastest, then y, then z)
+// is dispatched to XCD w % 8, and every XCD has its own L2. Tile ids are
+// renumbered so that each XCD receives one contiguous run of them: tiles
+// that are neighbours in tile-id order (and share an operand panel) then run
+// on the same XCD at about the same time and share its L2.
+// Only the first n_active workgroups get a tile (-1 for the rest), so that a
+// grid sized for the padded maximum spreads its real tiles over all XCDs.
+constexpr int kNumXcd = 8;
+DEV int xcd_tile_id(int n_active) {
+  const int w = blockIdx.x + gridDim.x * (blockIdx.y + gridDim.y * blockIdx.z);
+  const int n = min(n_active, (int)(gridDim.x * gridDim.y * gridDim.z));
+  if (w >= n) return -1;
+  const int per = n / kNumXcd, rem = n % kNumXcd;
+  const int x = w % kNumXcd, loc = w / kNumXcd;
+  return (x < rem ? x * (per + 1) : rem * (per + 1) + (x - rem) * per) + loc;
+}
+
 // Row/column of output element (i, j, r) of this lane within the tile.
 template <class Cfg>
 DEV int tile_row(int i, int r) {

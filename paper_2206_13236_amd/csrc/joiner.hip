@@ -34,7 +34,7 @@ namespace {
 // 8 waves in a 4 x 2 grid (32 x 64 wave tiles): about 100 registers per
 // lane, so two workgroups (four waves per SIMD) share a CU.
 constexpr int kGemmThreads = 512;
-using CfgF = GemmCfg<128, 128, 32, false, 4, 2>;
+using CfgF = GemmCfg<128, 128, 64, false, 4, 2>;
 using CfgB = GemmCfg<128, 128, 64, true, 4, 2>;
 static_assert(CfgF::NT == kGemmThreads && CfgB::NT == kGemmThreads, "joiner GEMM block size");
 static_assert(CfgF::WN == 64 && CfgB::WN == 64, "the forward's partial log-sum-exp slices are 64 columns");
@@ -56,57 +56,33 @@ struct In<true> {
 DEV float ld_in(const float* p, size_t i) { return p[i]; }
 DEV float ld_in(const uint16_t* p, size_t i) { return bf2f(p[i]); }
 
-// n consecutive elements of a row as fp32 (16-byte vector loads when aligned).
-template <int NV>
-DEV void load_vec(const float* p, float (&v)[NV]) {
-  if constexpr (NV == 4) {
-    float4 q = *reinterpret_cast<const float4*>(p);
-    v[0] = q.x; v[1] = q.y; v[2] = q.z; v[3] = q.w;
-  } else if constexpr (NV == 8) {
-    float4 q0 = *reinterpret_cast<const float4*>(p);
-    float4 q1 = *reinterpret_cast<const float4*>(p + 4);
-    v[0] = q0.x; v[1] = q0.y; v[2] = q0.z; v[3] = q0.w;
-    v[4] = q1.x; v[5] = q1.y; v[6] = q1.z; v[7] = q1.w;
-  } else {
-#pragma unroll
-    for (int i = 0; i < NV; ++i) v[i] = p[i];
-  }
-}
-template <int NV>
-DEV void load_vec(const uint16_t* p, float (&v)[NV]) {
-  if constexpr (NV == 8) {
-    uint4 q = *reinterpret_cast<const uint4*>(p);
-    uint32_t w[4] = {q.x, q.y, q.z, q.w};
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      v[2 * i] = __uint_as_float(w[i] << 16);
-      v[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
-    }
-  } else if constexpr (NV == 2) {
-    uint32_t w = *reinterpret_cast<const uint32_t*>(p);
-    v[0] = __uint_as_float(w << 16);
-    v[1] = __uint_as_float(w & 0xffff0000u);
-  } else if constexpr (NV == 4) {
-    uint2 q = *reinterpret_cast<const uint2*>(p);
-    v[0] = __uint_as_float(q.x << 16);
-    v[1] = __uint_as_float(q.x & 0xffff0000u);
-    v[2] = __uint_as_float(q.y << 16);
-    v[3] = __uint_as_float(q.y & 0xffff0000u);
-  } else {
-#pragma unroll
-    for (int i = 0; i < NV; ++i) v[i] = bf2f(p[i]);
-  }
+// ---------------------------------------------------------------------------
+// Operand loads through buffer resources. A buffer load whose byte offset
+// lies past the resource's size returns zeros, so masked-out lanes (rows
+// past the end, absent slots, k beyond K) load from kOob instead of taking a
+// divergent branch; the loads of a K-step then issue back to back. Every
+// operand array is below 2^31 bytes (checked by the entry points).
+// ---------------------------------------------------------------------------
+using Rsrc = __amdgpu_buffer_rsrc_t;
+constexpr uint32_t kOob = 0x80000000u;
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+DEV Rsrc make_rsrc(const void* p, size_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)(uint32_t)bytes, 0x00020000);
 }
 
-// Masked row segment [c, c+NV) of a row of length len: vector load when the
-// whole segment is inside and aligned, element loads otherwise.
-template <int NV, typename TIn>
-DEV void load_seg(const TIn* row, int c, int len, bool aligned, float (&v)[NV]) {
-  if (aligned && c + NV <= len) {
-    load_vec<NV>(row + c, v);
+template <int W>
+DEV void buf_words(Rsrc r, uint32_t off, uint32_t* w) {
+  if constexpr (W == 4) {
+    const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0);
+    w[0] = v.x; w[1] = v.y; w[2] = v.z; w[3] = v.w;
+  } else if constexpr (W == 2) {
+    const u32x2 v = __builtin_amdgcn_raw_buffer_load_b64(r, (int)off, 0, 0);
+    w[0] = v.x; w[1] = v.y;
   } else {
 #pragma unroll
-    for (int i = 0; i < NV; ++i) v[i] = (c + i < len) ? ld_in(row, (size_t)(c + i)) : 0.f;
+    for (int i = 0; i < W; ++i) w[i] = __builtin_amdgcn_raw_buffer_load_b32(r, (int)(off + 4 * i), 0, 0);
   }
 }
 
@@ -120,39 +96,38 @@ struct RawVec {
   uint32_t w[W];
 };
 
+// How a row segment may be loaded (uniform over a launch):
+//   kSegVector: rows are 16-byte aligned and every segment is entirely inside
+//               or entirely outside its row: one vector load;
+//   kSegWords:  32-bit words, each inside or outside (fp32, or bf16 rows of
+//               even length);
+//   kSegElems:  bf16 element by element (odd row length).
+enum SegMode { kSegVector = 0, kSegWords = 1, kSegElems = 2 };
+
+template <typename TIn>
+DEV int seg_mode(int row_len, int seg) {
+  if (row_len % seg == 0) return kSegVector;
+  return (sizeof(TIn) == 4 || row_len % 2 == 0) ? kSegWords : kSegElems;
+}
+
+// Loads the N elements at byte offset `off`, of which the first `nvalid` are
+// inside the row (nvalid <= 0: none; zeros beyond).
 template <typename TIn, int N>
-DEV void raw_load(const TIn* p, bool full, bool valid, int count, RawVec<TIn, N>& r) {
-  // full: the N elements at p are in range and aligned for one vector load;
-  // otherwise the first `count` elements are loaded one by one (0 beyond).
-  if (!valid) {
+DEV void raw_load(Rsrc r, uint32_t off, int nvalid, int mode, RawVec<TIn, N>& out) {
+  constexpr int W = RawVec<TIn, N>::W;
+  if (mode == kSegVector) {
+    buf_words<W>(r, nvalid > 0 ? off : kOob, out.w);
+  } else if (sizeof(TIn) == 4 || mode == kSegWords) {
+    constexpr int EPW = 4 / (int)sizeof(TIn);  // elements per word
 #pragma unroll
-    for (int i = 0; i < RawVec<TIn, N>::W; ++i) r.w[i] = 0u;
-    return;
-  }
-  if (full) {
-    if constexpr (RawVec<TIn, N>::W == 4) {
-      uint4 q = *reinterpret_cast<const uint4*>(p);
-      r.w[0] = q.x; r.w[1] = q.y; r.w[2] = q.z; r.w[3] = q.w;
-    } else if constexpr (RawVec<TIn, N>::W == 2) {
-      uint2 q = *reinterpret_cast<const uint2*>(p);
-      r.w[0] = q.x; r.w[1] = q.y;
-    } else if constexpr (RawVec<TIn, N>::W == 1) {
-      r.w[0] = *reinterpret_cast<const uint32_t*>(p);
-    } else {
-#pragma unroll
-      for (int i = 0; i < RawVec<TIn, N>::W; ++i) r.w[i] = reinterpret_cast<const uint32_t*>(p)[i];
-    }
-    return;
-  }
-  if constexpr (sizeof(TIn) == 4) {
-#pragma unroll
-    for (int i = 0; i < N; ++i) r.w[i] = (i < count) ? __float_as_uint(p[i]) : 0u;
+    for (int i = 0; i < W; ++i)
+      out.w[i] = __builtin_amdgcn_raw_buffer_load_b32(r, (int)(EPW * i < nvalid ? off + 4 * i : kOob), 0, 0);
   } else {
 #pragma unroll
-    for (int i = 0; i < RawVec<TIn, N>::W; ++i) {
-      const uint32_t lo = (2 * i < count) ? (uint32_t)p[2 * i] : 0u;
-      const uint32_t hi = (2 * i + 1 < count) ? (uint32_t)p[2 * i + 1] : 0u;
-      r.w[i] = lo | (hi << 16);
+    for (int i = 0; i < W; ++i) {
+      const uint32_t lo = __builtin_amdgcn_raw_buffer_load_b16(r, (int)(2 * i < nvalid ? off + 4 * i : kOob), 0, 0);
+      const uint32_t hi = __builtin_amdgcn_raw_buffer_load_b16(r, (int)(2 * i + 1 < nvalid ? off + 4 * i + 2 : kOob), 0, 0);
+      out.w[i] = lo | (hi << 16);
     }
   }
 }
@@ -189,19 +164,27 @@ DEV void finish_h(const RawH<TIn, N>& r, float (&v)[N]) {
   for (int i = 0; i < N; ++i) v[i] = fast_tanh(e[i] + d[i]);
 }
 
+// enc / dec resources of a launch (row offsets from rowinfo are element offsets).
+template <typename TIn>
+struct EncDec {
+  Rsrc enc, dec;
+  DEV EncDec(const JoinerArgs& a)
+      : enc(make_rsrc(a.enc, (size_t)a.b.N * a.b.T * a.J * sizeof(TIn))),
+        dec(make_rsrc(a.dec, (size_t)a.b.N * (a.b.U + 1) * a.J * sizeof(TIn))) {}
+};
+
 // A(m, j) = tanh(enc[row] + dec[row]) for the tile's rows (rowinfo in LDS).
 template <class Cfg, typename TIn>
 struct HSrcKC {
   using Raw = RawH<TIn, Cfg::KV>;
-  const TIn* enc;
-  const TIn* dec;
+  EncDec<TIn> ed;
   const int4* ri;
   int J;
   DEV void kc_load(int row, int k, Raw& r) const {
     const int4 q = ri[row];
-    const bool ok = q.w >= 0 && k < J;
-    raw_load(enc + (ok ? (size_t)q.x + k : 0), true, ok, Cfg::KV, r.e);
-    raw_load(dec + (ok ? (size_t)q.y + k : 0), true, ok, Cfg::KV, r.d);
+    const int n = (q.w >= 0 && k < J) ? Cfg::KV : 0;
+    raw_load(ed.enc, (uint32_t)(q.x + k) * sizeof(TIn), n, kSegVector, r.e);
+    raw_load(ed.dec, (uint32_t)(q.y + k) * sizeof(TIn), n, kSegVector, r.d);
   }
   DEV void kc_finish(const Raw& r, float (&v)[Cfg::KV]) const { finish_h(r, v); }
 };
@@ -211,13 +194,14 @@ template <class Cfg, typename TIn>
 struct WSrcMNC {
   static constexpr int NV = 16 / Cfg::KV;
   using Raw = RawVec<TIn, NV>;
-  const TIn* W;
-  int v0, V, J;
-  bool aligned;
+  Rsrc W;
+  int v0, V, J, mode;
+  DEV WSrcMNC(const JoinerArgs& a, int v0_)
+      : W(make_rsrc(a.W, (size_t)a.J * a.V * sizeof(TIn))), v0(v0_), V(a.V), J(a.J), mode(seg_mode<TIn>(a.V, NV)) {}
   DEV void mnc_load(int k, int col, Raw& r) const {
     const int c = v0 + col;
-    const bool ok = k < J && c < V;
-    raw_load(W + (ok ? (size_t)k * V + c : 0), aligned && c + NV <= V, ok, V - c, r);
+    const int n = (k < J) ? V - c : 0;
+    raw_load(W, (uint32_t)(k * V + c) * sizeof(TIn), n, mode, r);
   }
   DEV void mnc_finish(const Raw& r, float (&v)[NV]) const { raw_to_float(r, v); }
 };
@@ -225,13 +209,14 @@ struct WSrcMNC {
 // A(m, v) = dl[m][v] from the chunk buffer (rows padded to ldl with zeros).
 template <class Cfg>
 struct DlSrcKC {
-  using Raw = RawVec<typename Cfg::T, Cfg::KV>;
-  const typename Cfg::T* dl;  // row (m - cm0)
+  using T = typename Cfg::T;
+  using Raw = RawVec<T, Cfg::KV>;
+  Rsrc dl;  // row (m - cm0)
   int m0, cm0, mend, ldl;
   DEV void kc_load(int row, int k, Raw& r) const {
     const int m = m0 + row;
-    const bool ok = m < mend && k < ldl;
-    raw_load(dl + (ok ? (size_t)(m - cm0) * ldl + k : 0), true, ok, Cfg::KV, r);
+    const int n = (m < mend && k < ldl) ? Cfg::KV : 0;
+    raw_load(dl, (uint32_t)((m - cm0) * ldl + k) * sizeof(T), n, kSegVector, r);
   }
   DEV void kc_finish(const Raw& r, float (&v)[Cfg::KV]) const { raw_to_float(r, v); }
 };
@@ -240,33 +225,34 @@ struct DlSrcKC {
 template <class Cfg, typename TIn>
 struct WtSrcKC {
   using Raw = RawVec<TIn, Cfg::KV>;
-  const TIn* W;
-  int j0, J, V;
-  bool aligned;
+  Rsrc W;
+  int j0, J, V, mode;
+  DEV WtSrcKC(const JoinerArgs& a, int j0_)
+      : W(make_rsrc(a.W, (size_t)a.J * a.V * sizeof(TIn))), j0(j0_), J(a.J), V(a.V),
+        mode(seg_mode<TIn>(a.V, Cfg::KV)) {}
   DEV void kc_load(int row, int k, Raw& r) const {
     const int j = j0 + row;
-    const bool ok = j < J && k < V;
-    raw_load(W + (ok ? (size_t)j * V + k : 0), aligned && k + Cfg::KV <= V, ok, V - k, r);
+    const int n = (j < J) ? V - k : 0;
+    raw_load(W, (uint32_t)(j * V + k) * sizeof(TIn), n, mode, r);
   }
   DEV void kc_finish(const Raw& r, float (&v)[Cfg::KV]) const { raw_to_float(r, v); }
 };
 
-// A(j, m) = h(m, j): global is [m][j], j-contiguous; rowinfo read per row.
+// A(j, m) = h(m, j): global is [m][j], j-contiguous; rowinfo read per row
+// (from a clamped index, so the read is unconditional).
 template <class Cfg, typename TIn>
 struct HSrcMNC {
   static constexpr int NV = 16 / Cfg::KV;
   using Raw = RawH<TIn, NV>;
-  const TIn* enc;
-  const TIn* dec;
+  EncDec<TIn> ed;
   const int4* rowinfo;
   int j0, J, mend;
   DEV void mnc_load(int k, int col, Raw& r) const {
     const int j = j0 + col;
-    int4 q = make_int4(0, 0, -1, -1);
-    if (k < mend && j < J) q = rowinfo[k];
-    const bool ok = q.w >= 0;
-    raw_load(enc + (ok ? (size_t)q.x + j : 0), true, ok, NV, r.e);
-    raw_load(dec + (ok ? (size_t)q.y + j : 0), true, ok, NV, r.d);
+    const int4 q = rowinfo[min(k, mend - 1)];
+    const int n = (k < mend && j < J && q.w >= 0) ? NV : 0;
+    raw_load(ed.enc, (uint32_t)(q.x + j) * sizeof(TIn), n, kSegVector, r.e);
+    raw_load(ed.dec, (uint32_t)(q.y + j) * sizeof(TIn), n, kSegVector, r.d);
   }
   DEV void mnc_finish(const Raw& r, float (&v)[NV]) const { finish_h(r, v); }
 };
@@ -274,14 +260,15 @@ struct HSrcMNC {
 // B(m, v) = dl[m][v]: global row-contiguous along v.
 template <class Cfg>
 struct DlSrcMNC {
+  using T = typename Cfg::T;
   static constexpr int NV = 16 / Cfg::KV;
-  using Raw = RawVec<typename Cfg::T, NV>;
-  const typename Cfg::T* dl;
+  using Raw = RawVec<T, NV>;
+  Rsrc dl;
   int cm0, mend, v0, ldl;
   DEV void mnc_load(int k, int col, Raw& r) const {
     const int c = v0 + col;
-    const bool ok = k < mend && c < ldl;
-    raw_load(dl + (ok ? (size_t)(k - cm0) * ldl + c : 0), true, ok, NV, r);
+    const int n = (k < mend && c < ldl) ? NV : 0;
+    raw_load(dl, (uint32_t)((k - cm0) * ldl + c) * sizeof(T), n, kSegVector, r);
   }
   DEV void mnc_finish(const Raw& r, float (&v)[NV]) const { raw_to_float(r, v); }
 };
@@ -343,24 +330,27 @@ __global__ __launch_bounds__(kGemmThreads) void joiner_fwd_kernel(JoinerArgs a) 
   __shared__ __align__(16) typename Cfg::T smem[Cfg::SMEM_BYTES / sizeof(typename Cfg::T)];
   __shared__ int4 ri[Cfg::BM];
   const int M = a.frame_off[a.b.N] * a.S;
-  const int m0 = blockIdx.x * Cfg::BM;
-  if (m0 >= M) return;
-  const int v0 = blockIdx.y * Cfg::BN;
+  // the column tiles of one row tile are consecutive tile ids (one XCD, shared A panel)
+  const int tile = xcd_tile_id((M + Cfg::BM - 1) / Cfg::BM * gridDim.y);
+  if (tile < 0) return;
+  const int mt = tile / gridDim.y, nt = tile - mt * gridDim.y;
+  const int m0 = mt * Cfg::BM;
+  const int v0 = nt * Cfg::BN;
   const int V = a.V, J = a.J;
   for (int r = threadIdx.x; r < Cfg::BM; r += Cfg::NT)
     ri[r] = (m0 + r < M) ? a.rowinfo[m0 + r] : make_int4(0, 0, -1, -1);
   __syncthreads();
   const TIn* enc = reinterpret_cast<const TIn*>(a.enc);
   const TIn* dec = reinterpret_cast<const TIn*>(a.dec);
-  HSrcKC<Cfg, TIn> sa{enc, dec, ri, J};
-  WSrcMNC<Cfg, TIn> sb{reinterpret_cast<const TIn*>(a.W), v0, V, J, (V % WSrcMNC<Cfg, TIn>::NV) == 0};
+  HSrcKC<Cfg, TIn> sa{EncDec<TIn>(a), ri, J};
+  WSrcMNC<Cfg, TIn> sb(a, v0);
   KCLoader<Cfg, Cfg::BM, HSrcKC<Cfg, TIn>> la(sa);
   MNCLoader<Cfg, Cfg::BN, WSrcMNC<Cfg, TIn>> lb(sb);
   floatx4 acc[Cfg::FM][Cfg::FN];
   gemm_mainloop<Cfg>(la, lb, 0, J, smem, acc);
 
   const int lane = threadIdx.x & 63, wn = (threadIdx.x >> 6) % Cfg::WGN;
-  const int slice = blockIdx.y * Cfg::WGN + wn;
+  const int slice = nt * Cfg::WGN + wn;
   float bj[Cfg::FN];
 #pragma unroll
   for (int j = 0; j < Cfg::FN; ++j) {
@@ -449,9 +439,11 @@ __global__ __launch_bounds__(kGemmThreads) void joiner_dlogits_kernel(JoinerArgs
   __shared__ float4 rx[Cfg::BM];  // lse, gx, gy, scale
   const int M = a.frame_off[a.b.N] * a.S;
   const int mend = min(cm1, M);
-  const int m0 = cm0 + blockIdx.x * Cfg::BM;
-  if (m0 >= mend) return;
-  const int v0 = blockIdx.y * Cfg::BN;
+  const int tile = xcd_tile_id(mend > cm0 ? (mend - cm0 + Cfg::BM - 1) / Cfg::BM * gridDim.y : 0);
+  if (tile < 0) return;
+  const int mtl = tile / gridDim.y, nt = tile - mtl * gridDim.y;
+  const int m0 = cm0 + mtl * Cfg::BM;
+  const int v0 = nt * Cfg::BN;
   const int V = a.V, J = a.J, TS = a.b.T * a.S;
   for (int r = threadIdx.x; r < Cfg::BM; r += Cfg::NT) {
     int4 info = (m0 + r < mend) ? a.rowinfo[m0 + r] : make_int4(0, 0, -1, -1);
@@ -466,8 +458,8 @@ __global__ __launch_bounds__(kGemmThreads) void joiner_dlogits_kernel(JoinerArgs
   __syncthreads();
   const TIn* enc = reinterpret_cast<const TIn*>(a.enc);
   const TIn* dec = reinterpret_cast<const TIn*>(a.dec);
-  HSrcKC<Cfg, TIn> sa{enc, dec, ri, J};
-  WSrcMNC<Cfg, TIn> sb{reinterpret_cast<const TIn*>(a.W), v0, V, J, (V % WSrcMNC<Cfg, TIn>::NV) == 0};
+  HSrcKC<Cfg, TIn> sa{EncDec<TIn>(a), ri, J};
+  WSrcMNC<Cfg, TIn> sb(a, v0);
   KCLoader<Cfg, Cfg::BM, HSrcKC<Cfg, TIn>> la(sa);
   MNCLoader<Cfg, Cfg::BN, WSrcMNC<Cfg, TIn>> lb(sb);
   floatx4 acc[Cfg::FM][Cfg::FN];
@@ -644,16 +636,18 @@ __global__ __launch_bounds__(kGemmThreads) void joiner_dh_kernel(JoinerArgs a, i
   __shared__ int4 ri[Cfg::BM];
   const int M = a.frame_off[a.b.N] * a.S;
   const int mend = min(cm1, M);
-  const int m0 = cm0 + blockIdx.x * Cfg::BM;
-  if (m0 >= mend) return;
-  const int j0 = blockIdx.y * Cfg::BN;
+  const int tile = xcd_tile_id(mend > cm0 ? (mend - cm0 + Cfg::BM - 1) / Cfg::BM * gridDim.y : 0);
+  if (tile < 0) return;
+  const int mtl = tile / gridDim.y, nt = tile - mtl * gridDim.y;
+  const int m0 = cm0 + mtl * Cfg::BM;
+  const int j0 = nt * Cfg::BN;
   const int V = a.V, J = a.J;
   for (int r = threadIdx.x; r < Cfg::BM; r += Cfg::NT)
     ri[r] = (m0 + r < mend) ? a.rowinfo[m0 + r] : make_int4(0, 0, -1, -1);
   __syncthreads();
   const TIn* W = reinterpret_cast<const TIn*>(a.W);
-  DlSrcKC<Cfg> sa{reinterpret_cast<const typename Cfg::T*>(a.dl), m0, cm0, mend, a.ldl};
-  WtSrcKC<Cfg, TIn> sb{W, j0, J, V, (V % Cfg::KV) == 0};
+  DlSrcKC<Cfg> sa{make_rsrc(a.dl, (size_t)a.chunk_rows * a.ldl * sizeof(typename Cfg::T)), m0, cm0, mend, a.ldl};
+  WtSrcKC<Cfg, TIn> sb(a, j0);
   KCLoader<Cfg, Cfg::BM, DlSrcKC<Cfg>> la(sa);
   KCLoader<Cfg, Cfg::BN, WtSrcKC<Cfg, TIn>> lb(sb);
   floatx4 acc[Cfg::FM][Cfg::FN];
@@ -693,7 +687,12 @@ __global__ __launch_bounds__(kGemmThreads) void joiner_dw_kernel(JoinerArgs a, i
   __shared__ __align__(16) typename Cfg::T smem[Cfg::SMEM_BYTES / sizeof(typename Cfg::T)];
   const int M = a.frame_off[a.b.N] * a.S;
   const int mend = min(cm1, M);
-  const int j0 = blockIdx.x * Cfg::BM, v0 = blockIdx.y * Cfg::BN, z = blockIdx.z;
+  // the (j, v) tiles of one split are consecutive tile ids: one XCD reads that split's rows
+  const int tile = xcd_tile_id(gridDim.x * gridDim.y * gridDim.z);
+  const int per_split = gridDim.x * gridDim.y;
+  const int z = tile / per_split, jv = tile - z * per_split;
+  const int jt = jv / gridDim.y, vt = jv - jt * gridDim.y;
+  const int j0 = jt * Cfg::BM, v0 = vt * Cfg::BN;
   const int rows = cm1 - cm0;
   const int per = ((rows + a.splits - 1) / a.splits + Cfg::BK - 1) / Cfg::BK * Cfg::BK;
   const int kb = cm0 + z * per;
@@ -712,8 +711,8 @@ __global__ __launch_bounds__(kGemmThreads) void joiner_dw_kernel(JoinerArgs a, i
   }
   const TIn* enc = reinterpret_cast<const TIn*>(a.enc);
   const TIn* dec = reinterpret_cast<const TIn*>(a.dec);
-  HSrcMNC<Cfg, TIn> sa{enc, dec, a.rowinfo, j0, J, ke};
-  DlSrcMNC<Cfg> sb{reinterpret_cast<const typename Cfg::T*>(a.dl), cm0, ke, v0, a.ldl};
+  HSrcMNC<Cfg, TIn> sa{EncDec<TIn>(a), a.rowinfo, j0, J, ke};
+  DlSrcMNC<Cfg> sb{make_rsrc(a.dl, (size_t)a.chunk_rows * a.ldl * sizeof(typename Cfg::T)), cm0, ke, v0, a.ldl};
   MNCLoader<Cfg, Cfg::BM, HSrcMNC<Cfg, TIn>> la(sa);
   MNCLoader<Cfg, Cfg::BN, DlSrcMNC<Cfg>> lb(sb);
   floatx4 acc[Cfg::FM][Cfg::FN];
