@@ -92,10 +92,14 @@ struct SimpleWs {
   double* ry;
   double* cpx;
   double* cpy;
+  float* npart;
+  int nsplit;
+  float* lpart;
+  int lsplit;
   size_t bytes;
 };
 
-SimpleWs simple_layout(void* base, int N, int T, int U) {
+SimpleWs simple_layout(void* base, int N, int T, int U, int V) {
   Carve c(base);
   SimpleWs w;
   const size_t NT = (size_t)N * T, NU = (size_t)N * (U + 1), L = NT * (U + 1);
@@ -112,6 +116,10 @@ SimpleWs simple_layout(void* base, int N, int T, int U) {
   w.ry = c.take<double>(NT);
   w.cpx = c.take<double>((size_t)N * lattice_colblocks(T) * (U + 1));
   w.cpy = c.take<double>((size_t)N * lattice_colblocks(T) * (U + 1));
+  w.nsplit = normalizer_splits(N, T, U, V);
+  w.npart = c.take<float>((size_t)w.nsplit * L);
+  w.lsplit = dlm_splits(N, T, U, V);
+  w.lpart = c.take<float>((size_t)w.lsplit * NU * V);
   w.bytes = c.off;
   return w;
 }
@@ -201,7 +209,7 @@ const char* rnnt_last_error(void) { return g_err.c_str(); }
 
 size_t rnnt_simple_loss_workspace_size(int32_t N, int32_t T, int32_t U, int32_t V) {
   if (N < 1 || T < 1 || U < 0 || V < 1) return 0;
-  return simple_layout(nullptr, N, T, U).bytes;
+  return simple_layout(nullptr, N, T, U, V).bytes;
 }
 
 int rnnt_simple_loss(const rnnt_batch* batch, int32_t V, const float* am, const float* lm, const float* scale,
@@ -214,10 +222,10 @@ int rnnt_simple_loss(const rnnt_batch* batch, int32_t V, const float* am, const 
   if (!am || !lm) return fail(RNNT_EINVAL, "am and lm are required");
   if (!loss || !px_occ || !py_occ) return fail(RNNT_EINVAL, "loss, px_occ and py_occ are required");
   if ((px == nullptr) != (py == nullptr)) return fail(RNNT_EINVAL, "px and py must be given together");
-  const SimpleWs need = simple_layout(nullptr, batch->N, batch->T, batch->U);
+  const SimpleWs need = simple_layout(nullptr, batch->N, batch->T, batch->U, V);
   rc = check_ws(workspace, workspace_bytes, need.bytes);
   if (rc) return rc;
-  const SimpleWs w = simple_layout(workspace, batch->N, batch->T, batch->U);
+  const SimpleWs w = simple_layout(workspace, batch->N, batch->T, batch->U, V);
   hipStream_t s = static_cast<hipStream_t>(stream);
   SimpleArgs a{};
   a.b = to_dev(batch);
@@ -228,6 +236,10 @@ int rnnt_simple_loss(const rnnt_batch* batch, int32_t V, const float* am, const 
   a.m_a = w.m_a;
   a.m_l = w.m_l;
   a.Z = w.Z;
+  a.npart = w.npart;
+  a.nsplit = w.nsplit;
+  a.lpart = w.lpart;
+  a.lsplit = w.lsplit;
   a.px = px ? px : w.px;
   a.py = py ? py : w.py;
   a.alpha = w.alpha;

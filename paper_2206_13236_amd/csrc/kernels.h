@@ -15,6 +15,10 @@ struct SimpleArgs {
   float* m_a;          // ws [N*T]
   float* m_l;          // ws [N*(U+1)]
   float* Z;            // ws [N, T, U+1]
+  float* npart;        // ws [nsplit, N, T, U+1]: normaliser partial sums per K range
+  int nsplit;
+  float* lpart;        // ws [lsplit, N, U+1, V]: d lm partial sums per frame range
+  int lsplit;
   float* px;           // [N, T, U+1] (caller's or ws)
   float* py;
   double* alpha;       // ws [N, T, U+1], log2 domain
@@ -37,6 +41,8 @@ struct SimpleArgs {
 
 hipError_t launch_rowmax(const SimpleArgs& a, hipStream_t s);
 hipError_t launch_normalizer(const SimpleArgs& a, hipStream_t s);
+int normalizer_splits(int N, int T, int U, int V);
+int dlm_splits(int N, int T, int U, int V);
 hipError_t launch_lattice(const SimpleArgs& a, hipStream_t s);
 int lattice_colblocks(int T);
 hipError_t launch_simple_grads(const SimpleArgs& a, hipStream_t s);

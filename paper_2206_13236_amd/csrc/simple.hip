@@ -28,6 +28,9 @@ namespace {
 
 DEV float keep_nan_max(float m, float x) { return (x > m || x != x) ? x : m; }
 
+// Length of each of `splits` contiguous K ranges over [0, K), a multiple of bk.
+DEV int split_chunk(int K, int splits, int bk) { return ((K + splits - 1) / splits + bk - 1) / bk * bk; }
+
 // ---------------------------------------------------------------------------
 // Row maxima of am (rows t < T_n) and lm (rows u <= U_n): one wave per row.
 // ---------------------------------------------------------------------------
@@ -113,61 +116,77 @@ struct ExpRowsKC {  // rows r0 + row of x[.][V], value exp(x - max[row]); rows <
   DEV void kc_finish(const Raw& r, float (&v)[4]) const { finish_exp4(r, v); }
 };
 
+// Split over v into nsplit K ranges (the contraction alone has too few tiles
+// per batch to fill the chip); each writes its partial sums, and the
+// epilogue kernel adds them in split order.
 __global__ __launch_bounds__(256) void normalizer_kernel(SimpleArgs a) {
   using Cfg = NormCfg;
   __shared__ __align__(16) float smem[Cfg::SMEM_BYTES / sizeof(float)];
-  const int n = blockIdx.z;
+  const int n = blockIdx.z / a.nsplit, sk = blockIdx.z - n * a.nsplit;
   const int t0 = blockIdx.x * Cfg::BM, u0 = blockIdx.y * Cfg::BN;
   const int T = a.b.T, U1 = a.b.U + 1, V = a.V;
   int Tn, Un;
   utt_dims(a.b, n, Tn, Un);
-  const size_t base = (size_t)n * T * U1;
-  const bool active = (t0 < Tn) && (u0 <= Un);
+  if (t0 >= Tn || u0 > Un) return;
+  const int kc = split_chunk(V, a.nsplit, Cfg::BK);
+  const int k0 = min(V, sk * kc), k1 = min(V, k0 + kc);
   floatx4 acc[Cfg::FM][Cfg::FN];
-  if (active) {
-    ExpRowsKC sa{a.am + (size_t)n * T * V, a.m_a + (size_t)n * T, t0, Tn, V};
-    ExpRowsKC sb{a.lm + (size_t)n * U1 * V, a.m_l + (size_t)n * U1, u0, Un + 1, V};
-    KCLoader<Cfg, Cfg::BM, ExpRowsKC> la(sa);
-    KCLoader<Cfg, Cfg::BN, ExpRowsKC> lb(sb);
-    gemm_mainloop<Cfg>(la, lb, 0, V, smem, acc);
-  }
-  const int blank = a.b.blank;
-  const float* amn = a.am + (size_t)n * T * V;
-  const float* lmn = a.lm + (size_t)n * U1 * V;
+  ExpRowsKC sa{a.am + (size_t)n * T * V, a.m_a + (size_t)n * T, t0, Tn, V};
+  ExpRowsKC sb{a.lm + (size_t)n * U1 * V, a.m_l + (size_t)n * U1, u0, Un + 1, V};
+  KCLoader<Cfg, Cfg::BM, ExpRowsKC> la(sa);
+  KCLoader<Cfg, Cfg::BN, ExpRowsKC> lb(sb);
+  gemm_mainloop<Cfg>(la, lb, k0, k1, smem, acc);
+  float* part = a.npart + ((size_t)sk * a.b.N + n) * T * U1;
 #pragma unroll
   for (int j = 0; j < Cfg::FN; ++j) {
     const int u = u0 + tile_col<Cfg>(j);
-    if (u >= U1) continue;
-    bool sym_ok = true;
-    const int y = (u < Un) ? symbol_at(a.b, n, u, V, sym_ok) : 0;
-    const float ml = (u <= Un) ? a.m_l[(size_t)n * U1 + u] : 0.f;
+    if (u > Un) continue;
 #pragma unroll
     for (int i = 0; i < Cfg::FM; ++i)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int t = t0 + tile_row<Cfg>(i, r);
-        if (t >= T) continue;
-        const size_t idx = base + (size_t)t * U1 + u;
-        if (active && t < Tn && u <= Un) {
-          float s = acc[i][j][r];
-          s = (s > FLT_MIN || s != s) ? s : FLT_MIN;
-          const float z = a.m_a[(size_t)n * T + t] + ml + logf(s);
-          a.Z[idx] = z;
-          a.py[idx] = amn[(size_t)t * V + blank] + lmn[(size_t)u * V + blank] - z;
-          a.px[idx] = (u < Un) ? amn[(size_t)t * V + y] + lmn[(size_t)u * V + y] - z : kNegInfF;
-        } else {
-          a.Z[idx] = 0.f;
-          a.px[idx] = kNegInfF;
-          a.py[idx] = kNegInfF;
-        }
+        if (t < Tn) part[(size_t)t * U1 + u] = acc[i][j][r];
       }
   }
+}
+
+// Z = m_a + m_l + log(sum of the partials), px and py (Eqs. (1)-(2), (5)):
+// one thread per lattice node.
+__global__ __launch_bounds__(256) void normalizer_epi_kernel(SimpleArgs a) {
+  const int T = a.b.T, U1 = a.b.U + 1, V = a.V;
+  const size_t L = (size_t)a.b.N * T * U1;
+  const size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= L) return;
+  const int n = (int)(idx / ((size_t)T * U1));
+  const int rem = (int)(idx - (size_t)n * T * U1);
+  const int t = rem / U1, u = rem - t * U1;
+  int Tn, Un;
+  utt_dims(a.b, n, Tn, Un);
+  if (t >= Tn || u > Un) {
+    a.Z[idx] = 0.f;
+    a.px[idx] = kNegInfF;
+    a.py[idx] = kNegInfF;
+    return;
+  }
+  float s = 0.f;
+  for (int q = 0; q < a.nsplit; ++q) s += a.npart[(size_t)q * L + idx];
+  s = (s > FLT_MIN || s != s) ? s : FLT_MIN;
+  const float z = a.m_a[(size_t)n * T + t] + a.m_l[(size_t)n * U1 + u] + logf(s);
+  const float* amt = a.am + ((size_t)n * T + t) * V;
+  const float* lmu = a.lm + ((size_t)n * U1 + u) * V;
+  const int blank = a.b.blank;
+  a.Z[idx] = z;
+  a.py[idx] = amt[blank] + lmu[blank] - z;
+  bool ok = true;
+  const int y = (u < Un) ? symbol_at(a.b, n, u, V, ok) : 0;
+  a.px[idx] = (u < Un) ? amt[y] + lmu[y] - z : kNegInfF;
 }
 
 // ---------------------------------------------------------------------------
 // d am: per utterance C[t][v] = sum_u Wt[t][u] El[u][v]  (K = U_n + 1)
 // ---------------------------------------------------------------------------
-using DamCfg = GemmCfg<64, 128, 32, false>;
+using DamCfg = GemmCfg<32, 64, 32, false>;
 
 struct WtSrcKC {  // A(t, u) = Wt[t][u], rows padded to ldw (multiple of 4, zero-filled)
   using Raw = RawF<4>;
@@ -276,7 +295,7 @@ __global__ __launch_bounds__(256) void dam_kernel(SimpleArgs a) {
 // ---------------------------------------------------------------------------
 // d lm: per utterance C[u][v] = sum_t Wt[t][u] Ea[t][v]  (K = T_n)
 // ---------------------------------------------------------------------------
-using DlmCfg = GemmCfg<64, 128, 32, false>;
+using DlmCfg = GemmCfg<32, 64, 32, false>;
 
 struct WtSrcMNC {  // A(u, t) = Wt[t][u]: global is [t][u], u-contiguous
   using Raw = RawF<4>;
@@ -290,63 +309,85 @@ struct WtSrcMNC {  // A(u, t) = Wt[t][u]: global is [t][u], u-contiguous
   DEV void mnc_finish(const Raw& r, float (&v)[4]) const { finish_plain4(r, v); }
 };
 
+// Split over frames into lsplit K ranges; partial sums C[u][v] per split,
+// finished by dlm_epi_kernel.
 __global__ __launch_bounds__(256) void dlm_kernel(SimpleArgs a) {
   using Cfg = DlmCfg;
   __shared__ __align__(16) float smem[Cfg::SMEM_BYTES / sizeof(float)];
-  const int n = blockIdx.z;
+  const int n = blockIdx.z / a.lsplit, sk = blockIdx.z - n * a.lsplit;
   const int u0 = blockIdx.x * Cfg::BM, v0 = blockIdx.y * Cfg::BN;
   const int T = a.b.T, U1 = a.b.U + 1, V = a.V;
   int Tn, Un;
   utt_dims(a.b, n, Tn, Un);
-  const bool active = u0 <= Un;
+  if (u0 > Un) return;
+  const int kc = split_chunk(Tn, a.lsplit, Cfg::BK);
+  const int k0 = min(Tn, sk * kc), k1 = min(Tn, k0 + kc);
   floatx4 acc[Cfg::FM][Cfg::FN];
-  if (active) {
-    WtSrcMNC sa{a.Wt + (size_t)n * T * a.ldw, u0, Tn, a.ldw};
-    ExpSrcMNC sb{a.am + (size_t)n * T * V, a.m_a + (size_t)n * T, v0, Tn, V};
-    MNCLoader<Cfg, Cfg::BM, WtSrcMNC> la(sa);
-    MNCLoader<Cfg, Cfg::BN, ExpSrcMNC> lb(sb);
-    gemm_mainloop<Cfg>(la, lb, 0, Tn, smem, acc);
-  }
-  const float* lmn = a.lm + (size_t)n * U1 * V;
-  const float sc = a.scale ? a.scale[n] : 1.f;
-  const int blank = a.b.blank;
-  float* out = a.lm_grad + (size_t)n * U1 * V;
+  WtSrcMNC sa{a.Wt + (size_t)n * T * a.ldw, u0, Tn, a.ldw};
+  ExpSrcMNC sb{a.am + (size_t)n * T * V, a.m_a + (size_t)n * T, v0, Tn, V};
+  MNCLoader<Cfg, Cfg::BM, WtSrcMNC> la(sa);
+  MNCLoader<Cfg, Cfg::BN, ExpSrcMNC> lb(sb);
+  gemm_mainloop<Cfg>(la, lb, k0, k1, smem, acc);
+  float* part = a.lpart + ((size_t)sk * a.b.N + n) * U1 * V;
 #pragma unroll
   for (int i = 0; i < Cfg::FM; ++i)
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int u = u0 + tile_row<Cfg>(i, r);
-      if (u >= U1) continue;
-      const bool uv = active && u <= Un;
-      const float ml = uv ? a.m_l[(size_t)n * U1 + u] : 0.f;
-      bool ok = true;
-      const int y = (uv && u < Un) ? symbol_at(a.b, n, u, V, ok) : -1;
+      if (u > Un) continue;
 #pragma unroll
       for (int j = 0; j < Cfg::FN; ++j) {
         const int v = v0 + tile_col<Cfg>(j);
-        if (v >= V) continue;
-        float g = 0.f;
-        if (uv) {
-          // The target and blank columns collect sum_t gx(t,u) and sum_t gy(t,u):
-          // added from the per-16-frame partials in fixed order, in fp64, and
-          // rounded once.
-          double gd = (double)(expf(lmn[(size_t)u * V + v] - ml) * acc[i][j][r]);
-          if (v == y || v == blank) {
-            double cx = 0.0, cy = 0.0;
-            const double* px_ = a.cpx + (size_t)n * a.ncolblk * U1 + u;
-            const double* py_ = a.cpy + (size_t)n * a.ncolblk * U1 + u;
-            for (int q = 0; q < a.ncolblk; ++q) {
-              cx += px_[(size_t)q * U1];
-              cy += py_[(size_t)q * U1];
-            }
-            if (v == y) gd -= cx;
-            if (v == blank) gd -= cy;
-          }
-          g = (float)(sc * gd);
-        }
-        out[(size_t)u * V + v] = g;
+        if (v < V) part[(size_t)u * V + v] = acc[i][j][r];
       }
     }
+}
+
+// d lm[u,v] = sc (e^{lm - m_l} sum_splits C - [v = y_{u+1}] sum_t gx - [v = blank] sum_t gy);
+// one thread per 4 consecutive v of a row.
+__global__ __launch_bounds__(256) void dlm_epi_kernel(SimpleArgs a) {
+  const int U1 = a.b.U + 1, V = a.V;
+  const int nvg = (V + 3) / 4;
+  const size_t g = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (g >= (size_t)a.b.N * U1 * nvg) return;
+  const int row = (int)(g / nvg);  // n * U1 + u
+  const int v0 = (int)(g - (size_t)row * nvg) * 4;
+  const int n = row / U1, u = row - n * U1;
+  int Tn, Un;
+  utt_dims(a.b, n, Tn, Un);
+  float* out = a.lm_grad + (size_t)row * V;
+  if (u > Un) {
+    for (int v = v0; v < min(V, v0 + 4); ++v) out[v] = 0.f;
+    return;
+  }
+  const float sc = a.scale ? a.scale[n] : 1.f;
+  const int blank = a.b.blank;
+  bool ok = true;
+  const int y = (u < Un) ? symbol_at(a.b, n, u, V, ok) : -1;
+  const float ml = a.m_l[row];
+  const float* lmr = a.lm + (size_t)row * V;
+  const size_t stride = (size_t)a.b.N * U1 * V;
+  const size_t base = (size_t)row * V;
+  for (int v = v0; v < min(V, v0 + 4); ++v) {
+    float c = 0.f;
+    for (int q = 0; q < a.lsplit; ++q) c += a.lpart[(size_t)q * stride + base + v];
+    // The target and blank columns collect sum_t gx(t,u) and sum_t gy(t,u):
+    // added from the per-16-frame partials in fixed order, in fp64, and
+    // rounded once.
+    double gd = (double)(expf(lmr[v] - ml) * c);
+    if (v == y || v == blank) {
+      double cx = 0.0, cy = 0.0;
+      const double* px_ = a.cpx + (size_t)n * a.ncolblk * U1 + u;
+      const double* py_ = a.cpy + (size_t)n * a.ncolblk * U1 + u;
+      for (int q = 0; q < a.ncolblk; ++q) {
+        cx += px_[(size_t)q * U1];
+        cy += py_[(size_t)q * U1];
+      }
+      if (v == y) gd -= cx;
+      if (v == blank) gd -= cy;
+    }
+    out[v] = (float)(sc * gd);
+  }
 }
 
 __global__ void fill_f32_kernel(float* p, size_t n, float v) {
@@ -370,12 +411,37 @@ hipError_t launch_rowmax(const SimpleArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
+// Split counts: enough K ranges for about 1024 workgroups, each range at
+// least two K-steps long.
+static int split_count(long long tiles, int K, int bk) {
+  long long sk = (1024 + tiles - 1) / tiles;
+  const long long most = (K + 2 * bk - 1) / (2 * bk);
+  if (sk > most) sk = most;
+  if (sk > 16) sk = 16;
+  return sk < 1 ? 1 : (int)sk;
+}
+
+int normalizer_splits(int N, int T, int U, int V) {
+  const long long tiles = (long long)N * ((T + NormCfg::BM - 1) / NormCfg::BM) * ((U + 1 + NormCfg::BN - 1) / NormCfg::BN);
+  return split_count(tiles, V, NormCfg::BK);
+}
+
+int dlm_splits(int N, int T, int U, int V) {
+  const long long tiles = (long long)N * ((U + 1 + DlmCfg::BM - 1) / DlmCfg::BM) * ((V + DlmCfg::BN - 1) / DlmCfg::BN);
+  return split_count(tiles, T, DlmCfg::BK);
+}
+
 hipError_t launch_normalizer(const SimpleArgs& a, hipStream_t s) {
   const int T = a.b.T, U1 = a.b.U + 1;
-  dim3 grid((T + NormCfg::BM - 1) / NormCfg::BM, (U1 + NormCfg::BN - 1) / NormCfg::BN, a.b.N);
+  dim3 grid((T + NormCfg::BM - 1) / NormCfg::BM, (U1 + NormCfg::BN - 1) / NormCfg::BN, a.b.N * a.nsplit);
   {
     RNNT_PROF(s, "normalizer");
     hipLaunchKernelGGL(normalizer_kernel, grid, dim3(256), 0, s, a);
+  }
+  const size_t L = (size_t)a.b.N * T * U1;
+  {
+    RNNT_PROF(s, "normalizer_epi");
+    hipLaunchKernelGGL(normalizer_epi_kernel, dim3((unsigned)((L + 255) / 256)), dim3(256), 0, s, a);
   }
   return hipGetLastError();
 }
@@ -390,10 +456,15 @@ hipError_t launch_simple_grads(const SimpleArgs& a, hipStream_t s) {
     }
   }
   if (a.lm_grad) {
-    dim3 grid((U1 + DlmCfg::BM - 1) / DlmCfg::BM, (V + DlmCfg::BN - 1) / DlmCfg::BN, a.b.N);
+    dim3 grid((U1 + DlmCfg::BM - 1) / DlmCfg::BM, (V + DlmCfg::BN - 1) / DlmCfg::BN, a.b.N * a.lsplit);
     {
       RNNT_PROF(s, "simple_dlm");
       hipLaunchKernelGGL(dlm_kernel, grid, dim3(256), 0, s, a);
+    }
+    const size_t groups = (size_t)a.b.N * U1 * ((V + 3) / 4);
+    {
+      RNNT_PROF(s, "simple_dlm_epi");
+      hipLaunchKernelGGL(dlm_epi_kernel, dim3((unsigned)((groups + 255) / 256)), dim3(256), 0, s, a);
     }
   }
   return hipGetLastError();
