@@ -158,7 +158,7 @@ size_t rnnt_pruned_joiner_workspace_size(int32_t N, int32_t T, int32_t S, int32_
  *   absent slots).
  * Outputs, fp32 [N, T, S]: px = logits[y_{u+1}] - lse (u < U_n, else -inf),
  *   py = logits[blank] - lse, lse (0 for absent slots).
- * logits [N, T, S, V] fp32 (nullable, caller-owned): when given, the logits
+ * logits [N, T, S, V] fp32 (nullable, caller-owned, 16-byte aligned): when given, the logits
  *   are stored as well (entries of absent slots and padding frames are left
  *   untouched), so that rnnt_pruned_joiner_backward can stream them instead
  *   of recomputing the projection. This is the [N, T, S, V] memory the
@@ -195,7 +195,7 @@ size_t rnnt_pruned_joiner_backward_workspace_size(int32_t N, int32_t T, int32_t 
  * lse, px_occ, py_occ [N, T, S]: from rnnt_pruned_joiner / rnnt_pruned_loss.
  * logits [N, T, S, V] (nullable): the logits stored by rnnt_pruned_joiner
  *   for the same inputs; when null they are recomputed (one more GEMM).
- * Outputs (fp32): enc_grad [N, T, J], dec_grad [N, U+1, J] (required);
+ * Outputs (fp32): enc_grad [N, T, J], dec_grad [N, U+1, J] (required, 16-byte aligned);
  *   W_grad [J, V], bias_grad [V] (nullable);
  *   logits_grad [N, T, S, V] (nullable; debugging aid for small shapes).
  * Reductions run in a fixed order: results are bitwise reproducible.

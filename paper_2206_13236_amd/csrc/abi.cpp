@@ -183,6 +183,8 @@ int check_ws(void* ws, size_t have, size_t need) {
   return RNNT_OK;
 }
 
+bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
+
 int check_joiner_sizes(const rnnt_batch* b, int S, int J, int V, int dtype) {
   if (S < 1 || S > RNNT_MAX_S) return fail(RNNT_EUNSUPPORTED, "S = %d outside [1, %d]", S, RNNT_MAX_S);
   if (V < 1) return fail(RNNT_EINVAL, "V must be >= 1 (got %d)", V);
@@ -293,6 +295,7 @@ int rnnt_pruned_joiner(const rnnt_batch* batch, int32_t S, int32_t J, int32_t V,
   if (rc) return rc;
   if (!enc || !dec || !W || !ranges) return fail(RNNT_EINVAL, "enc, dec, W and ranges are required");
   if (!px || !py || !lse) return fail(RNNT_EINVAL, "px, py and lse are required");
+  if (!aligned16(logits)) return fail(RNNT_EINVAL, "logits must be 16-byte aligned");
   rc = check_ws(workspace, workspace_bytes, joiner_fwd_layout(nullptr, batch->N, batch->T, S, V).bytes);
   if (rc) return rc;
   const JoinerFwdWs w = joiner_fwd_layout(workspace, batch->N, batch->T, S, V);
@@ -384,6 +387,8 @@ int rnnt_pruned_joiner_backward(const rnnt_batch* batch, int32_t S, int32_t J, i
   if (!enc || !dec || !W || !ranges || !lse || !px_occ || !py_occ)
     return fail(RNNT_EINVAL, "enc, dec, W, ranges, lse, px_occ and py_occ are required");
   if (!enc_grad || !dec_grad) return fail(RNNT_EINVAL, "enc_grad and dec_grad are required");
+  if (!aligned16(enc_grad) || !aligned16(dec_grad) || !aligned16(logits))
+    return fail(RNNT_EINVAL, "enc_grad, dec_grad and logits must be 16-byte aligned");
   if (logits_grad && (long long)batch->N * batch->T * S * (long long)V > (1ll << 40))
     return fail(RNNT_EUNSUPPORTED, "logits_grad is a debugging aid for small shapes");
   const int bf = dtype == RNNT_BF16;

@@ -769,35 +769,60 @@ __global__ __launch_bounds__(1024) void joiner_dbsum_kernel(JoinerArgs a) {
 }
 
 // d enc[n,t] = sum_s dpre(row(t,s)); d dec[n,u] = sum over t of dpre(row(t, u - p_t))
-// for 0 <= u - p_t < S. One block per output row; threads over J.
-__global__ __launch_bounds__(256) void joiner_encdec_kernel(JoinerArgs a) {
-  extern __shared__ int sp[];  // p_t of the utterance (dec rows only)
-  const int T = a.b.T, U1 = a.b.U + 1, S = a.S, J = a.J;
-  const int rowsper = T + U1;
-  const int n = blockIdx.x / rowsper, i = blockIdx.x - n * rowsper;
+// for 0 <= u - p_t < S. Threads over float4 column groups of J, several
+// output rows per 256-thread block; every sum runs in ascending s or t.
+DEV int encdec_rows_per_block(int J) {
+  const int tpr = J / 4;
+  return tpr >= 256 ? 1 : 256 / tpr;
+}
+
+DEV float4 f4add(float4 a, float4 b) { return make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w); }
+
+__global__ __launch_bounds__(256) void joiner_enc_kernel(JoinerArgs a) {
+  const int T = a.b.T, S = a.S, J = a.J, tpr = J / 4;
+  const int R = encdec_rows_per_block(J);
+  const int rr = threadIdx.x / tpr, c = threadIdx.x - rr * tpr;
+  const int row = blockIdx.x * R + rr;  // n * T + t
+  if (rr >= R || row >= a.b.N * T) return;
+  const int n = row / T, t = row - n * T;
   int Tn, Un;
   utt_dims(a.b, n, Tn, Un);
-  const int off = a.frame_off[n];
-  if (i < T) {
-    float* out = a.enc_grad + ((size_t)n * T + i) * J;
-    for (int j = threadIdx.x; j < J; j += blockDim.x) {
-      float s = 0.f;
-      if (i < Tn) {
-        const float* d = a.dpre + (size_t)(off + i) * S * J + j;
-        for (int q = 0; q < S; ++q) s += d[(size_t)q * J];
+  for (int g = c; g < tpr; g += 256) {  // one pass unless J > 1024
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (t < Tn) {
+      const float4* d = reinterpret_cast<const float4*>(a.dpre + (size_t)(a.frame_off[n] + t) * S * J) + g;
+      float4 v[8];
+      int q = 0;
+      for (; q + 8 <= S; q += 8) {
+#pragma unroll
+        for (int k = 0; k < 8; ++k) v[k] = d[(size_t)(q + k) * tpr];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) acc = f4add(acc, v[k]);
       }
-      out[j] = s;
+      for (; q < S; ++q) acc = f4add(acc, d[(size_t)q * tpr]);
     }
-    return;
+    reinterpret_cast<float4*>(a.enc_grad + (size_t)row * J)[g] = acc;
   }
-  const int u = i - T;
-  float* out = a.dec_grad + ((size_t)n * U1 + u) * J;
-  if (u > Un) {
-    for (int j = threadIdx.x; j < J; j += blockDim.x) out[j] = 0.f;
-    return;
-  }
+}
+
+// grid (ceil((U+1)/R), N): the block's rows are dec rows u of utterance n.
+__global__ __launch_bounds__(256) void joiner_dec_kernel(JoinerArgs a) {
+  extern __shared__ int sp[];  // p_t of the utterance
+  const int T = a.b.T, U1 = a.b.U + 1, S = a.S, J = a.J, tpr = J / 4;
+  const int R = encdec_rows_per_block(J);
+  const int n = blockIdx.y;
+  int Tn, Un;
+  utt_dims(a.b, n, Tn, Un);
   for (int t = threadIdx.x; t < Tn; t += blockDim.x) sp[t] = a.ranges[((size_t)n * T + t) * S];
   __syncthreads();
+  const int rr = threadIdx.x / tpr, c = threadIdx.x - rr * tpr;
+  const int u = blockIdx.x * R + rr;
+  if (rr >= R || u >= U1) return;
+  float4* out = reinterpret_cast<float4*>(a.dec_grad + ((size_t)n * U1 + u) * J);
+  if (u > Un) {
+    for (int g = c; g < tpr; g += 256) out[g] = make_float4(0.f, 0.f, 0.f, 0.f);
+    return;
+  }
   // p_t is non-decreasing (Eq. (9)), so the frames whose band holds u form
   // the interval [first t with p_t > u - S, first t with p_t > u).
   int lo = 0, hi = Tn;
@@ -814,19 +839,20 @@ __global__ __launch_bounds__(256) void joiner_encdec_kernel(JoinerArgs a) {
     else lo = mid + 1;
   }
   const int t1 = lo;
-  for (int j = threadIdx.x; j < J; j += blockDim.x) {
-    float s = 0.f;
+  const float4* d = reinterpret_cast<const float4*>(a.dpre);
+  const size_t off = (size_t)a.frame_off[n];
+  for (int g = c; g < tpr; g += 256) {
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
     int t = t0;
-    // loads of 8 frames in flight, added in ascending t
-    for (; t + 8 <= t1; t += 8) {
-      float v[8];
+    for (; t + 8 <= t1; t += 8) {  // loads of 8 frames in flight, added in ascending t
+      float4 v[8];
 #pragma unroll
-      for (int q = 0; q < 8; ++q) v[q] = a.dpre[((size_t)(off + t + q) * S + (u - sp[t + q])) * J + j];
+      for (int k = 0; k < 8; ++k) v[k] = d[((off + t + k) * S + (u - sp[t + k])) * tpr + g];
 #pragma unroll
-      for (int q = 0; q < 8; ++q) s += v[q];
+      for (int k = 0; k < 8; ++k) acc = f4add(acc, v[k]);
     }
-    for (; t < t1; ++t) s += a.dpre[((size_t)(off + t) * S + (u - sp[t])) * J + j];
-    out[j] = s;
+    for (; t < t1; ++t) acc = f4add(acc, d[((off + t) * S + (u - sp[t])) * tpr + g]);
+    out[g] = acc;
   }
 }
 
@@ -942,10 +968,15 @@ hipError_t launch_joiner_bwd(const JoinerArgs& a, hipStream_t s) {
     RNNT_PROF(s, "joiner_dbsum");
     hipLaunchKernelGGL(joiner_dbsum_kernel, dim3((unsigned)((V + 63) / 64)), dim3(1024), 0, s, a);
   }
-  const int rows = a.b.N * (a.b.T + a.b.U + 1);
+  const int R = (J / 4 >= 256) ? 1 : 256 / (J / 4);
   {
-    RNNT_PROF(s, "joiner_encdec");
-    hipLaunchKernelGGL(joiner_encdec_kernel, dim3(rows), dim3(256), (size_t)a.b.T * sizeof(int), s, a);
+    RNNT_PROF(s, "joiner_enc");
+    hipLaunchKernelGGL(joiner_enc_kernel, dim3((a.b.N * a.b.T + R - 1) / R), dim3(256), 0, s, a);
+  }
+  {
+    RNNT_PROF(s, "joiner_dec");
+    hipLaunchKernelGGL(joiner_dec_kernel, dim3((a.b.U + 1 + R - 1) / R, a.b.N), dim3(256),
+                       (size_t)a.b.T * sizeof(int), s, a);
   }
   return hipGetLastError();
 }
