@@ -5,8 +5,8 @@
 // m = (frame_off[n] + t) * S + s (padding frames take no rows), so the GEMMs
 // see one dense M = S * sum_n T_n dimension. A prep kernel writes, per row,
 // the offsets of enc[n,t] and dec[n,u] (u = ranges[n,t,s]), the target symbol
-// y_{u+1} (-1 at u = U_n) and the output index n*T*S + t*S + s (-1 when the
-// slot is absent, u > U_n).
+// y_{u+1} (-1 at u = U_n, -2 when it lies outside [0, V)) and the output index
+// n*T*S + t*S + s (-1 when the slot is absent, u > U_n).
 //
 // Forward: logits = tanh(enc + dec) W + bias on MFMA (fp32 16x16x4 or bf16
 // 16x16x32, fp32 accumulation); the tanh is formed while staging the A tile.
@@ -312,6 +312,7 @@ __global__ __launch_bounds__(256) void joiner_prep_kernel(JoinerArgs a) {
       r.x = (int)(((size_t)n * T + t) * J);
       r.y = (int)(((size_t)n * U1 + u) * J);
       r.z = (u < Un) ? symbol_at(a.b, n, u, a.V, ok) : -1;
+      if (!ok) r.z = -2;  // symbol outside [0, V): px is NaN, so the utterance's loss is NaN
       r.w = (int)nts;
     } else {
       r = make_int4(0, 0, -1, -1);
@@ -419,7 +420,7 @@ __global__ __launch_bounds__(256) void joiner_combine_kernel(JoinerArgs a) {
       for (int p = 0; p < a.nparts; ++p) sum += pp[p].y * __expf(pp[p].x - M);
       l = M + __logf(sum);
       py = a.blk[m] - l;
-      px = (info.z >= 0) ? a.tgt[m] - l : kNegInfF;
+      px = (info.z >= 0) ? a.tgt[m] - l : (info.z == -2 ? __builtin_nanf("") : kNegInfF);
     }
   }
   a.px[i] = px;

@@ -70,3 +70,96 @@ def grad_atol(ref, bf16: bool, param: bool = False) -> float:
 
 def loss_rtol(bf16: bool) -> float:
     return 2e-2 if bf16 else 1e-5
+
+
+# ---------------------------------------------------------------------------
+# End-to-end comparison (PrunedRnntLoss.step against the oracle's pipeline)
+# ---------------------------------------------------------------------------
+
+def near_tie_utterances(gx, gy, t_len, u_len, S, delta=2e-5):
+    """Utterances with a frame whose two best window scores (Eq. (8)) are within delta.
+
+    End to end, the GPU scores come from its own fp32 occupations, which agree
+    with the oracle's to ~1e-6; where two windows score the same to that
+    precision (typically several windows that all retain the whole mass,
+    score 1.0), either choice is correct and the bounds are not unique.
+    """
+    import oracle as O
+    amb = set()
+    for n in range(len(t_len)):
+        sc = O.pruning_window_scores(gx[n], gy[n], t_len[n], u_len[n], S).astype(np.float64)
+        if sc.shape[1] < 2:
+            continue
+        top2 = np.sort(sc, axis=1)[:, -2:]
+        if np.any(top2[:, 1] - top2[:, 0] <= delta):
+            amb.add(n)
+    return amb
+
+
+def ranges_valid(r, t_len, u_len, S):
+    """Monotone, no-skip bounds from p_0 = 0 to p_{T-1} = min(P, (S-1)(T-1)) (Eqs. (9)-(10))."""
+    for n in range(len(t_len)):
+        Tn, Un = int(t_len[n]), int(u_len[n])
+        p = r[n, :Tn, 0]
+        P = max(0, Un - S + 1)
+        assert np.array_equal(r[n, :Tn], p[:, None] + np.arange(S)[None, :])
+        assert np.all(r[n, Tn:] == np.arange(S))
+        assert p[0] == 0 and p[-1] == min(P, (S - 1) * (Tn - 1))
+        assert np.all(np.diff(p) >= 0) and np.all(np.diff(p) < S) and np.all((p >= 0) & (p <= P))
+
+
+def run_step(b, S, bf16=None, keep_logits=True, simple_scale=0.5):
+    """The whole GPU path on batch b, as the benchmark runs it."""
+    bf = (b.wl.joiner_dtype == "bf16") if bf16 is None else bf16
+    batch = make_dev_batch(b)
+    step = P.PrunedRnntLoss(S, simple_scale=simple_scale, keep_logits=keep_logits)
+    out = step.step(batch, dev_f32(b.am), dev_f32(b.lm), dev_joiner(b.enc, bf), dev_joiner(b.dec, bf),
+                    dev_joiner(b.W, bf), dev_joiner(b.bias, bf))
+    torch.cuda.synchronize()
+    return {k: (v.cpu().numpy() if v.dtype == torch.int32 else host(v)) for k, v in out.items()}
+
+
+def oracle_step(b, S, idx=None, simple_scale=0.5):
+    """The oracle's pipeline on utterances idx (all by default) of batch b."""
+    import oracle as O
+    idx = np.arange(b.N) if idx is None else np.asarray(idx)
+    sym = b.symbols[idx]
+    tl, ul = b.t_len[idx], b.u_len[idx]
+    s1 = O.simple_stage(b.am[idx], b.lm[idx], sym, tl, ul, b.wl.blank, scale=np.full(len(idx), simple_scale))
+    ranges = O.prune_ranges(s1["gx"], s1["gy"], tl, ul, S)
+    st = O.pruned_stage(b.enc[idx], b.dec[idx], b.W, b.bias, ranges, sym, tl, ul, b.wl.blank)
+    return {"idx": idx, "s1": s1, "ranges": ranges, "st": st}
+
+
+def check_step(out, ref, b, S, bf16=None, whole_batch=True):
+    """Compare run_step's outputs with oracle_step's on the oracle's utterances.
+
+    Stage 1-2 outputs are unique and compared everywhere; the bounds are
+    compared exactly where the window argmax is unique (and checked valid
+    everywhere), and the pruned loss and joiner gradients on those
+    utterances. dW and db are batch sums: compared when the oracle covers the
+    whole batch and no utterance has a near tie. Returns the near-tie set.
+    """
+    bf = (b.wl.joiner_dtype == "bf16") if bf16 is None else bf16
+    idx = ref["idx"]
+    s1, st = ref["s1"], ref["st"]
+    tl, ul = b.t_len[idx], b.u_len[idx]
+    assert_close("simple_loss", out["simple_loss"][idx], s1["loss"], rtol=1e-5)
+    assert_close("am_grad", out["am_grad"][idx], s1["am_grad"], atol=1e-4)
+    assert_close("lm_grad", out["lm_grad"][idx], s1["lm_grad"], atol=1e-4)
+    assert_close("simple_px_occ", out["simple_px_occ"][idx], s1["gx"], atol=1e-4)
+    assert_close("simple_py_occ", out["simple_py_occ"][idx], s1["gy"], atol=1e-4)
+    got_r = out["ranges"][idx]
+    ranges_valid(got_r, tl, ul, S)
+    amb = near_tie_utterances(s1["gx"], s1["gy"], tl, ul, S)
+    for k, n in enumerate(idx):
+        if k in amb:
+            continue
+        assert np.array_equal(got_r[k], ref["ranges"][k]), f"utterance {n}: ranges differ without a near tie"
+        assert_close(f"pruned_loss[{n}]", out["pruned_loss"][n], st["loss"][k], rtol=loss_rtol(bf))
+        for key in ("enc_grad", "dec_grad"):
+            assert_close(f"{key}[{n}]", out[key][n], st[key][k], atol=grad_atol(st[key], bf))
+    if whole_batch and len(idx) == b.N and not amb:
+        for key in ("W_grad", "bias_grad"):
+            assert_close(key, out[key], st[key], atol=grad_atol(st[key], bf, param=True))
+    return amb

@@ -1,0 +1,170 @@
+"""GPU edge cases against the oracle: empty and one-frame utterances, a band
+that covers the whole lattice, a blank other than 0 (and a token equal to
+blank), NaN in the padding, out-of-range lengths and symbols, an infeasible
+band, S = 1 and the largest S, and U near the lattice limit.
+
+Each case is a small batch whose oracle pipeline finishes in well under a
+second; every batch still has ragged lengths and V not a multiple of the
+tile width.
+"""
+import dataclasses
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import paper_2206_13236_amd as P
+from gpu_common import (assert_close, check_step, dev_f32, dev_i32, host, make_dev_batch, oracle_step,
+                        run_step, say)
+from workloads import Workload, make_batch
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    assert torch.cuda.is_available(), "GPU tests need a ROCm device"
+    P.lib()
+
+
+def _small(seed=0, N=4, T_range=(12, 30), U_range=(3, 9), V=29, J=32, S=4, **wl_over):
+    b = make_batch("bpe", seed=seed, N=N, T_range=T_range, U_range=U_range, V=V, J=J, S=S)
+    if wl_over:
+        b = dataclasses.replace(b, wl=Workload(**{**b.wl.__dict__, **wl_over}))
+    return b
+
+
+def _with_lengths(b, t_len=None, u_len=None):
+    t = b.t_len.copy() if t_len is None else np.asarray(t_len, np.int32)
+    u = b.u_len.copy() if u_len is None else np.asarray(u_len, np.int32)
+    return dataclasses.replace(b, t_len=t, u_len=u)
+
+
+def test_empty_transcripts():
+    # U_n = 0 for some utterances: the lattice is one row, the loss the sum of blanks
+    b = _with_lengths(_small(seed=1), u_len=[0, 5, 0, 3])
+    say("[edge] U_n = 0")
+    out = run_step(b, 4)
+    check_step(out, oracle_step(b, 4), b, 4)
+
+
+def test_all_transcripts_empty():
+    b = _small(seed=2, U_range=(0, 0))
+    assert b.U == 0
+    say("[edge] U = 0 for the whole batch")
+    out = run_step(b, 3)
+    check_step(out, oracle_step(b, 3), b, 3)
+
+
+def test_one_frame_utterances():
+    # T_n = 1: one column; U_n <= (S-1) * T_n keeps the band feasible
+    b = _with_lengths(_small(seed=3), t_len=[1, 17, 1, 9], u_len=[2, 7, 0, 4])
+    say("[edge] T_n = 1")
+    out = run_step(b, 4)
+    check_step(out, oracle_step(b, 4), b, 4)
+
+
+def test_band_covering_the_lattice_equals_the_full_loss():
+    # S >= U+1: every p_t = 0 and the pruned loss is the unpruned loss (Sec. 3.2)
+    b = _small(seed=4, U_range=(2, 5))
+    S = b.U + 1
+    say(f"[edge] S = U+1 = {S}")
+    out = run_step(b, S)
+    assert np.all(out["ranges"] == np.arange(S)[None, None, :])
+    full, _, _ = O.full_joiner_loss(b.enc, b.dec, b.W, b.bias, b.symbols, b.t_len, b.u_len, b.wl.blank)
+    assert_close("pruned_loss vs full loss", out["pruned_loss"], full, rtol=1e-5)
+    check_step(out, oracle_step(b, S), b, S)
+
+
+def test_blank_not_zero_and_token_equal_to_blank():
+    b = _small(seed=5, blank=7)
+    sym = b.symbols.copy()
+    sym[0, 1] = 7  # a token equal to blank inside the transcript
+    sym[2, 0] = 7
+    b = dataclasses.replace(b, symbols=sym)
+    say("[edge] blank = 7")
+    out = run_step(b, 4)
+    check_step(out, oracle_step(b, 4), b, 4)
+
+
+def test_nan_in_padding_is_ignored():
+    b = _small(seed=6)
+    am, lm, enc, dec = b.am.copy(), b.lm.copy(), b.enc.copy(), b.dec.copy()
+    for n in range(b.N):
+        am[n, b.t_len[n]:] = np.nan
+        lm[n, b.u_len[n] + 1:] = np.nan
+        enc[n, b.t_len[n]:] = np.nan
+        dec[n, b.u_len[n] + 1:] = np.nan
+    poisoned = dataclasses.replace(b, am=am, lm=lm, enc=enc, dec=dec)
+    say("[edge] NaN padding")
+    out = run_step(poisoned, 4)
+    for k in ("simple_loss", "pruned_loss", "enc_grad", "dec_grad", "W_grad", "bias_grad", "am_grad", "lm_grad"):
+        assert np.all(np.isfinite(out[k])), f"{k} has non-finite values"
+    check_step(out, oracle_step(b, 4), b, 4)
+    # padding rows of the gradients are zero
+    for n in range(b.N):
+        assert np.all(out["am_grad"][n, b.t_len[n]:] == 0) and np.all(out["enc_grad"][n, b.t_len[n]:] == 0)
+        assert np.all(out["lm_grad"][n, b.u_len[n] + 1:] == 0) and np.all(out["dec_grad"][n, b.u_len[n] + 1:] == 0)
+
+
+def test_out_of_range_lengths_and_symbols_give_nan_for_that_utterance_only():
+    b = _small(seed=7, N=5)
+    t_len, u_len, sym = b.t_len.copy(), b.u_len.copy(), b.symbols.copy()
+    t_len[1] = b.T + 3       # longer than the padded T
+    u_len[2] = -1            # negative transcript length
+    sym[3, 0] = b.V + 5      # symbol outside [0, V)
+    bad = dataclasses.replace(b, t_len=t_len, u_len=u_len, symbols=sym)
+    say("[edge] invalid lengths / symbols")
+    out = run_step(bad, 4)
+    for n in (1, 2, 3):
+        assert np.isnan(out["simple_loss"][n]) and np.isnan(out["pruned_loss"][n]), f"utterance {n}"
+    good = [0, 4]
+    ref = oracle_step(b, 4, idx=good)
+    check_step(out, ref, b, 4, whole_batch=False)
+
+
+def test_infeasible_band_gives_inf_and_zero_joiner_gradients():
+    # U_n > (S-1) T_n: no band admits a complete path
+    b = _with_lengths(_small(seed=8, T_range=(10, 20), U_range=(6, 9)), t_len=[2, 15, 3, 12], u_len=[7, 8, 9, 6])
+    S = 3
+    say("[edge] infeasible band")
+    out = run_step(b, S)
+    ref = oracle_step(b, S)
+    infeasible = [n for n in range(b.N) if b.u_len[n] > (S - 1) * b.t_len[n]]
+    assert infeasible == [0, 2]
+    for n in infeasible:
+        assert out["pruned_loss"][n] == np.inf and ref["st"]["loss"][n] == np.inf
+        assert np.all(out["enc_grad"][n] == 0) and np.all(out["dec_grad"][n] == 0)
+    check_step(out, ref, b, S)
+
+
+def test_s_equal_one():
+    # S = 1: one node per frame, feasible only for U_n = 0
+    b = _small(seed=9, U_range=(0, 0))
+    say("[edge] S = 1")
+    out = run_step(b, 1)
+    check_step(out, oracle_step(b, 1), b, 1)
+
+
+def test_largest_s():
+    b = _small(seed=10, N=2, T_range=(20, 26), U_range=(30, 40), V=19, S=32)
+    say("[edge] S = 32")
+    out = run_step(b, 32)
+    check_step(out, oracle_step(b, 32), b, 32)
+
+
+def test_long_transcript_near_the_lattice_limit():
+    # U close to the 1023-row limit: 16 lattice rows per lane in the wavefront
+    b = _small(seed=11, N=2, T_range=(40, 48), U_range=(990, 1000), V=13, J=16, S=32)
+    say(f"[edge] U = {b.U}")
+    batch = make_dev_batch(b)
+    sc = np.full(b.N, 0.5, np.float32)
+    got = P.rnnt_simple_loss(batch, b.V, dev_f32(b.am), dev_f32(b.lm), dev_f32(sc), want_grads=True)
+    torch.cuda.synchronize()
+    s1 = O.simple_stage(b.am, b.lm, b.symbols, b.t_len, b.u_len, b.wl.blank, scale=sc)
+    assert_close("loss", host(got["loss"]), s1["loss"], rtol=1e-5)
+    assert_close("px_occ", host(got["px_occ"]), s1["gx"], atol=1e-4)
+    assert_close("py_occ", host(got["py_occ"]), s1["gy"], atol=1e-4)
+    assert_close("am_grad", host(got["am_grad"]), s1["am_grad"], atol=1e-4)
+    assert_close("lm_grad", host(got["lm_grad"]), s1["lm_grad"], atol=1e-4)

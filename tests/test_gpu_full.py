@@ -1,0 +1,137 @@
+"""Parity at the full workload sizes, in the configuration the benchmark times
+(PrunedRnntLoss.step with the logits kept for the backward).
+
+- bpe and long (the two V=500, S=5 workloads): the oracle's whole pipeline on
+  the whole batch, every output compared.
+- largev: the oracle on two sampled utterances (the shortest and the one with
+  the longest transcript).
+- stress: the oracle cannot run whole utterances in seconds (V=8000,
+  T up to 1000), so it checks sampled outputs one by one: the trivial joiner's
+  log-probs on sampled frames, and the pruned joiner's on sampled frames of a
+  full-size launch with fixed, valid bounds.
+
+Every workload is also checked against properties that hold at any size:
+flow conservation of both lattices' occupations, zero row sums of the
+log-softmax backward, and valid bounds.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import paper_2206_13236_amd as P
+from gpu_common import (assert_close, check_step, dev_f32, dev_i32, dev_joiner, host, make_dev_batch,
+                        oracle_step, ranges_valid, run_step, say)
+from workloads import make_batch
+
+pytestmark = pytest.mark.gpu
+
+_RUNS = {}
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    assert torch.cuda.is_available(), "GPU tests need a ROCm device"
+    P.lib()
+    yield
+    _RUNS.clear()
+
+
+def _run(name):
+    if name not in _RUNS:
+        _RUNS.clear()  # one full-size workload resident at a time
+        b = make_batch(name, seed=0)
+        say(f"[full] {name}: N={b.N} T={b.T} U={b.U} V={b.V} S={b.wl.S} J={b.wl.J} {b.wl.joiner_dtype}")
+        _RUNS[name] = (b, run_step(b, b.wl.S))
+        torch.cuda.empty_cache()
+    return _RUNS[name]
+
+
+@pytest.mark.parametrize("name", ["bpe", "long", "largev", "stress"])
+def test_full_size_invariants(name):
+    b, out = _run(name)
+    S = b.wl.S
+    ranges_valid(out["ranges"], b.t_len, b.u_len, S)
+    for n in range(b.N):
+        Tn, Un = int(b.t_len[n]), int(b.u_len[n])
+        assert np.isfinite(out["simple_loss"][n]) and out["simple_loss"][n] > 0
+        assert np.isfinite(out["pruned_loss"][n]) and out["pruned_loss"][n] > 0
+        # every complete path crosses each frame through one blank edge and emits each token once
+        gy, gx = out["simple_py_occ"][n], out["simple_px_occ"][n]
+        assert_close(f"sum_u gy[{n}]", gy[:Tn, :Un + 1].sum(1), np.ones(Tn), atol=2e-4)
+        if Un > 0:
+            assert_close(f"sum_t gx[{n}]", gx[:Tn, :Un].sum(0), np.ones(Un), atol=2e-4)
+        assert_close(f"band sum_s gy[{n}]", out["pruned_py_occ"][n, :Tn].sum(1), np.ones(Tn), atol=2e-4)
+        # the log-softmax backward has zero row sums
+        assert_close(f"am_grad rows[{n}]", out["am_grad"][n].sum(1), np.zeros(b.T), atol=2e-4)
+        assert_close(f"lm_grad rows[{n}]", out["lm_grad"][n].sum(1), np.zeros(b.U + 1), atol=2e-4)
+    assert abs(out["bias_grad"].sum()) <= 1e-4 * max(1.0, np.abs(out["bias_grad"]).max()) * np.sqrt(b.V)
+
+
+@pytest.mark.parametrize("name", ["bpe", "long"])
+def test_full_size_whole_batch_against_oracle(name):
+    b, out = _run(name)
+    say(f"[full] {name}: oracle on all {b.N} utterances")
+    amb = check_step(out, oracle_step(b, b.wl.S), b, b.wl.S)
+    say(f"  near-tie utterances {sorted(amb)}")
+
+
+def test_full_size_largev_sampled_utterances():
+    b, out = _run("largev")
+    idx = sorted({int(np.argmin(b.t_len)), int(np.argmax(b.u_len))})
+    say(f"[full] largev: oracle on utterances {idx}")
+    check_step(out, oracle_step(b, b.wl.S, idx=idx), b, b.wl.S, whole_batch=False)
+
+
+def _fixed_bounds(t_len, u_len, T, S):
+    """A valid band independent of any occupation: p_t = floor(t P / (T_n - 1))."""
+    N = len(t_len)
+    r = np.tile(np.arange(S, dtype=np.int32), (N, T, 1))
+    for n in range(N):
+        Tn, Un = int(t_len[n]), int(u_len[n])
+        P = max(0, Un - S + 1)
+        t = np.arange(Tn)
+        p = (t * P) // max(Tn - 1, 1)
+        r[n, :Tn] = (p[:, None] + np.arange(S)[None, :]).astype(np.int32)
+    return r
+
+
+def test_full_size_stress_sampled_outputs():
+    b = make_batch("stress", seed=0)
+    S = b.wl.S
+    _RUNS.clear()
+    say(f"[full] stress sampled: N={b.N} T={b.T} U={b.U} V={b.V}")
+    batch = make_dev_batch(b)
+    rng = np.random.default_rng(123)
+    picks = [(n, int(t)) for n in (0, b.N - 1) for t in rng.integers(0, b.t_len[n], size=3)]
+    # trivial joiner log-probs (Eqs. (1)-(2), (5)-(6)) on sampled frames
+    s = P.rnnt_simple_loss(batch, b.V, dev_f32(b.am), dev_f32(b.lm), want_logprobs=True)
+    torch.cuda.synchronize()
+    px, py = host(s["px"]), host(s["py"])
+    del s
+    for n, t in picks:
+        Un = int(b.u_len[n])
+        _, opx, opy = O.trivial_joiner_logprobs(b.am[n:n + 1, t:t + 1], b.lm[n:n + 1], b.symbols[n:n + 1],
+                                                np.array([1]), np.array([Un]), b.wl.blank)
+        assert_close(f"px[{n},{t}]", px[n, t, :Un + 1], opx[0, 0, :Un + 1], atol=5e-5)
+        assert_close(f"py[{n},{t}]", py[n, t, :Un + 1], opy[0, 0, :Un + 1], atol=5e-5)
+    # pruned joiner (full size, bf16 inputs) with fixed valid bounds, on sampled frames
+    ranges = _fixed_bounds(b.t_len, b.u_len, b.T, S)
+    ranges_valid(ranges, b.t_len, b.u_len, S)
+    bf = True
+    jo = P.rnnt_pruned_joiner(batch, S, dev_joiner(b.enc, bf), dev_joiner(b.dec, bf), dev_joiner(b.W, bf),
+                              dev_joiner(b.bias, bf), dev_i32(ranges), keep_logits=True)
+    torch.cuda.synchronize()
+    jpx, jpy, jlse = host(jo["px"]), host(jo["py"]), host(jo["lse"])
+    for n, t in picks:
+        sl = (slice(n, n + 1), slice(t, t + 1))
+        opx, opy, olse = O.pruned_joiner_logprobs(b.enc[sl], b.dec[n:n + 1], b.W, b.bias, ranges[sl],
+                                                  b.symbols[n:n + 1], np.array([1]), b.u_len[n:n + 1],
+                                                  b.wl.blank)
+        assert_close(f"joiner px[{n},{t}]", jpx[n, t], opx[0, 0], atol=2e-2)
+        assert_close(f"joiner py[{n},{t}]", jpy[n, t], opy[0, 0], atol=2e-2)
+        assert_close(f"joiner lse[{n},{t}]", jlse[n, t], olse[0, 0], atol=2e-2, rtol=2e-2)
+        lg = O.pruned_joiner_logits(b.enc[sl], b.dec[n:n + 1], b.W, b.bias, ranges[sl], np.array([1]),
+                                    b.u_len[n:n + 1])
+        present = ~np.isnan(lg[0, 0, :, 0])
+        assert_close(f"logits[{n},{t}]", host(jo["logits"][n, t])[present], lg[0, 0][present], atol=2e-2)

@@ -13,8 +13,8 @@ import torch
 
 import oracle as O
 import paper_2206_13236_amd as P
-from gpu_common import (DEV, assert_close, dev_f32, dev_i32, dev_joiner, grad_atol, host, loss_rtol,
-                        make_dev_batch, say)
+from gpu_common import (DEV, assert_close, check_step, dev_f32, dev_i32, dev_joiner, grad_atol, host,
+                        loss_rtol, make_dev_batch, oracle_step, run_step, say)
 from workloads import make_batch
 
 pytestmark = pytest.mark.gpu
@@ -175,71 +175,22 @@ def test_pruned_joiner_backward(name, stored):
         assert_close("logits_grad", host(out["logits_grad"]), ref["logits_grad"], atol=1e-5)
 
 
-def _near_tie_utterances(gx, gy, t_len, u_len, S, delta=2e-5):
-    """Utterances with a frame whose two best window scores (Eq. (8)) are within delta.
-
-    End to end, the GPU scores come from its own fp32 occupations, which agree
-    with the oracle's to ~1e-6; where two windows score the same to that
-    precision (typically several windows that all retain the whole mass,
-    score 1.0), either choice is correct and the bounds are not unique.
-    """
-    amb = set()
-    for n in range(len(t_len)):
-        sc = O.pruning_window_scores(gx[n], gy[n], t_len[n], u_len[n], S).astype(np.float64)
-        if sc.shape[1] < 2:
-            continue
-        top2 = np.sort(sc, axis=1)[:, -2:]
-        if np.any(top2[:, 1] - top2[:, 0] <= delta):
-            amb.add(n)
-    return amb
-
-
-def _ranges_valid(r, t_len, u_len, S):
-    for n in range(len(t_len)):
-        Tn, Un = int(t_len[n]), int(u_len[n])
-        p = r[n, :Tn, 0]
-        P = max(0, Un - S + 1)
-        assert np.array_equal(r[n, :Tn], p[:, None] + np.arange(S)[None, :])
-        assert np.all(r[n, Tn:] == np.arange(S))
-        assert p[0] == 0 and p[-1] == min(P, (S - 1) * (Tn - 1))
-        assert np.all(np.diff(p) >= 0) and np.all(np.diff(p) < S) and np.all((p >= 0) & (p <= P))
-
-
 @pytest.mark.parametrize("name", list(CASES))
 def test_end_to_end(name):
-    o = _oracle(name)
-    b = o["b"]
-    bf = b.wl.joiner_dtype == "bf16"
-    S = o["S"]
+    b = _case(name)
+    S = b.wl.S
     say(f"[e2e] {name}")
-    # the oracle end-to-end with the paper's weights: 0.5 * simple + pruned
-    sc_s = np.full(b.N, 0.5)
-    s1 = O.simple_stage(b.am, b.lm, b.symbols, b.t_len, b.u_len, b.wl.blank, scale=sc_s)
-    ranges = O.prune_ranges(s1["gx"], s1["gy"], b.t_len, b.u_len, S)
-    st = O.pruned_stage(b.enc, b.dec, b.W, b.bias, ranges, b.symbols, b.t_len, b.u_len, b.wl.blank)
-    batch = make_dev_batch(b)
-    step = P.PrunedRnntLoss(S, simple_scale=0.5)
-    out = step.step(batch, dev_f32(b.am), dev_f32(b.lm), dev_joiner(b.enc, bf), dev_joiner(b.dec, bf),
-                    dev_joiner(b.W, bf), dev_joiner(b.bias, bf))
-    torch.cuda.synchronize()
-    # stage 1-2 outputs are unique: compare all of them
-    assert_close("simple_loss", host(out["simple_loss"]), s1["loss"], rtol=1e-5)
-    assert_close("am_grad", host(out["am_grad"]), s1["am_grad"], atol=1e-4)
-    assert_close("lm_grad", host(out["lm_grad"]), s1["lm_grad"], atol=1e-4)
-    # bounds: exact where the argmax is unique, valid everywhere
-    got_r = out["ranges"].cpu().numpy()
-    _ranges_valid(got_r, b.t_len, b.u_len, S)
-    amb = _near_tie_utterances(s1["gx"], s1["gy"], b.t_len, b.u_len, S)
-    keep = [n for n in range(b.N) if n not in amb]
-    say(f"  near-tie utterances {sorted(amb)}; compared exactly: {keep}")
-    for n in keep:
-        assert np.array_equal(got_r[n], ranges[n]), f"utterance {n}: ranges differ without a near tie"
-        assert_close(f"pruned_loss[{n}]", host(out["pruned_loss"])[n], st["loss"][n], rtol=loss_rtol(bf))
-        for k in ("enc_grad", "dec_grad"):
-            assert_close(f"{k}[{n}]", host(out[k])[n], st[k][n], atol=grad_atol(st[k], bf))
-    if not amb:
-        for k in ("W_grad", "bias_grad"):
-            assert_close(k, host(out[k]), st[k], atol=grad_atol(st[k], bf, param=True))
+    out = run_step(b, S)
+    amb = check_step(out, oracle_step(b, S), b, S)
+    say(f"  near-tie utterances {sorted(amb)}")
+
+
+def test_end_to_end_recomputed_logits():
+    # the backward without the stored logits recomputes them (one chunk of rows at a time)
+    b = _case("small_f32")
+    say("[e2e] small_f32 keep_logits=False")
+    out = run_step(b, b.wl.S, keep_logits=False)
+    check_step(out, oracle_step(b, b.wl.S), b, b.wl.S)
 
 
 def test_deterministic_repeat():
