@@ -87,7 +87,6 @@ struct SimpleWs {
   double* alpha;
   double* beta;
   double* Lutt;
-  double* dummy;
   float* Wt;
   double* ry;
   double* cpx;
@@ -111,7 +110,6 @@ SimpleWs simple_layout(void* base, int N, int T, int U, int V) {
   w.alpha = c.take<double>(L);
   w.beta = c.take<double>(L);
   w.Lutt = c.take<double>((size_t)N);
-  w.dummy = c.take<double>((size_t)N * 2 * 1024);
   w.Wt =c.take<float>(NT * ldw_of(U));
   w.ry = c.take<double>(NT);
   w.cpx = c.take<double>((size_t)N * lattice_colblocks(T) * (U + 1));
@@ -247,7 +245,6 @@ int rnnt_simple_loss(const rnnt_batch* batch, int32_t V, const float* am, const 
   a.alpha = w.alpha;
   a.beta = w.beta;
   a.Lutt = w.Lutt;
-  a.dummy = w.dummy;
   a.loss = loss;
   a.gx = px_occ;
   a.gy = py_occ;
@@ -332,7 +329,6 @@ size_t rnnt_pruned_loss_workspace_size(int32_t N, int32_t T, int32_t S) {
   c.take<double>((size_t)N * T * S);
   c.take<double>((size_t)N * T * S);
   c.take<double>((size_t)N);
-  c.take<double>((size_t)N * 2 * 64);
   return c.off;
 }
 
@@ -359,7 +355,6 @@ int rnnt_pruned_loss(const rnnt_batch* batch, int32_t S, const float* px, const 
   a.alpha = c.take<double>((size_t)batch->N * batch->T * S);
   a.beta = c.take<double>((size_t)batch->N * batch->T * S);
   a.Lutt = c.take<double>((size_t)batch->N);
-  a.dummy = c.take<double>((size_t)batch->N * 2 * 64);
   a.loss = loss;
   a.gx = px_occ;
   a.gy = py_occ;

@@ -49,9 +49,10 @@ DEV void band_frame(const BandView& v, int t, int& e, int& ns) {
 // The step loops below are branch-free: frame switches are selects, the
 // geometry of the lane's following frame is re-read from LDS every step (and
 // only used at the next switch), the values of the next node are prefetched
-// every step, and lanes without a node store into a per-lane dummy slot.
-// Divergent branches with LDS reads would make every step wait for them.
-DEV void band_alpha(const BandView& v, double* __restrict__ alpha, double* __restrict__ dummy, int lane) {
+// every step, and lanes without a node store to kOob (a dropped buffer
+// store). Divergent branches with LDS reads would make every step wait for
+// them.
+DEV void band_alpha(const BandView& v, Rsrc alpha, int lane) {
   const int D = v.Tn + v.Un, S = v.S;
   int t = lane, e, ns;
   band_frame(v, t, e, ns);
@@ -76,8 +77,7 @@ DEV void band_alpha(const BandView& v, double* __restrict__ alpha, double* __res
     const double hin = (t == 0) ? kNegInfD : hin0;
     const double vin = (s == 0) ? kNegInfD : vout;
     const double al = (d == 0) ? 0.0 : log2add(hin, vin);
-    double* dst = act ? alpha + k : dummy + lane;
-    *dst = al;
+    buf_store_f64(alpha, act ? (uint32_t)k * 8u : kOob, al);
     hout = act ? al + y2 : kNegInfD;
     vout = act ? al + x2 : kNegInfD;
     // next node: (t, s+1) while the frame lasts, else the first node of frame t+64
@@ -87,7 +87,7 @@ DEV void band_alpha(const BandView& v, double* __restrict__ alpha, double* __res
   }
 }
 
-DEV void band_beta(const BandView& v, double* __restrict__ beta, double* __restrict__ dummy, int lane) {
+DEV void band_beta(const BandView& v, Rsrc beta, int lane) {
   const int D = v.Tn + v.Un, S = v.S;
   // this lane's frames in descending order: the largest t = lane (mod 64) below Tn
   int t = (lane < v.Tn) ? lane + 64 * ((v.Tn - 1 - lane) / 64) : -1;
@@ -115,8 +115,7 @@ DEV void band_beta(const BandView& v, double* __restrict__ beta, double* __restr
     const double hin = (t == v.Tn - 1) ? ((e - t + s == v.Un) ? 0.0 : kNegInfD) : hin0;
     const double vin = (s + 1 < ns) ? bout : kNegInfD;
     const double be = log2add(y2 + hin, x2 + vin);
-    double* dst = act ? beta + k : dummy + lane;
-    *dst = be;
+    buf_store_f64(beta, act ? (uint32_t)k * 8u : kOob, be);
     bout = act ? be : kNegInfD;
     // next node: (t, s-1) while the frame lasts, else the top node of frame t-64
     kn = act ? ((s > 0) ? k - 1 : (tn >= 0 ? tn * S + nsn - 1 : 0)) : kn;
@@ -150,12 +149,11 @@ __global__ __launch_bounds__(kBandThreads) void band_fb_kernel(BandArgs a) {
   v.Tn = Tn;
   v.Un = Un;
   v.S = S;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // uniform: the resources stay scalar
   double* alpha = a.alpha + base;
-  double* beta = a.beta + base;
-  double* dummy = a.dummy + ((size_t)n * 2 + wave) * 64;
-  if (wave == 0) band_alpha(v, alpha, dummy, lane);
-  else band_beta(v, beta, dummy, lane);
+  if (wave == 0) band_alpha(v, make_rsrc(alpha, (size_t)T * S * sizeof(double)), lane);
+  else band_beta(v, make_rsrc(a.beta + base, (size_t)T * S * sizeof(double)), lane);
   __syncthreads();
   if (threadIdx.x == 0) {
     const int se = Un - P[Tn - 1];

@@ -44,6 +44,24 @@ DEV int symbol_at(const BatchDev& b, int n, int u, int V, bool& ok) {
   return y;
 }
 
+// Buffer resources. A buffer access whose byte offset lies at or past the
+// resource's size reads zeros (loads) or is dropped (stores), so a lane with
+// nothing to load or store passes kOob instead of branching. Offsets are
+// 32-bit: every array accessed this way is below 2^31 bytes.
+using Rsrc = __amdgpu_buffer_rsrc_t;
+constexpr uint32_t kOob = 0x80000000u;
+
+DEV Rsrc make_rsrc(const void* p, size_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)(uint32_t)bytes, 0x00020000);
+}
+DEV float buf_load_f32(Rsrc r, uint32_t off) {
+  return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, (int)off, 0, 0));
+}
+DEV void buf_store_f64(Rsrc r, uint32_t off, double v) {
+  typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+  __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2_t, v), r, (int)off, 0, 0);
+}
+
 // log2(2^a + 2^b) for log2-domain values held in fp64. The large-magnitude
 // additions stay in fp64; only the bounded correction log2(1 + 2^-|a-b|),
 // which lies in [0, 1], goes through the fp32 hardware exp2/log2. NaN in either

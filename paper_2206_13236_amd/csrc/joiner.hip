@@ -57,20 +57,14 @@ DEV float ld_in(const float* p, size_t i) { return p[i]; }
 DEV float ld_in(const uint16_t* p, size_t i) { return bf2f(p[i]); }
 
 // ---------------------------------------------------------------------------
-// Operand loads through buffer resources. A buffer load whose byte offset
-// lies past the resource's size returns zeros, so masked-out lanes (rows
-// past the end, absent slots, k beyond K) load from kOob instead of taking a
-// divergent branch; the loads of a K-step then issue back to back. Every
-// operand array is below 2^31 bytes (checked by the entry points).
+// Operand loads through buffer resources (make_rsrc, kOob: see common.h). A
+// masked-out lane (row past the end, absent slot, k beyond K) loads from kOob
+// and reads zeros instead of taking a divergent branch, so the loads of a
+// K-step issue back to back. Every operand array is below 2^31 bytes
+// (checked by the entry points).
 // ---------------------------------------------------------------------------
-using Rsrc = __amdgpu_buffer_rsrc_t;
-constexpr uint32_t kOob = 0x80000000u;
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-
-DEV Rsrc make_rsrc(const void* p, size_t bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)(uint32_t)bytes, 0x00020000);
-}
 
 template <int W>
 DEV void buf_words(Rsrc r, uint32_t off, uint32_t* w) {

@@ -24,7 +24,6 @@ struct SimpleArgs {
   double* alpha;       // ws [N, T, U+1], log2 domain
   double* beta;        // ws [N, T, U+1], log2 domain
   double* Lutt;        // ws [N]: total log2-prob (NaN for an invalid utterance)
-  double* dummy;       // ws [N, 2, 1024]: store target of lanes outside the lattice
   float* loss;         // [N]
   float* gx;           // [N, T, U+1]
   float* gy;
@@ -114,7 +113,6 @@ struct BandArgs {
   double* alpha;       // ws [N, T, S] log2 domain
   double* beta;
   double* Lutt;        // ws [N]: total log2-prob (NaN for an invalid utterance)
-  double* dummy;       // ws [N, 2, 64]: store target of lanes without a node
   float* loss;
   float* gx;           // [N, T, S] or null
   float* gy;

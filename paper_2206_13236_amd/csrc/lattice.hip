@@ -29,93 +29,113 @@ namespace {
 
 constexpr int kOccFrames = 16;  // frames (waves) per workgroup of the occupation kernel
 
-// The recursion loops are kept free of branches: loads always read a valid
-// (clamped) address and select their value, and lanes whose node lies outside
-// the lattice store into a per-lane dummy slot. Conditional memory operations
-// would otherwise make the compiler wait for every outstanding load and store
-// at each step.
-template <int R, int P>
-DEV void lattice_load(const float* __restrict__ px, const float* __restrict__ py, int d, int lane, int Tn,
-                      int Un, int U1, float (&x)[R], float (&y)[R]) {
+// The recursion loops are kept free of branches and of 64-bit address
+// arithmetic: px, py and alpha/beta of the utterance are buffer resources,
+// a node's element offset is d*(U+1) + u*(1 - (U+1)) (one add per step), and
+// lanes whose node lies outside the lattice load from / store to kOob (reads
+// 0, store dropped). Conditional memory operations would otherwise make the
+// compiler wait for every outstanding load and store at each step.
+struct LatView {
+  Rsrc px, py, out;  // px, py [T, U+1] f32 and alpha or beta [T, U+1] f64 of the utterance
+  int Tn, Un, U1;
+};
+
+template <int R>
+DEV void lattice_load(const LatView& v, int d, const int (&rbase)[R], const bool (&rok)[R], int lane,
+                      float (&x)[R], float (&y)[R]) {
+  const int dU = d * v.U1;
 #pragma unroll
   for (int r = 0; r < R; ++r) {
-    const int u = lane * R + r, t = d - u;
-    const bool act = (t >= 0) && (t < Tn) && (u <= Un);
-    // inactive lanes load element 0; their value is discarded at use
-    const size_t idx = act ? (size_t)t * U1 + u : 0;
-    x[r] = px[idx];
-    y[r] = py[idx];
+    const int t = d - (lane * R + r);
+    const bool act = rok[r] && (unsigned)t < (unsigned)v.Tn;
+    const uint32_t off = act ? (uint32_t)(dU + rbase[r]) * 4u : kOob;
+    x[r] = buf_load_f32(v.px, off);
+    y[r] = buf_load_f32(v.py, off);
   }
 }
 
 template <int R, int P>
-DEV void alpha_pass(const float* __restrict__ px, const float* __restrict__ py, double* __restrict__ alpha,
-                    double* __restrict__ dummy, int Tn, int Un, int U1, int lane) {
-  const int D = Tn + Un;  // diagonals 0 .. Tn-1+Un (the loop may run up to P-1 idle steps past them)
+DEV void alpha_pass(const LatView& v, int lane) {
+  const int D = v.Tn + v.Un;  // diagonals 0 .. Tn-1+Un (the loop may run up to P-1 idle steps past them)
+  int rbase[R];
+  bool rok[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const int u = lane * R + r;
+    rbase[r] = u * (1 - v.U1);
+    rok[r] = u <= v.Un;
+  }
   double hout[R], vout[R];
 #pragma unroll
   for (int r = 0; r < R; ++r) hout[r] = vout[r] = kNegInfD;
   float xr[P][R], yr[P][R];
 #pragma unroll
-  for (int k = 0; k < P; ++k) lattice_load<R, P>(px, py, k, lane, Tn, Un, U1, xr[k], yr[k]);
+  for (int k = 0; k < P; ++k) lattice_load<R>(v, k, rbase, rok, lane, xr[k], yr[k]);
   for (int d0 = 0; d0 < D; d0 += P) {
 #pragma unroll
     for (int k = 0; k < P; ++k) {
       const int d = d0 + k;
+      const int dU = d * v.U1;
       const double vfirst = dpp_move_d<kDppWaveShr1>(vout[R - 1], kNegInfD);
       double nh[R], nv[R];
 #pragma unroll
       for (int r = 0; r < R; ++r) {
-        const int u = lane * R + r, t = d - u;
-        const bool act = (t >= 0) && (t < Tn) && (u <= Un);
+        const int t = d - (lane * R + r);
+        const bool act = rok[r] && (unsigned)t < (unsigned)v.Tn;
         const double vin = (r == 0) ? vfirst : vout[r - 1];
         const double al = (d == 0) ? 0.0 : log2add(hout[r], vin);
         nh[r] = act ? al + (double)yr[k][r] * kLog2e : kNegInfD;
         nv[r] = act ? al + (double)xr[k][r] * kLog2e : kNegInfD;
-        double* dst = act ? alpha + (size_t)t * U1 + u : dummy + lane * R + r;
-        *dst = al;
+        buf_store_f64(v.out, act ? (uint32_t)(dU + rbase[r]) * 8u : kOob, al);
       }
 #pragma unroll
       for (int r = 0; r < R; ++r) {
         hout[r] = nh[r];
         vout[r] = nv[r];
       }
-      lattice_load<R, P>(px, py, d + P, lane, Tn, Un, U1, xr[k], yr[k]);
+      lattice_load<R>(v, d + P, rbase, rok, lane, xr[k], yr[k]);
     }
   }
 }
 
 template <int R, int P>
-DEV void beta_pass(const float* __restrict__ px, const float* __restrict__ py, double* __restrict__ beta,
-                   double* __restrict__ dummy, int Tn, int Un, int U1, int lane) {
-  const int D = Tn + Un;
+DEV void beta_pass(const LatView& v, int lane) {
+  const int D = v.Tn + v.Un;
+  int rbase[R];
+  bool rok[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const int u = lane * R + r;
+    rbase[r] = u * (1 - v.U1);
+    rok[r] = u <= v.Un;
+  }
   // beta of my rows on the previous (higher) diagonal; the virtual node
   // (Tn, Un) after the final blank has beta = 0.
   double bprev[R];
 #pragma unroll
-  for (int r = 0; r < R; ++r) bprev[r] = (lane * R + r == Un) ? 0.0 : kNegInfD;
+  for (int r = 0; r < R; ++r) bprev[r] = (lane * R + r == v.Un) ? 0.0 : kNegInfD;
   float xr[P][R], yr[P][R];
 #pragma unroll
-  for (int k = 0; k < P; ++k) lattice_load<R, P>(px, py, D - 1 - k, lane, Tn, Un, U1, xr[k], yr[k]);
+  for (int k = 0; k < P; ++k) lattice_load<R>(v, D - 1 - k, rbase, rok, lane, xr[k], yr[k]);
   for (int d0 = D - 1; d0 >= 0; d0 -= P) {
 #pragma unroll
     for (int k = 0; k < P; ++k) {
       const int d = d0 - k;
+      const int dU = d * v.U1;
       const double vlast = dpp_move_d<kDppWaveShl1>(bprev[0], kNegInfD);
       double nb[R];
 #pragma unroll
       for (int r = 0; r < R; ++r) {
-        const int u = lane * R + r, t = d - u;
-        const bool act = (t >= 0) && (t < Tn) && (u <= Un);
+        const int t = d - (lane * R + r);
+        const bool act = rok[r] && (unsigned)t < (unsigned)v.Tn;
         const double vin = (r == R - 1) ? vlast : bprev[r + 1];
         const double be = log2add((double)yr[k][r] * kLog2e + bprev[r], (double)xr[k][r] * kLog2e + vin);
         nb[r] = act ? be : kNegInfD;
-        double* dst = act ? beta + (size_t)t * U1 + u : dummy + lane * R + r;
-        *dst = be;
+        buf_store_f64(v.out, act ? (uint32_t)(dU + rbase[r]) * 8u : kOob, be);
       }
 #pragma unroll
       for (int r = 0; r < R; ++r) bprev[r] = nb[r];
-      lattice_load<R, P>(px, py, d - P, lane, Tn, Un, U1, xr[k], yr[k]);
+      lattice_load<R>(v, d - P, rbase, rok, lane, xr[k], yr[k]);
     }
   }
 }
@@ -123,24 +143,32 @@ DEV void beta_pass(const float* __restrict__ px, const float* __restrict__ py, d
 template <int R, int P>
 __global__ __launch_bounds__(128) void lattice_fb_kernel(SimpleArgs a) {
   const int n = blockIdx.x;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: the resources stay scalar
   const int T = a.b.T, U1 = a.b.U + 1;
   int Tn, Un;
   const bool ok = utt_dims(a.b, n, Tn, Un);
   const size_t base = (size_t)n * T * U1;
-  const float* px = a.px + base;
-  const float* py = a.py + base;
-  double* alpha = a.alpha + base;
-  double* beta = a.beta + base;
-  double* dummy = a.dummy + ((size_t)n * 2 + wave) * 64 * R;
-  if (wave == 0) alpha_pass<R, P>(px, py, alpha, dummy, Tn, Un, U1, lane);
-  else beta_pass<R, P>(px, py, beta, dummy, Tn, Un, U1, lane);
+  const size_t cells = (size_t)T * U1;
+  LatView v;
+  v.px = make_rsrc(a.px + base, cells * sizeof(float));
+  v.py = make_rsrc(a.py + base, cells * sizeof(float));
+  v.Tn = Tn;
+  v.Un = Un;
+  v.U1 = U1;
+  if (wave == 0) {
+    v.out = make_rsrc(a.alpha + base, cells * sizeof(double));
+    alpha_pass<R, P>(v, lane);
+  } else {
+    v.out = make_rsrc(a.beta + base, cells * sizeof(double));
+    beta_pass<R, P>(v, lane);
+  }
   __syncthreads();
   if (tid == 0) {
     // symbols outside [0, V) make the utterance invalid
     bool sok = true;
     for (int u = 0; u < Un; ++u) symbol_at(a.b, n, u, a.V, sok);
-    const double L = alpha[(size_t)(Tn - 1) * U1 + Un] + (double)py[(size_t)(Tn - 1) * U1 + Un] * kLog2e;
+    const double L = a.alpha[base + (size_t)(Tn - 1) * U1 + Un] + (double)a.py[base + (size_t)(Tn - 1) * U1 + Un] * kLog2e;
     const double L2 = (ok && sok) ? L : __builtin_nan("");
     a.Lutt[n] = L2;
     a.loss[n] = (L2 == L2) ? (float)(-L2 * kLn2) : __builtin_nanf("");
