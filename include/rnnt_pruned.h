@@ -8,6 +8,11 @@
  *                              full-lattice recursion (Sec. 2, Eqs. (1)-(4));
  *                              yields the occupation counts of Sec. 3.2.2 and,
  *                              optionally, the gradients w.r.t. am and lm.
+ *      rnnt_simple_loss_backward
+ *                              those gradients later, from the state the
+ *                              forward call left in its workspace (so that a
+ *                              caller can run them on a second stream while
+ *                              the pruned stages proceed).
  *   2. rnnt_prune_ranges       locally optimal pruning bounds, Eq. (8), made
  *                              consistent with Eqs. (9)-(10) (Sec. 3.2.2).
  *   3. rnnt_pruned_joiner      the full non-linear joiner evaluated only at the
@@ -111,13 +116,30 @@ size_t rnnt_simple_loss_workspace_size(int32_t N, int32_t T, int32_t U, int32_t 
  *                       sum_n scale[n] * loss[n].
  *   scale  [N] fp32, nullable (all ones); only read when a gradient is asked.
  * workspace: device buffer of at least rnnt_simple_loss_workspace_size() bytes,
- *   256-byte aligned.
+ *   256-byte aligned. On return (in stream order) it holds what
+ *   rnnt_simple_loss_backward needs.
  */
 int rnnt_simple_loss(const rnnt_batch* batch, int32_t V,
                      const float* am, const float* lm, const float* scale,
                      float* loss, float* px_occ, float* py_occ,
                      float* px, float* py, float* am_grad, float* lm_grad,
                      void* workspace, size_t workspace_bytes, void* stream);
+
+/* Gradients of sum_n scale[n] * simple_loss[n] w.r.t. am and lm (the
+ * log-softmax backward through Eq. (5), two contractions of the forward's
+ * shape), computed from the state a preceding rnnt_simple_loss call left in
+ * `workspace`: the same batch, V, am, lm, its px_occ output, and the same
+ * workspace, unmodified since, with that call ordered before this one
+ * (same stream, or an event). Results equal those of the forward call asked
+ * for the gradients directly.
+ *
+ * px_occ [N, T, U+1]: the forward's px_occ output (required).
+ * am_grad [N, T, V], lm_grad [N, U+1, V] fp32: outputs (at least one).
+ */
+int rnnt_simple_loss_backward(const rnnt_batch* batch, int32_t V,
+                              const float* am, const float* lm, const float* scale,
+                              const float* px_occ, float* am_grad, float* lm_grad,
+                              void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------ */
 /* Stage 3: pruning bounds (Sec. 3.2.2)                                      */

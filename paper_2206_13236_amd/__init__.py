@@ -18,7 +18,8 @@ from ._native import (RNNT_BF16, RNNT_EHIP, RNNT_EINVAL, RNNT_EUNSUPPORTED, RNNT
                       RNNT_F32, RNNT_OK, RnntBatch, RnntError, check, lib)
 
 __all__ = [
-    "Batch", "RnntError", "rnnt_simple_loss", "rnnt_prune_ranges", "rnnt_pruned_joiner",
+    "Batch", "RnntError", "rnnt_simple_loss", "rnnt_simple_loss_backward", "rnnt_prune_ranges",
+    "rnnt_pruned_joiner", "pruned_rnnt_loss",
     "rnnt_pruned_loss", "rnnt_pruned_joiner_backward", "simple_loss_workspace_size",
     "pruned_joiner_workspace_size", "pruned_loss_workspace_size",
     "pruned_joiner_backward_workspace_size", "PrunedRnntLoss", "RNNT_F32", "RNNT_BF16",
@@ -140,6 +141,26 @@ def rnnt_simple_loss(batch: Batch, V: int, am: torch.Tensor, lm: torch.Tensor,
             "am_grad": am_grad, "lm_grad": lm_grad}
 
 
+def rnnt_simple_loss_backward(batch: Batch, V: int, am: torch.Tensor, lm: torch.Tensor, px_occ: torch.Tensor,
+                              workspace: torch.Tensor, scale: Optional[torch.Tensor] = None, am_grad=None,
+                              lm_grad=None, stream=None) -> dict:
+    """d am, d lm from the state a preceding rnnt_simple_loss call left in ``workspace``."""
+    N, T, U = batch.N, batch.T, batch.U
+    dev = batch.device
+    _need(am, "am", torch.float32, (N, T, V))
+    _need(lm, "lm", torch.float32, (N, U + 1, V))
+    _need(px_occ, "px_occ", torch.float32, (N, T, U + 1))
+    if scale is not None:
+        _need(scale, "scale", torch.float32, (N,))
+    f32 = dict(dtype=torch.float32, device=dev)
+    am_grad = torch.empty(N, T, V, **f32) if am_grad is None else am_grad
+    lm_grad = torch.empty(N, U + 1, V, **f32) if lm_grad is None else lm_grad
+    ws = _ws(simple_loss_workspace_size(N, T, U, V), dev, workspace)
+    check(lib().rnnt_simple_loss_backward(batch.c, V, _p(am), _p(lm), _p(scale), _p(px_occ), _p(am_grad),
+                                          _p(lm_grad), _p(ws), ws.numel(), _stream(stream)))
+    return {"am_grad": am_grad, "lm_grad": lm_grad}
+
+
 def rnnt_prune_ranges(batch: Batch, S: int, px_occ: torch.Tensor, py_occ: torch.Tensor,
                       ranges: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
     N, T, U = batch.N, batch.T, batch.U
@@ -223,24 +244,36 @@ def rnnt_pruned_joiner_backward(batch: Batch, S: int, enc, dec, W, bias, ranges,
 
 
 class PrunedRnntLoss:
-    """The paper's training loss on one batch: pruned + simple_scale * simple (Sec. 3.3).
+    """The paper's training loss on one batch: pruned_scale * pruned + simple_scale * simple (Sec. 3.3).
 
-    Holds the intermediate tensors and one workspace between calls so that
+    Holds the intermediate tensors and two workspaces between calls, so that
     repeated steps on same-shaped batches allocate nothing new. ``step``
-    enqueues the whole path (simple loss and its gradients, pruning bounds,
-    pruned joiner, pruned recursion, joiner backward) on the current stream.
+    enqueues the whole path on the caller's stream: the simple loss and its
+    occupations, the pruning bounds, the pruned joiner, the pruned recursion
+    and the joiner backward. The simple loss's own gradients (two
+    contractions that only the caller needs) run on a second stream at the
+    default priority, forked after the joiner forward so that they overlap
+    the pruned recursion, which occupies one workgroup per utterance, and
+    joined back before ``step`` returns (in stream order).
+
+    With ``pruned_scale == 0`` (the warm-up of Sec. 4: the pruned part is
+    disabled until the simple loss gives useful bounds) the pruned stages are
+    skipped and their loss and gradients are zero.
+
     With ``keep_logits`` the pruned logits [N, T, S, V] are kept between the
     joiner's forward and backward (the method's own memory footprint);
     without it the backward recomputes them and holds one row chunk at a time.
     """
 
     def __init__(self, S: int, simple_scale: float = 0.5, pruned_scale: float = 1.0,
-                 keep_logits: bool = True):
+                 keep_logits: bool = True, overlap: bool = True):
         self.S = int(S)
         self.simple_scale = float(simple_scale)
         self.pruned_scale = float(pruned_scale)
         self.keep_logits = bool(keep_logits)
+        self.overlap = bool(overlap)
         self._cache = {}
+        self._side = {}
 
     def _buf(self, key, shape, dtype, device):
         t = self._cache.get(key)
@@ -249,46 +282,131 @@ class PrunedRnntLoss:
             self._cache[key] = t
         return t
 
-    def step(self, batch: Batch, am, lm, enc, dec, W, bias=None, stream=None) -> dict:
+    def _side_stream(self, device):
+        key = device.index if device.index is not None else torch.cuda.current_device()
+        if key not in self._side:
+            self._side[key] = (torch.cuda.Stream(device=device), torch.cuda.Event(), torch.cuda.Event())
+        return self._side[key]
+
+    def step(self, batch: Batch, am, lm, enc, dec, W, bias=None, stream=None, out=None) -> dict:
+        """Run one step; ``out`` optionally maps output names to caller-owned tensors."""
         N, T, U, S = batch.N, batch.T, batch.U, self.S
         V = int(am.shape[2])
         J = int(W.shape[0])
         dev = batch.device
         dt = _jdtype(W)
         f32 = torch.float32
-        ws_bytes = max(simple_loss_workspace_size(N, T, U, V),
-                       pruned_joiner_workspace_size(N, T, S, J, V, dt),
-                       pruned_loss_workspace_size(N, T, S),
-                       pruned_joiner_backward_workspace_size(N, T, U, S, J, V, dt))
-        ws = self._buf("ws", (ws_bytes,), torch.uint8, dev)
+        out = {} if out is None else out
+        main = torch.cuda.current_stream(dev) if stream is None else stream
+
+        def o(key, shape, dtype=f32):
+            t = out.get(key)
+            return t if t is not None else self._buf(key, shape, dtype, dev)
+
+        ws_s = self._buf("ws_simple", (simple_loss_workspace_size(N, T, U, V),), torch.uint8, dev)
+        ws_p = self._buf("ws_pruned", (max(pruned_joiner_workspace_size(N, T, S, J, V, dt),
+                                           pruned_loss_workspace_size(N, T, S),
+                                           pruned_joiner_backward_workspace_size(N, T, U, S, J, V, dt)),),
+                         torch.uint8, dev)
         ssc = self._buf("ssc", (N,), f32, dev)
         psc = self._buf("psc", (N,), f32, dev)
         if self._cache.get("scales") != (N, self.simple_scale, self.pruned_scale):
-            ssc.fill_(self.simple_scale)
-            psc.fill_(self.pruned_scale)
+            with torch.cuda.stream(main):
+                ssc.fill_(self.simple_scale)
+                psc.fill_(self.pruned_scale)
             self._cache["scales"] = (N, self.simple_scale, self.pruned_scale)
-        out = rnnt_simple_loss(
-            batch, V, am, lm, ssc, loss=self._buf("sl", (N,), f32, dev),
-            px_occ=self._buf("sgx", (N, T, U + 1), f32, dev), py_occ=self._buf("sgy", (N, T, U + 1), f32, dev),
-            am_grad=self._buf("dam", (N, T, V), f32, dev), lm_grad=self._buf("dlm", (N, U + 1, V), f32, dev),
-            workspace=ws, stream=stream)
-        ranges = rnnt_prune_ranges(batch, S, out["px_occ"], out["py_occ"],
-                                   ranges=self._buf("rng", (N, T, S), torch.int32, dev), stream=stream)
-        logits = self._buf("logits", (N, T, S, V), f32, dev) if self.keep_logits else None
-        jo = rnnt_pruned_joiner(batch, S, enc, dec, W, bias, ranges, px=self._buf("ppx", (N, T, S), f32, dev),
-                                py=self._buf("ppy", (N, T, S), f32, dev), lse=self._buf("lse", (N, T, S), f32, dev),
-                                logits=logits, workspace=ws, stream=stream)
-        pl = rnnt_pruned_loss(batch, S, jo["px"], jo["py"], ranges, loss=self._buf("pl", (N,), f32, dev),
-                              px_occ=self._buf("pgx", (N, T, S), f32, dev),
-                              py_occ=self._buf("pgy", (N, T, S), f32, dev), workspace=ws, stream=stream)
-        jb = rnnt_pruned_joiner_backward(
+        sim = rnnt_simple_loss(
+            batch, V, am, lm, ssc, loss=o("simple_loss", (N,)),
+            px_occ=o("simple_px_occ", (N, T, U + 1)), py_occ=o("simple_py_occ", (N, T, U + 1)),
+            workspace=ws_s, stream=main)
+        res = {"simple_loss": sim["loss"], "simple_px_occ": sim["px_occ"], "simple_py_occ": sim["py_occ"]}
+        am_grad, lm_grad = o("am_grad", (N, T, V)), o("lm_grad", (N, U + 1, V))
+        enc_grad, dec_grad = o("enc_grad", (N, T, J)), o("dec_grad", (N, U + 1, J))
+        W_grad, bias_grad = o("W_grad", (J, V)), o("bias_grad", (V,))
+        res.update(am_grad=am_grad, lm_grad=lm_grad, enc_grad=enc_grad, dec_grad=dec_grad, W_grad=W_grad,
+                   bias_grad=bias_grad)
+
+        def simple_backward(s):
+            rnnt_simple_loss_backward(batch, V, am, lm, sim["px_occ"], ws_s, scale=ssc, am_grad=am_grad,
+                                      lm_grad=lm_grad, stream=s)
+
+        if self.pruned_scale == 0.0:
+            # warm-up: the pruned part carries no weight and is not evaluated
+            simple_backward(main)
+            with torch.cuda.stream(main):
+                pl = o("pruned_loss", (N,))
+                for t in (pl, enc_grad, dec_grad, W_grad, bias_grad):
+                    t.zero_()
+            res["pruned_loss"] = pl
+            return res
+
+        ranges = rnnt_prune_ranges(batch, S, sim["px_occ"], sim["py_occ"], ranges=o("ranges", (N, T, S), torch.int32),
+                                   stream=main)
+        logits = o("logits", (N, T, S, V)) if self.keep_logits else None
+        jo = rnnt_pruned_joiner(batch, S, enc, dec, W, bias, ranges, px=o("px", (N, T, S)), py=o("py", (N, T, S)),
+                                lse=o("lse", (N, T, S)), logits=logits, workspace=ws_p, stream=main)
+        if self.overlap:
+            side, fork, join = self._side_stream(dev)
+            fork.record(main)
+            side.wait_event(fork)
+            simple_backward(side)
+            join.record(side)
+        else:
+            simple_backward(main)
+        pl = rnnt_pruned_loss(batch, S, jo["px"], jo["py"], ranges, loss=o("pruned_loss", (N,)),
+                              px_occ=o("pruned_px_occ", (N, T, S)), py_occ=o("pruned_py_occ", (N, T, S)),
+                              workspace=ws_p, stream=main)
+        rnnt_pruned_joiner_backward(
             batch, S, enc, dec, W, bias, ranges, jo["lse"], pl["px_occ"], pl["py_occ"], scale=psc,
-            enc_grad=self._buf("denc", (N, T, J), f32, dev), dec_grad=self._buf("ddec", (N, U + 1, J), f32, dev),
-            W_grad=self._buf("dW", (J, V), f32, dev), bias_grad=self._buf("db", (V,), f32, dev),
-            workspace=ws, stream=stream, logits=logits)
-        return {"simple_loss": out["loss"], "pruned_loss": pl["loss"], "ranges": ranges,
-                "am_grad": out["am_grad"], "lm_grad": out["lm_grad"], "enc_grad": jb["enc_grad"],
-                "dec_grad": jb["dec_grad"], "W_grad": jb["W_grad"], "bias_grad": jb["bias_grad"],
-                "simple_px_occ": out["px_occ"], "simple_py_occ": out["py_occ"],
-                "px": jo["px"], "py": jo["py"], "lse": jo["lse"],
-                "pruned_px_occ": pl["px_occ"], "pruned_py_occ": pl["py_occ"]}
+            enc_grad=enc_grad, dec_grad=dec_grad, W_grad=W_grad, bias_grad=bias_grad, workspace=ws_p,
+            stream=main, logits=logits)
+        if self.overlap:
+            main.wait_event(join)
+        res.update(pruned_loss=pl["loss"], ranges=ranges, px=jo["px"], py=jo["py"], lse=jo["lse"],
+                   pruned_px_occ=pl["px_occ"], pruned_py_occ=pl["py_occ"])
+        return res
+
+
+class _PrunedRnntFunction(torch.autograd.Function):
+    """Forward computes the loss and every gradient at once (the kernels are
+    fused forward-backward); backward scales the stored gradients."""
+
+    @staticmethod
+    def forward(ctx, am, lm, enc, dec, W, bias, module, batch, reduction):
+        N, T, U, V, J = batch.N, batch.T, batch.U, int(am.shape[2]), int(W.shape[0])
+        f32 = dict(dtype=torch.float32, device=am.device)
+        fresh = {"am_grad": torch.empty(N, T, V, **f32), "lm_grad": torch.empty(N, U + 1, V, **f32),
+                 "enc_grad": torch.empty(N, T, J, **f32), "dec_grad": torch.empty(N, U + 1, J, **f32),
+                 "W_grad": torch.empty(J, V, **f32), "bias_grad": torch.empty(V, **f32)}
+        r = module.step(batch, am, lm, enc, dec, W, bias, out=fresh)
+        per_utt = module.simple_scale * r["simple_loss"] + module.pruned_scale * r["pruned_loss"]
+        loss = per_utt.sum()
+        if reduction == "mean":
+            loss = loss / N
+        ctx.reduction = reduction
+        ctx.N = N
+        ctx.has_bias = bias is not None
+        ctx.dtypes = (enc.dtype, dec.dtype, W.dtype)
+        ctx.save_for_backward(fresh["am_grad"], fresh["lm_grad"], fresh["enc_grad"], fresh["dec_grad"],
+                              fresh["W_grad"], fresh["bias_grad"])
+        return loss
+
+    @staticmethod
+    def backward(ctx, g):
+        am_g, lm_g, enc_g, dec_g, W_g, b_g = ctx.saved_tensors
+        if ctx.reduction == "mean":
+            g = g / ctx.N
+        ed, dd, wd = ctx.dtypes
+        return (am_g * g, lm_g * g, (enc_g * g).to(ed), (dec_g * g).to(dd), (W_g * g).to(wd),
+                (b_g * g).to(wd) if ctx.has_bias else None, None, None, None)
+
+
+def pruned_rnnt_loss(am, lm, enc, dec, W, bias, batch: Batch, S: int, simple_scale: float = 0.5,
+                     pruned_scale: float = 1.0, reduction: str = "sum", module: Optional[PrunedRnntLoss] = None):
+    """Differentiable training loss: sum (or mean) over utterances of
+    simple_scale * simple_loss + pruned_scale * pruned_loss (Sec. 3.3)."""
+    if reduction not in ("sum", "mean"):
+        raise ValueError("reduction must be 'sum' or 'mean'")
+    if module is None:
+        module = PrunedRnntLoss(S, simple_scale=simple_scale, pruned_scale=pruned_scale)
+    return _PrunedRnntFunction.apply(am, lm, enc, dec, W, bias, module, batch, reduction)

@@ -42,6 +42,8 @@ SIGNATURES = {
     "rnnt_simple_loss": (c_int32, [POINTER(RnntBatch), c_int32, c_void_p, c_void_p, c_void_p,
                                    c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
                                    c_void_p, c_size_t, c_void_p]),
+    "rnnt_simple_loss_backward": (c_int32, [POINTER(RnntBatch), c_int32, c_void_p, c_void_p, c_void_p, c_void_p,
+                                            c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]),
     "rnnt_prune_ranges": (c_int32, [POINTER(RnntBatch), c_int32, c_void_p, c_void_p, c_void_p, c_void_p]),
     "rnnt_pruned_joiner_workspace_size": (c_size_t, [c_int32] * 6),
     "rnnt_pruned_joiner": (c_int32, [POINTER(RnntBatch), c_int32, c_int32, c_int32, c_int32,

@@ -122,6 +122,38 @@ SimpleWs simple_layout(void* base, int N, int T, int U, int V) {
   return w;
 }
 
+// Arguments shared by the simple loss's forward and backward entry points:
+// everything but the caller's outputs. The occupation kernel always leaves
+// the backward's state (W(t,u), row and column sums) in the workspace.
+SimpleArgs simple_args(const rnnt_batch* batch, int V, const float* am, const float* lm, const float* scale,
+                       const SimpleWs& w) {
+  SimpleArgs a{};
+  a.b = to_dev(batch);
+  a.V = V;
+  a.am = am;
+  a.lm = lm;
+  a.scale = scale;
+  a.m_a = w.m_a;
+  a.m_l = w.m_l;
+  a.Z = w.Z;
+  a.npart = w.npart;
+  a.nsplit = w.nsplit;
+  a.lpart = w.lpart;
+  a.lsplit = w.lsplit;
+  a.px = w.px;
+  a.py = w.py;
+  a.alpha = w.alpha;
+  a.beta = w.beta;
+  a.Lutt = w.Lutt;
+  a.Wt = w.Wt;
+  a.ldw = ldw_of(batch->U);
+  a.ry = w.ry;
+  a.cpx = w.cpx;
+  a.cpy = w.cpy;
+  a.ncolblk = lattice_colblocks(batch->T);
+  return a;
+}
+
 struct JoinerFwdWs {
   int* frame_off;
   int4* rowinfo;
@@ -227,41 +259,39 @@ int rnnt_simple_loss(const rnnt_batch* batch, int32_t V, const float* am, const 
   if (rc) return rc;
   const SimpleWs w = simple_layout(workspace, batch->N, batch->T, batch->U, V);
   hipStream_t s = static_cast<hipStream_t>(stream);
-  SimpleArgs a{};
-  a.b = to_dev(batch);
-  a.V = V;
-  a.am = am;
-  a.lm = lm;
-  a.scale = scale;
-  a.m_a = w.m_a;
-  a.m_l = w.m_l;
-  a.Z = w.Z;
-  a.npart = w.npart;
-  a.nsplit = w.nsplit;
-  a.lpart = w.lpart;
-  a.lsplit = w.lsplit;
-  a.px = px ? px : w.px;
-  a.py = py ? py : w.py;
-  a.alpha = w.alpha;
-  a.beta = w.beta;
-  a.Lutt = w.Lutt;
+  SimpleArgs a = simple_args(batch, V, am, lm, scale, w);
+  if (px) a.px = px;
+  if (py) a.py = py;
   a.loss = loss;
   a.gx = px_occ;
   a.gy = py_occ;
-  a.want_bwd = (am_grad || lm_grad) ? 1 : 0;
-  a.Wt = w.Wt;
-  a.ldw = ldw_of(batch->U);
-  a.ry = w.ry;
-  a.cpx = w.cpx;
-  a.cpy = w.cpy;
-  a.ncolblk = lattice_colblocks(batch->T);
   a.am_grad = am_grad;
   a.lm_grad = lm_grad;
   hipError_t e = launch_rowmax(a, s);
   if (e == hipSuccess) e = launch_normalizer(a, s);
   if (e == hipSuccess) e = launch_lattice(a, s);
-  if (e == hipSuccess && a.want_bwd) e = launch_simple_grads(a, s);
+  if (e == hipSuccess && (am_grad || lm_grad)) e = launch_simple_grads(a, s);
   return hip_status(e, "rnnt_simple_loss");
+}
+
+int rnnt_simple_loss_backward(const rnnt_batch* batch, int32_t V, const float* am, const float* lm,
+                              const float* scale, const float* px_occ, float* am_grad, float* lm_grad,
+                              void* workspace, size_t workspace_bytes, void* stream) {
+  int rc = check_batch(batch, true);
+  if (rc) return rc;
+  if (V < 1) return fail(RNNT_EINVAL, "V must be >= 1 (got %d)", V);
+  if (batch->blank < 0 || batch->blank >= V) return fail(RNNT_EINVAL, "blank = %d outside [0, V)", batch->blank);
+  if (!am || !lm || !px_occ) return fail(RNNT_EINVAL, "am, lm and px_occ are required");
+  if (!am_grad && !lm_grad) return fail(RNNT_EINVAL, "at least one of am_grad and lm_grad is required");
+  const SimpleWs need = simple_layout(nullptr, batch->N, batch->T, batch->U, V);
+  rc = check_ws(workspace, workspace_bytes, need.bytes);
+  if (rc) return rc;
+  const SimpleWs w = simple_layout(workspace, batch->N, batch->T, batch->U, V);
+  SimpleArgs a = simple_args(batch, V, am, lm, scale, w);
+  a.gx = const_cast<float*>(px_occ);  // read only by the gradient kernels
+  a.am_grad = am_grad;
+  a.lm_grad = lm_grad;
+  return hip_status(launch_simple_grads(a, static_cast<hipStream_t>(stream)), "rnnt_simple_loss_backward");
 }
 
 int rnnt_prune_ranges(const rnnt_batch* batch, int32_t S, const float* px_occ, const float* py_occ,

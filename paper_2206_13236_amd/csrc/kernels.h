@@ -27,8 +27,7 @@ struct SimpleArgs {
   float* loss;         // [N]
   float* gx;           // [N, T, U+1]
   float* gy;
-  int want_bwd;
-  float* Wt;           // ws [N, T, ldw]
+  float* Wt;           // ws [N, T, ldw]: W(t,u) for the gradient (always written)
   int ldw;
   double* ry;          // ws [N*T]      row sums of gy (fp64)
   double* cpx;         // ws [N, ncolblk, U+1]: column sums of gx over 16-frame blocks

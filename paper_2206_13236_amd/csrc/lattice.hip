@@ -229,13 +229,11 @@ __global__ __launch_bounds__(64 * kOccFrames) void lattice_occ_kernel(SimpleArgs
       const size_t idx = base + (size_t)t * U1 + u;
       a.gx[idx] = gxv;
       a.gy[idx] = gyv;
-      if (a.want_bwd) {
-        a.Wt[((size_t)n * T + t) * a.ldw + u] =
-            (frow && u <= Un) ? (gxv + gyv) * expf(mat + a.m_l[(size_t)n * U1 + u] - a.Z[idx]) : 0.f;
-      }
+      a.Wt[((size_t)n * T + t) * a.ldw + u] =
+          (frow && u <= Un) ? (gxv + gyv) * expf(mat + a.m_l[(size_t)n * U1 + u] - a.Z[idx]) : 0.f;
     }
     ry += (double)gyv;
-    if (a.want_bwd) {
+    {
       sx[wave][lane] = (double)gxv;
       sy[wave][lane] = (double)gyv;
       __syncthreads();
@@ -252,7 +250,7 @@ __global__ __launch_bounds__(64 * kOccFrames) void lattice_occ_kernel(SimpleArgs
       __syncthreads();
     }
   }
-  if (a.want_bwd && trow) {
+  if (trow) {
     if (lane < a.ldw - U1) a.Wt[((size_t)n * T + t) * a.ldw + U1 + lane] = 0.f;
     ry = wave_sum_d(ry);
     if (lane == 0) a.ry[(size_t)n * T + t] = ry;
