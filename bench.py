@@ -37,6 +37,31 @@ WORKLOAD_TEXT = {
 }
 
 
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "joiner_hbm_traffic_bpe.md")
+
+
+def _traffic(kernel: str, workload: str):
+    """HBM bytes per launch of `kernel` from the committed FETCH_SIZE / WRITE_SIZE
+    runs (scaled by the copy calibration), or None when they were not taken on
+    this workload or the kernel's sources changed since."""
+    import hashlib
+    import re
+    if workload != "bpe" or not os.path.exists(TRAFFIC_FILE):
+        return None
+    m = re.search(r"```json\n(.*?)```", open(TRAFFIC_FILE).read(), re.S)
+    if not m:
+        return None
+    rec = json.loads(m.group(1))
+    h = hashlib.sha256()
+    for f in rec["sources"]:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    k = rec["kernels"].get(kernel)
+    if h.hexdigest() != rec["sources_sha256"] or k is None:
+        return None
+    return int(1024 * (k["fetch_kib"] * rec["fetch_scale"] + k["write_kib"] * rec["write_scale"]))
+
+
 def _cpu_baseline(b, S, budget_s: float) -> dict:
     """The CPU oracle (as is) on the first utterances of the same batch, one thread."""
     import numpy as np
@@ -182,7 +207,8 @@ def main() -> int:
     achieved = per_launch_flops / (timed["avg_us"] * 1e-6) / 1e12
     dt = "bf16" if bf else "f32"
     roofline = {"kernel": dom, "bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_TFLOPS[dt],
-                "unit": "TFLOP/s", "frac": round(achieved / PEAK_TFLOPS[dt], 4), "traffic": None,
+                "unit": "TFLOP/s", "frac": round(achieved / PEAK_TFLOPS[dt], 4),
+                "traffic": _traffic(dom, args.workload),
                 "algorithmic_flops_per_launch": per_launch_flops, "avg_launch_us": timed["avg_us"],
                 "launches_timed": timed["launches"]}
 
