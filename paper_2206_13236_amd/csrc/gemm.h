@@ -149,7 +149,8 @@ struct MNCLoader {
   }
 };
 
-template <class Cfg>
+// MFMAs of the k-slices [K0, K1) of one LDS stage.
+template <class Cfg, int K0 = 0, int K1 = Cfg::BK>
 DEV void gemm_compute_stage(const typename Cfg::T* As, const typename Cfg::T* Bs,
                             floatx4 (&acc)[Cfg::FM][Cfg::FN]) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -157,7 +158,7 @@ DEV void gemm_compute_stage(const typename Cfg::T* As, const typename Cfg::T* Bs
   const typename Cfg::T* a_base = As + (wm * Cfg::WM + (lane & 15)) * Cfg::LDK + (lane >> 4) * Cfg::KV;
   const typename Cfg::T* b_base = Bs + (wn * Cfg::WN + (lane & 15)) * Cfg::LDK + (lane >> 4) * Cfg::KV;
 #pragma unroll
-  for (int kk = 0; kk < Cfg::BK; kk += Cfg::KSLICE) {
+  for (int kk = K0; kk < K1; kk += Cfg::KSLICE) {
     if constexpr (Cfg::BF16) {
       bf16x8 fa[Cfg::FM], fb[Cfg::FN];
 #pragma unroll
@@ -208,18 +209,25 @@ DEV void gemm_mainloop(const LA& la, const LB& lb, int k_begin, int k_end,
   la.put(ra, As0);
   lb.put(rb, Bs0);
   __syncthreads();
+  // The next stage is staged between the two halves of the current stage's
+  // MFMAs: its global loads have the first half to land, and its transforms
+  // and LDS stores can issue while the second half's MFMAs execute.
+  constexpr int KH = (Cfg::BK / Cfg::KSLICE) / 2 * Cfg::KSLICE;
   for (int kt = 0; kt < nk; ++kt) {
     const bool more = kt + 1 < nk;
     if (more) {
       la.fetch(k_begin + (kt + 1) * Cfg::BK, ra);
       lb.fetch(k_begin + (kt + 1) * Cfg::BK, rb);
     }
-    if (kt & 1) gemm_compute_stage<Cfg>(As1, Bs1, acc);
-    else gemm_compute_stage<Cfg>(As0, Bs0, acc);
+    const bool odd = kt & 1;
+    const typename Cfg::T* Ac = odd ? As1 : As0;
+    const typename Cfg::T* Bc = odd ? Bs1 : Bs0;
+    gemm_compute_stage<Cfg, 0, KH>(Ac, Bc, acc);
     if (more) {
-      if (kt & 1) { la.put(ra, As0); lb.put(rb, Bs0); }
-      else { la.put(ra, As1); lb.put(rb, Bs1); }
+      la.put(ra, odd ? As0 : As1);
+      lb.put(rb, odd ? Bs0 : Bs1);
     }
+    gemm_compute_stage<Cfg, KH, Cfg::BK>(Ac, Bc, acc);
     __syncthreads();
   }
 }

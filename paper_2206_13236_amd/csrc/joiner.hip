@@ -870,7 +870,7 @@ int joiner_bwd_chunk_rows(int N, int T, int S, int J, int V, int bf16) {
 
 int joiner_bwd_splits(int J, int V) {
   const int tiles = ((J + 127) / 128) * ((V + 127) / 128);
-  int s = (512 + tiles - 1) / tiles;
+  int s = (256 + tiles - 1) / tiles;
   if (s < 1) s = 1;
   if (s > 32) s = 32;
   return s;
