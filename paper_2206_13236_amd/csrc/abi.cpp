@@ -181,6 +181,7 @@ struct JoinerBwdWs {
   int4* rowinfo;
   void* dl;
   float* dpre;
+  void* hbuf;
   float* dw_part;
   float* db_part;
   int chunk_rows, splits, n_db_rows;
@@ -199,6 +200,8 @@ JoinerBwdWs joiner_bwd_layout(void* base, int N, int T, int S, int J, int V, int
   const size_t dl_elems = (size_t)w.chunk_rows * joiner_ldl(V);
   w.dl = bf16 ? (void*)c.take<uint16_t>(dl_elems) : (void*)c.take<float>(dl_elems);
   w.dpre = c.take<float>(M * J);
+  const size_t h_elems = (size_t)w.chunk_rows * J;
+  w.hbuf = bf16 ? (void*)c.take<uint16_t>(h_elems) : (void*)c.take<float>(h_elems);
   w.dw_part = c.take<float>((size_t)w.splits * J * V);
   w.db_part = c.take<float>((size_t)w.n_db_rows * V);
   w.bytes = c.off;
@@ -442,6 +445,7 @@ int rnnt_pruned_joiner_backward(const rnnt_batch* batch, int32_t S, int32_t J, i
   a.ldl = joiner_ldl(V);
   a.chunk_rows = w.chunk_rows;
   a.dpre = w.dpre;
+  a.hbuf = w.hbuf;
   a.dw_part = w.dw_part;
   a.splits = w.splits;
   a.db_part = w.db_part;

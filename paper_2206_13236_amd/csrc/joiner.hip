@@ -251,6 +251,22 @@ struct HSrcMNC {
   DEV void mnc_finish(const Raw& r, float (&v)[NV]) const { finish_h(r, v); }
 };
 
+// A(j, m) = h(m, j) from the chunk's hbuf [rows, J] (j-contiguous).
+template <class Cfg>
+struct HbufSrcMNC {
+  using T = typename Cfg::T;
+  static constexpr int NV = 16 / Cfg::KV;
+  using Raw = RawVec<T, NV>;
+  Rsrc h;
+  int cm0, mend, j0, J;
+  DEV void mnc_load(int k, int col, Raw& r) const {
+    const int j = j0 + col;
+    const int n = (k < mend && j < J) ? NV : 0;
+    raw_load(h, (uint32_t)((k - cm0) * J + j) * sizeof(T), n, kSegVector, r);
+  }
+  DEV void mnc_finish(const Raw& r, float (&v)[NV]) const { raw_to_float(r, v); }
+};
+
 // B(m, v) = dl[m][v]: global row-contiguous along v.
 template <class Cfg>
 struct DlSrcMNC {
@@ -621,7 +637,8 @@ __global__ __launch_bounds__(kDlThreads) void joiner_dl_kernel(JoinerArgs a, int
 }
 
 // ---------------------------------------------------------------------------
-// Backward 2: dh = dl W^T, dpre = dh (1 - h^2)
+// Backward 2: dh = dl W^T, dpre = dh (1 - h^2); also leaves h of the chunk's
+// rows in hbuf (zero for absent slots) as the dW contraction's operand.
 // ---------------------------------------------------------------------------
 template <bool BF>
 __global__ __launch_bounds__(kGemmThreads) void joiner_dh_kernel(JoinerArgs a, int cm0, int cm1) {
@@ -650,6 +667,7 @@ __global__ __launch_bounds__(kGemmThreads) void joiner_dh_kernel(JoinerArgs a, i
 
   const TIn* enc = reinterpret_cast<const TIn*>(a.enc);
   const TIn* dec = reinterpret_cast<const TIn*>(a.dec);
+  typename Cfg::T* hbuf = reinterpret_cast<typename Cfg::T*>(a.hbuf);
 #pragma unroll
   for (int i = 0; i < Cfg::FM; ++i)
 #pragma unroll
@@ -662,12 +680,15 @@ __global__ __launch_bounds__(kGemmThreads) void joiner_dh_kernel(JoinerArgs a, i
       for (int j = 0; j < Cfg::FN; ++j) {
         const int jj = j0 + tile_col<Cfg>(j);
         if (jj >= J) continue;
-        float dp = 0.f;
+        float dp = 0.f, h = 0.f;
         if (info.w >= 0) {
-          const float h = fast_tanh(ld_in(enc, (size_t)info.x + jj) + ld_in(dec, (size_t)info.y + jj));
+          h = fast_tanh(ld_in(enc, (size_t)info.x + jj) + ld_in(dec, (size_t)info.y + jj));
           dp = acc[i][j][r] * (1.f - h * h);
         }
         a.dpre[(size_t)m * J + jj] = dp;
+        // h of the chunk's rows, in the GEMM operand type, for the dW contraction
+        if constexpr (BF) hbuf[(size_t)(m - cm0) * J + jj] = f2bf(h);
+        else hbuf[(size_t)(m - cm0) * J + jj] = h;
       }
     }
 }
@@ -706,9 +727,9 @@ __global__ __launch_bounds__(kGemmThreads) void joiner_dw_kernel(JoinerArgs a, i
   }
   const TIn* enc = reinterpret_cast<const TIn*>(a.enc);
   const TIn* dec = reinterpret_cast<const TIn*>(a.dec);
-  HSrcMNC<Cfg, TIn> sa{EncDec<TIn>(a), a.rowinfo, j0, J, ke};
+  HbufSrcMNC<Cfg> sa{make_rsrc(a.hbuf, (size_t)a.chunk_rows * J * sizeof(typename Cfg::T)), cm0, ke, j0, J};
   DlSrcMNC<Cfg> sb{make_rsrc(a.dl, (size_t)a.chunk_rows * a.ldl * sizeof(typename Cfg::T)), cm0, ke, v0, a.ldl};
-  MNCLoader<Cfg, Cfg::BM, HSrcMNC<Cfg, TIn>> la(sa);
+  MNCLoader<Cfg, Cfg::BM, HbufSrcMNC<Cfg>> la(sa);
   MNCLoader<Cfg, Cfg::BN, DlSrcMNC<Cfg>> lb(sb);
   floatx4 acc[Cfg::FM][Cfg::FN];
   gemm_mainloop<Cfg>(la, lb, kb, ke, smem, acc);

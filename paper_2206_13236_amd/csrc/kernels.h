@@ -82,6 +82,7 @@ struct JoinerArgs {
   int ldl;
   int chunk_rows;
   float* dpre;         // ws [N*T*S, J]
+  void* hbuf;          // ws chunk [chunk_rows, J] (f32 or bf16): h = tanh(enc + dec) of the chunk's rows
   float* dw_part;      // ws [splits, J, V]
   int splits;
   float* db_part;      // ws [n_db_rows, V]
