@@ -34,7 +34,7 @@ namespace {
 // 8 waves in a 4 x 2 grid (32 x 64 wave tiles): about 100 registers per
 // lane, so two workgroups (four waves per SIMD) share a CU.
 constexpr int kGemmThreads = 512;
-using CfgF = GemmCfg<128, 128, 64, false, 4, 2>;
+using CfgF = GemmCfg<128, 128, 32, false, 4, 2>;
 using CfgB = GemmCfg<128, 128, 64, true, 4, 2>;
 static_assert(CfgF::NT == kGemmThreads && CfgB::NT == kGemmThreads, "joiner GEMM block size");
 static_assert(CfgF::WN == 64 && CfgB::WN == 64, "the forward's partial log-sum-exp slices are 64 columns");
@@ -335,7 +335,7 @@ __global__ __launch_bounds__(256) void joiner_prep_kernel(JoinerArgs a) {
 // Forward GEMM + partial log-sum-exp
 // ---------------------------------------------------------------------------
 template <bool BF>
-__global__ __launch_bounds__(kGemmThreads) void joiner_fwd_kernel(JoinerArgs a) {
+__global__ __launch_bounds__(kGemmThreads, 4) void joiner_fwd_kernel(JoinerArgs a) {
   using TIn = typename In<BF>::T;
   using Cfg = typename In<BF>::Cfg;
   __shared__ __align__(16) typename Cfg::T smem[Cfg::SMEM_BYTES / sizeof(typename Cfg::T)];
@@ -641,7 +641,7 @@ __global__ __launch_bounds__(kDlThreads) void joiner_dl_kernel(JoinerArgs a, int
 // rows in hbuf (zero for absent slots) as the dW contraction's operand.
 // ---------------------------------------------------------------------------
 template <bool BF>
-__global__ __launch_bounds__(kGemmThreads) void joiner_dh_kernel(JoinerArgs a, int cm0, int cm1) {
+__global__ __launch_bounds__(kGemmThreads, 4) void joiner_dh_kernel(JoinerArgs a, int cm0, int cm1) {
   using TIn = typename In<BF>::T;
   using Cfg = typename In<BF>::Cfg;
   __shared__ __align__(16) typename Cfg::T smem[Cfg::SMEM_BYTES / sizeof(typename Cfg::T)];
@@ -697,7 +697,7 @@ __global__ __launch_bounds__(kGemmThreads) void joiner_dh_kernel(JoinerArgs a, i
 // Backward 3: dW partial += h^T dl over one split of the chunk's rows
 // ---------------------------------------------------------------------------
 template <bool BF>
-__global__ __launch_bounds__(kGemmThreads) void joiner_dw_kernel(JoinerArgs a, int cm0, int cm1, int first) {
+__global__ __launch_bounds__(kGemmThreads, 4) void joiner_dw_kernel(JoinerArgs a, int cm0, int cm1, int first) {
   using TIn = typename In<BF>::T;
   using Cfg = typename In<BF>::Cfg;
   __shared__ __align__(16) typename Cfg::T smem[Cfg::SMEM_BYTES / sizeof(typename Cfg::T)];
@@ -891,7 +891,7 @@ int joiner_bwd_chunk_rows(int N, int T, int S, int J, int V, int bf16) {
 
 int joiner_bwd_splits(int J, int V) {
   const int tiles = ((J + 127) / 128) * ((V + 127) / 128);
-  int s = (256 + tiles - 1) / tiles;
+  int s = (512 + tiles - 1) / tiles;  // two workgroups per CU
   if (s < 1) s = 1;
   if (s > 32) s = 32;
   return s;
