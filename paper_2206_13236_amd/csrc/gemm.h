@@ -112,7 +112,12 @@ struct MNCLoader {
   static constexpr int KV = Cfg::KV;
   static constexpr int NV = 16 / KV;                       // rows per block (4 fp32, 2 bf16)
   static constexpr int NBR = ROWS / NV;                    // blocks along rows
-  static constexpr int NBLK = (Cfg::BK / KV) * NBR;
+  static constexpr int NKB = Cfg::BK / KV;                 // blocks along k
+  static constexpr int NBLK = NKB * NBR;
+  // Consecutive lanes take consecutive k-blocks of the same rows: a transposed
+  // LDS store of NKB lanes then fills one padded row contiguously (fewer bank
+  // conflicts than lanes 4 rows apart), and each global load still reads
+  // NKB x 16 contiguous bytes per row.
   static constexpr int NPT = (NBLK + Cfg::NT - 1) / Cfg::NT;
   struct Reg { typename Src::Raw v[NPT][KV]; };
   const Src& src;
@@ -122,7 +127,7 @@ struct MNCLoader {
     for (int b = 0; b < NPT; ++b) {
       int blk = threadIdx.x + Cfg::NT * b;
       if (NBLK % Cfg::NT == 0 || blk < NBLK) {
-        int kb = blk / NBR, nb = blk % NBR;
+        const int kb = blk % NKB, nb = blk / NKB;
 #pragma unroll
         for (int i = 0; i < KV; ++i) src.mnc_load(k0 + kb * KV + i, nb * NV, r.v[b][i]);
       }
@@ -133,7 +138,7 @@ struct MNCLoader {
     for (int b = 0; b < NPT; ++b) {
       int blk = threadIdx.x + Cfg::NT * b;
       if (NBLK % Cfg::NT == 0 || blk < NBLK) {
-        int kb = blk / NBR, nb = blk % NBR;
+        const int kb = blk % NKB, nb = blk / NKB;
         float m[KV][NV];
 #pragma unroll
         for (int i = 0; i < KV; ++i) src.mnc_finish(r.v[b][i], m[i]);
