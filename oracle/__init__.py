@@ -32,5 +32,7 @@ from .rnnt import (  # noqa: F401
     full_joiner_logprobs,
     full_joiner_loss,
     simple_stage,
+    smoothed_joiner_logprobs,
+    smoothed_simple_stage,
     pruned_stage,
 )

@@ -234,6 +234,90 @@ def simple_stage(am, lm, symbols, t_len, u_len, blank=0, scale=None, grads=True)
 
 
 # ---------------------------------------------------------------------------
+# Sec. 3.3.1: the smoothed trivial joiner (small shapes: plain fp64 PyTorch)
+# ---------------------------------------------------------------------------
+
+def _smoothed_px_py(am_t, lm_t, symbols, t_len, u_len, blank, lm_only_scale, am_only_scale):
+    """px, py of the smoothed joiner as fp64 torch tensors (differentiable).
+
+    L_smoothed = (1 - a_lm - a_ac) L_trivial + a_lm L_lm + a_ac L_acoustic, with
+      L_trivial(t,u,v)  = LogSoftmax_v(am[t,v] + lm[u,v])        (Eq. (5)),
+      L_lm(u,v)         = LogSoftmax_v lm[u,v],
+      L_dec^avg(v)      = log (1/(U+1)) sum_{u=0..U} Softmax_v lm[u,v],
+      L_acoustic(t,v)   = LogSoftmax_v(am[t,v] + L_dec^avg(v)).
+    Reading: the third term of the printed combination (a second L_lm) is
+    L_acoustic, the only other joiner the section defines; L_dec^avg does not
+    depend on u, and its average runs over the utterance's own U_n + 1 rows.
+    """
+    import torch
+    N, T, _ = am_t.shape
+    U1 = lm_t.shape[1]
+    a, b = float(lm_only_scale), float(am_only_scale)
+    out_x, out_y = [], []
+    for n in range(N):
+        Tn, Un = int(t_len[n]), int(u_len[n])
+        amn, lmn = am_t[n, :Tn], lm_t[n, :Un + 1]
+        triv = torch.log_softmax(amn[:, None, :] + lmn[None, :, :], dim=-1)     # [Tn, Un+1, V]
+        llm = torch.log_softmax(lmn, dim=-1)                                     # [Un+1, V]
+        lavg = torch.log(torch.softmax(lmn, dim=-1).mean(dim=0))                 # [V]
+        lac = torch.log_softmax(amn + lavg[None, :], dim=-1)                     # [Tn, V]
+        sm = (1.0 - a - b) * triv + a * llm[None, :, :] + b * lac[:, None, :]    # [Tn, Un+1, V]
+        y = torch.as_tensor(np.asarray(symbols[n, :Un], np.int64))
+        # -inf outside the lattice, assembled without in-place writes
+        fx = torch.full((T, U1), NEG_INF, dtype=torch.float64)
+        fy = torch.full((T, U1), NEG_INF, dtype=torch.float64)
+        mx = torch.zeros((T, U1), dtype=torch.bool)
+        my = torch.zeros((T, U1), dtype=torch.bool)
+        mx[:Tn, :Un] = True
+        my[:Tn, :Un + 1] = True
+        if Un > 0:
+            fx = fx.masked_scatter(mx, sm[:, torch.arange(Un), y].reshape(-1))
+        fy = fy.masked_scatter(my, sm[:, :, blank].reshape(-1))
+        out_x.append(fx)
+        out_y.append(fy)
+    return torch.stack(out_x), torch.stack(out_y)
+
+
+def smoothed_joiner_logprobs(am, lm, symbols, t_len, u_len, blank=0, lm_only_scale=0.0,
+                             am_only_scale=0.0):
+    """px, py [N, T, U+1] (fp64 NumPy) of the smoothed trivial joiner (Sec. 3.3.1)."""
+    import torch
+    am_t = torch.as_tensor(np.asarray(am, np.float64))
+    lm_t = torch.as_tensor(np.asarray(lm, np.float64))
+    px, py = _smoothed_px_py(am_t, lm_t, symbols, t_len, u_len, blank, lm_only_scale, am_only_scale)
+    return px.numpy(), py.numpy()
+
+
+def smoothed_simple_stage(am, lm, symbols, t_len, u_len, blank=0, lm_only_scale=0.0, am_only_scale=0.0,
+                          scale=None, grads=True) -> dict:
+    """The simple loss with the smoothed joiner: recursion, occupations and the
+    gradients of sum_n sc_n * loss_n w.r.t. am and lm. The loss is -L and
+    dL/dpx = gx, dL/dpy = gy (Sec. 3.2.2), so the gradient is the
+    vector-Jacobian product of px, py with -sc * gx, -sc * gy, taken by
+    PyTorch's autograd in fp64 through the definitions above."""
+    import torch
+    am_t = torch.as_tensor(np.asarray(am, np.float64)).clone().requires_grad_(grads)
+    lm_t = torch.as_tensor(np.asarray(lm, np.float64)).clone().requires_grad_(grads)
+    px_t, py_t = _smoothed_px_py(am_t, lm_t, symbols, t_len, u_len, blank, lm_only_scale, am_only_scale)
+    px, py = px_t.detach().numpy(), py_t.detach().numpy()
+    loss, gx, gy = lattice_loss(px, py, t_len, u_len)
+    out = {"px": px, "py": py, "loss": loss, "gx": gx, "gy": gy}
+    if grads:
+        N = px.shape[0]
+        sc = torch.as_tensor(np.ones(N) if scale is None else np.asarray(scale, np.float64))
+        wx = -sc[:, None, None] * torch.as_tensor(gx)
+        wy = -sc[:, None, None] * torch.as_tensor(gy)
+        # entries outside the lattice are -inf constants with zero weight
+        fin_x, fin_y = torch.isfinite(px_t), torch.isfinite(py_t)
+        obj = (torch.where(fin_x, px_t, torch.zeros_like(px_t)) * wx).sum() + \
+              (torch.where(fin_y, py_t, torch.zeros_like(py_t)) * wy).sum()
+        d_am, d_lm = torch.autograd.grad(obj, (am_t, lm_t), allow_unused=True)
+        out["am_grad"] = np.zeros(am_t.shape) if d_am is None else d_am.numpy()
+        out["lm_grad"] = np.zeros(lm_t.shape) if d_lm is None else d_lm.numpy()
+    return out
+
+
+# ---------------------------------------------------------------------------
 # Sec. 3.2.2: locally optimal pruning bounds and the consistency constraints
 # ---------------------------------------------------------------------------
 

@@ -455,3 +455,71 @@ def test_infeasible_band_gives_infinite_loss_and_zero_occupation():
     pyb = np.take_along_axis(py, np.minimum(ranges[0], U), axis=1)[None]
     loss, gx, gy = O.pruned_loss(pxb, pyb, ranges, [T], [U])
     assert loss[0] == np.inf and np.all(gx == 0) and np.all(gy == 0)
+
+
+# ---------------------------------------------------------------------------
+# Sec. 3.3.1: the smoothed trivial joiner
+# ---------------------------------------------------------------------------
+
+def test_smoothed_joiner_reduces_to_the_trivial_joiner():
+    b = make_batch("tiny", seed=7)
+    px, py = O.smoothed_joiner_logprobs(b.am, b.lm, b.symbols, b.t_len, b.u_len, 0, 0.0, 0.0)
+    _, tpx, tpy = O.trivial_joiner_logprobs(b.am, b.lm, b.symbols, b.t_len, b.u_len, 0)
+    np.testing.assert_allclose(px, tpx, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(py, tpy, rtol=0, atol=1e-12)
+
+
+def test_smoothed_joiner_special_cases():
+    b = make_batch("tiny", seed=8)
+    N, T, V = b.am.shape
+    # acoustic only, with lm constant over v: the unigram prior is uniform and
+    # L_acoustic is the trivial joiner with lm = 0
+    lm0 = np.repeat(b.lm[:, :, :1], V, axis=2)
+    px, py = O.smoothed_joiner_logprobs(b.am, lm0, b.symbols, b.t_len, b.u_len, 0, 0.0, 1.0)
+    _, tpx, tpy = O.trivial_joiner_logprobs(b.am, np.zeros_like(b.lm), b.symbols, b.t_len, b.u_len, 0)
+    np.testing.assert_allclose(px, tpx, atol=1e-12)
+    np.testing.assert_allclose(py, tpy, atol=1e-12)
+    # LM only: px(t,u) and py(t,u) do not depend on t or on am
+    am2 = b.am + 3.0 * np.random.default_rng(0).standard_normal(b.am.shape).astype(np.float32)
+    pa, pb = O.smoothed_joiner_logprobs(b.am, b.lm, b.symbols, b.t_len, b.u_len, 0, 1.0, 0.0)
+    qa, qb = O.smoothed_joiner_logprobs(am2, b.lm, b.symbols, b.t_len, b.u_len, 0, 1.0, 0.0)
+    np.testing.assert_allclose(pa, qa, atol=1e-12)
+    np.testing.assert_allclose(pb, qb, atol=1e-12)
+    for n in range(N):
+        Tn = b.t_len[n]
+        np.testing.assert_allclose(pb[n, :Tn], np.broadcast_to(pb[n, :1], pb[n, :Tn].shape), atol=1e-12)
+    # every smoothed row is a mixture of log-softmaxes: for a = b = 1/2 at blank = 0
+    # exp(py) is bounded by 1 and positive
+    _, q = O.smoothed_joiner_logprobs(b.am, b.lm, b.symbols, b.t_len, b.u_len, 0, 0.5, 0.5)
+    fin = np.isfinite(q)
+    assert np.all(q[fin] < 0)
+
+
+def test_smoothed_simple_loss_finite_difference():
+    rng = np.random.default_rng(9)
+    N, T, U, V = 2, 5, 3, 6
+    am = rng.standard_normal((N, T, V))
+    lm = rng.standard_normal((N, U + 1, V))
+    sym = rng.integers(1, V, size=(N, U))
+    sym[1, 0] = 0  # a token equal to blank
+    tl, ul = np.array([5, 4]), np.array([3, 2])
+    sc = np.array([1.0, 0.7])
+    a, bb = 0.25, 0.15
+    out = O.smoothed_simple_stage(am, lm, sym, tl, ul, 0, a, bb, scale=sc)
+
+    def total(am_, lm_):
+        r = O.smoothed_simple_stage(am_, lm_, sym, tl, ul, 0, a, bb, grads=False)
+        return float((sc * r["loss"]).sum())
+
+    eps = 1e-6
+    for arr, key in ((am, "am_grad"), (lm, "lm_grad")):
+        num = np.zeros_like(arr)
+        for idx in np.ndindex(arr.shape):
+            a0 = arr[idx]
+            arr[idx] = a0 + eps
+            fp = total(am, lm)
+            arr[idx] = a0 - eps
+            fm = total(am, lm)
+            arr[idx] = a0
+            num[idx] = (fp - fm) / (2 * eps)
+        np.testing.assert_allclose(out[key], num, atol=2e-8, rtol=1e-6)
