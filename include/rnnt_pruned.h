@@ -115,12 +115,21 @@ size_t rnnt_simple_loss_workspace_size(int32_t N, int32_t T, int32_t U, int32_t 
  *   am_grad [N, T, V], lm_grad [N, U+1, V]  fp32, nullable: gradients of
  *                       sum_n scale[n] * loss[n].
  *   scale  [N] fp32, nullable (all ones); only read when a gradient is asked.
+ * lm_only_scale, am_only_scale: weights a_lm, a_ac >= 0 (a_lm + a_ac <= 1) of
+ *   the smoothed trivial joiner of Sec. 3.3.1,
+ *     L = (1 - a_lm - a_ac) L_trivial + a_lm L_lm + a_ac L_acoustic,
+ *   L_lm(u,v) = LogSoftmax_v lm[u,v], L_acoustic(t,v) = LogSoftmax_v(am[t,v] +
+ *   L_dec^avg(v)), L_dec^avg(v) = log of the mean over u <= U_n of
+ *   Softmax_v lm[u,v]. (The printed combination repeats L_lm in its third
+ *   term; the acoustic joiner the section defines is used.) 0, 0 gives the
+ *   plain trivial joiner.
  * workspace: device buffer of at least rnnt_simple_loss_workspace_size() bytes,
  *   256-byte aligned. On return (in stream order) it holds what
  *   rnnt_simple_loss_backward needs.
  */
 int rnnt_simple_loss(const rnnt_batch* batch, int32_t V,
                      const float* am, const float* lm, const float* scale,
+                     float lm_only_scale, float am_only_scale,
                      float* loss, float* px_occ, float* py_occ,
                      float* px, float* py, float* am_grad, float* lm_grad,
                      void* workspace, size_t workspace_bytes, void* stream);
@@ -128,16 +137,17 @@ int rnnt_simple_loss(const rnnt_batch* batch, int32_t V,
 /* Gradients of sum_n scale[n] * simple_loss[n] w.r.t. am and lm (the
  * log-softmax backward through Eq. (5), two contractions of the forward's
  * shape), computed from the state a preceding rnnt_simple_loss call left in
- * `workspace`: the same batch, V, am, lm, its px_occ output, and the same
- * workspace, unmodified since, with that call ordered before this one
- * (same stream, or an event). Results equal those of the forward call asked
- * for the gradients directly.
+ * `workspace`: the same batch, V, am, lm, smoothing weights, its px_occ
+ * output, and the same workspace, unmodified since, with that call ordered
+ * before this one (same stream, or an event). Results equal those of the
+ * forward call asked for the gradients directly.
  *
  * px_occ [N, T, U+1]: the forward's px_occ output (required).
  * am_grad [N, T, V], lm_grad [N, U+1, V] fp32: outputs (at least one).
  */
 int rnnt_simple_loss_backward(const rnnt_batch* batch, int32_t V,
                               const float* am, const float* lm, const float* scale,
+                              float lm_only_scale, float am_only_scale,
                               const float* px_occ, float* am_grad, float* lm_grad,
                               void* workspace, size_t workspace_bytes, void* stream);
 

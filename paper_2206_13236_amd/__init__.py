@@ -118,7 +118,8 @@ def pruned_joiner_backward_workspace_size(N, T, U, S, J, V, dtype) -> int:
 def rnnt_simple_loss(batch: Batch, V: int, am: torch.Tensor, lm: torch.Tensor,
                      scale: Optional[torch.Tensor] = None, loss=None, px_occ=None, py_occ=None,
                      px=None, py=None, am_grad=None, lm_grad=None, workspace=None, stream=None,
-                     want_logprobs: bool = False, want_grads: bool = False) -> dict:
+                     want_logprobs: bool = False, want_grads: bool = False, lm_only_scale: float = 0.0,
+                     am_only_scale: float = 0.0) -> dict:
     N, T, U = batch.N, batch.T, batch.U
     dev = batch.device
     _need(am, "am", torch.float32, (N, T, V))
@@ -134,7 +135,8 @@ def rnnt_simple_loss(batch: Batch, V: int, am: torch.Tensor, lm: torch.Tensor,
     if scale is not None:
         _need(scale, "scale", torch.float32, (N,))
     ws = _ws(simple_loss_workspace_size(N, T, U, V), dev, workspace)
-    check(lib().rnnt_simple_loss(batch.c, V, _p(am), _p(lm), _p(scale), _p(loss), _p(px_occ),
+    check(lib().rnnt_simple_loss(batch.c, V, _p(am), _p(lm), _p(scale), float(lm_only_scale),
+                                 float(am_only_scale), _p(loss), _p(px_occ),
                                  _p(py_occ), _p(px), _p(py), _p(am_grad), _p(lm_grad), _p(ws),
                                  ws.numel(), _stream(stream)))
     return {"loss": loss, "px_occ": px_occ, "py_occ": py_occ, "px": px, "py": py,
@@ -143,7 +145,8 @@ def rnnt_simple_loss(batch: Batch, V: int, am: torch.Tensor, lm: torch.Tensor,
 
 def rnnt_simple_loss_backward(batch: Batch, V: int, am: torch.Tensor, lm: torch.Tensor, px_occ: torch.Tensor,
                               workspace: torch.Tensor, scale: Optional[torch.Tensor] = None, am_grad=None,
-                              lm_grad=None, stream=None) -> dict:
+                              lm_grad=None, stream=None, lm_only_scale: float = 0.0,
+                              am_only_scale: float = 0.0) -> dict:
     """d am, d lm from the state a preceding rnnt_simple_loss call left in ``workspace``."""
     N, T, U = batch.N, batch.T, batch.U
     dev = batch.device
@@ -156,7 +159,8 @@ def rnnt_simple_loss_backward(batch: Batch, V: int, am: torch.Tensor, lm: torch.
     am_grad = torch.empty(N, T, V, **f32) if am_grad is None else am_grad
     lm_grad = torch.empty(N, U + 1, V, **f32) if lm_grad is None else lm_grad
     ws = _ws(simple_loss_workspace_size(N, T, U, V), dev, workspace)
-    check(lib().rnnt_simple_loss_backward(batch.c, V, _p(am), _p(lm), _p(scale), _p(px_occ), _p(am_grad),
+    check(lib().rnnt_simple_loss_backward(batch.c, V, _p(am), _p(lm), _p(scale), float(lm_only_scale),
+                                          float(am_only_scale), _p(px_occ), _p(am_grad),
                                           _p(lm_grad), _p(ws), ws.numel(), _stream(stream)))
     return {"am_grad": am_grad, "lm_grad": lm_grad}
 
@@ -263,13 +267,19 @@ class PrunedRnntLoss:
     With ``keep_logits`` the pruned logits [N, T, S, V] are kept between the
     joiner's forward and backward (the method's own memory footprint);
     without it the backward recomputes them and holds one row chunk at a time.
+
+    ``lm_only_scale`` and ``am_only_scale`` smooth the simple loss's joiner
+    (Sec. 3.3.1); both 0 gives the plain trivial joiner.
     """
 
     def __init__(self, S: int, simple_scale: float = 0.5, pruned_scale: float = 1.0,
-                 keep_logits: bool = True, overlap: bool = True):
+                 keep_logits: bool = True, overlap: bool = True, lm_only_scale: float = 0.0,
+                 am_only_scale: float = 0.0):
         self.S = int(S)
         self.simple_scale = float(simple_scale)
         self.pruned_scale = float(pruned_scale)
+        self.lm_only_scale = float(lm_only_scale)
+        self.am_only_scale = float(am_only_scale)
         self.keep_logits = bool(keep_logits)
         self.overlap = bool(overlap)
         self._cache = {}
@@ -318,7 +328,7 @@ class PrunedRnntLoss:
         sim = rnnt_simple_loss(
             batch, V, am, lm, ssc, loss=o("simple_loss", (N,)),
             px_occ=o("simple_px_occ", (N, T, U + 1)), py_occ=o("simple_py_occ", (N, T, U + 1)),
-            workspace=ws_s, stream=main)
+            workspace=ws_s, stream=main, lm_only_scale=self.lm_only_scale, am_only_scale=self.am_only_scale)
         res = {"simple_loss": sim["loss"], "simple_px_occ": sim["px_occ"], "simple_py_occ": sim["py_occ"]}
         am_grad, lm_grad = o("am_grad", (N, T, V)), o("lm_grad", (N, U + 1, V))
         enc_grad, dec_grad = o("enc_grad", (N, T, J)), o("dec_grad", (N, U + 1, J))
@@ -328,7 +338,8 @@ class PrunedRnntLoss:
 
         def simple_backward(s):
             rnnt_simple_loss_backward(batch, V, am, lm, sim["px_occ"], ws_s, scale=ssc, am_grad=am_grad,
-                                      lm_grad=lm_grad, stream=s)
+                                      lm_grad=lm_grad, stream=s, lm_only_scale=self.lm_only_scale,
+                                      am_only_scale=self.am_only_scale)
 
         if self.pruned_scale == 0.0:
             # warm-up: the pruned part carries no weight and is not evaluated
@@ -402,11 +413,14 @@ class _PrunedRnntFunction(torch.autograd.Function):
 
 
 def pruned_rnnt_loss(am, lm, enc, dec, W, bias, batch: Batch, S: int, simple_scale: float = 0.5,
-                     pruned_scale: float = 1.0, reduction: str = "sum", module: Optional[PrunedRnntLoss] = None):
+                     pruned_scale: float = 1.0, reduction: str = "sum", module: Optional[PrunedRnntLoss] = None,
+                     lm_only_scale: float = 0.0, am_only_scale: float = 0.0):
     """Differentiable training loss: sum (or mean) over utterances of
-    simple_scale * simple_loss + pruned_scale * pruned_loss (Sec. 3.3)."""
+    simple_scale * simple_loss + pruned_scale * pruned_loss (Sec. 3.3), the
+    simple loss optionally with the smoothed joiner (Sec. 3.3.1)."""
     if reduction not in ("sum", "mean"):
         raise ValueError("reduction must be 'sum' or 'mean'")
     if module is None:
-        module = PrunedRnntLoss(S, simple_scale=simple_scale, pruned_scale=pruned_scale)
+        module = PrunedRnntLoss(S, simple_scale=simple_scale, pruned_scale=pruned_scale,
+                                lm_only_scale=lm_only_scale, am_only_scale=am_only_scale)
     return _PrunedRnntFunction.apply(am, lm, enc, dec, W, bias, module, batch, reduction)

@@ -8,7 +8,7 @@ from __future__ import annotations
 
 import ctypes
 import os
-from ctypes import POINTER, c_char_p, c_int32, c_size_t, c_void_p
+from ctypes import c_float, POINTER, c_char_p, c_int32, c_size_t, c_void_p
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "librnnt_pruned.so")
 
@@ -39,11 +39,11 @@ SIGNATURES = {
     "rnnt_abi_version": (c_int32, []),
     "rnnt_last_error": (c_char_p, []),
     "rnnt_simple_loss_workspace_size": (c_size_t, [c_int32, c_int32, c_int32, c_int32]),
-    "rnnt_simple_loss": (c_int32, [POINTER(RnntBatch), c_int32, c_void_p, c_void_p, c_void_p,
+    "rnnt_simple_loss": (c_int32, [POINTER(RnntBatch), c_int32, c_void_p, c_void_p, c_void_p, c_float, c_float,
                                    c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
                                    c_void_p, c_size_t, c_void_p]),
-    "rnnt_simple_loss_backward": (c_int32, [POINTER(RnntBatch), c_int32, c_void_p, c_void_p, c_void_p, c_void_p,
-                                            c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]),
+    "rnnt_simple_loss_backward": (c_int32, [POINTER(RnntBatch), c_int32, c_void_p, c_void_p, c_void_p, c_float,
+                                            c_float, c_void_p, c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]),
     "rnnt_prune_ranges": (c_int32, [POINTER(RnntBatch), c_int32, c_void_p, c_void_p, c_void_p, c_void_p]),
     "rnnt_pruned_joiner_workspace_size": (c_size_t, [c_int32] * 6),
     "rnnt_pruned_joiner": (c_int32, [POINTER(RnntBatch), c_int32, c_int32, c_int32, c_int32,

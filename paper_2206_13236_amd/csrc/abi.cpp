@@ -95,6 +95,14 @@ struct SimpleWs {
   int nsplit;
   float* lpart;
   int lsplit;
+  double* rx;
+  double* Gx;
+  double* Gy;
+  float* Zlm;
+  float* lavg;
+  float* Zac;
+  float* q;
+  float* su;
   size_t bytes;
 };
 
@@ -118,6 +126,14 @@ SimpleWs simple_layout(void* base, int N, int T, int U, int V) {
   w.npart = c.take<float>((size_t)w.nsplit * L);
   w.lsplit = dlm_splits(N, T, U, V);
   w.lpart = c.take<float>((size_t)w.lsplit * NU * V);
+  w.rx = c.take<double>(NT);
+  w.Gx = c.take<double>(NU);
+  w.Gy = c.take<double>(NU);
+  w.Zlm = c.take<float>(NU);
+  w.lavg = c.take<float>((size_t)N * V);
+  w.Zac = c.take<float>(NT);
+  w.q = c.take<float>((size_t)N * V);
+  w.su = c.take<float>(NU);
   w.bytes = c.off;
   return w;
 }
@@ -126,10 +142,12 @@ SimpleWs simple_layout(void* base, int N, int T, int U, int V) {
 // everything but the caller's outputs. The occupation kernel always leaves
 // the backward's state (W(t,u), row and column sums) in the workspace.
 SimpleArgs simple_args(const rnnt_batch* batch, int V, const float* am, const float* lm, const float* scale,
-                       const SimpleWs& w) {
+                       float lm_only, float am_only, const SimpleWs& w) {
   SimpleArgs a{};
   a.b = to_dev(batch);
   a.V = V;
+  a.lm_only = lm_only;
+  a.am_only = am_only;
   a.am = am;
   a.lm = lm;
   a.scale = scale;
@@ -151,6 +169,14 @@ SimpleArgs simple_args(const rnnt_batch* batch, int V, const float* am, const fl
   a.cpx = w.cpx;
   a.cpy = w.cpy;
   a.ncolblk = lattice_colblocks(batch->T);
+  a.rx = w.rx;
+  a.Gx = w.Gx;
+  a.Gy = w.Gy;
+  a.Zlm = w.Zlm;
+  a.lavg = w.lavg;
+  a.Zac = w.Zac;
+  a.q = w.q;
+  a.su = w.su;
   return a;
 }
 
@@ -238,7 +264,7 @@ int check_joiner_sizes(const rnnt_batch* b, int S, int J, int V, int dtype) {
 
 extern "C" {
 
-int rnnt_abi_version(void) { return 2; }
+int rnnt_abi_version(void) { return 3; }
 
 const char* rnnt_last_error(void) { return g_err.c_str(); }
 
@@ -247,9 +273,16 @@ size_t rnnt_simple_loss_workspace_size(int32_t N, int32_t T, int32_t U, int32_t 
   return simple_layout(nullptr, N, T, U, V).bytes;
 }
 
+int check_smoothing(float lm_only, float am_only) {
+  if (!(lm_only >= 0.f && am_only >= 0.f && lm_only + am_only <= 1.f))
+    return fail(RNNT_EINVAL, "smoothing weights must be >= 0 with sum <= 1 (got %g, %g)", lm_only, am_only);
+  return RNNT_OK;
+}
+
 int rnnt_simple_loss(const rnnt_batch* batch, int32_t V, const float* am, const float* lm, const float* scale,
-                     float* loss, float* px_occ, float* py_occ, float* px, float* py, float* am_grad,
-                     float* lm_grad, void* workspace, size_t workspace_bytes, void* stream) {
+                     float lm_only_scale, float am_only_scale, float* loss, float* px_occ, float* py_occ,
+                     float* px, float* py, float* am_grad, float* lm_grad, void* workspace,
+                     size_t workspace_bytes, void* stream) {
   int rc = check_batch(batch, true);
   if (rc) return rc;
   if (V < 1) return fail(RNNT_EINVAL, "V must be >= 1 (got %d)", V);
@@ -257,12 +290,14 @@ int rnnt_simple_loss(const rnnt_batch* batch, int32_t V, const float* am, const 
   if (!am || !lm) return fail(RNNT_EINVAL, "am and lm are required");
   if (!loss || !px_occ || !py_occ) return fail(RNNT_EINVAL, "loss, px_occ and py_occ are required");
   if ((px == nullptr) != (py == nullptr)) return fail(RNNT_EINVAL, "px and py must be given together");
+  rc = check_smoothing(lm_only_scale, am_only_scale);
+  if (rc) return rc;
   const SimpleWs need = simple_layout(nullptr, batch->N, batch->T, batch->U, V);
   rc = check_ws(workspace, workspace_bytes, need.bytes);
   if (rc) return rc;
   const SimpleWs w = simple_layout(workspace, batch->N, batch->T, batch->U, V);
   hipStream_t s = static_cast<hipStream_t>(stream);
-  SimpleArgs a = simple_args(batch, V, am, lm, scale, w);
+  SimpleArgs a = simple_args(batch, V, am, lm, scale, lm_only_scale, am_only_scale, w);
   if (px) a.px = px;
   if (py) a.py = py;
   a.loss = loss;
@@ -271,6 +306,7 @@ int rnnt_simple_loss(const rnnt_batch* batch, int32_t V, const float* am, const 
   a.am_grad = am_grad;
   a.lm_grad = lm_grad;
   hipError_t e = launch_rowmax(a, s);
+  if (e == hipSuccess) e = launch_smoothing_stats(a, s);
   if (e == hipSuccess) e = launch_normalizer(a, s);
   if (e == hipSuccess) e = launch_lattice(a, s);
   if (e == hipSuccess && (am_grad || lm_grad)) e = launch_simple_grads(a, s);
@@ -278,7 +314,8 @@ int rnnt_simple_loss(const rnnt_batch* batch, int32_t V, const float* am, const 
 }
 
 int rnnt_simple_loss_backward(const rnnt_batch* batch, int32_t V, const float* am, const float* lm,
-                              const float* scale, const float* px_occ, float* am_grad, float* lm_grad,
+                              const float* scale, float lm_only_scale, float am_only_scale,
+                              const float* px_occ, float* am_grad, float* lm_grad,
                               void* workspace, size_t workspace_bytes, void* stream) {
   int rc = check_batch(batch, true);
   if (rc) return rc;
@@ -286,11 +323,13 @@ int rnnt_simple_loss_backward(const rnnt_batch* batch, int32_t V, const float* a
   if (batch->blank < 0 || batch->blank >= V) return fail(RNNT_EINVAL, "blank = %d outside [0, V)", batch->blank);
   if (!am || !lm || !px_occ) return fail(RNNT_EINVAL, "am, lm and px_occ are required");
   if (!am_grad && !lm_grad) return fail(RNNT_EINVAL, "at least one of am_grad and lm_grad is required");
+  rc = check_smoothing(lm_only_scale, am_only_scale);
+  if (rc) return rc;
   const SimpleWs need = simple_layout(nullptr, batch->N, batch->T, batch->U, V);
   rc = check_ws(workspace, workspace_bytes, need.bytes);
   if (rc) return rc;
   const SimpleWs w = simple_layout(workspace, batch->N, batch->T, batch->U, V);
-  SimpleArgs a = simple_args(batch, V, am, lm, scale, w);
+  SimpleArgs a = simple_args(batch, V, am, lm, scale, lm_only_scale, am_only_scale, w);
   a.gx = const_cast<float*>(px_occ);  // read only by the gradient kernels
   a.am_grad = am_grad;
   a.lm_grad = lm_grad;

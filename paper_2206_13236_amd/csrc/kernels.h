@@ -33,6 +33,17 @@ struct SimpleArgs {
   double* cpx;         // ws [N, ncolblk, U+1]: column sums of gx over 16-frame blocks
   double* cpy;         //                       same for gy
   int ncolblk;
+  double* rx;          // ws [N*T]      row sums of gx (fp64)
+  double* Gx;          // ws [N*(U+1)]  column sums of gx over frames (fp64)
+  double* Gy;          //               same for gy
+  // smoothed trivial joiner (Sec. 3.3.1): weights and per-utterance statistics
+  float lm_only;       // a_lm
+  float am_only;       // a_ac
+  float* Zlm;          // ws [N*(U+1)]  log sum_v exp(lm[u,v])
+  float* lavg;         // ws [N, V]     L_dec^avg(v)
+  float* Zac;          // ws [N*T]      log sum_v exp(am[t,v] + L_dec^avg(v))
+  float* q;            // ws [N, V]     gradient of the loss w.r.t. L_dec^avg, over (U_n+1) avg(v)
+  float* su;           // ws [N*(U+1)]  sum_v q(v) softmax(lm[u])(v)
   float* am_grad;      // [N, T, V] or null
   float* lm_grad;      // [N, U+1, V] or null
 };
@@ -43,6 +54,7 @@ int normalizer_splits(int N, int T, int U, int V);
 int dlm_splits(int N, int T, int U, int V);
 hipError_t launch_lattice(const SimpleArgs& a, hipStream_t s);
 int lattice_colblocks(int T);
+hipError_t launch_smoothing_stats(const SimpleArgs& a, hipStream_t s);
 hipError_t launch_simple_grads(const SimpleArgs& a, hipStream_t s);
 
 // ---- stage 3: pruning bounds -----------------------------------------------

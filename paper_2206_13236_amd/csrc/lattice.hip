@@ -17,7 +17,7 @@
 // The occupations of frame t are normalised by that frame's own sum, which
 // cancels the rounding the alpha and beta chains accumulate in common. The
 // kernel also writes W(t,u) = (gx + gy) e^{m_a + m_l - Z} for the gradient,
-// the row sums of gy and per-16-frame partial column sums of gx and gy.
+// the row sums of gx and gy and per-16-frame partial column sums of gx and gy.
 //
 // Precision: log2 domain with fp64 accumulators; only the bounded correction
 // term of LogAdd goes through fp32 exp2/log2 (see log2add). alpha and beta are
@@ -216,7 +216,7 @@ __global__ __launch_bounds__(64 * kOccFrames) void lattice_occ_kernel(SimpleArgs
   const double Lt = mx + log2(s);
   const bool trow = t < T;
   const float mat = frow ? a.m_a[(size_t)n * T + t] : 0.f;
-  double ry = 0.0;
+  double ry = 0.0, rx = 0.0;
 #pragma unroll
   for (int c = 0; c < R; ++c) {
     const int u = c * 64 + lane;
@@ -233,6 +233,7 @@ __global__ __launch_bounds__(64 * kOccFrames) void lattice_occ_kernel(SimpleArgs
           (frow && u <= Un) ? (gxv + gyv) * expf(mat + a.m_l[(size_t)n * U1 + u] - a.Z[idx]) : 0.f;
     }
     ry += (double)gyv;
+    rx += (double)gxv;
     {
       sx[wave][lane] = (double)gxv;
       sy[wave][lane] = (double)gyv;
@@ -253,7 +254,11 @@ __global__ __launch_bounds__(64 * kOccFrames) void lattice_occ_kernel(SimpleArgs
   if (trow) {
     if (lane < a.ldw - U1) a.Wt[((size_t)n * T + t) * a.ldw + U1 + lane] = 0.f;
     ry = wave_sum_d(ry);
-    if (lane == 0) a.ry[(size_t)n * T + t] = ry;
+    rx = wave_sum_d(rx);
+    if (lane == 0) {
+      a.ry[(size_t)n * T + t] = ry;
+      a.rx[(size_t)n * T + t] = rx;
+    }
   }
 }
 

@@ -18,6 +18,18 @@
 //                   - sum_t gx(t,u) [v = y_{u+1}] - sum_t gy(t,u) [v = blank])
 // with W(t,u) = (gx + gy)(t,u) e^{m_a + m_l - Z}: the log-softmax backward
 // (gradient of the target/blank entries minus softmax times their sum).
+//
+// Smoothed joiner (Sec. 3.3.1), with weights a = a_lm, b = a_ac, c = 1-a-b:
+//   L = c L_trivial + a L_lm + b L_acoustic,   L_lm(u,v) = lm[u,v] - Zlm[u],
+//   L_acoustic(t,v) = am[t,v] + lavg[v] - Zac[t],
+//   lavg[v] = log (1/(U+1)) sum_u e^{lm[u,v] - Zlm[u]},  Zlm, Zac row log-sum-exps.
+// With Gx(u), Gy(u) the column sums and R(t) the row sums of gx + gy, and
+// P_ac, P_lm the softmaxes of those joiners, the gradients gain
+//   d am += b (R(t) P_ac[t,v] - sparse)       (sparse: the target/blank terms)
+//   d lm += a ((Gx+Gy)(u) P_lm[u,v] - sparse) + b P_lm[u,v] (q[v] - s_u)
+// where q[v] = g[v] / ((U+1) e^{lavg[v]}), g[v] = sum_t R(t) P_ac[t,v] - Sy(v)
+// is the gradient w.r.t. lavg / b (Sy: target/blank column sums) and
+// s_u = sum_v q[v] P_lm[u,v] (the chain rule through the average of softmaxes).
 #include <float.h>
 
 #include "gemm.h"
@@ -64,6 +76,129 @@ __global__ __launch_bounds__(256) void rowmax_kernel(const float* __restrict__ x
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) m = keep_nan_max(m, __shfl_xor(m, off, 64));
   if (lane == 0) out[row] = m;
+}
+
+// ---------------------------------------------------------------------------
+// Smoothing statistics (Sec. 3.3.1), one utterance's rows at a time.
+// ---------------------------------------------------------------------------
+// Zlm[n,u] = m_l + log sum_v e^{lm[u,v] - m_l}: one wave per row u <= U_n.
+__global__ __launch_bounds__(256) void lm_lse_kernel(SimpleArgs a) {
+  const int U1 = a.b.U + 1, V = a.V;
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (row >= a.b.N * U1) return;
+  const int n = row / U1, u = row - n * U1;
+  int Tn, Un;
+  utt_dims(a.b, n, Tn, Un);
+  if (u > Un) {
+    if (lane == 0) a.Zlm[row] = 0.f;
+    return;
+  }
+  const float* x = a.lm + (size_t)row * V;
+  const float m = a.m_l[row];
+  float sum = 0.f;
+  for (int v = lane; v < V; v += 64) sum += expf(x[v] - m);
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) sum += __shfl_xor(sum, off, 64);
+  if (lane == 0) a.Zlm[row] = m + logf(sum);
+}
+
+// lavg[n,v] = log (1/(U_n+1)) sum_{u <= U_n} e^{lm[u,v] - Zlm[u]}: threads over v.
+__global__ __launch_bounds__(256) void lm_avg_kernel(SimpleArgs a) {
+  const int n = blockIdx.y, V = a.V, U1 = a.b.U + 1;
+  const int v = blockIdx.x * blockDim.x + threadIdx.x;
+  if (v >= V) return;
+  int Tn, Un;
+  utt_dims(a.b, n, Tn, Un);
+  const float* lmn = a.lm + (size_t)n * U1 * V;
+  const float* z = a.Zlm + (size_t)n * U1;
+  float s = 0.f;
+  for (int u = 0; u <= Un; ++u) s += expf(lmn[(size_t)u * V + v] - z[u]);
+  a.lavg[(size_t)n * V + v] = logf(s / (float)(Un + 1));
+}
+
+// Zac[n,t] = log sum_v e^{am[t,v] + lavg[v]}: one wave per frame t < T_n.
+__global__ __launch_bounds__(256) void ac_lse_kernel(SimpleArgs a) {
+  const int T = a.b.T, V = a.V;
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (row >= a.b.N * T) return;
+  const int n = row / T, t = row - n * T;
+  int Tn, Un;
+  utt_dims(a.b, n, Tn, Un);
+  if (t >= Tn) {
+    if (lane == 0) a.Zac[row] = 0.f;
+    return;
+  }
+  const float* x = a.am + (size_t)row * V;
+  const float* la = a.lavg + (size_t)n * V;
+  float m = kNegInfF;
+  for (int v = lane; v < V; v += 64) m = fmaxf(m, x[v] + la[v]);
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) m = fmaxf(m, __shfl_xor(m, off, 64));
+  float sum = 0.f;
+  for (int v = lane; v < V; v += 64) sum += expf(x[v] + la[v] - m);
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) sum += __shfl_xor(sum, off, 64);
+  if (lane == 0) a.Zac[row] = m + logf(sum);
+}
+
+// Gx[n,u], Gy[n,u]: column sums of the occupations over frames, from the
+// per-16-frame partials in fixed order (fp64).
+__global__ __launch_bounds__(256) void colsum_kernel(SimpleArgs a) {
+  const int U1 = a.b.U + 1;
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= a.b.N * U1) return;
+  const int n = i / U1, u = i - n * U1;
+  const double* px_ = a.cpx + (size_t)n * a.ncolblk * U1 + u;
+  const double* py_ = a.cpy + (size_t)n * a.ncolblk * U1 + u;
+  double cx = 0.0, cy = 0.0;
+  for (int q = 0; q < a.ncolblk; ++q) {
+    cx += px_[(size_t)q * U1];
+    cy += py_[(size_t)q * U1];
+  }
+  a.Gx[i] = cx;
+  a.Gy[i] = cy;
+}
+
+// q[n,v] = (sum_t R(t) P_ac[t,v] - Sy(v)) / ((U_n+1) e^{lavg[v]}): threads over v.
+__global__ __launch_bounds__(256) void ac_colsum_kernel(SimpleArgs a) {
+  const int n = blockIdx.y, V = a.V, T = a.b.T, U1 = a.b.U + 1;
+  const int v = blockIdx.x * blockDim.x + threadIdx.x;
+  if (v >= V) return;
+  int Tn, Un;
+  utt_dims(a.b, n, Tn, Un);
+  const float* amn = a.am + (size_t)n * T * V;
+  const float la = a.lavg[(size_t)n * V + v];
+  double g = 0.0;
+  for (int t = 0; t < Tn; ++t) {
+    const double R = a.rx[(size_t)n * T + t] + a.ry[(size_t)n * T + t];
+    g += R * (double)expf(amn[(size_t)t * V + v] + la - a.Zac[(size_t)n * T + t]);
+  }
+  for (int u = 0; u < Un; ++u) {
+    bool ok = true;
+    if (symbol_at(a.b, n, u, V, ok) == v) g -= a.Gx[(size_t)n * U1 + u];
+  }
+  if (v == a.b.blank)
+    for (int u = 0; u <= Un; ++u) g -= a.Gy[(size_t)n * U1 + u];
+  a.q[(size_t)n * V + v] = (float)(g / ((double)(Un + 1) * (double)expf(la)));
+}
+
+// su[n,u] = sum_v q[v] e^{lm[u,v] - Zlm[u]}: one wave per row u <= U_n.
+__global__ __launch_bounds__(256) void lm_s_kernel(SimpleArgs a) {
+  const int U1 = a.b.U + 1, V = a.V;
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (row >= a.b.N * U1) return;
+  const int n = row / U1, u = row - n * U1;
+  int Tn, Un;
+  utt_dims(a.b, n, Tn, Un);
+  if (u > Un) return;
+  const float* x = a.lm + (size_t)row * V;
+  const float* qn = a.q + (size_t)n * V;
+  const float z = a.Zlm[row];
+  float sum = 0.f;
+  for (int v = lane; v < V; v += 64) sum += qn[v] * expf(x[v] - z);
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) sum += __shfl_xor(sum, off, 64);
+  if (lane == 0) a.su[row] = sum;
 }
 
 // Loads x[row][k..k+3] and the row max for exp(x - max); positions beyond the
@@ -177,10 +312,20 @@ __global__ __launch_bounds__(256) void normalizer_epi_kernel(SimpleArgs a) {
   const float* lmu = a.lm + ((size_t)n * U1 + u) * V;
   const int blank = a.b.blank;
   a.Z[idx] = z;
-  a.py[idx] = amt[blank] + lmu[blank] - z;
   bool ok = true;
   const int y = (u < Un) ? symbol_at(a.b, n, u, V, ok) : 0;
-  a.px[idx] = (u < Un) ? amt[y] + lmu[y] - z : kNegInfF;
+  float py = amt[blank] + lmu[blank] - z;
+  float px = amt[y] + lmu[y] - z;
+  if (a.lm_only != 0.f || a.am_only != 0.f) {
+    // smoothed joiner: c L_trivial + a L_lm + b L_acoustic (Sec. 3.3.1)
+    const float c = 1.f - a.lm_only - a.am_only;
+    const float zl = a.Zlm[(size_t)n * U1 + u], za = a.Zac[(size_t)n * T + t];
+    const float* la = a.lavg + (size_t)n * V;
+    py = c * py + a.lm_only * (lmu[blank] - zl) + a.am_only * (amt[blank] + la[blank] - za);
+    px = c * px + a.lm_only * (lmu[y] - zl) + a.am_only * (amt[y] + la[y] - za);
+  }
+  a.py[idx] = py;
+  a.px[idx] = (u < Un) ? px : kNegInfF;
 }
 
 // ---------------------------------------------------------------------------
@@ -229,7 +374,10 @@ __global__ __launch_bounds__(256) void dam_kernel(SimpleArgs a) {
   const float* ma = a.m_a + (size_t)n * T;
   const float* gxn = a.gx + (size_t)n * T * U1;
   float* out = a.am_grad + (size_t)n * T * V;
-  // dense part: e^{am - m_a} * acc
+  const bool smooth = a.lm_only != 0.f || a.am_only != 0.f;
+  const float c = 1.f - a.lm_only - a.am_only;  // weight of the trivial joiner
+  const float ks = 1.f - a.lm_only;             // weight of the target/blank terms
+  // dense part: c e^{am - m_a} * acc (+ b R(t) P_ac[t,v] when smoothed)
   float res[Cfg::FM][Cfg::FN][4];
 #pragma unroll
   for (int i = 0; i < Cfg::FM; ++i)
@@ -238,10 +386,18 @@ __global__ __launch_bounds__(256) void dam_kernel(SimpleArgs a) {
       const int t = t0 + tile_row<Cfg>(i, r);
       const bool tv = active && t < Tn;
       const float mx = tv ? ma[t] : 0.f;
+      const float bR = (tv && smooth) ? a.am_only * (float)(a.rx[(size_t)n * T + t] + a.ry[(size_t)n * T + t]) : 0.f;
+      const float za = (tv && smooth) ? a.Zac[(size_t)n * T + t] : 0.f;
 #pragma unroll
       for (int j = 0; j < Cfg::FN; ++j) {
         const int v = v0 + tile_col<Cfg>(j);
-        res[i][j][r] = (tv && v < V) ? expf(amn[(size_t)t * V + v] - mx) * acc[i][j][r] : 0.f;
+        float d = 0.f;
+        if (tv && v < V) {
+          const float x = amn[(size_t)t * V + v];
+          d = c * expf(x - mx) * acc[i][j][r];
+          if (smooth) d += bR * expf(x + a.lavg[(size_t)n * V + v] - za);
+        }
+        res[i][j][r] = d;
       }
     }
   if (active) {
@@ -258,7 +414,7 @@ __global__ __launch_bounds__(256) void dam_kernel(SimpleArgs a) {
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
             const int t = t0 + tile_row<Cfg>(i, r);
-            if (t < Tn) res[i][j][r] -= gxn[(size_t)t * U1 + u];
+            if (t < Tn) res[i][j][r] -= ks * gxn[(size_t)t * U1 + u];
           }
       }
     }
@@ -272,7 +428,7 @@ __global__ __launch_bounds__(256) void dam_kernel(SimpleArgs a) {
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
             const int t = t0 + tile_row<Cfg>(i, r);
-            if (t < Tn) res[i][j][r] = (float)((double)res[i][j][r] - a.ry[(size_t)n * T + t]);
+            if (t < Tn) res[i][j][r] = (float)((double)res[i][j][r] - (double)ks * a.ry[(size_t)n * T + t]);
           }
       }
     }
@@ -368,24 +524,25 @@ __global__ __launch_bounds__(256) void dlm_epi_kernel(SimpleArgs a) {
   const float* lmr = a.lm + (size_t)row * V;
   const size_t stride = (size_t)a.b.N * U1 * V;
   const size_t base = (size_t)row * V;
+  const bool smooth = a.lm_only != 0.f || a.am_only != 0.f;
+  const float cw = 1.f - a.lm_only - a.am_only;  // weight of the trivial joiner
+  const double ks = 1.0 - (double)a.am_only;      // weight of the target/blank terms
+  // the target and blank columns collect Gx(u) = sum_t gx(t,u) and Gy(u) (fp64)
+  const double gx = a.Gx[row], gy = a.Gy[row];
+  const float zl = smooth ? a.Zlm[row] : 0.f;
+  const float aG = smooth ? a.lm_only * (float)(gx + gy) : 0.f;
+  const float su = smooth ? a.su[row] : 0.f;
   for (int v = v0; v < min(V, v0 + 4); ++v) {
     float c = 0.f;
     for (int q = 0; q < a.lsplit; ++q) c += a.lpart[(size_t)q * stride + base + v];
-    // The target and blank columns collect sum_t gx(t,u) and sum_t gy(t,u):
-    // added from the per-16-frame partials in fixed order, in fp64, and
-    // rounded once.
-    double gd = (double)(expf(lmr[v] - ml) * c);
-    if (v == y || v == blank) {
-      double cx = 0.0, cy = 0.0;
-      const double* px_ = a.cpx + (size_t)n * a.ncolblk * U1 + u;
-      const double* py_ = a.cpy + (size_t)n * a.ncolblk * U1 + u;
-      for (int q = 0; q < a.ncolblk; ++q) {
-        cx += px_[(size_t)q * U1];
-        cy += py_[(size_t)q * U1];
-      }
-      if (v == y) gd -= cx;
-      if (v == blank) gd -= cy;
+    float d = cw * expf(lmr[v] - ml) * c;
+    if (smooth) {
+      const float p = expf(lmr[v] - zl);
+      d += aG * p + a.am_only * p * (a.q[(size_t)n * V + v] - su);
     }
+    double gd = (double)d;
+    if (v == y) gd -= ks * gx;
+    if (v == blank) gd -= ks * gy;
     out[v] = (float)(sc * gd);
   }
 }
@@ -446,8 +603,29 @@ hipError_t launch_normalizer(const SimpleArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
+hipError_t launch_smoothing_stats(const SimpleArgs& a, hipStream_t s) {
+  if (a.lm_only == 0.f && a.am_only == 0.f) return hipSuccess;
+  const int N = a.b.N, T = a.b.T, U1 = a.b.U + 1;
+  {
+    RNNT_PROF(s, "smooth_stats");
+    hipLaunchKernelGGL(lm_lse_kernel, dim3((N * U1 + 3) / 4), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(lm_avg_kernel, dim3((a.V + 255) / 256, N), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(ac_lse_kernel, dim3((N * T + 3) / 4), dim3(256), 0, s, a);
+  }
+  return hipGetLastError();
+}
+
 hipError_t launch_simple_grads(const SimpleArgs& a, hipStream_t s) {
   const int T = a.b.T, U1 = a.b.U + 1, V = a.V;
+  {
+    RNNT_PROF(s, "simple_colsum");
+    hipLaunchKernelGGL(colsum_kernel, dim3((a.b.N * U1 + 255) / 256), dim3(256), 0, s, a);
+  }
+  if (a.lm_only != 0.f || a.am_only != 0.f) {
+    RNNT_PROF(s, "smooth_grad_stats");
+    hipLaunchKernelGGL(ac_colsum_kernel, dim3((V + 255) / 256, a.b.N), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(lm_s_kernel, dim3((a.b.N * U1 + 3) / 4), dim3(256), 0, s, a);
+  }
   if (a.am_grad) {
     dim3 grid((T + DamCfg::BM - 1) / DamCfg::BM, (V + DamCfg::BN - 1) / DamCfg::BN, a.b.N);
     {

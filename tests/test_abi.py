@@ -41,7 +41,7 @@ def test_library_exports_every_declared_symbol(L):
     missing = [n for n in _declared() if not hasattr(L, n)]
     assert not missing, f"not exported: {missing}"
     assert set(_declared()) == set(_native.SIGNATURES), "binding signatures out of sync with the header"
-    assert L.rnnt_abi_version() == 2
+    assert L.rnnt_abi_version() == 3
 
 
 def test_workspace_queries(L):
@@ -87,17 +87,21 @@ def test_validation_statuses(L):
     # simple loss: blank outside [0, V)
     b2 = _batch()
     b2.blank = 16
-    assert L.rnnt_simple_loss(ctypes.byref(b2), 16, fake, fake, None, fake, fake, fake, None, None, None, None,
+    assert L.rnnt_simple_loss(ctypes.byref(b2), 16, fake, fake, None, 0.0, 0.0, fake, fake, fake, None, None, None, None,
                               fake, 1 << 30, None) == N.RNNT_EINVAL
     # simple loss: workspace missing / too small / misaligned
-    assert L.rnnt_simple_loss(pb, 16, fake, fake, None, fake, fake, fake, None, None, None, None,
+    assert L.rnnt_simple_loss(pb, 16, fake, fake, None, 0.0, 0.0, fake, fake, fake, None, None, None, None,
                               None, 0, None) == N.RNNT_EWORKSPACE
-    assert L.rnnt_simple_loss(pb, 16, fake, fake, None, fake, fake, fake, None, None, None, None,
+    assert L.rnnt_simple_loss(pb, 16, fake, fake, None, 0.0, 0.0, fake, fake, fake, None, None, None, None,
                               fake, 16, None) == N.RNNT_EWORKSPACE
-    assert L.rnnt_simple_loss(pb, 16, fake, fake, None, fake, fake, fake, None, None, None, None,
+    assert L.rnnt_simple_loss(pb, 16, fake, fake, None, 0.0, 0.0, fake, fake, fake, None, None, None, None,
                               ctypes.c_void_p(0x4004), 1 << 30, None) == N.RNNT_EWORKSPACE
+    # smoothing weights outside a_lm, a_ac >= 0, a_lm + a_ac <= 1
+    for w in ((-0.1, 0.0), (0.0, -0.5), (0.7, 0.4)):
+        assert L.rnnt_simple_loss(pb, 16, fake, fake, None, w[0], w[1], fake, fake, fake, None, None, None, None,
+                                  fake, 1 << 30, None) == N.RNNT_EINVAL
     # px without py
-    assert L.rnnt_simple_loss(pb, 16, fake, fake, None, fake, fake, fake, fake, None, None, None,
+    assert L.rnnt_simple_loss(pb, 16, fake, fake, None, 0.0, 0.0, fake, fake, fake, fake, None, None, None,
                               fake, 1 << 30, None) == N.RNNT_EINVAL
     # negative sizes
     bad = _batch(N=0)
