@@ -62,6 +62,38 @@ def _traffic(kernel: str, workload: str):
     return int(1024 * (k["fetch_kib"] * rec["fetch_scale"] + k["write_kib"] * rec["write_scale"]))
 
 
+def _unpruned(P, batch, enc, dec, W, bias, frames, dev, steps: int = 5) -> dict:
+    """The unpruned loss with the same joiner at every (t, u), its (N, T, U+1, V)
+    logits kept (as a framework materialising them would), on the same batch:
+    the comparison of the method's speed and memory claims (Sec. 1, Sec. 3.2)."""
+    import torch
+    N, T, U = batch.N, batch.T, batch.U
+    J, V = int(W.shape[0]), int(W.shape[1])
+    torch.cuda.synchronize()
+    base = torch.cuda.memory_allocated(dev)
+    torch.cuda.reset_peak_memory_stats(dev)
+    f32 = dict(dtype=torch.float32, device=dev)
+    bufs = dict(loss=torch.empty(N, **f32), enc_grad=torch.empty(N, T, J, **f32),
+                dec_grad=torch.empty(N, U + 1, J, **f32), W_grad=torch.empty(J, V, **f32),
+                bias_grad=torch.empty(V, **f32), logits=torch.empty(N, T, U + 1, V, **f32))
+    ws = torch.empty(P.full_loss_workspace_size(N, T, U, J, V, P._jdtype(W)), dtype=torch.uint8, device=dev)
+    P.rnnt_full_loss(batch, enc, dec, W, bias, workspace=ws, **bufs)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        P.rnnt_full_loss(batch, enc, dec, W, bias, workspace=ws, **bufs)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    peak = torch.cuda.max_memory_allocated(dev) - base
+    del bufs, ws
+    torch.cuda.empty_cache()
+    return {"what": "unpruned RNN-T loss + gradients, same joiner at every (t, u), logits [N,T,U+1,V] kept",
+            "ms_per_step": round(ms, 4), "frames_per_s": round(frames / (ms / 1000.0), 1),
+            "peak_hbm_bytes_excl_inputs": int(peak), "steps": steps}
+
+
 def _cpu_baseline(b, S, budget_s: float) -> dict:
     """The CPU oracle (as is) on the first utterances of the same batch, one thread."""
     import numpy as np
@@ -98,6 +130,8 @@ def main() -> int:
     ap.add_argument("--workload", default="bpe", choices=sorted(WORKLOAD_TEXT))
     ap.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of oracle work for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-unpruned", action="store_true",
+                    help="skip the comparison with the unpruned loss (same joiner at every (t, u))")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="before the census, run one device-to-device copy of this many MiB (a plain copy "
                          "kernel of known size that scales rocprofv3's FETCH_SIZE / WRITE_SIZE)")
@@ -212,6 +246,7 @@ def main() -> int:
                 "algorithmic_flops_per_launch": per_launch_flops, "avg_launch_us": timed["avg_us"],
                 "launches_timed": timed["launches"]}
 
+    unpruned = None if args.no_unpruned else _unpruned(P, batch, enc, dec, W, bias, frames, dev)
     cpu = None if args.no_cpu_baseline else _cpu_baseline(b, S, args.cpu_budget)
     line = {
         "metric": "pruned RNN-T loss fwd+bwd frames/sec at V=500,S=5; peak HBM bytes",
@@ -232,6 +267,7 @@ def main() -> int:
         "peak_hbm_bytes_excl_inputs": int(peak - inputs_mem),
         "wall_s_timed": round(wall, 3),
         "roofline": roofline,
+        "unpruned": unpruned,
         "kernels": kernels,
         "kernels_census_steps": census_steps,
         "cpu_baseline": cpu,

@@ -242,6 +242,34 @@ int rnnt_pruned_joiner_backward(const rnnt_batch* batch, int32_t S, int32_t J, i
                                 void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------ */
+/* For comparison: the unpruned loss with the same joiner                    */
+/* ------------------------------------------------------------------------ */
+
+/* Workspace bytes for rnnt_full_loss. */
+size_t rnnt_full_loss_workspace_size(int32_t N, int32_t T, int32_t U, int32_t J, int32_t V, int32_t dtype);
+
+/* The RNN-T loss of Sec. 2 with the full joiner evaluated at every (t, u) of
+ * the lattice, the (N, T, U+1, V) computation that the pruned loss avoids
+ * (Sec. 1, Sec. 3.2), and its gradients: the same joiner, recursion and
+ * backward kernels as the pruned path, with every row of the lattice as the
+ * "band" (S = U+1, all p_t = 0). It is the in-library comparison for the
+ * method's memory and speed claims.
+ *
+ * enc, dec, W, bias, dtype: as in rnnt_pruned_joiner. scale [N] (nullable).
+ * Outputs: loss [N] fp32 (required); enc_grad [N, T, J], dec_grad [N, U+1, J]
+ *   (required, 16-byte aligned); W_grad [J, V], bias_grad [V] (nullable);
+ *   logits [N, T, U+1, V] fp32 (nullable, 16-byte aligned): when given, the
+ *   unpruned logits are stored and streamed by the backward, as a framework
+ *   that materialises them would; when null they are recomputed in row
+ *   chunks.
+ */
+int rnnt_full_loss(const rnnt_batch* batch, int32_t J, int32_t V, int32_t dtype,
+                   const void* enc, const void* dec, const void* W, const void* bias,
+                   const float* scale, float* loss, float* enc_grad, float* dec_grad,
+                   float* W_grad, float* bias_grad, float* logits,
+                   void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------ */
 /* Kernel timing (opt-in; for benchmarks and profiling)                      */
 /* ------------------------------------------------------------------------ */
 

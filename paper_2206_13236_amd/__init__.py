@@ -19,7 +19,7 @@ from ._native import (RNNT_BF16, RNNT_EHIP, RNNT_EINVAL, RNNT_EUNSUPPORTED, RNNT
 
 __all__ = [
     "Batch", "RnntError", "rnnt_simple_loss", "rnnt_simple_loss_backward", "rnnt_prune_ranges",
-    "rnnt_pruned_joiner", "pruned_rnnt_loss",
+    "rnnt_pruned_joiner", "pruned_rnnt_loss", "rnnt_full_loss", "full_loss_workspace_size",
     "rnnt_pruned_loss", "rnnt_pruned_joiner_backward", "simple_loss_workspace_size",
     "pruned_joiner_workspace_size", "pruned_loss_workspace_size",
     "pruned_joiner_backward_workspace_size", "PrunedRnntLoss", "RNNT_F32", "RNNT_BF16",
@@ -245,6 +245,39 @@ def rnnt_pruned_joiner_backward(batch: Batch, S: int, enc, dec, W, bias, ranges,
         _p(ws), ws.numel(), _stream(stream)))
     return {"enc_grad": enc_grad, "dec_grad": dec_grad, "W_grad": W_grad, "bias_grad": bias_grad,
             "logits_grad": logits_grad}
+
+
+def full_loss_workspace_size(N, T, U, J, V, dtype) -> int:
+    return int(lib().rnnt_full_loss_workspace_size(N, T, U, J, V, dtype))
+
+
+def rnnt_full_loss(batch: Batch, enc, dec, W, bias=None, scale=None, keep_logits: bool = False, loss=None,
+                   enc_grad=None, dec_grad=None, W_grad=None, bias_grad=None, logits=None, workspace=None,
+                   stream=None) -> dict:
+    """The unpruned RNN-T loss with the same joiner at every (t, u), and its gradients."""
+    N, T, U = batch.N, batch.T, batch.U
+    J, V = int(W.shape[0]), int(W.shape[1])
+    dt = _jdtype(W)
+    _need(enc, "enc", W.dtype, (N, T, J))
+    _need(dec, "dec", W.dtype, (N, U + 1, J))
+    if bias is not None:
+        _need(bias, "bias", W.dtype, (V,))
+    if scale is not None:
+        _need(scale, "scale", torch.float32, (N,))
+    f32 = dict(dtype=torch.float32, device=batch.device)
+    loss = torch.empty(N, **f32) if loss is None else loss
+    enc_grad = torch.empty(N, T, J, **f32) if enc_grad is None else enc_grad
+    dec_grad = torch.empty(N, U + 1, J, **f32) if dec_grad is None else dec_grad
+    W_grad = torch.empty(J, V, **f32) if W_grad is None else W_grad
+    bias_grad = torch.empty(V, **f32) if bias_grad is None else bias_grad
+    if keep_logits and logits is None:
+        logits = torch.empty(N, T, U + 1, V, **f32)
+    ws = _ws(full_loss_workspace_size(N, T, U, J, V, dt), batch.device, workspace)
+    check(lib().rnnt_full_loss(batch.c, J, V, dt, _p(enc), _p(dec), _p(W), _p(bias), _p(scale), _p(loss),
+                               _p(enc_grad), _p(dec_grad), _p(W_grad), _p(bias_grad), _p(logits), _p(ws),
+                               ws.numel(), _stream(stream)))
+    return {"loss": loss, "enc_grad": enc_grad, "dec_grad": dec_grad, "W_grad": W_grad, "bias_grad": bias_grad,
+            "logits": logits}
 
 
 class PrunedRnntLoss:

@@ -59,6 +59,10 @@ SIGNATURES = {
                                               c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
                                               c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
                                               c_void_p, c_size_t, c_void_p]),
+    "rnnt_full_loss_workspace_size": (c_size_t, [c_int32] * 6),
+    "rnnt_full_loss": (c_int32, [POINTER(RnntBatch), c_int32, c_int32, c_int32, c_void_p, c_void_p, c_void_p,
+                                 c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
+                                 c_void_p, c_size_t, c_void_p]),
     "rnnt_profile_enable": (c_int32, [c_int32]),
     "rnnt_profile_select": (c_int32, [c_char_p]),
     "rnnt_profile_reset": (c_int32, []),

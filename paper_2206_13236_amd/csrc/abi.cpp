@@ -260,6 +260,96 @@ int check_joiner_sizes(const rnnt_batch* b, int S, int J, int V, int dtype) {
   return RNNT_OK;
 }
 
+JoinerArgs joiner_args(const rnnt_batch* batch, int S, int J, int V, int dtype, const void* enc, const void* dec,
+                       const void* W, const void* bias, const int32_t* ranges) {
+  JoinerArgs a{};
+  a.b = to_dev(batch);
+  a.S = S;
+  a.J = J;
+  a.V = V;
+  a.bf16 = dtype == RNNT_BF16;
+  a.enc = enc;
+  a.dec = dec;
+  a.W = W;
+  a.bias = bias;
+  a.ranges = ranges;
+  return a;
+}
+
+void set_joiner_fwd(JoinerArgs& a, const JoinerFwdWs& w, float* px, float* py, float* lse, float* logits) {
+  a.frame_off = w.frame_off;
+  a.rowinfo = w.rowinfo;
+  a.part = w.part;
+  a.nparts = joiner_nparts(a.V);
+  a.tgt = w.tgt;
+  a.blk = w.blk;
+  a.px = px;
+  a.py = py;
+  a.lse = lse;
+  a.logits = logits;
+}
+
+void set_joiner_bwd(JoinerArgs& a, const JoinerBwdWs& w, const float* lse, const float* logits, const float* gx,
+                    const float* gy, const float* scale, float* enc_grad, float* dec_grad, float* W_grad,
+                    float* bias_grad, float* logits_grad) {
+  a.frame_off = w.frame_off;
+  a.rowinfo = w.rowinfo;
+  a.lse_in = lse;
+  a.logits_in = logits;
+  a.gxo = gx;
+  a.gyo = gy;
+  a.scale = scale;
+  a.dl = w.dl;
+  a.ldl = joiner_ldl(a.V);
+  a.chunk_rows = w.chunk_rows;
+  a.dpre = w.dpre;
+  a.hbuf = w.hbuf;
+  a.dw_part = w.dw_part;
+  a.splits = w.splits;
+  a.db_part = w.db_part;
+  a.n_db_rows = w.n_db_rows;
+  a.enc_grad = enc_grad;
+  a.dec_grad = dec_grad;
+  a.W_grad = W_grad;
+  a.bias_grad = bias_grad;
+  a.logits_grad = logits_grad;
+}
+
+// Workspace of rnnt_full_loss: the lattice-sized arrays, then one region
+// that the joiner's forward and backward use in turn.
+struct FullWs {
+  int* ranges;
+  float *px, *py, *lse, *gx, *gy;
+  double *alpha, *beta, *Lutt, *ry, *rx, *cpx, *cpy;
+  void* joiner;
+  size_t bytes;
+};
+
+FullWs full_layout(void* base, int N, int T, int U, int J, int V, int bf16) {
+  Carve c(base);
+  FullWs w;
+  const int S = U + 1;
+  const size_t L = (size_t)N * T * S;
+  w.ranges = c.take<int>(L);
+  w.px = c.take<float>(L);
+  w.py = c.take<float>(L);
+  w.lse = c.take<float>(L);
+  w.gx = c.take<float>(L);
+  w.gy = c.take<float>(L);
+  w.alpha = c.take<double>(L);
+  w.beta = c.take<double>(L);
+  w.Lutt = c.take<double>((size_t)N);
+  w.ry = c.take<double>((size_t)N * T);
+  w.rx = c.take<double>((size_t)N * T);
+  w.cpx = c.take<double>((size_t)N * lattice_colblocks(T) * S);
+  w.cpy = c.take<double>((size_t)N * lattice_colblocks(T) * S);
+  const size_t jf = joiner_fwd_layout(nullptr, N, T, S, V).bytes;
+  const size_t jb = joiner_bwd_layout(nullptr, N, T, S, J, V, bf16).bytes;
+  w.joiner = c.take<unsigned char>(jf > jb ? jf : jb);
+  w.bytes = c.off;
+  return w;
+}
+
 }  // namespace
 
 extern "C" {
@@ -368,27 +458,8 @@ int rnnt_pruned_joiner(const rnnt_batch* batch, int32_t S, int32_t J, int32_t V,
   rc = check_ws(workspace, workspace_bytes, joiner_fwd_layout(nullptr, batch->N, batch->T, S, V).bytes);
   if (rc) return rc;
   const JoinerFwdWs w = joiner_fwd_layout(workspace, batch->N, batch->T, S, V);
-  JoinerArgs a{};
-  a.b = to_dev(batch);
-  a.S = S;
-  a.J = J;
-  a.V = V;
-  a.bf16 = dtype == RNNT_BF16;
-  a.enc = enc;
-  a.dec = dec;
-  a.W = W;
-  a.bias = bias;
-  a.ranges = ranges;
-  a.frame_off = w.frame_off;
-  a.rowinfo = w.rowinfo;
-  a.part = w.part;
-  a.nparts = joiner_nparts(V);
-  a.tgt = w.tgt;
-  a.blk = w.blk;
-  a.px = px;
-  a.py = py;
-  a.lse = lse;
-  a.logits = logits;
+  JoinerArgs a = joiner_args(batch, S, J, V, dtype, enc, dec, W, bias, ranges);
+  set_joiner_fwd(a, w, px, py, lse, logits);
   hipStream_t s = static_cast<hipStream_t>(stream);
   hipError_t e = launch_joiner_prep(a, s);
   if (e == hipSuccess) e = launch_joiner_fwd(a, s);
@@ -462,42 +533,77 @@ int rnnt_pruned_joiner_backward(const rnnt_batch* batch, int32_t S, int32_t J, i
   rc = check_ws(workspace, workspace_bytes, joiner_bwd_layout(nullptr, batch->N, batch->T, S, J, V, bf).bytes);
   if (rc) return rc;
   const JoinerBwdWs w = joiner_bwd_layout(workspace, batch->N, batch->T, S, J, V, bf);
-  JoinerArgs a{};
-  a.b = to_dev(batch);
-  a.S = S;
-  a.J = J;
-  a.V = V;
-  a.bf16 = bf;
-  a.enc = enc;
-  a.dec = dec;
-  a.W = W;
-  a.bias = bias;
-  a.ranges = ranges;
-  a.frame_off = w.frame_off;
-  a.rowinfo = w.rowinfo;
-  a.lse_in = lse;
-  a.logits_in = logits;
-  a.gxo = px_occ;
-  a.gyo = py_occ;
-  a.scale = scale;
-  a.dl = w.dl;
-  a.ldl = joiner_ldl(V);
-  a.chunk_rows = w.chunk_rows;
-  a.dpre = w.dpre;
-  a.hbuf = w.hbuf;
-  a.dw_part = w.dw_part;
-  a.splits = w.splits;
-  a.db_part = w.db_part;
-  a.n_db_rows = w.n_db_rows;
-  a.enc_grad = enc_grad;
-  a.dec_grad = dec_grad;
-  a.W_grad = W_grad;
-  a.bias_grad = bias_grad;
-  a.logits_grad = logits_grad;
+  JoinerArgs a = joiner_args(batch, S, J, V, dtype, enc, dec, W, bias, ranges);
+  set_joiner_bwd(a, w, lse, logits, px_occ, py_occ, scale, enc_grad, dec_grad, W_grad, bias_grad, logits_grad);
   hipStream_t s = static_cast<hipStream_t>(stream);
   hipError_t e = launch_joiner_prep(a, s);
   if (e == hipSuccess) e = launch_joiner_bwd(a, s);
   return hip_status(e, "rnnt_pruned_joiner_backward");
+}
+
+size_t rnnt_full_loss_workspace_size(int32_t N, int32_t T, int32_t U, int32_t J, int32_t V, int32_t dtype) {
+  if (N < 1 || T < 1 || U < 0 || J < 1 || V < 1) return 0;
+  return full_layout(nullptr, N, T, U, J, V, dtype == RNNT_BF16).bytes;
+}
+
+int rnnt_full_loss(const rnnt_batch* batch, int32_t J, int32_t V, int32_t dtype, const void* enc, const void* dec,
+                   const void* W, const void* bias, const float* scale, float* loss, float* enc_grad,
+                   float* dec_grad, float* W_grad, float* bias_grad, float* logits, void* workspace,
+                   size_t workspace_bytes, void* stream) {
+  int rc = check_batch(batch, true);
+  if (rc) return rc;
+  const int S = batch->U + 1;
+  if (V < 1) return fail(RNNT_EINVAL, "V must be >= 1 (got %d)", V);
+  if (batch->blank < 0 || batch->blank >= V) return fail(RNNT_EINVAL, "blank = %d outside [0, V)", batch->blank);
+  if (J < 8 || J % 8 != 0) return fail(RNNT_EUNSUPPORTED, "J = %d must be a positive multiple of 8", J);
+  if (dtype != RNNT_F32 && dtype != RNNT_BF16) return fail(RNNT_EINVAL, "dtype must be RNNT_F32 or RNNT_BF16");
+  const long long esz = dtype == RNNT_BF16 ? 2 : 4;
+  if ((long long)batch->N * batch->T * S > kI32 || (long long)batch->N * batch->T * J * esz > kI32 ||
+      (long long)batch->N * S * J * esz > kI32 || (long long)J * V * esz > kI32 ||
+      (long long)batch->N * batch->T * S * J * 4 > (1ll << 40))
+    return fail(RNNT_EUNSUPPORTED, "the unpruned joiner is too large for this build");
+  if (!enc || !dec || !W || !loss) return fail(RNNT_EINVAL, "enc, dec, W and loss are required");
+  if (!enc_grad || !dec_grad) return fail(RNNT_EINVAL, "enc_grad and dec_grad are required");
+  if (!aligned16(enc_grad) || !aligned16(dec_grad) || !aligned16(logits))
+    return fail(RNNT_EINVAL, "enc_grad, dec_grad and logits must be 16-byte aligned");
+  const int bf = dtype == RNNT_BF16;
+  const FullWs need = full_layout(nullptr, batch->N, batch->T, batch->U, J, V, bf);
+  rc = check_ws(workspace, workspace_bytes, need.bytes);
+  if (rc) return rc;
+  const FullWs w = full_layout(workspace, batch->N, batch->T, batch->U, J, V, bf);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  // the joiner on every (t, u): ranges[n,t,s] = s with S = U + 1
+  hipError_t e = launch_full_ranges(w.ranges, batch->N, batch->T, S, s);
+  JoinerArgs jf = joiner_args(batch, S, J, V, dtype, enc, dec, W, bias, w.ranges);
+  set_joiner_fwd(jf, joiner_fwd_layout(w.joiner, batch->N, batch->T, S, V), w.px, w.py, w.lse, logits);
+  if (e == hipSuccess) e = launch_joiner_prep(jf, s);
+  if (e == hipSuccess) e = launch_joiner_fwd(jf, s);
+  // the recursion of Eq. (3) on the [T, U+1] lattice and its occupations
+  SimpleArgs la{};
+  la.b = to_dev(batch);
+  la.V = V;
+  la.px = w.px;
+  la.py = w.py;
+  la.alpha = w.alpha;
+  la.beta = w.beta;
+  la.Lutt = w.Lutt;
+  la.loss = loss;
+  la.gx = w.gx;
+  la.gy = w.gy;
+  la.Wt = nullptr;
+  la.ry = w.ry;
+  la.rx = w.rx;
+  la.cpx = w.cpx;
+  la.cpy = w.cpy;
+  la.ncolblk = lattice_colblocks(batch->T);
+  if (e == hipSuccess) e = launch_lattice(la, s);
+  // the joiner's backward on every (t, u)
+  JoinerArgs jb = joiner_args(batch, S, J, V, dtype, enc, dec, W, bias, w.ranges);
+  set_joiner_bwd(jb, joiner_bwd_layout(w.joiner, batch->N, batch->T, S, J, V, bf), w.lse, logits, w.gx, w.gy,
+                 scale, enc_grad, dec_grad, W_grad, bias_grad, nullptr);
+  if (e == hipSuccess) e = launch_joiner_prep(jb, s);
+  if (e == hipSuccess) e = launch_joiner_bwd(jb, s);
+  return hip_status(e, "rnnt_full_loss");
 }
 
 }  // extern "C"

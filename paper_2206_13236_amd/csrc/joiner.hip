@@ -872,7 +872,22 @@ __global__ __launch_bounds__(256) void joiner_dec_kernel(JoinerArgs a) {
   }
 }
 
+// ranges[n,t,s] = s: every (t, u) of the lattice as a "band" of width U+1.
+__global__ __launch_bounds__(256) void full_ranges_kernel(int* ranges, size_t total, int S) {
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < total) ranges[i] = (int)(i % (size_t)S);
+}
+
 }  // namespace
+
+hipError_t launch_full_ranges(int* ranges, int N, int T, int S, hipStream_t s) {
+  const size_t total = (size_t)N * T * S;
+  {
+    RNNT_PROF(s, "full_ranges");
+    hipLaunchKernelGGL(full_ranges_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, ranges, total, S);
+  }
+  return hipGetLastError();
+}
 
 int joiner_nparts(int V) { return (V + 63) / 64; }
 int joiner_ldl(int V) { return (V + 7) / 8 * 8; }

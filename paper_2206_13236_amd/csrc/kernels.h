@@ -27,7 +27,7 @@ struct SimpleArgs {
   float* loss;         // [N]
   float* gx;           // [N, T, U+1]
   float* gy;
-  float* Wt;           // ws [N, T, ldw]: W(t,u) for the gradient (always written)
+  float* Wt;           // ws [N, T, ldw]: W(t,u) for the simple loss's gradient (null: not written)
   int ldw;
   double* ry;          // ws [N*T]      row sums of gy (fp64)
   double* cpx;         // ws [N, ncolblk, U+1]: column sums of gx over 16-frame blocks
@@ -107,6 +107,7 @@ struct JoinerArgs {
 };
 
 hipError_t launch_joiner_prep(const JoinerArgs& a, hipStream_t s);
+hipError_t launch_full_ranges(int* ranges, int N, int T, int S, hipStream_t s);
 hipError_t launch_joiner_fwd(const JoinerArgs& a, hipStream_t s);
 hipError_t launch_joiner_bwd(const JoinerArgs& a, hipStream_t s);
 int joiner_bwd_chunk_rows(int N, int T, int S, int J, int V, int bf16);

@@ -215,7 +215,7 @@ __global__ __launch_bounds__(64 * kOccFrames) void lattice_occ_kernel(SimpleArgs
   s = wave_sum_d(s);
   const double Lt = mx + log2(s);
   const bool trow = t < T;
-  const float mat = frow ? a.m_a[(size_t)n * T + t] : 0.f;
+  const float mat = (frow && a.Wt) ? a.m_a[(size_t)n * T + t] : 0.f;
   double ry = 0.0, rx = 0.0;
 #pragma unroll
   for (int c = 0; c < R; ++c) {
@@ -229,8 +229,9 @@ __global__ __launch_bounds__(64 * kOccFrames) void lattice_occ_kernel(SimpleArgs
       const size_t idx = base + (size_t)t * U1 + u;
       a.gx[idx] = gxv;
       a.gy[idx] = gyv;
-      a.Wt[((size_t)n * T + t) * a.ldw + u] =
-          (frow && u <= Un) ? (gxv + gyv) * expf(mat + a.m_l[(size_t)n * U1 + u] - a.Z[idx]) : 0.f;
+      if (a.Wt)
+        a.Wt[((size_t)n * T + t) * a.ldw + u] =
+            (frow && u <= Un) ? (gxv + gyv) * expf(mat + a.m_l[(size_t)n * U1 + u] - a.Z[idx]) : 0.f;
     }
     ry += (double)gyv;
     rx += (double)gxv;
@@ -252,7 +253,7 @@ __global__ __launch_bounds__(64 * kOccFrames) void lattice_occ_kernel(SimpleArgs
     }
   }
   if (trow) {
-    if (lane < a.ldw - U1) a.Wt[((size_t)n * T + t) * a.ldw + U1 + lane] = 0.f;
+    if (a.Wt && lane < a.ldw - U1) a.Wt[((size_t)n * T + t) * a.ldw + U1 + lane] = 0.f;
     ry = wave_sum_d(ry);
     rx = wave_sum_d(rx);
     if (lane == 0) {
