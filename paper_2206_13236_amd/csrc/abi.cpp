@@ -84,6 +84,8 @@ struct SimpleWs {
   float* Z;
   float* px;
   float* py;
+  float* pxd;
+  float* pyd;
   double* alpha;
   double* beta;
   double* Lutt;
@@ -115,10 +117,13 @@ SimpleWs simple_layout(void* base, int N, int T, int U, int V) {
   w.Z = c.take<float>(L);
   w.px = c.take<float>(L);
   w.py = c.take<float>(L);
-  w.alpha = c.take<double>(L);
-  w.beta = c.take<double>(L);
+  const size_t LD = (size_t)N * lattice_diag_cells(T, U);
+  w.pxd = c.take<float>(LD);
+  w.pyd = c.take<float>(LD);
+  w.alpha = c.take<double>(LD);
+  w.beta = c.take<double>(LD);
   w.Lutt = c.take<double>((size_t)N);
-  w.Wt =c.take<float>(NT * ldw_of(U));
+  w.Wt = c.take<float>(NT * ldw_of(U));
   w.ry = c.take<double>(NT);
   w.cpx = c.take<double>((size_t)N * lattice_colblocks(T) * (U + 1));
   w.cpy = c.take<double>((size_t)N * lattice_colblocks(T) * (U + 1));
@@ -160,6 +165,8 @@ SimpleArgs simple_args(const rnnt_batch* batch, int V, const float* am, const fl
   a.lsplit = w.lsplit;
   a.px = w.px;
   a.py = w.py;
+  a.pxd = w.pxd;
+  a.pyd = w.pyd;
   a.alpha = w.alpha;
   a.beta = w.beta;
   a.Lutt = w.Lutt;
@@ -319,7 +326,7 @@ void set_joiner_bwd(JoinerArgs& a, const JoinerBwdWs& w, const float* lse, const
 // that the joiner's forward and backward use in turn.
 struct FullWs {
   int* ranges;
-  float *px, *py, *lse, *gx, *gy;
+  float *px, *py, *lse, *gx, *gy, *pxd, *pyd;
   double *alpha, *beta, *Lutt, *ry, *rx, *cpx, *cpy;
   void* joiner;
   size_t bytes;
@@ -336,8 +343,11 @@ FullWs full_layout(void* base, int N, int T, int U, int J, int V, int bf16) {
   w.lse = c.take<float>(L);
   w.gx = c.take<float>(L);
   w.gy = c.take<float>(L);
-  w.alpha = c.take<double>(L);
-  w.beta = c.take<double>(L);
+  const size_t LD = (size_t)N * lattice_diag_cells(T, U);
+  w.pxd = c.take<float>(LD);
+  w.pyd = c.take<float>(LD);
+  w.alpha = c.take<double>(LD);
+  w.beta = c.take<double>(LD);
   w.Lutt = c.take<double>((size_t)N);
   w.ry = c.take<double>((size_t)N * T);
   w.rx = c.take<double>((size_t)N * T);
@@ -584,6 +594,8 @@ int rnnt_full_loss(const rnnt_batch* batch, int32_t J, int32_t V, int32_t dtype,
   la.V = V;
   la.px = w.px;
   la.py = w.py;
+  la.pxd = w.pxd;
+  la.pyd = w.pyd;
   la.alpha = w.alpha;
   la.beta = w.beta;
   la.Lutt = w.Lutt;
@@ -596,6 +608,7 @@ int rnnt_full_loss(const rnnt_batch* batch, int32_t J, int32_t V, int32_t dtype,
   la.cpx = w.cpx;
   la.cpy = w.cpy;
   la.ncolblk = lattice_colblocks(batch->T);
+  if (e == hipSuccess) e = launch_lattice_diag_copy(la, s);
   if (e == hipSuccess) e = launch_lattice(la, s);
   // the joiner's backward on every (t, u)
   JoinerArgs jb = joiner_args(batch, S, J, V, dtype, enc, dec, W, bias, w.ranges);

@@ -21,8 +21,10 @@ struct SimpleArgs {
   int lsplit;
   float* px;           // [N, T, U+1] (caller's or ws)
   float* py;
-  double* alpha;       // ws [N, T, U+1], log2 domain
-  double* beta;        // ws [N, T, U+1], log2 domain
+  float* pxd;          // ws [N, D, W]: px, py in the diagonal-major lattice layout
+  float* pyd;
+  double* alpha;       // ws [N, D, W], log2 domain, diagonal-major
+  double* beta;        // ws [N, D, W], log2 domain, diagonal-major
   double* Lutt;        // ws [N]: total log2-prob (NaN for an invalid utterance)
   float* loss;         // [N]
   float* gx;           // [N, T, U+1]
@@ -53,7 +55,23 @@ hipError_t launch_normalizer(const SimpleArgs& a, hipStream_t s);
 int normalizer_splits(int N, int T, int U, int V);
 int dlm_splits(int N, int T, int U, int V);
 hipError_t launch_lattice(const SimpleArgs& a, hipStream_t s);
+hipError_t launch_lattice_diag_copy(const SimpleArgs& a, hipStream_t s);
 int lattice_colblocks(int T);
+
+// Diagonal-major lattice layout (internal): node (t, u) of an utterance sits
+// on diagonal d = t + u at slot (u % R) * 64 + u / R of a row of W = 64 R
+// slots, where R = lattice_rows_per_lane(U + 1) rows of the lattice belong
+// to each lane of the recursion's wave. One anti-diagonal step of the
+// recursion then reads and writes contiguous slots. D = T + U diagonals.
+int lattice_rows_per_lane(int U1);
+inline size_t lattice_diag_cells(int T, int U) {
+  return (size_t)(T + U) * 64 * lattice_rows_per_lane(U + 1);
+}
+DEV int lattice_slot(int u, int R) { return (u % R) * 64 + u / R; }
+DEV int lattice_rows_per_lane_dev(int U1) {
+  const int need = (U1 + 63) / 64;
+  return need <= 1 ? 1 : need <= 2 ? 2 : need <= 4 ? 4 : need <= 8 ? 8 : 16;
+}
 hipError_t launch_smoothing_stats(const SimpleArgs& a, hipStream_t s);
 hipError_t launch_simple_grads(const SimpleArgs& a, hipStream_t s);
 

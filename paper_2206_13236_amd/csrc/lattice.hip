@@ -9,6 +9,9 @@
 // per step. Lane l owns the rows u in [l*R, l*R + R); the only cross-lane
 // value per step is the neighbouring row's output, moved by one DPP wave
 // shift. The px/py loads of each row's node are issued P diagonals ahead.
+// The recursion reads copies of px, py and writes alpha, beta in the
+// diagonal-major layout described in kernels.h, so that every load and
+// store of a step is contiguous across the wave.
 //
 // lattice_occ_kernel: one wave per frame over the whole batch. Every complete
 // path leaves frame t through exactly one blank edge (t,u) -> (t+1,u) (the
@@ -30,25 +33,26 @@ namespace {
 constexpr int kOccFrames = 16;  // frames (waves) per workgroup of the occupation kernel
 
 // The recursion loops are kept free of branches and of 64-bit address
-// arithmetic: px, py and alpha/beta of the utterance are buffer resources,
-// a node's element offset is d*(U+1) + u*(1 - (U+1)) (one add per step), and
-// lanes whose node lies outside the lattice load from / store to kOob (reads
-// 0, store dropped). Conditional memory operations would otherwise make the
-// compiler wait for every outstanding load and store at each step.
+// arithmetic: px, py and alpha/beta of the utterance are buffer resources in
+// the diagonal-major layout, so the lane's row r of diagonal d sits at
+// d*W + r*64 + lane and every load and store of a step is contiguous across
+// the wave; lanes whose node lies outside the lattice load from / store to
+// kOob (reads 0, store dropped). Conditional memory operations would
+// otherwise make the compiler wait for every outstanding load and store at
+// each step.
 struct LatView {
-  Rsrc px, py, out;  // px, py [T, U+1] f32 and alpha or beta [T, U+1] f64 of the utterance
-  int Tn, Un, U1;
+  Rsrc px, py, out;  // pxd, pyd (f32) and alpha or beta (f64) of the utterance, [D, W]
+  int Tn, Un, W;
 };
 
 template <int R>
-DEV void lattice_load(const LatView& v, int d, const int (&rbase)[R], const bool (&rok)[R], int lane,
-                      float (&x)[R], float (&y)[R]) {
-  const int dU = d * v.U1;
+DEV void lattice_load(const LatView& v, int d, const bool (&rok)[R], int lane, float (&x)[R], float (&y)[R]) {
+  const int dW = d * v.W + lane;
 #pragma unroll
   for (int r = 0; r < R; ++r) {
     const int t = d - (lane * R + r);
     const bool act = rok[r] && (unsigned)t < (unsigned)v.Tn;
-    const uint32_t off = act ? (uint32_t)(dU + rbase[r]) * 4u : kOob;
+    const uint32_t off = act ? (uint32_t)(dW + r * 64) * 4u : kOob;
     x[r] = buf_load_f32(v.px, off);
     y[r] = buf_load_f32(v.py, off);
   }
@@ -57,25 +61,20 @@ DEV void lattice_load(const LatView& v, int d, const int (&rbase)[R], const bool
 template <int R, int P>
 DEV void alpha_pass(const LatView& v, int lane) {
   const int D = v.Tn + v.Un;  // diagonals 0 .. Tn-1+Un (the loop may run up to P-1 idle steps past them)
-  int rbase[R];
   bool rok[R];
 #pragma unroll
-  for (int r = 0; r < R; ++r) {
-    const int u = lane * R + r;
-    rbase[r] = u * (1 - v.U1);
-    rok[r] = u <= v.Un;
-  }
+  for (int r = 0; r < R; ++r) rok[r] = lane * R + r <= v.Un;
   double hout[R], vout[R];
 #pragma unroll
   for (int r = 0; r < R; ++r) hout[r] = vout[r] = kNegInfD;
   float xr[P][R], yr[P][R];
 #pragma unroll
-  for (int k = 0; k < P; ++k) lattice_load<R>(v, k, rbase, rok, lane, xr[k], yr[k]);
+  for (int k = 0; k < P; ++k) lattice_load<R>(v, k, rok, lane, xr[k], yr[k]);
   for (int d0 = 0; d0 < D; d0 += P) {
 #pragma unroll
     for (int k = 0; k < P; ++k) {
       const int d = d0 + k;
-      const int dU = d * v.U1;
+      const int dW = d * v.W + lane;
       const double vfirst = dpp_move_d<kDppWaveShr1>(vout[R - 1], kNegInfD);
       double nh[R], nv[R];
 #pragma unroll
@@ -86,14 +85,14 @@ DEV void alpha_pass(const LatView& v, int lane) {
         const double al = (d == 0) ? 0.0 : log2add(hout[r], vin);
         nh[r] = act ? al + (double)yr[k][r] * kLog2e : kNegInfD;
         nv[r] = act ? al + (double)xr[k][r] * kLog2e : kNegInfD;
-        buf_store_f64(v.out, act ? (uint32_t)(dU + rbase[r]) * 8u : kOob, al);
+        buf_store_f64(v.out, act ? (uint32_t)(dW + r * 64) * 8u : kOob, al);
       }
 #pragma unroll
       for (int r = 0; r < R; ++r) {
         hout[r] = nh[r];
         vout[r] = nv[r];
       }
-      lattice_load<R>(v, d + P, rbase, rok, lane, xr[k], yr[k]);
+      lattice_load<R>(v, d + P, rok, lane, xr[k], yr[k]);
     }
   }
 }
@@ -101,14 +100,9 @@ DEV void alpha_pass(const LatView& v, int lane) {
 template <int R, int P>
 DEV void beta_pass(const LatView& v, int lane) {
   const int D = v.Tn + v.Un;
-  int rbase[R];
   bool rok[R];
 #pragma unroll
-  for (int r = 0; r < R; ++r) {
-    const int u = lane * R + r;
-    rbase[r] = u * (1 - v.U1);
-    rok[r] = u <= v.Un;
-  }
+  for (int r = 0; r < R; ++r) rok[r] = lane * R + r <= v.Un;
   // beta of my rows on the previous (higher) diagonal; the virtual node
   // (Tn, Un) after the final blank has beta = 0.
   double bprev[R];
@@ -116,12 +110,12 @@ DEV void beta_pass(const LatView& v, int lane) {
   for (int r = 0; r < R; ++r) bprev[r] = (lane * R + r == v.Un) ? 0.0 : kNegInfD;
   float xr[P][R], yr[P][R];
 #pragma unroll
-  for (int k = 0; k < P; ++k) lattice_load<R>(v, D - 1 - k, rbase, rok, lane, xr[k], yr[k]);
+  for (int k = 0; k < P; ++k) lattice_load<R>(v, D - 1 - k, rok, lane, xr[k], yr[k]);
   for (int d0 = D - 1; d0 >= 0; d0 -= P) {
 #pragma unroll
     for (int k = 0; k < P; ++k) {
       const int d = d0 - k;
-      const int dU = d * v.U1;
+      const int dW = d * v.W + lane;
       const double vlast = dpp_move_d<kDppWaveShl1>(bprev[0], kNegInfD);
       double nb[R];
 #pragma unroll
@@ -131,11 +125,11 @@ DEV void beta_pass(const LatView& v, int lane) {
         const double vin = (r == R - 1) ? vlast : bprev[r + 1];
         const double be = log2add((double)yr[k][r] * kLog2e + bprev[r], (double)xr[k][r] * kLog2e + vin);
         nb[r] = act ? be : kNegInfD;
-        buf_store_f64(v.out, act ? (uint32_t)(dU + rbase[r]) * 8u : kOob, be);
+        buf_store_f64(v.out, act ? (uint32_t)(dW + r * 64) * 8u : kOob, be);
       }
 #pragma unroll
       for (int r = 0; r < R; ++r) bprev[r] = nb[r];
-      lattice_load<R>(v, d - P, rbase, rok, lane, xr[k], yr[k]);
+      lattice_load<R>(v, d - P, rok, lane, xr[k], yr[k]);
     }
   }
 }
@@ -148,14 +142,15 @@ __global__ __launch_bounds__(128) void lattice_fb_kernel(SimpleArgs a) {
   const int T = a.b.T, U1 = a.b.U + 1;
   int Tn, Un;
   const bool ok = utt_dims(a.b, n, Tn, Un);
-  const size_t base = (size_t)n * T * U1;
-  const size_t cells = (size_t)T * U1;
+  const int W = 64 * R;
+  const size_t cells = (size_t)(T + U1 - 1) * W;
+  const size_t base = (size_t)n * cells;
   LatView v;
-  v.px = make_rsrc(a.px + base, cells * sizeof(float));
-  v.py = make_rsrc(a.py + base, cells * sizeof(float));
+  v.px = make_rsrc(a.pxd + base, cells * sizeof(float));
+  v.py = make_rsrc(a.pyd + base, cells * sizeof(float));
   v.Tn = Tn;
   v.Un = Un;
-  v.U1 = U1;
+  v.W = W;
   if (wave == 0) {
     v.out = make_rsrc(a.alpha + base, cells * sizeof(double));
     alpha_pass<R, P>(v, lane);
@@ -168,11 +163,27 @@ __global__ __launch_bounds__(128) void lattice_fb_kernel(SimpleArgs a) {
     // symbols outside [0, V) make the utterance invalid
     bool sok = true;
     for (int u = 0; u < Un; ++u) symbol_at(a.b, n, u, a.V, sok);
-    const double L = a.alpha[base + (size_t)(Tn - 1) * U1 + Un] + (double)a.py[base + (size_t)(Tn - 1) * U1 + Un] * kLog2e;
+    const size_t last = base + (size_t)(Tn - 1 + Un) * W + lattice_slot(Un, R);
+    const double L = a.alpha[last] + (double)a.pyd[last] * kLog2e;
     const double L2 = (ok && sok) ? L : __builtin_nan("");
     a.Lutt[n] = L2;
     a.loss[n] = (L2 == L2) ? (float)(-L2 * kLn2) : __builtin_nanf("");
   }
+}
+
+// px, py [N, T, U+1] -> the diagonal-major copies (for producers that do not
+// write them directly).
+__global__ __launch_bounds__(256) void lattice_diag_copy_kernel(SimpleArgs a, int R) {
+  const int T = a.b.T, U1 = a.b.U + 1;
+  const size_t L = (size_t)a.b.N * T * U1;
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= L) return;
+  const int n = (int)(i / ((size_t)T * U1));
+  const int rem = (int)(i - (size_t)n * T * U1);
+  const int t = rem / U1, u = rem - t * U1;
+  const size_t o = (size_t)n * (T + U1 - 1) * 64 * R + (size_t)(t + u) * 64 * R + lattice_slot(u, R);
+  a.pxd[o] = a.px[i];
+  a.pyd[o] = a.py[i];
 }
 
 template <int R>
@@ -187,8 +198,9 @@ __global__ __launch_bounds__(64 * kOccFrames) void lattice_occ_kernel(SimpleArgs
   const double Lu = a.Lutt[n];
   const bool frow = (Lu == Lu) && (Lu != kNegInfD) && t < Tn;
   const size_t base = (size_t)n * T * U1;
-  const double* alpha = a.alpha + base;
-  const double* beta = a.beta + base;
+  const int W = 64 * R;
+  const double* alpha = a.alpha + (size_t)n * (T + U1 - 1) * W;
+  const double* beta = a.beta + (size_t)n * (T + U1 - 1) * W;
   const float* px = a.px + base;
   const float* py = a.py + base;
   // log2-domain weights of the frame's blank edges (ey) and vertical edges (ex)
@@ -201,10 +213,11 @@ __global__ __launch_bounds__(64 * kOccFrames) void lattice_occ_kernel(SimpleArgs
     const size_t idx = on ? (size_t)t * U1 + u : 0;
     ey[c] = ex[c] = kNegInfD;
     if (on) {
-      const double al = alpha[idx];
-      const double nb = (t + 1 < Tn) ? beta[idx + U1] : (u == Un ? 0.0 : kNegInfD);
+      const size_t dg = (size_t)(t + u) * W;  // diagonal of (t, u); (t+1, u) and (t, u+1) lie on the next
+      const double al = alpha[dg + lattice_slot(u, R)];
+      const double nb = (t + 1 < Tn) ? beta[dg + W + lattice_slot(u, R)] : (u == Un ? 0.0 : kNegInfD);
       ey[c] = al + (double)py[idx] * kLog2e + nb;
-      if (u < Un) ex[c] = al + (double)px[idx] * kLog2e + beta[idx + 1];
+      if (u < Un) ex[c] = al + (double)px[idx] * kLog2e + beta[dg + W + lattice_slot(u + 1, R)];
     }
     mx = ey[c] > mx ? ey[c] : mx;
   }
@@ -279,14 +292,30 @@ void launch_lattice_r(const SimpleArgs& a, hipStream_t s) {
 
 int lattice_colblocks(int T) { return (T + kOccFrames - 1) / kOccFrames; }
 
+int lattice_rows_per_lane(int U1) {
+  const int need = (U1 + 63) / 64;
+  return need <= 1 ? 1 : need <= 2 ? 2 : need <= 4 ? 4 : need <= 8 ? 8 : 16;
+}
+
+hipError_t launch_lattice_diag_copy(const SimpleArgs& a, hipStream_t s) {
+  const size_t L = (size_t)a.b.N * a.b.T * (a.b.U + 1);
+  {
+    RNNT_PROF(s, "lattice_diag_copy");
+    hipLaunchKernelGGL(lattice_diag_copy_kernel, dim3((unsigned)((L + 255) / 256)), dim3(256), 0, s, a,
+                       lattice_rows_per_lane(a.b.U + 1));
+  }
+  return hipGetLastError();
+}
+
 hipError_t launch_lattice(const SimpleArgs& a, hipStream_t s) {
   const int U1 = a.b.U + 1;
-  const int need = (U1 + 63) / 64;
-  if (need <= 1) launch_lattice_r<1, 8>(a, s);
-  else if (need <= 2) launch_lattice_r<2, 8>(a, s);
-  else if (need <= 4) launch_lattice_r<4, 4>(a, s);
-  else if (need <= 8) launch_lattice_r<8, 2>(a, s);
-  else if (need <= 16) launch_lattice_r<16, 2>(a, s);
-  else return hipErrorInvalidValue;
+  if (U1 > 64 * 16) return hipErrorInvalidValue;
+  switch (lattice_rows_per_lane(U1)) {
+    case 1: launch_lattice_r<1, 8>(a, s); break;
+    case 2: launch_lattice_r<2, 8>(a, s); break;
+    case 4: launch_lattice_r<4, 4>(a, s); break;
+    case 8: launch_lattice_r<8, 2>(a, s); break;
+    default: launch_lattice_r<16, 2>(a, s); break;
+  }
   return hipGetLastError();
 }

@@ -304,6 +304,8 @@ __global__ __launch_bounds__(256) void normalizer_epi_kernel(SimpleArgs a) {
     a.py[idx] = kNegInfF;
     return;
   }
+  const int R = lattice_rows_per_lane_dev(U1);
+  const size_t od = (size_t)n * (T + U1 - 1) * 64 * R + (size_t)(t + u) * 64 * R + lattice_slot(u, R);
   float s = 0.f;
   for (int q = 0; q < a.nsplit; ++q) s += a.npart[(size_t)q * L + idx];
   s = (s > FLT_MIN || s != s) ? s : FLT_MIN;
@@ -326,6 +328,8 @@ __global__ __launch_bounds__(256) void normalizer_epi_kernel(SimpleArgs a) {
   }
   a.py[idx] = py;
   a.px[idx] = (u < Un) ? px : kNegInfF;
+  a.pyd[od] = py;
+  a.pxd[od] = (u < Un) ? px : kNegInfF;
 }
 
 // ---------------------------------------------------------------------------
