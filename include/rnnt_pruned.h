@@ -202,7 +202,7 @@ int rnnt_pruned_joiner(const rnnt_batch* batch, int32_t S, int32_t J, int32_t V,
                        void* workspace, size_t workspace_bytes, void* stream);
 
 /* Workspace bytes for rnnt_pruned_loss. */
-size_t rnnt_pruned_loss_workspace_size(int32_t N, int32_t T, int32_t S);
+size_t rnnt_pruned_loss_workspace_size(int32_t N, int32_t T, int32_t U, int32_t S);
 
 /* The recursion of Eq. (3) on the pruned lattice (Sec. 3.2): entries outside
  * p_t <= u < p_t + S are -inf. px, py [N, T, S] fp32 are the band log-probs

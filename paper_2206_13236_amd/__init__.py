@@ -103,8 +103,8 @@ def pruned_joiner_workspace_size(N, T, S, J, V, dtype) -> int:
     return int(lib().rnnt_pruned_joiner_workspace_size(N, T, S, J, V, dtype))
 
 
-def pruned_loss_workspace_size(N, T, S) -> int:
-    return int(lib().rnnt_pruned_loss_workspace_size(N, T, S))
+def pruned_loss_workspace_size(N, T, U, S) -> int:
+    return int(lib().rnnt_pruned_loss_workspace_size(N, T, U, S))
 
 
 def pruned_joiner_backward_workspace_size(N, T, U, S, J, V, dtype) -> int:
@@ -211,7 +211,7 @@ def rnnt_pruned_loss(batch: Batch, S: int, px: torch.Tensor, py: torch.Tensor, r
     loss = torch.empty(N, **f32) if loss is None else loss
     if want_occupations and px_occ is None:
         px_occ, py_occ = torch.empty(N, T, S, **f32), torch.empty(N, T, S, **f32)
-    ws = _ws(pruned_loss_workspace_size(N, T, S), batch.device, workspace)
+    ws = _ws(pruned_loss_workspace_size(N, T, batch.U, S), batch.device, workspace)
     check(lib().rnnt_pruned_loss(batch.c, S, _p(px), _p(py), _p(ranges), _p(loss), _p(px_occ), _p(py_occ),
                                  _p(ws), ws.numel(), _stream(stream)))
     return {"loss": loss, "px_occ": px_occ, "py_occ": py_occ}
@@ -348,7 +348,7 @@ class PrunedRnntLoss:
 
         ws_s = self._buf("ws_simple", (simple_loss_workspace_size(N, T, U, V),), torch.uint8, dev)
         ws_p = self._buf("ws_pruned", (max(pruned_joiner_workspace_size(N, T, S, J, V, dt),
-                                           pruned_loss_workspace_size(N, T, S),
+                                           pruned_loss_workspace_size(N, T, U, S),
                                            pruned_joiner_backward_workspace_size(N, T, U, S, J, V, dt)),),
                          torch.uint8, dev)
         ssc = self._buf("ssc", (N,), f32, dev)

@@ -364,7 +364,7 @@ FullWs full_layout(void* base, int N, int T, int U, int J, int V, int bf16) {
 
 extern "C" {
 
-int rnnt_abi_version(void) { return 3; }
+int rnnt_abi_version(void) { return 4; }
 
 const char* rnnt_last_error(void) { return g_err.c_str(); }
 
@@ -476,13 +476,32 @@ int rnnt_pruned_joiner(const rnnt_batch* batch, int32_t S, int32_t J, int32_t V,
   return hip_status(e, "rnnt_pruned_joiner");
 }
 
-size_t rnnt_pruned_loss_workspace_size(int32_t N, int32_t T, int32_t S) {
-  if (N < 1 || T < 1 || S < 1) return 0;
-  Carve c(nullptr);
-  c.take<double>((size_t)N * T * S);
-  c.take<double>((size_t)N * T * S);
-  c.take<double>((size_t)N);
-  return c.off;
+// Workspace of rnnt_pruned_loss: the band in a diagonal-major layout of
+// band_slots(U, S) slots per diagonal (the per-slot meta only on the slot layout).
+struct BandWs {
+  float *pxd, *pyd;
+  uint32_t* meta;
+  double *alpha, *beta, *Lutt;
+  size_t bytes;
+};
+
+BandWs band_layout(void* base, int N, int T, int U, int S) {
+  Carve c(base);
+  BandWs w;
+  const size_t cells = (size_t)N * band_diagonals(T, U, S) * band_slots(U, S);
+  w.pxd = c.take<float>(cells);
+  w.pyd = c.take<float>(cells);
+  w.meta = band_masked(U, S) ? nullptr : c.take<uint32_t>(cells);
+  w.alpha = c.take<double>(cells);
+  w.beta = c.take<double>(cells);
+  w.Lutt = c.take<double>((size_t)N);
+  w.bytes = c.off;
+  return w;
+}
+
+size_t rnnt_pruned_loss_workspace_size(int32_t N, int32_t T, int32_t U, int32_t S) {
+  if (N < 1 || T < 1 || U < 0 || S < 1) return 0;
+  return band_layout(nullptr, N, T, U, S).bytes;
 }
 
 int rnnt_pruned_loss(const rnnt_batch* batch, int32_t S, const float* px, const float* py, const int32_t* ranges,
@@ -492,22 +511,30 @@ int rnnt_pruned_loss(const rnnt_batch* batch, int32_t S, const float* px, const 
   if (rc) return rc;
   if (S < 1 || S > RNNT_MAX_S) return fail(RNNT_EUNSUPPORTED, "S = %d outside [1, %d]", S, RNNT_MAX_S);
   if (!px || !py || !ranges || !loss) return fail(RNNT_EINVAL, "px, py, ranges and loss are required");
-  if ((long long)batch->N * batch->T * S > kI32) return fail(RNNT_EUNSUPPORTED, "N*T*S exceeds 2^31-1");
-  if (band_smem_bytes(batch->T, batch->U, S) > 150 * 1024)
-    return fail(RNNT_EUNSUPPORTED, "T*S = %d*%d too large for the LDS-resident band", batch->T, S);
-  const size_t need = rnnt_pruned_loss_workspace_size(batch->N, batch->T, S);
-  rc = check_ws(workspace, workspace_bytes, need);
+  const int D = band_diagonals(batch->T, batch->U, S);
+  const int Wb = band_slots(batch->U, S);
+  if ((long long)batch->N * batch->T * S > kI32 || (long long)D * Wb * 8 > kI32 ||
+      (long long)batch->N * D * Wb > kI32)
+    return fail(RNNT_EUNSUPPORTED, "N*T*S or the band of one utterance is too large");
+  const BandWs need = band_layout(nullptr, batch->N, batch->T, batch->U, S);
+  rc = check_ws(workspace, workspace_bytes, need.bytes);
   if (rc) return rc;
-  Carve c(workspace);
+  const BandWs w = band_layout(workspace, batch->N, batch->T, batch->U, S);
   BandArgs a{};
   a.b = to_dev(batch);
   a.S = S;
+  a.D = D;
+  a.W = Wb;
+  a.masked = band_masked(batch->U, S);
   a.px = px;
   a.py = py;
   a.ranges = ranges;
-  a.alpha = c.take<double>((size_t)batch->N * batch->T * S);
-  a.beta = c.take<double>((size_t)batch->N * batch->T * S);
-  a.Lutt = c.take<double>((size_t)batch->N);
+  a.pxd = w.pxd;
+  a.pyd = w.pyd;
+  a.meta = w.meta;
+  a.alpha = w.alpha;
+  a.beta = w.beta;
+  a.Lutt = w.Lutt;
   a.loss = loss;
   a.gx = px_occ;
   a.gy = py_occ;

@@ -56,6 +56,8 @@ int normalizer_splits(int N, int T, int U, int V);
 int dlm_splits(int N, int T, int U, int V);
 hipError_t launch_lattice(const SimpleArgs& a, hipStream_t s);
 hipError_t launch_lattice_diag_copy(const SimpleArgs& a, hipStream_t s);
+// the recursion alone (no occupations) on a.pxd / a.pyd; a.V = 0 skips the symbol check
+hipError_t launch_lattice_recursion(const SimpleArgs& a, hipStream_t s);
 int lattice_colblocks(int T);
 
 // Diagonal-major lattice layout (internal): node (t, u) of an utterance sits
@@ -138,10 +140,16 @@ int joiner_ldl(int V);
 struct BandArgs {
   BatchDev b;
   int S;
+  int D;               // diagonals of the layout: band_diagonals(T, U, S)
+  int W;               // slots per diagonal: band_slots(U, S)
+  bool masked;         // W == 64: the lattice layout with R = 1 (slot u), else slot s = u - p_t
   const float* px;     // [N, T, S]
   const float* py;
   const int* ranges;   // [N, T, S]
-  double* alpha;       // ws [N, T, S] log2 domain
+  float* pxd;          // ws [N, D, W]: px, py in a diagonal-major layout
+  float* pyd;
+  uint32_t* meta;      // ws [N, D, W] per-slot shifts and validity (band path only)
+  double* alpha;       // ws [N, D, W] log2 domain, diagonal-major
   double* beta;
   double* Lutt;        // ws [N]: total log2-prob (NaN for an invalid utterance)
   float* loss;
@@ -149,7 +157,14 @@ struct BandArgs {
   float* gy;
 };
 hipError_t launch_band(const BandArgs& a, hipStream_t s);
-size_t band_smem_bytes(int T, int U, int S);
+int band_diagonals(int T, int U, int S);
+// Two layouts for the band recursion. U + 1 <= 64: the full lattice's
+// diagonal-major layout with one row per lane (W = 64, slot u), band nodes
+// holding their log-probs and every other node -inf, so the full recursion
+// computes the band's sums. Otherwise one slot per band offset (W = S, slot
+// s = u - p_t), each slot carrying the shifts to its predecessors.
+bool band_masked(int U, int S);
+int band_slots(int U, int S);  // W
 
 // ---- generic fills -----------------------------------------------------------
 hipError_t launch_fill_f32(float* p, size_t n, float v, hipStream_t s);

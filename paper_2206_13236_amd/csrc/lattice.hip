@@ -160,9 +160,10 @@ __global__ __launch_bounds__(128) void lattice_fb_kernel(SimpleArgs a) {
   }
   __syncthreads();
   if (tid == 0) {
-    // symbols outside [0, V) make the utterance invalid
+    // symbols outside [0, V) make the utterance invalid (V = 0: not checked here)
     bool sok = true;
-    for (int u = 0; u < Un; ++u) symbol_at(a.b, n, u, a.V, sok);
+    if (a.V > 0)
+      for (int u = 0; u < Un; ++u) symbol_at(a.b, n, u, a.V, sok);
     const size_t last = base + (size_t)(Tn - 1 + Un) * W + lattice_slot(Un, R);
     const double L = a.alpha[last] + (double)a.pyd[last] * kLog2e;
     const double L2 = (ok && sok) ? L : __builtin_nan("");
@@ -303,6 +304,19 @@ hipError_t launch_lattice_diag_copy(const SimpleArgs& a, hipStream_t s) {
     RNNT_PROF(s, "lattice_diag_copy");
     hipLaunchKernelGGL(lattice_diag_copy_kernel, dim3((unsigned)((L + 255) / 256)), dim3(256), 0, s, a,
                        lattice_rows_per_lane(a.b.U + 1));
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_lattice_recursion(const SimpleArgs& a, hipStream_t s) {
+  if (a.b.U + 1 > 64 * 16) return hipErrorInvalidValue;
+  RNNT_PROF(s, "band_fb");
+  switch (lattice_rows_per_lane(a.b.U + 1)) {
+    case 1: hipLaunchKernelGGL((lattice_fb_kernel<1, 8>), dim3(a.b.N), dim3(128), 0, s, a); break;
+    case 2: hipLaunchKernelGGL((lattice_fb_kernel<2, 8>), dim3(a.b.N), dim3(128), 0, s, a); break;
+    case 4: hipLaunchKernelGGL((lattice_fb_kernel<4, 4>), dim3(a.b.N), dim3(128), 0, s, a); break;
+    case 8: hipLaunchKernelGGL((lattice_fb_kernel<8, 2>), dim3(a.b.N), dim3(128), 0, s, a); break;
+    default: hipLaunchKernelGGL((lattice_fb_kernel<16, 2>), dim3(a.b.N), dim3(128), 0, s, a); break;
   }
   return hipGetLastError();
 }

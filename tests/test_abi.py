@@ -41,14 +41,14 @@ def test_library_exports_every_declared_symbol(L):
     missing = [n for n in _declared() if not hasattr(L, n)]
     assert not missing, f"not exported: {missing}"
     assert set(_declared()) == set(_native.SIGNATURES), "binding signatures out of sync with the header"
-    assert L.rnnt_abi_version() == 3
+    assert L.rnnt_abi_version() == 4
 
 
 def test_workspace_queries(L):
     from paper_2206_13236_amd import _native as N
     a = L.rnnt_simple_loss_workspace_size(16, 250, 60, 500)
-    assert a > 0 and a % 256 == 0 or a > 0
-    assert L.rnnt_simple_loss_workspace_size(16, 250, 60, 500) == a
+    assert a > 0
+    assert L.rnnt_simple_loss_workspace_size(16, 250, 60, 500) == a  # a pure function of the sizes
     assert L.rnnt_simple_loss_workspace_size(0, 250, 60, 500) == 0
     # bigger shapes need more
     assert L.rnnt_simple_loss_workspace_size(16, 250, 61, 500) >= a
@@ -57,8 +57,11 @@ def test_workspace_queries(L):
     b32 = L.rnnt_pruned_joiner_backward_workspace_size(16, 250, 60, 5, 512, 500, N.RNNT_F32)
     b16 = L.rnnt_pruned_joiner_backward_workspace_size(16, 250, 60, 5, 512, 500, N.RNNT_BF16)
     assert b32 > b16 > 0
-    assert L.rnnt_pruned_loss_workspace_size(16, 250, 5) == 2 * 16 * 250 * 5 * 8 or \
-        L.rnnt_pruned_loss_workspace_size(16, 250, 5) >= 2 * 16 * 250 * 5 * 8
+    # the band's alpha and beta (fp64) over min(T+U, S T) diagonals of S slots, at least
+    p = L.rnnt_pruned_loss_workspace_size(16, 250, 60, 5)
+    assert p >= 2 * 16 * (250 + 60) * 5 * 8
+    assert L.rnnt_pruned_loss_workspace_size(16, 250, 60, 0) == 0
+    assert L.rnnt_full_loss_workspace_size(2, 20, 5, 32, 16, N.RNNT_F32) > 0
 
 
 def _batch(N=2, T=10, U=3):
