@@ -201,7 +201,7 @@ int rnnt_pruned_joiner(const rnnt_batch* batch, int32_t S, int32_t J, int32_t V,
                        const int32_t* ranges, float* px, float* py, float* lse, float* logits,
                        void* workspace, size_t workspace_bytes, void* stream);
 
-/* Workspace bytes for rnnt_pruned_loss. */
+/* Workspace bytes for rnnt_pruned_loss (the algorithm it picks). */
 size_t rnnt_pruned_loss_workspace_size(int32_t N, int32_t T, int32_t U, int32_t S);
 
 /* The recursion of Eq. (3) on the pruned lattice (Sec. 3.2): entries outside
@@ -214,6 +214,40 @@ int rnnt_pruned_loss(const rnnt_batch* batch, int32_t S,
                      const float* px, const float* py, const int32_t* ranges,
                      float* loss, float* px_occ, float* py_occ,
                      void* workspace, size_t workspace_bytes, void* stream);
+
+/* Algorithms of the pruned recursion (same results up to rounding order):
+ *   RNNT_BAND_AUTO       the library's choice for the shapes;
+ *   RNNT_BAND_WAVEFRONT  anti-diagonal wavefront, depth T_n + U_n steps;
+ *   RNNT_BAND_SCAN       chunked scan over frames, depth about 2C + T_n / C
+ *                        frame steps for chunks of C frames (S <= 16 only).
+ */
+#define RNNT_BAND_AUTO 0
+#define RNNT_BAND_WAVEFRONT 1
+#define RNNT_BAND_SCAN 2
+#define RNNT_SCAN_MAX_S 16
+#define RNNT_SCAN_MAX_CHUNK 32
+
+/* Workspace bytes for rnnt_pruned_loss_ex with the given algorithm and chunk
+ * (chunk 0 = the library's choice; 0 is returned for unsupported choices).
+ */
+size_t rnnt_pruned_loss_ex_workspace_size(int32_t N, int32_t T, int32_t U, int32_t S,
+                                          int32_t algorithm, int32_t chunk);
+
+/* rnnt_pruned_loss with an explicit algorithm. The band recursion of
+ * Eq. (3) composes frame by frame: inside a frame only symbol moves occur
+ * (an affine recurrence over the band's slots in the log semiring) and the
+ * blank moves map one frame's band onto the next, so RNNT_BAND_SCAN forms
+ * the S x S transfer matrix of every chunk of `chunk` frames in parallel,
+ * chains the matrices per utterance and replays each chunk from its
+ * incoming messages. chunk in [1, RNNT_SCAN_MAX_CHUNK], or 0 for the
+ * library's choice; ignored by the wavefront. Arguments, outputs and error
+ * behaviour are those of rnnt_pruned_loss; RNNT_EUNSUPPORTED for the scan
+ * with S > RNNT_SCAN_MAX_S.
+ */
+int rnnt_pruned_loss_ex(const rnnt_batch* batch, int32_t S, int32_t algorithm, int32_t chunk,
+                        const float* px, const float* py, const int32_t* ranges,
+                        float* loss, float* px_occ, float* py_occ,
+                        void* workspace, size_t workspace_bytes, void* stream);
 
 /* Workspace bytes for rnnt_pruned_joiner_backward. */
 size_t rnnt_pruned_joiner_backward_workspace_size(int32_t N, int32_t T, int32_t U, int32_t S,

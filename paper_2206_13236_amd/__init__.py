@@ -21,7 +21,7 @@ __all__ = [
     "Batch", "RnntError", "rnnt_simple_loss", "rnnt_simple_loss_backward", "rnnt_prune_ranges",
     "rnnt_pruned_joiner", "pruned_rnnt_loss", "rnnt_full_loss", "full_loss_workspace_size",
     "rnnt_pruned_loss", "rnnt_pruned_joiner_backward", "simple_loss_workspace_size",
-    "pruned_joiner_workspace_size", "pruned_loss_workspace_size",
+    "pruned_joiner_workspace_size", "pruned_loss_workspace_size", "BAND_ALGORITHMS",
     "pruned_joiner_backward_workspace_size", "PrunedRnntLoss", "RNNT_F32", "RNNT_BF16",
 ]
 
@@ -103,8 +103,10 @@ def pruned_joiner_workspace_size(N, T, S, J, V, dtype) -> int:
     return int(lib().rnnt_pruned_joiner_workspace_size(N, T, S, J, V, dtype))
 
 
-def pruned_loss_workspace_size(N, T, U, S) -> int:
-    return int(lib().rnnt_pruned_loss_workspace_size(N, T, U, S))
+def pruned_loss_workspace_size(N, T, U, S, algorithm=None, chunk=0) -> int:
+    if algorithm is None:
+        return int(lib().rnnt_pruned_loss_workspace_size(N, T, U, S))
+    return int(lib().rnnt_pruned_loss_ex_workspace_size(N, T, U, S, BAND_ALGORITHMS[algorithm], chunk))
 
 
 def pruned_joiner_backward_workspace_size(N, T, U, S, J, V, dtype) -> int:
@@ -200,9 +202,15 @@ def rnnt_pruned_joiner(batch: Batch, S: int, enc: torch.Tensor, dec: torch.Tenso
     return {"px": px, "py": py, "lse": lse, "logits": logits}
 
 
+# algorithms of the pruned recursion (rnnt_pruned_loss_ex)
+BAND_ALGORITHMS = {"auto": 0, "wavefront": 1, "scan": 2}
+
+
 def rnnt_pruned_loss(batch: Batch, S: int, px: torch.Tensor, py: torch.Tensor, ranges: torch.Tensor,
                      loss=None, px_occ=None, py_occ=None, workspace=None, stream=None,
-                     want_occupations: bool = True) -> dict:
+                     want_occupations: bool = True, algorithm: str = None, chunk: int = 0) -> dict:
+    """The pruned recursion; `algorithm` ("auto", "wavefront" or "scan") and
+    `chunk` select rnnt_pruned_loss_ex, None calls rnnt_pruned_loss."""
     N, T = batch.N, batch.T
     _need(px, "px", torch.float32, (N, T, S))
     _need(py, "py", torch.float32, (N, T, S))
@@ -211,9 +219,14 @@ def rnnt_pruned_loss(batch: Batch, S: int, px: torch.Tensor, py: torch.Tensor, r
     loss = torch.empty(N, **f32) if loss is None else loss
     if want_occupations and px_occ is None:
         px_occ, py_occ = torch.empty(N, T, S, **f32), torch.empty(N, T, S, **f32)
-    ws = _ws(pruned_loss_workspace_size(N, T, batch.U, S), batch.device, workspace)
-    check(lib().rnnt_pruned_loss(batch.c, S, _p(px), _p(py), _p(ranges), _p(loss), _p(px_occ), _p(py_occ),
-                                 _p(ws), ws.numel(), _stream(stream)))
+    ws = _ws(pruned_loss_workspace_size(N, T, batch.U, S, algorithm, chunk), batch.device, workspace)
+    if algorithm is None:
+        check(lib().rnnt_pruned_loss(batch.c, S, _p(px), _p(py), _p(ranges), _p(loss), _p(px_occ), _p(py_occ),
+                                     _p(ws), ws.numel(), _stream(stream)))
+    else:
+        check(lib().rnnt_pruned_loss_ex(batch.c, S, BAND_ALGORITHMS[algorithm], chunk, _p(px), _p(py),
+                                        _p(ranges), _p(loss), _p(px_occ), _p(py_occ), _p(ws), ws.numel(),
+                                        _stream(stream)))
     return {"loss": loss, "px_occ": px_occ, "py_occ": py_occ}
 
 

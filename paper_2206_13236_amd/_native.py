@@ -53,6 +53,9 @@ SIGNATURES = {
     "rnnt_pruned_loss_workspace_size": (c_size_t, [c_int32] * 4),
     "rnnt_pruned_loss": (c_int32, [POINTER(RnntBatch), c_int32, c_void_p, c_void_p, c_void_p,
                                    c_void_p, c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]),
+    "rnnt_pruned_loss_ex_workspace_size": (c_size_t, [c_int32] * 6),
+    "rnnt_pruned_loss_ex": (c_int32, [POINTER(RnntBatch), c_int32, c_int32, c_int32, c_void_p, c_void_p,
+                                      c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]),
     "rnnt_pruned_joiner_backward_workspace_size": (c_size_t, [c_int32] * 7),
     "rnnt_pruned_joiner_backward": (c_int32, [POINTER(RnntBatch), c_int32, c_int32, c_int32, c_int32,
                                               c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,

@@ -364,7 +364,7 @@ FullWs full_layout(void* base, int N, int T, int U, int J, int V, int bf16) {
 
 extern "C" {
 
-int rnnt_abi_version(void) { return 4; }
+int rnnt_abi_version(void) { return 5; }
 
 const char* rnnt_last_error(void) { return g_err.c_str(); }
 
@@ -499,18 +499,92 @@ BandWs band_layout(void* base, int N, int T, int U, int S) {
   return w;
 }
 
-size_t rnnt_pruned_loss_workspace_size(int32_t N, int32_t T, int32_t U, int32_t S) {
+// Workspace of the chunked scan.
+struct ScanWs {
+  double *M, *E, *V, *Wb, *Lutt;
+  size_t bytes;
+};
+
+ScanWs scan_layout(void* base, int N, int T, int S, int C) {
+  Carve c(base);
+  ScanWs w;
+  const size_t nc = (size_t)(T + C - 1) / C;
+  w.M = c.take<double>((size_t)N * nc * S * S);
+  w.E = c.take<double>((size_t)N * S);
+  w.V = c.take<double>((size_t)N * nc * S);
+  w.Wb = c.take<double>((size_t)N * nc * S);
+  w.Lutt = c.take<double>((size_t)N);
+  w.bytes = c.off;
+  return w;
+}
+
+// The algorithm rnnt_pruned_loss uses: the scan wherever it applies.
+int band_auto(int S) { return S <= kScanMaxS ? RNNT_BAND_SCAN : RNNT_BAND_WAVEFRONT; }
+
+size_t pruned_ws_bytes(int N, int T, int U, int S, int algorithm, int chunk) {
   if (N < 1 || T < 1 || U < 0 || S < 1) return 0;
-  return band_layout(nullptr, N, T, U, S).bytes;
+  if (algorithm == RNNT_BAND_AUTO) algorithm = band_auto(S);
+  if (algorithm == RNNT_BAND_WAVEFRONT) return band_layout(nullptr, N, T, U, S).bytes;
+  if (algorithm != RNNT_BAND_SCAN || S > kScanMaxS || chunk < 0 || chunk > kScanMaxC) return 0;
+  return scan_layout(nullptr, N, T, S, chunk ? chunk : band_scan_chunk(T)).bytes;
+}
+
+size_t rnnt_pruned_loss_workspace_size(int32_t N, int32_t T, int32_t U, int32_t S) {
+  return pruned_ws_bytes(N, T, U, S, RNNT_BAND_AUTO, 0);
+}
+
+size_t rnnt_pruned_loss_ex_workspace_size(int32_t N, int32_t T, int32_t U, int32_t S, int32_t algorithm,
+                                          int32_t chunk) {
+  return pruned_ws_bytes(N, T, U, S, algorithm, chunk);
 }
 
 int rnnt_pruned_loss(const rnnt_batch* batch, int32_t S, const float* px, const float* py, const int32_t* ranges,
                      float* loss, float* px_occ, float* py_occ, void* workspace, size_t workspace_bytes,
                      void* stream) {
+  return rnnt_pruned_loss_ex(batch, S, RNNT_BAND_AUTO, 0, px, py, ranges, loss, px_occ, py_occ, workspace,
+                             workspace_bytes, stream);
+}
+
+int rnnt_pruned_loss_ex(const rnnt_batch* batch, int32_t S, int32_t algorithm, int32_t chunk, const float* px,
+                        const float* py, const int32_t* ranges, float* loss, float* px_occ, float* py_occ,
+                        void* workspace, size_t workspace_bytes, void* stream) {
   int rc = check_batch(batch, false);
   if (rc) return rc;
   if (S < 1 || S > RNNT_MAX_S) return fail(RNNT_EUNSUPPORTED, "S = %d outside [1, %d]", S, RNNT_MAX_S);
   if (!px || !py || !ranges || !loss) return fail(RNNT_EINVAL, "px, py, ranges and loss are required");
+  if (algorithm < RNNT_BAND_AUTO || algorithm > RNNT_BAND_SCAN)
+    return fail(RNNT_EINVAL, "unknown algorithm %d", algorithm);
+  if (algorithm == RNNT_BAND_AUTO) algorithm = band_auto(S);
+  if (algorithm == RNNT_BAND_SCAN) {
+    if (S > kScanMaxS) return fail(RNNT_EUNSUPPORTED, "the scan needs S <= %d (S = %d)", kScanMaxS, S);
+    if (chunk < 0 || chunk > kScanMaxC)
+      return fail(RNNT_EINVAL, "chunk = %d outside [0, %d]", chunk, kScanMaxC);
+    if ((long long)batch->N * batch->T * S > kI32)
+      return fail(RNNT_EUNSUPPORTED, "N*T*S is too large");
+    const int C = chunk ? chunk : band_scan_chunk(batch->T);
+    const ScanWs need = scan_layout(nullptr, batch->N, batch->T, S, C);
+    rc = check_ws(workspace, workspace_bytes, need.bytes);
+    if (rc) return rc;
+    const ScanWs w = scan_layout(workspace, batch->N, batch->T, S, C);
+    BandArgs a{};
+    a.b = to_dev(batch);
+    a.S = S;
+    a.px = px;
+    a.py = py;
+    a.ranges = ranges;
+    a.Lutt = w.Lutt;
+    a.loss = loss;
+    a.gx = px_occ;
+    a.gy = py_occ;
+    a.C = C;
+    a.nchunk = (batch->T + C - 1) / C;
+    a.M = w.M;
+    a.E = w.E;
+    a.V = w.V;
+    a.Wb = w.Wb;
+    hipError_t e = launch_band_scan(a, static_cast<hipStream_t>(stream));
+    return hip_status(e, "rnnt_pruned_loss");
+  }
   const int D = band_diagonals(batch->T, batch->U, S);
   const int Wb = band_slots(batch->U, S);
   if ((long long)batch->N * batch->T * S > kI32 || (long long)D * Wb * 8 > kI32 ||

@@ -155,8 +155,19 @@ struct BandArgs {
   float* loss;
   float* gx;           // [N, T, S] or null
   float* gy;
+  // chunked scan over frames (S <= 16)
+  int C;               // frames per chunk
+  int nchunk;          // chunks of the padded T: ceil(T / C)
+  double* M;           // ws [N, nchunk, S, S]: arrivals at a chunk's first frame -> at the next chunk's
+  double* E;           // ws [N, S]: arrivals at the last chunk's first frame -> end of the lattice
+  double* V;           // ws [N, nchunk, S]: arrivals (forward messages) at each chunk's first frame
+  double* Wb;          // ws [N, nchunk, S]: beta at each chunk's first frame
 };
 hipError_t launch_band(const BandArgs& a, hipStream_t s);
+hipError_t launch_band_scan(const BandArgs& a, hipStream_t s);
+constexpr int kScanMaxS = 16;   // band width the scan supports (one 16-lane row per chain)
+constexpr int kScanMaxC = 32;   // frames per chunk at most
+int band_scan_chunk(int T);     // default frames per chunk for a padded length T
 int band_diagonals(int T, int U, int S);
 // Two layouts for the band recursion. U + 1 <= 64: the full lattice's
 // diagonal-major layout with one row per lane (W = 64, slot u), band nodes

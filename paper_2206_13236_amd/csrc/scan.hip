@@ -1,0 +1,492 @@
+// Stage 4b as a chunked scan over frames: the pruned recursion (Eq. (3)
+// restricted to the band of Sec. 3.2) with a dependency chain of O(C + T/C)
+// frames instead of the O(T + U) anti-diagonals of the wavefront kernels.
+//
+// Within frame t only symbol (vertical) moves happen, so the band's alpha
+// row is an affine recurrence over the slots,
+//   alpha(t, s) = ain(t, s) (+) (alpha(t, s-1) + px(t, s-1)),
+// where ain(t, s) is what arrives at slot s by the blank from frame t-1 and
+// (+) is log-add. Such a recurrence composes associatively, so the whole row
+// comes out of a log2(S)-step Hillis-Steele scan across the lanes of a
+// 16-lane DPP row; beta is the mirror-image suffix scan. The blank moves from
+// frame t to t+1 shift slots by p_{t+1} - p_t (one ds_bpermute). Composing
+// the frames of a chunk of C frames gives an S x S log-semiring transfer
+// matrix from the arrivals at its first frame to the arrivals at the next
+// chunk's first frame.
+//
+//   scan_chunk_kernel   every chunk's matrix, one chain per start slot
+//                       (4 chains per wave, one per 16-lane row);
+//   scan_sweep_kernel   per utterance, the vector-matrix products over the
+//                       chunks: forward messages V (wave 0) and beta at each
+//                       chunk's first frame (wave 1), and the loss;
+//   scan_replay_kernel  each chunk again from its V and its successor's beta,
+//                       alpha (wave 0) and beta (wave 1) at every band node
+//                       into LDS, then the occupations of every frame,
+//                       normalised by the frame's own total as in the
+//                       wavefront kernels.
+//
+// Log2 domain, fp64 values, fp32 exp2/log2 only for bounded correction
+// terms, as everywhere else in the library. Inputs and outputs are the
+// frame-major [N, T, S] arrays themselves; no layout copy.
+#include "kernels.h"
+#include "prof.h"
+
+namespace {
+
+// Frames loaded ahead. The frame loops end every step with a scheduling
+// barrier, so that no step's arithmetic is hoisted next to loads issued
+// later and the wait counts only ever cover loads a full ring old.
+constexpr int kPrefetch = 4;
+
+constexpr int row_shr(int d) { return 0x110 + d; }  // lane s <- lane s-d of the same 16-lane row
+constexpr int row_shl(int d) { return 0x100 + d; }  // lane s <- lane s+d of the same 16-lane row
+
+DEV double bperm_d(double v, int src_lane) {
+  const int lo = __builtin_amdgcn_ds_bpermute(src_lane * 4, __double2loint(v));
+  const int hi = __builtin_amdgcn_ds_bpermute(src_lane * 4, __double2hiint(v));
+  return __hiloint2double(hi, lo);
+}
+
+// Row of frame t: alpha(s) = A(s) (+) (alpha(s-1) + x(s-1)), A = arrivals
+// (-inf on lanes outside the frame's nodes). Element s stands for the map
+// a -> A(s) (+) (a + B(s)) with B(s) = x(s-1); the map of a run of slots
+// [j, s] composes as (A, B) = (A_R (+) (A_L + B_R), B_L + B_R).
+template <int K>
+DEV double row_alpha(double A, double x) {
+  double B = dpp_move_d<row_shr(1)>(x, kNegInfD);
+#pragma unroll
+  for (int k = 0; k < K; ++k) {
+    const int d = 1 << k;
+    double Al, Bl;
+    if (d == 1) {
+      Al = dpp_move_d<row_shr(1)>(A, kNegInfD);
+      Bl = dpp_move_d<row_shr(1)>(B, 0.0);
+    } else if (d == 2) {
+      Al = dpp_move_d<row_shr(2)>(A, kNegInfD);
+      Bl = dpp_move_d<row_shr(2)>(B, 0.0);
+    } else if (d == 4) {
+      Al = dpp_move_d<row_shr(4)>(A, kNegInfD);
+      Bl = dpp_move_d<row_shr(4)>(B, 0.0);
+    } else {
+      Al = dpp_move_d<row_shr(8)>(A, kNegInfD);
+      Bl = dpp_move_d<row_shr(8)>(B, 0.0);
+    }
+    A = log2add(A, Al + B);
+    B = Bl + B;
+  }
+  return A;
+}
+
+// Mirror image: beta(s) = Cv(s) (+) (x(s) + beta(s+1)), Cv = blank term.
+template <int K>
+DEV double row_beta(double Cv, double x) {
+  double B = x;
+#pragma unroll
+  for (int k = 0; k < K; ++k) {
+    const int d = 1 << k;
+    double Cr, Br;
+    if (d == 1) {
+      Cr = dpp_move_d<row_shl(1)>(Cv, kNegInfD);
+      Br = dpp_move_d<row_shl(1)>(B, 0.0);
+    } else if (d == 2) {
+      Cr = dpp_move_d<row_shl(2)>(Cv, kNegInfD);
+      Br = dpp_move_d<row_shl(2)>(B, 0.0);
+    } else if (d == 4) {
+      Cr = dpp_move_d<row_shl(4)>(Cv, kNegInfD);
+      Br = dpp_move_d<row_shl(4)>(B, 0.0);
+    } else {
+      Cr = dpp_move_d<row_shl(8)>(Cv, kNegInfD);
+      Br = dpp_move_d<row_shl(8)>(B, 0.0);
+    }
+    Cv = log2add(Cv, Cr + B);
+    B = B + Br;
+  }
+  return Cv;
+}
+
+// The band of one utterance as buffer resources over its [T, S] rows.
+struct ScanSrc {
+  Rsrc px, py, rg;
+  int S, Tn, Un;
+};
+
+DEV ScanSrc scan_src(const BandArgs& a, int n, int Tn, int Un) {
+  const size_t off = (size_t)n * a.b.T * a.S;
+  const size_t bytes = (size_t)a.b.T * a.S * 4;
+  ScanSrc v;
+  v.px = make_rsrc(a.px + off, bytes);
+  v.py = make_rsrc(a.py + off, bytes);
+  v.rg = make_rsrc(a.ranges + off, bytes);
+  v.S = a.S;
+  v.Tn = Tn;
+  v.Un = Un;
+  return v;
+}
+
+// What one lane needs of frame t: its slot's px, py and the frame's p_t,
+// p_{t+1}, as loaded (clamped where used, so that no arithmetic waits on a
+// load before the frame's turn). Frame T_n is the virtual end frame
+// (p = U_n, one node).
+struct FrameIn {
+  float x, y;
+  uint32_t p, pn;
+  bool last;  // t + 1 == T_n (or no frame)
+};
+
+DEV int clamp_p(int p, int Un) { return min(max(p, 0), Un); }
+
+DEV FrameIn scan_load(const ScanSrc& v, int t, int s) {
+  FrameIn f;
+  const bool in = t >= 0 && t < v.Tn;
+  const uint32_t o = (in && s < v.S) ? (uint32_t)(t * v.S + s) * 4u : kOob;
+  f.x = buf_load_f32(v.px, o);
+  f.y = buf_load_f32(v.py, o);
+  const uint32_t po = in ? (uint32_t)(t * v.S) * 4u : kOob;
+  const uint32_t pno = (in && t + 1 < v.Tn) ? (uint32_t)((t + 1) * v.S) * 4u : kOob;
+  f.p = __builtin_amdgcn_raw_buffer_load_b32(v.rg, (int)po, 0, 0);
+  f.pn = __builtin_amdgcn_raw_buffer_load_b32(v.rg, (int)pno, 0, 0);
+  f.last = !(in && t + 1 < v.Tn);
+  return f;
+}
+
+DEV int frame_p(const FrameIn& f, const ScanSrc& v) { return clamp_p((int)f.p, v.Un); }
+DEV int frame_pn(const FrameIn& f, const ScanSrc& v) { return f.last ? v.Un : clamp_p((int)f.pn, v.Un); }
+
+DEV int frame_nodes(int S, int Un, int p) { return min(S, Un - p + 1); }
+
+// One forward frame: returns alpha(t, s) and replaces ain by the arrivals at
+// frame t+1 (at the virtual end frame: the end value in slot 0). Inactive
+// lanes keep ain.
+template <int K>
+DEV double alpha_frame(double& ain, const FrameIn& f, const ScanSrc& v, int s, int rowbase, bool act) {
+  const int p = frame_p(f, v), pn = frame_pn(f, v);
+  const int ns = frame_nodes(v.S, v.Un, p);
+  const int nsn = frame_nodes(v.S, v.Un, pn);
+  const bool valid = act && s < ns;
+  const double x = valid ? (double)f.x * kLog2e : kNegInfD;
+  const double y = valid ? (double)f.y * kLog2e : kNegInfD;
+  const double al = row_alpha<K>(valid ? ain : kNegInfD, x);
+  const double h = valid ? al + y : kNegInfD;
+  const int src = s + (pn - p);
+  const bool ok = src >= 0 && src < ns && s < nsn;
+  const double hs = bperm_d(h, rowbase + (ok ? src : s));
+  ain = act ? (ok ? hs : kNegInfD) : ain;
+  return valid ? al : kNegInfD;
+}
+
+// One backward frame: bt holds beta of frame t+1 (slots relative to
+// p_{t+1}); returns beta(t, s), and the blank and symbol terms the
+// occupations add to alpha: eyp = py + beta(t+1, .), exq = px + beta(t, s+1).
+template <int K>
+DEV void beta_frame(double& bt, const FrameIn& f, const ScanSrc& v, int s, int rowbase, bool act, double& eyp,
+                    double& exq) {
+  const int p = frame_p(f, v), pn = frame_pn(f, v);
+  const int ns = frame_nodes(v.S, v.Un, p);
+  const int nsn = frame_nodes(v.S, v.Un, pn);
+  const bool valid = act && s < ns;
+  const double x = valid ? (double)f.x * kLog2e : kNegInfD;
+  const double y = valid ? (double)f.y * kLog2e : kNegInfD;
+  const int src = s - (pn - p);
+  const bool ok = valid && src >= 0 && src < nsn;
+  const double bs = bperm_d(bt, rowbase + (ok ? src : s));
+  const double bn = ok ? bs : kNegInfD;
+  const double cv = valid ? y + bn : kNegInfD;
+  const double be0 = row_beta<K>(cv, x);
+  const double be = valid ? be0 : kNegInfD;
+  const double bnext = dpp_move_d<row_shl(1)>(be, kNegInfD);
+  eyp = cv;
+  exq = valid ? x + bnext : kNegInfD;
+  bt = act ? be : bt;
+}
+
+// Wave w of the grid: chains 4g .. 4g+3 (one per 16-lane row) of chunk c of
+// utterance n. Each chain starts from a unit arrival at slot i of the
+// chunk's first frame and runs the chunk's frames; the arrivals at the next
+// chunk's first frame are row i of M, or for the last chunk the end value
+// is E[i].
+template <int K>
+__global__ __launch_bounds__(256) void scan_chunk_kernel(BandArgs a) {
+  const int lane = threadIdx.x & 63, row = lane >> 4, s = lane & 15;
+  const int S = a.S, nc = a.nchunk, G = (S + 3) >> 2;
+  const int w = blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // uniform: scalar resources
+  if (w >= a.b.N * nc * G) return;
+  const int g = w % G, c = (w / G) % nc, n = w / (G * nc);
+  int Tn, Un;
+  utt_dims(a.b, n, Tn, Un);
+  const int t0 = c * a.C;
+  if (t0 >= Tn) return;
+  const int len = min(a.C, Tn - t0);
+  const ScanSrc v = scan_src(a, n, Tn, Un);
+  const int i = 4 * g + row;
+  const int rowbase = row << 4;
+  double ain = (s == i) ? 0.0 : kNegInfD;
+  bool nan_in = false;  // a NaN among the log-probs the recursion uses
+  FrameIn ring[kPrefetch];
+#pragma unroll
+  for (int j = 0; j < kPrefetch; ++j) ring[j] = scan_load(v, t0 + j, s);
+  for (int k0 = 0; k0 < len; k0 += kPrefetch) {
+#pragma unroll
+    for (int j = 0; j < kPrefetch; ++j) {
+      const int k = k0 + j;
+      const FrameIn& f = ring[j];
+      const int p = frame_p(f, v);
+      const bool used = (k < len) & (s < frame_nodes(S, Un, p));
+      nan_in |= used & ((f.y != f.y) | ((p + s < Un) & (f.x != f.x)));
+      alpha_frame<K>(ain, f, v, s, rowbase, k < len);
+      ring[j] = scan_load(v, t0 + k + kPrefetch, s);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+  // A NaN poisons the whole chunk matrix, so that it reaches the loss
+  // whatever the band's paths through it.
+  if (__ballot(nan_in) != 0) ain = __builtin_nan("");
+  if (i >= S) return;
+  if (t0 + len < Tn) {
+    if (s < S) a.M[(((size_t)n * nc + c) * S + i) * S + s] = ain;
+  } else if (s == 0) {
+    a.E[(size_t)n * S + i] = ain;
+  }
+}
+
+// lse of the NS values a lane holds (entries beyond S are -inf; fixed
+// order; a NaN entry gives NaN).
+template <int NS>
+DEV double lse_vals(const double (&xs)[NS]) {
+  double mx = xs[0];
+#pragma unroll
+  for (int i = 1; i < NS; ++i) mx = (xs[i] > mx || xs[i] != xs[i]) ? xs[i] : mx;
+  if (mx == kNegInfD || mx != mx) return mx;
+  float sum = 0.f;
+#pragma unroll
+  for (int i = 0; i < NS; ++i) sum += __builtin_amdgcn_exp2f((float)(xs[i] - mx));
+  return mx + (double)__builtin_amdgcn_logf(sum);
+}
+
+DEV double readlane_d(double v, int l) {
+  const int lo = __builtin_amdgcn_readlane(__double2loint(v), l);
+  const int hi = __builtin_amdgcn_readlane(__double2hiint(v), l);
+  return __hiloint2double(hi, lo);
+}
+
+DEV double buf_load_f64(Rsrc r, uint32_t off) {
+  typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+  return __builtin_bit_cast(double, __builtin_amdgcn_raw_buffer_load_b64(r, (int)off, 0, 0));
+}
+
+// Per utterance: wave 0 carries the arrivals forward through the chunk
+// matrices (V) and forms the loss; wave 1 carries beta backward (Wb). Lane j
+// holds slot j; the other lanes' values come in by readlane. The matrix
+// entries of the next step are loaded while the current one is computed
+// (straight-line buffer loads, so the wait counts stay exact).
+template <int K>
+__global__ __launch_bounds__(128) void scan_sweep_kernel(BandArgs a) {
+  constexpr int NS = 1 << K;  // slots carried: S <= NS
+  const int n = blockIdx.x;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int S = a.S, nc = a.nchunk;
+  int Tn, Un;
+  const bool ok = utt_dims(a.b, n, Tn, Un);
+  const int ncn = (Tn + a.C - 1) / a.C;
+  const Rsrc Mr = make_rsrc(a.M + (size_t)n * nc * S * S, (size_t)nc * S * S * 8);
+  const Rsrc Vr = make_rsrc(a.V + (size_t)n * nc * S, (size_t)nc * S * 8);
+  const Rsrc Wr = make_rsrc(a.Wb + (size_t)n * nc * S, (size_t)nc * S * 8);
+  const bool live = lane < S;
+  double m[NS], mnext[NS];
+  if (wave == 0) {
+    const int p0 = clamp_p(a.ranges[(size_t)n * a.b.T * S], Un);
+    double vv = (lane == 0 && p0 == 0) ? 0.0 : kNegInfD;
+    // M_c[i][lane] of the chunk applied next
+#pragma unroll
+    for (int i = 0; i < NS; ++i)
+      mnext[i] = buf_load_f64(Mr, (live && i < S && ncn > 1) ? (uint32_t)(i * S + lane) * 8u : kOob);
+    buf_store_f64(Vr, live ? (uint32_t)lane * 8u : kOob, vv);
+    for (int c = 0; c < ncn - 1; ++c) {
+#pragma unroll
+      for (int i = 0; i < NS; ++i) m[i] = mnext[i];
+      const bool more = c + 2 < ncn;
+#pragma unroll
+      for (int i = 0; i < NS; ++i)
+        mnext[i] = buf_load_f64(Mr, (more && live && i < S) ? (uint32_t)(((c + 1) * S + i) * S + lane) * 8u : kOob);
+      double xs[NS];
+#pragma unroll
+      for (int i = 0; i < NS; ++i) xs[i] = readlane_d(vv, i) + m[i];  // lanes >= S hold -inf
+      const double nv = lse_vals<NS>(xs);
+      vv = live ? nv : kNegInfD;
+      buf_store_f64(Vr, live ? (uint32_t)((c + 1) * S + lane) * 8u : kOob, vv);
+    }
+    // loss: the arrivals at the last chunk times its end vector
+    const double e = live ? a.E[(size_t)n * S + lane] : kNegInfD;
+    const double ve = vv + e;
+    double xs[NS];
+#pragma unroll
+    for (int i = 0; i < NS; ++i) xs[i] = readlane_d(ve, i);
+    const double L = lse_vals<NS>(xs);
+    if (lane == 0) {
+      const double L2 = ok ? L : __builtin_nan("");
+      a.Lutt[n] = L2;
+      a.loss[n] = (L2 == L2) ? (float)(-L2 * kLn2) : __builtin_nanf("");
+    }
+  } else {
+    double ww = live ? a.E[(size_t)n * S + lane] : kNegInfD;
+    // row `lane` of M_{c-1}
+#pragma unroll
+    for (int j = 0; j < NS; ++j)
+      mnext[j] =
+          buf_load_f64(Mr, (live && j < S && ncn > 1) ? (uint32_t)(((ncn - 2) * S + lane) * S + j) * 8u : kOob);
+    buf_store_f64(Wr, live ? (uint32_t)((ncn - 1) * S + lane) * 8u : kOob, ww);
+    for (int c = ncn - 1; c > 0; --c) {
+#pragma unroll
+      for (int j = 0; j < NS; ++j) m[j] = mnext[j];
+      const bool more = c >= 2;
+#pragma unroll
+      for (int j = 0; j < NS; ++j)
+        mnext[j] = buf_load_f64(Mr, (more && live && j < S) ? (uint32_t)(((c - 2) * S + lane) * S + j) * 8u : kOob);
+      double xs[NS];
+#pragma unroll
+      for (int j = 0; j < NS; ++j) xs[j] = (j < S) ? m[j] + readlane_d(ww, j) : kNegInfD;
+      const double nw = lse_vals<NS>(xs);
+      ww = live ? nw : kNegInfD;
+      buf_store_f64(Wr, live ? (uint32_t)((c - 1) * S + lane) * 8u : kOob, ww);
+    }
+  }
+}
+
+// Four chunks per workgroup (one per 16-lane row). Wave 0 replays alpha from
+// the chunk's forward message, wave 1 beta from the next chunk's beta (or the
+// end of the lattice); both keep their rows in LDS, then all lanes form the
+// occupations frame by frame.
+template <int K>
+__global__ __launch_bounds__(128) void scan_replay_kernel(BandArgs a) {
+  // one spare frame row takes the stores of steps past a chunk's end
+  __shared__ double s_al[4][kScanMaxC + 1][16];
+  __shared__ double s_ey[4][kScanMaxC + 1][16];
+  __shared__ double s_ex[4][kScanMaxC + 1][16];
+  const int n = blockIdx.y;
+  const int lane = threadIdx.x & 63, row = lane >> 4, s = lane & 15;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int S = a.S, nc = a.nchunk, C = a.C, T = a.b.T;
+  int Tn, Un;
+  utt_dims(a.b, n, Tn, Un);
+  const ScanSrc v = scan_src(a, n, Tn, Un);
+  const int rowbase = row << 4;
+  const int c = blockIdx.x * 4 + row;
+  const int t0 = c * C;
+  const int len = max(0, min(C, Tn - t0));
+  FrameIn ring[kPrefetch];
+  if (wave == 0) {
+    double ain = (len > 0 && s < S) ? a.V[((size_t)n * nc + c) * S + s] : kNegInfD;
+#pragma unroll
+    for (int j = 0; j < kPrefetch; ++j) ring[j] = scan_load(v, j < len ? t0 + j : -1, s);
+    for (int k0 = 0; k0 < C; k0 += kPrefetch) {
+#pragma unroll
+      for (int j = 0; j < kPrefetch; ++j) {
+        const int k = k0 + j;
+        const double al = alpha_frame<K>(ain, ring[j], v, s, rowbase, k < len);
+        s_al[row][k < len ? k : kScanMaxC][s] = al;
+        const int kk = k + kPrefetch;
+        ring[j] = scan_load(v, kk < len ? t0 + kk : -1, s);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+  } else {
+    const int t1 = t0 + len;
+    double bt;
+    if (t1 < Tn) bt = (len > 0 && s < S) ? a.Wb[((size_t)n * nc + c + 1) * S + s] : kNegInfD;
+    else bt = (s == 0) ? 0.0 : kNegInfD;  // the virtual end frame: one node, beta 0
+#pragma unroll
+    for (int j = 0; j < kPrefetch; ++j) ring[j] = scan_load(v, len - 1 - j >= 0 ? t0 + len - 1 - j : -1, s);
+    for (int k0 = 0; k0 < C; k0 += kPrefetch) {
+#pragma unroll
+      for (int j = 0; j < kPrefetch; ++j) {
+        const int k = len - 1 - (k0 + j);  // frame t0 + k, descending
+        double eyp, exq;
+        beta_frame<K>(bt, ring[j], v, s, rowbase, k >= 0, eyp, exq);
+        const int kk0 = k >= 0 ? k : kScanMaxC;
+        s_ey[row][kk0][s] = eyp;
+        s_ex[row][kk0][s] = exq;
+        const int kk = k - kPrefetch;
+        ring[j] = scan_load(v, kk >= 0 ? t0 + kk : -1, s);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+  }
+  __syncthreads();
+  const double Lu = a.Lutt[n];
+  const bool lv = (Lu == Lu) && (Lu != kNegInfD);
+  // occupations: 8 frames (16-lane rows) at a time over the 4 chunks
+  const int q0 = threadIdx.x >> 4;
+  for (int q = q0; q < 4 * C; q += 8) {
+    const int cr = q / C, k = q - cr * C;
+    const int t = (blockIdx.x * 4 + cr) * C + k;
+    if (t >= T) continue;  // uniform per 16-lane row
+    const bool live = lv && t < Tn;
+    double ey = kNegInfD, ex = kNegInfD;
+    if (live && s < S) {
+      const double al = s_al[cr][k][s];
+      ey = al + s_ey[cr][k][s];
+      ex = al + s_ex[cr][k][s];
+    }
+    // frame total over the row (butterfly within 16 lanes)
+    double mx = ey;
+#pragma unroll
+    for (int off = 8; off >= 1; off >>= 1) {
+      const double o = __shfl_xor(mx, off, 16);
+      mx = o > mx ? o : mx;
+    }
+    double sm = (ey != kNegInfD) ? (double)__builtin_amdgcn_exp2f((float)(ey - mx)) : 0.0;
+#pragma unroll
+    for (int off = 8; off >= 1; off >>= 1) sm += __shfl_xor(sm, off, 16);
+    const double Lt = mx + log2(sm);
+    if (s < S) {
+      float gxv = 0.f, gyv = 0.f;
+      if (live && ey != kNegInfD) gyv = exp2_occ(ey - Lt);
+      if (live && ex != kNegInfD) gxv = exp2_occ(ex - Lt);
+      const size_t o = ((size_t)n * T + t) * S + s;
+      if (a.gx) a.gx[o] = gxv;
+      if (a.gy) a.gy[o] = gyv;
+    }
+  }
+}
+
+int scan_steps(int S) { return S <= 1 ? 0 : S <= 2 ? 1 : S <= 4 ? 2 : S <= 8 ? 3 : 4; }
+
+template <int K>
+hipError_t launch_scan_k(const BandArgs& a, hipStream_t s) {
+  const int G = (a.S + 3) / 4;
+  const long long waves = (long long)a.b.N * a.nchunk * G;
+  {
+    RNNT_PROF(s, "scan_chunk");
+    hipLaunchKernelGGL((scan_chunk_kernel<K>), dim3((unsigned)((waves + 3) / 4)), dim3(256), 0, s, a);
+  }
+  {
+    RNNT_PROF(s, "scan_sweep");
+    hipLaunchKernelGGL((scan_sweep_kernel<K>), dim3(a.b.N), dim3(128), 0, s, a);
+  }
+  {
+    RNNT_PROF(s, "scan_replay");
+    hipLaunchKernelGGL((scan_replay_kernel<K>), dim3((a.nchunk + 3) / 4, a.b.N), dim3(128), 0, s, a);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace
+
+int band_scan_chunk(int T) {
+  // the chain is about C frames in each of the chunk and replay kernels plus
+  // T / C matrix-vector steps in the sweep
+  int C = 4;
+  while (C < kScanMaxC && 2 * C * C < T) C *= 2;
+  return C;
+}
+
+hipError_t launch_band_scan(const BandArgs& a, hipStream_t s) {
+  if (a.S > kScanMaxS || a.C < 1 || a.C > kScanMaxC) return hipErrorInvalidValue;
+  switch (scan_steps(a.S)) {
+    case 0: return launch_scan_k<0>(a, s);
+    case 1: return launch_scan_k<1>(a, s);
+    case 2: return launch_scan_k<2>(a, s);
+    case 3: return launch_scan_k<3>(a, s);
+    default: return launch_scan_k<4>(a, s);
+  }
+}

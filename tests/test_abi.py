@@ -41,7 +41,7 @@ def test_library_exports_every_declared_symbol(L):
     missing = [n for n in _declared() if not hasattr(L, n)]
     assert not missing, f"not exported: {missing}"
     assert set(_declared()) == set(_native.SIGNATURES), "binding signatures out of sync with the header"
-    assert L.rnnt_abi_version() == 4
+    assert L.rnnt_abi_version() == 5
 
 
 def test_workspace_queries(L):
@@ -57,9 +57,20 @@ def test_workspace_queries(L):
     b32 = L.rnnt_pruned_joiner_backward_workspace_size(16, 250, 60, 5, 512, 500, N.RNNT_F32)
     b16 = L.rnnt_pruned_joiner_backward_workspace_size(16, 250, 60, 5, 512, 500, N.RNNT_BF16)
     assert b32 > b16 > 0
-    # the band's alpha and beta (fp64) over min(T+U, S T) diagonals of S slots, at least
-    p = L.rnnt_pruned_loss_workspace_size(16, 250, 60, 5)
-    assert p >= 2 * 16 * (250 + 60) * 5 * 8
+    # wavefront: alpha and beta (fp64) over T+U diagonals of at least S slots
+    wf = L.rnnt_pruned_loss_ex_workspace_size(16, 250, 60, 5, 1, 0)
+    assert wf >= 2 * 16 * (250 + 60) * 5 * 8
+    # scan with chunks of C frames: an S x S matrix per chunk (fp64), at least
+    for C in (1, 8, 32):
+        assert L.rnnt_pruned_loss_ex_workspace_size(16, 250, 60, 5, 2, C) >= 16 * (-(-250 // C)) * 25 * 8
+    assert L.rnnt_pruned_loss_ex_workspace_size(16, 250, 60, 5, 2, 33) == 0    # chunk too long
+    assert L.rnnt_pruned_loss_ex_workspace_size(16, 250, 60, 17, 2, 0) == 0    # S beyond the scan
+    assert L.rnnt_pruned_loss_ex_workspace_size(16, 250, 60, 5, 3, 0) == 0     # no such algorithm
+    # rnnt_pruned_loss: the automatic choice, the scan for S <= 16
+    assert L.rnnt_pruned_loss_workspace_size(16, 250, 60, 5) == L.rnnt_pruned_loss_ex_workspace_size(
+        16, 250, 60, 5, 2, 0)
+    assert L.rnnt_pruned_loss_workspace_size(16, 250, 60, 20) == L.rnnt_pruned_loss_ex_workspace_size(
+        16, 250, 60, 20, 1, 0)
     assert L.rnnt_pruned_loss_workspace_size(16, 250, 60, 0) == 0
     assert L.rnnt_full_loss_workspace_size(2, 20, 5, 32, 16, N.RNNT_F32) > 0
 
@@ -110,6 +121,15 @@ def test_validation_statuses(L):
     bad = _batch(N=0)
     assert L.rnnt_pruned_loss(ctypes.byref(bad), 4, fake, fake, fake, fake, None, None, fake, 1 << 30,
                               None) == N.RNNT_EINVAL
+    # pruned loss: unknown algorithm, scan beyond S = 16, chunk out of range
+    assert L.rnnt_pruned_loss_ex(pb, 4, 3, 0, fake, fake, fake, fake, None, None, fake, 1 << 30,
+                                 None) == N.RNNT_EINVAL
+    assert L.rnnt_pruned_loss_ex(pb, 17, 2, 0, fake, fake, fake, fake, None, None, fake, 1 << 30,
+                                 None) == N.RNNT_EUNSUPPORTED
+    assert L.rnnt_pruned_loss_ex(pb, 4, 2, 33, fake, fake, fake, fake, None, None, fake, 1 << 30,
+                                 None) == N.RNNT_EINVAL
+    assert L.rnnt_pruned_loss_ex(pb, 4, 2, 0, fake, fake, fake, fake, None, None, fake, 8,
+                                 None) == N.RNNT_EWORKSPACE
     # U beyond the lattice limit
     big = _batch(U=1024)
     assert L.rnnt_prune_ranges(ctypes.byref(big), 4, fake, fake, fake, None) == N.RNNT_EUNSUPPORTED

@@ -168,3 +168,28 @@ def test_long_transcript_near_the_lattice_limit():
     assert_close("py_occ", host(got["py_occ"]), s1["gy"], atol=1e-4)
     assert_close("am_grad", host(got["am_grad"]), s1["am_grad"], atol=1e-4)
     assert_close("lm_grad", host(got["lm_grad"]), s1["lm_grad"], atol=1e-4)
+
+
+@pytest.mark.parametrize("alg,chunk", [("wavefront", 0), ("scan", 0), ("scan", 1), ("scan", 2), ("scan", 7)])
+def test_band_algorithms_on_a_mixed_batch(alg, chunk):
+    # T_n = 1, U_n = 0, an infeasible utterance and ragged lengths in one
+    # batch; bounds from the oracle's pruning of random occupations
+    N, T, U, S = 6, 23, 9, 4
+    rng = np.random.default_rng(21)
+    t_len = np.array([1, 23, 5, 17, 2, 11], np.int32)
+    u_len = np.array([0, 9, 3, 6, 7, 0], np.int32)
+    gx = rng.random((N, T, U + 1))
+    gy = rng.random((N, T, U + 1))
+    ranges = O.prune_ranges(gx, gy, t_len, u_len, S)
+    px = (-1.0 - np.abs(rng.standard_normal((N, T, S)))).astype(np.float32)
+    py = (-1.0 - np.abs(rng.standard_normal((N, T, S)))).astype(np.float32)
+    loss_ref, gx_ref, gy_ref = O.pruned_loss(px.astype(np.float64), py.astype(np.float64), ranges, t_len, u_len)
+    assert loss_ref[4] == np.inf  # U_n = 7 > (S-1) T_n = 6
+    b = dataclasses.replace(_small(seed=12, N=N, T_range=(T, T), U_range=(U, U), S=S), t_len=t_len, u_len=u_len)
+    say(f"[edge] mixed batch, band algorithm {alg} chunk {chunk}")
+    batch = make_dev_batch(b)
+    r = P.rnnt_pruned_loss(batch, S, dev_f32(px), dev_f32(py), dev_i32(ranges), algorithm=alg, chunk=chunk)
+    torch.cuda.synchronize()
+    assert_close("loss", host(r["loss"]), loss_ref, rtol=1e-5)
+    assert_close("px_occ", host(r["px_occ"]), gx_ref, atol=1e-4)
+    assert_close("py_occ", host(r["py_occ"]), gy_ref, atol=1e-4)

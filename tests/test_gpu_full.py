@@ -68,6 +68,25 @@ def test_full_size_invariants(name):
     assert abs(out["bias_grad"].sum()) <= 1e-4 * max(1.0, np.abs(out["bias_grad"]).max()) * np.sqrt(b.V)
 
 
+@pytest.mark.parametrize("name", ["bpe", "long", "largev", "stress"])
+def test_full_size_band_recursion_against_oracle(name):
+    # both algorithms of the pruned recursion at the full size, on the GPU
+    # joiner's own band log-probs and bounds (fp32, as the library takes them)
+    b, out = _run(name)
+    S = b.wl.S
+    px, py, rg = out["px"].astype(np.float32), out["py"].astype(np.float32), out["ranges"]
+    say(f"[full] {name}: oracle band recursion")
+    loss_ref, gx_ref, gy_ref = O.pruned_loss(px.astype(np.float64), py.astype(np.float64), rg, b.t_len, b.u_len)
+    batch = make_dev_batch(b)
+    for alg in ("wavefront", "scan"):
+        say(f"[full] {name}: band algorithm {alg}")
+        r = P.rnnt_pruned_loss(batch, S, dev_f32(px), dev_f32(py), dev_i32(rg), algorithm=alg)
+        torch.cuda.synchronize()
+        assert_close(f"{alg} loss", host(r["loss"]), loss_ref, rtol=1e-5)
+        assert_close(f"{alg} px_occ", host(r["px_occ"]), gx_ref, atol=1e-4)
+        assert_close(f"{alg} py_occ", host(r["py_occ"]), gy_ref, atol=1e-4)
+
+
 @pytest.mark.parametrize("name", ["bpe", "long"])
 def test_full_size_whole_batch_against_oracle(name):
     b, out = _run(name)

@@ -124,18 +124,25 @@ def test_pruned_joiner(name):
     assert_close("logits", host(out["logits"])[present], ref[present], atol=tol)
 
 
+# the pruned recursion's algorithms: the library's choice, the wavefront, and
+# the chunked scan with its default chunk and with chunks of 1, 3 and 32 frames
+BAND_ALGS = [(None, 0), ("wavefront", 0), ("scan", 0), ("scan", 1), ("scan", 3), ("scan", 32)]
+
+
+@pytest.mark.parametrize("alg,chunk", BAND_ALGS, ids=[f"{a}{c or ''}" for a, c in BAND_ALGS])
 @pytest.mark.parametrize("name", list(CASES))
-def test_pruned_loss(name):
+def test_pruned_loss(name, alg, chunk):
     o = _oracle(name)
     b = o["b"]
-    say(f"[band] {name}")
+    say(f"[band] {name} algorithm={alg} chunk={chunk}")
     st = o["st"]
     # both sides take the same fp32 band log-probs
     px32, py32 = st["px"].astype(np.float32), st["py"].astype(np.float32)
     loss_ref, gx_ref, gy_ref = O.pruned_loss(px32.astype(np.float64), py32.astype(np.float64), o["ranges"],
                                              b.t_len, b.u_len)
     batch = make_dev_batch(b)
-    out = P.rnnt_pruned_loss(batch, o["S"], dev_f32(px32), dev_f32(py32), dev_i32(o["ranges"]))
+    out = P.rnnt_pruned_loss(batch, o["S"], dev_f32(px32), dev_f32(py32), dev_i32(o["ranges"]), algorithm=alg,
+                             chunk=chunk)
     torch.cuda.synchronize()
     assert_close("loss", host(out["loss"]), loss_ref, rtol=1e-5)
     assert_close("px_occ", host(out["px_occ"]), gx_ref, atol=1e-4)
