@@ -94,8 +94,43 @@ def _unpruned(P, batch, enc, dec, W, bias, frames, dev, steps: int = 5) -> dict:
             "peak_hbm_bytes_excl_inputs": int(peak), "steps": steps}
 
 
-def _cpu_baseline(b, S, budget_s: float) -> dict:
-    """The CPU oracle (as is) on the first utterances of the same batch, one thread."""
+def _band_algorithms(P, batch, S, out, reps: int = 20) -> dict:
+    """The pruned recursion alone (loss and band occupations), each algorithm
+    on this workload's own band log-probs and bounds from one step: the
+    anti-diagonal wavefront (depth T_n + U_n) and the chunked scan over frames
+    (depth about 2C + T_n / C)."""
+    import torch
+    px, py, rg = out["px"], out["py"], out["ranges"]
+    N, T, U = batch.N, batch.T, batch.U
+    res = {}
+    for alg, chunk in (("wavefront", 0), ("scan", 0)):
+        nbytes = P.pruned_loss_workspace_size(N, T, U, S, alg, chunk)
+        if nbytes == 0:
+            continue  # S beyond what the algorithm supports
+        ws = torch.empty(nbytes, dtype=torch.uint8, device=px.device)
+        loss = torch.empty(N, dtype=torch.float32, device=px.device)
+        gx, gy = torch.empty_like(px), torch.empty_like(px)
+        run = lambda: P.rnnt_pruned_loss(batch, S, px, py, rg, loss=loss, px_occ=gx, py_occ=gy, workspace=ws,
+                                         algorithm=alg, chunk=chunk)
+        for _ in range(3):
+            run()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            run()
+        e1.record()
+        torch.cuda.synchronize()
+        res[alg] = {"us_per_call": round(1000 * e0.elapsed_time(e1) / reps, 1), "workspace_bytes": nbytes}
+    res["auto"] = "scan" if S <= 16 else "wavefront"
+    res["reps"] = reps
+    return res
+
+
+def _cpu_baseline(b, S, budget_s: float, min_s: float = 10.0) -> dict:
+    """The CPU oracle (as is) on the utterances of the same batch, one thread,
+    in whole passes over the batch until at least min_s seconds of work (and
+    no further utterance once budget_s is spent)."""
     import numpy as np
     from threadpoolctl import threadpool_limits
 
@@ -104,7 +139,8 @@ def _cpu_baseline(b, S, budget_s: float) -> dict:
     done = 0
     t0 = time.perf_counter()
     with threadpool_limits(1):
-        for n in range(b.N):
+        while True:
+            n = done % b.N
             sl = slice(n, n + 1)
             s1 = O.simple_stage(b.am[sl], b.lm[sl], b.symbols[sl], b.t_len[sl], b.u_len[sl], b.wl.blank,
                                 scale=np.full(1, 0.5))
@@ -113,13 +149,14 @@ def _cpu_baseline(b, S, budget_s: float) -> dict:
                            b.wl.blank)
             frames += int(b.t_len[n])
             done += 1
-            if time.perf_counter() - t0 > budget_s:
+            el = time.perf_counter() - t0
+            if el > budget_s or (el > min_s and done % b.N == 0):
                 break
     dt = time.perf_counter() - t0
     return {"value": round(frames / dt, 2), "unit": "frames/s", "cores": 1, "kind": "oracle",
-            "sample": f"{done} of {b.N} utterances of the same batch ({frames} frames), full oracle path "
-                      f"(trivial joiner, lattice, am/lm grads, bounds, pruned joiner, pruned lattice, joiner grads), "
-                      f"fp64 NumPy, 1 thread, {dt:.1f} s"}
+            "sample": f"{done} utterance runs over the {b.N} utterances of the same batch ({frames} frames), "
+                      f"full oracle path (trivial joiner, lattice, am/lm grads, bounds, pruned joiner, pruned "
+                      f"lattice, joiner grads), fp64 NumPy, 1 thread, {dt:.1f} s"}
 
 
 def main() -> int:
@@ -132,6 +169,8 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-unpruned", action="store_true",
                     help="skip the comparison with the unpruned loss (same joiner at every (t, u))")
+    ap.add_argument("--no-band-algorithms", action="store_true",
+                    help="skip timing the pruned recursion's algorithms one by one")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="before the census, run one device-to-device copy of this many MiB (a plain copy "
                          "kernel of known size that scales rocprofv3's FETCH_SIZE / WRITE_SIZE)")
@@ -246,6 +285,8 @@ def main() -> int:
                 "algorithmic_flops_per_launch": per_launch_flops, "avg_launch_us": timed["avg_us"],
                 "launches_timed": timed["launches"]}
 
+    band = None if args.no_band_algorithms else _band_algorithms(P, batch, S,
+                                                                 step.step(batch, am, lm, enc, dec, W, bias))
     unpruned = None if args.no_unpruned else _unpruned(P, batch, enc, dec, W, bias, frames, dev)
     cpu = None if args.no_cpu_baseline else _cpu_baseline(b, S, args.cpu_budget)
     line = {
@@ -267,6 +308,7 @@ def main() -> int:
         "peak_hbm_bytes_excl_inputs": int(peak - inputs_mem),
         "wall_s_timed": round(wall, 3),
         "roofline": roofline,
+        "band_algorithms": band,
         "unpruned": unpruned,
         "kernels": kernels,
         "kernels_census_steps": census_steps,
