@@ -193,18 +193,23 @@ struct JoinerFwdWs {
   float2* part;
   float* tgt;
   float* blk;
+  void* h;
+  int chunk_rows;
   size_t bytes;
 };
 
-JoinerFwdWs joiner_fwd_layout(void* base, int N, int T, int S, int V) {
+JoinerFwdWs joiner_fwd_layout(void* base, int N, int T, int S, int J, int V, int bf16) {
   Carve c(base);
   JoinerFwdWs w;
   const size_t M = (size_t)N * T * S;
+  w.chunk_rows = joiner_fwd_chunk_rows(N, T, S, J, bf16);
   w.frame_off = c.take<int>((size_t)N + 1);
   w.rowinfo = c.take<int4>(M);
   w.part = c.take<float2>(M * joiner_nparts(V));
   w.tgt = c.take<float>(M);
   w.blk = c.take<float>(M);
+  const size_t h_elems = joiner_fwd_uses_hbuf(bf16) ? (size_t)w.chunk_rows * J : 0;
+  w.h = h_elems == 0 ? nullptr : bf16 ? (void*)c.take<uint16_t>(h_elems) : (void*)c.take<float>(h_elems);
   w.bytes = c.off;
   return w;
 }
@@ -290,6 +295,8 @@ void set_joiner_fwd(JoinerArgs& a, const JoinerFwdWs& w, float* px, float* py, f
   a.nparts = joiner_nparts(a.V);
   a.tgt = w.tgt;
   a.blk = w.blk;
+  a.hbuf = w.h;
+  a.chunk_rows = w.chunk_rows;
   a.px = px;
   a.py = py;
   a.lse = lse;
@@ -353,7 +360,7 @@ FullWs full_layout(void* base, int N, int T, int U, int J, int V, int bf16) {
   w.rx = c.take<double>((size_t)N * T);
   w.cpx = c.take<double>((size_t)N * lattice_colblocks(T) * S);
   w.cpy = c.take<double>((size_t)N * lattice_colblocks(T) * S);
-  const size_t jf = joiner_fwd_layout(nullptr, N, T, S, V).bytes;
+  const size_t jf = joiner_fwd_layout(nullptr, N, T, S, J, V, bf16).bytes;
   const size_t jb = joiner_bwd_layout(nullptr, N, T, S, J, V, bf16).bytes;
   w.joiner = c.take<unsigned char>(jf > jb ? jf : jb);
   w.bytes = c.off;
@@ -449,10 +456,8 @@ int rnnt_prune_ranges(const rnnt_batch* batch, int32_t S, const float* px_occ, c
 }
 
 size_t rnnt_pruned_joiner_workspace_size(int32_t N, int32_t T, int32_t S, int32_t J, int32_t V, int32_t dtype) {
-  (void)J;
-  (void)dtype;
-  if (N < 1 || T < 1 || S < 1 || V < 1) return 0;
-  return joiner_fwd_layout(nullptr, N, T, S, V).bytes;
+  if (N < 1 || T < 1 || S < 1 || J < 1 || V < 1) return 0;
+  return joiner_fwd_layout(nullptr, N, T, S, J, V, dtype == RNNT_BF16).bytes;
 }
 
 int rnnt_pruned_joiner(const rnnt_batch* batch, int32_t S, int32_t J, int32_t V, int32_t dtype, const void* enc,
@@ -465,9 +470,10 @@ int rnnt_pruned_joiner(const rnnt_batch* batch, int32_t S, int32_t J, int32_t V,
   if (!enc || !dec || !W || !ranges) return fail(RNNT_EINVAL, "enc, dec, W and ranges are required");
   if (!px || !py || !lse) return fail(RNNT_EINVAL, "px, py and lse are required");
   if (!aligned16(logits)) return fail(RNNT_EINVAL, "logits must be 16-byte aligned");
-  rc = check_ws(workspace, workspace_bytes, joiner_fwd_layout(nullptr, batch->N, batch->T, S, V).bytes);
+  const int bf = dtype == RNNT_BF16;
+  rc = check_ws(workspace, workspace_bytes, joiner_fwd_layout(nullptr, batch->N, batch->T, S, J, V, bf).bytes);
   if (rc) return rc;
-  const JoinerFwdWs w = joiner_fwd_layout(workspace, batch->N, batch->T, S, V);
+  const JoinerFwdWs w = joiner_fwd_layout(workspace, batch->N, batch->T, S, J, V, bf);
   JoinerArgs a = joiner_args(batch, S, J, V, dtype, enc, dec, W, bias, ranges);
   set_joiner_fwd(a, w, px, py, lse, logits);
   hipStream_t s = static_cast<hipStream_t>(stream);
@@ -686,7 +692,7 @@ int rnnt_full_loss(const rnnt_batch* batch, int32_t J, int32_t V, int32_t dtype,
   // the joiner on every (t, u): ranges[n,t,s] = s with S = U + 1
   hipError_t e = launch_full_ranges(w.ranges, batch->N, batch->T, S, s);
   JoinerArgs jf = joiner_args(batch, S, J, V, dtype, enc, dec, W, bias, w.ranges);
-  set_joiner_fwd(jf, joiner_fwd_layout(w.joiner, batch->N, batch->T, S, V), w.px, w.py, w.lse, logits);
+  set_joiner_fwd(jf, joiner_fwd_layout(w.joiner, batch->N, batch->T, S, J, V, bf), w.px, w.py, w.lse, logits);
   if (e == hipSuccess) e = launch_joiner_prep(jf, s);
   if (e == hipSuccess) e = launch_joiner_fwd(jf, s);
   // the recursion of Eq. (3) on the [T, U+1] lattice and its occupations

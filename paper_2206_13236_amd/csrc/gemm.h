@@ -9,8 +9,9 @@
 //         and B, which leaves the sum unchanged);
 //   bf16: v_mfma_f32_16x16x32_bf16, a fragment holds 8 consecutive k.
 // Accumulation is fp32 in both cases. Global -> register fetches of the next
-// K-step are issued before the MFMAs of the current one; LDS is double
-// buffered, so there is one barrier per K-step.
+// K-step (or the one after, for DEEP configurations) are issued before the
+// MFMAs of the current one; LDS is double buffered, so there is one barrier
+// per K-step.
 //
 // Operand sources are supplied by each kernel, in two halves so that global
 // loads for the next K-step stay in flight while the current one computes:
@@ -19,8 +20,11 @@
 //     kc_finish(const Raw&, v[KV])     turn them into KV fp32 values
 //   MNC source (global is row-contiguous): mnc_load(k, row, Raw&) and
 //     mnc_finish(const Raw&, v[16/KV]).
-// Generated operands (tanh(enc+dec), exp(x - max)) are formed in *_finish,
+// Generated operands (exp(x - max), widened inputs) are formed in *_finish,
 // which runs after the MFMAs of the current K-step; the loader packs them.
+// A source whose raw registers already hold the LDS element type declares
+// kDirect: its words go to LDS as loaded (KC), or regrouped by byte
+// permutes (MNC transpose), with no conversion.
 //
 // Output element (i, j, r) of a lane: row = wm*WM + i*16 + 4*(lane>>4) + r,
 // col = wn*WN + j*16 + (lane & 15).
@@ -30,10 +34,13 @@
 
 #include "common.h"
 
-template <int BM_, int BN_, int BK_, bool BF16_, int WGM_ = 2, int WGN_ = 2>
+// DEEP_: global fetches run two K-steps ahead (two register sets; for
+// configurations whose K-step is too short to cover a load's latency).
+template <int BM_, int BN_, int BK_, bool BF16_, int WGM_ = 2, int WGN_ = 2, bool DEEP_ = false>
 struct GemmCfg {
   static constexpr int BM = BM_, BN = BN_, BK = BK_;
   static constexpr bool BF16 = BF16_;
+  static constexpr bool DEEP = DEEP_;
   using T = typename std::conditional<BF16_, uint16_t, float>::type;
   static constexpr int ESZ = (int)sizeof(T);
   static constexpr int KV = 16 / ESZ;         // k values per 16-byte fragment
@@ -49,6 +56,12 @@ struct GemmCfg {
   static_assert(BK % KSLICE == 0, "BK must be a multiple of the fragment k-slice");
   static_assert(FM >= 1 && FN >= 1, "tile too small");
 };
+
+// Whether a source declares kDirect = true (absent: false).
+template <class S, class = void>
+struct src_direct : std::false_type {};
+template <class S>
+struct src_direct<S, std::void_t<decltype(S::kDirect)>> : std::bool_constant<S::kDirect> {};
 
 // Raw operand registers of a source whose values need no transform.
 template <int N>
@@ -97,9 +110,15 @@ struct KCLoader {
     for (int i = 0; i < NCH; ++i) {
       int c = threadIdx.x + Cfg::NT * i;
       if (ROWS * CPR % Cfg::NT == 0 || c < ROWS * CPR) {
-        float v[KV];
-        src.kc_finish(r.v[i], v);
-        pack_store16<Cfg>(lds + (c / CPR) * Cfg::LDK + (c % CPR) * KV, v);
+        typename Cfg::T* dst = lds + (c / CPR) * Cfg::LDK + (c % CPR) * KV;
+        if constexpr (src_direct<Src>::value) {
+          const uint32_t* w = r.v[i].w;
+          *reinterpret_cast<uint4*>(dst) = make_uint4(w[0], w[1], w[2], w[3]);
+        } else {
+          float v[KV];
+          src.kc_finish(r.v[i], v);
+          pack_store16<Cfg>(dst, v);
+        }
       }
     }
   }
@@ -139,15 +158,35 @@ struct MNCLoader {
       int blk = threadIdx.x + Cfg::NT * b;
       if (NBLK % Cfg::NT == 0 || blk < NBLK) {
         const int kb = blk % NKB, nb = blk / NKB;
-        float m[KV][NV];
+        if constexpr (src_direct<Src>::value) {
+          // r.v[b][i] holds row elements nb*NV .. nb*NV+NV-1 at k = kb*KV + i
 #pragma unroll
-        for (int i = 0; i < KV; ++i) src.mnc_finish(r.v[b][i], m[i]);
+          for (int c = 0; c < NV; ++c) {
+            uint32_t o[4];
+            if constexpr (Cfg::BF16) {
+              // two bf16 rows per word: row c's k pair (2q, 2q+1) is the low
+              // (c = 0) or high (c = 1) halves of the words of k = 2q, 2q+1
 #pragma unroll
-        for (int c = 0; c < NV; ++c) {
-          float col[KV];
+              for (int q = 0; q < 4; ++q)
+                o[q] = __builtin_amdgcn_perm(r.v[b][2 * q + 1].w[0], r.v[b][2 * q].w[0],
+                                             c == 0 ? 0x05040100u : 0x07060302u);
+            } else {
 #pragma unroll
-          for (int i = 0; i < KV; ++i) col[i] = m[i][c];
-          pack_store16<Cfg>(lds + (nb * NV + c) * Cfg::LDK + kb * KV, col);
+              for (int q = 0; q < 4; ++q) o[q] = r.v[b][q].w[c];
+            }
+            *reinterpret_cast<uint4*>(lds + (nb * NV + c) * Cfg::LDK + kb * KV) = make_uint4(o[0], o[1], o[2], o[3]);
+          }
+        } else {
+          float m[KV][NV];
+#pragma unroll
+          for (int i = 0; i < KV; ++i) src.mnc_finish(r.v[b][i], m[i]);
+#pragma unroll
+          for (int c = 0; c < NV; ++c) {
+            float col[KV];
+#pragma unroll
+            for (int i = 0; i < KV; ++i) col[i] = m[i][c];
+            pack_store16<Cfg>(lds + (nb * NV + c) * Cfg::LDK + kb * KV, col);
+          }
         }
       }
     }
@@ -207,6 +246,43 @@ DEV void gemm_mainloop(const LA& la, const LB& lb, int k_begin, int k_end,
   typename Cfg::T* Bs0 = smem + Cfg::A_ELEMS;
   typename Cfg::T* As1 = smem + Cfg::STAGE_ELEMS;
   typename Cfg::T* Bs1 = smem + Cfg::STAGE_ELEMS + Cfg::A_ELEMS;
+  constexpr int KH = (Cfg::BK / Cfg::KSLICE) / 2 * Cfg::KSLICE;
+  if constexpr (Cfg::DEEP) {
+    // Register set p holds the fetch of K-step kt+1 while step kt computes;
+    // step kt+2 is fetched into the other set, freed by the previous put.
+    typename LA::Reg ra[2];
+    typename LB::Reg rb[2];
+    la.fetch(k_begin, ra[0]);
+    lb.fetch(k_begin, rb[0]);
+    if (nk > 1) {
+      la.fetch(k_begin + Cfg::BK, ra[1]);
+      lb.fetch(k_begin + Cfg::BK, rb[1]);
+    }
+    la.put(ra[0], As0);
+    lb.put(rb[0], Bs0);
+    __syncthreads();
+    auto step = [&](int kt, auto par) {
+      constexpr int P = decltype(par)::value;  // kt & 1
+      if (kt + 2 < nk) {
+        la.fetch(k_begin + (kt + 2) * Cfg::BK, ra[P]);
+        lb.fetch(k_begin + (kt + 2) * Cfg::BK, rb[P]);
+      }
+      const typename Cfg::T* Ac = P ? As1 : As0;
+      const typename Cfg::T* Bc = P ? Bs1 : Bs0;
+      gemm_compute_stage<Cfg, 0, KH>(Ac, Bc, acc);
+      if (kt + 1 < nk) {
+        la.put(ra[1 - P], P ? As0 : As1);
+        lb.put(rb[1 - P], P ? Bs0 : Bs1);
+      }
+      gemm_compute_stage<Cfg, KH, Cfg::BK>(Ac, Bc, acc);
+      __syncthreads();
+    };
+    for (int kt = 0; kt < nk; kt += 2) {
+      step(kt, std::integral_constant<int, 0>{});
+      if (kt + 1 < nk) step(kt + 1, std::integral_constant<int, 1>{});
+    }
+    return;
+  }
   typename LA::Reg ra;
   typename LB::Reg rb;
   la.fetch(k_begin, ra);
@@ -217,7 +293,6 @@ DEV void gemm_mainloop(const LA& la, const LB& lb, int k_begin, int k_end,
   // The next stage is staged between the two halves of the current stage's
   // MFMAs: its global loads have the first half to land, and its transforms
   // and LDS stores can issue while the second half's MFMAs execute.
-  constexpr int KH = (Cfg::BK / Cfg::KSLICE) / 2 * Cfg::KSLICE;
   for (int kt = 0; kt < nk; ++kt) {
     const bool more = kt + 1 < nk;
     if (more) {

@@ -8,8 +8,9 @@
 // y_{u+1} (-1 at u = U_n, -2 when it lies outside [0, V)) and the output index
 // n*T*S + t*S + s (-1 when the slot is absent, u > U_n).
 //
-// Forward: logits = tanh(enc + dec) W + bias on MFMA (fp32 16x16x4 or bf16
-// 16x16x32, fp32 accumulation); the tanh is formed while staging the A tile.
+// Forward (per chunk of rows): h = tanh(enc + dec) once per element into a
+// chunk buffer, then logits = h W + bias on MFMA (fp32 16x16x4 or bf16
+// 16x16x32, fp32 accumulation), both operands staged without conversion.
 // The epilogue reduces every (row, 64-column slice) to (max, sum exp) and
 // captures the target and blank logits; a combine kernel turns them into
 // lse, px = logit[y_{u+1}] - lse and py = logit[blank] - lse. The logits
@@ -19,7 +20,7 @@
 // Backward (per chunk of rows, so that d(logits) is held for one chunk only):
 //   1. dl = sc * ((gx+gy) softmax - gx [v=y] - gy [v=blank]) (log-softmax
 //      backward) from the stored logits by a streaming kernel, or, without
-//      them, by recomputing the logits GEMM; write the chunk and column
+//      them, by recomputing h and the logits GEMM; write the chunk and column
 //      sums (db);
 //   2. dh = dl W^T, dpre = dh (1 - h^2)  (tanh backward);
 //   3. dW += h^T dl with split-K partial sums;
@@ -35,7 +36,9 @@ namespace {
 // lane, so two workgroups (four waves per SIMD) share a CU.
 constexpr int kGemmThreads = 512;
 using CfgF = GemmCfg<128, 128, 32, false, 4, 2>;
-using CfgB = GemmCfg<128, 128, 64, true, 4, 2>;
+using CfgB = GemmCfg<128, 128, 64, true, 4, 2, false>;
+// dW stages both operands through register transposes: one fetch set fits
+using CfgBw = GemmCfg<128, 128, 64, true, 4, 2, false>;
 static_assert(CfgF::NT == kGemmThreads && CfgB::NT == kGemmThreads, "joiner GEMM block size");
 static_assert(CfgF::WN == 64 && CfgB::WN == 64, "the forward's partial log-sum-exp slices are 64 columns");
 static_assert(CfgF::BM == CfgB::BM && CfgF::WGM == CfgB::WGM, "db partial rows per row tile");
@@ -52,6 +55,13 @@ struct In<true> {
   using T = uint16_t;
   using Cfg = CfgB;
 };
+
+// Whether the forward reads h from a buffer written by the h kernel (bf16:
+// its MFMA K-steps are too short to hide the tanh work of staging) or forms
+// it while staging the A tile (fp32: measured ~5 us faster per step at the
+// BPE size than a separate h pass).
+template <bool BF>
+constexpr bool kFwdHbuf = BF;
 
 DEV float ld_in(const float* p, size_t i) { return p[i]; }
 DEV float ld_in(const uint16_t* p, size_t i) { return bf2f(p[i]); }
@@ -144,20 +154,6 @@ DEV void raw_to_float(const RawVec<TIn, N>& r, float (&v)[N]) {
 // Operand sources
 // ---------------------------------------------------------------------------
 
-// h = tanh(enc + dec) from two raw segments.
-template <typename TIn, int N>
-struct RawH {
-  RawVec<TIn, N> e, d;
-};
-template <typename TIn, int N>
-DEV void finish_h(const RawH<TIn, N>& r, float (&v)[N]) {
-  float e[N], d[N];
-  raw_to_float(r.e, e);
-  raw_to_float(r.d, d);
-#pragma unroll
-  for (int i = 0; i < N; ++i) v[i] = fast_tanh(e[i] + d[i]);
-}
-
 // enc / dec resources of a launch (row offsets from rowinfo are element offsets).
 template <typename TIn>
 struct EncDec {
@@ -167,10 +163,14 @@ struct EncDec {
         dec(make_rsrc(a.dec, (size_t)a.b.N * (a.b.U + 1) * a.J * sizeof(TIn))) {}
 };
 
-// A(m, j) = tanh(enc[row] + dec[row]) for the tile's rows (rowinfo in LDS).
+// A(m, j) = tanh(enc[row] + dec[row]) formed while staging (rowinfo of the
+// tile's rows in LDS): the fp32 forward, where the tanh work hides under the
+// MFMAs and a separate h pass would only add its HBM traffic.
 template <class Cfg, typename TIn>
 struct HSrcKC {
-  using Raw = RawH<TIn, Cfg::KV>;
+  struct Raw {
+    RawVec<TIn, Cfg::KV> e, d;
+  };
   EncDec<TIn> ed;
   const int4* ri;
   int J;
@@ -180,18 +180,45 @@ struct HSrcKC {
     raw_load(ed.enc, (uint32_t)(q.x + k) * sizeof(TIn), n, kSegVector, r.e);
     raw_load(ed.dec, (uint32_t)(q.y + k) * sizeof(TIn), n, kSegVector, r.d);
   }
-  DEV void kc_finish(const Raw& r, float (&v)[Cfg::KV]) const { finish_h(r, v); }
+  DEV void kc_finish(const Raw& r, float (&v)[Cfg::KV]) const {
+    float e[Cfg::KV], d[Cfg::KV];
+    raw_to_float(r.e, e);
+    raw_to_float(r.d, d);
+#pragma unroll
+    for (int i = 0; i < Cfg::KV; ++i) v[i] = fast_tanh(e[i] + d[i]);
+  }
+};
+
+// A(m, j) = h[m - cm0][j] from a chunk buffer of h = tanh(enc + dec) (zero
+// rows for absent slots).
+template <class Cfg>
+struct HbufSrcKC {
+  static constexpr bool kDirect = true;
+  using T = typename Cfg::T;
+  using Raw = RawVec<T, Cfg::KV>;
+  Rsrc h;
+  int m0, cm0, mend, J;
+  DEV void kc_load(int row, int k, Raw& r) const {
+    const int m = m0 + row;
+    const int n = (m < mend && k < J) ? Cfg::KV : 0;
+    raw_load(h, (uint32_t)((m - cm0) * J + k) * sizeof(T), n, kSegVector, r);
+  }
+  DEV void kc_finish(const Raw& r, float (&v)[Cfg::KV]) const { raw_to_float(r, v); }
 };
 
 // B(j, v) = W[j][v]: global row-contiguous along v.
-template <class Cfg, typename TIn>
+// MODE = seg_mode<TIn>(V, NV), fixed per launch so that the loads compile
+// without branches.
+template <class Cfg, typename TIn, int MODE>
 struct WSrcMNC {
+  static constexpr bool kDirect = true;
   static constexpr int NV = 16 / Cfg::KV;
+  static constexpr int mode = MODE;
   using Raw = RawVec<TIn, NV>;
   Rsrc W;
-  int v0, V, J, mode;
+  int v0, V, J;
   DEV WSrcMNC(const JoinerArgs& a, int v0_)
-      : W(make_rsrc(a.W, (size_t)a.J * a.V * sizeof(TIn))), v0(v0_), V(a.V), J(a.J), mode(seg_mode<TIn>(a.V, NV)) {}
+      : W(make_rsrc(a.W, (size_t)a.J * a.V * sizeof(TIn))), v0(v0_), V(a.V), J(a.J) {}
   DEV void mnc_load(int k, int col, Raw& r) const {
     const int c = v0 + col;
     const int n = (k < J) ? V - c : 0;
@@ -203,6 +230,7 @@ struct WSrcMNC {
 // A(m, v) = dl[m][v] from the chunk buffer (rows padded to ldl with zeros).
 template <class Cfg>
 struct DlSrcKC {
+  static constexpr bool kDirect = true;
   using T = typename Cfg::T;
   using Raw = RawVec<T, Cfg::KV>;
   Rsrc dl;  // row (m - cm0)
@@ -216,14 +244,16 @@ struct DlSrcKC {
 };
 
 // B(v, j) = W[j][v]: global k-contiguous along v for each j.
-template <class Cfg, typename TIn>
+// MODE = seg_mode<TIn>(V, KV), fixed per launch.
+template <class Cfg, typename TIn, int MODE>
 struct WtSrcKC {
+  static constexpr bool kDirect = true;
+  static constexpr int mode = MODE;
   using Raw = RawVec<TIn, Cfg::KV>;
   Rsrc W;
-  int j0, J, V, mode;
+  int j0, J, V;
   DEV WtSrcKC(const JoinerArgs& a, int j0_)
-      : W(make_rsrc(a.W, (size_t)a.J * a.V * sizeof(TIn))), j0(j0_), J(a.J), V(a.V),
-        mode(seg_mode<TIn>(a.V, Cfg::KV)) {}
+      : W(make_rsrc(a.W, (size_t)a.J * a.V * sizeof(TIn))), j0(j0_), J(a.J), V(a.V) {}
   DEV void kc_load(int row, int k, Raw& r) const {
     const int j = j0 + row;
     const int n = (j < J) ? V - k : 0;
@@ -232,28 +262,10 @@ struct WtSrcKC {
   DEV void kc_finish(const Raw& r, float (&v)[Cfg::KV]) const { raw_to_float(r, v); }
 };
 
-// A(j, m) = h(m, j): global is [m][j], j-contiguous; rowinfo read per row
-// (from a clamped index, so the read is unconditional).
-template <class Cfg, typename TIn>
-struct HSrcMNC {
-  static constexpr int NV = 16 / Cfg::KV;
-  using Raw = RawH<TIn, NV>;
-  EncDec<TIn> ed;
-  const int4* rowinfo;
-  int j0, J, mend;
-  DEV void mnc_load(int k, int col, Raw& r) const {
-    const int j = j0 + col;
-    const int4 q = rowinfo[min(k, mend - 1)];
-    const int n = (k < mend && j < J && q.w >= 0) ? NV : 0;
-    raw_load(ed.enc, (uint32_t)(q.x + j) * sizeof(TIn), n, kSegVector, r.e);
-    raw_load(ed.dec, (uint32_t)(q.y + j) * sizeof(TIn), n, kSegVector, r.d);
-  }
-  DEV void mnc_finish(const Raw& r, float (&v)[NV]) const { finish_h(r, v); }
-};
-
 // A(j, m) = h(m, j) from the chunk's hbuf [rows, J] (j-contiguous).
 template <class Cfg>
 struct HbufSrcMNC {
+  static constexpr bool kDirect = true;
   using T = typename Cfg::T;
   static constexpr int NV = 16 / Cfg::KV;
   using Raw = RawVec<T, NV>;
@@ -270,6 +282,7 @@ struct HbufSrcMNC {
 // B(m, v) = dl[m][v]: global row-contiguous along v.
 template <class Cfg>
 struct DlSrcMNC {
+  static constexpr bool kDirect = true;
   using T = typename Cfg::T;
   static constexpr int NV = 16 / Cfg::KV;
   using Raw = RawVec<T, NV>;
@@ -332,33 +345,78 @@ __global__ __launch_bounds__(256) void joiner_prep_kernel(JoinerArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Forward GEMM + partial log-sum-exp
+// h = tanh(enc + dec) of the rows [cm0, min(cm1, M)) into the chunk buffer
+// hbuf [rows, J] in the GEMM operand type (zero rows for absent slots): one
+// 16-byte group of J per thread.
 // ---------------------------------------------------------------------------
 template <bool BF>
-__global__ __launch_bounds__(kGemmThreads, 4) void joiner_fwd_kernel(JoinerArgs a) {
+__global__ __launch_bounds__(256) void joiner_h_kernel(JoinerArgs a, int cm0, int cm1) {
+  using TIn = typename In<BF>::T;
+  constexpr int KV = 16 / (int)sizeof(TIn);
+  const int M = a.frame_off[a.b.N] * a.S;
+  const int mend = min(cm1, M);
+  const int cpr = a.J / KV;
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int rr = (int)(i / cpr), c = (int)(i - (size_t)rr * cpr);
+  const int m = cm0 + rr;
+  if (m >= mend) return;
+  const int4 info = a.rowinfo[m];
+  const int j = c * KV;
+  const EncDec<TIn> ed(a);
+  RawVec<TIn, KV> e, d;
+  const int n = info.w >= 0 ? KV : 0;
+  raw_load(ed.enc, (uint32_t)(info.x + j) * sizeof(TIn), n, kSegVector, e);
+  raw_load(ed.dec, (uint32_t)(info.y + j) * sizeof(TIn), n, kSegVector, d);
+  float fe[KV], fd[KV], h[KV];
+  raw_to_float(e, fe);
+  raw_to_float(d, fd);
+#pragma unroll
+  for (int q = 0; q < KV; ++q) h[q] = info.w >= 0 ? fast_tanh(fe[q] + fd[q]) : 0.f;
+  uint4 o;
+  if constexpr (BF) {
+    uint32_t w[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) w[q] = (uint32_t)f2bf(h[2 * q]) | ((uint32_t)f2bf(h[2 * q + 1]) << 16);
+    o = make_uint4(w[0], w[1], w[2], w[3]);
+  } else {
+    o = make_uint4(__float_as_uint(h[0]), __float_as_uint(h[1]), __float_as_uint(h[2]), __float_as_uint(h[3]));
+  }
+  *reinterpret_cast<uint4*>(reinterpret_cast<TIn*>(a.hbuf) + (size_t)rr * a.J + j) = o;
+}
+
+// ---------------------------------------------------------------------------
+// Forward GEMM + partial log-sum-exp over the rows [cm0, cm1) (h in hbuf)
+// ---------------------------------------------------------------------------
+template <bool BF, int WM>
+__global__ __launch_bounds__(kGemmThreads, 4) void joiner_fwd_kernel(JoinerArgs a, int cm0, int cm1) {
   using TIn = typename In<BF>::T;
   using Cfg = typename In<BF>::Cfg;
   __shared__ __align__(16) typename Cfg::T smem[Cfg::SMEM_BYTES / sizeof(typename Cfg::T)];
   __shared__ int4 ri[Cfg::BM];
   const int M = a.frame_off[a.b.N] * a.S;
+  const int mend = min(cm1, M);
   // the column tiles of one row tile are consecutive tile ids (one XCD, shared A panel)
-  const int tile = xcd_tile_id((M + Cfg::BM - 1) / Cfg::BM * gridDim.y);
+  const int tile = xcd_tile_id(mend > cm0 ? (mend - cm0 + Cfg::BM - 1) / Cfg::BM * gridDim.y : 0);
   if (tile < 0) return;
   const int mt = tile / gridDim.y, nt = tile - mt * gridDim.y;
-  const int m0 = mt * Cfg::BM;
+  const int m0 = cm0 + mt * Cfg::BM;
   const int v0 = nt * Cfg::BN;
   const int V = a.V, J = a.J;
   for (int r = threadIdx.x; r < Cfg::BM; r += Cfg::NT)
-    ri[r] = (m0 + r < M) ? a.rowinfo[m0 + r] : make_int4(0, 0, -1, -1);
+    ri[r] = (m0 + r < mend) ? a.rowinfo[m0 + r] : make_int4(0, 0, -1, -1);
   __syncthreads();
-  const TIn* enc = reinterpret_cast<const TIn*>(a.enc);
-  const TIn* dec = reinterpret_cast<const TIn*>(a.dec);
-  HSrcKC<Cfg, TIn> sa{EncDec<TIn>(a), ri, J};
-  WSrcMNC<Cfg, TIn> sb(a, v0);
-  KCLoader<Cfg, Cfg::BM, HSrcKC<Cfg, TIn>> la(sa);
-  MNCLoader<Cfg, Cfg::BN, WSrcMNC<Cfg, TIn>> lb(sb);
+  WSrcMNC<Cfg, TIn, WM> sb(a, v0);
+  MNCLoader<Cfg, Cfg::BN, WSrcMNC<Cfg, TIn, WM>> lb(sb);
   floatx4 acc[Cfg::FM][Cfg::FN];
-  gemm_mainloop<Cfg>(la, lb, 0, J, smem, acc);
+  if constexpr (kFwdHbuf<BF>) {
+    HbufSrcKC<Cfg> sa{make_rsrc(a.hbuf, (size_t)a.chunk_rows * J * sizeof(typename Cfg::T)), m0, cm0, mend, J};
+    KCLoader<Cfg, Cfg::BM, HbufSrcKC<Cfg>> la(sa);
+    gemm_mainloop<Cfg>(la, lb, 0, J, smem, acc);
+  } else {
+    HSrcKC<Cfg, TIn> sa{EncDec<TIn>(a), ri, J};
+    KCLoader<Cfg, Cfg::BM, HSrcKC<Cfg, TIn>> la(sa);
+    gemm_mainloop<Cfg>(la, lb, 0, J, smem, acc);
+  }
 
   const int lane = threadIdx.x & 63, wn = (threadIdx.x >> 6) % Cfg::WGN;
   const int slice = nt * Cfg::WGN + wn;
@@ -439,9 +497,10 @@ __global__ __launch_bounds__(256) void joiner_combine_kernel(JoinerArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Backward 1: recompute logits, d(logits) for a chunk of rows, db partials.
+// Backward 1: recompute logits from h (hbuf), d(logits) for a chunk of rows,
+// db partials.
 // ---------------------------------------------------------------------------
-template <bool BF>
+template <bool BF, int WM>
 __global__ __launch_bounds__(kGemmThreads) void joiner_dlogits_kernel(JoinerArgs a, int cm0, int cm1) {
   using TIn = typename In<BF>::T;
   using Cfg = typename In<BF>::Cfg;
@@ -467,12 +526,10 @@ __global__ __launch_bounds__(kGemmThreads) void joiner_dlogits_kernel(JoinerArgs
     rx[r] = x;
   }
   __syncthreads();
-  const TIn* enc = reinterpret_cast<const TIn*>(a.enc);
-  const TIn* dec = reinterpret_cast<const TIn*>(a.dec);
-  HSrcKC<Cfg, TIn> sa{EncDec<TIn>(a), ri, J};
-  WSrcMNC<Cfg, TIn> sb(a, v0);
-  KCLoader<Cfg, Cfg::BM, HSrcKC<Cfg, TIn>> la(sa);
-  MNCLoader<Cfg, Cfg::BN, WSrcMNC<Cfg, TIn>> lb(sb);
+  HbufSrcKC<Cfg> sa{make_rsrc(a.hbuf, (size_t)a.chunk_rows * J * sizeof(typename Cfg::T)), m0, cm0, mend, J};
+  WSrcMNC<Cfg, TIn, WM> sb(a, v0);
+  KCLoader<Cfg, Cfg::BM, HbufSrcKC<Cfg>> la(sa);
+  MNCLoader<Cfg, Cfg::BN, WSrcMNC<Cfg, TIn, WM>> lb(sb);
   floatx4 acc[Cfg::FM][Cfg::FN];
   gemm_mainloop<Cfg>(la, lb, 0, J, smem, acc);
 
@@ -640,7 +697,7 @@ __global__ __launch_bounds__(kDlThreads) void joiner_dl_kernel(JoinerArgs a, int
 // Backward 2: dh = dl W^T, dpre = dh (1 - h^2); also leaves h of the chunk's
 // rows in hbuf (zero for absent slots) as the dW contraction's operand.
 // ---------------------------------------------------------------------------
-template <bool BF>
+template <bool BF, int WM>
 __global__ __launch_bounds__(kGemmThreads, 4) void joiner_dh_kernel(JoinerArgs a, int cm0, int cm1) {
   using TIn = typename In<BF>::T;
   using Cfg = typename In<BF>::Cfg;
@@ -659,9 +716,9 @@ __global__ __launch_bounds__(kGemmThreads, 4) void joiner_dh_kernel(JoinerArgs a
   __syncthreads();
   const TIn* W = reinterpret_cast<const TIn*>(a.W);
   DlSrcKC<Cfg> sa{make_rsrc(a.dl, (size_t)a.chunk_rows * a.ldl * sizeof(typename Cfg::T)), m0, cm0, mend, a.ldl};
-  WtSrcKC<Cfg, TIn> sb(a, j0);
+  WtSrcKC<Cfg, TIn, WM> sb(a, j0);
   KCLoader<Cfg, Cfg::BM, DlSrcKC<Cfg>> la(sa);
-  KCLoader<Cfg, Cfg::BN, WtSrcKC<Cfg, TIn>> lb(sb);
+  KCLoader<Cfg, Cfg::BN, WtSrcKC<Cfg, TIn, WM>> lb(sb);
   floatx4 acc[Cfg::FM][Cfg::FN];
   gemm_mainloop<Cfg>(la, lb, 0, V, smem, acc);
 
@@ -699,7 +756,7 @@ __global__ __launch_bounds__(kGemmThreads, 4) void joiner_dh_kernel(JoinerArgs a
 template <bool BF>
 __global__ __launch_bounds__(kGemmThreads, 4) void joiner_dw_kernel(JoinerArgs a, int cm0, int cm1, int first) {
   using TIn = typename In<BF>::T;
-  using Cfg = typename In<BF>::Cfg;
+  using Cfg = typename std::conditional<BF, CfgBw, CfgF>::type;
   __shared__ __align__(16) typename Cfg::T smem[Cfg::SMEM_BYTES / sizeof(typename Cfg::T)];
   const int M = a.frame_off[a.b.N] * a.S;
   const int mend = min(cm1, M);
@@ -725,8 +782,6 @@ __global__ __launch_bounds__(kGemmThreads, 4) void joiner_dw_kernel(JoinerArgs a
     }
     return;
   }
-  const TIn* enc = reinterpret_cast<const TIn*>(a.enc);
-  const TIn* dec = reinterpret_cast<const TIn*>(a.dec);
   HbufSrcMNC<Cfg> sa{make_rsrc(a.hbuf, (size_t)a.chunk_rows * J * sizeof(typename Cfg::T)), cm0, ke, j0, J};
   DlSrcMNC<Cfg> sb{make_rsrc(a.dl, (size_t)a.chunk_rows * a.ldl * sizeof(typename Cfg::T)), cm0, ke, v0, a.ldl};
   MNCLoader<Cfg, Cfg::BM, HbufSrcMNC<Cfg>> la(sa);
@@ -806,16 +861,19 @@ __global__ __launch_bounds__(256) void joiner_enc_kernel(JoinerArgs a) {
   for (int g = c; g < tpr; g += 256) {  // one pass unless J > 1024
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
     if (t < Tn) {
+      // batches of 8 slots with every load of a batch in flight together
+      // (slots past S load nothing and add zero); sums in ascending s
       const float4* d = reinterpret_cast<const float4*>(a.dpre + (size_t)(a.frame_off[n] + t) * S * J) + g;
-      float4 v[8];
-      int q = 0;
-      for (; q + 8 <= S; q += 8) {
+      for (int q = 0; q < S; q += 8) {
+        float4 v[8];
 #pragma unroll
-        for (int k = 0; k < 8; ++k) v[k] = d[(size_t)(q + k) * tpr];
+        for (int k = 0; k < 8; ++k) {
+          const float4 x = d[(size_t)min(q + k, S - 1) * tpr];  // always a valid row
+          v[k] = (q + k < S) ? x : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
 #pragma unroll
         for (int k = 0; k < 8; ++k) acc = f4add(acc, v[k]);
       }
-      for (; q < S; ++q) acc = f4add(acc, d[(size_t)q * tpr]);
     }
     reinterpret_cast<float4*>(a.enc_grad + (size_t)row * J)[g] = acc;
   }
@@ -904,6 +962,19 @@ int joiner_bwd_chunk_rows(int N, int T, int S, int J, int V, int bf16) {
   return (int)rows;
 }
 
+int joiner_fwd_chunk_rows(int N, int T, int S, int J, int bf16) {
+  const long long mmax = (long long)N * T * S;
+  if (!(bf16 ? kFwdHbuf<true> : kFwdHbuf<false>)) return (int)((mmax + 127) / 128 * 128);  // no h buffer
+  const long long budget = 128ll << 20;  // h of one chunk
+  long long rows = budget / ((long long)J * (bf16 ? 2 : 4));
+  rows = rows / 128 * 128;
+  if (rows < 128) rows = 128;
+  if (rows > mmax) rows = (mmax + 127) / 128 * 128;
+  return (int)rows;
+}
+
+bool joiner_fwd_uses_hbuf(int bf16) { return bf16 ? kFwdHbuf<true> : kFwdHbuf<false>; }
+
 int joiner_bwd_splits(int J, int V) {
   const int tiles = ((J + 127) / 128) * ((V + 127) / 128);
   int s = (512 + tiles - 1) / tiles;  // two workgroups per CU
@@ -927,13 +998,41 @@ hipError_t launch_joiner_prep(const JoinerArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
+// seg_mode on the host: how rows of length row_len split into segments of seg elements
+static int host_seg_mode(int row_len, int seg, int bf16) {
+  if (row_len % seg == 0) return kSegVector;
+  return (!bf16 || row_len % 2 == 0) ? kSegWords : kSegElems;
+}
+
+hipError_t launch_joiner_h(const JoinerArgs& a, int cm0, int cm1, hipStream_t s) {
+  const size_t groups = (size_t)(cm1 - cm0) * (a.J / (a.bf16 ? 8 : 4));
+  const dim3 grid((unsigned)((groups + 255) / 256));
+  RNNT_PROF(s, "joiner_h");
+  if (a.bf16) hipLaunchKernelGGL(joiner_h_kernel<true>, grid, dim3(256), 0, s, a, cm0, cm1);
+  else hipLaunchKernelGGL(joiner_h_kernel<false>, grid, dim3(256), 0, s, a, cm0, cm1);
+  return hipGetLastError();
+}
+
 hipError_t launch_joiner_fwd(const JoinerArgs& a, hipStream_t s) {
   const int mmax = a.b.N * a.b.T * a.S;
-  dim3 grid((mmax + 127) / 128, (a.V + 127) / 128);
-  {
+  for (int cm0 = 0; cm0 < mmax; cm0 += a.chunk_rows) {
+    const int cm1 = (cm0 + a.chunk_rows < mmax) ? cm0 + a.chunk_rows : mmax;
+    if (a.bf16 ? kFwdHbuf<true> : kFwdHbuf<false>) {
+      const hipError_t e = launch_joiner_h(a, cm0, cm1, s);
+      if (e != hipSuccess) return e;
+    }
+    const dim3 grid((cm1 - cm0 + 127) / 128, (a.V + 127) / 128);
     RNNT_PROF(s, "joiner_fwd");
-    if (a.bf16) hipLaunchKernelGGL(joiner_fwd_kernel<true>, grid, dim3(kGemmThreads), 0, s, a);
-  else hipLaunchKernelGGL(joiner_fwd_kernel<false>, grid, dim3(kGemmThreads), 0, s, a);
+    // W rows (length V) are read in segments of 16 / KV elements
+    const int wm = host_seg_mode(a.V, a.bf16 ? 2 : 4, a.bf16);
+    if (a.bf16) {
+      if (wm == kSegVector) hipLaunchKernelGGL((joiner_fwd_kernel<true, kSegVector>), grid, dim3(kGemmThreads), 0, s, a, cm0, cm1);
+      else if (wm == kSegWords) hipLaunchKernelGGL((joiner_fwd_kernel<true, kSegWords>), grid, dim3(kGemmThreads), 0, s, a, cm0, cm1);
+      else hipLaunchKernelGGL((joiner_fwd_kernel<true, kSegElems>), grid, dim3(kGemmThreads), 0, s, a, cm0, cm1);
+    } else {
+      if (wm == kSegVector) hipLaunchKernelGGL((joiner_fwd_kernel<false, kSegVector>), grid, dim3(kGemmThreads), 0, s, a, cm0, cm1);
+      else hipLaunchKernelGGL((joiner_fwd_kernel<false, kSegWords>), grid, dim3(kGemmThreads), 0, s, a, cm0, cm1);
+    }
   }
   const size_t total = (size_t)a.b.N * a.b.T * a.S;
   {
@@ -951,6 +1050,10 @@ hipError_t launch_joiner_bwd(const JoinerArgs& a, hipStream_t s) {
     e = launch_fill_f32(a.logits_grad, (size_t)mmax * V, 0.f, s);
     if (e != hipSuccess) return e;
   }
+  // segment modes of the W reads: the recomputed forward reads W rows in
+  // segments of 16 / KV elements, dh reads them k-contiguous in KV
+  const int wm_f = host_seg_mode(V, a.bf16 ? 2 : 4, a.bf16);
+  const int wm_h = host_seg_mode(V, a.bf16 ? 8 : 4, a.bf16);
   for (int cm0 = 0; cm0 < mmax; cm0 += a.chunk_rows) {
     const int cm1 = (cm0 + a.chunk_rows < mmax) ? cm0 + a.chunk_rows : mmax;
     const int mt = (cm1 - cm0 + 127) / 128;
@@ -961,12 +1064,18 @@ hipError_t launch_joiner_bwd(const JoinerArgs& a, hipStream_t s) {
         RNNT_PROF(s, "joiner_dl");
         hipLaunchKernelGGL(joiner_dl_kernel<true>, gdl, dim3(kDlThreads), 0, s, a, cm0, cm1);
       } else {
+        e = launch_joiner_h(a, cm0, cm1, s);
+        if (e != hipSuccess) return e;
         RNNT_PROF(s, "joiner_dlogits");
-        hipLaunchKernelGGL(joiner_dlogits_kernel<true>, g1, dim3(kGemmThreads), 0, s, a, cm0, cm1);
+        if (wm_f == kSegVector) hipLaunchKernelGGL((joiner_dlogits_kernel<true, kSegVector>), g1, dim3(kGemmThreads), 0, s, a, cm0, cm1);
+        else if (wm_f == kSegWords) hipLaunchKernelGGL((joiner_dlogits_kernel<true, kSegWords>), g1, dim3(kGemmThreads), 0, s, a, cm0, cm1);
+        else hipLaunchKernelGGL((joiner_dlogits_kernel<true, kSegElems>), g1, dim3(kGemmThreads), 0, s, a, cm0, cm1);
       }
       {
         RNNT_PROF(s, "joiner_dh");
-        hipLaunchKernelGGL(joiner_dh_kernel<true>, g2, dim3(kGemmThreads), 0, s, a, cm0, cm1);
+        if (wm_h == kSegVector) hipLaunchKernelGGL((joiner_dh_kernel<true, kSegVector>), g2, dim3(kGemmThreads), 0, s, a, cm0, cm1);
+        else if (wm_h == kSegWords) hipLaunchKernelGGL((joiner_dh_kernel<true, kSegWords>), g2, dim3(kGemmThreads), 0, s, a, cm0, cm1);
+        else hipLaunchKernelGGL((joiner_dh_kernel<true, kSegElems>), g2, dim3(kGemmThreads), 0, s, a, cm0, cm1);
       }
       {
         RNNT_PROF(s, "joiner_dw");
@@ -977,12 +1086,16 @@ hipError_t launch_joiner_bwd(const JoinerArgs& a, hipStream_t s) {
         RNNT_PROF(s, "joiner_dl");
         hipLaunchKernelGGL(joiner_dl_kernel<false>, gdl, dim3(kDlThreads), 0, s, a, cm0, cm1);
       } else {
+        e = launch_joiner_h(a, cm0, cm1, s);
+        if (e != hipSuccess) return e;
         RNNT_PROF(s, "joiner_dlogits");
-        hipLaunchKernelGGL(joiner_dlogits_kernel<false>, g1, dim3(kGemmThreads), 0, s, a, cm0, cm1);
+        if (wm_f == kSegVector) hipLaunchKernelGGL((joiner_dlogits_kernel<false, kSegVector>), g1, dim3(kGemmThreads), 0, s, a, cm0, cm1);
+        else hipLaunchKernelGGL((joiner_dlogits_kernel<false, kSegWords>), g1, dim3(kGemmThreads), 0, s, a, cm0, cm1);
       }
       {
         RNNT_PROF(s, "joiner_dh");
-        hipLaunchKernelGGL(joiner_dh_kernel<false>, g2, dim3(kGemmThreads), 0, s, a, cm0, cm1);
+        if (wm_h == kSegVector) hipLaunchKernelGGL((joiner_dh_kernel<false, kSegVector>), g2, dim3(kGemmThreads), 0, s, a, cm0, cm1);
+        else hipLaunchKernelGGL((joiner_dh_kernel<false, kSegWords>), g2, dim3(kGemmThreads), 0, s, a, cm0, cm1);
       }
       {
         RNNT_PROF(s, "joiner_dw");

@@ -115,6 +115,7 @@ struct JoinerArgs {
   int chunk_rows;
   float* dpre;         // ws [N*T*S, J]
   void* hbuf;          // ws chunk [chunk_rows, J] (f32 or bf16): h = tanh(enc + dec) of the chunk's rows
+                       // (forward and recomputed backward: written by the h kernel; backward: by dh)
   float* dw_part;      // ws [splits, J, V]
   int splits;
   float* db_part;      // ws [n_db_rows, V]
@@ -131,6 +132,8 @@ hipError_t launch_full_ranges(int* ranges, int N, int T, int S, hipStream_t s);
 hipError_t launch_joiner_fwd(const JoinerArgs& a, hipStream_t s);
 hipError_t launch_joiner_bwd(const JoinerArgs& a, hipStream_t s);
 int joiner_bwd_chunk_rows(int N, int T, int S, int J, int V, int bf16);
+int joiner_fwd_chunk_rows(int N, int T, int S, int J, int bf16);
+bool joiner_fwd_uses_hbuf(int bf16);
 int joiner_bwd_splits(int J, int V);
 int joiner_db_rows(int N, int T, int S);
 int joiner_nparts(int V);
