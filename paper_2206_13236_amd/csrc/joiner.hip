@@ -305,20 +305,22 @@ DEV float bias_at(const void* bias, int bf16, int v) {
 // Prep: per-utterance frame offsets and per-row info.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void joiner_prep_kernel(JoinerArgs a) {
-  __shared__ int s_off;
+  __shared__ int s_part[4];
   const int n = blockIdx.x;
   const int T = a.b.T, U1 = a.b.U + 1, S = a.S, J = a.J;
-  if (threadIdx.x == 0) {
-    int off = 0;
-    for (int q = 0; q < n; ++q) {
-      int Tq, Uq;
-      utt_dims(a.b, q, Tq, Uq);
-      off += Tq;
-    }
-    s_off = off;
+  // frame offset of utterance n: sum of T_q over q < n, the lengths loaded
+  // in parallel and summed by a block reduction
+  int part = 0;
+  for (int q = threadIdx.x; q < n; q += blockDim.x) {
+    int Tq, Uq;
+    utt_dims(a.b, q, Tq, Uq);
+    part += Tq;
   }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) part += __shfl_xor(part, o, 64);
+  if ((threadIdx.x & 63) == 0) s_part[threadIdx.x >> 6] = part;
   __syncthreads();
-  const int off = s_off;
+  const int off = s_part[0] + s_part[1] + s_part[2] + s_part[3];
   int Tn, Un;
   utt_dims(a.b, n, Tn, Un);
   if (threadIdx.x == 0) {

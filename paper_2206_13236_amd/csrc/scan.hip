@@ -474,10 +474,9 @@ hipError_t launch_scan_k(const BandArgs& a, hipStream_t s) {
 
 int band_scan_chunk(int T) {
   // the chain is about C frames in each of the chunk and replay kernels plus
-  // T / C matrix-vector steps in the sweep
-  int C = 4;
-  while (C < kScanMaxC && 2 * C * C < T) C *= 2;
-  return C;
+  // T / C matrix-vector steps in the sweep; thresholds measured on the four
+  // workload shapes (T up to 250, 300, 500, 1000)
+  return T <= 256 ? 8 : T <= 640 ? 16 : 32;
 }
 
 hipError_t launch_band_scan(const BandArgs& a, hipStream_t s) {

@@ -46,11 +46,18 @@ DEV int split_chunk(int K, int splits, int bk) { return ((K + splits - 1) / spli
 // ---------------------------------------------------------------------------
 // Row maxima of am (rows t < T_n) and lm (rows u <= U_n): one wave per row.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void rowmax_kernel(const float* __restrict__ x, int N, int R, int V,
-                                                     BatchDev b, int is_lm, float* __restrict__ out) {
-  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+// One wave per row: rows [0, N*T) of am, then rows [0, N*(U+1)) of lm.
+__global__ __launch_bounds__(256) void rowmax_kernel(const float* __restrict__ am, const float* __restrict__ lm,
+                                                     int N, int T, int U1, int V, BatchDev b,
+                                                     float* __restrict__ m_a, float* __restrict__ m_l) {
+  const int gr = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
-  if (row >= N * R) return;
+  if (gr >= N * (T + U1)) return;
+  const int is_lm = gr >= N * T;
+  const int row = is_lm ? gr - N * T : gr;
+  const int R = is_lm ? U1 : T;
+  const float* x = is_lm ? lm : am;
+  float* out = is_lm ? m_l : m_a;
   const int n = row / R, i = row % R;
   int Tn, Un;
   utt_dims(b, n, Tn, Un);
@@ -563,11 +570,8 @@ hipError_t launch_rowmax(const SimpleArgs& a, hipStream_t s) {
   const int N = a.b.N, T = a.b.T, U1 = a.b.U + 1;
   {
     RNNT_PROF(s, "rowmax");
-    hipLaunchKernelGGL(rowmax_kernel, dim3((N * T + 3) / 4), dim3(256), 0, s, a.am, N, T, a.V, a.b, 0, a.m_a);
-  }
-  {
-    RNNT_PROF(s, "rowmax");
-    hipLaunchKernelGGL(rowmax_kernel, dim3((N * U1 + 3) / 4), dim3(256), 0, s, a.lm, N, U1, a.V, a.b, 1, a.m_l);
+    hipLaunchKernelGGL(rowmax_kernel, dim3((N * (T + U1) + 3) / 4), dim3(256), 0, s, a.am, a.lm, N, T, U1, a.V, a.b,
+                       a.m_a, a.m_l);
   }
   return hipGetLastError();
 }
