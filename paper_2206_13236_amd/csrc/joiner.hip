@@ -881,22 +881,22 @@ __global__ __launch_bounds__(256) void joiner_enc_kernel(JoinerArgs a) {
   }
 }
 
-// grid (ceil((U+1)/R), N): the block's rows are dec rows u of utterance n.
+// grid (U+1, N): block (u, n) computes dec row u of utterance n, threads over
+// float4 column groups of J (one dec row per block measured faster than two).
 __global__ __launch_bounds__(256) void joiner_dec_kernel(JoinerArgs a) {
   extern __shared__ int sp[];  // p_t of the utterance
   const int T = a.b.T, U1 = a.b.U + 1, S = a.S, J = a.J, tpr = J / 4;
-  const int R = encdec_rows_per_block(J);
   const int n = blockIdx.y;
   int Tn, Un;
   utt_dims(a.b, n, Tn, Un);
   for (int t = threadIdx.x; t < Tn; t += blockDim.x) sp[t] = a.ranges[((size_t)n * T + t) * S];
   __syncthreads();
-  const int rr = threadIdx.x / tpr, c = threadIdx.x - rr * tpr;
-  const int u = blockIdx.x * R + rr;
-  if (rr >= R || u >= U1) return;
+  const int c = threadIdx.x;
+  const int u = blockIdx.x;
+  if (u >= U1) return;
   float4* out = reinterpret_cast<float4*>(a.dec_grad + ((size_t)n * U1 + u) * J);
   if (u > Un) {
-    for (int g = c; g < tpr; g += 256) out[g] = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int g = c; g < tpr; g += blockDim.x) out[g] = make_float4(0.f, 0.f, 0.f, 0.f);
     return;
   }
   // p_t is non-decreasing (Eq. (9)), so the frames whose band holds u form
@@ -917,7 +917,7 @@ __global__ __launch_bounds__(256) void joiner_dec_kernel(JoinerArgs a) {
   const int t1 = lo;
   const float4* d = reinterpret_cast<const float4*>(a.dpre);
   const size_t off = (size_t)a.frame_off[n];
-  for (int g = c; g < tpr; g += 256) {
+  for (int g = c; g < tpr; g += blockDim.x) {
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
     int t = t0;
     for (; t + 8 <= t1; t += 8) {  // loads of 8 frames in flight, added in ascending t
@@ -1121,8 +1121,8 @@ hipError_t launch_joiner_bwd(const JoinerArgs& a, hipStream_t s) {
   }
   {
     RNNT_PROF(s, "joiner_dec");
-    hipLaunchKernelGGL(joiner_dec_kernel, dim3((a.b.U + 1 + R - 1) / R, a.b.N), dim3(256),
-                       (size_t)a.b.T * sizeof(int), s, a);
+    const int threads = (J / 4 >= 256) ? 256 : (J / 4 + 63) / 64 * 64;
+    hipLaunchKernelGGL(joiner_dec_kernel, dim3(a.b.U + 1, a.b.N), dim3(threads), (size_t)a.b.T * sizeof(int), s, a);
   }
   return hipGetLastError();
 }
