@@ -807,10 +807,16 @@ __global__ __launch_bounds__(kGemmThreads, 4) void joiner_dw_kernel(JoinerArgs a
     }
 }
 
-// dW = sum of the split partials, in split order.
-__global__ __launch_bounds__(256) void joiner_wsum_kernel(JoinerArgs a) {
+// The tail of the backward: dW and db summed from their partials, d enc and
+// d dec reduced from dpre. Four independent, latency-bound reductions, run as
+// one launch whose block ranges take one part each (d dec, d enc, dW, db), so
+// that their memory latencies overlap.
+constexpr int kTailThreads = 256;
+
+// dW = sum of the split partials, in split order (one element per thread).
+DEV void tail_wsum(const JoinerArgs& a, int b) {
   const size_t JV = (size_t)a.J * a.V;
-  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const size_t i = (size_t)b * kTailThreads + threadIdx.x;
   if (i >= JV) return;
   float s = 0.f;
 #pragma unroll 8
@@ -819,52 +825,47 @@ __global__ __launch_bounds__(256) void joiner_wsum_kernel(JoinerArgs a) {
 }
 
 // db = sum of the column partials written by the d(logits) kernel (one per
-// 64 rows streamed, one per wave row of a GEMM tile recomputed): 16
+// 64 rows streamed, one per wave row of a GEMM tile recomputed): 4
 // interleaved parts per column, then the parts in order.
-__global__ __launch_bounds__(1024) void joiner_dbsum_kernel(JoinerArgs a) {
-  __shared__ float red[16][64];
+DEV void tail_dbsum(const JoinerArgs& a, int b, float (*red)[64]) {
   const int c = threadIdx.x & 63, part = threadIdx.x >> 6;
-  const int v = blockIdx.x * 64 + c;
+  const int v = b * 64 + c;
   const int M = a.frame_off[a.b.N] * a.S;
   const int rows = a.logits_in ? (M + kDlRows - 1) / kDlRows : CfgF::WGM * ((M + CfgF::BM - 1) / CfgF::BM);
   float s = 0.f;
   if (v < a.V) {
 #pragma unroll 4
-    for (int r = part; r < rows; r += 16) s += a.db_part[(size_t)r * a.V + v];
+    for (int r = part; r < rows; r += 4) s += a.db_part[(size_t)r * a.V + v];
   }
   red[part][c] = s;
   __syncthreads();
-  if (part == 0 && v < a.V) {
-    float t = 0.f;
-    for (int q = 0; q < 16; ++q) t += red[q][c];
-    a.bias_grad[v] = t;
-  }
+  if (part == 0 && v < a.V) a.bias_grad[v] = ((red[0][c] + red[1][c]) + red[2][c]) + red[3][c];
 }
 
 // d enc[n,t] = sum_s dpre(row(t,s)); d dec[n,u] = sum over t of dpre(row(t, u - p_t))
 // for 0 <= u - p_t < S. Threads over float4 column groups of J, several
-// output rows per 256-thread block; every sum runs in ascending s or t.
+// output rows per block; every sum runs in ascending s or t.
 DEV int encdec_rows_per_block(int J) {
   const int tpr = J / 4;
-  return tpr >= 256 ? 1 : 256 / tpr;
+  return tpr >= kTailThreads ? 1 : kTailThreads / tpr;
 }
 
 DEV float4 f4add(float4 a, float4 b) { return make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w); }
 
-__global__ __launch_bounds__(256) void joiner_enc_kernel(JoinerArgs a) {
+DEV void tail_enc(const JoinerArgs& a, int b) {
   const int T = a.b.T, S = a.S, J = a.J, tpr = J / 4;
   const int R = encdec_rows_per_block(J);
   const int rr = threadIdx.x / tpr, c = threadIdx.x - rr * tpr;
-  const int row = blockIdx.x * R + rr;  // n * T + t
+  const int row = b * R + rr;  // n * T + t
   if (rr >= R || row >= a.b.N * T) return;
   const int n = row / T, t = row - n * T;
   int Tn, Un;
   utt_dims(a.b, n, Tn, Un);
-  for (int g = c; g < tpr; g += 256) {  // one pass unless J > 1024
+  for (int g = c; g < tpr; g += kTailThreads) {  // one pass unless J > 1024
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
     if (t < Tn) {
       // batches of 8 slots with every load of a batch in flight together
-      // (slots past S load nothing and add zero); sums in ascending s
+      // (slots past S add zero); sums in ascending s
       const float4* d = reinterpret_cast<const float4*>(a.dpre + (size_t)(a.frame_off[n] + t) * S * J) + g;
       for (int q = 0; q < S; q += 8) {
         float4 v[8];
@@ -881,22 +882,22 @@ __global__ __launch_bounds__(256) void joiner_enc_kernel(JoinerArgs a) {
   }
 }
 
-// grid (U+1, N): block (u, n) computes dec row u of utterance n, threads over
-// float4 column groups of J (one dec row per block measured faster than two).
-__global__ __launch_bounds__(256) void joiner_dec_kernel(JoinerArgs a) {
-  extern __shared__ int sp[];  // p_t of the utterance
+// Block b: dec rows u = (b % ceil((U+1)/R)) * R + rr of utterance n = b / ceil((U+1)/R).
+DEV void tail_dec(const JoinerArgs& a, int b, int* sp) {
   const int T = a.b.T, U1 = a.b.U + 1, S = a.S, J = a.J, tpr = J / 4;
-  const int n = blockIdx.y;
+  const int R = encdec_rows_per_block(J);
+  const int ub = (U1 + R - 1) / R;
+  const int n = b / ub;
   int Tn, Un;
   utt_dims(a.b, n, Tn, Un);
-  for (int t = threadIdx.x; t < Tn; t += blockDim.x) sp[t] = a.ranges[((size_t)n * T + t) * S];
+  for (int t = threadIdx.x; t < Tn; t += kTailThreads) sp[t] = a.ranges[((size_t)n * T + t) * S];
   __syncthreads();
-  const int c = threadIdx.x;
-  const int u = blockIdx.x;
-  if (u >= U1) return;
+  const int rr = threadIdx.x / tpr, c = threadIdx.x - rr * tpr;
+  const int u = (b - n * ub) * R + rr;
+  if (rr >= R || u >= U1) return;
   float4* out = reinterpret_cast<float4*>(a.dec_grad + ((size_t)n * U1 + u) * J);
   if (u > Un) {
-    for (int g = c; g < tpr; g += blockDim.x) out[g] = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int g = c; g < tpr; g += kTailThreads) out[g] = make_float4(0.f, 0.f, 0.f, 0.f);
     return;
   }
   // p_t is non-decreasing (Eq. (9)), so the frames whose band holds u form
@@ -917,7 +918,7 @@ __global__ __launch_bounds__(256) void joiner_dec_kernel(JoinerArgs a) {
   const int t1 = lo;
   const float4* d = reinterpret_cast<const float4*>(a.dpre);
   const size_t off = (size_t)a.frame_off[n];
-  for (int g = c; g < tpr; g += blockDim.x) {
+  for (int g = c; g < tpr; g += kTailThreads) {
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
     int t = t0;
     for (; t + 8 <= t1; t += 8) {  // loads of 8 frames in flight, added in ascending t
@@ -930,6 +931,23 @@ __global__ __launch_bounds__(256) void joiner_dec_kernel(JoinerArgs a) {
     for (; t < t1; ++t) acc = f4add(acc, d[((off + t) * S + (u - sp[t])) * tpr + g]);
     out[g] = acc;
   }
+}
+
+struct TailRanges {
+  int dec, enc, wsum, dbsum;  // block counts, in launch order
+};
+
+__global__ __launch_bounds__(kTailThreads) void joiner_tail_kernel(JoinerArgs a, TailRanges r) {
+  extern __shared__ int sp[];  // p_t of one utterance (d dec blocks)
+  __shared__ float red[4][64];  // db blocks
+  int b = blockIdx.x;
+  if (b < r.dec) { tail_dec(a, b, sp); return; }
+  b -= r.dec;
+  if (b < r.enc) { tail_enc(a, b); return; }
+  b -= r.enc;
+  if (b < r.wsum) { tail_wsum(a, b); return; }
+  b -= r.wsum;
+  tail_dbsum(a, b, red);
 }
 
 // ranges[n,t,s] = s: every (t, u) of the lattice as a "band" of width U+1.
@@ -1106,23 +1124,16 @@ hipError_t launch_joiner_bwd(const JoinerArgs& a, hipStream_t s) {
     }
   }
   const size_t JV = (size_t)J * V;
-  if (a.W_grad) {
-    RNNT_PROF(s, "joiner_wsum");
-    hipLaunchKernelGGL(joiner_wsum_kernel, dim3((unsigned)((JV + 255) / 256)), dim3(256), 0, s, a);
-  }
-  if (a.bias_grad) {
-    RNNT_PROF(s, "joiner_dbsum");
-    hipLaunchKernelGGL(joiner_dbsum_kernel, dim3((unsigned)((V + 63) / 64)), dim3(1024), 0, s, a);
-  }
-  const int R = (J / 4 >= 256) ? 1 : 256 / (J / 4);
+  const int R = (J / 4 >= kTailThreads) ? 1 : kTailThreads / (J / 4);
+  TailRanges tr;
+  tr.dec = ((a.b.U + 1 + R - 1) / R) * a.b.N;
+  tr.enc = (a.b.N * a.b.T + R - 1) / R;
+  tr.wsum = a.W_grad ? (int)((JV + kTailThreads - 1) / kTailThreads) : 0;
+  tr.dbsum = a.bias_grad ? (V + 63) / 64 : 0;
   {
-    RNNT_PROF(s, "joiner_enc");
-    hipLaunchKernelGGL(joiner_enc_kernel, dim3((a.b.N * a.b.T + R - 1) / R), dim3(256), 0, s, a);
-  }
-  {
-    RNNT_PROF(s, "joiner_dec");
-    const int threads = (J / 4 >= 256) ? 256 : (J / 4 + 63) / 64 * 64;
-    hipLaunchKernelGGL(joiner_dec_kernel, dim3(a.b.U + 1, a.b.N), dim3(threads), (size_t)a.b.T * sizeof(int), s, a);
+    RNNT_PROF(s, "joiner_tail");
+    hipLaunchKernelGGL(joiner_tail_kernel, dim3(tr.dec + tr.enc + tr.wsum + tr.dbsum), dim3(kTailThreads),
+                       (size_t)a.b.T * sizeof(int), s, a, tr);
   }
   return hipGetLastError();
 }
