@@ -218,6 +218,7 @@ struct JoinerBwdWs {
   int* frame_off;
   int4* rowinfo;
   void* dl;
+  void* dlT;
   float* dpre;
   void* hbuf;
   float* dw_part;
@@ -237,6 +238,7 @@ JoinerBwdWs joiner_bwd_layout(void* base, int N, int T, int S, int J, int V, int
   w.rowinfo = c.take<int4>(M);
   const size_t dl_elems = (size_t)w.chunk_rows * joiner_ldl(V);
   w.dl = bf16 ? (void*)c.take<uint16_t>(dl_elems) : (void*)c.take<float>(dl_elems);
+  w.dlT = bf16 ? (void*)c.take<uint16_t>(dl_elems) : nullptr;
   w.dpre = c.take<float>(M * J);
   const size_t h_elems = (size_t)w.chunk_rows * J;
   w.hbuf = bf16 ? (void*)c.take<uint16_t>(h_elems) : (void*)c.take<float>(h_elems);
@@ -314,6 +316,7 @@ void set_joiner_bwd(JoinerArgs& a, const JoinerBwdWs& w, const float* lse, const
   a.gyo = gy;
   a.scale = scale;
   a.dl = w.dl;
+  a.dlT = w.dlT;
   a.ldl = joiner_ldl(a.V);
   a.chunk_rows = w.chunk_rows;
   a.dpre = w.dpre;

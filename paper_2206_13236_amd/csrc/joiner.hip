@@ -262,6 +262,25 @@ struct WtSrcKC {
   DEV void kc_finish(const Raw& r, float (&v)[Cfg::KV]) const { raw_to_float(r, v); }
 };
 
+// bf16 dW operands from transposed chunk buffers (k = m contiguous):
+// A(j, m) = hT[j][m - cm0], B(v, m) = dlT[v][m - cm0]. Rows past mend hold
+// zeros up to the 128-row tile end, so a 16-byte segment that crosses mend
+// reads zeros there; split boundaries inside a chunk are K-step aligned.
+template <class Cfg>
+struct TrSrcKC {
+  static constexpr bool kDirect = true;
+  using T = typename Cfg::T;
+  using Raw = RawVec<T, Cfg::KV>;
+  Rsrc p;
+  int cm0, ke, r0, nrows, ld;
+  DEV void kc_load(int row, int k, Raw& r) const {
+    const int q = r0 + row;
+    const int n = (q < nrows && k < ke) ? Cfg::KV : 0;
+    raw_load(p, (uint32_t)(q * ld + (k - cm0)) * sizeof(T), n, kSegVector, r);
+  }
+  DEV void kc_finish(const Raw& r, float (&v)[Cfg::KV]) const { raw_to_float(r, v); }
+};
+
 // A(j, m) = h(m, j) from the chunk's hbuf [rows, J] (j-contiguous).
 template <class Cfg>
 struct HbufSrcMNC {
@@ -697,7 +716,8 @@ __global__ __launch_bounds__(kDlThreads) void joiner_dl_kernel(JoinerArgs a, int
 
 // ---------------------------------------------------------------------------
 // Backward 2: dh = dl W^T, dpre = dh (1 - h^2); also leaves h of the chunk's
-// rows in hbuf (zero for absent slots) as the dW contraction's operand.
+// rows in hbuf (zero for absent slots) as the dW contraction's operand:
+// [rows, J] for fp32, transposed [J, chunk_rows] for bf16.
 // ---------------------------------------------------------------------------
 template <bool BF, int WM>
 __global__ __launch_bounds__(kGemmThreads, 4) void joiner_dh_kernel(JoinerArgs a, int cm0, int cm1) {
@@ -730,26 +750,69 @@ __global__ __launch_bounds__(kGemmThreads, 4) void joiner_dh_kernel(JoinerArgs a
 #pragma unroll
   for (int i = 0; i < Cfg::FM; ++i)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int row = tile_row<Cfg>(i, r);
-      const int m = m0 + row;
-      if (m >= mend) continue;
-      const int4 info = ri[row];
+    for (int j = 0; j < Cfg::FN; ++j) {
+      const int jj = j0 + tile_col<Cfg>(j);
+      if (jj >= J) continue;
+      float hv[4];
 #pragma unroll
-      for (int j = 0; j < Cfg::FN; ++j) {
-        const int jj = j0 + tile_col<Cfg>(j);
-        if (jj >= J) continue;
+      for (int r = 0; r < 4; ++r) {
+        const int row = tile_row<Cfg>(i, r);
+        const int m = m0 + row;
+        const int4 info = ri[row];  // absent (w < 0) for rows past mend
         float dp = 0.f, h = 0.f;
         if (info.w >= 0) {
           h = fast_tanh(ld_in(enc, (size_t)info.x + jj) + ld_in(dec, (size_t)info.y + jj));
           dp = acc[i][j][r] * (1.f - h * h);
         }
-        a.dpre[(size_t)m * J + jj] = dp;
-        // h of the chunk's rows, in the GEMM operand type, for the dW contraction
-        if constexpr (BF) hbuf[(size_t)(m - cm0) * J + jj] = f2bf(h);
-        else hbuf[(size_t)(m - cm0) * J + jj] = h;
+        hv[r] = h;
+        if (m < mend) a.dpre[(size_t)m * J + jj] = dp;
+        if constexpr (!BF) {
+          if (m < mend) hbuf[(size_t)(m - cm0) * J + jj] = h;  // h [rows, J] for the fp32 dW
+        }
+      }
+      if constexpr (BF) {
+        // h^T [J, chunk_rows] for the bf16 dW: the lane's 4 consecutive rows
+        // as one 8-byte store (rows past mend hold 0)
+        const int mr0 = m0 + tile_row<Cfg>(i, 0) - cm0;
+        *reinterpret_cast<uint2*>(hbuf + (size_t)jj * a.chunk_rows + mr0) =
+            make_uint2((uint32_t)f2bf(hv[0]) | ((uint32_t)f2bf(hv[1]) << 16),
+                       (uint32_t)f2bf(hv[2]) | ((uint32_t)f2bf(hv[3]) << 16));
       }
     }
+}
+
+// ---------------------------------------------------------------------------
+// bf16 d(logits) transposed for the dW contraction: dlT[v][m - cm0] for the
+// chunk's rows, zero for rows past mend up to the 128-row tile end. 64 x 64
+// tiles through LDS; every global access is 16 bytes per thread.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void joiner_dlt_kernel(JoinerArgs a, int cm0, int cm1) {
+  __shared__ uint16_t tile[64][64 + 8];
+  const int M = a.frame_off[a.b.N] * a.S;
+  const int mend = min(cm1, M);
+  const int r0 = blockIdx.x * 64, c0 = blockIdx.y * 64;  // rows (m - cm0), columns v
+  const uint16_t* dl = reinterpret_cast<const uint16_t*>(a.dl);
+  uint16_t* dlT = reinterpret_cast<uint16_t*>(a.dlT);
+  const int ty = threadIdx.x >> 3, tx = threadIdx.x & 7;
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int r = ty + 32 * h;
+    const int c = c0 + tx * 8;
+    uint4 v = make_uint4(0, 0, 0, 0);
+    if (cm0 + r0 + r < mend && c < a.ldl) v = *reinterpret_cast<const uint4*>(dl + (size_t)(r0 + r) * a.ldl + c);
+    *reinterpret_cast<uint4*>(&tile[r][tx * 8]) = v;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int c = ty + 32 * h;  // column within the tile: dlT row
+    if (c0 + c >= a.ldl) continue;
+    uint32_t w[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      w[q] = (uint32_t)tile[tx * 8 + 2 * q][c] | ((uint32_t)tile[tx * 8 + 2 * q + 1][c] << 16);
+    *reinterpret_cast<uint4*>(dlT + (size_t)(c0 + c) * a.chunk_rows + r0 + tx * 8) = make_uint4(w[0], w[1], w[2], w[3]);
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -784,12 +847,21 @@ __global__ __launch_bounds__(kGemmThreads, 4) void joiner_dw_kernel(JoinerArgs a
     }
     return;
   }
-  HbufSrcMNC<Cfg> sa{make_rsrc(a.hbuf, (size_t)a.chunk_rows * J * sizeof(typename Cfg::T)), cm0, ke, j0, J};
-  DlSrcMNC<Cfg> sb{make_rsrc(a.dl, (size_t)a.chunk_rows * a.ldl * sizeof(typename Cfg::T)), cm0, ke, v0, a.ldl};
-  MNCLoader<Cfg, Cfg::BM, HbufSrcMNC<Cfg>> la(sa);
-  MNCLoader<Cfg, Cfg::BN, DlSrcMNC<Cfg>> lb(sb);
   floatx4 acc[Cfg::FM][Cfg::FN];
-  gemm_mainloop<Cfg>(la, lb, kb, ke, smem, acc);
+  if constexpr (BF) {
+    const size_t tb = (size_t)a.chunk_rows * sizeof(typename Cfg::T);
+    TrSrcKC<Cfg> sa{make_rsrc(a.hbuf, tb * J), cm0, ke, j0, J, a.chunk_rows};
+    TrSrcKC<Cfg> sb{make_rsrc(a.dlT, tb * a.ldl), cm0, ke, v0, V, a.chunk_rows};
+    KCLoader<Cfg, Cfg::BM, TrSrcKC<Cfg>> la(sa);
+    KCLoader<Cfg, Cfg::BN, TrSrcKC<Cfg>> lb(sb);
+    gemm_mainloop<Cfg>(la, lb, kb, ke, smem, acc);
+  } else {
+    HbufSrcMNC<Cfg> sa{make_rsrc(a.hbuf, (size_t)a.chunk_rows * J * sizeof(typename Cfg::T)), cm0, ke, j0, J};
+    DlSrcMNC<Cfg> sb{make_rsrc(a.dl, (size_t)a.chunk_rows * a.ldl * sizeof(typename Cfg::T)), cm0, ke, v0, a.ldl};
+    MNCLoader<Cfg, Cfg::BM, HbufSrcMNC<Cfg>> la(sa);
+    MNCLoader<Cfg, Cfg::BN, DlSrcMNC<Cfg>> lb(sb);
+    gemm_mainloop<Cfg>(la, lb, kb, ke, smem, acc);
+  }
 #pragma unroll
   for (int i = 0; i < Cfg::FM; ++i)
 #pragma unroll
@@ -1096,6 +1168,11 @@ hipError_t launch_joiner_bwd(const JoinerArgs& a, hipStream_t s) {
         if (wm_h == kSegVector) hipLaunchKernelGGL((joiner_dh_kernel<true, kSegVector>), g2, dim3(kGemmThreads), 0, s, a, cm0, cm1);
         else if (wm_h == kSegWords) hipLaunchKernelGGL((joiner_dh_kernel<true, kSegWords>), g2, dim3(kGemmThreads), 0, s, a, cm0, cm1);
         else hipLaunchKernelGGL((joiner_dh_kernel<true, kSegElems>), g2, dim3(kGemmThreads), 0, s, a, cm0, cm1);
+      }
+      {
+        RNNT_PROF(s, "joiner_dlt");
+        const dim3 gt((cm1 - cm0 + 63) / 64, (a.ldl + 63) / 64);
+        hipLaunchKernelGGL(joiner_dlt_kernel, gt, dim3(256), 0, s, a, cm0, cm1);
       }
       {
         RNNT_PROF(s, "joiner_dw");

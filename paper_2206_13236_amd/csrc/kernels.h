@@ -112,6 +112,7 @@ struct JoinerArgs {
   const float* scale;  // [N] or null
   void* dl;            // ws chunk [chunk_rows, ldl] (f32 or bf16)
   int ldl;
+  void* dlT;           // ws chunk [ldl, chunk_rows] (bf16 only): d(logits) transposed for dW
   int chunk_rows;
   float* dpre;         // ws [N*T*S, J]
   void* hbuf;          // ws chunk [chunk_rows, J] (f32 or bf16): h = tanh(enc + dec) of the chunk's rows
