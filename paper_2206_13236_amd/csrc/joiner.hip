@@ -744,41 +744,69 @@ __global__ __launch_bounds__(kGemmThreads, 4) void joiner_dh_kernel(JoinerArgs a
   floatx4 acc[Cfg::FM][Cfg::FN];
   gemm_mainloop<Cfg>(la, lb, 0, V, smem, acc);
 
-  const TIn* enc = reinterpret_cast<const TIn*>(a.enc);
-  const TIn* dec = reinterpret_cast<const TIn*>(a.dec);
+  // Epilogue through LDS (the operand stages are free after the main loop's
+  // last barrier): the tile goes to LDS in the MFMA layout and comes back row
+  // by row, so that enc, dec, dpre and h are read and written with 16-byte
+  // accesses per thread along J.
   typename Cfg::T* hbuf = reinterpret_cast<typename Cfg::T*>(a.hbuf);
+  constexpr int LDC = Cfg::BN + 4;
+  static_assert(Cfg::BM * LDC * 4 <= Cfg::SMEM_BYTES, "epilogue tile fits the operand stages");
+  float* C = reinterpret_cast<float*>(smem);
 #pragma unroll
   for (int i = 0; i < Cfg::FM; ++i)
 #pragma unroll
-    for (int j = 0; j < Cfg::FN; ++j) {
-      const int jj = j0 + tile_col<Cfg>(j);
-      if (jj >= J) continue;
-      float hv[4];
+    for (int j = 0; j < Cfg::FN; ++j)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int row = tile_row<Cfg>(i, r);
-        const int m = m0 + row;
-        const int4 info = ri[row];  // absent (w < 0) for rows past mend
-        float dp = 0.f, h = 0.f;
-        if (info.w >= 0) {
-          h = fast_tanh(ld_in(enc, (size_t)info.x + jj) + ld_in(dec, (size_t)info.y + jj));
-          dp = acc[i][j][r] * (1.f - h * h);
-        }
-        hv[r] = h;
-        if (m < mend) a.dpre[(size_t)m * J + jj] = dp;
-        if constexpr (!BF) {
-          if (m < mend) hbuf[(size_t)(m - cm0) * J + jj] = h;  // h [rows, J] for the fp32 dW
-        }
-      }
-      if constexpr (BF) {
-        // h^T [J, chunk_rows] for the bf16 dW: the lane's 4 consecutive rows
-        // as one 8-byte store (rows past mend hold 0)
+      for (int r = 0; r < 4; ++r) C[tile_row<Cfg>(i, r) * LDC + tile_col<Cfg>(j)] = acc[i][j][r];
+  __syncthreads();
+  const EncDec<TIn> ed(a);
+  for (int it = threadIdx.x; it < Cfg::BM * Cfg::BN / 4; it += Cfg::NT) {
+    const int row = it / (Cfg::BN / 4), cg = it - row * (Cfg::BN / 4);
+    const int m = m0 + row, jj = j0 + cg * 4;
+    if (jj >= J) continue;  // J is a multiple of 8: the group is all in or all out
+    float* cr = C + row * LDC + cg * 4;
+    const int4 info = ri[row];  // absent (w < 0) for rows past mend
+    const bool on = info.w >= 0;
+    RawVec<TIn, 4> e, d;
+    raw_load(ed.enc, (uint32_t)(info.x + jj) * sizeof(TIn), on ? 4 : 0, kSegVector, e);
+    raw_load(ed.dec, (uint32_t)(info.y + jj) * sizeof(TIn), on ? 4 : 0, kSegVector, d);
+    float fe[4], fd[4], h[4], dp[4];
+    raw_to_float(e, fe);
+    raw_to_float(d, fd);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      h[q] = on ? fast_tanh(fe[q] + fd[q]) : 0.f;
+      dp[q] = on ? cr[q] * (1.f - h[q] * h[q]) : 0.f;
+    }
+    if (m < mend) {
+      *reinterpret_cast<float4*>(a.dpre + (size_t)m * J + jj) = make_float4(dp[0], dp[1], dp[2], dp[3]);
+      if constexpr (!BF)  // h [rows, J] for the fp32 dW
+        *reinterpret_cast<float4*>(hbuf + (size_t)(m - cm0) * J + jj) = make_float4(h[0], h[1], h[2], h[3]);
+    }
+    if constexpr (BF) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) cr[q] = h[q];  // h back to the tile (0 past mend) for the transposed store
+    }
+  }
+  if constexpr (BF) {
+    // h^T [J, chunk_rows] for the bf16 dW: the lane's 4 consecutive rows of
+    // the MFMA layout as one 8-byte store
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < Cfg::FM; ++i)
+#pragma unroll
+      for (int j = 0; j < Cfg::FN; ++j) {
+        const int jj = j0 + tile_col<Cfg>(j);
+        if (jj >= J) continue;
+        float hv[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) hv[r] = C[tile_row<Cfg>(i, r) * LDC + tile_col<Cfg>(j)];
         const int mr0 = m0 + tile_row<Cfg>(i, 0) - cm0;
         *reinterpret_cast<uint2*>(hbuf + (size_t)jj * a.chunk_rows + mr0) =
             make_uint2((uint32_t)f2bf(hv[0]) | ((uint32_t)f2bf(hv[1]) << 16),
                        (uint32_t)f2bf(hv[2]) | ((uint32_t)f2bf(hv[3]) << 16));
       }
-    }
+  }
 }
 
 // ---------------------------------------------------------------------------
