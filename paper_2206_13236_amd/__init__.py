@@ -303,7 +303,7 @@ class PrunedRnntLoss:
     and the joiner backward. The simple loss's own gradients (two
     contractions that only the caller needs) run on a second stream at the
     default priority, forked after the joiner forward so that they overlap
-    the pruned recursion, which occupies one workgroup per utterance, and
+    the pruned recursion, which occupies a few workgroups per utterance, and
     joined back before ``step`` returns (in stream order).
 
     With ``pruned_scale == 0`` (the warm-up of Sec. 4: the pruned part is
