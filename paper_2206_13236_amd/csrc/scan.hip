@@ -359,9 +359,13 @@ __global__ __launch_bounds__(128) void scan_sweep_kernel(BandArgs a) {
 template <int K>
 __global__ __launch_bounds__(128) void scan_replay_kernel(BandArgs a) {
   // one spare frame row takes the stores of steps past a chunk's end
-  __shared__ double s_al[4][kScanMaxC + 1][16];
-  __shared__ double s_ey[4][kScanMaxC + 1][16];
-  __shared__ double s_ex[4][kScanMaxC + 1][16];
+  // [4 rows][C + 1 frames][16 slots] each, sized by C at launch; frame C is
+  // the spare row that takes the stores of steps past a chunk's end
+  extern __shared__ double s_dyn[];
+  const int CP = a.C + 1;
+  double* s_al = s_dyn;
+  double* s_ey = s_dyn + 4 * CP * 16;
+  double* s_ex = s_dyn + 8 * CP * 16;
   const int n = blockIdx.y;
   const int lane = threadIdx.x & 63, row = lane >> 4, s = lane & 15;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -383,7 +387,7 @@ __global__ __launch_bounds__(128) void scan_replay_kernel(BandArgs a) {
       for (int j = 0; j < kPrefetch; ++j) {
         const int k = k0 + j;
         const double al = alpha_frame<K>(ain, ring[j], v, s, rowbase, k < len);
-        s_al[row][k < len ? k : kScanMaxC][s] = al;
+        s_al[(row * CP + (k < len ? k : C)) * 16 + s] = al;
         const int kk = k + kPrefetch;
         ring[j] = scan_load(v, kk < len ? t0 + kk : -1, s);
         __builtin_amdgcn_sched_barrier(0);
@@ -402,9 +406,9 @@ __global__ __launch_bounds__(128) void scan_replay_kernel(BandArgs a) {
         const int k = len - 1 - (k0 + j);  // frame t0 + k, descending
         double eyp, exq;
         beta_frame<K>(bt, ring[j], v, s, rowbase, k >= 0, eyp, exq);
-        const int kk0 = k >= 0 ? k : kScanMaxC;
-        s_ey[row][kk0][s] = eyp;
-        s_ex[row][kk0][s] = exq;
+        const int kk0 = k >= 0 ? k : C;
+        s_ey[(row * CP + kk0) * 16 + s] = eyp;
+        s_ex[(row * CP + kk0) * 16 + s] = exq;
         const int kk = k - kPrefetch;
         ring[j] = scan_load(v, kk >= 0 ? t0 + kk : -1, s);
         __builtin_amdgcn_sched_barrier(0);
@@ -423,9 +427,10 @@ __global__ __launch_bounds__(128) void scan_replay_kernel(BandArgs a) {
     const bool live = lv && t < Tn;
     double ey = kNegInfD, ex = kNegInfD;
     if (live && s < S) {
-      const double al = s_al[cr][k][s];
-      ey = al + s_ey[cr][k][s];
-      ex = al + s_ex[cr][k][s];
+      const int o = (cr * CP + k) * 16 + s;
+      const double al = s_al[o];
+      ey = al + s_ey[o];
+      ex = al + s_ex[o];
     }
     // frame total over the row (butterfly within 16 lanes)
     double mx = ey;
@@ -465,7 +470,8 @@ hipError_t launch_scan_k(const BandArgs& a, hipStream_t s) {
   }
   {
     RNNT_PROF(s, "scan_replay");
-    hipLaunchKernelGGL((scan_replay_kernel<K>), dim3((a.nchunk + 3) / 4, a.b.N), dim3(128), 0, s, a);
+    const size_t lds = (size_t)3 * 4 * (a.C + 1) * 16 * sizeof(double);
+    hipLaunchKernelGGL((scan_replay_kernel<K>), dim3((a.nchunk + 3) / 4, a.b.N), dim3(128), lds, s, a);
   }
   return hipGetLastError();
 }
