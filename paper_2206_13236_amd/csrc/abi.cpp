@@ -84,8 +84,8 @@ struct SimpleWs {
   float* Z;
   float* px;
   float* py;
-  float* pxd;
-  float* pyd;
+  DiagT* pxd;
+  DiagT* pyd;
   double* alpha;
   double* beta;
   double* Lutt;
@@ -118,8 +118,8 @@ SimpleWs simple_layout(void* base, int N, int T, int U, int V) {
   w.px = c.take<float>(L);
   w.py = c.take<float>(L);
   const size_t LD = (size_t)N * lattice_diag_cells(T, U);
-  w.pxd = c.take<float>(LD);
-  w.pyd = c.take<float>(LD);
+  w.pxd = c.take<DiagT>(LD);
+  w.pyd = c.take<DiagT>(LD);
   w.alpha = c.take<double>(LD);
   w.beta = c.take<double>(LD);
   w.Lutt = c.take<double>((size_t)N);
@@ -336,7 +336,8 @@ void set_joiner_bwd(JoinerArgs& a, const JoinerBwdWs& w, const float* lse, const
 // that the joiner's forward and backward use in turn.
 struct FullWs {
   int* ranges;
-  float *px, *py, *lse, *gx, *gy, *pxd, *pyd;
+  float *px, *py, *lse, *gx, *gy;
+  DiagT *pxd, *pyd;
   double *alpha, *beta, *Lutt, *ry, *rx, *cpx, *cpy;
   void* joiner;
   size_t bytes;
@@ -354,8 +355,8 @@ FullWs full_layout(void* base, int N, int T, int U, int J, int V, int bf16) {
   w.gx = c.take<float>(L);
   w.gy = c.take<float>(L);
   const size_t LD = (size_t)N * lattice_diag_cells(T, U);
-  w.pxd = c.take<float>(LD);
-  w.pyd = c.take<float>(LD);
+  w.pxd = c.take<DiagT>(LD);
+  w.pyd = c.take<DiagT>(LD);
   w.alpha = c.take<double>(LD);
   w.beta = c.take<double>(LD);
   w.Lutt = c.take<double>((size_t)N);
@@ -488,7 +489,7 @@ int rnnt_pruned_joiner(const rnnt_batch* batch, int32_t S, int32_t J, int32_t V,
 // Workspace of rnnt_pruned_loss: the band in a diagonal-major layout of
 // band_slots(U, S) slots per diagonal (the per-slot meta only on the slot layout).
 struct BandWs {
-  float *pxd, *pyd;
+  DiagT *pxd, *pyd;
   uint32_t* meta;
   double *alpha, *beta, *Lutt;
   size_t bytes;
@@ -498,8 +499,8 @@ BandWs band_layout(void* base, int N, int T, int U, int S) {
   Carve c(base);
   BandWs w;
   const size_t cells = (size_t)N * band_diagonals(T, U, S) * band_slots(U, S);
-  w.pxd = c.take<float>(cells);
-  w.pyd = c.take<float>(cells);
+  w.pxd = c.take<DiagT>(cells);
+  w.pyd = c.take<DiagT>(cells);
   w.meta = band_masked(U, S) ? nullptr : c.take<uint32_t>(cells);
   w.alpha = c.take<double>(cells);
   w.beta = c.take<double>(cells);

@@ -83,8 +83,8 @@ __global__ __launch_bounds__(256) void band_prep_kernel(BandArgs a) {
       const size_t o = row0 + (size_t)d * S + s;
       if (ee == e && s < ns) {
         const int db = (t + 1 < Tn) ? db_next : ((p + s == Un) ? kEndNode : kNoShift);
-        a.pxd[o] = a.px[src + s];
-        a.pyd[o] = a.py[src + s];
+        a.pxd[o] = (DiagT)((double)a.px[src + s] * kLog2e);
+        a.pyd[o] = (DiagT)((double)a.py[src + s] * kLog2e);
         a.meta[o] = kValid | (uint32_t)da | ((uint32_t)db << 8);
       } else {
         a.meta[o] = 0u;
@@ -94,7 +94,8 @@ __global__ __launch_bounds__(256) void band_prep_kernel(BandArgs a) {
 }
 
 // Masked-lattice path: one thread per cell (d, u) of the [D, 64] layout of
-// every utterance; cells off the utterance's lattice are never read.
+// every utterance, in log2 units; -inf off the band and at every cell that is
+// no node of the utterance's lattice, as the lattice recursion requires.
 __global__ __launch_bounds__(256) void band_mask_kernel(BandArgs a) {
   const int T = a.b.T, S = a.S, D = a.D;
   const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -105,16 +106,17 @@ __global__ __launch_bounds__(256) void band_mask_kernel(BandArgs a) {
   const int t = d - u;
   int Tn, Un;
   utt_dims(a.b, n, Tn, Un);
-  if (t < 0 || t >= Tn || u > Un) return;
-  const int s = u - band_p(a, n, t, Un);
-  float x = -__builtin_inff(), y = -__builtin_inff();
-  if (s >= 0 && s < S) {
-    const size_t k = ((size_t)n * T + t) * S + s;
-    x = a.px[k];
-    y = a.py[k];
+  double x = kNegInfD, y = kNegInfD;
+  if (t >= 0 && t < Tn && u <= Un) {
+    const int s = u - band_p(a, n, t, Un);
+    if (s >= 0 && s < S) {
+      const size_t k = ((size_t)n * T + t) * S + s;
+      x = (double)a.px[k] * kLog2e;
+      y = (double)a.py[k] * kLog2e;
+    }
   }
-  a.pxd[i] = x;
-  a.pyd[i] = y;
+  a.pxd[i] = (DiagT)x;
+  a.pyd[i] = (DiagT)y;
 }
 
 DEV double bpermute_d(double v, int src_lane) {
@@ -130,18 +132,18 @@ struct BandDiag {
 
 // Slot s of diagonal d (start diagonal e = d - s >= 0; slots with e < 0 are
 // never written and read as invalid).
-DEV void band_load(const BandDiag& v, int d, int lane, bool live, float& x, float& y, uint32_t& m) {
+DEV void band_load(const BandDiag& v, int d, int lane, bool live, DiagT& x, DiagT& y, uint32_t& m) {
   const bool in = live && d >= lane && d < v.Dn;
-  const uint32_t off = in ? (uint32_t)(d * v.S + lane) * 4u : kOob;
-  x = buf_load_f32(v.px, off);
-  y = buf_load_f32(v.py, off);
-  m = __builtin_amdgcn_raw_buffer_load_b32(v.meta, (int)off, 0, 0);  // 0 (invalid) out of range
+  const uint32_t cell = (uint32_t)(d * v.S + lane);
+  x = diag_load(v.px, in ? cell * (uint32_t)sizeof(DiagT) : kOob);
+  y = diag_load(v.py, in ? cell * (uint32_t)sizeof(DiagT) : kOob);
+  m = __builtin_amdgcn_raw_buffer_load_b32(v.meta, (int)(in ? cell * 4u : kOob), 0, 0);  // 0 (invalid) out of range
 }
 
 DEV void band_alpha(const BandDiag& v, int lane) {
   const bool live = lane < v.S;
   double hout = kNegInfD, vout = kNegInfD;
-  float xr[kBandPrefetch], yr[kBandPrefetch];
+  DiagT xr[kBandPrefetch], yr[kBandPrefetch];
   uint32_t mr[kBandPrefetch];
 #pragma unroll
   for (int k = 0; k < kBandPrefetch; ++k) band_load(v, k, lane, live, xr[k], yr[k], mr[k]);
@@ -159,8 +161,8 @@ DEV void band_alpha(const BandDiag& v, int lane) {
       const double hin = (da == kNoShift) ? kNegInfD : hin0;
       const double al = (d == 0) ? 0.0 : log2add(hin, vin);
       buf_store_f64(v.out, act ? (uint32_t)(d * v.S + lane) * 8u : kOob, al);
-      hout = act ? al + (double)yr[k] * kLog2e : kNegInfD;
-      vout = act ? al + (double)xr[k] * kLog2e : kNegInfD;
+      hout = act ? al + (double)yr[k] : kNegInfD;
+      vout = act ? al + (double)xr[k] : kNegInfD;
       band_load(v, d + kBandPrefetch, lane, live, xr[k], yr[k], mr[k]);
     }
   }
@@ -169,7 +171,7 @@ DEV void band_alpha(const BandDiag& v, int lane) {
 DEV void band_beta(const BandDiag& v, int lane) {
   const bool live = lane < v.S;
   double bout = kNegInfD;
-  float xr[kBandPrefetch], yr[kBandPrefetch];
+  DiagT xr[kBandPrefetch], yr[kBandPrefetch];
   uint32_t mr[kBandPrefetch];
 #pragma unroll
   for (int k = 0; k < kBandPrefetch; ++k) band_load(v, v.Dn - 1 - k, lane, live, xr[k], yr[k], mr[k]);
@@ -185,7 +187,7 @@ DEV void band_beta(const BandDiag& v, int lane) {
       const double h0 = bpermute_d(bout, src);
       const double vn = dpp_move_d<kDppWaveShl1>(bout, kNegInfD);
       const double hin = (db == kEndNode) ? 0.0 : ((db == kNoShift || lane - db < 0) ? kNegInfD : h0);
-      const double be = log2add((double)yr[k] * kLog2e + hin, (double)xr[k] * kLog2e + vn);
+      const double be = log2add((double)yr[k] + hin, (double)xr[k] + vn);
       buf_store_f64(v.out, act ? (uint32_t)(d * v.S + lane) * 8u : kOob, be);
       bout = act ? be : kNegInfD;
       band_load(v, d - kBandPrefetch, lane, live, xr[k], yr[k], mr[k]);
@@ -203,8 +205,8 @@ __global__ __launch_bounds__(kBandThreads) void band_fb_kernel(BandArgs a) {
   const size_t base = (size_t)n * D * S;
   const size_t cells = (size_t)D * S;
   BandDiag v;
-  v.px = make_rsrc(a.pxd + base, cells * sizeof(float));
-  v.py = make_rsrc(a.pyd + base, cells * sizeof(float));
+  v.px = make_rsrc(a.pxd + base, cells * sizeof(DiagT));
+  v.py = make_rsrc(a.pyd + base, cells * sizeof(DiagT));
   v.meta = make_rsrc(a.meta + base, cells * sizeof(uint32_t));
   v.S = S;
   v.Dn = Tn + Un;
@@ -222,7 +224,7 @@ __global__ __launch_bounds__(kBandThreads) void band_fb_kernel(BandArgs a) {
     double L = kNegInfD;
     if (se >= 0 && se < S) {
       const size_t o = base + (size_t)(Tn - 1 + Un) * S + se;
-      L = a.alpha[o] + (double)a.pyd[o] * kLog2e;
+      L = a.alpha[o] + (double)a.pyd[o];
     }
     const double L2 = ok ? L : __builtin_nan("");
     a.Lutt[n] = L2;

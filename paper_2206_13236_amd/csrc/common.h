@@ -57,6 +57,9 @@ DEV Rsrc make_rsrc(const void* p, size_t bytes) {
 DEV float buf_load_f32(Rsrc r, uint32_t off) {
   return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, (int)off, 0, 0));
 }
+DEV double buf_load_f64(Rsrc r, uint32_t off) {
+  return __builtin_bit_cast(double, __builtin_amdgcn_raw_buffer_load_b64(r, (int)off, 0, 0));
+}
 DEV void buf_store_f64(Rsrc r, uint32_t off, double v) {
   typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
   __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2_t, v), r, (int)off, 0, 0);
@@ -73,6 +76,16 @@ DEV double log2add(double a, double b) {
   float d = (float)(mn - mx);
   float c = __builtin_amdgcn_logf(1.0f + __builtin_amdgcn_exp2f(d));
   return mx + (double)c;
+}
+
+// The same sum for recursions that detect NaN inputs on the side: no
+// compare-and-select on the dependency chain. v_max/v_min pass over a NaN;
+// the difference is clamped to <= 0, which also turns the NaN of
+// (-inf) - (-inf) into 0, so that two -inf give -inf + 1 = -inf.
+DEV double log2add_nonan(double a, double b) {
+  const double mx = __builtin_fmax(a, b), mn = __builtin_fmin(a, b);
+  const float d = __builtin_fminf((float)(mn - mx), 0.0f);
+  return mx + (double)__builtin_amdgcn_logf(1.0f + __builtin_amdgcn_exp2f(d));
 }
 
 // 2^x for an fp64 log2-domain argument that is <= ~0 (an occupation).

@@ -325,7 +325,8 @@ DEV float bias_at(const void* bias, int bf16, int v) {
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void joiner_prep_kernel(JoinerArgs a) {
   __shared__ int s_part[4];
-  const int n = blockIdx.x;
+  const int per = (a.b.T * a.S + 255) / 256;  // blocks per utterance: one (t, s) slot per thread
+  const int n = blockIdx.x / per, i = (blockIdx.x - n * per) * 256 + threadIdx.x;
   const int T = a.b.T, U1 = a.b.U + 1, S = a.S, J = a.J;
   // frame offset of utterance n: sum of T_q over q < n, the lengths loaded
   // in parallel and summed by a block reduction
@@ -342,27 +343,26 @@ __global__ __launch_bounds__(256) void joiner_prep_kernel(JoinerArgs a) {
   const int off = s_part[0] + s_part[1] + s_part[2] + s_part[3];
   int Tn, Un;
   utt_dims(a.b, n, Tn, Un);
-  if (threadIdx.x == 0) {
+  if (i == 0) {
     a.frame_off[n] = off;
     if (n == a.b.N - 1) a.frame_off[a.b.N] = off + Tn;
   }
-  for (int i = threadIdx.x; i < Tn * S; i += blockDim.x) {
-    const int t = i / S, s = i - t * S;
-    const size_t nts = ((size_t)n * T + t) * S + s;
-    const int u = a.ranges[nts];
-    int4 r;
-    if (u >= 0 && u <= Un) {
-      bool ok = true;
-      r.x = (int)(((size_t)n * T + t) * J);
-      r.y = (int)(((size_t)n * U1 + u) * J);
-      r.z = (u < Un) ? symbol_at(a.b, n, u, a.V, ok) : -1;
-      if (!ok) r.z = -2;  // symbol outside [0, V): px is NaN, so the utterance's loss is NaN
-      r.w = (int)nts;
-    } else {
-      r = make_int4(0, 0, -1, -1);
-    }
-    a.rowinfo[(size_t)(off + t) * S + s] = r;
+  if (i >= Tn * S) return;
+  const int t = i / S, s = i - t * S;
+  const size_t nts = ((size_t)n * T + t) * S + s;
+  const int u = a.ranges[nts];
+  int4 r;
+  if (u >= 0 && u <= Un) {
+    bool ok = true;
+    r.x = (int)(((size_t)n * T + t) * J);
+    r.y = (int)(((size_t)n * U1 + u) * J);
+    r.z = (u < Un) ? symbol_at(a.b, n, u, a.V, ok) : -1;
+    if (!ok) r.z = -2;  // symbol outside [0, V): px is NaN, so the utterance's loss is NaN
+    r.w = (int)nts;
+  } else {
+    r = make_int4(0, 0, -1, -1);
   }
+  a.rowinfo[(size_t)(off + t) * S + s] = r;
 }
 
 // ---------------------------------------------------------------------------
@@ -1113,7 +1113,7 @@ int joiner_db_rows(int N, int T, int S) {
 hipError_t launch_joiner_prep(const JoinerArgs& a, hipStream_t s) {
   {
     RNNT_PROF(s, "joiner_prep");
-    hipLaunchKernelGGL(joiner_prep_kernel, dim3(a.b.N), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(joiner_prep_kernel, dim3(a.b.N * ((a.b.T * a.S + 255) / 256)), dim3(256), 0, s, a);
   }
   return hipGetLastError();
 }

@@ -5,6 +5,12 @@
 
 #include "common.h"
 
+// Element type of the diagonal-major copies of px and py that the lattice
+// recursions read (log2 units), and its load from a buffer resource. fp64:
+// the wavefront step then adds them without a conversion.
+using DiagT = double;
+DEV DiagT diag_load(Rsrc r, uint32_t byte_off) { return buf_load_f64(r, byte_off); }
+
 // ---- stage 1-2: trivial joiner, full lattice --------------------------------
 struct SimpleArgs {
   BatchDev b;
@@ -21,8 +27,8 @@ struct SimpleArgs {
   int lsplit;
   float* px;           // [N, T, U+1] (caller's or ws)
   float* py;
-  float* pxd;          // ws [N, D, W]: px, py in the diagonal-major lattice layout
-  float* pyd;
+  DiagT* pxd;          // ws [N, D, W]: px, py in the diagonal-major lattice layout, log2 units
+  DiagT* pyd;          //   (times log2 e), -inf at every cell that is no node of the utterance
   double* alpha;       // ws [N, D, W], log2 domain, diagonal-major
   double* beta;        // ws [N, D, W], log2 domain, diagonal-major
   double* Lutt;        // ws [N]: total log2-prob (NaN for an invalid utterance)
@@ -69,7 +75,27 @@ int lattice_rows_per_lane(int U1);
 inline size_t lattice_diag_cells(int T, int U) {
   return (size_t)(T + U) * 64 * lattice_rows_per_lane(U + 1);
 }
+inline int lattice_fill_blocks(int T, int U) { return (int)((lattice_diag_cells(T, U) + 255) / 256); }
 DEV int lattice_slot(int u, int R) { return (u % R) * 64 + u / R; }
+// Cells of the diagonal-major layout [T+U, 64R] of an utterance's lattice
+// that no (t, u) of the [T, U+1] rectangle maps to are set to -inf in both
+// copies by a fill of 256-cell blocks per utterance (32-bit index arithmetic;
+// the rectangle's own cells are written by their producer).
+DEV int lattice_fill_blocks_dev(int T, int U1, int R) { return ((T + U1 - 1) * 64 * R + 255) / 256; }
+DEV void lattice_fill_outside(DiagT* pxd, DiagT* pyd, int blk, int tid, int T, int U1, int R) {
+  const int per = lattice_fill_blocks_dev(T, U1, R);
+  const int n = blk / per;
+  const uint32_t W = 64u * (uint32_t)R, DW = (uint32_t)(T + U1 - 1) * W;
+  const uint32_t c = (uint32_t)(blk - n * per) * 256u + (uint32_t)tid;
+  if (c >= DW) return;
+  const int d = (int)(c / W), slot = (int)(c % W);  // W is a power of two
+  const int u = (slot & 63) * R + (slot >> 6), t = d - u;
+  if (u >= U1 || t < 0 || t >= T) {
+    const size_t j = (size_t)n * DW + c;
+    pxd[j] = (DiagT)kNegInfD;
+    pyd[j] = (DiagT)kNegInfD;
+  }
+}
 DEV int lattice_rows_per_lane_dev(int U1) {
   const int need = (U1 + 63) / 64;
   return need <= 1 ? 1 : need <= 2 ? 2 : need <= 4 ? 4 : need <= 8 ? 8 : 16;
@@ -150,8 +176,8 @@ struct BandArgs {
   const float* px;     // [N, T, S]
   const float* py;
   const int* ranges;   // [N, T, S]
-  float* pxd;          // ws [N, D, W]: px, py in a diagonal-major layout
-  float* pyd;
+  DiagT* pxd;          // ws [N, D, W]: px, py in a diagonal-major layout, log2 units
+  DiagT* pyd;
   uint32_t* meta;      // ws [N, D, W] per-slot shifts and validity (band path only)
   double* alpha;       // ws [N, D, W] log2 domain, diagonal-major
   double* beta;

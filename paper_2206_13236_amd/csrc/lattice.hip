@@ -25,6 +25,8 @@
 // Precision: log2 domain with fp64 accumulators; only the bounded correction
 // term of LogAdd goes through fp32 exp2/log2 (see log2add). alpha and beta are
 // stored in fp64.
+// A NaN px or py at a node of the lattice is flagged on the side and makes
+// the utterance's loss NaN, like an out-of-range length or symbol.
 #include "kernels.h"
 #include "prof.h"
 
@@ -32,44 +34,62 @@ namespace {
 
 constexpr int kOccFrames = 16;  // frames (waves) per workgroup of the occupation kernel
 
-// The recursion loops are kept free of branches and of 64-bit address
-// arithmetic: px, py and alpha/beta of the utterance are buffer resources in
-// the diagonal-major layout, so the lane's row r of diagonal d sits at
-// d*W + r*64 + lane and every load and store of a step is contiguous across
-// the wave; lanes whose node lies outside the lattice load from / store to
-// kOob (reads 0, store dropped). Conditional memory operations would
-// otherwise make the compiler wait for every outstanding load and store at
-// each step.
+// The recursion loops are kept free of branches, selects and 64-bit address
+// arithmetic. px, py (fp64, log2 units) and alpha/beta of the utterance are
+// buffer resources over the diagonal-major layout [D, W], so the lane's row r
+// of diagonal d sits at d*W + r*64 + lane and every load and store of a step
+// is contiguous across the wave. Every cell that is no node of the utterance
+// holds -inf in px and py, so a node outside the lattice needs no test:
+//   alpha: a node at t < 0 has only such nodes before it and stays -inf; a
+//          node at t >= T_n or u > U_n may take a finite value, but both of
+//          its outgoing sums add its own -inf inputs, so nothing reaches a
+//          node of the lattice from it;
+//   beta:  every such node gets -inf (both of its terms add its own -inf
+//          inputs), except the virtual node (T_n, U_n) after the final
+//          blank, which is the initial value 0.
+// Their stored values land in cells that no reader takes. Diagonals beyond
+// the layout (the idle steps at the end of a loop) have byte offsets at or
+// past the resource's size, negative ones included after the unsigned
+// conversion: their loads read 0 and their stores are dropped.
 struct LatView {
-  Rsrc px, py, out;  // pxd, pyd (f32) and alpha or beta (f64) of the utterance, [D, W]
+  Rsrc px, py, out;  // pxd, pyd (DiagT) and alpha or beta (f64) of the utterance, [D, W]
   int Tn, Un, W;
 };
 
 template <int R>
-DEV void lattice_load(const LatView& v, int d, const bool (&rok)[R], int lane, float (&x)[R], float (&y)[R]) {
+DEV void lattice_load(const LatView& v, int d, int lane, DiagT (&x)[R], DiagT (&y)[R]) {
   const int dW = d * v.W + lane;
 #pragma unroll
   for (int r = 0; r < R; ++r) {
-    const int t = d - (lane * R + r);
-    const bool act = rok[r] && (unsigned)t < (unsigned)v.Tn;
-    const uint32_t off = act ? (uint32_t)(dW + r * 64) * 4u : kOob;
-    x[r] = buf_load_f32(v.px, off);
-    y[r] = buf_load_f32(v.py, off);
+    const uint32_t off = (uint32_t)(dW + r * 64) * (uint32_t)sizeof(DiagT);
+    x[r] = diag_load(v.px, off);
+    y[r] = diag_load(v.py, off);
   }
 }
 
-template <int R, int P>
-DEV void alpha_pass(const LatView& v, int lane) {
-  const int D = v.Tn + v.Un;  // diagonals 0 .. Tn-1+Un (the loop may run up to P-1 idle steps past them)
-  bool rok[R];
+// A NaN among the inputs of a step is flagged in `bad` rather than carried
+// through the recursion.
+template <int R>
+DEV void lattice_check(const DiagT (&x)[R], const DiagT (&y)[R], bool& bad) {
 #pragma unroll
-  for (int r = 0; r < R; ++r) rok[r] = lane * R + r <= v.Un;
+  for (int r = 0; r < R; ++r) bad |= __builtin_isunordered(x[r], y[r]);
+}
+
+// Returns whether this lane saw a NaN input.
+template <int R, int P>
+DEV bool alpha_pass(const LatView& v, int lane) {
+  const int D = v.Tn + v.Un;  // diagonals 0 .. Tn-1+Un (the loop may run up to P-1 idle steps past them)
+  // alpha(0, 0) = 0 comes out of the first step as LogAdd(0, -inf)
   double hout[R], vout[R];
 #pragma unroll
-  for (int r = 0; r < R; ++r) hout[r] = vout[r] = kNegInfD;
-  float xr[P][R], yr[P][R];
+  for (int r = 0; r < R; ++r) {
+    hout[r] = (lane * R + r == 0) ? 0.0 : kNegInfD;
+    vout[r] = kNegInfD;
+  }
+  bool bad = false;
+  DiagT xr[P][R], yr[P][R];  // converted at use, not at load
 #pragma unroll
-  for (int k = 0; k < P; ++k) lattice_load<R>(v, k, rok, lane, xr[k], yr[k]);
+  for (int k = 0; k < P; ++k) lattice_load<R>(v, k, lane, xr[k], yr[k]);
   for (int d0 = 0; d0 < D; d0 += P) {
 #pragma unroll
     for (int k = 0; k < P; ++k) {
@@ -79,38 +99,39 @@ DEV void alpha_pass(const LatView& v, int lane) {
       double nh[R], nv[R];
 #pragma unroll
       for (int r = 0; r < R; ++r) {
-        const int t = d - (lane * R + r);
-        const bool act = rok[r] && (unsigned)t < (unsigned)v.Tn;
         const double vin = (r == 0) ? vfirst : vout[r - 1];
-        const double al = (d == 0) ? 0.0 : log2add(hout[r], vin);
-        nh[r] = act ? al + (double)yr[k][r] * kLog2e : kNegInfD;
-        nv[r] = act ? al + (double)xr[k][r] * kLog2e : kNegInfD;
-        buf_store_f64(v.out, act ? (uint32_t)(dW + r * 64) * 8u : kOob, al);
+        const double al = log2add_nonan(hout[r], vin);
+        nh[r] = al + (double)yr[k][r];
+        nv[r] = al + (double)xr[k][r];
+        buf_store_f64(v.out, (uint32_t)(dW + r * 64) * 8u, al);
       }
 #pragma unroll
       for (int r = 0; r < R; ++r) {
         hout[r] = nh[r];
         vout[r] = nv[r];
       }
-      lattice_load<R>(v, d + P, rok, lane, xr[k], yr[k]);
+      lattice_check<R>(xr[k], yr[k], bad);
+      lattice_load<R>(v, d + P, lane, xr[k], yr[k]);
+      // no later step's work is hoisted into this one, where it would wait
+      // for loads issued a step ago
+      __builtin_amdgcn_sched_barrier(0);
     }
   }
+  return bad;
 }
 
 template <int R, int P>
-DEV void beta_pass(const LatView& v, int lane) {
+DEV bool beta_pass(const LatView& v, int lane) {
   const int D = v.Tn + v.Un;
-  bool rok[R];
-#pragma unroll
-  for (int r = 0; r < R; ++r) rok[r] = lane * R + r <= v.Un;
   // beta of my rows on the previous (higher) diagonal; the virtual node
   // (Tn, Un) after the final blank has beta = 0.
   double bprev[R];
 #pragma unroll
   for (int r = 0; r < R; ++r) bprev[r] = (lane * R + r == v.Un) ? 0.0 : kNegInfD;
-  float xr[P][R], yr[P][R];
+  bool bad = false;
+  DiagT xr[P][R], yr[P][R];  // converted at use, not at load
 #pragma unroll
-  for (int k = 0; k < P; ++k) lattice_load<R>(v, D - 1 - k, rok, lane, xr[k], yr[k]);
+  for (int k = 0; k < P; ++k) lattice_load<R>(v, D - 1 - k, lane, xr[k], yr[k]);
   for (int d0 = D - 1; d0 >= 0; d0 -= P) {
 #pragma unroll
     for (int k = 0; k < P; ++k) {
@@ -120,18 +141,18 @@ DEV void beta_pass(const LatView& v, int lane) {
       double nb[R];
 #pragma unroll
       for (int r = 0; r < R; ++r) {
-        const int t = d - (lane * R + r);
-        const bool act = rok[r] && (unsigned)t < (unsigned)v.Tn;
         const double vin = (r == R - 1) ? vlast : bprev[r + 1];
-        const double be = log2add((double)yr[k][r] * kLog2e + bprev[r], (double)xr[k][r] * kLog2e + vin);
-        nb[r] = act ? be : kNegInfD;
-        buf_store_f64(v.out, act ? (uint32_t)(dW + r * 64) * 8u : kOob, be);
+        nb[r] = log2add_nonan((double)yr[k][r] + bprev[r], (double)xr[k][r] + vin);
+        buf_store_f64(v.out, (uint32_t)(dW + r * 64) * 8u, nb[r]);
       }
 #pragma unroll
       for (int r = 0; r < R; ++r) bprev[r] = nb[r];
-      lattice_load<R>(v, d - P, rok, lane, xr[k], yr[k]);
+      lattice_check<R>(xr[k], yr[k], bad);
+      lattice_load<R>(v, d - P, lane, xr[k], yr[k]);
+      __builtin_amdgcn_sched_barrier(0);
     }
   }
+  return bad;
 }
 
 template <int R, int P>
@@ -146,45 +167,57 @@ __global__ __launch_bounds__(128) void lattice_fb_kernel(SimpleArgs a) {
   const size_t cells = (size_t)(T + U1 - 1) * W;
   const size_t base = (size_t)n * cells;
   LatView v;
-  v.px = make_rsrc(a.pxd + base, cells * sizeof(float));
-  v.py = make_rsrc(a.pyd + base, cells * sizeof(float));
+  v.px = make_rsrc(a.pxd + base, cells * sizeof(DiagT));
+  v.py = make_rsrc(a.pyd + base, cells * sizeof(DiagT));
   v.Tn = Tn;
   v.Un = Un;
   v.W = W;
+  bool bad;
   if (wave == 0) {
     v.out = make_rsrc(a.alpha + base, cells * sizeof(double));
-    alpha_pass<R, P>(v, lane);
+    bad = alpha_pass<R, P>(v, lane);
   } else {
     v.out = make_rsrc(a.beta + base, cells * sizeof(double));
-    beta_pass<R, P>(v, lane);
+    bad = beta_pass<R, P>(v, lane);
   }
-  __syncthreads();
+  // symbols outside [0, V) make the utterance invalid (V = 0: not checked here);
+  // each thread checks a strided share of them
+  bool sok = true;
+  if (a.V > 0)
+    for (int u = tid; u < Un; u += blockDim.x) symbol_at(a.b, n, u, a.V, sok);
+  const bool sbad = __syncthreads_or(!sok || bad) != 0;  // or a NaN input
   if (tid == 0) {
-    // symbols outside [0, V) make the utterance invalid (V = 0: not checked here)
-    bool sok = true;
-    if (a.V > 0)
-      for (int u = 0; u < Un; ++u) symbol_at(a.b, n, u, a.V, sok);
     const size_t last = base + (size_t)(Tn - 1 + Un) * W + lattice_slot(Un, R);
-    const double L = a.alpha[last] + (double)a.pyd[last] * kLog2e;
-    const double L2 = (ok && sok) ? L : __builtin_nan("");
+    const double L = a.alpha[last] + (double)a.pyd[last];
+    const double L2 = (ok && !sbad) ? L : __builtin_nan("");
     a.Lutt[n] = L2;
     a.loss[n] = (L2 == L2) ? (float)(-L2 * kLn2) : __builtin_nanf("");
   }
 }
 
-// px, py [N, T, U+1] -> the diagonal-major copies (for producers that do not
-// write them directly).
+// px, py [N, T, U+1] -> the diagonal-major copies in log2 units (for
+// producers that do not write them directly): one thread per node of the
+// rectangle, then one per cell of the copies, which take -inf where no node
+// of the utterance lies.
 __global__ __launch_bounds__(256) void lattice_diag_copy_kernel(SimpleArgs a, int R) {
   const int T = a.b.T, U1 = a.b.U + 1;
   const size_t L = (size_t)a.b.N * T * U1;
+  const int rect_blocks = (int)((L + 255) / 256);  // blocks of 256 threads
+  if ((int)blockIdx.x >= rect_blocks) {
+    lattice_fill_outside(a.pxd, a.pyd, (int)blockIdx.x - rect_blocks, threadIdx.x, T, U1, R);
+    return;
+  }
   const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= L) return;
   const int n = (int)(i / ((size_t)T * U1));
   const int rem = (int)(i - (size_t)n * T * U1);
   const int t = rem / U1, u = rem - t * U1;
+  int Tn, Un;
+  utt_dims(a.b, n, Tn, Un);
+  const bool node = t < Tn && u <= Un;
   const size_t o = (size_t)n * (T + U1 - 1) * 64 * R + (size_t)(t + u) * 64 * R + lattice_slot(u, R);
-  a.pxd[o] = a.px[i];
-  a.pyd[o] = a.py[i];
+  a.pxd[o] = (DiagT)((node && u < Un) ? (double)a.px[i] * kLog2e : kNegInfD);
+  a.pyd[o] = (DiagT)(node ? (double)a.py[i] * kLog2e : kNegInfD);
 }
 
 template <int R>
@@ -299,10 +332,11 @@ int lattice_rows_per_lane(int U1) {
 }
 
 hipError_t launch_lattice_diag_copy(const SimpleArgs& a, hipStream_t s) {
-  const size_t L = (size_t)a.b.N * a.b.T * (a.b.U + 1);
+  const size_t blocks =
+      ((size_t)a.b.N * a.b.T * (a.b.U + 1) + 255) / 256 + (size_t)a.b.N * lattice_fill_blocks(a.b.T, a.b.U);
   {
     RNNT_PROF(s, "lattice_diag_copy");
-    hipLaunchKernelGGL(lattice_diag_copy_kernel, dim3((unsigned)((L + 255) / 256)), dim3(256), 0, s, a,
+    hipLaunchKernelGGL(lattice_diag_copy_kernel, dim3((unsigned)blocks), dim3(256), 0, s, a,
                        lattice_rows_per_lane(a.b.U + 1));
   }
   return hipGetLastError();
@@ -314,8 +348,8 @@ hipError_t launch_lattice_recursion(const SimpleArgs& a, hipStream_t s) {
   switch (lattice_rows_per_lane(a.b.U + 1)) {
     case 1: hipLaunchKernelGGL((lattice_fb_kernel<1, 8>), dim3(a.b.N), dim3(128), 0, s, a); break;
     case 2: hipLaunchKernelGGL((lattice_fb_kernel<2, 8>), dim3(a.b.N), dim3(128), 0, s, a); break;
-    case 4: hipLaunchKernelGGL((lattice_fb_kernel<4, 4>), dim3(a.b.N), dim3(128), 0, s, a); break;
-    case 8: hipLaunchKernelGGL((lattice_fb_kernel<8, 2>), dim3(a.b.N), dim3(128), 0, s, a); break;
+    case 4: hipLaunchKernelGGL((lattice_fb_kernel<4, 8>), dim3(a.b.N), dim3(128), 0, s, a); break;
+    case 8: hipLaunchKernelGGL((lattice_fb_kernel<8, 4>), dim3(a.b.N), dim3(128), 0, s, a); break;
     default: hipLaunchKernelGGL((lattice_fb_kernel<16, 2>), dim3(a.b.N), dim3(128), 0, s, a); break;
   }
   return hipGetLastError();
@@ -327,8 +361,8 @@ hipError_t launch_lattice(const SimpleArgs& a, hipStream_t s) {
   switch (lattice_rows_per_lane(U1)) {
     case 1: launch_lattice_r<1, 8>(a, s); break;
     case 2: launch_lattice_r<2, 8>(a, s); break;
-    case 4: launch_lattice_r<4, 4>(a, s); break;
-    case 8: launch_lattice_r<8, 2>(a, s); break;
+    case 4: launch_lattice_r<4, 8>(a, s); break;
+    case 8: launch_lattice_r<8, 4>(a, s); break;
     default: launch_lattice_r<16, 2>(a, s); break;
   }
   return hipGetLastError();

@@ -249,28 +249,34 @@ __global__ __launch_bounds__(256) void scan_chunk_kernel(BandArgs a) {
 }
 
 // lse of the NS values a lane holds (entries beyond S are -inf; fixed
-// order; a NaN entry gives NaN).
+// order: pairwise trees). Branch-free: the max is v_max_f64, which passes
+// over a NaN, and a NaN entry reaches the result through its own term of the
+// sum; an all -inf set is shifted by 0, so that the sum is 0 and the result
+// -inf.
 template <int NS>
 DEV double lse_vals(const double (&xs)[NS]) {
-  double mx = xs[0];
+  double m[NS];
 #pragma unroll
-  for (int i = 1; i < NS; ++i) mx = (xs[i] > mx || xs[i] != xs[i]) ? xs[i] : mx;
-  if (mx == kNegInfD || mx != mx) return mx;
-  float sum = 0.f;
+  for (int i = 0; i < NS; ++i) m[i] = xs[i];
 #pragma unroll
-  for (int i = 0; i < NS; ++i) sum += __builtin_amdgcn_exp2f((float)(xs[i] - mx));
-  return mx + (double)__builtin_amdgcn_logf(sum);
+  for (int w = NS / 2; w >= 1; w >>= 1)
+#pragma unroll
+    for (int i = 0; i < w; ++i) m[i] = __builtin_fmax(m[i], m[i + w]);
+  const double sh = (m[0] == kNegInfD) ? 0.0 : m[0];
+  float e[NS];
+#pragma unroll
+  for (int i = 0; i < NS; ++i) e[i] = __builtin_amdgcn_exp2f((float)(xs[i] - sh));
+#pragma unroll
+  for (int w = NS / 2; w >= 1; w >>= 1)
+#pragma unroll
+    for (int i = 0; i < w; ++i) e[i] += e[i + w];
+  return sh + (double)__builtin_amdgcn_logf(e[0]);
 }
 
 DEV double readlane_d(double v, int l) {
   const int lo = __builtin_amdgcn_readlane(__double2loint(v), l);
   const int hi = __builtin_amdgcn_readlane(__double2hiint(v), l);
   return __hiloint2double(hi, lo);
-}
-
-DEV double buf_load_f64(Rsrc r, uint32_t off) {
-  typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
-  return __builtin_bit_cast(double, __builtin_amdgcn_raw_buffer_load_b64(r, (int)off, 0, 0));
 }
 
 // Per utterance: wave 0 carries the arrivals forward through the chunk

@@ -294,25 +294,33 @@ __global__ __launch_bounds__(256) void normalizer_kernel(SimpleArgs a) {
 }
 
 // Z = m_a + m_l + log(sum of the partials), px and py (Eqs. (1)-(2), (5)):
-// one thread per lattice node.
+// one thread per node of the [T, U+1] rectangle, then one per cell of the
+// diagonal-major copies, which take -inf where no node of the rectangle lies.
 __global__ __launch_bounds__(256) void normalizer_epi_kernel(SimpleArgs a) {
   const int T = a.b.T, U1 = a.b.U + 1, V = a.V;
+  const int R = lattice_rows_per_lane_dev(U1);
   const size_t L = (size_t)a.b.N * T * U1;
+  const int rect_blocks = (int)((L + 255) / 256);  // blocks of 256 threads
+  if ((int)blockIdx.x >= rect_blocks) {
+    lattice_fill_outside(a.pxd, a.pyd, (int)blockIdx.x - rect_blocks, threadIdx.x, T, U1, R);
+    return;
+  }
   const size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (idx >= L) return;
   const int n = (int)(idx / ((size_t)T * U1));
   const int rem = (int)(idx - (size_t)n * T * U1);
   const int t = rem / U1, u = rem - t * U1;
+  const size_t od = (size_t)n * (T + U1 - 1) * 64 * R + (size_t)(t + u) * 64 * R + lattice_slot(u, R);
   int Tn, Un;
   utt_dims(a.b, n, Tn, Un);
   if (t >= Tn || u > Un) {
     a.Z[idx] = 0.f;
     a.px[idx] = kNegInfF;
     a.py[idx] = kNegInfF;
+    a.pxd[od] = (DiagT)kNegInfD;
+    a.pyd[od] = (DiagT)kNegInfD;
     return;
   }
-  const int R = lattice_rows_per_lane_dev(U1);
-  const size_t od = (size_t)n * (T + U1 - 1) * 64 * R + (size_t)(t + u) * 64 * R + lattice_slot(u, R);
   float s = 0.f;
   for (int q = 0; q < a.nsplit; ++q) s += a.npart[(size_t)q * L + idx];
   s = (s > FLT_MIN || s != s) ? s : FLT_MIN;
@@ -335,8 +343,8 @@ __global__ __launch_bounds__(256) void normalizer_epi_kernel(SimpleArgs a) {
   }
   a.py[idx] = py;
   a.px[idx] = (u < Un) ? px : kNegInfF;
-  a.pyd[od] = py;
-  a.pxd[od] = (u < Un) ? px : kNegInfF;
+  a.pyd[od] = (DiagT)((double)py * kLog2e);
+  a.pxd[od] = (DiagT)((u < Un) ? (double)px * kLog2e : kNegInfD);
 }
 
 // ---------------------------------------------------------------------------
@@ -412,21 +420,34 @@ __global__ __launch_bounds__(256) void dam_kernel(SimpleArgs a) {
       }
     }
   if (active) {
-    // sparse part: target columns, in ascending u (deterministic)
-    for (int u = 0; u < Un; ++u) {
-      bool ok = true;
-      const int y = symbol_at(a.b, n, u, V, ok);
-      if (y < v0 || y >= v0 + Cfg::BN) continue;
+    // sparse part: target columns, in ascending u (deterministic). The
+    // symbols go through LDS (free once the main loop is done) in chunks, so
+    // the loop over u reads broadcasts instead of a chain of dependent loads.
+    constexpr int kSymChunk = Cfg::SMEM_BYTES / (int)sizeof(int);
+    int* ssym = reinterpret_cast<int*>(smem);
+    for (int c0 = 0; c0 < Un; c0 += kSymChunk) {
+      const int cn = min(kSymChunk, Un - c0);
+      __syncthreads();  // the previous user of smem is done
+      for (int k = threadIdx.x; k < cn; k += blockDim.x) {
+        bool ok = true;
+        ssym[k] = symbol_at(a.b, n, c0 + k, V, ok);
+      }
+      __syncthreads();
+      for (int k = 0; k < cn; ++k) {
+        const int y = ssym[k];
+        if (y < v0 || y >= v0 + Cfg::BN) continue;
+        const int u = c0 + k;
 #pragma unroll
-      for (int j = 0; j < Cfg::FN; ++j) {
-        if (v0 + tile_col<Cfg>(j) != y) continue;
+        for (int j = 0; j < Cfg::FN; ++j) {
+          if (v0 + tile_col<Cfg>(j) != y) continue;
 #pragma unroll
-        for (int i = 0; i < Cfg::FM; ++i)
+          for (int i = 0; i < Cfg::FM; ++i)
 #pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int t = t0 + tile_row<Cfg>(i, r);
-            if (t < Tn) res[i][j][r] -= ks * gxn[(size_t)t * U1 + u];
-          }
+            for (int r = 0; r < 4; ++r) {
+              const int t = t0 + tile_row<Cfg>(i, r);
+              if (t < Tn) res[i][j][r] -= ks * gxn[(size_t)t * U1 + u];
+            }
+        }
       }
     }
     const int blank = a.b.blank;
@@ -603,10 +624,11 @@ hipError_t launch_normalizer(const SimpleArgs& a, hipStream_t s) {
     RNNT_PROF(s, "normalizer");
     hipLaunchKernelGGL(normalizer_kernel, grid, dim3(256), 0, s, a);
   }
-  const size_t L = (size_t)a.b.N * T * U1;
+  // the rectangle's nodes, then the cells of the diagonal-major copies
+  const size_t blocks = ((size_t)a.b.N * T * U1 + 255) / 256 + (size_t)a.b.N * lattice_fill_blocks(T, a.b.U);
   {
     RNNT_PROF(s, "normalizer_epi");
-    hipLaunchKernelGGL(normalizer_epi_kernel, dim3((unsigned)((L + 255) / 256)), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(normalizer_epi_kernel, dim3((unsigned)blocks), dim3(256), 0, s, a);
   }
   return hipGetLastError();
 }
