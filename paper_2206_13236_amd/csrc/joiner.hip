@@ -925,17 +925,25 @@ DEV void tail_wsum(const JoinerArgs& a, int b) {
 }
 
 // db = sum of the column partials written by the d(logits) kernel (one per
-// 64 rows streamed, one per wave row of a GEMM tile recomputed): 4
-// interleaved parts per column, then the parts in order.
+// 64 rows streamed, one per wave row of a GEMM tile recomputed): each wave
+// sums a contiguous quarter of the rows in ascending order, 8 loads in
+// flight, then the quarters in order.
 DEV void tail_dbsum(const JoinerArgs& a, int b, float (*red)[64]) {
   const int c = threadIdx.x & 63, part = threadIdx.x >> 6;
   const int v = b * 64 + c;
   const int M = a.frame_off[a.b.N] * a.S;
   const int rows = a.logits_in ? (M + kDlRows - 1) / kDlRows : CfgF::WGM * ((M + CfgF::BM - 1) / CfgF::BM);
+  const int q = (rows + 3) / 4, r0 = min(rows, part * q), r1 = min(rows, r0 + q);
   float s = 0.f;
   if (v < a.V) {
-#pragma unroll 4
-    for (int r = part; r < rows; r += 4) s += a.db_part[(size_t)r * a.V + v];
+    const float* col = a.db_part + v;
+    for (int r = r0; r < r1; r += 8) {
+      float x[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) x[k] = (r + k < r1) ? col[(size_t)(r + k) * a.V] : 0.f;
+#pragma unroll
+      for (int k = 0; k < 8; ++k) s += x[k];
+    }
   }
   red[part][c] = s;
   __syncthreads();

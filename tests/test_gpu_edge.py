@@ -193,3 +193,53 @@ def test_band_algorithms_on_a_mixed_batch(alg, chunk):
     assert_close("loss", host(r["loss"]), loss_ref, rtol=1e-5)
     assert_close("px_occ", host(r["px_occ"]), gx_ref, atol=1e-4)
     assert_close("py_occ", host(r["py_occ"]), gy_ref, atol=1e-4)
+
+
+@pytest.mark.parametrize("U_range", [(3, 9), (70, 90)])
+def test_nan_inside_the_lattice_gives_nan_for_that_utterance_only(U_range):
+    # a NaN logit at a node of the lattice (one row or more per lane of the
+    # recursion's wave): that utterance's simple loss is NaN, the others
+    # match the oracle on the clean batch
+    b = _small(seed=31, N=4, T_range=(12, 30), U_range=U_range)
+    am, lm = b.am.copy(), b.lm.copy()
+    am[1, min(2, b.t_len[1] - 1), 3] = np.nan
+    lm[2, b.u_len[2] // 2, 5] = np.nan
+    say(f"[edge] NaN inside the lattice, U in {U_range}")
+    batch = make_dev_batch(b)
+    sc = np.full(b.N, 0.5, np.float32)
+    got = P.rnnt_simple_loss(batch, b.V, dev_f32(am), dev_f32(lm), dev_f32(sc), want_grads=True)
+    torch.cuda.synchronize()
+    loss = host(got["loss"])
+    assert np.isnan(loss[1]) and np.isnan(loss[2])
+    good = [0, 3]
+    s1 = O.simple_stage(b.am[good], b.lm[good], b.symbols[good], b.t_len[good], b.u_len[good], b.wl.blank,
+                        scale=sc[good])
+    assert_close("loss", loss[good], s1["loss"], rtol=1e-5)
+    assert_close("px_occ", host(got["px_occ"])[good], s1["gx"], atol=1e-4)
+    assert_close("py_occ", host(got["py_occ"])[good], s1["gy"], atol=1e-4)
+    assert_close("am_grad", host(got["am_grad"])[good], s1["am_grad"], atol=1e-4)
+
+
+@pytest.mark.parametrize("alg,chunk", [("wavefront", 0), ("scan", 0), ("scan", 3)])
+def test_nan_inside_the_band_gives_nan_for_that_utterance_only(alg, chunk):
+    N, T, U, S = 4, 19, 8, 4
+    rng = np.random.default_rng(33)
+    t_len = np.array([19, 14, 9, 17], np.int32)
+    u_len = np.array([8, 5, 3, 6], np.int32)
+    ranges = O.prune_ranges(rng.random((N, T, U + 1)), rng.random((N, T, U + 1)), t_len, u_len, S)
+    px = (-1.0 - np.abs(rng.standard_normal((N, T, S)))).astype(np.float32)
+    py = (-1.0 - np.abs(rng.standard_normal((N, T, S)))).astype(np.float32)
+    loss_ref, gx_ref, gy_ref = O.pruned_loss(px.astype(np.float64), py.astype(np.float64), ranges, t_len, u_len)
+    bad = px.copy()
+    bad[1, 4, 1] = np.nan
+    b = dataclasses.replace(_small(seed=13, N=N, T_range=(T, T), U_range=(U, U), S=S), t_len=t_len, u_len=u_len)
+    say(f"[edge] NaN inside the band, algorithm {alg} chunk {chunk}")
+    batch = make_dev_batch(b)
+    r = P.rnnt_pruned_loss(batch, S, dev_f32(bad), dev_f32(py), dev_i32(ranges), algorithm=alg, chunk=chunk)
+    torch.cuda.synchronize()
+    loss = host(r["loss"])
+    assert np.isnan(loss[1])
+    good = [0, 2, 3]
+    assert_close("loss", loss[good], loss_ref[good], rtol=1e-5)
+    assert_close("px_occ", host(r["px_occ"])[good], gx_ref[good], atol=1e-4)
+    assert_close("py_occ", host(r["py_occ"])[good], gy_ref[good], atol=1e-4)
