@@ -990,24 +990,24 @@ DEV void tail_enc(const JoinerArgs& a, int b) {
   }
 }
 
-// Block b: dec rows u = (b % ceil((U+1)/R)) * R + rr of utterance n = b / ceil((U+1)/R).
-DEV void tail_dec(const JoinerArgs& a, int b, int* sp) {
+// Block b: dec row u = b % (U+1) of utterance n = b / (U+1). The frames
+// whose band holds u are split into contiguous subranges, one per group of
+// J/4 threads (two at J = 512), each summed in ascending t with 8 buffer
+// loads in flight (frames past the subrange read zero); the subranges are
+// then added in order.
+DEV void tail_dec(const JoinerArgs& a, int b, int* sp, float4* red4) {
   const int T = a.b.T, U1 = a.b.U + 1, S = a.S, J = a.J, tpr = J / 4;
-  const int R = encdec_rows_per_block(J);
-  const int ub = (U1 + R - 1) / R;
-  const int n = b / ub;
+  const int nsub = tpr >= kTailThreads ? 1 : kTailThreads / tpr;
+  const int n = b / U1, u = b - n * U1;
   int Tn, Un;
   utt_dims(a.b, n, Tn, Un);
-  for (int t = threadIdx.x; t < Tn; t += kTailThreads) sp[t] = a.ranges[((size_t)n * T + t) * S];
-  __syncthreads();
-  const int rr = threadIdx.x / tpr, c = threadIdx.x - rr * tpr;
-  const int u = (b - n * ub) * R + rr;
-  if (rr >= R || u >= U1) return;
   float4* out = reinterpret_cast<float4*>(a.dec_grad + ((size_t)n * U1 + u) * J);
   if (u > Un) {
-    for (int g = c; g < tpr; g += kTailThreads) out[g] = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int g = threadIdx.x; g < tpr; g += kTailThreads) out[g] = make_float4(0.f, 0.f, 0.f, 0.f);
     return;
   }
+  for (int t = threadIdx.x; t < Tn; t += kTailThreads) sp[t] = a.ranges[((size_t)n * T + t) * S];
+  __syncthreads();
   // p_t is non-decreasing (Eq. (9)), so the frames whose band holds u form
   // the interval [first t with p_t > u - S, first t with p_t > u).
   int lo = 0, hi = Tn;
@@ -1024,20 +1024,37 @@ DEV void tail_dec(const JoinerArgs& a, int b, int* sp) {
     else lo = mid + 1;
   }
   const int t1 = lo;
-  const float4* d = reinterpret_cast<const float4*>(a.dpre);
-  const size_t off = (size_t)a.frame_off[n];
-  for (int g = c; g < tpr; g += kTailThreads) {
+  const int sub = threadIdx.x / tpr, c = threadIdx.x - sub * tpr;
+  const int per = (t1 - t0 + nsub - 1) / nsub;
+  const int ta = min(t1, t0 + sub * per), tb = min(t1, ta + per);
+  // the resource must be uniform (scalar registers): its size is read once
+  const int frames = __builtin_amdgcn_readfirstlane(a.frame_off[a.b.N]);
+  const Rsrc dr = make_rsrc(a.dpre, (size_t)frames * S * J * sizeof(float));
+  const int off = a.frame_off[n];
+  for (int g = c; g < tpr && sub < nsub; g += (nsub == 1 ? kTailThreads : tpr)) {
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-    int t = t0;
-    for (; t + 8 <= t1; t += 8) {  // loads of 8 frames in flight, added in ascending t
+    for (int t = ta; t < tb; t += 8) {
       float4 v[8];
 #pragma unroll
-      for (int k = 0; k < 8; ++k) v[k] = d[((off + t + k) * S + (u - sp[t + k])) * tpr + g];
+      for (int k = 0; k < 8; ++k) {
+        const int tk = min(t + k, tb - 1);
+        const uint32_t o = (uint32_t)((((off + tk) * S + (u - sp[tk])) * J + 4 * g) * (int)sizeof(float));
+        const u32x4 w = __builtin_amdgcn_raw_buffer_load_b128(dr, (int)(t + k < tb ? o : kOob), 0, 0);
+        v[k] = make_float4(__uint_as_float(w.x), __uint_as_float(w.y), __uint_as_float(w.z), __uint_as_float(w.w));
+      }
 #pragma unroll
       for (int k = 0; k < 8; ++k) acc = f4add(acc, v[k]);
     }
-    for (; t < t1; ++t) acc = f4add(acc, d[((off + t) * S + (u - sp[t])) * tpr + g]);
-    out[g] = acc;
+    if (nsub == 1) out[g] = acc;
+    else red4[threadIdx.x] = acc;
+  }
+  if (nsub > 1) {
+    __syncthreads();
+    if (sub == 0) {
+      float4 r = red4[c];
+      for (int q = 1; q < nsub; ++q) r = f4add(r, red4[q * tpr + c]);
+      out[c] = r;
+    }
   }
 }
 
@@ -1048,8 +1065,9 @@ struct TailRanges {
 __global__ __launch_bounds__(kTailThreads) void joiner_tail_kernel(JoinerArgs a, TailRanges r) {
   extern __shared__ int sp[];  // p_t of one utterance (d dec blocks)
   __shared__ float red[4][64];  // db blocks
+  __shared__ float4 red4[kTailThreads];  // d dec subrange sums
   int b = blockIdx.x;
-  if (b < r.dec) { tail_dec(a, b, sp); return; }
+  if (b < r.dec) { tail_dec(a, b, sp, red4); return; }
   b -= r.dec;
   if (b < r.enc) { tail_enc(a, b); return; }
   b -= r.enc;
@@ -1239,7 +1257,7 @@ hipError_t launch_joiner_bwd(const JoinerArgs& a, hipStream_t s) {
   const size_t JV = (size_t)J * V;
   const int R = (J / 4 >= kTailThreads) ? 1 : kTailThreads / (J / 4);
   TailRanges tr;
-  tr.dec = ((a.b.U + 1 + R - 1) / R) * a.b.N;
+  tr.dec = (a.b.U + 1) * a.b.N;
   tr.enc = (a.b.N * a.b.T + R - 1) / R;
   tr.wsum = a.W_grad ? (int)((JV + kTailThreads - 1) / kTailThreads) : 0;
   tr.dbsum = a.bias_grad ? (V + 63) / 64 : 0;
