@@ -216,10 +216,13 @@ JoinerFwdWs joiner_fwd_layout(void* base, int N, int T, int S, int J, int V, int
 
 struct JoinerBwdWs {
   int* frame_off;
+  int* frame_nt;
+  int* frame_p;
   int4* rowinfo;
   void* dl;
   void* dlT;
   float* dpre;
+  float* enc_part;
   void* hbuf;
   float* dw_part;
   float* db_part;
@@ -235,11 +238,14 @@ JoinerBwdWs joiner_bwd_layout(void* base, int N, int T, int S, int J, int V, int
   w.splits = joiner_bwd_splits(J, V);
   w.n_db_rows = joiner_db_rows(N, T, S);
   w.frame_off = c.take<int>((size_t)N + 1);
+  w.frame_nt = c.take<int>((size_t)N * T);
+  w.frame_p = c.take<int>((size_t)N * T);
   w.rowinfo = c.take<int4>(M);
   const size_t dl_elems = (size_t)w.chunk_rows * joiner_ldl(V);
   w.dl = bf16 ? (void*)c.take<uint16_t>(dl_elems) : (void*)c.take<float>(dl_elems);
   w.dlT = bf16 ? (void*)c.take<uint16_t>(dl_elems) : nullptr;
   w.dpre = c.take<float>(M * J);
+  w.enc_part = bf16 ? nullptr : c.take<float>((M + 127) / 128 * 2 * J);
   const size_t h_elems = (size_t)w.chunk_rows * J;
   w.hbuf = bf16 ? (void*)c.take<uint16_t>(h_elems) : (void*)c.take<float>(h_elems);
   w.dw_part = c.take<float>((size_t)w.splits * J * V);
@@ -309,6 +315,8 @@ void set_joiner_bwd(JoinerArgs& a, const JoinerBwdWs& w, const float* lse, const
                     const float* gy, const float* scale, float* enc_grad, float* dec_grad, float* W_grad,
                     float* bias_grad, float* logits_grad) {
   a.frame_off = w.frame_off;
+  a.frame_nt = w.frame_nt;
+  a.frame_p = w.frame_p;
   a.rowinfo = w.rowinfo;
   a.lse_in = lse;
   a.logits_in = logits;
@@ -320,6 +328,7 @@ void set_joiner_bwd(JoinerArgs& a, const JoinerBwdWs& w, const float* lse, const
   a.ldl = joiner_ldl(a.V);
   a.chunk_rows = w.chunk_rows;
   a.dpre = w.dpre;
+  a.enc_part = w.enc_part;
   a.hbuf = w.hbuf;
   a.dw_part = w.dw_part;
   a.splits = w.splits;

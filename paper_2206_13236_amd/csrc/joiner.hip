@@ -150,6 +150,8 @@ DEV void raw_to_float(const RawVec<TIn, N>& r, float (&v)[N]) {
   }
 }
 
+DEV float4 f4add(float4 a, float4 b) { return make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w); }
+
 // ---------------------------------------------------------------------------
 // Operand sources
 // ---------------------------------------------------------------------------
@@ -351,6 +353,10 @@ __global__ __launch_bounds__(256) void joiner_prep_kernel(JoinerArgs a) {
   const int t = i / S, s = i - t * S;
   const size_t nts = ((size_t)n * T + t) * S + s;
   const int u = a.ranges[nts];
+  if (s == 0 && a.frame_nt) {
+    a.frame_nt[off + t] = n * T + t;
+    a.frame_p[off + t] = u;
+  }
   int4 r;
   if (u >= 0 && u <= Un) {
     bool ok = true;
@@ -715,6 +721,110 @@ __global__ __launch_bounds__(kDlThreads) void joiner_dl_kernel(JoinerArgs a, int
 }
 
 // ---------------------------------------------------------------------------
+// d enc and d dec pieces of one row tile of dpre (fp32 joiner), formed from
+// the tile in LDS so that dpre never goes to HBM. Rows are (frame, slot)
+// pairs, S per frame, frames of the batch in order; slot s of frame (n, t)
+// is node u = p_t + s.
+//   d enc: a frame whose S rows all lie in the tile is summed (ascending s)
+//          straight into enc_grad; a frame cut by the tile's first or last
+//          row leaves its piece in enc_part[tile][0 (cut at the start) or
+//          1], for the tail to add the pieces in tile order.
+//   d dec: the rows of one u in the tile (one per frame, slot decreasing as
+//          p_t grows) are summed in ascending t into the row of dpre of the
+//          first of them; the tail adds those pieces of u in tile order.
+// ---------------------------------------------------------------------------
+constexpr int kTileFrames = 130;  // frames a 128-row tile can touch (S = 1: 128; plus cut ends)
+
+// Frames [fa, fa + nf) touched by rows [m0, mt_end) of a tile.
+DEV void tile_frames(int m0, int mt_end, int S, int& fa, int& nf) {
+  fa = m0 / S;
+  nf = (mt_end - 1) / S - fa + 1;
+}
+
+// Thread k < nf: frame_nt and frame_p of frame fa + k, loaded before the
+// main loop so that their latency hides under it.
+struct TileFrameRegs {
+  int nt, p;
+};
+DEV TileFrameRegs tile_frames_fetch(const JoinerArgs& a, int m0, int mend, int bm) {
+  int fa, nf;
+  tile_frames(m0, min(m0 + bm, mend), a.S, fa, nf);
+  TileFrameRegs r{0, 0};
+  if ((int)threadIdx.x < nf) {
+    r.nt = a.frame_nt[fa + threadIdx.x];
+    r.p = a.frame_p[fa + threadIdx.x];
+  }
+  return r;
+}
+
+template <class Cfg>
+DEV void tile_enc_dec(const JoinerArgs& a, const float* C, int LDC, int m0, int mend, int j0, const int4* ri,
+                      TileFrameRegs fr) {
+  static_assert(Cfg::NT >= kTileFrames && Cfg::NT >= Cfg::BM, "one thread per frame and per row of the tile");
+  __shared__ int fr_nt[kTileFrames], fr_n[kTileFrames], fr_p[kTileFrames];
+  __shared__ int16_t next_row[Cfg::BM];  // tile row of the next frame's row of the same u, or -1
+  __shared__ int16_t first_row[Cfg::BM];  // rows that start a d dec piece (any order)
+  __shared__ int n_first;
+  const int S = a.S, J = a.J, T = a.b.T;
+  const int mt_end = min(m0 + Cfg::BM, mend);  // rows [m0, mt_end) of the tile
+  const int rows = mt_end - m0;
+  int fa, nf;
+  tile_frames(m0, mt_end, S, fa, nf);
+  if ((int)threadIdx.x < nf) {
+    fr_nt[threadIdx.x] = fr.nt;
+    fr_n[threadIdx.x] = fr.nt / T;
+    fr_p[threadIdx.x] = fr.p;
+  }
+  if (threadIdx.x == 0) n_first = 0;
+  __syncthreads();
+  // one thread per row: is it the first row of its u in the tile (the
+  // previous frame's row of u, slot u - p_{t-1}, is absent, of another
+  // utterance or before the tile), and which row of the tile comes next
+  if ((int)threadIdx.x < rows && ri[threadIdx.x].w >= 0) {
+    const int r = threadIdx.x, m = m0 + r, f = m / S, s = m - f * S, k = f - fa;
+    const int n = fr_n[k], u = fr_p[k] + s;
+    bool first = true;
+    if (k > 0 && fr_n[k - 1] == n) {
+      const int sp = u - fr_p[k - 1];
+      first = !(sp < S && r - s - S + sp >= 0);
+    }
+    int nx = -1;
+    if (k + 1 < nf && fr_n[k + 1] == n) {
+      const int s2 = u - fr_p[k + 1], r2 = r - s + S + s2;
+      if (s2 >= 0 && r2 < rows) nx = r2;
+    }
+    next_row[r] = (int16_t)nx;
+    if (first) first_row[atomicAdd(&n_first, 1)] = (int16_t)r;
+  }
+  __syncthreads();
+  constexpr int CG = Cfg::BN / 4;  // 4-column groups
+  const int tile = m0 / Cfg::BM;
+  // d enc
+  for (int it = threadIdx.x; it < nf * CG; it += Cfg::NT) {
+    const int k = it / CG, cg = it - k * CG, jj = j0 + 4 * cg;
+    if (jj >= J) continue;
+    const int fs = (fa + k) * S, r0 = max(fs, m0), r1 = min(fs + S, mt_end);
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int m = r0; m < r1; ++m) acc = f4add(acc, *reinterpret_cast<const float4*>(C + (m - m0) * LDC + 4 * cg));
+    float* dst;
+    if (fs >= m0 && fs + S <= mt_end) dst = a.enc_grad + (size_t)fr_nt[k] * J + jj;
+    else dst = a.enc_part + ((size_t)tile * 2 + (fs <= m0 ? 0 : 1)) * J + jj;
+    *reinterpret_cast<float4*>(dst) = acc;
+  }
+  // d dec: each piece's rows in ascending t, into the row of its first one
+  const int nfirst = n_first;
+  for (int it = threadIdx.x; it < nfirst * CG; it += Cfg::NT) {
+    const int i = it / CG, cg = it - i * CG, jj = j0 + 4 * cg;
+    if (jj >= J) continue;
+    const int r = first_row[i];
+    float4 acc = *reinterpret_cast<const float4*>(C + r * LDC + 4 * cg);
+    for (int r2 = next_row[r]; r2 >= 0; r2 = next_row[r2])
+      acc = f4add(acc, *reinterpret_cast<const float4*>(C + r2 * LDC + 4 * cg));
+    *reinterpret_cast<float4*>(a.dpre + (size_t)(m0 + r) * J + jj) = acc;
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Backward 2: dh = dl W^T, dpre = dh (1 - h^2); also leaves h of the chunk's
 // rows in hbuf (zero for absent slots) as the dW contraction's operand:
 // [rows, J] for fp32, transposed [J, chunk_rows] for bf16.
@@ -741,6 +851,8 @@ __global__ __launch_bounds__(kGemmThreads, 4) void joiner_dh_kernel(JoinerArgs a
   WtSrcKC<Cfg, TIn, WM> sb(a, j0);
   KCLoader<Cfg, Cfg::BM, DlSrcKC<Cfg>> la(sa);
   KCLoader<Cfg, Cfg::BN, WtSrcKC<Cfg, TIn, WM>> lb(sb);
+  TileFrameRegs fr{0, 0};
+  if constexpr (!BF) fr = tile_frames_fetch(a, m0, mend, Cfg::BM);
   floatx4 acc[Cfg::FM][Cfg::FN];
   gemm_mainloop<Cfg>(la, lb, 0, V, smem, acc);
 
@@ -778,15 +890,20 @@ __global__ __launch_bounds__(kGemmThreads, 4) void joiner_dh_kernel(JoinerArgs a
       h[q] = on ? fast_tanh(fe[q] + fd[q]) : 0.f;
       dp[q] = on ? cr[q] * (1.f - h[q] * h[q]) : 0.f;
     }
-    if (m < mend) {
-      *reinterpret_cast<float4*>(a.dpre + (size_t)m * J + jj) = make_float4(dp[0], dp[1], dp[2], dp[3]);
-      if constexpr (!BF)  // h [rows, J] for the fp32 dW
-        *reinterpret_cast<float4*>(hbuf + (size_t)(m - cm0) * J + jj) = make_float4(h[0], h[1], h[2], h[3]);
-    }
     if constexpr (BF) {
+      if (m < mend) *reinterpret_cast<float4*>(a.dpre + (size_t)m * J + jj) = make_float4(dp[0], dp[1], dp[2], dp[3]);
 #pragma unroll
       for (int q = 0; q < 4; ++q) cr[q] = h[q];  // h back to the tile (0 past mend) for the transposed store
+    } else {
+      // h [rows, J] for the fp32 dW; dpre stays in the tile for the d enc / d dec pieces
+      if (m < mend) *reinterpret_cast<float4*>(hbuf + (size_t)(m - cm0) * J + jj) = make_float4(h[0], h[1], h[2], h[3]);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) cr[q] = dp[q];
     }
+  }
+  if constexpr (!BF) {
+    __syncthreads();
+    tile_enc_dec<Cfg>(a, C, LDC, m0, mend, j0, ri, fr);
   }
   if constexpr (BF) {
     // h^T [J, chunk_rows] for the bf16 dW: the lane's 4 consecutive rows of
@@ -958,7 +1075,6 @@ DEV int encdec_rows_per_block(int J) {
   return tpr >= kTailThreads ? 1 : kTailThreads / tpr;
 }
 
-DEV float4 f4add(float4 a, float4 b) { return make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w); }
 
 DEV void tail_enc(const JoinerArgs& a, int b) {
   const int T = a.b.T, S = a.S, J = a.J, tpr = J / 4;
@@ -1058,6 +1174,99 @@ DEV void tail_dec(const JoinerArgs& a, int b, int* sp, float4* red4) {
   }
 }
 
+// fp32 joiner: d enc and d dec from the pieces the dh kernel left (see
+// tile_enc_dec). d enc: frames cut by a row tile add their pieces in tile
+// order (the others are already written); zero rows past T_n.
+constexpr int kTileRows = CfgF::BM;
+
+DEV void tail_enc_pieces(const JoinerArgs& a, int b) {
+  const int T = a.b.T, S = a.S, J = a.J, tpr = J / 4;
+  const int R = encdec_rows_per_block(J);
+  const int rr = threadIdx.x / tpr, c = threadIdx.x - rr * tpr;
+  const int row = b * R + rr;  // n * T + t
+  if (rr >= R || row >= a.b.N * T) return;
+  const int n = row / T, t = row - n * T;
+  int Tn, Un;
+  utt_dims(a.b, n, Tn, Un);
+  float4* out = reinterpret_cast<float4*>(a.enc_grad + (size_t)row * J);
+  if (t >= Tn) {
+    for (int g = c; g < tpr; g += kTailThreads) out[g] = make_float4(0.f, 0.f, 0.f, 0.f);
+    return;
+  }
+  const int fs = (a.frame_off[n] + t) * S, ia = fs / kTileRows, ib = (fs + S - 1) / kTileRows;
+  if (ia == ib) return;  // the frame lies in one tile: written by the dh kernel
+  for (int g = c; g < tpr; g += kTailThreads) {
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int i = ia; i <= ib; ++i)
+      acc = f4add(acc, reinterpret_cast<const float4*>(a.enc_part + ((size_t)i * 2 + (fs <= i * kTileRows ? 0 : 1)) * J)[g]);
+    out[g] = acc;
+  }
+}
+
+// d dec[n, u]: the pieces of u, one per row tile that holds rows of u, each
+// in the row of dpre of its first row (ascending t). The row of u in frame t,
+// m_t = (frame_off[n] + t) S + u - p_t, grows with t (p_{t+1} - p_t < S while
+// u stays in the band), so the first frame of each tile is found by a binary
+// search; the pieces are loaded 8 at a time and added in tile order.
+DEV void tail_dec_pieces(const JoinerArgs& a, int b, int* sp) {
+  const int T = a.b.T, U1 = a.b.U + 1, S = a.S, J = a.J, tpr = J / 4;
+  const int n = b / U1, u = b - n * U1;
+  int Tn, Un;
+  utt_dims(a.b, n, Tn, Un);
+  float4* out = reinterpret_cast<float4*>(a.dec_grad + ((size_t)n * U1 + u) * J);
+  if (u > Un) {
+    for (int g = threadIdx.x; g < tpr; g += kTailThreads) out[g] = make_float4(0.f, 0.f, 0.f, 0.f);
+    return;
+  }
+  for (int t = threadIdx.x; t < Tn; t += kTailThreads) sp[t] = a.ranges[((size_t)n * T + t) * S];
+  __syncthreads();
+  int lo = 0, hi = Tn;
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    if (sp[mid] > u - S) hi = mid;
+    else lo = mid + 1;
+  }
+  const int t0 = lo;
+  hi = Tn;
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    if (sp[mid] > u) hi = mid;
+    else lo = mid + 1;
+  }
+  const int t1 = lo;
+  const int off = a.frame_off[n];
+  auto row_of = [&](int t) { return (off + t) * S + u - sp[t]; };
+  const int frames = __builtin_amdgcn_readfirstlane(a.frame_off[a.b.N]);  // keeps the resource scalar
+  const Rsrc dr = make_rsrc(a.dpre, (size_t)frames * S * J * sizeof(float));
+  const int ia = t1 > t0 ? row_of(t0) / kTileRows : 0, ib = t1 > t0 ? row_of(t1 - 1) / kTileRows : -1;
+  for (int g = threadIdx.x; g < tpr; g += kTailThreads) {
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int i0 = ia; i0 <= ib; i0 += 8) {
+      float4 v[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const int i = i0 + k;
+        int t = t0;
+        if (i > ia && i <= ib) {  // first frame whose row of u lies in tile i
+          int l = t0, h = t1 - 1;
+          while (l < h) {
+            const int mid = (l + h) >> 1;
+            if (row_of(mid) >= i * kTileRows) h = mid;
+            else l = mid + 1;
+          }
+          t = l;
+        }
+        const uint32_t o = (uint32_t)(((size_t)row_of(t) * J + 4 * g) * sizeof(float));
+        const u32x4 w = __builtin_amdgcn_raw_buffer_load_b128(dr, (int)(i <= ib ? o : kOob), 0, 0);
+        v[k] = make_float4(__uint_as_float(w.x), __uint_as_float(w.y), __uint_as_float(w.z), __uint_as_float(w.w));
+      }
+#pragma unroll
+      for (int k = 0; k < 8; ++k) acc = f4add(acc, v[k]);
+    }
+    out[g] = acc;
+  }
+}
+
 struct TailRanges {
   int dec, enc, wsum, dbsum;  // block counts, in launch order
 };
@@ -1067,9 +1276,18 @@ __global__ __launch_bounds__(kTailThreads) void joiner_tail_kernel(JoinerArgs a,
   __shared__ float red[4][64];  // db blocks
   __shared__ float4 red4[kTailThreads];  // d dec subrange sums
   int b = blockIdx.x;
-  if (b < r.dec) { tail_dec(a, b, sp, red4); return; }
+  const bool pieces = a.enc_part != nullptr;  // fp32 joiner: dpre stayed in the dh tiles
+  if (b < r.dec) {
+    if (pieces) tail_dec_pieces(a, b, sp);
+    else tail_dec(a, b, sp, red4);
+    return;
+  }
   b -= r.dec;
-  if (b < r.enc) { tail_enc(a, b); return; }
+  if (b < r.enc) {
+    if (pieces) tail_enc_pieces(a, b);
+    else tail_enc(a, b);
+    return;
+  }
   b -= r.enc;
   if (b < r.wsum) { tail_wsum(a, b); return; }
   b -= r.wsum;

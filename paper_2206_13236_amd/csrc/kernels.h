@@ -119,7 +119,8 @@ struct JoinerArgs {
   const void* bias;    // [V] or null
   const int* ranges;   // [N, T, S]
   int* frame_off;      // ws [N+1]
-  int* frame_map;      // ws [N*T]
+  int* frame_nt;       // ws [N*T] (backward only, else null): n*T + t of the f-th frame of the batch
+  int* frame_p;        //                                    and its band start p_t
   int4* rowinfo;       // ws [N*T*S]: enc_off, dec_off, sym (-1: none), out index (-1: absent)
   // forward
   float2* part;        // ws [N*T*S, nparts] (max, sum exp) per 64-column slice
@@ -140,7 +141,8 @@ struct JoinerArgs {
   int ldl;
   void* dlT;           // ws chunk [ldl, chunk_rows] (bf16 only): d(logits) transposed for dW
   int chunk_rows;
-  float* dpre;         // ws [N*T*S, J]
+  float* dpre;         // ws [N*T*S, J]: dpre rows (bf16 joiner); fp32 joiner: the d dec pieces below
+  float* enc_part;     // ws [ceil(N*T*S/128), 2, J] (fp32 joiner): d enc pieces of frames split by a row tile
   void* hbuf;          // ws chunk [chunk_rows, J] (f32 or bf16): h = tanh(enc + dec) of the chunk's rows
                        // (forward and recomputed backward: written by the h kernel; backward: by dh)
   float* dw_part;      // ws [splits, J, V]
