@@ -245,7 +245,7 @@ JoinerBwdWs joiner_bwd_layout(void* base, int N, int T, int S, int J, int V, int
   w.dl = bf16 ? (void*)c.take<uint16_t>(dl_elems) : (void*)c.take<float>(dl_elems);
   w.dlT = bf16 ? (void*)c.take<uint16_t>(dl_elems) : nullptr;
   w.dpre = c.take<float>(M * J);
-  w.enc_part = bf16 ? nullptr : c.take<float>((M + 127) / 128 * 2 * J);
+  w.enc_part = c.take<float>((M + 127) / 128 * 2 * J);
   const size_t h_elems = (size_t)w.chunk_rows * J;
   w.hbuf = bf16 ? (void*)c.take<uint16_t>(h_elems) : (void*)c.take<float>(h_elems);
   w.dw_part = c.take<float>((size_t)w.splits * J * V);

@@ -22,10 +22,13 @@
 //      backward) from the stored logits by a streaming kernel, or, without
 //      them, by recomputing h and the logits GEMM; write the chunk and column
 //      sums (db);
-//   2. dh = dl W^T, dpre = dh (1 - h^2)  (tanh backward);
+//   2. dh = dl W^T, dpre = dh (1 - h^2)  (tanh backward), kept in LDS: the
+//      epilogue sums it into d enc[n,t] = sum_s dpre(row(t,s)) for the frames
+//      inside the 128-row tile, and into per-tile pieces of the frames the
+//      tile cuts and of d dec[n,u] = sum over the (t,s) with p_t + s = u;
 //   3. dW += h^T dl with split-K partial sums;
-// then d enc[n,t] = sum_s dpre(row(t,s)), d dec[n,u] = sum over the (t,s)
-// with p_t + s = u, dW and db summed over their partials, all in a fixed order.
+// then a tail kernel adds the d enc / d dec pieces in tile order and sums dW
+// and db over their partials, all in a fixed order.
 #include "gemm.h"
 #include "kernels.h"
 #include "prof.h"
@@ -721,8 +724,8 @@ __global__ __launch_bounds__(kDlThreads) void joiner_dl_kernel(JoinerArgs a, int
 }
 
 // ---------------------------------------------------------------------------
-// d enc and d dec pieces of one row tile of dpre (fp32 joiner), formed from
-// the tile in LDS so that dpre never goes to HBM. Rows are (frame, slot)
+// d enc and d dec pieces of one row tile of dpre, formed from the tile in
+// LDS so that dpre never goes to HBM. Rows are (frame, slot)
 // pairs, S per frame, frames of the batch in order; slot s of frame (n, t)
 // is node u = p_t + s.
 //   d enc: a frame whose S rows all lie in the tile is summed (ascending s)
@@ -825,9 +828,10 @@ DEV void tile_enc_dec(const JoinerArgs& a, const float* C, int LDC, int m0, int 
 }
 
 // ---------------------------------------------------------------------------
-// Backward 2: dh = dl W^T, dpre = dh (1 - h^2); also leaves h of the chunk's
-// rows in hbuf (zero for absent slots) as the dW contraction's operand:
-// [rows, J] for fp32, transposed [J, chunk_rows] for bf16.
+// Backward 2: dh = dl W^T, dpre = dh (1 - h^2), summed into the d enc / d dec
+// pieces in LDS; also leaves h of the chunk's rows in hbuf (zero for absent
+// slots) as the dW contraction's operand: [rows, J] for fp32, transposed
+// [J, chunk_rows] for bf16.
 // ---------------------------------------------------------------------------
 template <bool BF, int WM>
 __global__ __launch_bounds__(kGemmThreads, 4) void joiner_dh_kernel(JoinerArgs a, int cm0, int cm1) {
@@ -851,8 +855,7 @@ __global__ __launch_bounds__(kGemmThreads, 4) void joiner_dh_kernel(JoinerArgs a
   WtSrcKC<Cfg, TIn, WM> sb(a, j0);
   KCLoader<Cfg, Cfg::BM, DlSrcKC<Cfg>> la(sa);
   KCLoader<Cfg, Cfg::BN, WtSrcKC<Cfg, TIn, WM>> lb(sb);
-  TileFrameRegs fr{0, 0};
-  if constexpr (!BF) fr = tile_frames_fetch(a, m0, mend, Cfg::BM);
+  const TileFrameRegs fr = tile_frames_fetch(a, m0, mend, Cfg::BM);
   floatx4 acc[Cfg::FM][Cfg::FN];
   gemm_mainloop<Cfg>(la, lb, 0, V, smem, acc);
 
@@ -872,9 +875,15 @@ __global__ __launch_bounds__(kGemmThreads, 4) void joiner_dh_kernel(JoinerArgs a
       for (int r = 0; r < 4; ++r) C[tile_row<Cfg>(i, r) * LDC + tile_col<Cfg>(j)] = acc[i][j][r];
   __syncthreads();
   const EncDec<TIn> ed(a);
-  for (int it = threadIdx.x; it < Cfg::BM * Cfg::BN / 4; it += Cfg::NT) {
+  constexpr int NIT = Cfg::BM * Cfg::BN / 4 / Cfg::NT;  // 4-column groups per thread
+  static_assert(Cfg::BM * Cfg::BN / 4 % Cfg::NT == 0, "whole groups per thread");
+  float4 hk[BF ? NIT : 1];  // bf16: h of this thread's groups, back to the tile after the d enc / d dec pieces
+#pragma unroll
+  for (int q8 = 0; q8 < NIT; ++q8) {
+    const int it = threadIdx.x + q8 * Cfg::NT;
     const int row = it / (Cfg::BN / 4), cg = it - row * (Cfg::BN / 4);
     const int m = m0 + row, jj = j0 + cg * 4;
+    if constexpr (BF) hk[q8] = make_float4(0.f, 0.f, 0.f, 0.f);
     if (jj >= J) continue;  // J is a multiple of 8: the group is all in or all out
     float* cr = C + row * LDC + cg * 4;
     const int4 info = ri[row];  // absent (w < 0) for rows past mend
@@ -891,23 +900,27 @@ __global__ __launch_bounds__(kGemmThreads, 4) void joiner_dh_kernel(JoinerArgs a
       dp[q] = on ? cr[q] * (1.f - h[q] * h[q]) : 0.f;
     }
     if constexpr (BF) {
-      if (m < mend) *reinterpret_cast<float4*>(a.dpre + (size_t)m * J + jj) = make_float4(dp[0], dp[1], dp[2], dp[3]);
-#pragma unroll
-      for (int q = 0; q < 4; ++q) cr[q] = h[q];  // h back to the tile (0 past mend) for the transposed store
+      hk[q8] = make_float4(h[0], h[1], h[2], h[3]);
     } else {
-      // h [rows, J] for the fp32 dW; dpre stays in the tile for the d enc / d dec pieces
+      // h [rows, J] for the fp32 dW
       if (m < mend) *reinterpret_cast<float4*>(hbuf + (size_t)(m - cm0) * J + jj) = make_float4(h[0], h[1], h[2], h[3]);
-#pragma unroll
-      for (int q = 0; q < 4; ++q) cr[q] = dp[q];
     }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) cr[q] = dp[q];  // dpre stays in the tile for the d enc / d dec pieces
   }
-  if constexpr (!BF) {
-    __syncthreads();
-    tile_enc_dec<Cfg>(a, C, LDC, m0, mend, j0, ri, fr);
-  }
+  __syncthreads();
+  tile_enc_dec<Cfg>(a, C, LDC, m0, mend, j0, ri, fr);
   if constexpr (BF) {
-    // h^T [J, chunk_rows] for the bf16 dW: the lane's 4 consecutive rows of
-    // the MFMA layout as one 8-byte store
+    // h back to the tile (0 past mend), then h^T [J, chunk_rows] for the
+    // bf16 dW: the lane's 4 consecutive rows of the MFMA layout as one
+    // 8-byte store
+    __syncthreads();
+#pragma unroll
+    for (int q8 = 0; q8 < NIT; ++q8) {
+      const int it = threadIdx.x + q8 * Cfg::NT;
+      const int row = it / (Cfg::BN / 4), cg = it - row * (Cfg::BN / 4);
+      *reinterpret_cast<float4*>(C + row * LDC + cg * 4) = hk[q8];
+    }
     __syncthreads();
 #pragma unroll
     for (int i = 0; i < Cfg::FM; ++i)
@@ -1025,7 +1038,7 @@ __global__ __launch_bounds__(kGemmThreads, 4) void joiner_dw_kernel(JoinerArgs a
 }
 
 // The tail of the backward: dW and db summed from their partials, d enc and
-// d dec reduced from dpre. Four independent, latency-bound reductions, run as
+// d dec from their pieces. Four independent, latency-bound reductions, run as
 // one launch whose block ranges take one part each (d dec, d enc, dW, db), so
 // that their memory latencies overlap.
 constexpr int kTailThreads = 256;
@@ -1067,117 +1080,17 @@ DEV void tail_dbsum(const JoinerArgs& a, int b, float (*red)[64]) {
   if (part == 0 && v < a.V) a.bias_grad[v] = ((red[0][c] + red[1][c]) + red[2][c]) + red[3][c];
 }
 
-// d enc[n,t] = sum_s dpre(row(t,s)); d dec[n,u] = sum over t of dpre(row(t, u - p_t))
-// for 0 <= u - p_t < S. Threads over float4 column groups of J, several
-// output rows per block; every sum runs in ascending s or t.
+// d enc rows per block: threads over float4 column groups of J.
 DEV int encdec_rows_per_block(int J) {
   const int tpr = J / 4;
   return tpr >= kTailThreads ? 1 : kTailThreads / tpr;
 }
 
 
-DEV void tail_enc(const JoinerArgs& a, int b) {
-  const int T = a.b.T, S = a.S, J = a.J, tpr = J / 4;
-  const int R = encdec_rows_per_block(J);
-  const int rr = threadIdx.x / tpr, c = threadIdx.x - rr * tpr;
-  const int row = b * R + rr;  // n * T + t
-  if (rr >= R || row >= a.b.N * T) return;
-  const int n = row / T, t = row - n * T;
-  int Tn, Un;
-  utt_dims(a.b, n, Tn, Un);
-  for (int g = c; g < tpr; g += kTailThreads) {  // one pass unless J > 1024
-    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (t < Tn) {
-      // batches of 8 slots with every load of a batch in flight together
-      // (slots past S add zero); sums in ascending s
-      const float4* d = reinterpret_cast<const float4*>(a.dpre + (size_t)(a.frame_off[n] + t) * S * J) + g;
-      for (int q = 0; q < S; q += 8) {
-        float4 v[8];
-#pragma unroll
-        for (int k = 0; k < 8; ++k) {
-          const float4 x = d[(size_t)min(q + k, S - 1) * tpr];  // always a valid row
-          v[k] = (q + k < S) ? x : make_float4(0.f, 0.f, 0.f, 0.f);
-        }
-#pragma unroll
-        for (int k = 0; k < 8; ++k) acc = f4add(acc, v[k]);
-      }
-    }
-    reinterpret_cast<float4*>(a.enc_grad + (size_t)row * J)[g] = acc;
-  }
-}
-
-// Block b: dec row u = b % (U+1) of utterance n = b / (U+1). The frames
-// whose band holds u are split into contiguous subranges, one per group of
-// J/4 threads (two at J = 512), each summed in ascending t with 8 buffer
-// loads in flight (frames past the subrange read zero); the subranges are
-// then added in order.
-DEV void tail_dec(const JoinerArgs& a, int b, int* sp, float4* red4) {
-  const int T = a.b.T, U1 = a.b.U + 1, S = a.S, J = a.J, tpr = J / 4;
-  const int nsub = tpr >= kTailThreads ? 1 : kTailThreads / tpr;
-  const int n = b / U1, u = b - n * U1;
-  int Tn, Un;
-  utt_dims(a.b, n, Tn, Un);
-  float4* out = reinterpret_cast<float4*>(a.dec_grad + ((size_t)n * U1 + u) * J);
-  if (u > Un) {
-    for (int g = threadIdx.x; g < tpr; g += kTailThreads) out[g] = make_float4(0.f, 0.f, 0.f, 0.f);
-    return;
-  }
-  for (int t = threadIdx.x; t < Tn; t += kTailThreads) sp[t] = a.ranges[((size_t)n * T + t) * S];
-  __syncthreads();
-  // p_t is non-decreasing (Eq. (9)), so the frames whose band holds u form
-  // the interval [first t with p_t > u - S, first t with p_t > u).
-  int lo = 0, hi = Tn;
-  while (lo < hi) {
-    const int mid = (lo + hi) >> 1;
-    if (sp[mid] > u - S) hi = mid;
-    else lo = mid + 1;
-  }
-  const int t0 = lo;
-  hi = Tn;
-  while (lo < hi) {
-    const int mid = (lo + hi) >> 1;
-    if (sp[mid] > u) hi = mid;
-    else lo = mid + 1;
-  }
-  const int t1 = lo;
-  const int sub = threadIdx.x / tpr, c = threadIdx.x - sub * tpr;
-  const int per = (t1 - t0 + nsub - 1) / nsub;
-  const int ta = min(t1, t0 + sub * per), tb = min(t1, ta + per);
-  // the resource must be uniform (scalar registers): its size is read once
-  const int frames = __builtin_amdgcn_readfirstlane(a.frame_off[a.b.N]);
-  const Rsrc dr = make_rsrc(a.dpre, (size_t)frames * S * J * sizeof(float));
-  const int off = a.frame_off[n];
-  for (int g = c; g < tpr && sub < nsub; g += (nsub == 1 ? kTailThreads : tpr)) {
-    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-    for (int t = ta; t < tb; t += 8) {
-      float4 v[8];
-#pragma unroll
-      for (int k = 0; k < 8; ++k) {
-        const int tk = min(t + k, tb - 1);
-        const uint32_t o = (uint32_t)((((off + tk) * S + (u - sp[tk])) * J + 4 * g) * (int)sizeof(float));
-        const u32x4 w = __builtin_amdgcn_raw_buffer_load_b128(dr, (int)(t + k < tb ? o : kOob), 0, 0);
-        v[k] = make_float4(__uint_as_float(w.x), __uint_as_float(w.y), __uint_as_float(w.z), __uint_as_float(w.w));
-      }
-#pragma unroll
-      for (int k = 0; k < 8; ++k) acc = f4add(acc, v[k]);
-    }
-    if (nsub == 1) out[g] = acc;
-    else red4[threadIdx.x] = acc;
-  }
-  if (nsub > 1) {
-    __syncthreads();
-    if (sub == 0) {
-      float4 r = red4[c];
-      for (int q = 1; q < nsub; ++q) r = f4add(r, red4[q * tpr + c]);
-      out[c] = r;
-    }
-  }
-}
-
-// fp32 joiner: d enc and d dec from the pieces the dh kernel left (see
-// tile_enc_dec). d enc: frames cut by a row tile add their pieces in tile
-// order (the others are already written); zero rows past T_n.
-constexpr int kTileRows = CfgF::BM;
+// d enc and d dec from the pieces the dh kernel left (see tile_enc_dec).
+// d enc: frames cut by a row tile add their pieces in tile order (the others
+// are already written); zero rows past T_n.
+constexpr int kTileRows = CfgF::BM;  // the dh row tile (both configurations)
 
 DEV void tail_enc_pieces(const JoinerArgs& a, int b) {
   const int T = a.b.T, S = a.S, J = a.J, tpr = J / 4;
@@ -1274,20 +1187,10 @@ struct TailRanges {
 __global__ __launch_bounds__(kTailThreads) void joiner_tail_kernel(JoinerArgs a, TailRanges r) {
   extern __shared__ int sp[];  // p_t of one utterance (d dec blocks)
   __shared__ float red[4][64];  // db blocks
-  __shared__ float4 red4[kTailThreads];  // d dec subrange sums
   int b = blockIdx.x;
-  const bool pieces = a.enc_part != nullptr;  // fp32 joiner: dpre stayed in the dh tiles
-  if (b < r.dec) {
-    if (pieces) tail_dec_pieces(a, b, sp);
-    else tail_dec(a, b, sp, red4);
-    return;
-  }
+  if (b < r.dec) { tail_dec_pieces(a, b, sp); return; }
   b -= r.dec;
-  if (b < r.enc) {
-    if (pieces) tail_enc_pieces(a, b);
-    else tail_enc(a, b);
-    return;
-  }
+  if (b < r.enc) { tail_enc_pieces(a, b); return; }
   b -= r.enc;
   if (b < r.wsum) { tail_wsum(a, b); return; }
   b -= r.wsum;

@@ -141,8 +141,8 @@ struct JoinerArgs {
   int ldl;
   void* dlT;           // ws chunk [ldl, chunk_rows] (bf16 only): d(logits) transposed for dW
   int chunk_rows;
-  float* dpre;         // ws [N*T*S, J]: dpre rows (bf16 joiner); fp32 joiner: the d dec pieces below
-  float* enc_part;     // ws [ceil(N*T*S/128), 2, J] (fp32 joiner): d enc pieces of frames split by a row tile
+  float* dpre;         // ws [N*T*S, J]: the d dec pieces, each in the row of dpre of its first row
+  float* enc_part;     // ws [ceil(N*T*S/128), 2, J]: d enc pieces of frames cut by a 128-row tile
   void* hbuf;          // ws chunk [chunk_rows, J] (f32 or bf16): h = tanh(enc + dec) of the chunk's rows
                        // (forward and recomputed backward: written by the h kernel; backward: by dh)
   float* dw_part;      // ws [splits, J, V]
