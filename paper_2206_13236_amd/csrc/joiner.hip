@@ -1055,15 +1055,19 @@ DEV void tail_wsum(const JoinerArgs& a, int b) {
 }
 
 // db = sum of the column partials written by the d(logits) kernel (one per
-// 64 rows streamed, one per wave row of a GEMM tile recomputed): each wave
-// sums a contiguous quarter of the rows in ascending order, 8 loads in
-// flight, then the quarters in order.
-DEV void tail_dbsum(const JoinerArgs& a, int b, float (*red)[64]) {
-  const int c = threadIdx.x & 63, part = threadIdx.x >> 6;
-  const int v = b * 64 + c;
+// 64 rows streamed, one per wave row of a GEMM tile recomputed): a block takes
+// 16 columns; each of its 16 thread groups sums a contiguous sixteenth of the
+// rows in ascending order, 8 loads in flight, then the sixteenths are added
+// in order.
+constexpr int kDbCols = 16;
+
+DEV void tail_dbsum(const JoinerArgs& a, int b, float (*red)[kDbCols]) {
+  const int c = threadIdx.x % kDbCols, part = threadIdx.x / kDbCols;  // 16 parts
+  constexpr int kParts = kTailThreads / kDbCols;
+  const int v = b * kDbCols + c;
   const int M = a.frame_off[a.b.N] * a.S;
   const int rows = a.logits_in ? (M + kDlRows - 1) / kDlRows : CfgF::WGM * ((M + CfgF::BM - 1) / CfgF::BM);
-  const int q = (rows + 3) / 4, r0 = min(rows, part * q), r1 = min(rows, r0 + q);
+  const int q = (rows + kParts - 1) / kParts, r0 = min(rows, part * q), r1 = min(rows, r0 + q);
   float s = 0.f;
   if (v < a.V) {
     const float* col = a.db_part + v;
@@ -1077,7 +1081,11 @@ DEV void tail_dbsum(const JoinerArgs& a, int b, float (*red)[64]) {
   }
   red[part][c] = s;
   __syncthreads();
-  if (part == 0 && v < a.V) a.bias_grad[v] = ((red[0][c] + red[1][c]) + red[2][c]) + red[3][c];
+  if (part == 0 && v < a.V) {
+    float t = red[0][c];
+    for (int k = 1; k < kParts; ++k) t += red[k][c];
+    a.bias_grad[v] = t;
+  }
 }
 
 // d enc rows per block: threads over float4 column groups of J.
@@ -1186,7 +1194,7 @@ struct TailRanges {
 
 __global__ __launch_bounds__(kTailThreads) void joiner_tail_kernel(JoinerArgs a, TailRanges r) {
   extern __shared__ int sp[];  // p_t of one utterance (d dec blocks)
-  __shared__ float red[4][64];  // db blocks
+  __shared__ float red[kTailThreads / kDbCols][kDbCols];  // db blocks
   int b = blockIdx.x;
   if (b < r.dec) { tail_dec_pieces(a, b, sp); return; }
   b -= r.dec;
@@ -1381,7 +1389,7 @@ hipError_t launch_joiner_bwd(const JoinerArgs& a, hipStream_t s) {
   tr.dec = (a.b.U + 1) * a.b.N;
   tr.enc = (a.b.N * a.b.T + R - 1) / R;
   tr.wsum = a.W_grad ? (int)((JV + kTailThreads - 1) / kTailThreads) : 0;
-  tr.dbsum = a.bias_grad ? (V + 63) / 64 : 0;
+  tr.dbsum = a.bias_grad ? (V + kDbCols - 1) / kDbCols : 0;
   {
     RNNT_PROF(s, "joiner_tail");
     hipLaunchKernelGGL(joiner_tail_kernel, dim3(tr.dec + tr.enc + tr.wsum + tr.dbsum), dim3(kTailThreads),
