@@ -249,27 +249,27 @@ __global__ __launch_bounds__(256) void scan_chunk_kernel(BandArgs a) {
 }
 
 // lse of the NS values a lane holds (entries beyond S are -inf; fixed
-// order: pairwise trees). Branch-free: the max is v_max_f64, which passes
-// over a NaN, and a NaN entry reaches the result through its own term of the
-// sum; an all -inf set is shifted by 0, so that the sum is 0 and the result
-// -inf.
+// order: pairwise trees, the odd one out carried up a level). Branch-free:
+// the max is v_max_f64, which passes over a NaN, and a NaN entry reaches the
+// result through its own term of the sum; an all -inf set is shifted by 0,
+// so that the sum is 0 and the result -inf.
 template <int NS>
 DEV double lse_vals(const double (&xs)[NS]) {
   double m[NS];
 #pragma unroll
   for (int i = 0; i < NS; ++i) m[i] = xs[i];
 #pragma unroll
-  for (int w = NS / 2; w >= 1; w >>= 1)
+  for (int w = NS; w > 1; w = (w + 1) / 2)
 #pragma unroll
-    for (int i = 0; i < w; ++i) m[i] = __builtin_fmax(m[i], m[i + w]);
+    for (int i = 0; i < w / 2; ++i) m[i] = __builtin_fmax(m[i], m[i + (w + 1) / 2]);
   const double sh = (m[0] == kNegInfD) ? 0.0 : m[0];
   float e[NS];
 #pragma unroll
   for (int i = 0; i < NS; ++i) e[i] = __builtin_amdgcn_exp2f((float)(xs[i] - sh));
 #pragma unroll
-  for (int w = NS / 2; w >= 1; w >>= 1)
+  for (int w = NS; w > 1; w = (w + 1) / 2)
 #pragma unroll
-    for (int i = 0; i < w; ++i) e[i] += e[i + w];
+    for (int i = 0; i < w / 2; ++i) e[i] += e[i + (w + 1) / 2];
   return sh + (double)__builtin_amdgcn_logf(e[0]);
 }
 
@@ -284,9 +284,8 @@ DEV double readlane_d(double v, int l) {
 // holds slot j; the other lanes' values come in by readlane. The matrix
 // entries of the next step are loaded while the current one is computed
 // (straight-line buffer loads, so the wait counts stay exact).
-template <int K>
+template <int NS>  // slots carried: S <= NS (NS = S up to 8, so that no step works on padding slots)
 __global__ __launch_bounds__(128) void scan_sweep_kernel(BandArgs a) {
-  constexpr int NS = 1 << K;  // slots carried: S <= NS
   const int n = blockIdx.x;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -472,7 +471,18 @@ hipError_t launch_scan_k(const BandArgs& a, hipStream_t s) {
   }
   {
     RNNT_PROF(s, "scan_sweep");
-    hipLaunchKernelGGL((scan_sweep_kernel<K>), dim3(a.b.N), dim3(128), 0, s, a);
+    const dim3 g(a.b.N), b(128);
+    switch (a.S) {
+      case 1: hipLaunchKernelGGL((scan_sweep_kernel<1>), g, b, 0, s, a); break;
+      case 2: hipLaunchKernelGGL((scan_sweep_kernel<2>), g, b, 0, s, a); break;
+      case 3: hipLaunchKernelGGL((scan_sweep_kernel<3>), g, b, 0, s, a); break;
+      case 4: hipLaunchKernelGGL((scan_sweep_kernel<4>), g, b, 0, s, a); break;
+      case 5: hipLaunchKernelGGL((scan_sweep_kernel<5>), g, b, 0, s, a); break;
+      case 6: hipLaunchKernelGGL((scan_sweep_kernel<6>), g, b, 0, s, a); break;
+      case 7: hipLaunchKernelGGL((scan_sweep_kernel<7>), g, b, 0, s, a); break;
+      case 8: hipLaunchKernelGGL((scan_sweep_kernel<8>), g, b, 0, s, a); break;
+      default: hipLaunchKernelGGL((scan_sweep_kernel<16>), g, b, 0, s, a); break;
+    }
   }
   {
     RNNT_PROF(s, "scan_replay");
