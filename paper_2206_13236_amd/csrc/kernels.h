@@ -75,18 +75,18 @@ int lattice_rows_per_lane(int U1);
 inline size_t lattice_diag_cells(int T, int U) {
   return (size_t)(T + U) * 64 * lattice_rows_per_lane(U + 1);
 }
-inline int lattice_fill_blocks(int T, int U) { return (int)((lattice_diag_cells(T, U) + 255) / 256); }
+inline int lattice_fill_blocks(int T, int U, int bs) { return (int)((lattice_diag_cells(T, U) + bs - 1) / bs); }
 DEV int lattice_slot(int u, int R) { return (u % R) * 64 + u / R; }
 // Cells of the diagonal-major layout [T+U, 64R] of an utterance's lattice
 // that no (t, u) of the [T, U+1] rectangle maps to are set to -inf in both
-// copies by a fill of 256-cell blocks per utterance (32-bit index arithmetic;
-// the rectangle's own cells are written by their producer).
-DEV int lattice_fill_blocks_dev(int T, int U1, int R) { return ((T + U1 - 1) * 64 * R + 255) / 256; }
-DEV void lattice_fill_outside(DiagT* pxd, DiagT* pyd, int blk, int tid, int T, int U1, int R) {
-  const int per = lattice_fill_blocks_dev(T, U1, R);
+// copies by a fill of bs-cell blocks (bs threads) per utterance (32-bit index
+// arithmetic; the rectangle's own cells are written by their producer).
+DEV int lattice_fill_blocks_dev(int T, int U1, int R, int bs) { return ((T + U1 - 1) * 64 * R + bs - 1) / bs; }
+DEV void lattice_fill_outside(DiagT* pxd, DiagT* pyd, int blk, int tid, int bs, int T, int U1, int R) {
+  const int per = lattice_fill_blocks_dev(T, U1, R, bs);
   const int n = blk / per;
   const uint32_t W = 64u * (uint32_t)R, DW = (uint32_t)(T + U1 - 1) * W;
-  const uint32_t c = (uint32_t)(blk - n * per) * 256u + (uint32_t)tid;
+  const uint32_t c = (uint32_t)(blk - n * per) * (uint32_t)bs + (uint32_t)tid;
   if (c >= DW) return;
   const int d = (int)(c / W), slot = (int)(c % W);  // W is a power of two
   const int u = (slot & 63) * R + (slot >> 6), t = d - u;

@@ -204,7 +204,7 @@ __global__ __launch_bounds__(256) void lattice_diag_copy_kernel(SimpleArgs a, in
   const size_t L = (size_t)a.b.N * T * U1;
   const int rect_blocks = (int)((L + 255) / 256);  // blocks of 256 threads
   if ((int)blockIdx.x >= rect_blocks) {
-    lattice_fill_outside(a.pxd, a.pyd, (int)blockIdx.x - rect_blocks, threadIdx.x, T, U1, R);
+    lattice_fill_outside(a.pxd, a.pyd, (int)blockIdx.x - rect_blocks, threadIdx.x, 256, T, U1, R);
     return;
   }
   const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -333,7 +333,7 @@ int lattice_rows_per_lane(int U1) {
 
 hipError_t launch_lattice_diag_copy(const SimpleArgs& a, hipStream_t s) {
   const size_t blocks =
-      ((size_t)a.b.N * a.b.T * (a.b.U + 1) + 255) / 256 + (size_t)a.b.N * lattice_fill_blocks(a.b.T, a.b.U);
+      ((size_t)a.b.N * a.b.T * (a.b.U + 1) + 255) / 256 + (size_t)a.b.N * lattice_fill_blocks(a.b.T, a.b.U, 256);
   {
     RNNT_PROF(s, "lattice_diag_copy");
     hipLaunchKernelGGL(lattice_diag_copy_kernel, dim3((unsigned)blocks), dim3(256), 0, s, a,

@@ -293,58 +293,94 @@ __global__ __launch_bounds__(256) void normalizer_kernel(SimpleArgs a) {
   }
 }
 
-// Z = m_a + m_l + log(sum of the partials), px and py (Eqs. (1)-(2), (5)):
-// one thread per node of the [T, U+1] rectangle, then one per cell of the
-// diagonal-major copies, which take -inf where no node of the rectangle lies.
-__global__ __launch_bounds__(256) void normalizer_epi_kernel(SimpleArgs a) {
+// Z = m_a + m_l + log(sum of the partials), px and py (Eqs. (1)-(2), (5)).
+// A block takes a tile of kEpiCells nodes: FT = kEpiCells / (64 R) frames of
+// one utterance times the 64 R rows of a lane-row of the lattice layout. The
+// nodes are formed in row-major order (coalesced reads of the partials and
+// writes of Z, px, py), their diagonal-major copies go to LDS, and are then
+// written diagonal by diagonal, so that the cells of one diagonal in the
+// tile (consecutive slots) are written together. The blocks after the tiles
+// fill the cells of the copies that no node of the rectangle maps to.
+constexpr int kEpiCells = 512;                 // threads per block: one node per thread
+constexpr int kEpiMaxCells = 64 * 16;          // a tile holds at least one lane-row of 64 R slots
+static_assert(kEpiCells <= kEpiMaxCells, "tile buffer");
+
+__host__ __device__ inline int epi_tile_frames(int R) { return kEpiCells / (64 * R) > 1 ? kEpiCells / (64 * R) : 1; }
+
+__global__ __launch_bounds__(kEpiCells) void normalizer_epi_kernel(SimpleArgs a) {
+  __shared__ double tx[kEpiMaxCells], ty[kEpiMaxCells];  // [frame of the tile][slot]
   const int T = a.b.T, U1 = a.b.U + 1, V = a.V;
-  const int R = lattice_rows_per_lane_dev(U1);
-  const size_t L = (size_t)a.b.N * T * U1;
-  const int rect_blocks = (int)((L + 255) / 256);  // blocks of 256 threads
-  if ((int)blockIdx.x >= rect_blocks) {
-    lattice_fill_outside(a.pxd, a.pyd, (int)blockIdx.x - rect_blocks, threadIdx.x, T, U1, R);
+  const int R = lattice_rows_per_lane_dev(U1), W = 64 * R, FT = epi_tile_frames(R);
+  const int tiles_per_utt = (T + FT - 1) / FT;
+  const int tile_blocks = a.b.N * tiles_per_utt;
+  if ((int)blockIdx.x >= tile_blocks) {
+    lattice_fill_outside(a.pxd, a.pyd, (int)blockIdx.x - tile_blocks, threadIdx.x, kEpiCells, T, U1, R);
     return;
   }
-  const size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx >= L) return;
-  const int n = (int)(idx / ((size_t)T * U1));
-  const int rem = (int)(idx - (size_t)n * T * U1);
-  const int t = rem / U1, u = rem - t * U1;
-  const size_t od = (size_t)n * (T + U1 - 1) * 64 * R + (size_t)(t + u) * 64 * R + lattice_slot(u, R);
+  const int n = blockIdx.x / tiles_per_utt, t0 = (blockIdx.x - n * tiles_per_utt) * FT;
+  const size_t L = (size_t)a.b.N * T * U1;
   int Tn, Un;
   utt_dims(a.b, n, Tn, Un);
-  if (t >= Tn || u > Un) {
-    a.Z[idx] = 0.f;
-    a.px[idx] = kNegInfF;
-    a.py[idx] = kNegInfF;
-    a.pxd[od] = (DiagT)kNegInfD;
-    a.pyd[od] = (DiagT)kNegInfD;
-    return;
-  }
-  float s = 0.f;
-  for (int q = 0; q < a.nsplit; ++q) s += a.npart[(size_t)q * L + idx];
-  s = (s > FLT_MIN || s != s) ? s : FLT_MIN;
-  const float z = a.m_a[(size_t)n * T + t] + a.m_l[(size_t)n * U1 + u] + logf(s);
-  const float* amt = a.am + ((size_t)n * T + t) * V;
-  const float* lmu = a.lm + ((size_t)n * U1 + u) * V;
   const int blank = a.b.blank;
-  a.Z[idx] = z;
-  bool ok = true;
-  const int y = (u < Un) ? symbol_at(a.b, n, u, V, ok) : 0;
-  float py = amt[blank] + lmu[blank] - z;
-  float px = amt[y] + lmu[y] - z;
-  if (a.lm_only != 0.f || a.am_only != 0.f) {
-    // smoothed joiner: c L_trivial + a L_lm + b L_acoustic (Sec. 3.3.1)
-    const float c = 1.f - a.lm_only - a.am_only;
-    const float zl = a.Zlm[(size_t)n * U1 + u], za = a.Zac[(size_t)n * T + t];
-    const float* la = a.lavg + (size_t)n * V;
-    py = c * py + a.lm_only * (lmu[blank] - zl) + a.am_only * (amt[blank] + la[blank] - za);
-    px = c * px + a.lm_only * (lmu[y] - zl) + a.am_only * (amt[y] + la[y] - za);
+  for (int c = threadIdx.x; c < FT * W; c += blockDim.x) {
+    const int tl = c / W, u = c - tl * W, t = t0 + tl;
+    double dx = kNegInfD, dy = kNegInfD;
+    if (u < U1 && t < T) {
+      const size_t idx = ((size_t)n * T + t) * U1 + u;
+      if (t >= Tn || u > Un) {
+        a.Z[idx] = 0.f;
+        a.px[idx] = kNegInfF;
+        a.py[idx] = kNegInfF;
+      } else {
+        float sm = 0.f;  // the split partials in order, loads of 8 issued together
+        for (int q0 = 0; q0 < a.nsplit; q0 += 8) {
+          float pv[8];
+#pragma unroll
+          for (int k = 0; k < 8; ++k) pv[k] = (q0 + k < a.nsplit) ? a.npart[(size_t)(q0 + k) * L + idx] : 0.f;
+#pragma unroll
+          for (int k = 0; k < 8; ++k) sm += pv[k];
+        }
+        sm = (sm > FLT_MIN || sm != sm) ? sm : FLT_MIN;
+        const float z = a.m_a[(size_t)n * T + t] + a.m_l[(size_t)n * U1 + u] + logf(sm);
+        const float* amt = a.am + ((size_t)n * T + t) * V;
+        const float* lmu = a.lm + ((size_t)n * U1 + u) * V;
+        a.Z[idx] = z;
+        bool ok = true;
+        const int y = (u < Un) ? symbol_at(a.b, n, u, V, ok) : 0;
+        float py = amt[blank] + lmu[blank] - z;
+        float px = amt[y] + lmu[y] - z;
+        if (a.lm_only != 0.f || a.am_only != 0.f) {
+          // smoothed joiner: c L_trivial + a L_lm + b L_acoustic (Sec. 3.3.1)
+          const float cw = 1.f - a.lm_only - a.am_only;
+          const float zl = a.Zlm[(size_t)n * U1 + u], za = a.Zac[(size_t)n * T + t];
+          const float* la = a.lavg + (size_t)n * V;
+          py = cw * py + a.lm_only * (lmu[blank] - zl) + a.am_only * (amt[blank] + la[blank] - za);
+          px = cw * px + a.lm_only * (lmu[y] - zl) + a.am_only * (amt[y] + la[y] - za);
+        }
+        a.py[idx] = py;
+        a.px[idx] = (u < Un) ? px : kNegInfF;
+        dy = (double)py * kLog2e;
+        dx = (u < Un) ? (double)px * kLog2e : kNegInfD;
+      }
+    }
+    tx[tl * W + lattice_slot(u, R)] = dx;
+    ty[tl * W + lattice_slot(u, R)] = dy;
   }
-  a.py[idx] = py;
-  a.px[idx] = (u < Un) ? px : kNegInfF;
-  a.pyd[od] = (DiagT)((double)py * kLog2e);
-  a.pxd[od] = (DiagT)((u < Un) ? (double)px * kLog2e : kNegInfD);
+  __syncthreads();
+  // diagonal d = t0 + k holds the tile's nodes (t0 + FT-1-j', u = d - t) for
+  // the FT frames; item (k, j): u = k - (FT-1) + j, so that consecutive j are
+  // consecutive u on one diagonal
+  const int ft = min(FT, T - t0), nd = FT - 1 + U1;
+  const size_t base = (size_t)n * (T + U1 - 1) * W;
+  for (int it = threadIdx.x; it < nd * FT; it += blockDim.x) {
+    const int k = it / FT, j = it - k * FT;
+    const int u = k - (FT - 1) + j, tl = k - u;
+    if (u < 0 || u >= U1 || tl < 0 || tl >= ft) continue;
+    const int sl = lattice_slot(u, R);
+    const size_t o = base + (size_t)(t0 + k) * W + sl;
+    a.pxd[o] = (DiagT)tx[tl * W + sl];
+    a.pyd[o] = (DiagT)ty[tl * W + sl];
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -624,11 +660,12 @@ hipError_t launch_normalizer(const SimpleArgs& a, hipStream_t s) {
     RNNT_PROF(s, "normalizer");
     hipLaunchKernelGGL(normalizer_kernel, grid, dim3(256), 0, s, a);
   }
-  // the rectangle's nodes, then the cells of the diagonal-major copies
-  const size_t blocks = ((size_t)a.b.N * T * U1 + 255) / 256 + (size_t)a.b.N * lattice_fill_blocks(T, a.b.U);
+  // tiles of the rectangle's nodes, then the cells of the diagonal-major copies
+  const int FT = epi_tile_frames(lattice_rows_per_lane(U1));
+  const size_t blocks = (size_t)a.b.N * ((T + FT - 1) / FT) + (size_t)a.b.N * lattice_fill_blocks(T, a.b.U, kEpiCells);
   {
     RNNT_PROF(s, "normalizer_epi");
-    hipLaunchKernelGGL(normalizer_epi_kernel, dim3((unsigned)blocks), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(normalizer_epi_kernel, dim3((unsigned)blocks), dim3(kEpiCells), 0, s, a);
   }
   return hipGetLastError();
 }
