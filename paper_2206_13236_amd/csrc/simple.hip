@@ -387,6 +387,7 @@ __global__ __launch_bounds__(kEpiCells) void normalizer_epi_kernel(SimpleArgs a)
 // d am: per utterance C[t][v] = sum_u Wt[t][u] El[u][v]  (K = U_n + 1)
 // ---------------------------------------------------------------------------
 using DamCfg = GemmCfg<32, 64, 32, false>;
+constexpr int kDamSymChunk = 128;  // symbols per pass of the d am kernel's target columns
 
 struct WtSrcKC {  // A(t, u) = Wt[t][u], rows padded to ldw (multiple of 4, zero-filled)
   using Raw = RawF<4>;
@@ -456,33 +457,55 @@ __global__ __launch_bounds__(256) void dam_kernel(SimpleArgs a) {
       }
     }
   if (active) {
-    // sparse part: target columns, in ascending u (deterministic). The
-    // symbols go through LDS (free once the main loop is done) in chunks, so
-    // the loop over u reads broadcasts instead of a chain of dependent loads.
-    constexpr int kSymChunk = Cfg::SMEM_BYTES / (int)sizeof(int);
-    int* ssym = reinterpret_cast<int*>(smem);
-    for (int c0 = 0; c0 < Un; c0 += kSymChunk) {
-      const int cn = min(kSymChunk, Un - c0);
+    // sparse part: the target columns. Per chunk of kDamSymChunk symbols the
+    // u whose symbol falls in the tile's columns are listed in ascending
+    // order (ballot compaction), their gx values for the tile's frames are
+    // gathered by all threads at once, and each lane subtracts them in the
+    // list's order (ascending u: deterministic).
+    constexpr int kChunk = kDamSymChunk;
+    int* mu = reinterpret_cast<int*>(smem);  // [kChunk] listed u
+    int* my = mu + kChunk;                   // [kChunk] their symbols
+    int* wcnt = my + kChunk;                 // [4] per-wave counts
+    float* g = reinterpret_cast<float*>(wcnt + 4);  // [kChunk][BM] gathered gx
+    static_assert((2 * kChunk + 4) * 4 + kChunk * Cfg::BM * 4 <= Cfg::SMEM_BYTES, "sparse chunk fits");
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    for (int c0 = 0; c0 < Un; c0 += kChunk) {
       __syncthreads();  // the previous user of smem is done
-      for (int k = threadIdx.x; k < cn; k += blockDim.x) {
+      const int u = c0 + threadIdx.x;
+      int y = -1;
+      if (threadIdx.x < kChunk && u < Un) {
         bool ok = true;
-        ssym[k] = symbol_at(a.b, n, c0 + k, V, ok);
+        y = symbol_at(a.b, n, u, V, ok);
+      }
+      const bool hit = y >= v0 && y < v0 + Cfg::BN;
+      const uint64_t bal = __ballot(hit);
+      if (lane == 0) wcnt[wv] = __popcll(bal);
+      __syncthreads();
+      int base = 0, nm = 0;
+      for (int w = 0; w < (int)(blockDim.x >> 6); ++w) {
+        base += (w < wv) ? wcnt[w] : 0;
+        nm += wcnt[w];
+      }
+      if (hit) {
+        const int k = base + __popcll(bal & ((1ull << lane) - 1));
+        mu[k] = u;
+        my[k] = y;
       }
       __syncthreads();
-      for (int k = 0; k < cn; ++k) {
-        const int y = ssym[k];
-        if (y < v0 || y >= v0 + Cfg::BN) continue;
-        const int u = c0 + k;
+      for (int it = threadIdx.x; it < nm * Cfg::BM; it += blockDim.x) {
+        const int k = it / Cfg::BM, tr = it - k * Cfg::BM, t = t0 + tr;
+        g[it] = (t < Tn) ? gxn[(size_t)t * U1 + mu[k]] : 0.f;
+      }
+      __syncthreads();
+      for (int k = 0; k < nm; ++k) {
+        const int yk = my[k];
 #pragma unroll
         for (int j = 0; j < Cfg::FN; ++j) {
-          if (v0 + tile_col<Cfg>(j) != y) continue;
+          if (v0 + tile_col<Cfg>(j) != yk) continue;
 #pragma unroll
           for (int i = 0; i < Cfg::FM; ++i)
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-              const int t = t0 + tile_row<Cfg>(i, r);
-              if (t < Tn) res[i][j][r] -= ks * gxn[(size_t)t * U1 + u];
-            }
+            for (int r = 0; r < 4; ++r) res[i][j][r] -= ks * g[k * Cfg::BM + tile_row<Cfg>(i, r)];
         }
       }
     }
