@@ -289,6 +289,19 @@ def main() -> int:
                 "algorithmic_flops_per_launch": per_launch_flops, "avg_launch_us": timed["avg_us"],
                 "launches_timed": timed["launches"], "bracketed_steps": f"every {BRACKET_EVERY}th timed step"}
 
+    # step-time spread (after the timed region): each step bracketed on its own
+    per_step = []
+    for _ in range(args.steps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        step.step(batch, am, lm, enc, dec, W, bias)
+        e1.record(stream)
+        e1.synchronize()
+        per_step.append(e0.elapsed_time(e1))
+    q = np.percentile(np.asarray(per_step), [10, 50, 90])
+    spread = {"p10": round(float(q[0]), 4), "median": round(float(q[1]), 4), "p90": round(float(q[2]), 4),
+              "steps": len(per_step), "note": "each step bracketed by its own events, after the timed region"}
+
     band = None if args.no_band_algorithms else _band_algorithms(P, batch, S,
                                                                  step.step(batch, am, lm, enc, dec, W, bias))
     unpruned = None if args.no_unpruned else _unpruned(P, batch, enc, dec, W, bias, frames, dev)
@@ -301,6 +314,7 @@ def main() -> int:
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms_step, 4),
+        "ms_per_step_spread": spread,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
