@@ -619,8 +619,9 @@ __global__ __launch_bounds__(kGemmThreads) void joiner_dlogits_kernel(JoinerArgs
 // with their loads issued together; the block's column sums are one db_part
 // row.
 // ---------------------------------------------------------------------------
-constexpr int kDlRows = 64;
-constexpr int kDlThreads = 512;
+constexpr int kDlRows = 32;
+constexpr int kDlThreads = 256;
+constexpr int kDlInFlight = 16;  // rows per thread whose loads are issued together
 
 template <bool BF>
 __global__ __launch_bounds__(kDlThreads) void joiner_dl_kernel(JoinerArgs a, int cm0, int cm1) {
@@ -656,10 +657,10 @@ __global__ __launch_bounds__(kDlThreads) void joiner_dl_kernel(JoinerArgs a, int
     const bool gok = g0 + ct < ng;
     float cs[4] = {0.f, 0.f, 0.f, 0.f};
     if (gok) {
-      for (int r0 = rg; r0 < nrows; r0 += 4 * nrg) {
-        float l[4][4];
+      for (int r0 = rg; r0 < nrows; r0 += kDlInFlight * nrg) {
+        float l[kDlInFlight][4];
 #pragma unroll
-        for (int k = 0; k < 4; ++k) {
+        for (int k = 0; k < kDlInFlight; ++k) {
           const int r = r0 + k * nrg;
           const int4 info = ri[min(r, kDlRows - 1)];
           const bool ok = r < nrows && info.w >= 0 && c < V;
@@ -673,7 +674,7 @@ __global__ __launch_bounds__(kDlThreads) void joiner_dl_kernel(JoinerArgs a, int
           }
         }
 #pragma unroll
-        for (int k = 0; k < 4; ++k) {
+        for (int k = 0; k < kDlInFlight; ++k) {
           const int r = r0 + k * nrg;
           if (r >= nrows) break;
           const int4 info = ri[r];
@@ -1043,10 +1044,31 @@ __global__ __launch_bounds__(kGemmThreads, 4) void joiner_dw_kernel(JoinerArgs a
 // that their memory latencies overlap.
 constexpr int kTailThreads = 256;
 
-// dW = sum of the split partials, in split order (one element per thread).
+// dW = sum of the split partials, in split order: four consecutive elements
+// per thread (16-byte loads, 16 partials in flight) where J*V and dW's
+// address allow, else one.
+constexpr int kWsumVec = 4;
+
+DEV bool tail_wsum_vec(const JoinerArgs& a) {
+  return (((size_t)a.J * a.V) % kWsumVec) == 0 && (reinterpret_cast<uintptr_t>(a.W_grad) & 15) == 0;
+}
+
 DEV void tail_wsum(const JoinerArgs& a, int b) {
   const size_t JV = (size_t)a.J * a.V;
   const size_t i = (size_t)b * kTailThreads + threadIdx.x;
+  if (tail_wsum_vec(a)) {
+    if (i * kWsumVec >= JV) return;
+    const float4* src = reinterpret_cast<const float4*>(a.dw_part) + i;
+    const size_t stride = JV / kWsumVec;
+    float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll 16
+    for (int z = 0; z < a.splits; ++z) {
+      const float4 v = src[(size_t)z * stride];
+      s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
+    }
+    reinterpret_cast<float4*>(a.W_grad)[i] = s;
+    return;
+  }
   if (i >= JV) return;
   float s = 0.f;
 #pragma unroll 8
@@ -1388,7 +1410,9 @@ hipError_t launch_joiner_bwd(const JoinerArgs& a, hipStream_t s) {
   TailRanges tr;
   tr.dec = (a.b.U + 1) * a.b.N;
   tr.enc = (a.b.N * a.b.T + R - 1) / R;
-  tr.wsum = a.W_grad ? (int)((JV + kTailThreads - 1) / kTailThreads) : 0;
+  const bool wvec = JV % kWsumVec == 0 && (reinterpret_cast<uintptr_t>(a.W_grad) & 15) == 0;
+  const size_t wthreads = wvec ? JV / kWsumVec : JV;
+  tr.wsum = a.W_grad ? (int)((wthreads + kTailThreads - 1) / kTailThreads) : 0;
   tr.dbsum = a.bias_grad ? (V + kDbCols - 1) / kDbCols : 0;
   {
     RNNT_PROF(s, "joiner_tail");
