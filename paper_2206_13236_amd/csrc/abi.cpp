@@ -221,6 +221,7 @@ struct JoinerBwdWs {
   int4* rowinfo;
   void* dl;
   void* dlT;
+  void* wpad;
   float* dpre;
   float* enc_part;
   void* hbuf;
@@ -244,6 +245,7 @@ JoinerBwdWs joiner_bwd_layout(void* base, int N, int T, int S, int J, int V, int
   const size_t dl_elems = (size_t)w.chunk_rows * joiner_ldl(V);
   w.dl = bf16 ? (void*)c.take<uint16_t>(dl_elems) : (void*)c.take<float>(dl_elems);
   w.dlT = bf16 ? (void*)c.take<uint16_t>(dl_elems) : nullptr;
+  w.wpad = (bf16 && V % 8 != 0) ? (void*)c.take<uint16_t>((size_t)J * joiner_ldl(V)) : nullptr;
   w.dpre = c.take<float>(M * J);
   w.enc_part = c.take<float>((M + 127) / 128 * 2 * J);
   const size_t h_elems = (size_t)w.chunk_rows * J;
@@ -325,6 +327,7 @@ void set_joiner_bwd(JoinerArgs& a, const JoinerBwdWs& w, const float* lse, const
   a.scale = scale;
   a.dl = w.dl;
   a.dlT = w.dlT;
+  a.wpad = w.wpad;
   a.ldl = joiner_ldl(a.V);
   a.chunk_rows = w.chunk_rows;
   a.dpre = w.dpre;

@@ -256,13 +256,14 @@ struct WtSrcKC {
   static constexpr int mode = MODE;
   using Raw = RawVec<TIn, Cfg::KV>;
   Rsrc W;
-  int j0, J, V;
+  int j0, J, V, ld;  // ld: row stride of W, or of its zero-padded copy
   DEV WtSrcKC(const JoinerArgs& a, int j0_)
-      : W(make_rsrc(a.W, (size_t)a.J * a.V * sizeof(TIn))), j0(j0_), J(a.J), V(a.V) {}
+      : W(make_rsrc(a.wpad ? a.wpad : a.W, (size_t)a.J * (a.wpad ? a.ldl : a.V) * sizeof(TIn))),
+        j0(j0_), J(a.J), V(a.V), ld(a.wpad ? a.ldl : a.V) {}
   DEV void kc_load(int row, int k, Raw& r) const {
     const int j = j0 + row;
     const int n = (j < J) ? V - k : 0;
-    raw_load(W, (uint32_t)(j * V + k) * sizeof(TIn), n, mode, r);
+    raw_load(W, (uint32_t)(j * ld + k) * sizeof(TIn), n, mode, r);
   }
   DEV void kc_finish(const Raw& r, float (&v)[Cfg::KV]) const { raw_to_float(r, v); }
 };
@@ -328,9 +329,33 @@ DEV float bias_at(const void* bias, int bf16, int v) {
 // ---------------------------------------------------------------------------
 // Prep: per-utterance frame offsets and per-row info.
 // ---------------------------------------------------------------------------
+// W [J, V] bf16 copied into wpad [J, ldl] with zeros after column V: one
+// 8-element group per thread.
+DEV void prep_wpad(const JoinerArgs& a, int b) {
+  const int gpr = a.ldl / 8;
+  const int g = b * 256 + threadIdx.x;
+  if (g >= a.J * gpr) return;
+  const int j = g / gpr, c = (g - j * gpr) * 8;
+  const uint16_t* src = reinterpret_cast<const uint16_t*>(a.W) + (size_t)j * a.V;
+  uint32_t w[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const uint32_t lo = (c + 2 * q < a.V) ? src[c + 2 * q] : 0u;
+    const uint32_t hi = (c + 2 * q + 1 < a.V) ? src[c + 2 * q + 1] : 0u;
+    w[q] = lo | (hi << 16);
+  }
+  *reinterpret_cast<uint4*>(reinterpret_cast<uint16_t*>(a.wpad) + (size_t)j * a.ldl + c) = make_uint4(w[0], w[1], w[2], w[3]);
+}
+
+int prep_wpad_blocks(const JoinerArgs& a) { return a.wpad ? (a.J * (a.ldl / 8) + 255) / 256 : 0; }
+
 __global__ __launch_bounds__(256) void joiner_prep_kernel(JoinerArgs a) {
   __shared__ int s_part[4];
   const int per = (a.b.T * a.S + 255) / 256;  // blocks per utterance: one (t, s) slot per thread
+  if ((int)blockIdx.x >= a.b.N * per) {  // blocks after the utterances' copy W for dh
+    prep_wpad(a, blockIdx.x - a.b.N * per);
+    return;
+  }
   const int n = blockIdx.x / per, i = (blockIdx.x - n * per) * 256 + threadIdx.x;
   const int T = a.b.T, U1 = a.b.U + 1, S = a.S, J = a.J;
   // frame offset of utterance n: sum of T_q over q < n, the lengths loaded
@@ -1290,7 +1315,7 @@ int joiner_db_rows(int N, int T, int S) {
 hipError_t launch_joiner_prep(const JoinerArgs& a, hipStream_t s) {
   {
     RNNT_PROF(s, "joiner_prep");
-    hipLaunchKernelGGL(joiner_prep_kernel, dim3(a.b.N * ((a.b.T * a.S + 255) / 256)), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(joiner_prep_kernel, dim3(a.b.N * ((a.b.T * a.S + 255) / 256) + prep_wpad_blocks(a)), dim3(256), 0, s, a);
   }
   return hipGetLastError();
 }
@@ -1348,9 +1373,10 @@ hipError_t launch_joiner_bwd(const JoinerArgs& a, hipStream_t s) {
     if (e != hipSuccess) return e;
   }
   // segment modes of the W reads: the recomputed forward reads W rows in
-  // segments of 16 / KV elements, dh reads them k-contiguous in KV
+  // segments of 16 / KV elements, dh reads them k-contiguous in KV (bf16 W
+  // with V not a multiple of 8: from its zero-padded copy, in 16-byte segments)
   const int wm_f = host_seg_mode(V, a.bf16 ? 2 : 4, a.bf16);
-  const int wm_h = host_seg_mode(V, a.bf16 ? 8 : 4, a.bf16);
+  const int wm_h = a.wpad ? (int)kSegVector : host_seg_mode(V, a.bf16 ? 8 : 4, a.bf16);
   for (int cm0 = 0; cm0 < mmax; cm0 += a.chunk_rows) {
     const int cm1 = (cm0 + a.chunk_rows < mmax) ? cm0 + a.chunk_rows : mmax;
     const int mt = (cm1 - cm0 + 127) / 128;

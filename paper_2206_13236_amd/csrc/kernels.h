@@ -140,6 +140,8 @@ struct JoinerArgs {
   void* dl;            // ws chunk [chunk_rows, ldl] (f32 or bf16)
   int ldl;
   void* dlT;           // ws chunk [ldl, chunk_rows] (bf16 only): d(logits) transposed for dW
+  void* wpad;          // ws [J, ldl] bf16 or null: W with its rows padded by zeros to ldl elements, so
+                       // that dh reads W in 16-byte segments when V is not a multiple of 8
   int chunk_rows;
   float* dpre;         // ws [N*T*S, J]: the d dec pieces, each in the row of dpre of its first row
   float* enc_part;     // ws [ceil(N*T*S/128), 2, J]: d enc pieces of frames cut by a 128-row tile
