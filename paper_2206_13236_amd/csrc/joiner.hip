@@ -1102,7 +1102,7 @@ DEV void tail_wsum(const JoinerArgs& a, int b) {
 }
 
 // db = sum of the column partials written by the d(logits) kernel (one per
-// 64 rows streamed, one per wave row of a GEMM tile recomputed): a block takes
+// 32 rows streamed, one per wave row of a GEMM tile recomputed): a block takes
 // 16 columns; each of its 16 thread groups sums a contiguous sixteenth of the
 // rows in ascending order, 8 loads in flight, then the sixteenths are added
 // in order.
