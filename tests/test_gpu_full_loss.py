@@ -17,6 +17,7 @@ CASES = {
     "tiny": dict(wl="tiny"),
     "small_f32": dict(wl="bpe", N=3, T_range=(20, 40), U_range=(3, 12), V=37, J=64),
     "small_bf16": dict(wl="long", N=2, T_range=(20, 30), U_range=(5, 10), V=72, J=64),
+    "small_bf16_oddv": dict(wl="long", N=2, T_range=(20, 30), U_range=(5, 10), V=37, J=64),
 }
 
 

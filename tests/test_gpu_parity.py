@@ -23,6 +23,9 @@ CASES = {
     "tiny": dict(wl="tiny"),
     "small_f32": dict(wl="bpe", N=3, T_range=(40, 70), U_range=(5, 20), V=37, J=64, S=5),
     "small_bf16": dict(wl="long", N=3, T_range=(40, 70), U_range=(5, 20), V=72, J=64, S=4),
+    # bf16 rows of odd length: element-wise W segments in the forward, the
+    # zero-padded copy of W in dh
+    "small_bf16_oddv": dict(wl="long", N=3, T_range=(30, 50), U_range=(4, 15), V=37, J=64, S=4),
     "bpe_sub": dict(wl="bpe", N=3),
     "long_sub": dict(wl="long", N=2),
 }
