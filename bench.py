@@ -178,8 +178,9 @@ def main() -> int:
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py measures one GPU: this build has no multi-GPU path (the loss is per-utterance; "
-              "data-parallel sharding over utterances is described in DESIGN.md). Run with --gpus 1.",
+        print("bench.py measures one GPU: the library has no multi-GPU path (the loss is per utterance, "
+              "so a batch shards over GPUs by utterance with no communication in the loss itself). "
+              "Run with --gpus 1.",
               file=sys.stderr)
         return 2
 

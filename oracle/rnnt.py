@@ -19,7 +19,7 @@ Arrays use the conventions of the C ABI: ``symbols[n, u]`` is y_{u+1}
 [N, T, U+1] with minus infinity outside the lattice; the loss of utterance n
 is minus its total log-probability.
 
-Readings where the paper is silent (each one is listed in the design doc):
+Readings where the paper is silent:
 * y'(t, -1) in Eq. (8) is taken as 0 (the p = 0 window has no red arc);
 * Eq. (8) is evaluated in fp32, left to right, and ties go to the smallest p;
   a NaN score never wins;

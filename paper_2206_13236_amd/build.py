@@ -22,7 +22,8 @@ SOURCES = ["abi.cpp", "prof.cpp", "simple.hip", "lattice.hip", "prune.hip", "joi
 
 ARCH = os.environ.get("RNNT_OFFLOAD_ARCH", "gfx950")
 
-# Packed fp32 instructions are disabled for all device code;
+# Packed fp32 instructions are disabled for all device code (some of their
+# forms have given wrong results on this hardware without an error);
 # no fast-math, so the pruning scores are plain IEEE fp32 additions.
 COMMON_FLAGS = [
     f"--offload-arch={ARCH}",
