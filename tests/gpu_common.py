@@ -34,7 +34,10 @@ def dev_joiner(a, bf16: bool):
 
 
 def host(t: torch.Tensor) -> np.ndarray:
-    return t.detach().float().cpu().numpy().astype(np.float64)
+    # outputs the library leaves untouched (absent logits slots) may hold any
+    # bit pattern, signalling NaNs included: the cast must not warn on them
+    with np.errstate(invalid="ignore"):
+        return t.detach().float().cpu().numpy().astype(np.float64)
 
 
 def make_dev_batch(b, blank=None) -> P.Batch:
