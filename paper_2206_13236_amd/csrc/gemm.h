@@ -126,7 +126,10 @@ struct KCLoader {
 
 // Operand tile whose global source is row-contiguous ([k][row]); the loader
 // transposes KV x (16/KV) blocks in registers so LDS stays k-contiguous.
-template <class Cfg, int ROWS, class Src>
+// Blocks go to threads from TOFF on (modulo NT): when both operands of a
+// contraction have fewer blocks than threads, giving them disjoint threads
+// spreads the staging over all waves.
+template <class Cfg, int ROWS, class Src, int TOFF = 0>
 struct MNCLoader {
   static constexpr int KV = Cfg::KV;
   static constexpr int NV = 16 / KV;                       // rows per block (4 fp32, 2 bf16)
@@ -144,7 +147,7 @@ struct MNCLoader {
   DEV void fetch(int k0, Reg& r) const {
 #pragma unroll
     for (int b = 0; b < NPT; ++b) {
-      int blk = threadIdx.x + Cfg::NT * b;
+      int blk = (threadIdx.x + TOFF) % Cfg::NT + Cfg::NT * b;
       if (NBLK % Cfg::NT == 0 || blk < NBLK) {
         const int kb = blk % NKB, nb = blk / NKB;
 #pragma unroll
@@ -155,7 +158,7 @@ struct MNCLoader {
   DEV void put(const Reg& r, typename Cfg::T* lds) const {
 #pragma unroll
     for (int b = 0; b < NPT; ++b) {
-      int blk = threadIdx.x + Cfg::NT * b;
+      int blk = (threadIdx.x + TOFF) % Cfg::NT + Cfg::NT * b;
       if (NBLK % Cfg::NT == 0 || blk < NBLK) {
         const int kb = blk % NKB, nb = blk / NKB;
         if constexpr (src_direct<Src>::value) {

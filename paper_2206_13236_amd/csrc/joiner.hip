@@ -1043,7 +1043,7 @@ __global__ __launch_bounds__(kGemmThreads, 4) void joiner_dw_kernel(JoinerArgs a
     HbufSrcMNC<Cfg> sa{make_rsrc(a.hbuf, (size_t)a.chunk_rows * J * sizeof(typename Cfg::T)), cm0, ke, j0, J};
     DlSrcMNC<Cfg> sb{make_rsrc(a.dl, (size_t)a.chunk_rows * a.ldl * sizeof(typename Cfg::T)), cm0, ke, v0, a.ldl};
     MNCLoader<Cfg, Cfg::BM, HbufSrcMNC<Cfg>> la(sa);
-    MNCLoader<Cfg, Cfg::BN, DlSrcMNC<Cfg>> lb(sb);
+    MNCLoader<Cfg, Cfg::BN, DlSrcMNC<Cfg>, decltype(la)::NBLK> lb(sb);  // threads after A's blocks
     gemm_mainloop<Cfg>(la, lb, kb, ke, smem, acc);
   }
 #pragma unroll

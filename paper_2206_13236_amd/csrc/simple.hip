@@ -573,7 +573,7 @@ __global__ __launch_bounds__(256) void dlm_kernel(SimpleArgs a) {
   WtSrcMNC sa{a.Wt + (size_t)n * T * a.ldw, u0, Tn, a.ldw};
   ExpSrcMNC sb{a.am + (size_t)n * T * V, a.m_a + (size_t)n * T, v0, Tn, V};
   MNCLoader<Cfg, Cfg::BM, WtSrcMNC> la(sa);
-  MNCLoader<Cfg, Cfg::BN, ExpSrcMNC> lb(sb);
+  MNCLoader<Cfg, Cfg::BN, ExpSrcMNC, decltype(la)::NBLK> lb(sb);  // threads after A's blocks
   gemm_mainloop<Cfg>(la, lb, k0, k1, smem, acc);
   float* part = a.lpart + ((size_t)sk * a.b.N + n) * U1 * V;
 #pragma unroll
