@@ -106,6 +106,35 @@ def test_prune_ranges_bit_exact(name):
     assert np.array_equal(got, o["ranges"]), f"{(got != o['ranges']).sum()} range entries differ"
 
 
+def _tie_cases():
+    """Occupations with exact fp32 window ties and an all-NaN frame (T = 6,
+    U = 4, S = 2, so P = 3), and the bounds p_t worked out by hand through
+    Eq. (8), the envelope clamp and the adjustment (ties to the smallest p,
+    NaN never wins, an all-NaN frame takes 0)."""
+    T, U, S = 6, 4, 2
+    gx = np.zeros((4, T, U + 1), np.float32)
+    gy = np.zeros((4, T, U + 1), np.float32)
+    gy[:, 2, :4] = 0.25            # windows p = 0, 1, 2 of frame 2 all score 1/2
+    gy[1:3, 3, 3:] = 0.5           # frame 3: window p = 3 scores 1
+    gx[2, 3] = np.nan              # ... but utterance 2's frame 3 is all NaN
+    gy[2, 3] = np.nan
+    gy[3, 2] = [0.0, 0.25, 0.25, 0.25, 0.25]  # windows 1, 2, 3 tie at 1/2
+    expect = [[0, 0, 0, 1, 2, 3], [0, 0, 1, 2, 2, 3], [0, 0, 0, 1, 2, 3], [0, 0, 1, 1, 2, 3]]
+    return T, U, S, gx, gy, np.array(expect)
+
+
+def test_prune_ranges_exact_ties_and_nan_frames():
+    T, U, S, gx, gy, expect = _tie_cases()
+    N = gx.shape[0]
+    tl, ul = np.full(N, T, np.int32), np.full(N, U, np.int32)
+    ref = O.prune_ranges(gx, gy, tl, ul, S)
+    assert np.array_equal(ref[:, :, 0], expect)
+    say("[prune] exact ties and all-NaN frames")
+    batch = P.Batch(dev_i32(tl), dev_i32(ul), dev_i32(np.ones((N, U), np.int32)), T, U, 0)
+    got = P.rnnt_prune_ranges(batch, S, dev_f32(gx), dev_f32(gy)).cpu().numpy()
+    assert np.array_equal(got, ref), f"GPU bounds {got[:, :, 0].tolist()} vs {expect.tolist()}"
+
+
 @pytest.mark.parametrize("name", list(CASES))
 def test_pruned_joiner(name):
     o = _oracle(name)

@@ -303,6 +303,61 @@ def test_ranges_invariants_random():
             assert np.all(p == 0)
 
 
+def test_argmax_ties_go_to_the_smallest_start_and_nan_never_wins():
+    # Eq. (8) picks the window with the largest score; with this build's
+    # reading, exact ties go to the smallest p and a NaN score never wins.
+    sc = np.array([[0.2, 0.7, 0.7, 0.1],      # tie between p = 1 and p = 2
+                   [0.5, 0.5, 0.5, 0.5],      # all tied
+                   [np.nan, 0.3, np.nan, 0.3],  # NaN skipped, then the tie
+                   [np.nan, np.nan, np.nan, np.nan],  # nothing wins: p = 0
+                   [0.1, np.nan, 0.9, -np.inf]], dtype=np.float32)
+    assert O.raw_pruning_bounds(sc).tolist() == [1, 0, 1, 0, 2]
+
+
+def test_exact_fp32_window_tie_through_the_scores():
+    # One frame of a T = 6, U = 4, S = 2 lattice (P = 3) whose blank
+    # occupations make windows p = 0, 1, 2 score exactly 0.5 in fp32:
+    # gy(2, .) = [1/4, 1/4, 1/4, 1/4, 0] and gx(2, .) = 0, so
+    # score(p) = -0 + gy(p) + gy(p+1) = 1/2 for p <= 2 and 1/4 for p = 3.
+    # Frame 2's envelope is [3 - (5 - 2), min(3, 2)] = [0, 2], so the raw
+    # bound is not clamped; the smallest-p rule gives 0 (a largest-p rule 2).
+    T, U, S = 6, 4, 2
+    gx = np.zeros((T, U + 1), np.float32)
+    gy = np.zeros((T, U + 1), np.float32)
+    gy[2, :4] = 0.25
+    sc = O.pruning_window_scores(gx, gy, T, U, S)
+    assert sc[2].tolist() == [0.5, 0.5, 0.5, 0.25]
+    assert O.raw_pruning_bounds(sc)[2] == 0
+    # the same frame with every occupation NaN: no score wins, p = 0
+    gy2 = gy.copy()
+    gy2[2] = np.nan
+    gx2 = gx.copy()
+    gx2[2] = np.nan
+    assert O.raw_pruning_bounds(O.pruning_window_scores(gx2, gy2, T, U, S))[2] == 0
+    # every frame all-zero except frame 2: every other frame ties everywhere
+    # and takes its smallest feasible start; the whole range set follows
+    # from the envelope clamp and the adjustment: p = [0, 0, 0, 1, 2, 3]
+    r = O.prune_ranges(gx[None], gy[None], [T], [U], S)
+    assert r[0, :, 0].tolist() == [0, 0, 0, 1, 2, 3]
+
+
+def test_ties_and_nan_frames_through_the_whole_bound_computation():
+    # The GPU test of the bounds uses the same four utterances (T = 6, U = 4,
+    # S = 2); the expected p_t were worked by hand through Eq. (8), the
+    # envelope clamp and the adjustment.
+    T, U, S = 6, 4, 2
+    gx = np.zeros((4, T, U + 1), np.float32)
+    gy = np.zeros((4, T, U + 1), np.float32)
+    gy[:, 2, :4] = 0.25
+    gy[1:3, 3, 3:] = 0.5
+    gx[2, 3] = np.nan
+    gy[2, 3] = np.nan
+    gy[3, 2] = [0.0, 0.25, 0.25, 0.25, 0.25]
+    r = O.prune_ranges(gx, gy, [T] * 4, [U] * 4, S)
+    assert r[:, :, 0].tolist() == [[0, 0, 0, 1, 2, 3], [0, 0, 1, 2, 2, 3], [0, 0, 0, 1, 2, 3],
+                                   [0, 0, 1, 1, 2, 3]]
+
+
 def test_pruning_keeps_a_dominant_path():
     # One alignment carries (almost) all the mass: its occupations are ~1 and
     # the bounds must keep the whole path inside the band, so the pruned
@@ -493,6 +548,38 @@ def test_smoothed_joiner_special_cases():
     _, q = O.smoothed_joiner_logprobs(b.am, b.lm, b.symbols, b.t_len, b.u_len, 0, 0.5, 0.5)
     fin = np.isfinite(q)
     assert np.all(q[fin] < 0)
+
+
+def test_smoothed_unigram_prior_is_the_log_of_the_mean_softmax():
+    # Sec. 3.3.1: L_dec^avg(v) is the log of the mean over the utterance's
+    # decoder rows of Softmax_v lm[u, v] (not the mean of the log-softmaxes).
+    # V = 2, blank = 0, y_1 = 1; lm rows with softmaxes (1/4, 3/4) and
+    # (1/2, 1/2): the prior is (log 3/8, log 5/8). With am = 0 the acoustic
+    # joiner (a_ac = 1) is then exactly that prior: py = log 3/8 and
+    # px = log 5/8 at every node. The mean of the log-softmaxes would give
+    # softmax weights proportional to (1/8)^(1/2), (3/8)^(1/2) instead:
+    # 0.366 / 0.634 rather than 0.375 / 0.625. A third lm row (padding,
+    # u > U_n) must not enter the average.
+    lm = np.array([[[0.0, math.log(3.0)], [0.0, 0.0], [5.0, -5.0]]])
+    am = np.zeros((1, 3, 2))
+    sym = np.array([[1, 1]])
+    px, py = O.smoothed_joiner_logprobs(am, lm, sym, [3], [1], 0, 0.0, 1.0)
+    np.testing.assert_allclose(py[0, :3, :2], math.log(3 / 8), rtol=0, atol=1e-14)
+    np.testing.assert_allclose(px[0, :3, :1], math.log(5 / 8), rtol=0, atol=1e-14)
+    # with a non-zero am the acoustic joiner is LogSoftmax_v(am + prior)
+    am2 = np.array([[[0.3, -1.2], [2.0, 0.5], [0.0, 0.0]]])
+    px2, py2 = O.smoothed_joiner_logprobs(am2, lm, sym, [3], [1], 0, 0.0, 1.0)
+    for t in range(3):
+        z0 = am2[0, t, 0] + math.log(3 / 8)
+        z1 = am2[0, t, 1] + math.log(5 / 8)
+        lse = math.log(math.exp(z0) + math.exp(z1))
+        assert abs(py2[0, t, 0] - (z0 - lse)) < 1e-14
+        assert abs(px2[0, t, 0] - (z1 - lse)) < 1e-14
+    # LM only (a_lm = 1): px = log softmax(lm[u])[y_{u+1}] = log 3/4 at u = 0
+    px3, py3 = O.smoothed_joiner_logprobs(am2, lm, sym, [3], [1], 0, 1.0, 0.0)
+    np.testing.assert_allclose(px3[0, :3, 0], math.log(3 / 4), atol=1e-14)
+    np.testing.assert_allclose(py3[0, :3, 0], math.log(1 / 4), atol=1e-14)
+    np.testing.assert_allclose(py3[0, :3, 1], math.log(1 / 2), atol=1e-14)
 
 
 def test_smoothed_simple_loss_finite_difference():
