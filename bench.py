@@ -4,16 +4,22 @@
 One step is the whole path on one batch resident in HBM:
   trivial joiner + full-lattice forward/backward + d am, d lm (simple loss,
   scaled 0.5 as in Sec. 3.3), pruning bounds, the full joiner on the pruned
-  (t, u) pairs, the pruned recursion, and the joiner backward to d enc, d dec,
-  dW, db.
-The workload is the BPE-sized batch (N=16, T ~ U[150,250], U ~ U[20,60],
-V=500, S=5, J=512, fp32), synthetic and seeded; frames = sum of valid T_n.
+  (t, u) pairs, the pruned recursion, the joiner backward to d enc, d dec,
+  dW, db, and the training loss (0.5 simple + pruned, summed).
+No [N, T, S, V] array is kept: the joiner's forward reduces its logits to
+lse and the target / blank log-probs, and the backward recomputes them in
+chunks of rows whose size does not depend on N or T.
+The headline workload is the BPE-sized batch (N=16, T ~ U[150,250],
+U ~ U[20,60], V=500, S=5, J=512, fp32), synthetic and seeded; frames = sum of
+valid T_n.
 
 Prints one JSON line: frames/s, peak HBM bytes, the roofline of the dominant
 contraction (HIP events recorded by the library on the launch stream around
 that kernel only, during the timed steps), a per-kernel census from a short
-untimed pass with every launch bracketed, and the CPU oracle's throughput on
-the host cores.
+untimed pass with every launch bracketed, the same step with the logits kept
+between forward and backward (`kept_logits`), the long-batch workload (bf16
+joiner, V=500, S=5) measured the same way (`long`), and the CPU oracle's
+throughput on the host cores.
 """
 from __future__ import annotations
 
@@ -128,95 +134,85 @@ def _band_algorithms(P, batch, S, out, reps: int = 20) -> dict:
     return res
 
 
-def _cpu_baseline(b, S, budget_s: float, min_s: float = 10.0) -> dict:
-    """The CPU oracle (as is) on the utterances of the same batch, one thread,
-    in whole passes over the batch until at least min_s seconds of work (and
-    no further utterance once budget_s is spent)."""
-    import numpy as np
+_CPU_BATCH = None
+
+
+def _cpu_worker_init():
     from threadpoolctl import threadpool_limits
+    threadpool_limits(1)
+
+
+def _cpu_one(n):
+    """The oracle's whole path on utterance n of the batch (stages 1-4 with gradients)."""
+    import numpy as np
 
     import oracle as O
-    frames = 0
-    done = 0
-    t0 = time.perf_counter()
-    with threadpool_limits(1):
+    b = _CPU_BATCH
+    sl = slice(n, n + 1)
+    S = b.wl.S
+    s1 = O.simple_stage(b.am[sl], b.lm[sl], b.symbols[sl], b.t_len[sl], b.u_len[sl], b.wl.blank,
+                        scale=np.full(1, 0.5))
+    r = O.prune_ranges(s1["gx"], s1["gy"], b.t_len[sl], b.u_len[sl], S)
+    O.pruned_stage(b.enc[sl], b.dec[sl], b.W, b.bias, r, b.symbols[sl], b.t_len[sl], b.u_len[sl], b.wl.blank)
+    return int(b.t_len[n])
+
+
+def _cpu_baseline(b, budget_s: float) -> dict:
+    """The CPU oracle (as is) on the utterances of the same batch, one
+    utterance per task over a pool of worker processes (one BLAS thread
+    each, one per host core up to 16), in whole passes over the batch for
+    about budget_s seconds. Run before the GPU is touched (the workers are
+    forked)."""
+    import multiprocessing as mp
+    global _CPU_BATCH
+    _CPU_BATCH = b
+    workers = max(1, min(16, os.cpu_count() or 1))
+    ctx = mp.get_context("fork")
+    frames = done = 0
+    with ctx.Pool(workers, initializer=_cpu_worker_init) as pool:
+        t0 = time.perf_counter()
         while True:
-            n = done % b.N
-            sl = slice(n, n + 1)
-            s1 = O.simple_stage(b.am[sl], b.lm[sl], b.symbols[sl], b.t_len[sl], b.u_len[sl], b.wl.blank,
-                                scale=np.full(1, 0.5))
-            r = O.prune_ranges(s1["gx"], s1["gy"], b.t_len[sl], b.u_len[sl], S)
-            O.pruned_stage(b.enc[sl], b.dec[sl], b.W, b.bias, r, b.symbols[sl], b.t_len[sl], b.u_len[sl],
-                           b.wl.blank)
-            frames += int(b.t_len[n])
-            done += 1
-            el = time.perf_counter() - t0
-            if el > budget_s or (el > min_s and done % b.N == 0):
+            frames += sum(pool.map(_cpu_one, list(range(b.N)) * max(1, workers // b.N), chunksize=1))
+            done += b.N * max(1, workers // b.N)
+            if time.perf_counter() - t0 > budget_s:
                 break
-    dt = time.perf_counter() - t0
-    return {"value": round(frames / dt, 2), "unit": "frames/s", "cores": 1, "kind": "oracle",
+        dt = time.perf_counter() - t0
+    return {"value": round(frames / dt, 2), "unit": "frames/s", "cores": workers, "kind": "oracle",
             "sample": f"{done} utterance runs over the {b.N} utterances of the same batch ({frames} frames), "
                       f"full oracle path (trivial joiner, lattice, am/lm grads, bounds, pruned joiner, pruned "
-                      f"lattice, joiner grads), fp64 NumPy, 1 thread, {dt:.1f} s"}
+                      f"lattice, joiner grads), fp64 NumPy, {workers} processes with 1 BLAS thread each, "
+                      f"{dt:.1f} s"}
 
 
-def main() -> int:
-    ap = argparse.ArgumentParser(description=__doc__)
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="bpe", choices=sorted(WORKLOAD_TEXT))
-    ap.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of oracle work for cpu_baseline")
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-unpruned", action="store_true",
-                    help="skip the comparison with the unpruned loss (same joiner at every (t, u))")
-    ap.add_argument("--no-band-algorithms", action="store_true",
-                    help="skip timing the pruned recursion's algorithms one by one")
-    ap.add_argument("--copy-mib", type=int, default=0,
-                    help="before the census, run one device-to-device copy of this many MiB (a plain copy "
-                         "kernel of known size that scales rocprofv3's FETCH_SIZE / WRITE_SIZE)")
-    args = ap.parse_args()
-    world = int(os.environ.get("WORLD_SIZE", "1"))
-    if args.gpus != 1 or world != 1:
-        print("bench.py measures one GPU: the library has no multi-GPU path (the loss is per utterance, "
-              "so a batch shards over GPUs by utterance with no communication in the loss itself). "
-              "Run with --gpus 1.",
-              file=sys.stderr)
-        return 2
-
+def _measure(P, _native, b, args, keep_logits: bool, roofline: bool, census: bool, spread: bool) -> dict:
+    """One workload's step on the GPU: warm-up, optionally a census pass with
+    every kernel bracketed, then the timed steps (the dominant contraction
+    bracketed by HIP events on every BRACKET_EVERY-th step when `roofline`)."""
     import ctypes
 
     import numpy as np
     import torch
 
-    import paper_2206_13236_amd as P
-    from paper_2206_13236_amd import _native
-    from workloads import make_batch
-
-    assert torch.cuda.is_available(), "bench.py needs a ROCm GPU"
     dev = torch.device("cuda:0")
-    torch.cuda.set_device(dev)
-    torch.zeros(1, device=dev)
-    torch.cuda.synchronize()
-    b = make_batch(args.workload, seed=0)
     bf = b.wl.joiner_dtype == "bf16"
     S, J, V = b.wl.S, b.wl.J, b.V
     frames = b.frames
     M = S * frames
-
     f32 = lambda a: torch.from_numpy(np.ascontiguousarray(a, np.float32)).to(dev)
     i32 = lambda a: torch.from_numpy(np.ascontiguousarray(a, np.int32)).to(dev)
     jt = (lambda a: f32(a).to(torch.bfloat16)) if bf else f32
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
     torch.cuda.reset_peak_memory_stats(dev)
     base_mem = torch.cuda.memory_allocated(dev)
     batch = P.Batch(i32(b.t_len), i32(b.u_len), i32(b.symbols), b.T, b.U, b.wl.blank)
     am, lm = f32(b.am), f32(b.lm)
     enc, dec, W, bias = jt(b.enc), jt(b.dec), jt(b.W), jt(b.bias)
     inputs_mem = torch.cuda.memory_allocated(dev) - base_mem
-    step = P.PrunedRnntLoss(S, simple_scale=0.5)
-
+    step = P.PrunedRnntLoss(S, simple_scale=0.5, keep_logits=keep_logits)
+    run = lambda: step.step(batch, am, lm, enc, dec, W, bias)
     for _ in range(args.warmup):
-        step.step(batch, am, lm, enc, dec, W, bias)
+        run()
     torch.cuda.synchronize()
     L = _native.lib()
 
@@ -232,105 +228,181 @@ def main() -> int:
                          "us_per_step": round(1000 * tot.value / nsteps, 2)}
         return out
 
-    if args.copy_mib > 0:
-        src = torch.ones(args.copy_mib << 18, dtype=torch.float32, device=dev)
-        dst = torch.empty_like(src)
+    res = {}
+    kernels = None
+    if census or roofline:
+        if args.copy_mib > 0 and census:
+            src = torch.ones(args.copy_mib << 18, dtype=torch.float32, device=dev)
+            dst = torch.empty_like(src)
+            torch.cuda.synchronize()
+            dst.copy_(src)
+            torch.cuda.synchronize()
+            del src, dst
+        # census: every kernel bracketed by events, outside the timed region
+        # (the event packets themselves cost ~5 us per launch)
+        census_steps = max(1, min(args.steps, 5))
+        L.rnnt_profile_reset()
+        L.rnnt_profile_select(None)
+        L.rnnt_profile_enable(1)
+        for _ in range(census_steps):
+            run()
         torch.cuda.synchronize()
-        dst.copy_(src)
-        torch.cuda.synchronize()
-        del src, dst
-
-    # census: every kernel bracketed by events, outside the timed region (the
-    # event packets themselves cost ~5 us per launch)
-    census_steps = max(1, min(args.steps, 5))
-    L.rnnt_profile_reset()
-    L.rnnt_profile_select(None)
-    L.rnnt_profile_enable(1)
-    for _ in range(census_steps):
-        step.step(batch, am, lm, enc, dec, W, bias)
-    torch.cuda.synchronize()
-    L.rnnt_profile_enable(0)
-    kernels = kernel_table(census_steps)
-    launches_per_step = {k: v["launches"] / census_steps for k, v in kernels.items()}
-    L.rnnt_profile_reset()
-    # the dominant contraction: joiner GEMMs with algorithmic work 2*M*J*V each
-    # (a recompute of the logits in the backward would be overhead, not work)
+        L.rnnt_profile_enable(0)
+        kernels = kernel_table(census_steps)
+        L.rnnt_profile_reset()
+        if census:
+            res["kernels"] = kernels
+            res["kernels_census_steps"] = census_steps
+    # the dominant contraction: joiner GEMMs with algorithmic work 2*M*J*V
+    # each (the backward's recomputation of the logits is overhead, not work)
     work = {"joiner_fwd": 2.0 * M * J * V, "joiner_dh": 2.0 * M * J * V, "joiner_dw": 2.0 * M * J * V}
-    dom = max((k for k in work if k in kernels), key=lambda k: kernels[k]["us_per_step"])
-
-    # timed region: events around the dominant kernel only, on every
-    # BRACKET_EVERY-th step (an event pair costs a few microseconds of
-    # pipeline bubble; the others run unbracketed)
-    L.rnnt_profile_select(dom.encode())
+    dom = None
+    if roofline:
+        dom = max((k for k in work if k in kernels), key=lambda k: kernels[k]["us_per_step"])
+        L.rnnt_profile_select(dom.encode())
     stream = torch.cuda.current_stream()
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     ev0.record(stream)
     for i in range(args.steps):
-        L.rnnt_profile_enable(1 if i % BRACKET_EVERY == BRACKET_EVERY - 1 or args.steps < BRACKET_EVERY else 0)
-        step.step(batch, am, lm, enc, dec, W, bias)
+        if roofline:
+            L.rnnt_profile_enable(1 if i % BRACKET_EVERY == BRACKET_EVERY - 1 or args.steps < BRACKET_EVERY else 0)
+        run()
     ev1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     L.rnnt_profile_enable(0)
     ms_total = ev0.elapsed_time(ev1)
-    ms_step = ms_total / args.steps
     peak = torch.cuda.max_memory_allocated(dev) - base_mem
+    res.update({"value": round(frames * args.steps / (ms_total / 1000.0), 1),
+                "ms_per_step": round(ms_total / args.steps, 4), "peak_hbm_bytes": int(peak),
+                "peak_hbm_bytes_excl_inputs": int(peak - inputs_mem), "wall_s_timed": round(wall, 3),
+                "frames": frames, "rows_M": M, "dtype": "bf16" if bf else "f32"})
+    if roofline:
+        timed = kernel_table(args.steps)[dom]
+        L.rnnt_profile_reset()
+        L.rnnt_profile_select(None)
+        per_launch_flops = work[dom] / (kernels[dom]["launches"] / res.get("kernels_census_steps", 5))
+        achieved = per_launch_flops / (timed["avg_us"] * 1e-6) / 1e12
+        dt = res["dtype"]
+        res["roofline"] = {"kernel": dom, "bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_TFLOPS[dt],
+                           "unit": "TFLOP/s", "frac": round(achieved / PEAK_TFLOPS[dt], 4),
+                           "traffic": _traffic(dom, b.wl.name),
+                           "algorithmic_flops_per_launch": per_launch_flops, "avg_launch_us": timed["avg_us"],
+                           "launches_timed": timed["launches"],
+                           "bracketed_steps": f"every {BRACKET_EVERY}th timed step"}
+    if spread:
+        # step-time spread (after the timed region): each step bracketed on its own
+        per_step = []
+        for _ in range(args.steps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            run()
+            e1.record(stream)
+            e1.synchronize()
+            per_step.append(e0.elapsed_time(e1))
+        q = np.percentile(np.asarray(per_step), [10, 50, 90])
+        res["ms_per_step_spread"] = {"p10": round(float(q[0]), 4), "median": round(float(q[1]), 4),
+                                     "p90": round(float(q[2]), 4), "steps": len(per_step),
+                                     "note": "each step bracketed by its own events, after the timed region"}
+    res["_ctx"] = (step, batch, enc, dec, W, bias, run)
+    return res
 
-    timed = kernel_table(args.steps)[dom]
-    L.rnnt_profile_reset()
-    L.rnnt_profile_select(None)
-    per_launch_flops = work[dom] / (launches_per_step[dom])
-    achieved = per_launch_flops / (timed["avg_us"] * 1e-6) / 1e12
-    dt = "bf16" if bf else "f32"
-    roofline = {"kernel": dom, "bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_TFLOPS[dt],
-                "unit": "TFLOP/s", "frac": round(achieved / PEAK_TFLOPS[dt], 4),
-                "traffic": _traffic(dom, args.workload),
-                "algorithmic_flops_per_launch": per_launch_flops, "avg_launch_us": timed["avg_us"],
-                "launches_timed": timed["launches"], "bracketed_steps": f"every {BRACKET_EVERY}th timed step"}
 
-    # step-time spread (after the timed region): each step bracketed on its own
-    per_step = []
-    for _ in range(args.steps):
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        step.step(batch, am, lm, enc, dec, W, bias)
-        e1.record(stream)
-        e1.synchronize()
-        per_step.append(e0.elapsed_time(e1))
-    q = np.percentile(np.asarray(per_step), [10, 50, 90])
-    spread = {"p10": round(float(q[0]), 4), "median": round(float(q[1]), 4), "p90": round(float(q[2]), 4),
-              "steps": len(per_step), "note": "each step bracketed by its own events, after the timed region"}
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="bpe", choices=sorted(WORKLOAD_TEXT))
+    ap.add_argument("--keep-logits", action="store_true",
+                    help="headline step with the [N,T,S,V] logits kept between forward and backward")
+    ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work for cpu_baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-unpruned", action="store_true",
+                    help="skip the comparison with the unpruned loss (same joiner at every (t, u))")
+    ap.add_argument("--no-band-algorithms", action="store_true",
+                    help="skip timing the pruned recursion's algorithms one by one")
+    ap.add_argument("--no-extra", action="store_true",
+                    help="skip the kept-logits step and the long-batch workload")
+    ap.add_argument("--copy-mib", type=int, default=0,
+                    help="before the census, run one device-to-device copy of this many MiB (a plain copy "
+                         "kernel of known size that scales rocprofv3's FETCH_SIZE / WRITE_SIZE)")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU: the library has no multi-GPU path (the loss is per utterance, "
+              "so a batch shards over GPUs by utterance with no communication in the loss itself). "
+              "Run with --gpus 1.",
+              file=sys.stderr)
+        return 2
 
-    band = None if args.no_band_algorithms else _band_algorithms(P, batch, S,
-                                                                 step.step(batch, am, lm, enc, dec, W, bias))
-    unpruned = None if args.no_unpruned else _unpruned(P, batch, enc, dec, W, bias, frames, dev)
-    cpu = None if args.no_cpu_baseline else _cpu_baseline(b, S, args.cpu_budget)
+    from workloads import make_batch
+    b = make_batch(args.workload, seed=0)
+    # the CPU baseline first, in forked workers, before anything touches the GPU
+    cpu = None if args.no_cpu_baseline else _cpu_baseline(b, args.cpu_budget)
+
+    import torch
+
+    import paper_2206_13236_amd as P
+    from paper_2206_13236_amd import _native
+
+    assert torch.cuda.is_available(), "bench.py needs a ROCm GPU"
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    torch.zeros(1, device=dev)
+    torch.cuda.synchronize()
+
+    head = _measure(P, _native, b, args, keep_logits=args.keep_logits, roofline=True, census=True, spread=True)
+    step, batch, enc, dec, W, bias, run = head.pop("_ctx")
+    band = None if args.no_band_algorithms else _band_algorithms(P, batch, b.wl.S, run())
+    unpruned = None if args.no_unpruned else _unpruned(P, batch, enc, dec, W, bias, b.frames, dev)
+    del step, batch, enc, dec, W, bias, run
+    extra = {}
+    if not args.no_extra:
+        # the same workload with the logits kept (one GEMM less, [N,T,S,V] more memory)
+        k = _measure(P, _native, b, args, keep_logits=not args.keep_logits, roofline=False, census=False,
+                     spread=False)
+        k.pop("_ctx")
+        extra["kept_logits" if not args.keep_logits else "recomputed_logits"] = {
+            "what": "same step with the [N,T,S,V] logits " + ("kept" if not args.keep_logits else "not kept"),
+            **{key: k[key] for key in ("value", "ms_per_step", "peak_hbm_bytes", "peak_hbm_bytes_excl_inputs")}}
+        if args.workload != "long":
+            bl = make_batch("long", seed=0)
+            lg = _measure(P, _native, bl, args, keep_logits=args.keep_logits, roofline=True, census=False,
+                          spread=False)
+            lg.pop("_ctx")
+            extra["long"] = {"workload": WORKLOAD_TEXT["long"], "frames_per_step": bl.frames,
+                             **{key: lg[key] for key in ("value", "ms_per_step", "peak_hbm_bytes",
+                                                         "peak_hbm_bytes_excl_inputs", "dtype", "roofline")}}
+    S, J, V = b.wl.S, b.wl.J, b.V
     line = {
         "metric": "pruned RNN-T loss fwd+bwd frames/sec at V=500,S=5; peak HBM bytes",
-        "value": round(frames * args.steps / (ms_total / 1000.0), 1),
+        "value": head["value"],
         "unit": "frames/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(ms_step, 4),
-        "ms_per_step_spread": spread,
+        "ms_per_step": head["ms_per_step"],
+        "ms_per_step_spread": head["ms_per_step_spread"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32" if not bf else "bf16",
+        "dtype": head["dtype"],
         "data": "synthetic",
-        "config": {"workload": WORKLOAD_TEXT[args.workload], "frames_per_step": frames, "rows_M": M,
-                   "N": b.N, "T": b.T, "U": b.U, "V": V, "S": S, "J": J, "seed": 0},
-        "peak_hbm_bytes": int(peak),
-        "peak_hbm_bytes_excl_inputs": int(peak - inputs_mem),
-        "wall_s_timed": round(wall, 3),
-        "roofline": roofline,
+        "config": {"workload": WORKLOAD_TEXT[args.workload], "frames_per_step": b.frames, "rows_M": head["rows_M"],
+                   "N": b.N, "T": b.T, "U": b.U, "V": V, "S": S, "J": J, "seed": 0,
+                   "logits_kept": bool(args.keep_logits)},
+        "peak_hbm_bytes": head["peak_hbm_bytes"],
+        "peak_hbm_bytes_excl_inputs": head["peak_hbm_bytes_excl_inputs"],
+        "wall_s_timed": head["wall_s_timed"],
+        "roofline": head["roofline"],
+        **extra,
         "band_algorithms": band,
         "unpruned": unpruned,
-        "kernels": kernels,
-        "kernels_census_steps": census_steps,
+        "kernels": head["kernels"],
+        "kernels_census_steps": head["kernels_census_steps"],
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)

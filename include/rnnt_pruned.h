@@ -23,6 +23,11 @@
  *      rnnt_pruned_joiner_backward
  *                              the pruned loss's gradients w.r.t. the joiner
  *                              inputs and parameters.
+ *   4. rnnt_combine_losses     the training loss of Sec. 3.3: the scaled sum
+ *                              of the simple and the pruned losses, per
+ *                              utterance and summed or averaged.
+ *   rnnt_validate_inputs       a synchronous check of a batch against the
+ *                              problem statement of Sec. 2 (debugging aid).
  *
  * Conventions shared by every entry point
  * ---------------------------------------
@@ -30,7 +35,8 @@
  *   caller owns all memory; the library never allocates or frees device
  *   memory and keeps no state between calls.
  * - Every call only enqueues kernels on `stream` (a hipStream_t; NULL = the
- *   null stream) and returns without synchronising.
+ *   null stream) and returns without synchronising (except the debugging
+ *   aid rnnt_validate_inputs, which waits for its result).
  * - Scalars and pointers are checked on the host before any launch; a failed
  *   check returns a non-zero status and enqueues nothing. The message is
  *   available from rnnt_last_error() (thread-local).
@@ -254,9 +260,12 @@ size_t rnnt_pruned_joiner_backward_workspace_size(int32_t N, int32_t T, int32_t 
                                                   int32_t J, int32_t V, int32_t dtype);
 
 /* Gradients of sum_n scale[n] * pruned_loss[n] through the log-softmax, the
- * projection, tanh and the sum enc + dec, in row chunks: d(logits) is held
- * for one chunk at a time and never for the whole [N, T, S, V] at once
- * unless it fits the chunk.
+ * projection, tanh and the sum enc + dec, in chunks of rows (the S rows of
+ * every valid frame, frames in batch order): d(logits), h and the d dec
+ * pieces are held for one chunk at a time. The chunk's size depends on J, V
+ * and the dtype only, never on N or T (8,192 to 16,384 rows: d(logits) of
+ * about 16 MiB at V = 500), so without the forward's logits no [N, T, S, V]
+ * array exists at any time.
  *
  * lse, px_occ, py_occ [N, T, S]: from rnnt_pruned_joiner / rnnt_pruned_loss.
  * logits [N, T, S, V] (nullable): the logits stored by rnnt_pruned_joiner
@@ -274,6 +283,84 @@ int rnnt_pruned_joiner_backward(const rnnt_batch* batch, int32_t S, int32_t J, i
                                 const float* scale, float* enc_grad, float* dec_grad,
                                 float* W_grad, float* bias_grad, float* logits_grad,
                                 void* workspace, size_t workspace_bytes, void* stream);
+
+/* Workspace bytes for rnnt_pruned_joiner_backward_ex with this chunk size
+ * (0 = the library's choice; 0 is returned for an invalid chunk size). */
+size_t rnnt_pruned_joiner_backward_ex_workspace_size(int32_t N, int32_t T, int32_t U, int32_t S,
+                                                     int32_t J, int32_t V, int32_t dtype,
+                                                     int32_t chunk_rows);
+
+/* rnnt_pruned_joiner_backward with an explicit chunk size: chunk_rows rows
+ * (a positive multiple of 128, at most what keeps each chunk buffer below
+ * 2^31 bytes: RNNT_EUNSUPPORTED beyond), or 0 for the library's choice. The
+ * results do not depend on the chunk size (the reductions keep their order
+ * across chunks); a smaller chunk holds less memory and launches more
+ * kernels. Everything else is as in rnnt_pruned_joiner_backward. */
+int rnnt_pruned_joiner_backward_ex(const rnnt_batch* batch, int32_t S, int32_t J, int32_t V,
+                                   int32_t dtype, int32_t chunk_rows, const void* enc,
+                                   const void* dec, const void* W, const void* bias,
+                                   const int32_t* ranges, const float* lse, const float* logits,
+                                   const float* px_occ, const float* py_occ, const float* scale,
+                                   float* enc_grad, float* dec_grad, float* W_grad,
+                                   float* bias_grad, float* logits_grad, void* workspace,
+                                   size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* The training loss (Sec. 3.3)                                              */
+/* ------------------------------------------------------------------------ */
+
+#define RNNT_REDUCE_SUM 0
+#define RNNT_REDUCE_MEAN 1
+
+/* The paper trains on a weighted sum of the simple loss (Sec. 3.1) and the
+ * pruned loss (Sec. 3.2), Sec. 3.3 (0.5 and 1 in its experiments):
+ *   loss[n] = simple_scale * simple_loss[n] + pruned_scale * pruned_loss[n]
+ * and total[0] = sum_n loss[n] (RNNT_REDUCE_SUM) or that sum / N
+ * (RNNT_REDUCE_MEAN), accumulated in fp64 in a fixed order. A term whose
+ * scale is 0 contributes exactly 0, whatever its loss (the pruned part is
+ * switched off during the warm-up of Sec. 4; pruned_loss may then be NULL).
+ * simple_loss, pruned_loss [N] fp32 device (each required when its scale is
+ * non-zero); scales >= 0; outputs loss [N] and total [1] fp32 device, at
+ * least one given. Asynchronous on `stream`; no workspace. */
+int rnnt_combine_losses(int32_t N, const float* simple_loss, const float* pruned_loss,
+                        float simple_scale, float pruned_scale, int32_t reduction,
+                        float* loss, float* total, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Input validation (debugging aid; synchronous)                             */
+/* ------------------------------------------------------------------------ */
+
+/* Bits of the per-utterance flags written by rnnt_validate_inputs. */
+#define RNNT_FLAG_T_LEN 1     /* t_len[n] outside [1, T]                                 */
+#define RNNT_FLAG_U_LEN 2     /* u_len[n] outside [0, U]                                 */
+#define RNNT_FLAG_SYMBOL 4    /* some y_{u+1}, u < U_n, outside [0, V)                   */
+#define RNNT_FLAG_AM 8        /* am[n, t, v] not finite for some t < T_n                 */
+#define RNNT_FLAG_LM 16       /* lm[n, u, v] not finite for some u <= U_n                */
+#define RNNT_FLAG_ENC 32      /* enc[n, t, j] not finite for some t < T_n                */
+#define RNNT_FLAG_DEC 64      /* dec[n, u, j] not finite for some u <= U_n               */
+#define RNNT_FLAG_NO_BAND 128 /* U_n > (S-1) T_n: no complete path fits a band of width S
+                                 (the pruned loss is then +inf)                         */
+
+/* Checks every utterance of a batch against the problem statement of Sec. 2:
+ * T_n frames with 1 <= T_n <= T, U_n tokens with 0 <= U_n <= U, each token
+ * y_1..y_{U_n} in [0, V) (y_0 is the blank, Sec. 2), finite scores on the
+ * utterance's own frames and tokens (padding is not inspected), and, for
+ * S > 0, that a band of width S can hold a complete path (Sec. 3.2.2:
+ * Eqs. (9)-(10) with p_0 = 0 allow at most U_n <= (S-1) T_n). The other
+ * entry points never fail on such data (an utterance that breaks the
+ * statement gets a NaN loss, an infeasible band +inf); this call says why.
+ *
+ * am [N, T, V], lm [N, U+1, V] fp32 and enc [N, T, J], dec [N, U+1, J]
+ * (dtype RNNT_F32 or RNNT_BF16) are device pointers, each nullable (not
+ * inspected). S = 0 skips the band check; J and dtype are read only with enc
+ * or dec. flags [N] int32 device (required): the RNNT_FLAG_* bits of each
+ * utterance, 0 when it is valid. n_bad (host, nullable): the number of
+ * utterances with a non-zero flag. Enqueues on `stream` and waits for it
+ * (synchronous), so it is not meant for a training loop's hot path.
+ */
+int rnnt_validate_inputs(const rnnt_batch* batch, int32_t V, int32_t S, int32_t J, int32_t dtype,
+                         const float* am, const float* lm, const void* enc, const void* dec,
+                         int32_t* flags, int32_t* n_bad, void* stream);
 
 /* ------------------------------------------------------------------------ */
 /* For comparison: the unpruned loss with the same joiner                    */

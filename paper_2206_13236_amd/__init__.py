@@ -15,7 +15,8 @@ from typing import Optional
 import torch
 
 from ._native import (RNNT_BF16, RNNT_EHIP, RNNT_EINVAL, RNNT_EUNSUPPORTED, RNNT_EWORKSPACE,  # noqa: F401
-                      RNNT_F32, RNNT_OK, RnntBatch, RnntError, check, lib)
+                      RNNT_F32, RNNT_FLAGS, RNNT_OK, RNNT_REDUCE_MEAN, RNNT_REDUCE_SUM, RnntBatch, RnntError,
+                      check, lib)
 
 __all__ = [
     "Batch", "RnntError", "rnnt_simple_loss", "rnnt_simple_loss_backward", "rnnt_prune_ranges",
@@ -23,6 +24,7 @@ __all__ = [
     "rnnt_pruned_loss", "rnnt_pruned_joiner_backward", "simple_loss_workspace_size",
     "pruned_joiner_workspace_size", "pruned_loss_workspace_size", "BAND_ALGORITHMS",
     "pruned_joiner_backward_workspace_size", "PrunedRnntLoss", "RNNT_F32", "RNNT_BF16",
+    "rnnt_combine_losses", "rnnt_validate_inputs", "RNNT_FLAGS",
 ]
 
 
@@ -109,8 +111,10 @@ def pruned_loss_workspace_size(N, T, U, S, algorithm=None, chunk=0) -> int:
     return int(lib().rnnt_pruned_loss_ex_workspace_size(N, T, U, S, BAND_ALGORITHMS[algorithm], chunk))
 
 
-def pruned_joiner_backward_workspace_size(N, T, U, S, J, V, dtype) -> int:
-    return int(lib().rnnt_pruned_joiner_backward_workspace_size(N, T, U, S, J, V, dtype))
+def pruned_joiner_backward_workspace_size(N, T, U, S, J, V, dtype, chunk_rows: int = 0) -> int:
+    if chunk_rows == 0:
+        return int(lib().rnnt_pruned_joiner_backward_workspace_size(N, T, U, S, J, V, dtype))
+    return int(lib().rnnt_pruned_joiner_backward_ex_workspace_size(N, T, U, S, J, V, dtype, chunk_rows))
 
 
 # --------------------------------------------------------------------------
@@ -233,7 +237,9 @@ def rnnt_pruned_loss(batch: Batch, S: int, px: torch.Tensor, py: torch.Tensor, r
 def rnnt_pruned_joiner_backward(batch: Batch, S: int, enc, dec, W, bias, ranges, lse, px_occ, py_occ,
                                 scale=None, enc_grad=None, dec_grad=None, W_grad=None, bias_grad=None,
                                 logits_grad=None, workspace=None, stream=None, want_param_grads=True,
-                                want_logits_grad=False, logits=None) -> dict:
+                                want_logits_grad=False, logits=None, chunk_rows: int = 0) -> dict:
+    """The joiner backward; chunk_rows != 0 (a multiple of 128) selects
+    rnnt_pruned_joiner_backward_ex with that chunk size."""
     N, T, U = batch.N, batch.T, batch.U
     J, V = int(W.shape[0]), int(W.shape[1])
     dt = _jdtype(W)
@@ -251,13 +257,63 @@ def rnnt_pruned_joiner_backward(batch: Batch, S: int, enc, dec, W, bias, ranges,
         W_grad, bias_grad = torch.empty(J, V, **f32), torch.empty(V, **f32)
     if want_logits_grad and logits_grad is None:
         logits_grad = torch.empty(N, T, S, V, **f32)
-    ws = _ws(pruned_joiner_backward_workspace_size(N, T, U, S, J, V, dt), batch.device, workspace)
-    check(lib().rnnt_pruned_joiner_backward(
-        batch.c, S, J, V, dt, _p(enc), _p(dec), _p(W), _p(bias), _p(ranges), _p(lse), _p(logits), _p(px_occ),
-        _p(py_occ), _p(scale), _p(enc_grad), _p(dec_grad), _p(W_grad), _p(bias_grad), _p(logits_grad),
-        _p(ws), ws.numel(), _stream(stream)))
+    ws = _ws(pruned_joiner_backward_workspace_size(N, T, U, S, J, V, dt, chunk_rows), batch.device, workspace)
+    rest = (_p(enc), _p(dec), _p(W), _p(bias), _p(ranges), _p(lse), _p(logits), _p(px_occ), _p(py_occ), _p(scale),
+            _p(enc_grad), _p(dec_grad), _p(W_grad), _p(bias_grad), _p(logits_grad), _p(ws), ws.numel(),
+            _stream(stream))
+    if chunk_rows == 0:
+        check(lib().rnnt_pruned_joiner_backward(batch.c, S, J, V, dt, *rest))
+    else:
+        check(lib().rnnt_pruned_joiner_backward_ex(batch.c, S, J, V, dt, int(chunk_rows), *rest))
     return {"enc_grad": enc_grad, "dec_grad": dec_grad, "W_grad": W_grad, "bias_grad": bias_grad,
             "logits_grad": logits_grad}
+
+
+_REDUCTIONS = {"sum": RNNT_REDUCE_SUM, "mean": RNNT_REDUCE_MEAN}
+
+
+def rnnt_combine_losses(simple_loss: Optional[torch.Tensor], pruned_loss: Optional[torch.Tensor],
+                        simple_scale: float, pruned_scale: float, reduction: str = "sum", loss=None, total=None,
+                        stream=None) -> dict:
+    """The training loss of Sec. 3.3 per utterance and summed (or averaged), in the library."""
+    ref = simple_loss if simple_loss is not None else pruned_loss
+    N = int(ref.shape[0])
+    for name, t in (("simple_loss", simple_loss), ("pruned_loss", pruned_loss)):
+        if t is not None:
+            _need(t, name, torch.float32, (N,))
+    f32 = dict(dtype=torch.float32, device=ref.device)
+    loss = torch.empty(N, **f32) if loss is None else loss
+    total = torch.empty((), **f32) if total is None else total
+    check(lib().rnnt_combine_losses(N, _p(simple_loss), _p(pruned_loss), float(simple_scale), float(pruned_scale),
+                                    _REDUCTIONS[reduction], _p(loss), _p(total), _stream(stream)))
+    return {"loss": loss, "total": total}
+
+
+def rnnt_validate_inputs(batch: Batch, V: int, S: int = 0, am=None, lm=None, enc=None, dec=None, flags=None,
+                         stream=None) -> dict:
+    """Synchronous check of a batch (Sec. 2's problem statement; the band
+    condition for S > 0). Returns the per-utterance flag tensor, the number of
+    flagged utterances and, per flagged utterance, the names of its flags."""
+    N, T, U = batch.N, batch.T, batch.U
+    if am is not None:
+        _need(am, "am", torch.float32, (N, T, V))
+    if lm is not None:
+        _need(lm, "lm", torch.float32, (N, U + 1, V))
+    J, dt = 0, RNNT_F32
+    if enc is not None or dec is not None:
+        ref = enc if enc is not None else dec
+        J, dt = int(ref.shape[-1]), _jdtype(ref)
+        if enc is not None:
+            _need(enc, "enc", ref.dtype, (N, T, J))
+        if dec is not None:
+            _need(dec, "dec", ref.dtype, (N, U + 1, J))
+    flags = torch.empty(N, dtype=torch.int32, device=batch.device) if flags is None else flags
+    n_bad = ctypes.c_int32(0)
+    check(lib().rnnt_validate_inputs(batch.c, V, S, J, dt, _p(am), _p(lm), _p(enc), _p(dec), _p(flags),
+                                     ctypes.byref(n_bad), _stream(stream)))
+    fl = flags.cpu().tolist()
+    bad = {n: [k for k, bit in RNNT_FLAGS.items() if f & bit] for n, f in enumerate(fl) if f}
+    return {"flags": flags, "n_bad": int(n_bad.value), "bad": bad}
 
 
 def full_loss_workspace_size(N, T, U, J, V, dtype) -> int:
@@ -310,17 +366,23 @@ class PrunedRnntLoss:
     disabled until the simple loss gives useful bounds) the pruned stages are
     skipped and their loss and gradients are zero.
 
-    With ``keep_logits`` the pruned logits [N, T, S, V] are kept between the
-    joiner's forward and backward (the method's own memory footprint);
-    without it the backward recomputes them and holds one row chunk at a time.
+    By default no [N, T, S, V] array is kept: the backward recomputes the
+    logits in chunks of rows whose size does not depend on N or T. With
+    ``keep_logits`` the pruned logits [N, T, S, V] are stored by the forward
+    and streamed by the backward instead (one GEMM less, the logits' memory
+    more). ``bwd_chunk_rows`` (a multiple of 128, 0 = the library's choice)
+    sets the backward's chunk.
+
+    ``step`` also returns the training loss per utterance (``loss``) and its
+    sum or mean (``total``), formed by the library (rnnt_combine_losses).
 
     ``lm_only_scale`` and ``am_only_scale`` smooth the simple loss's joiner
     (Sec. 3.3.1); both 0 gives the plain trivial joiner.
     """
 
     def __init__(self, S: int, simple_scale: float = 0.5, pruned_scale: float = 1.0,
-                 keep_logits: bool = True, overlap: bool = True, lm_only_scale: float = 0.0,
-                 am_only_scale: float = 0.0):
+                 keep_logits: bool = False, overlap: bool = True, lm_only_scale: float = 0.0,
+                 am_only_scale: float = 0.0, bwd_chunk_rows: int = 0):
         self.S = int(S)
         self.simple_scale = float(simple_scale)
         self.pruned_scale = float(pruned_scale)
@@ -328,6 +390,7 @@ class PrunedRnntLoss:
         self.am_only_scale = float(am_only_scale)
         self.keep_logits = bool(keep_logits)
         self.overlap = bool(overlap)
+        self.bwd_chunk_rows = int(bwd_chunk_rows)
         self._cache = {}
         self._side = {}
 
@@ -344,8 +407,10 @@ class PrunedRnntLoss:
             self._side[key] = (torch.cuda.Stream(device=device), torch.cuda.Event(), torch.cuda.Event())
         return self._side[key]
 
-    def step(self, batch: Batch, am, lm, enc, dec, W, bias=None, stream=None, out=None) -> dict:
-        """Run one step; ``out`` optionally maps output names to caller-owned tensors."""
+    def step(self, batch: Batch, am, lm, enc, dec, W, bias=None, stream=None, out=None,
+             reduction: str = "sum") -> dict:
+        """Run one step; ``out`` optionally maps output names to caller-owned
+        tensors; ``reduction`` ("sum" or "mean") is that of ``total``."""
         N, T, U, S = batch.N, batch.T, batch.U, self.S
         V = int(am.shape[2])
         J = int(W.shape[0])
@@ -362,7 +427,8 @@ class PrunedRnntLoss:
         ws_s = self._buf("ws_simple", (simple_loss_workspace_size(N, T, U, V),), torch.uint8, dev)
         ws_p = self._buf("ws_pruned", (max(pruned_joiner_workspace_size(N, T, S, J, V, dt),
                                            pruned_loss_workspace_size(N, T, U, S),
-                                           pruned_joiner_backward_workspace_size(N, T, U, S, J, V, dt)),),
+                                           pruned_joiner_backward_workspace_size(N, T, U, S, J, V, dt,
+                                                                                 self.bwd_chunk_rows)),),
                          torch.uint8, dev)
         ssc = self._buf("ssc", (N,), f32, dev)
         psc = self._buf("psc", (N,), f32, dev)
@@ -395,6 +461,8 @@ class PrunedRnntLoss:
                 for t in (pl, enc_grad, dec_grad, W_grad, bias_grad):
                     t.zero_()
             res["pruned_loss"] = pl
+            res.update(rnnt_combine_losses(sim["loss"], None, self.simple_scale, 0.0, reduction,
+                                           loss=o("loss", (N,)), total=o("total", ()), stream=main))
             return res
 
         ranges = rnnt_prune_ranges(batch, S, sim["px_occ"], sim["py_occ"], ranges=o("ranges", (N, T, S), torch.int32),
@@ -416,7 +484,9 @@ class PrunedRnntLoss:
         rnnt_pruned_joiner_backward(
             batch, S, enc, dec, W, bias, ranges, jo["lse"], pl["px_occ"], pl["py_occ"], scale=psc,
             enc_grad=enc_grad, dec_grad=dec_grad, W_grad=W_grad, bias_grad=bias_grad, workspace=ws_p,
-            stream=main, logits=logits)
+            stream=main, logits=logits, chunk_rows=self.bwd_chunk_rows)
+        res.update(rnnt_combine_losses(sim["loss"], pl["loss"], self.simple_scale, self.pruned_scale, reduction,
+                                       loss=o("loss", (N,)), total=o("total", ()), stream=main))
         if self.overlap:
             main.wait_event(join)
         res.update(pruned_loss=pl["loss"], ranges=ranges, px=jo["px"], py=jo["py"], lse=jo["lse"],
@@ -435,11 +505,9 @@ class _PrunedRnntFunction(torch.autograd.Function):
         fresh = {"am_grad": torch.empty(N, T, V, **f32), "lm_grad": torch.empty(N, U + 1, V, **f32),
                  "enc_grad": torch.empty(N, T, J, **f32), "dec_grad": torch.empty(N, U + 1, J, **f32),
                  "W_grad": torch.empty(J, V, **f32), "bias_grad": torch.empty(V, **f32)}
-        r = module.step(batch, am, lm, enc, dec, W, bias, out=fresh)
-        per_utt = module.simple_scale * r["simple_loss"] + module.pruned_scale * r["pruned_loss"]
-        loss = per_utt.sum()
-        if reduction == "mean":
-            loss = loss / N
+        fresh["total"] = torch.empty((), **f32)
+        r = module.step(batch, am, lm, enc, dec, W, bias, out=fresh, reduction=reduction)
+        loss = r["total"]
         ctx.reduction = reduction
         ctx.N = N
         ctx.has_bias = bias is not None

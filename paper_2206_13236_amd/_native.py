@@ -21,6 +21,14 @@ RNNT_EHIP = 4
 RNNT_F32 = 0
 RNNT_BF16 = 1
 
+RNNT_REDUCE_SUM = 0
+RNNT_REDUCE_MEAN = 1
+
+# bits of the per-utterance flags of rnnt_validate_inputs
+RNNT_FLAGS = {
+    "t_len": 1, "u_len": 2, "symbol": 4, "am": 8, "lm": 16, "enc": 32, "dec": 64, "no_band": 128,
+}
+
 
 class RnntBatch(ctypes.Structure):
     _fields_ = [
@@ -62,6 +70,16 @@ SIGNATURES = {
                                               c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
                                               c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
                                               c_void_p, c_size_t, c_void_p]),
+    "rnnt_pruned_joiner_backward_ex_workspace_size": (c_size_t, [c_int32] * 8),
+    "rnnt_pruned_joiner_backward_ex": (c_int32, [POINTER(RnntBatch), c_int32, c_int32, c_int32, c_int32, c_int32,
+                                                 c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
+                                                 c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
+                                                 c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
+                                                 c_void_p, c_size_t, c_void_p]),
+    "rnnt_combine_losses": (c_int32, [c_int32, c_void_p, c_void_p, c_float, c_float, c_int32, c_void_p, c_void_p,
+                                      c_void_p]),
+    "rnnt_validate_inputs": (c_int32, [POINTER(RnntBatch), c_int32, c_int32, c_int32, c_int32, c_void_p, c_void_p,
+                                       c_void_p, c_void_p, c_void_p, POINTER(c_int32), c_void_p]),
     "rnnt_full_loss_workspace_size": (c_size_t, [c_int32] * 6),
     "rnnt_full_loss": (c_int32, [POINTER(RnntBatch), c_int32, c_int32, c_int32, c_void_p, c_void_p, c_void_p,
                                  c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,

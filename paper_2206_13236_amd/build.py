@@ -18,7 +18,8 @@ BUILD_DIR = os.path.join(ROOT, "_build")
 LIB_NAME = "librnnt_pruned.so"
 LIB_PATH = os.path.join(PKG, LIB_NAME)
 
-SOURCES = ["abi.cpp", "prof.cpp", "simple.hip", "lattice.hip", "prune.hip", "joiner.hip", "band.hip", "scan.hip"]
+SOURCES = ["abi.cpp", "prof.cpp", "simple.hip", "lattice.hip", "prune.hip", "joiner.hip", "band.hip", "scan.hip",
+           "utterance.hip"]
 
 ARCH = os.environ.get("RNNT_OFFLOAD_ARCH", "gfx950")
 

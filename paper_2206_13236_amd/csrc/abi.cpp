@@ -6,6 +6,7 @@
 #include <stdio.h>
 
 #include <string>
+#include <vector>
 
 #include "kernels.h"
 #include "rnnt_pruned.h"
@@ -231,13 +232,13 @@ struct JoinerBwdWs {
   size_t bytes;
 };
 
-JoinerBwdWs joiner_bwd_layout(void* base, int N, int T, int S, int J, int V, int bf16) {
+JoinerBwdWs joiner_bwd_layout(void* base, int N, int T, int S, int J, int V, int bf16, int chunk_request = 0) {
   Carve c(base);
   JoinerBwdWs w;
   const size_t M = (size_t)N * T * S;
-  w.chunk_rows = joiner_bwd_chunk_rows(N, T, S, J, V, bf16);
+  w.chunk_rows = joiner_bwd_chunk_rows(N, T, S, J, V, bf16, chunk_request);
   w.splits = joiner_bwd_splits(J, V);
-  w.n_db_rows = joiner_db_rows(N, T, S);
+  w.n_db_rows = joiner_db_rows(w.chunk_rows);
   w.frame_off = c.take<int>((size_t)N + 1);
   w.frame_nt = c.take<int>((size_t)N * T);
   w.frame_p = c.take<int>((size_t)N * T);
@@ -246,7 +247,7 @@ JoinerBwdWs joiner_bwd_layout(void* base, int N, int T, int S, int J, int V, int
   w.dl = bf16 ? (void*)c.take<uint16_t>(dl_elems) : (void*)c.take<float>(dl_elems);
   w.dlT = bf16 ? (void*)c.take<uint16_t>(dl_elems) : nullptr;
   w.wpad = (bf16 && V % 8 != 0) ? (void*)c.take<uint16_t>((size_t)J * joiner_ldl(V)) : nullptr;
-  w.dpre = c.take<float>(M * J);
+  w.dpre = c.take<float>((size_t)w.chunk_rows * J);
   w.enc_part = c.take<float>((M + 127) / 128 * 2 * J);
   const size_t h_elems = (size_t)w.chunk_rows * J;
   w.hbuf = bf16 ? (void*)c.take<uint16_t>(h_elems) : (void*)c.take<float>(h_elems);
@@ -276,9 +277,23 @@ int check_joiner_sizes(const rnnt_batch* b, int S, int J, int V, int dtype) {
   // operands are read through 32-bit buffer offsets: each array stays below 2^31 bytes
   const long long esz = dtype == RNNT_BF16 ? 2 : 4;
   if ((long long)b->N * b->T * J * esz > kI32 || (long long)b->N * (b->U + 1) * J * esz > kI32 ||
-      (long long)J * V * esz > kI32)
+      (long long)J * joiner_ldl(V) * esz > kI32)
     return fail(RNNT_EUNSUPPORTED, "enc, dec or W exceeds 2^31-1 bytes");
+  // the row-chunk buffers (h, d(logits), the d dec pieces) must hold one
+  // 128-row tile below 2^31 bytes
+  if (joiner_bwd_chunk_max_rows(J, V) < 128)
+    return fail(RNNT_EUNSUPPORTED, "J = %d or V = %d too large for one 128-row chunk", J, V);
   if ((size_t)b->T * sizeof(int) > 64 * 1024) return fail(RNNT_EUNSUPPORTED, "T = %d too large", b->T);
+  return RNNT_OK;
+}
+
+int check_chunk_request(int J, int V, int chunk_rows) {
+  if (chunk_rows == 0) return RNNT_OK;
+  if (chunk_rows < 128 || chunk_rows % 128 != 0)
+    return fail(RNNT_EINVAL, "chunk_rows = %d must be 0 or a positive multiple of 128", chunk_rows);
+  if (chunk_rows > joiner_bwd_chunk_max_rows(J, V))
+    return fail(RNNT_EUNSUPPORTED, "chunk_rows = %d exceeds %d (buffers below 2^31 bytes)", chunk_rows,
+                joiner_bwd_chunk_max_rows(J, V));
   return RNNT_OK;
 }
 
@@ -387,7 +402,7 @@ FullWs full_layout(void* base, int N, int T, int U, int J, int V, int bf16) {
 
 extern "C" {
 
-int rnnt_abi_version(void) { return 5; }
+int rnnt_abi_version(void) { return 6; }
 
 const char* rnnt_last_error(void) { return g_err.c_str(); }
 
@@ -638,22 +653,30 @@ int rnnt_pruned_loss_ex(const rnnt_batch* batch, int32_t S, int32_t algorithm, i
   return hip_status(e, "rnnt_pruned_loss");
 }
 
-size_t rnnt_pruned_joiner_backward_workspace_size(int32_t N, int32_t T, int32_t U, int32_t S, int32_t J, int32_t V,
-                                                  int32_t dtype) {
+size_t rnnt_pruned_joiner_backward_ex_workspace_size(int32_t N, int32_t T, int32_t U, int32_t S, int32_t J,
+                                                     int32_t V, int32_t dtype, int32_t chunk_rows) {
   (void)U;
-  if (N < 1 || T < 1 || S < 1 || J < 1 || V < 1) return 0;
-  return joiner_bwd_layout(nullptr, N, T, S, J, V, dtype == RNNT_BF16).bytes;
+  if (N < 1 || T < 1 || S < 1 || J < 1 || V < 1 || chunk_rows < 0 || chunk_rows % 128 != 0) return 0;
+  if (chunk_rows > joiner_bwd_chunk_max_rows(J, V)) return 0;
+  return joiner_bwd_layout(nullptr, N, T, S, J, V, dtype == RNNT_BF16, chunk_rows).bytes;
 }
 
-int rnnt_pruned_joiner_backward(const rnnt_batch* batch, int32_t S, int32_t J, int32_t V, int32_t dtype,
-                                const void* enc, const void* dec, const void* W, const void* bias,
-                                const int32_t* ranges, const float* lse, const float* logits,
-                                const float* px_occ, const float* py_occ,
-                                const float* scale, float* enc_grad, float* dec_grad, float* W_grad, float* bias_grad,
-                                float* logits_grad, void* workspace, size_t workspace_bytes, void* stream) {
+size_t rnnt_pruned_joiner_backward_workspace_size(int32_t N, int32_t T, int32_t U, int32_t S, int32_t J, int32_t V,
+                                                  int32_t dtype) {
+  return rnnt_pruned_joiner_backward_ex_workspace_size(N, T, U, S, J, V, dtype, 0);
+}
+
+int rnnt_pruned_joiner_backward_ex(const rnnt_batch* batch, int32_t S, int32_t J, int32_t V, int32_t dtype,
+                                   int32_t chunk_rows, const void* enc, const void* dec, const void* W,
+                                   const void* bias, const int32_t* ranges, const float* lse, const float* logits,
+                                   const float* px_occ, const float* py_occ, const float* scale, float* enc_grad,
+                                   float* dec_grad, float* W_grad, float* bias_grad, float* logits_grad,
+                                   void* workspace, size_t workspace_bytes, void* stream) {
   int rc = check_batch(batch, true);
   if (rc) return rc;
   rc = check_joiner_sizes(batch, S, J, V, dtype);
+  if (rc) return rc;
+  rc = check_chunk_request(J, V, chunk_rows);
   if (rc) return rc;
   if (!enc || !dec || !W || !ranges || !lse || !px_occ || !py_occ)
     return fail(RNNT_EINVAL, "enc, dec, W, ranges, lse, px_occ and py_occ are required");
@@ -663,15 +686,69 @@ int rnnt_pruned_joiner_backward(const rnnt_batch* batch, int32_t S, int32_t J, i
   if (logits_grad && (long long)batch->N * batch->T * S * (long long)V > (1ll << 40))
     return fail(RNNT_EUNSUPPORTED, "logits_grad is a debugging aid for small shapes");
   const int bf = dtype == RNNT_BF16;
-  rc = check_ws(workspace, workspace_bytes, joiner_bwd_layout(nullptr, batch->N, batch->T, S, J, V, bf).bytes);
+  rc = check_ws(workspace, workspace_bytes,
+                joiner_bwd_layout(nullptr, batch->N, batch->T, S, J, V, bf, chunk_rows).bytes);
   if (rc) return rc;
-  const JoinerBwdWs w = joiner_bwd_layout(workspace, batch->N, batch->T, S, J, V, bf);
+  const JoinerBwdWs w = joiner_bwd_layout(workspace, batch->N, batch->T, S, J, V, bf, chunk_rows);
   JoinerArgs a = joiner_args(batch, S, J, V, dtype, enc, dec, W, bias, ranges);
   set_joiner_bwd(a, w, lse, logits, px_occ, py_occ, scale, enc_grad, dec_grad, W_grad, bias_grad, logits_grad);
   hipStream_t s = static_cast<hipStream_t>(stream);
   hipError_t e = launch_joiner_prep(a, s);
   if (e == hipSuccess) e = launch_joiner_bwd(a, s);
   return hip_status(e, "rnnt_pruned_joiner_backward");
+}
+
+int rnnt_pruned_joiner_backward(const rnnt_batch* batch, int32_t S, int32_t J, int32_t V, int32_t dtype,
+                                const void* enc, const void* dec, const void* W, const void* bias,
+                                const int32_t* ranges, const float* lse, const float* logits,
+                                const float* px_occ, const float* py_occ,
+                                const float* scale, float* enc_grad, float* dec_grad, float* W_grad, float* bias_grad,
+                                float* logits_grad, void* workspace, size_t workspace_bytes, void* stream) {
+  return rnnt_pruned_joiner_backward_ex(batch, S, J, V, dtype, 0, enc, dec, W, bias, ranges, lse, logits, px_occ,
+                                        py_occ, scale, enc_grad, dec_grad, W_grad, bias_grad, logits_grad, workspace,
+                                        workspace_bytes, stream);
+}
+
+int rnnt_validate_inputs(const rnnt_batch* batch, int32_t V, int32_t S, int32_t J, int32_t dtype, const float* am,
+                         const float* lm, const void* enc, const void* dec, int32_t* flags, int32_t* n_bad,
+                         void* stream) {
+  int rc = check_batch(batch, true);
+  if (rc) return rc;
+  if (V < 1) return fail(RNNT_EINVAL, "V must be >= 1 (got %d)", V);
+  if (batch->blank < 0 || batch->blank >= V) return fail(RNNT_EINVAL, "blank = %d outside [0, V)", batch->blank);
+  if (S < 0 || S > RNNT_MAX_S) return fail(RNNT_EINVAL, "S = %d outside [0, %d]", S, RNNT_MAX_S);
+  if ((enc || dec) && J < 1) return fail(RNNT_EINVAL, "J must be >= 1 with enc or dec (got %d)", J);
+  if ((enc || dec) && dtype != RNNT_F32 && dtype != RNNT_BF16)
+    return fail(RNNT_EINVAL, "dtype must be RNNT_F32 or RNNT_BF16");
+  if (!flags) return fail(RNNT_EINVAL, "flags is required");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e = launch_validate(to_dev(batch), V, S, J, dtype == RNNT_BF16, am, lm, enc, dec, flags, s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  if (e != hipSuccess) return hip_status(e, "rnnt_validate_inputs");
+  if (n_bad) {
+    std::vector<int32_t> h((size_t)batch->N);
+    e = hipMemcpy(h.data(), flags, h.size() * sizeof(int32_t), hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return hip_status(e, "rnnt_validate_inputs");
+    int32_t c = 0;
+    for (int32_t f : h) c += f != 0;
+    *n_bad = c;
+  }
+  return ok();
+}
+
+int rnnt_combine_losses(int32_t N, const float* simple_loss, const float* pruned_loss, float simple_scale,
+                        float pruned_scale, int32_t reduction, float* loss, float* total, void* stream) {
+  if (N < 1) return fail(RNNT_EINVAL, "N must be >= 1 (got %d)", N);
+  if (reduction != RNNT_REDUCE_SUM && reduction != RNNT_REDUCE_MEAN)
+    return fail(RNNT_EINVAL, "reduction must be RNNT_REDUCE_SUM or RNNT_REDUCE_MEAN");
+  if (!(simple_scale >= 0.f) || !(pruned_scale >= 0.f))
+    return fail(RNNT_EINVAL, "the scales must be >= 0 (got %g, %g)", simple_scale, pruned_scale);
+  if (simple_scale != 0.f && !simple_loss) return fail(RNNT_EINVAL, "simple_loss is required with simple_scale != 0");
+  if (pruned_scale != 0.f && !pruned_loss) return fail(RNNT_EINVAL, "pruned_loss is required with pruned_scale != 0");
+  if (!loss && !total) return fail(RNNT_EINVAL, "at least one of loss and total is required");
+  hipError_t e = launch_combine_losses(N, simple_loss, pruned_loss, simple_scale, pruned_scale,
+                                       reduction == RNNT_REDUCE_MEAN, loss, total, static_cast<hipStream_t>(stream));
+  return hip_status(e, "rnnt_combine_losses");
 }
 
 size_t rnnt_full_loss_workspace_size(int32_t N, int32_t T, int32_t U, int32_t J, int32_t V, int32_t dtype) {
@@ -692,9 +769,10 @@ int rnnt_full_loss(const rnnt_batch* batch, int32_t J, int32_t V, int32_t dtype,
   if (dtype != RNNT_F32 && dtype != RNNT_BF16) return fail(RNNT_EINVAL, "dtype must be RNNT_F32 or RNNT_BF16");
   const long long esz = dtype == RNNT_BF16 ? 2 : 4;
   if ((long long)batch->N * batch->T * S > kI32 || (long long)batch->N * batch->T * J * esz > kI32 ||
-      (long long)batch->N * S * J * esz > kI32 || (long long)J * V * esz > kI32 ||
-      (long long)batch->N * batch->T * S * J * 4 > (1ll << 40))
+      (long long)batch->N * S * J * esz > kI32 || (long long)J * joiner_ldl(V) * esz > kI32 ||
+      joiner_bwd_chunk_max_rows(J, V) < 128)
     return fail(RNNT_EUNSUPPORTED, "the unpruned joiner is too large for this build");
+  if ((size_t)batch->T * sizeof(int) > 64 * 1024) return fail(RNNT_EUNSUPPORTED, "T = %d too large", batch->T);
   if (!enc || !dec || !W || !loss) return fail(RNNT_EINVAL, "enc, dec, W and loss are required");
   if (!enc_grad || !dec_grad) return fail(RNNT_EINVAL, "enc_grad and dec_grad are required");
   if (!aligned16(enc_grad) || !aligned16(dec_grad) || !aligned16(logits))

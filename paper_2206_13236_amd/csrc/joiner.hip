@@ -17,18 +17,21 @@
 // reach memory only when the caller asks for them ([N, T, S, V], the size
 // the method's memory scales with).
 //
-// Backward (per chunk of rows, so that d(logits) is held for one chunk only):
+// Backward (per chunk of at most a fixed number of rows, independent of the
+// batch, so that d(logits), h and the d dec pieces are held for one chunk
+// only and no [N, T, S, V] array exists):
 //   1. dl = sc * ((gx+gy) softmax - gx [v=y] - gy [v=blank]) (log-softmax
-//      backward) from the stored logits by a streaming kernel, or, without
-//      them, by recomputing h and the logits GEMM; write the chunk and column
-//      sums (db);
+//      backward) by recomputing h and the logits GEMM (or, when the caller
+//      kept the forward's logits, by a streaming kernel over them); write the
+//      chunk and column sums (db);
 //   2. dh = dl W^T, dpre = dh (1 - h^2)  (tanh backward), kept in LDS: the
 //      epilogue sums it into d enc[n,t] = sum_s dpre(row(t,s)) for the frames
 //      inside the 128-row tile, and into per-tile pieces of the frames the
 //      tile cuts and of d dec[n,u] = sum over the (t,s) with p_t + s = u;
 //   3. dW += h^T dl with split-K partial sums;
-// then a tail kernel adds the d enc / d dec pieces in tile order and sums dW
-// and db over their partials, all in a fixed order.
+//   4. the d dec pieces of the chunk are added to d dec in tile order;
+// then a tail kernel adds the d enc pieces in tile order and sums dW and db
+// over their partials, all in a fixed order.
 #include "gemm.h"
 #include "kernels.h"
 #include "prof.h"
@@ -625,15 +628,19 @@ __global__ __launch_bounds__(kGemmThreads) void joiner_dlogits_kernel(JoinerArgs
         colsum[j] += d;
       }
     }
-  // db partial: sum over this wave's WM rows, one row of db_part per (m-tile, wave row).
-  const int mt = m0 / Cfg::BM;
+  // db partial: sum over this wave's WM rows, one row of db_part per (m-tile
+  // of the chunk, wave row); the first chunk writes it, later ones add to it.
+  const int mt = (m0 - cm0) / Cfg::BM;
 #pragma unroll
   for (int j = 0; j < Cfg::FN; ++j) {
     float s = colsum[j];
     s += __shfl_xor(s, 16, 64);
     s += __shfl_xor(s, 32, 64);
     const int col = v0 + tile_col<Cfg>(j);
-    if (lane < 16 && col < V) a.db_part[((size_t)mt * Cfg::WGM + wm) * V + col] = s;
+    if (lane < 16 && col < V) {
+      float* q = a.db_part + ((size_t)mt * Cfg::WGM + wm) * V + col;
+      *q = cm0 == 0 ? s : *q + s;
+    }
   }
 }
 
@@ -741,10 +748,10 @@ __global__ __launch_bounds__(kDlThreads) void joiner_dl_kernel(JoinerArgs a, int
       }
     }
     if (rg == 0 && gok) {
-      float* db = a.db_part + (size_t)(m0 / kDlRows) * V;
+      float* db = a.db_part + (size_t)((m0 - cm0) / kDlRows) * V;  // the chunk's row; later chunks add
 #pragma unroll
       for (int q = 0; q < 4; ++q)
-        if (c + q < V) db[c + q] = cs[q];
+        if (c + q < V) db[c + q] = cm0 == 0 ? cs[q] : db[c + q] + cs[q];
     }
   }
 }
@@ -759,8 +766,9 @@ __global__ __launch_bounds__(kDlThreads) void joiner_dl_kernel(JoinerArgs a, int
 //          row leaves its piece in enc_part[tile][0 (cut at the start) or
 //          1], for the tail to add the pieces in tile order.
 //   d dec: the rows of one u in the tile (one per frame, slot decreasing as
-//          p_t grows) are summed in ascending t into the row of dpre of the
-//          first of them; the tail adds those pieces of u in tile order.
+//          p_t grows) are summed in ascending t into the chunk's row of dpre
+//          of the first of them; the chunk's d dec pass adds those pieces of
+//          u to d dec in tile order.
 // ---------------------------------------------------------------------------
 constexpr int kTileFrames = 130;  // frames a 128-row tile can touch (S = 1: 128; plus cut ends)
 
@@ -787,8 +795,8 @@ DEV TileFrameRegs tile_frames_fetch(const JoinerArgs& a, int m0, int mend, int b
 }
 
 template <class Cfg>
-DEV void tile_enc_dec(const JoinerArgs& a, const float* C, int LDC, int m0, int mend, int j0, const int4* ri,
-                      TileFrameRegs fr) {
+DEV void tile_enc_dec(const JoinerArgs& a, const float* C, int LDC, int cm0, int m0, int mend, int j0,
+                      const int4* ri, TileFrameRegs fr) {
   static_assert(Cfg::NT >= kTileFrames && Cfg::NT >= Cfg::BM, "one thread per frame and per row of the tile");
   __shared__ int fr_nt[kTileFrames], fr_n[kTileFrames], fr_p[kTileFrames];
   __shared__ int16_t next_row[Cfg::BM];  // tile row of the next frame's row of the same u, or -1
@@ -849,7 +857,7 @@ DEV void tile_enc_dec(const JoinerArgs& a, const float* C, int LDC, int m0, int 
     float4 acc = *reinterpret_cast<const float4*>(C + r * LDC + 4 * cg);
     for (int r2 = next_row[r]; r2 >= 0; r2 = next_row[r2])
       acc = f4add(acc, *reinterpret_cast<const float4*>(C + r2 * LDC + 4 * cg));
-    *reinterpret_cast<float4*>(a.dpre + (size_t)(m0 + r) * J + jj) = acc;
+    *reinterpret_cast<float4*>(a.dpre + (size_t)(m0 - cm0 + r) * J + jj) = acc;  // the chunk's row
   }
 }
 
@@ -935,7 +943,7 @@ __global__ __launch_bounds__(kGemmThreads, 4) void joiner_dh_kernel(JoinerArgs a
     for (int q = 0; q < 4; ++q) cr[q] = dp[q];  // dpre stays in the tile for the d enc / d dec pieces
   }
   __syncthreads();
-  tile_enc_dec<Cfg>(a, C, LDC, m0, mend, j0, ri, fr);
+  tile_enc_dec<Cfg>(a, C, LDC, cm0, m0, mend, j0, ri, fr);
   if constexpr (BF) {
     // h back to the tile (0 past mend), then h^T [J, chunk_rows] for the
     // bf16 dW: the lane's 4 consecutive rows of the MFMA layout as one
@@ -1102,17 +1110,17 @@ DEV void tail_wsum(const JoinerArgs& a, int b) {
 }
 
 // db = sum of the column partials written by the d(logits) kernel (one per
-// 32 rows streamed, one per wave row of a GEMM tile recomputed): a block takes
-// 16 columns; each of its 16 thread groups sums a contiguous sixteenth of the
-// rows in ascending order, 8 loads in flight, then the sixteenths are added
-// in order.
+// 32 rows of a chunk streamed, one per wave row of a GEMM tile recomputed,
+// each summed over the chunks): a block takes 16 columns; each of its 16
+// thread groups sums a contiguous sixteenth of the rows in ascending order,
+// 8 loads in flight, then the sixteenths are added in order.
 constexpr int kDbCols = 16;
 
 DEV void tail_dbsum(const JoinerArgs& a, int b, float (*red)[kDbCols]) {
   const int c = threadIdx.x % kDbCols, part = threadIdx.x / kDbCols;  // 16 parts
   constexpr int kParts = kTailThreads / kDbCols;
   const int v = b * kDbCols + c;
-  const int M = a.frame_off[a.b.N] * a.S;
+  const int M = min(a.frame_off[a.b.N] * a.S, a.chunk_rows);  // rows of the first (largest) chunk
   const int rows = a.logits_in ? (M + kDlRows - 1) / kDlRows : CfgF::WGM * ((M + CfgF::BM - 1) / CfgF::BM);
   const int q = (rows + kParts - 1) / kParts, r0 = min(rows, part * q), r1 = min(rows, r0 + q);
   float s = 0.f;
@@ -1171,23 +1179,30 @@ DEV void tail_enc_pieces(const JoinerArgs& a, int b) {
   }
 }
 
-// d dec[n, u]: the pieces of u, one per row tile that holds rows of u, each
-// in the row of dpre of its first row (ascending t). The row of u in frame t,
-// m_t = (frame_off[n] + t) S + u - p_t, grows with t (p_{t+1} - p_t < S while
-// u stays in the band), so the first frame of each tile is found by a binary
-// search; the pieces are loaded 8 at a time and added in tile order.
-DEV void tail_dec_pieces(const JoinerArgs& a, int b, int* sp) {
+// d dec[n, u] from the pieces of u in one chunk of rows [cm0, cm1): one
+// piece per row tile that holds rows of u, each in the chunk's row of dpre
+// of its first row (ascending t). The row of u in frame t,
+// m_t = (frame_off[n] + t) S + u - p_t, grows with t (p_{t+1} - p_t < S
+// while u stays in the band), so the chunk's frames of u and the first frame
+// of each tile are found by binary searches; the pieces are loaded 8 at a
+// time and added in tile order, onto d dec as the earlier chunks left it
+// (0 in the chunk that holds the first row of u), so that the sum's order is
+// that of one pass over all tiles. The first chunk also writes the zero rows
+// (u > U_n, or u in no frame's band).
+DEV void tail_dec_pieces(const JoinerArgs& a, int b, int* sp, int cm0, int cm1) {
   const int T = a.b.T, U1 = a.b.U + 1, S = a.S, J = a.J, tpr = J / 4;
   const int n = b / U1, u = b - n * U1;
   int Tn, Un;
   utt_dims(a.b, n, Tn, Un);
   float4* out = reinterpret_cast<float4*>(a.dec_grad + ((size_t)n * U1 + u) * J);
   if (u > Un) {
-    for (int g = threadIdx.x; g < tpr; g += kTailThreads) out[g] = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (cm0 == 0)
+      for (int g = threadIdx.x; g < tpr; g += kTailThreads) out[g] = make_float4(0.f, 0.f, 0.f, 0.f);
     return;
   }
   for (int t = threadIdx.x; t < Tn; t += kTailThreads) sp[t] = a.ranges[((size_t)n * T + t) * S];
   __syncthreads();
+  // frames [t0, t1) whose band holds u
   int lo = 0, hi = Tn;
   while (lo < hi) {
     const int mid = (lo + hi) >> 1;
@@ -1204,27 +1219,37 @@ DEV void tail_dec_pieces(const JoinerArgs& a, int b, int* sp) {
   const int t1 = lo;
   const int off = a.frame_off[n];
   auto row_of = [&](int t) { return (off + t) * S + u - sp[t]; };
-  const int frames = __builtin_amdgcn_readfirstlane(a.frame_off[a.b.N]);  // keeps the resource scalar
-  const Rsrc dr = make_rsrc(a.dpre, (size_t)frames * S * J * sizeof(float));
-  const int ia = t1 > t0 ? row_of(t0) / kTileRows : 0, ib = t1 > t0 ? row_of(t1 - 1) / kTileRows : -1;
+  // the first frame in [l, h] whose row of u is at least r (h + 1: none)
+  auto first_at = [&](int l, int h, int r) {
+    int e = h + 1;
+    while (l < e) {
+      const int mid = (l + e) >> 1;
+      if (row_of(mid) >= r) e = mid;
+      else l = mid + 1;
+    }
+    return l;
+  };
+  if (t1 <= t0) {
+    if (cm0 == 0)
+      for (int g = threadIdx.x; g < tpr; g += kTailThreads) out[g] = make_float4(0.f, 0.f, 0.f, 0.f);
+    return;
+  }
+  const int mend = min(cm1, a.frame_off[a.b.N] * S);
+  const int ta = first_at(t0, t1 - 1, cm0), tb = first_at(ta, t1 - 1, mend);  // frames of u in the chunk
+  if (ta >= tb) return;
+  const bool starts = row_of(t0) >= cm0;  // the chunk holds the first row of u
+  const int rows = __builtin_amdgcn_readfirstlane(a.chunk_rows);  // keeps the resource scalar
+  const Rsrc dr = make_rsrc(a.dpre, (size_t)rows * J * sizeof(float));
+  const int ia = row_of(ta) / kTileRows, ib = row_of(tb - 1) / kTileRows;
   for (int g = threadIdx.x; g < tpr; g += kTailThreads) {
-    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    float4 acc = starts ? make_float4(0.f, 0.f, 0.f, 0.f) : out[g];
     for (int i0 = ia; i0 <= ib; i0 += 8) {
       float4 v[8];
 #pragma unroll
       for (int k = 0; k < 8; ++k) {
         const int i = i0 + k;
-        int t = t0;
-        if (i > ia && i <= ib) {  // first frame whose row of u lies in tile i
-          int l = t0, h = t1 - 1;
-          while (l < h) {
-            const int mid = (l + h) >> 1;
-            if (row_of(mid) >= i * kTileRows) h = mid;
-            else l = mid + 1;
-          }
-          t = l;
-        }
-        const uint32_t o = (uint32_t)(((size_t)row_of(t) * J + 4 * g) * sizeof(float));
+        const int t = (i > ia && i <= ib) ? first_at(ta, tb - 1, i * kTileRows) : ta;  // first frame of u in tile i
+        const uint32_t o = (uint32_t)(((size_t)(row_of(t) - cm0) * J + 4 * g) * sizeof(float));
         const u32x4 w = __builtin_amdgcn_raw_buffer_load_b128(dr, (int)(i <= ib ? o : kOob), 0, 0);
         v[k] = make_float4(__uint_as_float(w.x), __uint_as_float(w.y), __uint_as_float(w.z), __uint_as_float(w.w));
       }
@@ -1237,13 +1262,16 @@ DEV void tail_dec_pieces(const JoinerArgs& a, int b, int* sp) {
 
 struct TailRanges {
   int dec, enc, wsum, dbsum;  // block counts, in launch order
+  int cm0, cm1;               // the chunk whose d dec pieces the dec blocks add
 };
 
+// One launch per chunk of rows: its d dec pieces; the last chunk's launch
+// also runs the d enc, dW and db reductions.
 __global__ __launch_bounds__(kTailThreads) void joiner_tail_kernel(JoinerArgs a, TailRanges r) {
   extern __shared__ int sp[];  // p_t of one utterance (d dec blocks)
   __shared__ float red[kTailThreads / kDbCols][kDbCols];  // db blocks
   int b = blockIdx.x;
-  if (b < r.dec) { tail_dec_pieces(a, b, sp); return; }
+  if (b < r.dec) { tail_dec_pieces(a, b, sp, r.cm0, r.cm1); return; }
   b -= r.dec;
   if (b < r.enc) { tail_enc_pieces(a, b); return; }
   b -= r.enc;
@@ -1272,27 +1300,49 @@ hipError_t launch_full_ranges(int* ranges, int N, int T, int S, hipStream_t s) {
 int joiner_nparts(int V) { return (V + 63) / 64; }
 int joiner_ldl(int V) { return (V + 7) / 8 * 8; }
 
-int joiner_bwd_chunk_rows(int N, int T, int S, int J, int V, int bf16) {
-  (void)J;
+// Rows of a chunk buffer whose rows of `row_elems` fp32 words stay below
+// 2^31 bytes (chunk buffers are read through 32-bit buffer offsets), as a
+// multiple of the 128-row tile; 0 when not even one tile fits.
+static long long joiner_rsrc_rows(long long row_elems) {
+  return ((0x7fffffffll / (row_elems * 4)) / 128) * 128;
+}
+
+int joiner_bwd_chunk_max_rows(int J, int V) {
+  const long long w = (long long)(J > joiner_ldl(V) ? J : joiner_ldl(V));
+  const long long r = joiner_rsrc_rows(w);
+  return (int)(r < (1ll << 30) ? r : (1ll << 30));
+}
+
+// The padded row count mmax in chunks of at most `cap` rows, split evenly
+// (so that no chunk is left nearly empty), as a multiple of the 128-row tile.
+static long long even_chunk(long long mmax, long long cap) {
+  const long long n = (mmax + cap - 1) / cap;
+  return ((mmax + n - 1) / n + 127) / 128 * 128;
+}
+
+// The backward's chunk: at most d(logits) of about 20 MiB, but 8,192 to
+// 16,384 rows (64 to 128 row tiles, so that each chunk's dh and recomputed
+// logits put one or two workgroups on every CU), and within the 32-bit
+// limit. The bound depends on J, V and the dtype only, not on N or T;
+// `request` (a multiple of 128, or 0) overrides it.
+int joiner_bwd_chunk_rows(int N, int T, int S, int J, int V, int bf16, int request) {
   const long long mmax = (long long)N * T * S;
+  if (request > 0) return (int)(request < mmax ? request : (mmax + 127) / 128 * 128);
   const long long bytes_per_row = (long long)joiner_ldl(V) * (bf16 ? 2 : 4);
-  const long long budget = 256ll << 20;  // one chunk of d(logits) stays within the 256 MB Infinity Cache
-  long long rows = budget / bytes_per_row;
-  rows = rows / 128 * 128;
-  if (rows < 128) rows = 128;
-  if (rows > mmax) rows = (mmax + 127) / 128 * 128;
-  return (int)rows;
+  long long cap = ((20ll << 20) / bytes_per_row) / 128 * 128;
+  cap = cap < 8192 ? 8192 : cap > 16384 ? 16384 : cap;
+  const long long lim = joiner_bwd_chunk_max_rows(J, V);
+  if (cap > lim) cap = lim;
+  return (int)even_chunk(mmax, cap);
 }
 
 int joiner_fwd_chunk_rows(int N, int T, int S, int J, int bf16) {
   const long long mmax = (long long)N * T * S;
   if (!(bf16 ? kFwdHbuf<true> : kFwdHbuf<false>)) return (int)((mmax + 127) / 128 * 128);  // no h buffer
-  const long long budget = 128ll << 20;  // h of one chunk
-  long long rows = budget / ((long long)J * (bf16 ? 2 : 4));
-  rows = rows / 128 * 128;
-  if (rows < 128) rows = 128;
-  if (rows > mmax) rows = (mmax + 127) / 128 * 128;
-  return (int)rows;
+  long long cap = 32768;  // h of one chunk: at most 32,768 rows (48 MiB at J = 768, bf16)
+  const long long lim = joiner_rsrc_rows(J);
+  if (cap > lim) cap = lim;
+  return (int)even_chunk(mmax, cap);
 }
 
 bool joiner_fwd_uses_hbuf(int bf16) { return bf16 ? kFwdHbuf<true> : kFwdHbuf<false>; }
@@ -1305,8 +1355,8 @@ int joiner_bwd_splits(int J, int V) {
   return s;
 }
 
-int joiner_db_rows(int N, int T, int S) {
-  const long long mmax = (long long)N * T * S;
+int joiner_db_rows(int chunk_rows) {
+  const long long mmax = chunk_rows;
   const long long streamed = (mmax + kDlRows - 1) / kDlRows;
   const long long tiled = ((mmax + CfgF::BM - 1) / CfgF::BM) * CfgF::WGM;
   return (int)(streamed > tiled ? streamed : tiled);
@@ -1430,20 +1480,24 @@ hipError_t launch_joiner_bwd(const JoinerArgs& a, hipStream_t s) {
         hipLaunchKernelGGL(joiner_dw_kernel<false>, g3, dim3(kGemmThreads), 0, s, a, cm0, cm1, cm0 == 0);
       }
     }
-  }
-  const size_t JV = (size_t)J * V;
-  const int R = (J / 4 >= kTailThreads) ? 1 : kTailThreads / (J / 4);
-  TailRanges tr;
-  tr.dec = (a.b.U + 1) * a.b.N;
-  tr.enc = (a.b.N * a.b.T + R - 1) / R;
-  const bool wvec = JV % kWsumVec == 0 && (reinterpret_cast<uintptr_t>(a.W_grad) & 15) == 0;
-  const size_t wthreads = wvec ? JV / kWsumVec : JV;
-  tr.wsum = a.W_grad ? (int)((wthreads + kTailThreads - 1) / kTailThreads) : 0;
-  tr.dbsum = a.bias_grad ? (V + kDbCols - 1) / kDbCols : 0;
-  {
-    RNNT_PROF(s, "joiner_tail");
-    hipLaunchKernelGGL(joiner_tail_kernel, dim3(tr.dec + tr.enc + tr.wsum + tr.dbsum), dim3(kTailThreads),
-                       (size_t)a.b.T * sizeof(int), s, a, tr);
+    // the chunk's d dec pieces; after the last chunk also d enc, dW and db
+    const bool last = cm1 >= mmax;
+    const size_t JV = (size_t)J * V;
+    const int R = (J / 4 >= kTailThreads) ? 1 : kTailThreads / (J / 4);
+    TailRanges tr;
+    tr.cm0 = cm0;
+    tr.cm1 = cm1;
+    tr.dec = (a.b.U + 1) * a.b.N;
+    tr.enc = last ? (a.b.N * a.b.T + R - 1) / R : 0;
+    const bool wvec = JV % kWsumVec == 0 && (reinterpret_cast<uintptr_t>(a.W_grad) & 15) == 0;
+    const size_t wthreads = wvec ? JV / kWsumVec : JV;
+    tr.wsum = (last && a.W_grad) ? (int)((wthreads + kTailThreads - 1) / kTailThreads) : 0;
+    tr.dbsum = (last && a.bias_grad) ? (V + kDbCols - 1) / kDbCols : 0;
+    {
+      RNNT_PROF(s, last ? "joiner_tail" : "joiner_dec");
+      hipLaunchKernelGGL(joiner_tail_kernel, dim3(tr.dec + tr.enc + tr.wsum + tr.dbsum), dim3(kTailThreads),
+                         (size_t)a.b.T * sizeof(int), s, a, tr);
+    }
   }
   return hipGetLastError();
 }

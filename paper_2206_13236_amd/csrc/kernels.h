@@ -143,13 +143,13 @@ struct JoinerArgs {
   void* wpad;          // ws [J, ldl] bf16 or null: W with its rows padded by zeros to ldl elements, so
                        // that dh reads W in 16-byte segments when V is not a multiple of 8
   int chunk_rows;
-  float* dpre;         // ws [N*T*S, J]: the d dec pieces, each in the row of dpre of its first row
+  float* dpre;         // ws chunk [chunk_rows, J]: the chunk's d dec pieces, each in the row of its first row
   float* enc_part;     // ws [ceil(N*T*S/128), 2, J]: d enc pieces of frames cut by a 128-row tile
   void* hbuf;          // ws chunk [chunk_rows, J] (f32 or bf16): h = tanh(enc + dec) of the chunk's rows
                        // (forward and recomputed backward: written by the h kernel; backward: by dh)
   float* dw_part;      // ws [splits, J, V]
   int splits;
-  float* db_part;      // ws [n_db_rows, V]
+  float* db_part;      // ws [n_db_rows, V]: column sums per row group of a chunk, summed over the chunks
   int n_db_rows;
   float* enc_grad;
   float* dec_grad;
@@ -162,11 +162,14 @@ hipError_t launch_joiner_prep(const JoinerArgs& a, hipStream_t s);
 hipError_t launch_full_ranges(int* ranges, int N, int T, int S, hipStream_t s);
 hipError_t launch_joiner_fwd(const JoinerArgs& a, hipStream_t s);
 hipError_t launch_joiner_bwd(const JoinerArgs& a, hipStream_t s);
-int joiner_bwd_chunk_rows(int N, int T, int S, int J, int V, int bf16);
+// rows of the backward's chunk (request: a multiple of 128 overriding the
+// library's choice, or 0), and the largest chunk the 32-bit offsets allow
+int joiner_bwd_chunk_rows(int N, int T, int S, int J, int V, int bf16, int request);
+int joiner_bwd_chunk_max_rows(int J, int V);
 int joiner_fwd_chunk_rows(int N, int T, int S, int J, int bf16);
 bool joiner_fwd_uses_hbuf(int bf16);
 int joiner_bwd_splits(int J, int V);
-int joiner_db_rows(int N, int T, int S);
+int joiner_db_rows(int chunk_rows);  // db partial rows of one chunk
 int joiner_nparts(int V);
 int joiner_ldl(int V);
 
@@ -210,6 +213,13 @@ int band_diagonals(int T, int U, int S);
 // s = u - p_t), each slot carrying the shifts to its predecessors.
 bool band_masked(int U, int S);
 int band_slots(int U, int S);  // W
+
+// ---- per-utterance validation and the training loss --------------------------
+// flags[n] (cleared first) gets the RNNT_FLAG_* bits of utterance n
+hipError_t launch_validate(const BatchDev& b, int V, int S, int J, int bf16, const float* am, const float* lm,
+                           const void* enc, const void* dec, int* flags, hipStream_t s);
+hipError_t launch_combine_losses(int N, const float* simple, const float* pruned, float ss, float ps, int mean,
+                                 float* loss, float* total, hipStream_t s);
 
 // ---- generic fills -----------------------------------------------------------
 hipError_t launch_fill_f32(float* p, size_t n, float v, hipStream_t s);

@@ -111,11 +111,12 @@ def ranges_valid(r, t_len, u_len, S):
         assert np.all(np.diff(p) >= 0) and np.all(np.diff(p) < S) and np.all((p >= 0) & (p <= P))
 
 
-def run_step(b, S, bf16=None, keep_logits=True, simple_scale=0.5):
-    """The whole GPU path on batch b, as the benchmark runs it."""
+def run_step(b, S, bf16=None, keep_logits=False, simple_scale=0.5, bwd_chunk_rows=0):
+    """The whole GPU path on batch b, as the benchmark runs it (by default
+    without the [N, T, S, V] logits: the backward recomputes them per chunk)."""
     bf = (b.wl.joiner_dtype == "bf16") if bf16 is None else bf16
     batch = make_dev_batch(b)
-    step = P.PrunedRnntLoss(S, simple_scale=simple_scale, keep_logits=keep_logits)
+    step = P.PrunedRnntLoss(S, simple_scale=simple_scale, keep_logits=keep_logits, bwd_chunk_rows=bwd_chunk_rows)
     out = step.step(batch, dev_f32(b.am), dev_f32(b.lm), dev_joiner(b.enc, bf), dev_joiner(b.dec, bf),
                     dev_joiner(b.W, bf), dev_joiner(b.bias, bf))
     torch.cuda.synchronize()
@@ -123,29 +124,39 @@ def run_step(b, S, bf16=None, keep_logits=True, simple_scale=0.5):
 
 
 def oracle_step(b, S, idx=None, simple_scale=0.5):
-    """The oracle's pipeline on utterances idx (all by default) of batch b."""
+    """The oracle's stages 1-3 on utterances idx (all by default) of batch b:
+    the simple loss, its occupations and gradients, and the bounds from its
+    own occupations. Stage 4 runs in check_step, on the bounds the GPU
+    chose."""
     import oracle as O
     idx = np.arange(b.N) if idx is None else np.asarray(idx)
     sym = b.symbols[idx]
     tl, ul = b.t_len[idx], b.u_len[idx]
     s1 = O.simple_stage(b.am[idx], b.lm[idx], sym, tl, ul, b.wl.blank, scale=np.full(len(idx), simple_scale))
     ranges = O.prune_ranges(s1["gx"], s1["gy"], tl, ul, S)
-    st = O.pruned_stage(b.enc[idx], b.dec[idx], b.W, b.bias, ranges, sym, tl, ul, b.wl.blank)
-    return {"idx": idx, "s1": s1, "ranges": ranges, "st": st}
+    return {"idx": idx, "s1": s1, "ranges": ranges, "simple_scale": simple_scale}
 
 
-def check_step(out, ref, b, S, bf16=None, whole_batch=True):
-    """Compare run_step's outputs with oracle_step's on the oracle's utterances.
+def sub_batch(b, idx):
+    """Utterances idx of batch b as a batch of their own (same padded T, U)."""
+    import dataclasses
+    idx = np.asarray(idx)
+    return dataclasses.replace(b, t_len=b.t_len[idx], u_len=b.u_len[idx], symbols=b.symbols[idx], am=b.am[idx],
+                               lm=b.lm[idx], enc=b.enc[idx], dec=b.dec[idx])
 
-    Stage 1-2 outputs are unique and compared everywhere; the bounds are
-    compared exactly where the window argmax is unique (and checked valid
-    everywhere), and the pruned loss and joiner gradients on those
-    utterances. dW and db are batch sums: compared when the oracle covers the
-    whole batch and no utterance has a near tie. Returns the near-tie set.
-    """
-    bf = (b.wl.joiner_dtype == "bf16") if bf16 is None else bf16
+
+def check_simple_part(out, ref, b, S):
+    """Stages 1-3 of run_step's outputs against the oracle on the oracle's
+    utterances: simple loss, occupations, d am, d lm with the oracle's own;
+    the bounds bit-exactly with the oracle's Eq. (8) procedure run on the
+    GPU's own fp32 occupations (the bounds are a fixed fp32 function of
+    them), valid (Eqs. (9)-(10)), and equal to the oracle's bounds from its
+    own occupations wherever the window argmax is unique to 2e-5. Leaves the
+    oracle's bounds on the GPU's occupations in ref["r_own"]; returns the
+    set of utterances with a near tie (for information)."""
+    import oracle as O
     idx = ref["idx"]
-    s1, st = ref["s1"], ref["st"]
+    s1 = ref["s1"]
     tl, ul = b.t_len[idx], b.u_len[idx]
     assert_close("simple_loss", out["simple_loss"][idx], s1["loss"], rtol=1e-5)
     assert_close("am_grad", out["am_grad"][idx], s1["am_grad"], atol=1e-4)
@@ -154,15 +165,66 @@ def check_step(out, ref, b, S, bf16=None, whole_batch=True):
     assert_close("simple_py_occ", out["simple_py_occ"][idx], s1["gy"], atol=1e-4)
     got_r = out["ranges"][idx]
     ranges_valid(got_r, tl, ul, S)
+    r_own = own_bounds(out, b, S, idx)
+    for k, n in enumerate(idx):
+        assert np.array_equal(got_r[k], r_own[k]), \
+            f"utterance {n}: {int((got_r[k] != r_own[k]).sum())} bounds differ from Eq. (8) on the GPU's occupations"
+    ref["r_own"] = r_own
     amb = near_tie_utterances(s1["gx"], s1["gy"], tl, ul, S)
     for k, n in enumerate(idx):
-        if k in amb:
-            continue
-        assert np.array_equal(got_r[k], ref["ranges"][k]), f"utterance {n}: ranges differ without a near tie"
-        assert_close(f"pruned_loss[{n}]", out["pruned_loss"][n], st["loss"][k], rtol=loss_rtol(bf))
-        for key in ("enc_grad", "dec_grad"):
-            assert_close(f"{key}[{n}]", out[key][n], st[key][k], atol=grad_atol(st[key], bf))
-    if whole_batch and len(idx) == b.N and not amb:
+        if k not in amb:
+            assert np.array_equal(got_r[k], ref["ranges"][k]), f"utterance {n}: ranges differ without a near tie"
+    return amb
+
+
+def own_bounds(out, b, S, idx):
+    """The oracle's bounds (Eq. (8) and the adjustment, fp32) on the GPU's own occupations."""
+    import oracle as O
+    gx32 = out["simple_px_occ"][idx].astype(np.float32)
+    gy32 = out["simple_py_occ"][idx].astype(np.float32)
+    return O.prune_ranges(gx32, gy32, b.t_len[idx], b.u_len[idx], S)
+
+
+def check_pruned_part(out, b, S, idx, ranges, simple_loss=None, simple_scale=0.5, bf16=None, whole_batch=True):
+    """Stage 4 of run_step's outputs against the oracle's pruned stage on the
+    bounds the GPU chose (ranges [len(idx), T, S]): band log-probs, lse,
+    pruned loss, band occupations, d enc, d dec, and dW and db when idx is
+    the whole batch; with the oracle's simple losses also the training loss
+    of Sec. 3.3 per utterance and summed. Returns the oracle's stage 4."""
+    import oracle as O
+    bf = (b.wl.joiner_dtype == "bf16") if bf16 is None else bf16
+    idx = np.asarray(idx)
+    tl, ul = b.t_len[idx], b.u_len[idx]
+    st = O.pruned_stage(b.enc[idx], b.dec[idx], b.W, b.bias, ranges, b.symbols[idx], tl, ul, b.wl.blank)
+    lp_tol = 2e-2 if bf else 5e-5
+    occ_tol = 2e-2 if bf else 1e-4
+    for key in ("px", "py"):
+        assert_close(f"band {key}", out[key][idx], st[key], atol=lp_tol)
+    assert_close("band lse", out["lse"][idx], st["lse"], atol=lp_tol, rtol=lp_tol)
+    assert_close("pruned_loss", out["pruned_loss"][idx], st["loss"], rtol=loss_rtol(bf))
+    assert_close("pruned_px_occ", out["pruned_px_occ"][idx], st["gx"], atol=occ_tol)
+    assert_close("pruned_py_occ", out["pruned_py_occ"][idx], st["gy"], atol=occ_tol)
+    for key in ("enc_grad", "dec_grad"):
+        assert_close(key, out[key][idx], st[key], atol=grad_atol(st[key], bf))
+    if whole_batch and len(idx) == b.N:
         for key in ("W_grad", "bias_grad"):
             assert_close(key, out[key], st[key], atol=grad_atol(st[key], bf, param=True))
+    if simple_loss is not None:
+        # Sec. 3.3: simple_scale * simple + pruned, per utterance and summed
+        comb = simple_scale * simple_loss + st["loss"]
+        assert_close("training loss", out["loss"][idx], comb, rtol=loss_rtol(bf))
+        if len(idx) == b.N:
+            assert_close("training loss total", out["total"], comb.sum(), rtol=loss_rtol(bf))
+    return st
+
+
+def check_step(out, ref, b, S, bf16=None, whole_batch=True):
+    """Compare run_step's outputs with the oracle on the oracle's utterances,
+    every output of every utterance: stages 1-3 (check_simple_part), then
+    stage 4 on the bounds the GPU chose and the training loss
+    (check_pruned_part). Leaves the oracle's stage 4 in ref["st"]; returns
+    the set of utterances with a near tie (for information)."""
+    amb = check_simple_part(out, ref, b, S)
+    ref["st"] = check_pruned_part(out, b, S, ref["idx"], ref["r_own"], simple_loss=ref["s1"]["loss"],
+                                  simple_scale=ref["simple_scale"], bf16=bf16, whole_batch=whole_batch)
     return amb

@@ -32,7 +32,8 @@ def _declared():
 def test_header_declares_the_entry_points():
     names = _declared()
     for n in ("rnnt_simple_loss", "rnnt_prune_ranges", "rnnt_pruned_joiner", "rnnt_pruned_loss",
-              "rnnt_pruned_joiner_backward", "rnnt_last_error", "rnnt_abi_version"):
+              "rnnt_pruned_joiner_backward", "rnnt_last_error", "rnnt_abi_version", "rnnt_validate_inputs",
+              "rnnt_combine_losses", "rnnt_pruned_joiner_backward_ex"):
         assert n in names
 
 
@@ -41,7 +42,7 @@ def test_library_exports_every_declared_symbol(L):
     missing = [n for n in _declared() if not hasattr(L, n)]
     assert not missing, f"not exported: {missing}"
     assert set(_declared()) == set(_native.SIGNATURES), "binding signatures out of sync with the header"
-    assert L.rnnt_abi_version() == 5
+    assert L.rnnt_abi_version() == 6
 
 
 def test_workspace_queries(L):
@@ -152,3 +153,87 @@ def test_python_binding_checks_shapes_on_cpu():
     with pytest.raises(ValueError):
         P.Batch(torch.zeros(2, dtype=torch.int32), torch.zeros(2, dtype=torch.int32),
                 torch.zeros(2, 3, dtype=torch.int32), 10, 3)  # CPU tensors are rejected
+
+
+def test_backward_chunk_memory_does_not_grow_with_the_batch(L):
+    # The backward holds d(logits), h and the d dec pieces for one chunk of
+    # rows whose size depends on J, V and the dtype only: ten times the
+    # utterances add only per-row bookkeeping (row info, d enc pieces), far
+    # below the V * 4 bytes per row that [N, T, S, V] logits would take.
+    from paper_2206_13236_amd import _native as N
+    shapes = {"bpe": (16, 248, 58, 5, 512, 500, N.RNNT_F32), "long": (32, 495, 100, 5, 512, 500, N.RNNT_BF16),
+              "largev": (16, 298, 78, 5, 512, 5000, N.RNNT_F32), "stress": (8, 970, 298, 10, 768, 8000, N.RNNT_BF16)}
+    for name, (n, t, u, s_, j, v, dt) in shapes.items():
+        a = L.rnnt_pruned_joiner_backward_workspace_size(n, t, u, s_, j, v, dt)
+        b = L.rnnt_pruned_joiner_backward_workspace_size(10 * n, t, u, s_, j, v, dt)
+        per_row = (b - a) / (9 * n * t * s_)
+        assert 0 < per_row < 16 + 8 * j / 64 + 8, (name, per_row)
+    # the chunk override: a smaller chunk needs less workspace, an invalid one none
+    big = L.rnnt_pruned_joiner_backward_ex_workspace_size(16, 248, 58, 5, 512, 500, N.RNNT_F32, 0)
+    small = L.rnnt_pruned_joiner_backward_ex_workspace_size(16, 248, 58, 5, 512, 500, N.RNNT_F32, 256)
+    assert 0 < small < big
+    assert big == L.rnnt_pruned_joiner_backward_workspace_size(16, 248, 58, 5, 512, 500, N.RNNT_F32)
+    assert L.rnnt_pruned_joiner_backward_ex_workspace_size(16, 248, 58, 5, 512, 500, N.RNNT_F32, 100) == 0
+    assert L.rnnt_pruned_joiner_backward_ex_workspace_size(16, 248, 58, 5, 512, 500, N.RNNT_F32, -128) == 0
+
+
+def test_sizes_beyond_32_bit_buffer_offsets_are_refused(L):
+    # Chunk buffers are read through 32-bit buffer offsets: a vocabulary so
+    # large that one 128-row tile of d(logits) reaches 2^31 bytes is refused
+    # before any launch; so is an explicit chunk beyond that limit.
+    from paper_2206_13236_amd import _native as N
+    b = _batch(N=1, T=4, U=2)
+    pb = ctypes.byref(b)
+    fake = ctypes.c_void_p(0x4000)
+    V = 5_000_000
+    assert L.rnnt_pruned_joiner(pb, 2, 8, V, N.RNNT_F32, fake, fake, fake, None, fake, fake, fake, fake, None,
+                                fake, 1 << 40, None) == N.RNNT_EUNSUPPORTED
+    assert "too large" in _err(L)
+    assert L.rnnt_pruned_joiner_backward(pb, 2, 8, V, N.RNNT_F32, fake, fake, fake, None, fake, fake, None,
+                                         fake, fake, None, fake, fake, None, None, None, fake, 1 << 40,
+                                         None) == N.RNNT_EUNSUPPORTED
+    assert L.rnnt_full_loss(pb, 8, V, N.RNNT_F32, fake, fake, fake, None, None, fake, fake, fake, None, None,
+                            None, fake, 1 << 40, None) == N.RNNT_EUNSUPPORTED
+    # V = 500, J = 512: at most (2^31 - 1) / (512 * 4) rows, rounded down to 1,024
+    args = (fake, fake, fake, None, fake, fake, None, fake, fake, None, fake, fake, None, None, None, fake, 1 << 40,
+            None)
+    assert L.rnnt_pruned_joiner_backward_ex(pb, 2, 512, 500, N.RNNT_F32, 1 << 20, *args) == N.RNNT_EUNSUPPORTED
+    assert L.rnnt_pruned_joiner_backward_ex(pb, 2, 512, 500, N.RNNT_F32, 100, *args) == N.RNNT_EINVAL
+    # the unpruned loss at the largest workload's shape (8 x 1000 x 301 rows of
+    # J = 768) passes the size checks now that its row buffers are chunked:
+    # only the (deliberately tiny) workspace is refused
+    big = _batch(N=8, T=1000, U=300)
+    assert L.rnnt_full_loss(ctypes.byref(big), 768, 8000, N.RNNT_BF16, fake, fake, fake, None, None, fake, fake,
+                            fake, None, None, None, fake, 16, None) == N.RNNT_EWORKSPACE
+    ws = L.rnnt_full_loss_workspace_size(8, 1000, 300, 768, 8000, N.RNNT_BF16)
+    assert 0 < ws < 8 * 1000 * 301 * 768 * 4  # far below an [M, J] fp32 array
+
+
+def test_combine_and_validate_statuses(L):
+    from paper_2206_13236_amd import _native as N
+    fake = ctypes.c_void_p(0x4000)
+    # combine: N, reduction, scales, required inputs and outputs
+    assert L.rnnt_combine_losses(0, fake, fake, 0.5, 1.0, 0, fake, fake, None) == N.RNNT_EINVAL
+    assert L.rnnt_combine_losses(4, fake, fake, 0.5, 1.0, 2, fake, fake, None) == N.RNNT_EINVAL
+    assert L.rnnt_combine_losses(4, fake, fake, -0.5, 1.0, 0, fake, fake, None) == N.RNNT_EINVAL
+    assert L.rnnt_combine_losses(4, fake, None, 0.5, 1.0, 0, fake, fake, None) == N.RNNT_EINVAL
+    assert L.rnnt_combine_losses(4, None, fake, 0.5, 1.0, 0, fake, fake, None) == N.RNNT_EINVAL
+    assert L.rnnt_combine_losses(4, fake, fake, 0.5, 1.0, 0, None, None, None) == N.RNNT_EINVAL
+    # validate: V, blank, S, J with enc, dtype, flags
+    b = _batch()
+    pb = ctypes.byref(b)
+    n_bad = ctypes.c_int32()
+    assert L.rnnt_validate_inputs(pb, 0, 4, 0, 0, None, None, None, None, fake, ctypes.byref(n_bad),
+                                  None) == N.RNNT_EINVAL
+    assert L.rnnt_validate_inputs(pb, 16, 33, 0, 0, None, None, None, None, fake, ctypes.byref(n_bad),
+                                  None) == N.RNNT_EINVAL
+    assert L.rnnt_validate_inputs(pb, 16, 4, 0, 0, None, None, fake, None, fake, ctypes.byref(n_bad),
+                                  None) == N.RNNT_EINVAL
+    assert L.rnnt_validate_inputs(pb, 16, 4, 32, 5, None, None, fake, None, fake, ctypes.byref(n_bad),
+                                  None) == N.RNNT_EINVAL
+    assert L.rnnt_validate_inputs(pb, 16, 4, 0, 0, None, None, None, None, None, ctypes.byref(n_bad),
+                                  None) == N.RNNT_EINVAL
+    b2 = _batch()
+    b2.blank = 16
+    assert L.rnnt_validate_inputs(ctypes.byref(b2), 16, 4, 0, 0, None, None, None, None, fake, None,
+                                  None) == N.RNNT_EINVAL

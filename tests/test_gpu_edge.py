@@ -131,12 +131,12 @@ def test_infeasible_band_gives_inf_and_zero_joiner_gradients():
     say("[edge] infeasible band")
     out = run_step(b, S)
     ref = oracle_step(b, S)
+    check_step(out, ref, b, S)
     infeasible = [n for n in range(b.N) if b.u_len[n] > (S - 1) * b.t_len[n]]
     assert infeasible == [0, 2]
     for n in infeasible:
         assert out["pruned_loss"][n] == np.inf and ref["st"]["loss"][n] == np.inf
         assert np.all(out["enc_grad"][n] == 0) and np.all(out["dec_grad"][n] == 0)
-    check_step(out, ref, b, S)
 
 
 def test_s_equal_one():

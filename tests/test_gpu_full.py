@@ -1,14 +1,19 @@
 """Parity at the full workload sizes, in the configuration the benchmark times
-(PrunedRnntLoss.step with the logits kept for the backward).
+(PrunedRnntLoss.step: no [N, T, S, V] logits kept, the backward recomputes
+them in chunks of rows).
 
 - bpe and long (the two V=500, S=5 workloads): the oracle's whole pipeline on
-  the whole batch, every output compared.
-- largev: the oracle on two sampled utterances (the shortest and the one with
-  the longest transcript).
-- stress: the oracle cannot run whole utterances in seconds (V=8000,
-  T up to 1000), so it checks sampled outputs one by one: the trivial joiner's
-  log-probs on sampled frames, and the pruned joiner's on sampled frames of a
-  full-size launch with fixed, valid bounds.
+  the whole batch, every output of every utterance compared (stage 4 and
+  the bounds on the GPU's own occupations, see gpu_common.check_step).
+- largev: the same on two sampled utterances of the full batch, and on those
+  two as a batch of their own (so that dW and db are compared too), with the
+  library's chunking and with chunks of 1,024 rows.
+- stress: one full utterance as a batch of its own (two backward chunks),
+  every output compared, in two tests (the oracle's simple stage, then its
+  pruned stage: about a minute each); on the full batch the oracle checks
+  sampled outputs one by one: the trivial joiner's log-probs on sampled
+  frames, and the pruned joiner's on sampled frames of a full-size launch
+  with fixed, valid bounds.
 
 Every workload is also checked against properties that hold at any size:
 flow conservation of both lattices' occupations, zero row sums of the
@@ -20,8 +25,9 @@ import torch
 
 import oracle as O
 import paper_2206_13236_amd as P
-from gpu_common import (assert_close, check_step, dev_f32, dev_i32, dev_joiner, host, make_dev_batch,
-                        oracle_step, ranges_valid, run_step, say)
+from gpu_common import (assert_close, check_pruned_part, check_simple_part, check_step, dev_f32, dev_i32,
+                        dev_joiner, host, make_dev_batch, oracle_step, own_bounds, ranges_valid, run_step, say,
+                        sub_batch)
 from workloads import make_batch
 
 pytestmark = pytest.mark.gpu
@@ -95,11 +101,61 @@ def test_full_size_whole_batch_against_oracle(name):
     say(f"  near-tie utterances {sorted(amb)}")
 
 
+def _largev_pick(b):
+    return sorted({int(np.argmin(b.t_len)), int(np.argmax(b.u_len))})
+
+
 def test_full_size_largev_sampled_utterances():
     b, out = _run("largev")
-    idx = sorted({int(np.argmin(b.t_len)), int(np.argmax(b.u_len))})
+    idx = _largev_pick(b)
     say(f"[full] largev: oracle on utterances {idx}")
     check_step(out, oracle_step(b, b.wl.S, idx=idx), b, b.wl.S, whole_batch=False)
+
+
+@pytest.mark.parametrize("chunk", [0, 1024])
+def test_largev_two_utterances_as_a_batch(chunk):
+    # V = 5000, J = 512, fp32: every output including dW and db; chunks of
+    # 1,024 rows split the ~2,500 rows three ways (S = 5 does not divide 1,024,
+    # so frames straddle chunk edges)
+    full = make_batch("largev", seed=0)
+    b = sub_batch(full, _largev_pick(full))
+    say(f"[full] largev as a 2-utterance batch, backward chunk {chunk or 'default'}")
+    out = run_step(b, b.wl.S, bwd_chunk_rows=chunk)
+    check_step(out, oracle_step(b, b.wl.S), b, b.wl.S)
+
+
+_STRESS1 = {}
+
+
+def _stress_one():
+    """Utterance 0 of the stress batch as a batch of its own (T = 970, U_n = 217,
+    V = 8000, J = 768, S = 10, bf16 joiner): 9,700 padded rows, two backward
+    chunks."""
+    if not _STRESS1:
+        _RUNS.clear()
+        b = sub_batch(make_batch("stress", seed=0), [0])
+        say(f"[full] stress utterance 0: T={b.t_len[0]} U={b.u_len[0]} V={b.V}")
+        _STRESS1["b"] = b
+        _STRESS1["out"] = run_step(b, b.wl.S)
+        torch.cuda.empty_cache()
+    return _STRESS1["b"], _STRESS1["out"]
+
+
+def test_stress_utterance_simple_stage_against_oracle():
+    b, out = _stress_one()
+    say("[full] stress utterance 0: oracle simple stage (about a minute)")
+    ref = oracle_step(b, b.wl.S)
+    check_simple_part(out, ref, b, b.wl.S)
+    _STRESS1["simple_loss"] = ref["s1"]["loss"]
+
+
+def test_stress_utterance_pruned_stage_against_oracle():
+    b, out = _stress_one()
+    say("[full] stress utterance 0: oracle pruned stage on the GPU's bounds (about a minute)")
+    idx = np.arange(b.N)
+    r = own_bounds(out, b, b.wl.S, idx)
+    assert np.array_equal(out["ranges"], r)
+    check_pruned_part(out, b, b.wl.S, idx, r, simple_loss=_STRESS1.get("simple_loss"))
 
 
 def _fixed_bounds(t_len, u_len, T, S):

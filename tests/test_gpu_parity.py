@@ -181,13 +181,11 @@ def test_pruned_loss(name, alg, chunk):
     assert_close("py_occ", host(out["py_occ"]), gy_ref, atol=1e-4)
 
 
-@pytest.mark.parametrize("stored", [False, True], ids=["recompute", "stored_logits"])
-@pytest.mark.parametrize("name", list(CASES))
-def test_pruned_joiner_backward(name, stored):
+def _joiner_backward(name, stored, chunk_rows=0):
     o = _oracle(name)
     b = o["b"]
     bf = b.wl.joiner_dtype == "bf16"
-    say(f"[joiner-bwd] {name} bf16={bf} stored_logits={stored}")
+    say(f"[joiner-bwd] {name} bf16={bf} stored_logits={stored} chunk_rows={chunk_rows}")
     st = o["st"]
     lse32 = st["lse"].astype(np.float32)
     gx32, gy32 = st["gx"].astype(np.float32), st["gy"].astype(np.float32)
@@ -204,7 +202,7 @@ def test_pruned_joiner_backward(name, stored):
         logits, lse = fw["logits"], fw["lse"]
     out = P.rnnt_pruned_joiner_backward(
         batch, o["S"], *args, rng, lse, dev_f32(gx32), dev_f32(gy32), scale=dev_f32(o["sc"]),
-        want_logits_grad=(name == "tiny"), logits=logits)
+        want_logits_grad=(name == "tiny"), logits=logits, chunk_rows=chunk_rows)
     torch.cuda.synchronize()
     for k in ("enc_grad", "dec_grad"):
         assert_close(k, host(out[k]), ref[k], atol=grad_atol(ref[k], bf))
@@ -212,6 +210,31 @@ def test_pruned_joiner_backward(name, stored):
         assert_close(k, host(out[k]), ref[k], atol=grad_atol(ref[k], bf, param=True))
     if name == "tiny":
         assert_close("logits_grad", host(out["logits_grad"]), ref["logits_grad"], atol=1e-5)
+    return out
+
+
+@pytest.mark.parametrize("stored", [False, True], ids=["recompute", "stored_logits"])
+@pytest.mark.parametrize("name", list(CASES))
+def test_pruned_joiner_backward(name, stored):
+    _joiner_backward(name, stored)
+
+
+# chunks of rows that S does not divide (frames straddle chunk edges), three
+# or more chunks per batch
+CHUNKED = [("small_f32", 128), ("small_f32", 384), ("small_bf16", 128), ("small_bf16_oddv", 256), ("bpe_sub", 1024)]
+
+
+@pytest.mark.parametrize("stored", [False, True], ids=["recompute", "stored_logits"])
+@pytest.mark.parametrize("name,chunk", CHUNKED, ids=[f"{n}-{c}" for n, c in CHUNKED])
+def test_pruned_joiner_backward_in_chunks(name, chunk, stored):
+    b = _oracle(name)["b"]
+    assert -(-b.N * b.T * _oracle(name)["S"] // chunk) >= 3, "the case must span at least three chunks"
+    got = _joiner_backward(name, stored, chunk_rows=chunk)
+    # d enc and d dec add their pieces in tile order whatever the chunking:
+    # bitwise equal to the library's own chunk choice
+    one = _joiner_backward(name, stored)
+    for k in ("enc_grad", "dec_grad"):
+        assert torch.equal(got[k], one[k]), f"{k} depends on the chunking"
 
 
 @pytest.mark.parametrize("name", list(CASES))
@@ -224,11 +247,20 @@ def test_end_to_end(name):
     say(f"  near-tie utterances {sorted(amb)}")
 
 
-def test_end_to_end_recomputed_logits():
-    # the backward without the stored logits recomputes them (one chunk of rows at a time)
+@pytest.mark.parametrize("name", ["small_f32", "small_bf16"])
+def test_end_to_end_kept_logits(name):
+    # the forward stores the [N, T, S, V] logits and the backward streams them
+    b = _case(name)
+    say(f"[e2e] {name} keep_logits=True")
+    out = run_step(b, b.wl.S, keep_logits=True)
+    check_step(out, oracle_step(b, b.wl.S), b, b.wl.S)
+
+
+def test_end_to_end_small_chunks():
+    # the training step with backward chunks of 128 rows (seven chunks)
     b = _case("small_f32")
-    say("[e2e] small_f32 keep_logits=False")
-    out = run_step(b, b.wl.S, keep_logits=False)
+    say("[e2e] small_f32 backward chunks of 128 rows")
+    out = run_step(b, b.wl.S, bwd_chunk_rows=128)
     check_step(out, oracle_step(b, b.wl.S), b, b.wl.S)
 
 

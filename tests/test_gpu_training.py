@@ -77,6 +77,9 @@ def test_warmup_switch_skips_the_pruned_stages():
     for k in ("pruned_loss", "enc_grad", "dec_grad", "W_grad", "bias_grad"):
         assert torch.count_nonzero(warm[k]) == 0, k
     assert "ranges" not in warm
+    # the training loss is the scaled simple loss alone (formed by the library)
+    assert torch.equal(warm["loss"], 0.5 * warm["simple_loss"])
+    assert_close("total", host(warm["total"]), host(0.5 * warm["simple_loss"]).sum(), rtol=1e-6)
 
 
 @pytest.mark.parametrize("reduction", ["sum", "mean"])
@@ -90,6 +93,7 @@ def test_autograd_function_against_the_oracle(reduction):
     (3.0 * loss).backward()
     torch.cuda.synchronize()
     ref = oracle_step(b, S)
+    ref["st"] = O.pruned_stage(b.enc, b.dec, b.W, b.bias, ref["ranges"], b.symbols, b.t_len, b.u_len, b.wl.blank)
     total = 0.5 * ref["s1"]["loss"].sum() + ref["st"]["loss"].sum()
     k = 3.0 / (b.N if reduction == "mean" else 1)
     assert_close("loss", loss.item(), total / (b.N if reduction == "mean" else 1), rtol=1e-5)
