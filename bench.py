@@ -184,7 +184,8 @@ def _cpu_baseline(b, budget_s: float) -> dict:
                       f"{dt:.1f} s"}
 
 
-def _measure(P, _native, b, args, keep_logits: bool, roofline: bool, census: bool, spread: bool) -> dict:
+def _measure(P, _native, b, args, keep_logits: bool, roofline: bool, census: bool, spread: bool,
+             settle_s: float = 0.0) -> dict:
     """One workload's step on the GPU: warm-up, optionally a census pass with
     every kernel bracketed, then the timed steps (the dominant contraction
     bracketed by HIP events on every BRACKET_EVERY-th step when `roofline`)."""
@@ -214,6 +215,15 @@ def _measure(P, _native, b, args, keep_logits: bool, roofline: bool, census: boo
     for _ in range(args.warmup):
         run()
     torch.cuda.synchronize()
+    if settle_s > 0:
+        # untimed steps until the device has run busy for settle_s seconds:
+        # after a long idle phase (the CPU baseline) the first ~0.5 s of work
+        # run measurably slower than steady state
+        t_end = time.perf_counter() + settle_s
+        while time.perf_counter() < t_end:
+            for _ in range(10):
+                run()
+            torch.cuda.synchronize()
     L = _native.lib()
 
     def kernel_table(nsteps):
@@ -253,9 +263,13 @@ def _measure(P, _native, b, args, keep_logits: bool, roofline: bool, census: boo
         if census:
             res["kernels"] = kernels
             res["kernels_census_steps"] = census_steps
-    # the dominant contraction: joiner GEMMs with algorithmic work 2*M*J*V
-    # each (the backward's recomputation of the logits is overhead, not work)
-    work = {"joiner_fwd": 2.0 * M * J * V, "joiner_dh": 2.0 * M * J * V, "joiner_dw": 2.0 * M * J * V}
+    # the dominant contraction among the joiner GEMMs, algorithmic work per
+    # step: 2 M J V for the forward, for dh and for dW; the recomputed
+    # path's pipelined backward launches ("joiner_bwd": the next chunk's
+    # recomputed logits with the current chunk's dh and dW) do dh and dW,
+    # 4 M J V per step (the recomputation is overhead: time, not work)
+    work = {"joiner_fwd": 2.0 * M * J * V, "joiner_dh": 2.0 * M * J * V, "joiner_dw": 2.0 * M * J * V,
+            "joiner_bwd": 4.0 * M * J * V}
     dom = None
     if roofline:
         dom = max((k for k in work if k in kernels), key=lambda k: kernels[k]["us_per_step"])
@@ -354,7 +368,8 @@ def main() -> int:
     torch.zeros(1, device=dev)
     torch.cuda.synchronize()
 
-    head = _measure(P, _native, b, args, keep_logits=args.keep_logits, roofline=True, census=True, spread=True)
+    head = _measure(P, _native, b, args, keep_logits=args.keep_logits, roofline=True, census=True, spread=True,
+                    settle_s=0.5)
     step, batch, enc, dec, W, bias, run = head.pop("_ctx")
     band = None if args.no_band_algorithms else _band_algorithms(P, batch, b.wl.S, run())
     unpruned = None if args.no_unpruned else _unpruned(P, batch, enc, dec, W, bias, b.frames, dev)

@@ -220,12 +220,13 @@ struct JoinerBwdWs {
   int* frame_nt;
   int* frame_p;
   int4* rowinfo;
-  void* dl;
-  void* dlT;
+  void* dl[2];
+  void* dlT[2];
   void* wpad;
   float* dpre;
   float* enc_part;
-  void* hbuf;
+  void* hbuf[2];
+  void* hT[2];
   float* dw_part;
   float* db_part;
   int chunk_rows, splits, n_db_rows;
@@ -237,20 +238,24 @@ JoinerBwdWs joiner_bwd_layout(void* base, int N, int T, int S, int J, int V, int
   JoinerBwdWs w;
   const size_t M = (size_t)N * T * S;
   w.chunk_rows = joiner_bwd_chunk_rows(N, T, S, J, V, bf16, chunk_request);
-  w.splits = joiner_bwd_splits(J, V);
+  w.splits = joiner_bwd_splits(J, V, w.chunk_rows);
   w.n_db_rows = joiner_db_rows(w.chunk_rows);
   w.frame_off = c.take<int>((size_t)N + 1);
   w.frame_nt = c.take<int>((size_t)N * T);
   w.frame_p = c.take<int>((size_t)N * T);
   w.rowinfo = c.take<int4>(M);
+  // two ring slots of chunk buffers: d(logits), its bf16 transpose, h, its bf16 transpose
   const size_t dl_elems = (size_t)w.chunk_rows * joiner_ldl(V);
-  w.dl = bf16 ? (void*)c.take<uint16_t>(dl_elems) : (void*)c.take<float>(dl_elems);
-  w.dlT = bf16 ? (void*)c.take<uint16_t>(dl_elems) : nullptr;
+  const size_t h_elems = (size_t)w.chunk_rows * J;
+  for (int k = 0; k < 2; ++k) {
+    w.dl[k] = bf16 ? (void*)c.take<uint16_t>(dl_elems) : (void*)c.take<float>(dl_elems);
+    w.dlT[k] = bf16 ? (void*)c.take<uint16_t>(dl_elems) : nullptr;
+    w.hbuf[k] = bf16 ? (void*)c.take<uint16_t>(h_elems) : (void*)c.take<float>(h_elems);
+    w.hT[k] = bf16 ? (void*)c.take<uint16_t>(h_elems) : nullptr;
+  }
   w.wpad = (bf16 && V % 8 != 0) ? (void*)c.take<uint16_t>((size_t)J * joiner_ldl(V)) : nullptr;
   w.dpre = c.take<float>((size_t)w.chunk_rows * J);
   w.enc_part = c.take<float>((M + 127) / 128 * 2 * J);
-  const size_t h_elems = (size_t)w.chunk_rows * J;
-  w.hbuf = bf16 ? (void*)c.take<uint16_t>(h_elems) : (void*)c.take<float>(h_elems);
   w.dw_part = c.take<float>((size_t)w.splits * J * V);
   w.db_part = c.take<float>((size_t)w.n_db_rows * V);
   w.bytes = c.off;
@@ -340,14 +345,19 @@ void set_joiner_bwd(JoinerArgs& a, const JoinerBwdWs& w, const float* lse, const
   a.gxo = gx;
   a.gyo = gy;
   a.scale = scale;
-  a.dl = w.dl;
-  a.dlT = w.dlT;
+  a.dl = w.dl[0];
+  a.dlT = w.dlT[0];
+  a.hT = w.hT[0];
+  a.ring1[0] = w.hbuf[1];
+  a.ring1[1] = w.hT[1];
+  a.ring1[2] = w.dl[1];
+  a.ring1[3] = w.dlT[1];
   a.wpad = w.wpad;
   a.ldl = joiner_ldl(a.V);
   a.chunk_rows = w.chunk_rows;
   a.dpre = w.dpre;
   a.enc_part = w.enc_part;
-  a.hbuf = w.hbuf;
+  a.hbuf = w.hbuf[0];
   a.dw_part = w.dw_part;
   a.splits = w.splits;
   a.db_part = w.db_part;

@@ -555,21 +555,57 @@ __global__ __launch_bounds__(256) void joiner_combine_kernel(JoinerArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Backward 1: recompute logits from h (hbuf), d(logits) for a chunk of rows,
-// db partials.
+// LDS of the backward's GEMM tiles: the operand stages (also the epilogue's
+// C tile), then per-row info and per-row scalars of the row tile. One size
+// for all of them, so that tiles of different kinds share one launch.
+// ---------------------------------------------------------------------------
+constexpr int kBwdStageBytes = CfgF::SMEM_BYTES > CfgB::SMEM_BYTES ? CfgF::SMEM_BYTES : CfgB::SMEM_BYTES;
+static_assert(CfgBw::SMEM_BYTES <= kBwdStageBytes, "dW stages fit");
+constexpr int kBwdLdsBytes = kBwdStageBytes + CfgF::BM * (int)sizeof(int4) + CfgF::BM * (int)sizeof(float4);
+
+template <class Cfg>
+DEV typename Cfg::T* lds_stages(unsigned char* lds) { return reinterpret_cast<typename Cfg::T*>(lds); }
+DEV int4* lds_rowinfo(unsigned char* lds) { return reinterpret_cast<int4*>(lds + kBwdStageBytes); }
+DEV float4* lds_rowx(unsigned char* lds) {
+  return reinterpret_cast<float4*>(lds + kBwdStageBytes + CfgF::BM * sizeof(int4));
+}
+
+// Tile `tile` (row tile tile / ncol, column tile tile % ncol) of the rows
+// [cm0, cm1) whose count of active tiles (rows present) is computed here: -1
+// for blocks beyond it. The XCD-aware order of xcd_tile_id over a part of a
+// launch: v is the block's index within its part of nblocks blocks.
+DEV int part_tile(int v, int nblocks, int n_active) {
+  const int n = min(n_active, nblocks);
+  if (v >= n) return -1;
+  const int per = n / kNumXcd, rem = n % kNumXcd;
+  const int x = v % kNumXcd, loc = v / kNumXcd;
+  return (x < rem ? x * (per + 1) : rem * (per + 1) + (x - rem) * per) + loc;
+}
+DEV int chunk_row_tiles(const JoinerArgs& a, int cm0, int cm1, int bm) {
+  const int mend = min(cm1, a.frame_off[a.b.N] * a.S);
+  return mend > cm0 ? (mend - cm0 + bm - 1) / bm : 0;
+}
+
+// ---------------------------------------------------------------------------
+// Backward 1: recompute logits from h (hbuf, rows of the chunk), d(logits)
+// of one 128 x 128 tile into the chunk buffer dl (and, for bf16, its
+// transpose dlT, the dW operand: the lane's 4 consecutive rows of one column
+// as one 8-byte store; rows past the chunk's end up to the tile end get
+// zeros), db partials (one row per wave row of each row tile of the chunk;
+// the first chunk writes them, later chunks add to them).
 // ---------------------------------------------------------------------------
 template <bool BF, int WM>
-__global__ __launch_bounds__(kGemmThreads) void joiner_dlogits_kernel(JoinerArgs a, int cm0, int cm1) {
+DEV void dlogits_tile(const JoinerArgs& a, int cm0, int cm1, int v, int nblocks, int ncol, unsigned char* lds) {
   using TIn = typename In<BF>::T;
   using Cfg = typename In<BF>::Cfg;
-  __shared__ __align__(16) typename Cfg::T smem[Cfg::SMEM_BYTES / sizeof(typename Cfg::T)];
-  __shared__ int4 ri[Cfg::BM];
-  __shared__ float4 rx[Cfg::BM];  // lse, gx, gy, scale
+  typename Cfg::T* smem = lds_stages<Cfg>(lds);
+  int4* ri = lds_rowinfo(lds);
+  float4* rx = lds_rowx(lds);  // lse, gx, gy, scale
   const int M = a.frame_off[a.b.N] * a.S;
   const int mend = min(cm1, M);
-  const int tile = xcd_tile_id(mend > cm0 ? (mend - cm0 + Cfg::BM - 1) / Cfg::BM * gridDim.y : 0);
+  const int tile = part_tile(v, nblocks, chunk_row_tiles(a, cm0, cm1, Cfg::BM) * ncol);
   if (tile < 0) return;
-  const int mtl = tile / gridDim.y, nt = tile - mtl * gridDim.y;
+  const int mtl = tile / ncol, nt = tile - mtl * ncol;
   const int m0 = cm0 + mtl * Cfg::BM;
   const int v0 = nt * Cfg::BN;
   const int V = a.V, J = a.J, TS = a.b.T * a.S;
@@ -626,8 +662,23 @@ __global__ __launch_bounds__(kGemmThreads) void joiner_dlogits_kernel(JoinerArgs
           else dl[(size_t)(m - cm0) * a.ldl + col] = d;
         }
         colsum[j] += d;
+        acc[i][j][r] = d;
       }
     }
+  if constexpr (BF) {
+    uint16_t* dlT = reinterpret_cast<uint16_t*>(a.dlT);
+#pragma unroll
+    for (int i = 0; i < Cfg::FM; ++i)
+#pragma unroll
+      for (int j = 0; j < Cfg::FN; ++j) {
+        const int col = v0 + tile_col<Cfg>(j);
+        if (col >= a.ldl) continue;
+        const int mr0 = m0 + tile_row<Cfg>(i, 0) - cm0;
+        *reinterpret_cast<uint2*>(dlT + (size_t)col * a.chunk_rows + mr0) =
+            make_uint2((uint32_t)f2bf(acc[i][j][0]) | ((uint32_t)f2bf(acc[i][j][1]) << 16),
+                       (uint32_t)f2bf(acc[i][j][2]) | ((uint32_t)f2bf(acc[i][j][3]) << 16));
+      }
+  }
   // db partial: sum over this wave's WM rows, one row of db_part per (m-tile
   // of the chunk, wave row); the first chunk writes it, later ones add to it.
   const int mt = (m0 - cm0) / Cfg::BM;
@@ -863,41 +914,41 @@ DEV void tile_enc_dec(const JoinerArgs& a, const float* C, int LDC, int cm0, int
 
 // ---------------------------------------------------------------------------
 // Backward 2: dh = dl W^T, dpre = dh (1 - h^2), summed into the d enc / d dec
-// pieces in LDS; also leaves h of the chunk's rows in hbuf (zero for absent
-// slots) as the dW contraction's operand: [rows, J] for fp32, transposed
-// [J, chunk_rows] for bf16.
+// pieces in LDS. With `write_h` (the path that streams stored logits, where
+// no h pass ran) it also leaves h of the chunk's rows as the dW
+// contraction's operand (zero for absent slots): [rows, J] in hbuf for fp32,
+// transposed [J, chunk_rows] in hT for bf16.
 // ---------------------------------------------------------------------------
 template <bool BF, int WM>
-__global__ __launch_bounds__(kGemmThreads, 4) void joiner_dh_kernel(JoinerArgs a, int cm0, int cm1) {
+DEV void dh_tile(const JoinerArgs& a, int cm0, int cm1, int v, int nblocks, int ncol, unsigned char* lds,
+                 bool write_h) {
   using TIn = typename In<BF>::T;
   using Cfg = typename In<BF>::Cfg;
-  __shared__ __align__(16) typename Cfg::T smem[Cfg::SMEM_BYTES / sizeof(typename Cfg::T)];
-  __shared__ int4 ri[Cfg::BM];
+  typename Cfg::T* smem = lds_stages<Cfg>(lds);
+  int4* ri = lds_rowinfo(lds);
   const int M = a.frame_off[a.b.N] * a.S;
   const int mend = min(cm1, M);
-  const int tile = xcd_tile_id(mend > cm0 ? (mend - cm0 + Cfg::BM - 1) / Cfg::BM * gridDim.y : 0);
+  const int tile = part_tile(v, nblocks, chunk_row_tiles(a, cm0, cm1, Cfg::BM) * ncol);
   if (tile < 0) return;
-  const int mtl = tile / gridDim.y, nt = tile - mtl * gridDim.y;
+  const int mtl = tile / ncol, nt = tile - mtl * ncol;
   const int m0 = cm0 + mtl * Cfg::BM;
   const int j0 = nt * Cfg::BN;
-  const int V = a.V, J = a.J;
+  const int J = a.J;
   for (int r = threadIdx.x; r < Cfg::BM; r += Cfg::NT)
     ri[r] = (m0 + r < mend) ? a.rowinfo[m0 + r] : make_int4(0, 0, -1, -1);
   __syncthreads();
-  const TIn* W = reinterpret_cast<const TIn*>(a.W);
   DlSrcKC<Cfg> sa{make_rsrc(a.dl, (size_t)a.chunk_rows * a.ldl * sizeof(typename Cfg::T)), m0, cm0, mend, a.ldl};
   WtSrcKC<Cfg, TIn, WM> sb(a, j0);
   KCLoader<Cfg, Cfg::BM, DlSrcKC<Cfg>> la(sa);
   KCLoader<Cfg, Cfg::BN, WtSrcKC<Cfg, TIn, WM>> lb(sb);
   const TileFrameRegs fr = tile_frames_fetch(a, m0, mend, Cfg::BM);
   floatx4 acc[Cfg::FM][Cfg::FN];
-  gemm_mainloop<Cfg>(la, lb, 0, V, smem, acc);
+  gemm_mainloop<Cfg>(la, lb, 0, a.V, smem, acc);
 
   // Epilogue through LDS (the operand stages are free after the main loop's
   // last barrier): the tile goes to LDS in the MFMA layout and comes back row
   // by row, so that enc, dec, dpre and h are read and written with 16-byte
   // accesses per thread along J.
-  typename Cfg::T* hbuf = reinterpret_cast<typename Cfg::T*>(a.hbuf);
   constexpr int LDC = Cfg::BN + 4;
   static_assert(Cfg::BM * LDC * 4 <= Cfg::SMEM_BYTES, "epilogue tile fits the operand stages");
   float* C = reinterpret_cast<float*>(smem);
@@ -937,7 +988,9 @@ __global__ __launch_bounds__(kGemmThreads, 4) void joiner_dh_kernel(JoinerArgs a
       hk[q8] = make_float4(h[0], h[1], h[2], h[3]);
     } else {
       // h [rows, J] for the fp32 dW
-      if (m < mend) *reinterpret_cast<float4*>(hbuf + (size_t)(m - cm0) * J + jj) = make_float4(h[0], h[1], h[2], h[3]);
+      if (write_h && m < mend)
+        *reinterpret_cast<float4*>(reinterpret_cast<float*>(a.hbuf) + (size_t)(m - cm0) * J + jj) =
+            make_float4(h[0], h[1], h[2], h[3]);
     }
 #pragma unroll
     for (int q = 0; q < 4; ++q) cr[q] = dp[q];  // dpre stays in the tile for the d enc / d dec pieces
@@ -945,6 +998,7 @@ __global__ __launch_bounds__(kGemmThreads, 4) void joiner_dh_kernel(JoinerArgs a
   __syncthreads();
   tile_enc_dec<Cfg>(a, C, LDC, cm0, m0, mend, j0, ri, fr);
   if constexpr (BF) {
+    if (!write_h) return;
     // h back to the tile (0 past mend), then h^T [J, chunk_rows] for the
     // bf16 dW: the lane's 4 consecutive rows of the MFMA layout as one
     // 8-byte store
@@ -956,6 +1010,7 @@ __global__ __launch_bounds__(kGemmThreads, 4) void joiner_dh_kernel(JoinerArgs a
       *reinterpret_cast<float4*>(C + row * LDC + cg * 4) = hk[q8];
     }
     __syncthreads();
+    uint16_t* hT = reinterpret_cast<uint16_t*>(a.hT);
 #pragma unroll
     for (int i = 0; i < Cfg::FM; ++i)
 #pragma unroll
@@ -966,7 +1021,7 @@ __global__ __launch_bounds__(kGemmThreads, 4) void joiner_dh_kernel(JoinerArgs a
 #pragma unroll
         for (int r = 0; r < 4; ++r) hv[r] = C[tile_row<Cfg>(i, r) * LDC + tile_col<Cfg>(j)];
         const int mr0 = m0 + tile_row<Cfg>(i, 0) - cm0;
-        *reinterpret_cast<uint2*>(hbuf + (size_t)jj * a.chunk_rows + mr0) =
+        *reinterpret_cast<uint2*>(hT + (size_t)jj * a.chunk_rows + mr0) =
             make_uint2((uint32_t)f2bf(hv[0]) | ((uint32_t)f2bf(hv[1]) << 16),
                        (uint32_t)f2bf(hv[2]) | ((uint32_t)f2bf(hv[3]) << 16));
       }
@@ -1008,20 +1063,21 @@ __global__ __launch_bounds__(256) void joiner_dlt_kernel(JoinerArgs a, int cm0, 
 }
 
 // ---------------------------------------------------------------------------
-// Backward 3: dW partial += h^T dl over one split of the chunk's rows
+// Backward 3: dW partial += h^T dl over one split of the chunk's rows (the
+// first chunk writes the partials, later chunks add to them). Tiles: the
+// (j, v) tiles of one split are consecutive tile ids, so one XCD reads that
+// split's rows.
 // ---------------------------------------------------------------------------
 template <bool BF>
-__global__ __launch_bounds__(kGemmThreads, 4) void joiner_dw_kernel(JoinerArgs a, int cm0, int cm1, int first) {
-  using TIn = typename In<BF>::T;
+DEV void dw_tile(const JoinerArgs& a, int cm0, int cm1, int first, int v, int nj, int nv, unsigned char* lds) {
   using Cfg = typename std::conditional<BF, CfgBw, CfgF>::type;
-  __shared__ __align__(16) typename Cfg::T smem[Cfg::SMEM_BYTES / sizeof(typename Cfg::T)];
+  typename Cfg::T* smem = lds_stages<Cfg>(lds);
   const int M = a.frame_off[a.b.N] * a.S;
   const int mend = min(cm1, M);
-  // the (j, v) tiles of one split are consecutive tile ids: one XCD reads that split's rows
-  const int tile = xcd_tile_id(gridDim.x * gridDim.y * gridDim.z);
-  const int per_split = gridDim.x * gridDim.y;
+  const int per_split = nj * nv;
+  const int tile = part_tile(v, per_split * a.splits, per_split * a.splits);
   const int z = tile / per_split, jv = tile - z * per_split;
-  const int jt = jv / gridDim.y, vt = jv - jt * gridDim.y;
+  const int jt = jv / nv, vt = jv - jt * nv;
   const int j0 = jt * Cfg::BM, v0 = vt * Cfg::BN;
   const int rows = cm1 - cm0;
   const int per = ((rows + a.splits - 1) / a.splits + Cfg::BK - 1) / Cfg::BK * Cfg::BK;
@@ -1033,8 +1089,8 @@ __global__ __launch_bounds__(kGemmThreads, 4) void joiner_dw_kernel(JoinerArgs a
     // no rows for this split: the first chunk still defines the partial
     if (first) {
       for (int e = threadIdx.x; e < Cfg::BM * Cfg::BN; e += Cfg::NT) {
-        const int j = j0 + e / Cfg::BN, v = v0 + e % Cfg::BN;
-        if (j < J && v < V) part[(size_t)j * V + v] = 0.f;
+        const int j = j0 + e / Cfg::BN, vv = v0 + e % Cfg::BN;
+        if (j < J && vv < V) part[(size_t)j * V + vv] = 0.f;
       }
     }
     return;
@@ -1042,7 +1098,7 @@ __global__ __launch_bounds__(kGemmThreads, 4) void joiner_dw_kernel(JoinerArgs a
   floatx4 acc[Cfg::FM][Cfg::FN];
   if constexpr (BF) {
     const size_t tb = (size_t)a.chunk_rows * sizeof(typename Cfg::T);
-    TrSrcKC<Cfg> sa{make_rsrc(a.hbuf, tb * J), cm0, ke, j0, J, a.chunk_rows};
+    TrSrcKC<Cfg> sa{make_rsrc(a.hT, tb * J), cm0, ke, j0, J, a.chunk_rows};
     TrSrcKC<Cfg> sb{make_rsrc(a.dlT, tb * a.ldl), cm0, ke, v0, V, a.chunk_rows};
     KCLoader<Cfg, Cfg::BM, TrSrcKC<Cfg>> la(sa);
     KCLoader<Cfg, Cfg::BN, TrSrcKC<Cfg>> lb(sb);
@@ -1062,13 +1118,43 @@ __global__ __launch_bounds__(kGemmThreads, 4) void joiner_dw_kernel(JoinerArgs a
       if (j >= J) continue;
 #pragma unroll
       for (int jj = 0; jj < Cfg::FN; ++jj) {
-        const int v = v0 + tile_col<Cfg>(jj);
-        if (v < V) {
-          float* q = part + (size_t)j * V + v;
+        const int vv = v0 + tile_col<Cfg>(jj);
+        if (vv < V) {
+          float* q = part + (size_t)j * V + vv;
           *q = first ? acc[i][jj][r] : *q + acc[i][jj][r];
         }
       }
     }
+}
+
+// The backward's GEMM kernel. Every tile kind runs in one kernel, each on
+// its own range of blocks, so that the recomputed logits of the next chunk
+// (L), dh of the current chunk (D) and its dW (W) share a launch: a chunk's
+// dh alone puts only one workgroup on each CU.
+struct BwdParts {
+  int nL, nLcol;   // blocks and column tiles of L (chunk [lm0, lm1) of `nxt`)
+  int nD, nDcol;   // blocks and column tiles of D (chunk [cm0, cm1) of `cur`)
+  int nW, nWj, nWv;  // blocks and (j, v) tiles per split of W (same chunk)
+  int lm0, lm1, cm0, cm1, first;
+  int write_h;     // D also leaves h for a later W (no h pass ran)
+};
+
+// Blocks in the order W, D, L: the dW tiles, the longest, start first.
+template <bool BF, int WMF, int WMH>
+__global__ __launch_bounds__(kGemmThreads, 4) void joiner_bwd_gemm_kernel(JoinerArgs cur, JoinerArgs nxt, BwdParts p) {
+  __shared__ __align__(16) unsigned char lds[kBwdLdsBytes];
+  int b = blockIdx.x;
+  if (b < p.nW) {
+    dw_tile<BF>(cur, p.cm0, p.cm1, p.first, b, p.nWj, p.nWv, lds);
+    return;
+  }
+  b -= p.nW;
+  if (b < p.nD) {
+    dh_tile<BF, WMH>(cur, p.cm0, p.cm1, b, p.nD, p.nDcol, lds, p.write_h != 0);
+    return;
+  }
+  b -= p.nD;
+  dlogits_tile<BF, WMF>(nxt, p.lm0, p.lm1, b, p.nL, p.nLcol, lds);
 }
 
 // The tail of the backward: dW and db summed from their partials, d enc and
@@ -1260,16 +1346,106 @@ DEV void tail_dec_pieces(const JoinerArgs& a, int b, int* sp, int cm0, int cm1) 
   }
 }
 
+// h = tanh(enc + dec) of a chunk's rows [cm0, cm1) for the recomputed logits
+// (rows [rows, J] in h) and, for bf16, for dW (transposed [J, chunk_rows] in
+// hT), zero for absent slots and, in hT, for rows past the last row up to
+// the 128-row tile end (the dW loads read 16-byte segments across it).
+struct HPass {
+  int blocks, cm0, cm1;
+  void* h;
+  void* hT;
+};
+
+// fp32: one 16-byte group of J per thread.
+DEV void h_pass_f32(const JoinerArgs& a, const HPass& hp, int b) {
+  const int M = a.frame_off[a.b.N] * a.S;
+  const int mend = min(hp.cm1, M);
+  const int cpr = a.J / 4;
+  const size_t i = (size_t)b * kTailThreads + threadIdx.x;
+  const int rr = (int)(i / cpr), c = (int)(i - (size_t)rr * cpr);
+  const int m = hp.cm0 + rr;
+  if (m >= mend) return;
+  const int4 info = a.rowinfo[m];
+  const int j = c * 4;
+  const EncDec<float> ed(a);
+  RawVec<float, 4> e, d;
+  const int n = info.w >= 0 ? 4 : 0;
+  raw_load(ed.enc, (uint32_t)(info.x + j) * 4, n, kSegVector, e);
+  raw_load(ed.dec, (uint32_t)(info.y + j) * 4, n, kSegVector, d);
+  float fe[4], fd[4], h[4];
+  raw_to_float(e, fe);
+  raw_to_float(d, fd);
+#pragma unroll
+  for (int q = 0; q < 4; ++q) h[q] = info.w >= 0 ? fast_tanh(fe[q] + fd[q]) : 0.f;
+  *reinterpret_cast<float4*>(reinterpret_cast<float*>(hp.h) + (size_t)rr * a.J + j) = make_float4(h[0], h[1], h[2], h[3]);
+}
+
+// bf16: a 64-row x 64-column tile per block through LDS, both layouts
+// written 16 bytes per thread.
+constexpr int kHTile = 64;
+static int h_pass_bf16_blocks(int rows, int J) {
+  const int rt = (rows + CfgF::BM - 1) / CfgF::BM * (CfgF::BM / kHTile);  // to the 128-row tile end
+  return rt * ((J + kHTile - 1) / kHTile);
+}
+DEV void h_pass_bf16(const JoinerArgs& a, const HPass& hp, int b, uint16_t (*tile)[kHTile + 8]) {
+  const int M = a.frame_off[a.b.N] * a.S;
+  const int mend = min(hp.cm1, M);
+  const int ncj = (a.J + kHTile - 1) / kHTile;
+  const int rt = b / ncj, jt = b - rt * ncj;
+  const int r0 = rt * kHTile, j0 = jt * kHTile;  // rows (m - cm0), columns j
+  const int ty = threadIdx.x >> 3, tx = threadIdx.x & 7;
+  const EncDec<uint16_t> ed(a);
+#pragma unroll
+  for (int hh = 0; hh < 2; ++hh) {
+    const int r = ty + 32 * hh, m = hp.cm0 + r0 + r, j = j0 + tx * 8;
+    uint4 o = make_uint4(0, 0, 0, 0);
+    if (m < mend && j < a.J) {
+      const int4 info = a.rowinfo[m];
+      if (info.w >= 0) {
+        RawVec<uint16_t, 8> e, d;
+        raw_load(ed.enc, (uint32_t)(info.x + j) * 2, 8, kSegVector, e);
+        raw_load(ed.dec, (uint32_t)(info.y + j) * 2, 8, kSegVector, d);
+        float fe[8], fd[8];
+        raw_to_float(e, fe);
+        raw_to_float(d, fd);
+        uint32_t w[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          w[q] = (uint32_t)f2bf(fast_tanh(fe[2 * q] + fd[2 * q])) |
+                 ((uint32_t)f2bf(fast_tanh(fe[2 * q + 1] + fd[2 * q + 1])) << 16);
+        o = make_uint4(w[0], w[1], w[2], w[3]);
+      }
+      *reinterpret_cast<uint4*>(reinterpret_cast<uint16_t*>(hp.h) + (size_t)(r0 + r) * a.J + j) = o;
+    }
+    *reinterpret_cast<uint4*>(&tile[r][tx * 8]) = o;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int hh = 0; hh < 2; ++hh) {
+    const int c = ty + 32 * hh;  // column within the tile: hT row
+    if (j0 + c >= a.J) continue;
+    uint32_t w[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      w[q] = (uint32_t)tile[tx * 8 + 2 * q][c] | ((uint32_t)tile[tx * 8 + 2 * q + 1][c] << 16);
+    *reinterpret_cast<uint4*>(reinterpret_cast<uint16_t*>(hp.hT) + (size_t)(j0 + c) * a.chunk_rows + r0 + tx * 8) =
+        make_uint4(w[0], w[1], w[2], w[3]);
+  }
+}
+
 struct TailRanges {
   int dec, enc, wsum, dbsum;  // block counts, in launch order
   int cm0, cm1;               // the chunk whose d dec pieces the dec blocks add
+  HPass h0, h1;               // h passes of later chunks (recomputed path), run after them
 };
 
-// One launch per chunk of rows: its d dec pieces; the last chunk's launch
-// also runs the d enc, dW and db reductions.
+// One launch per chunk of rows: its d dec pieces and the h passes of later
+// chunks; the last chunk's launch also runs the d enc, dW and db reductions.
+template <bool BF>
 __global__ __launch_bounds__(kTailThreads) void joiner_tail_kernel(JoinerArgs a, TailRanges r) {
   extern __shared__ int sp[];  // p_t of one utterance (d dec blocks)
   __shared__ float red[kTailThreads / kDbCols][kDbCols];  // db blocks
+  __shared__ uint16_t htile[BF ? kHTile : 1][kHTile + 8];  // bf16 h pass
   int b = blockIdx.x;
   if (b < r.dec) { tail_dec_pieces(a, b, sp, r.cm0, r.cm1); return; }
   b -= r.dec;
@@ -1277,7 +1453,12 @@ __global__ __launch_bounds__(kTailThreads) void joiner_tail_kernel(JoinerArgs a,
   b -= r.enc;
   if (b < r.wsum) { tail_wsum(a, b); return; }
   b -= r.wsum;
-  tail_dbsum(a, b, red);
+  if (b < r.dbsum) { tail_dbsum(a, b, red); return; }
+  b -= r.dbsum;
+  const HPass& hp = b < r.h0.blocks ? r.h0 : r.h1;
+  if (b >= r.h0.blocks) b -= r.h0.blocks;
+  if constexpr (BF) h_pass_bf16(a, hp, b, htile);
+  else h_pass_f32(a, hp, b);
 }
 
 // ranges[n,t,s] = s: every (t, u) of the lattice as a "band" of width U+1.
@@ -1320,20 +1501,25 @@ static long long even_chunk(long long mmax, long long cap) {
   return ((mmax + n - 1) / n + 127) / 128 * 128;
 }
 
-// The backward's chunk: at most d(logits) of about 20 MiB, but 8,192 to
-// 16,384 rows (64 to 128 row tiles, so that each chunk's dh and recomputed
-// logits put one or two workgroups on every CU), and within the 32-bit
-// limit. The bound depends on J, V and the dtype only, not on N or T;
-// `request` (a multiple of 128, or 0) overrides it.
+// The backward's chunk: d(logits) of about 16 MiB, but 8,192 to 16,384 rows
+// (64 to 128 row tiles, so that each launch of the pipelined backward puts
+// one or two workgroups of every kind on each CU), within the 32-bit limit.
+// The bound depends on J, V and the dtype only, not on N or T. Chunks are
+// taken whole from the start of the padded rows: rows past the last frame of
+// the batch (padding frames take none) are absent, so a trailing chunk that
+// holds only those costs a few empty launches, while splitting the present
+// rows evenly would leave both chunks under-filled. `request` (a multiple of
+// 128, or 0) overrides the size.
 int joiner_bwd_chunk_rows(int N, int T, int S, int J, int V, int bf16, int request) {
   const long long mmax = (long long)N * T * S;
-  if (request > 0) return (int)(request < mmax ? request : (mmax + 127) / 128 * 128);
+  const long long all = (mmax + 127) / 128 * 128;
+  if (request > 0) return (int)(request < all ? request : all);
   const long long bytes_per_row = (long long)joiner_ldl(V) * (bf16 ? 2 : 4);
-  long long cap = ((20ll << 20) / bytes_per_row) / 128 * 128;
+  long long cap = ((16ll << 20) / bytes_per_row) / 128 * 128;
   cap = cap < 8192 ? 8192 : cap > 16384 ? 16384 : cap;
   const long long lim = joiner_bwd_chunk_max_rows(J, V);
   if (cap > lim) cap = lim;
-  return (int)even_chunk(mmax, cap);
+  return (int)(cap < all ? cap : all);
 }
 
 int joiner_fwd_chunk_rows(int N, int T, int S, int J, int bf16) {
@@ -1347,9 +1533,12 @@ int joiner_fwd_chunk_rows(int N, int T, int S, int J, int bf16) {
 
 bool joiner_fwd_uses_hbuf(int bf16) { return bf16 ? kFwdHbuf<true> : kFwdHbuf<false>; }
 
-int joiner_bwd_splits(int J, int V) {
-  const int tiles = ((J + 127) / 128) * ((V + 127) / 128);
-  int s = (512 + tiles - 1) / tiles;  // two workgroups per CU
+// dW splits a chunk's rows into ranges of about 2 max(J, V) rows, so that a
+// dW tile does about twice the work of a dh or recomputed-logits tile of the
+// same launch (their K is V or J): long enough K loops, few partials.
+int joiner_bwd_splits(int J, int V, int chunk_rows) {
+  const int target = 2 * (J > V ? J : V);
+  int s = (chunk_rows + target / 2) / target;
   if (s < 1) s = 1;
   if (s > 32) s = 32;
   return s;
@@ -1414,90 +1603,163 @@ hipError_t launch_joiner_fwd(const JoinerArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_joiner_bwd(const JoinerArgs& a, hipStream_t s) {
-  const int mmax = a.b.N * a.b.T * a.S;
-  const int V = a.V, J = a.J;
-  hipError_t e = hipSuccess;
-  if (a.logits_grad) {
-    e = launch_fill_f32(a.logits_grad, (size_t)mmax * V, 0.f, s);
-    if (e != hipSuccess) return e;
+// Joiner args for ring slot k % 2 of the recomputed path's chunk buffers.
+static JoinerArgs ring_slot(const JoinerArgs& a, int k) {
+  JoinerArgs c = a;
+  if (k & 1) {
+    c.hbuf = a.ring1[0];
+    c.hT = a.ring1[1];
+    c.dl = a.ring1[2];
+    c.dlT = a.ring1[3];
   }
-  // segment modes of the W reads: the recomputed forward reads W rows in
+  return c;
+}
+
+static TailRanges tail_ranges(const JoinerArgs& a, int cm0, int cm1, bool last) {
+  const size_t JV = (size_t)a.J * a.V;
+  const int R = (a.J / 4 >= kTailThreads) ? 1 : kTailThreads / (a.J / 4);
+  TailRanges tr{};
+  tr.cm0 = cm0;
+  tr.cm1 = cm1;
+  tr.dec = (cm1 > cm0) ? (a.b.U + 1) * a.b.N : 0;
+  tr.enc = last ? (a.b.N * a.b.T + R - 1) / R : 0;
+  const bool wvec = JV % kWsumVec == 0 && (reinterpret_cast<uintptr_t>(a.W_grad) & 15) == 0;
+  const size_t wthreads = wvec ? JV / kWsumVec : JV;
+  tr.wsum = (last && a.W_grad) ? (int)((wthreads + kTailThreads - 1) / kTailThreads) : 0;
+  tr.dbsum = (last && a.bias_grad) ? (a.V + kDbCols - 1) / kDbCols : 0;
+  return tr;
+}
+
+static HPass h_pass(const JoinerArgs& slot, int cm0, int cm1) {
+  HPass h{};
+  h.cm0 = cm0;
+  h.cm1 = cm1;
+  h.h = slot.hbuf;
+  h.hT = slot.hT;
+  const int rows = cm1 - cm0;
+  h.blocks = slot.bf16 ? h_pass_bf16_blocks(rows, slot.J)
+                       : (int)(((size_t)rows * (slot.J / 4) + kTailThreads - 1) / kTailThreads);
+  return h;
+}
+
+static hipError_t launch_tail(const JoinerArgs& a, const TailRanges& tr, hipStream_t s, const char* name) {
+  const int blocks = tr.dec + tr.enc + tr.wsum + tr.dbsum + tr.h0.blocks + tr.h1.blocks;
+  if (blocks == 0) return hipSuccess;
+  RNNT_PROF(s, name);
+  const size_t sh = (size_t)a.b.T * sizeof(int);
+  if (a.bf16) hipLaunchKernelGGL(joiner_tail_kernel<true>, dim3(blocks), dim3(kTailThreads), sh, s, a, tr);
+  else hipLaunchKernelGGL(joiner_tail_kernel<false>, dim3(blocks), dim3(kTailThreads), sh, s, a, tr);
+  return hipGetLastError();
+}
+
+// A GEMM launch of the backward: L of chunk [lm0, lm1) (ring slot of
+// `nxt`), D and/or W of chunk [cm0, cm1) (slot of `cur`); an empty range or
+// a false flag skips its part.
+static hipError_t launch_bwd_gemms(const JoinerArgs& cur, const JoinerArgs& nxt, int lm0, int lm1, int cm0,
+                                   int cm1, bool do_D, bool do_W, bool write_h, hipStream_t s) {
+  const int V = cur.V, J = cur.J;
+  BwdParts p{};
+  p.lm0 = lm0;
+  p.lm1 = lm1;
+  p.cm0 = cm0;
+  p.cm1 = cm1;
+  p.first = cm0 == 0;
+  p.write_h = write_h;
+  p.nLcol = (V + 127) / 128;
+  p.nL = lm1 > lm0 ? (lm1 - lm0 + 127) / 128 * p.nLcol : 0;
+  p.nDcol = (J + 127) / 128;
+  p.nD = (do_D && cm1 > cm0) ? (cm1 - cm0 + 127) / 128 * p.nDcol : 0;
+  p.nWj = (J + 127) / 128;
+  p.nWv = (V + 127) / 128;
+  p.nW = (do_W && cm1 > cm0) ? p.nWj * p.nWv * cur.splits : 0;
+  const int blocks = p.nL + p.nD + p.nW;
+  if (blocks == 0) return hipSuccess;
+  // profiling names: the stored-logits path's separate dh and dW launches,
+  // and every launch of the recomputed path's pipeline as one kernel
+  const char* name = (p.nD && !p.nL && !p.nW) ? "joiner_dh" : (p.nW && !p.nL && !p.nD) ? "joiner_dw" : "joiner_bwd";
+  RNNT_PROF(s, name);
+  // segment modes of the W reads: the recomputed logits read W rows in
   // segments of 16 / KV elements, dh reads them k-contiguous in KV (bf16 W
   // with V not a multiple of 8: from its zero-padded copy, in 16-byte segments)
-  const int wm_f = host_seg_mode(V, a.bf16 ? 2 : 4, a.bf16);
-  const int wm_h = a.wpad ? (int)kSegVector : host_seg_mode(V, a.bf16 ? 8 : 4, a.bf16);
-  for (int cm0 = 0; cm0 < mmax; cm0 += a.chunk_rows) {
-    const int cm1 = (cm0 + a.chunk_rows < mmax) ? cm0 + a.chunk_rows : mmax;
-    const int mt = (cm1 - cm0 + 127) / 128;
-    dim3 g1(mt, (V + 127) / 128), g2(mt, (J + 127) / 128), g3((J + 127) / 128, (V + 127) / 128, a.splits);
-    const dim3 gdl((cm1 - cm0 + kDlRows - 1) / kDlRows);
-    if (a.bf16) {
-      if (a.logits_in) {
-        RNNT_PROF(s, "joiner_dl");
-        hipLaunchKernelGGL(joiner_dl_kernel<true>, gdl, dim3(kDlThreads), 0, s, a, cm0, cm1);
-      } else {
-        e = launch_joiner_h(a, cm0, cm1, s);
-        if (e != hipSuccess) return e;
-        RNNT_PROF(s, "joiner_dlogits");
-        if (wm_f == kSegVector) hipLaunchKernelGGL((joiner_dlogits_kernel<true, kSegVector>), g1, dim3(kGemmThreads), 0, s, a, cm0, cm1);
-        else if (wm_f == kSegWords) hipLaunchKernelGGL((joiner_dlogits_kernel<true, kSegWords>), g1, dim3(kGemmThreads), 0, s, a, cm0, cm1);
-        else hipLaunchKernelGGL((joiner_dlogits_kernel<true, kSegElems>), g1, dim3(kGemmThreads), 0, s, a, cm0, cm1);
-      }
-      {
-        RNNT_PROF(s, "joiner_dh");
-        if (wm_h == kSegVector) hipLaunchKernelGGL((joiner_dh_kernel<true, kSegVector>), g2, dim3(kGemmThreads), 0, s, a, cm0, cm1);
-        else if (wm_h == kSegWords) hipLaunchKernelGGL((joiner_dh_kernel<true, kSegWords>), g2, dim3(kGemmThreads), 0, s, a, cm0, cm1);
-        else hipLaunchKernelGGL((joiner_dh_kernel<true, kSegElems>), g2, dim3(kGemmThreads), 0, s, a, cm0, cm1);
-      }
-      {
-        RNNT_PROF(s, "joiner_dlt");
-        const dim3 gt((cm1 - cm0 + 63) / 64, (a.ldl + 63) / 64);
-        hipLaunchKernelGGL(joiner_dlt_kernel, gt, dim3(256), 0, s, a, cm0, cm1);
-      }
-      {
-        RNNT_PROF(s, "joiner_dw");
-        hipLaunchKernelGGL(joiner_dw_kernel<true>, g3, dim3(kGemmThreads), 0, s, a, cm0, cm1, cm0 == 0);
-      }
-    } else {
-      if (a.logits_in) {
-        RNNT_PROF(s, "joiner_dl");
-        hipLaunchKernelGGL(joiner_dl_kernel<false>, gdl, dim3(kDlThreads), 0, s, a, cm0, cm1);
-      } else {
-        e = launch_joiner_h(a, cm0, cm1, s);
-        if (e != hipSuccess) return e;
-        RNNT_PROF(s, "joiner_dlogits");
-        if (wm_f == kSegVector) hipLaunchKernelGGL((joiner_dlogits_kernel<false, kSegVector>), g1, dim3(kGemmThreads), 0, s, a, cm0, cm1);
-        else hipLaunchKernelGGL((joiner_dlogits_kernel<false, kSegWords>), g1, dim3(kGemmThreads), 0, s, a, cm0, cm1);
-      }
-      {
-        RNNT_PROF(s, "joiner_dh");
-        if (wm_h == kSegVector) hipLaunchKernelGGL((joiner_dh_kernel<false, kSegVector>), g2, dim3(kGemmThreads), 0, s, a, cm0, cm1);
-        else hipLaunchKernelGGL((joiner_dh_kernel<false, kSegWords>), g2, dim3(kGemmThreads), 0, s, a, cm0, cm1);
-      }
-      {
-        RNNT_PROF(s, "joiner_dw");
-        hipLaunchKernelGGL(joiner_dw_kernel<false>, g3, dim3(kGemmThreads), 0, s, a, cm0, cm1, cm0 == 0);
-      }
-    }
-    // the chunk's d dec pieces; after the last chunk also d enc, dW and db
-    const bool last = cm1 >= mmax;
-    const size_t JV = (size_t)J * V;
-    const int R = (J / 4 >= kTailThreads) ? 1 : kTailThreads / (J / 4);
-    TailRanges tr;
-    tr.cm0 = cm0;
-    tr.cm1 = cm1;
-    tr.dec = (a.b.U + 1) * a.b.N;
-    tr.enc = last ? (a.b.N * a.b.T + R - 1) / R : 0;
-    const bool wvec = JV % kWsumVec == 0 && (reinterpret_cast<uintptr_t>(a.W_grad) & 15) == 0;
-    const size_t wthreads = wvec ? JV / kWsumVec : JV;
-    tr.wsum = (last && a.W_grad) ? (int)((wthreads + kTailThreads - 1) / kTailThreads) : 0;
-    tr.dbsum = (last && a.bias_grad) ? (V + kDbCols - 1) / kDbCols : 0;
-    {
-      RNNT_PROF(s, last ? "joiner_tail" : "joiner_dec");
-      hipLaunchKernelGGL(joiner_tail_kernel, dim3(tr.dec + tr.enc + tr.wsum + tr.dbsum), dim3(kTailThreads),
-                         (size_t)a.b.T * sizeof(int), s, a, tr);
-    }
+  const int wm_f = host_seg_mode(V, cur.bf16 ? 2 : 4, cur.bf16);
+  const int wm_h = cur.wpad ? (int)kSegVector : host_seg_mode(V, cur.bf16 ? 8 : 4, cur.bf16);
+  const dim3 g(blocks), t(kGemmThreads);
+  if (cur.bf16) {
+    if (wm_h != kSegVector) return hipErrorInvalidValue;  // bf16 dh always reads W in 16-byte segments
+    if (wm_f == kSegVector) hipLaunchKernelGGL((joiner_bwd_gemm_kernel<true, kSegVector, kSegVector>), g, t, 0, s, cur, nxt, p);
+    else if (wm_f == kSegWords) hipLaunchKernelGGL((joiner_bwd_gemm_kernel<true, kSegWords, kSegVector>), g, t, 0, s, cur, nxt, p);
+    else hipLaunchKernelGGL((joiner_bwd_gemm_kernel<true, kSegElems, kSegVector>), g, t, 0, s, cur, nxt, p);
+  } else {
+    if (wm_f != wm_h) return hipErrorInvalidValue;  // both follow V % 4
+    if (wm_f == kSegVector) hipLaunchKernelGGL((joiner_bwd_gemm_kernel<false, kSegVector, kSegVector>), g, t, 0, s, cur, nxt, p);
+    else hipLaunchKernelGGL((joiner_bwd_gemm_kernel<false, kSegWords, kSegWords>), g, t, 0, s, cur, nxt, p);
   }
   return hipGetLastError();
+}
+
+// Stored logits: per chunk, d(logits) streamed from them, then dh (which
+// also leaves h for dW), for bf16 the transpose of d(logits), dW, and the
+// chunk's d dec pass (one ring slot).
+static hipError_t launch_joiner_bwd_stored(const JoinerArgs& a, hipStream_t s) {
+  const int mmax = a.b.N * a.b.T * a.S;
+  hipError_t e = hipSuccess;
+  for (int cm0 = 0; cm0 < mmax && e == hipSuccess; cm0 += a.chunk_rows) {
+    const int cm1 = (cm0 + a.chunk_rows < mmax) ? cm0 + a.chunk_rows : mmax;
+    const dim3 gdl((cm1 - cm0 + kDlRows - 1) / kDlRows);
+    {
+      RNNT_PROF(s, "joiner_dl");
+      if (a.bf16) hipLaunchKernelGGL(joiner_dl_kernel<true>, gdl, dim3(kDlThreads), 0, s, a, cm0, cm1);
+      else hipLaunchKernelGGL(joiner_dl_kernel<false>, gdl, dim3(kDlThreads), 0, s, a, cm0, cm1);
+    }
+    e = hipGetLastError();
+    if (e == hipSuccess) e = launch_bwd_gemms(a, a, 0, 0, cm0, cm1, true, false, true, s);  // dh, leaves h
+    if (e == hipSuccess && a.bf16) {
+      RNNT_PROF(s, "joiner_dlt");
+      const dim3 gt((cm1 - cm0 + 63) / 64, (a.ldl + 63) / 64);
+      hipLaunchKernelGGL(joiner_dlt_kernel, gt, dim3(256), 0, s, a, cm0, cm1);
+      e = hipGetLastError();
+    }
+    if (e == hipSuccess) e = launch_bwd_gemms(a, a, 0, 0, cm0, cm1, false, true, false, s);  // dW
+    if (e == hipSuccess) e = launch_tail(a, tail_ranges(a, cm0, cm1, cm1 >= mmax), s, cm1 >= mmax ? "joiner_tail" : "joiner_dec");
+  }
+  return e;
+}
+
+hipError_t launch_joiner_bwd(const JoinerArgs& a, hipStream_t s) {
+  const int mmax = a.b.N * a.b.T * a.S;
+  const int C = a.chunk_rows;
+  hipError_t e = hipSuccess;
+  if (a.logits_grad) {
+    e = launch_fill_f32(a.logits_grad, (size_t)mmax * a.V, 0.f, s);
+    if (e != hipSuccess) return e;
+  }
+  if (a.logits_in) return launch_joiner_bwd_stored(a, s);
+  // Recomputed logits, software-pipelined over the chunks with two ring
+  // slots of chunk buffers (h, d(logits) and their transposes):
+  //   tail{H(0), H(1)}; gemm{L(0)};
+  //   for each chunk k: gemm{L(k+1), D(k), W(k)}; tail{dec(k), H(k+2)}
+  // (H: h pass, L: recomputed logits and d(logits), D: dh and the d enc /
+  // d dec pieces, W: dW, dec: the chunk's d dec pass; the last tail also sums
+  // d enc, dW and db). Every launch's reads were written by earlier launches
+  // on the stream, and a slot is rewritten only after its last reader.
+  const int nch = (mmax + C - 1) / C;
+  auto lo = [&](int k) { return k * C; };
+  auto hi = [&](int k) { return (k + 1) * C < mmax ? (k + 1) * C : mmax; };
+  {
+    TailRanges tr{};
+    tr.h0 = h_pass(ring_slot(a, 0), lo(0), hi(0));
+    if (nch > 1) tr.h1 = h_pass(ring_slot(a, 1), lo(1), hi(1));
+    e = launch_tail(a, tr, s, "joiner_h");
+  }
+  if (e == hipSuccess) e = launch_bwd_gemms(ring_slot(a, 0), ring_slot(a, 0), lo(0), hi(0), 0, 0, false, false, false, s);
+  for (int k = 0; k < nch && e == hipSuccess; ++k) {
+    const JoinerArgs cur = ring_slot(a, k), nxt = ring_slot(a, k + 1);
+    const bool more = k + 1 < nch;
+    e = launch_bwd_gemms(cur, nxt, more ? lo(k + 1) : 0, more ? hi(k + 1) : 0, lo(k), hi(k), true, true, false, s);
+    if (e != hipSuccess) break;
+    TailRanges tr = tail_ranges(cur, lo(k), hi(k), k == nch - 1);
+    if (k + 2 < nch) tr.h0 = h_pass(ring_slot(a, k + 2), lo(k + 2), hi(k + 2));
+    e = launch_tail(cur, tr, s, k == nch - 1 ? "joiner_tail" : "joiner_dec");
+  }
+  return e;
 }

@@ -146,7 +146,9 @@ struct JoinerArgs {
   float* dpre;         // ws chunk [chunk_rows, J]: the chunk's d dec pieces, each in the row of its first row
   float* enc_part;     // ws [ceil(N*T*S/128), 2, J]: d enc pieces of frames cut by a 128-row tile
   void* hbuf;          // ws chunk [chunk_rows, J] (f32 or bf16): h = tanh(enc + dec) of the chunk's rows
-                       // (forward and recomputed backward: written by the h kernel; backward: by dh)
+                       // (written by an h pass, or by dh when the logits were stored)
+  void* hT;            // ws chunk [J, chunk_rows] (bf16 only): h transposed, the dW operand
+  void* ring1[4];      // the second ring slot of the recomputed backward: hbuf, hT, dl, dlT
   float* dw_part;      // ws [splits, J, V]
   int splits;
   float* db_part;      // ws [n_db_rows, V]: column sums per row group of a chunk, summed over the chunks
@@ -168,7 +170,7 @@ int joiner_bwd_chunk_rows(int N, int T, int S, int J, int V, int bf16, int reque
 int joiner_bwd_chunk_max_rows(int J, int V);
 int joiner_fwd_chunk_rows(int N, int T, int S, int J, int bf16);
 bool joiner_fwd_uses_hbuf(int bf16);
-int joiner_bwd_splits(int J, int V);
+int joiner_bwd_splits(int J, int V, int chunk_rows);
 int joiner_db_rows(int chunk_rows);  // db partial rows of one chunk
 int joiner_nparts(int V);
 int joiner_ldl(int V);

