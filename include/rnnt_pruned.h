@@ -255,6 +255,25 @@ int rnnt_pruned_loss_ex(const rnnt_batch* batch, int32_t S, int32_t algorithm, i
                         float* loss, float* px_occ, float* py_occ,
                         void* workspace, size_t workspace_bytes, void* stream);
 
+/* rnnt_pruned_loss for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the same recursion (the library's choice of algorithm), with
+ * its workspace in a static device array of the library, RNNT_SCRATCH_BYTES
+ * per GPU, held from the first call on a GPU until the process ends. No
+ * allocation of any kind happens in the call. Arguments, outputs and error
+ * behaviour are those of rnnt_pruned_loss; a batch whose workspace would
+ * exceed the scratch is refused with RNNT_EUNSUPPORTED before any device
+ * call (rnnt_pruned_loss_workspace_size tells). The device that owns
+ * `stream` must be current. Every call on a GPU uses that GPU's one scratch:
+ * calls that overlap on one GPU (on different streams or host threads
+ * without ordering) race and give undefined results. Nothing in the scratch
+ * needs to start at zero: each call writes what it reads.
+ */
+#define RNNT_SCRATCH_BYTES (4u << 20)
+int rnnt_pruned_loss_noalloc(const rnnt_batch* batch, int32_t S, const float* px, const float* py,
+                             const int32_t* ranges, float* loss, float* px_occ, float* py_occ,
+                             void* stream);
+
 /* Workspace bytes for rnnt_pruned_joiner_backward. */
 size_t rnnt_pruned_joiner_backward_workspace_size(int32_t N, int32_t T, int32_t U, int32_t S,
                                                   int32_t J, int32_t V, int32_t dtype);

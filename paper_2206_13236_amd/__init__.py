@@ -24,7 +24,7 @@ __all__ = [
     "rnnt_pruned_loss", "rnnt_pruned_joiner_backward", "simple_loss_workspace_size",
     "pruned_joiner_workspace_size", "pruned_loss_workspace_size", "BAND_ALGORITHMS",
     "pruned_joiner_backward_workspace_size", "PrunedRnntLoss", "RNNT_F32", "RNNT_BF16",
-    "rnnt_combine_losses", "rnnt_validate_inputs", "RNNT_FLAGS",
+    "rnnt_combine_losses", "rnnt_validate_inputs", "RNNT_FLAGS", "rnnt_pruned_loss_noalloc",
 ]
 
 
@@ -231,6 +231,21 @@ def rnnt_pruned_loss(batch: Batch, S: int, px: torch.Tensor, py: torch.Tensor, r
         check(lib().rnnt_pruned_loss_ex(batch.c, S, BAND_ALGORITHMS[algorithm], chunk, _p(px), _p(py),
                                         _p(ranges), _p(loss), _p(px_occ), _p(py_occ), _p(ws), ws.numel(),
                                         _stream(stream)))
+    return {"loss": loss, "px_occ": px_occ, "py_occ": py_occ}
+
+
+def rnnt_pruned_loss_noalloc(batch: Batch, S: int, px: torch.Tensor, py: torch.Tensor, ranges: torch.Tensor,
+                             loss=None, px_occ=None, py_occ=None, stream=None) -> dict:
+    """rnnt_pruned_loss with its workspace in the library's static device
+    scratch (no allocation in the call; overlapping calls on one GPU race)."""
+    N, T = batch.N, batch.T
+    _need(px, "px", torch.float32, (N, T, S))
+    _need(py, "py", torch.float32, (N, T, S))
+    _need(ranges, "ranges", torch.int32, (N, T, S))
+    f32 = dict(dtype=torch.float32, device=batch.device)
+    loss = torch.empty(N, **f32) if loss is None else loss
+    check(lib().rnnt_pruned_loss_noalloc(batch.c, S, _p(px), _p(py), _p(ranges), _p(loss), _p(px_occ), _p(py_occ),
+                                         _stream(stream)))
     return {"loss": loss, "px_occ": px_occ, "py_occ": py_occ}
 
 

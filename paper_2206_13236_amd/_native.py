@@ -21,6 +21,8 @@ RNNT_EHIP = 4
 RNNT_F32 = 0
 RNNT_BF16 = 1
 
+RNNT_SCRATCH_BYTES = 4 << 20  # static device scratch of rnnt_pruned_loss_noalloc
+
 RNNT_REDUCE_SUM = 0
 RNNT_REDUCE_MEAN = 1
 
@@ -64,6 +66,8 @@ SIGNATURES = {
     "rnnt_pruned_loss_ex_workspace_size": (c_size_t, [c_int32] * 6),
     "rnnt_pruned_loss_ex": (c_int32, [POINTER(RnntBatch), c_int32, c_int32, c_int32, c_void_p, c_void_p,
                                       c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]),
+    "rnnt_pruned_loss_noalloc": (c_int32, [POINTER(RnntBatch), c_int32, c_void_p, c_void_p, c_void_p, c_void_p,
+                                           c_void_p, c_void_p, c_void_p]),
     "rnnt_pruned_joiner_backward_workspace_size": (c_size_t, [c_int32] * 7),
     "rnnt_pruned_joiner_backward": (c_int32, [POINTER(RnntBatch), c_int32, c_int32, c_int32, c_int32,
                                               c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,

@@ -5,6 +5,7 @@
 #include <stdarg.h>
 #include <stdio.h>
 
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -408,11 +409,52 @@ FullWs full_layout(void* base, int N, int T, int U, int J, int V, int bf16) {
   return w;
 }
 
+// Workspace of rnnt_pruned_loss_noalloc: a file-scope device array, one copy
+// per GPU for the life of the process. Host code never passes its name to a
+// kernel (in host code it is a stand-in, not a device address): each
+// device's address comes from hipGetSymbolAddress, taken once per device with
+// that device current and kept in g_scratch_ptr.
+constexpr size_t kScratchBytes = RNNT_SCRATCH_BYTES;
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+}  // namespace
+
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+namespace {
+
+// The scratch's address on the device that owns `stream` (which must be the
+// current device), resolved on the first call on that device.
+int scratch_for(hipStream_t stream, void** out) {
+  int cur = -1;
+  hipError_t e = hipGetDevice(&cur);
+  if (e != hipSuccess) return hip_status(e, "hipGetDevice");
+  if (stream) {
+    hipDevice_t sd = -1;
+    e = hipStreamGetDevice(stream, &sd);
+    if (e != hipSuccess) return hip_status(e, "hipStreamGetDevice");
+    if ((int)sd != cur) return fail(RNNT_EINVAL, "the stream's device (%d) must be the current device (%d)", (int)sd, cur);
+  }
+  if (cur < 0 || cur >= kMaxDevices) return fail(RNNT_EUNSUPPORTED, "device %d beyond %d devices", cur, kMaxDevices);
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[cur]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_status(e, "hipGetSymbolAddress(scratch)");
+    if (!p) return fail(RNNT_EHIP, "hipGetSymbolAddress(scratch) returned NULL");
+    g_scratch_ptr[cur] = p;
+  }
+  *out = g_scratch_ptr[cur];
+  return RNNT_OK;
+}
+
 }  // namespace
 
 extern "C" {
 
-int rnnt_abi_version(void) { return 6; }
+int rnnt_abi_version(void) { return 7; }
 
 const char* rnnt_last_error(void) { return g_err.c_str(); }
 
@@ -661,6 +703,29 @@ int rnnt_pruned_loss_ex(const rnnt_batch* batch, int32_t S, int32_t algorithm, i
   a.gy = py_occ;
   hipError_t e = launch_band(a, static_cast<hipStream_t>(stream));
   return hip_status(e, "rnnt_pruned_loss");
+}
+
+int rnnt_pruned_loss_noalloc(const rnnt_batch* batch, int32_t S, const float* px, const float* py,
+                             const int32_t* ranges, float* loss, float* px_occ, float* py_occ, void* stream) {
+  // host-side checks first, so that a refused call touches no device
+  int rc = check_batch(batch, false);
+  if (rc) return rc;
+  if (S < 1 || S > RNNT_MAX_S) return fail(RNNT_EUNSUPPORTED, "S = %d outside [1, %d]", S, RNNT_MAX_S);
+  if (!px || !py || !ranges || !loss) return fail(RNNT_EINVAL, "px, py, ranges and loss are required");
+  const size_t need = pruned_ws_bytes(batch->N, batch->T, batch->U, S, RNNT_BAND_AUTO, 0);
+  if (need == 0) return fail(RNNT_EUNSUPPORTED, "sizes outside what the pruned recursion supports");
+  if (need > kScratchBytes)
+    return fail(RNNT_EUNSUPPORTED,
+                "this batch needs %zu bytes of workspace, the static scratch holds %zu: call rnnt_pruned_loss "
+                "with a workspace",
+                need, kScratchBytes);
+  void* ws = nullptr;
+  rc = scratch_for(static_cast<hipStream_t>(stream), &ws);
+  if (rc) return rc;
+  // the kernels write every workspace element they read before reading it,
+  // so nothing in the scratch needs clearing between calls
+  return rnnt_pruned_loss_ex(batch, S, RNNT_BAND_AUTO, 0, px, py, ranges, loss, px_occ, py_occ, ws, kScratchBytes,
+                             stream);
 }
 
 size_t rnnt_pruned_joiner_backward_ex_workspace_size(int32_t N, int32_t T, int32_t U, int32_t S, int32_t J,

@@ -42,7 +42,7 @@ def test_library_exports_every_declared_symbol(L):
     missing = [n for n in _declared() if not hasattr(L, n)]
     assert not missing, f"not exported: {missing}"
     assert set(_declared()) == set(_native.SIGNATURES), "binding signatures out of sync with the header"
-    assert L.rnnt_abi_version() == 6
+    assert L.rnnt_abi_version() == 7
 
 
 def test_workspace_queries(L):
@@ -237,3 +237,25 @@ def test_combine_and_validate_statuses(L):
     b2.blank = 16
     assert L.rnnt_validate_inputs(ctypes.byref(b2), 16, 4, 0, 0, None, None, None, None, fake, None,
                                   None) == N.RNNT_EINVAL
+
+
+def test_noalloc_entry_refuses_batches_beyond_its_scratch(L):
+    # the allocation-free pruned recursion checks its workspace need against
+    # the static scratch on the host, before any device call
+    from paper_2206_13236_amd import _native as N
+    fake = ctypes.c_void_p(0x4000)
+    big = _batch(N=64, T=4096, U=0)
+    need = L.rnnt_pruned_loss_workspace_size(64, 4096, 0, 16)
+    assert need > N.RNNT_SCRATCH_BYTES
+    assert L.rnnt_pruned_loss_noalloc(ctypes.byref(big), 16, fake, fake, fake, fake, None, None,
+                                      None) == N.RNNT_EUNSUPPORTED
+    assert "static scratch" in _err(L) and str(need) in _err(L)
+    # argument checks as for rnnt_pruned_loss
+    b = _batch()
+    assert L.rnnt_pruned_loss_noalloc(ctypes.byref(b), 0, fake, fake, fake, fake, None, None,
+                                      None) == N.RNNT_EUNSUPPORTED
+    assert L.rnnt_pruned_loss_noalloc(ctypes.byref(b), 4, fake, fake, fake, None, None, None,
+                                      None) == N.RNNT_EINVAL
+    # the workloads' batches fit
+    for n, t, u, s_ in ((16, 248, 58, 5), (32, 495, 100, 5), (8, 970, 298, 10)):
+        assert 0 < L.rnnt_pruned_loss_workspace_size(n, t, u, s_) <= N.RNNT_SCRATCH_BYTES
