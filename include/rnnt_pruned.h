@@ -207,6 +207,20 @@ int rnnt_pruned_joiner(const rnnt_batch* batch, int32_t S, int32_t J, int32_t V,
                        const int32_t* ranges, float* px, float* py, float* lse, float* logits,
                        void* workspace, size_t workspace_bytes, void* stream);
 
+/* rnnt_pruned_joiner that also keeps the logits of the backward's first
+ * chunk of rows: head [head_rows, ldl] fp32 (ldl = V rounded up to a
+ * multiple of 8; caller-owned, 16-byte aligned, nullable) receives the
+ * logits of joiner rows 0 .. head_rows-1 in the library's own row order
+ * (an opaque cache: pass it unmodified to rnnt_pruned_joiner_backward_ex
+ * with the same head_rows). head_rows: a positive multiple of 128, normally
+ * rnnt_pruned_joiner_backward_chunk_rows(); ignored when head is NULL. At
+ * most 16,384 rows: a bounded buffer, not the [N, T, S, V] logits. */
+int rnnt_pruned_joiner_ex(const rnnt_batch* batch, int32_t S, int32_t J, int32_t V, int32_t dtype,
+                          const void* enc, const void* dec, const void* W, const void* bias,
+                          const int32_t* ranges, float* px, float* py, float* lse, float* logits,
+                          float* head, int32_t head_rows, void* workspace, size_t workspace_bytes,
+                          void* stream);
+
 /* Workspace bytes for rnnt_pruned_loss (the algorithm it picks). */
 size_t rnnt_pruned_loss_workspace_size(int32_t N, int32_t T, int32_t U, int32_t S);
 
@@ -309,16 +323,29 @@ size_t rnnt_pruned_joiner_backward_ex_workspace_size(int32_t N, int32_t T, int32
                                                      int32_t J, int32_t V, int32_t dtype,
                                                      int32_t chunk_rows);
 
-/* rnnt_pruned_joiner_backward with an explicit chunk size: chunk_rows rows
- * (a positive multiple of 128, at most what keeps each chunk buffer below
- * 2^31 bytes: RNNT_EUNSUPPORTED beyond), or 0 for the library's choice. The
- * results do not depend on the chunk size (the reductions keep their order
- * across chunks); a smaller chunk holds less memory and launches more
- * kernels. Everything else is as in rnnt_pruned_joiner_backward. */
+/* Rows of the backward's chunk for these sizes and chunk request (0 = the
+ * library's choice); 0 for an invalid request. */
+int32_t rnnt_pruned_joiner_backward_chunk_rows(int32_t N, int32_t T, int32_t S, int32_t J, int32_t V,
+                                               int32_t dtype, int32_t chunk_rows);
+
+/* rnnt_pruned_joiner_backward with an explicit chunk size and, optionally,
+ * the first chunk's logits kept by rnnt_pruned_joiner_ex.
+ * chunk_rows: rows of a chunk (a positive multiple of 128, at most what
+ *   keeps each chunk buffer below 2^31 bytes: RNNT_EUNSUPPORTED beyond), or 0
+ *   for the library's choice. The results do not depend on the chunk size
+ *   up to the summation order of dW and db; d enc and d dec are bitwise the
+ *   same. A smaller chunk holds less memory and launches more kernels.
+ * head, head_rows: the head written by rnnt_pruned_joiner_ex for the same
+ *   inputs (nullable); head_rows must equal
+ *   rnnt_pruned_joiner_backward_chunk_rows(..., chunk_rows) (RNNT_EINVAL
+ *   otherwise). The first chunk's d(logits) is then streamed from it instead
+ *   of recomputing its logits. Ignored when logits is given.
+ * Everything else is as in rnnt_pruned_joiner_backward. */
 int rnnt_pruned_joiner_backward_ex(const rnnt_batch* batch, int32_t S, int32_t J, int32_t V,
                                    int32_t dtype, int32_t chunk_rows, const void* enc,
                                    const void* dec, const void* W, const void* bias,
                                    const int32_t* ranges, const float* lse, const float* logits,
+                                   const float* head, int32_t head_rows,
                                    const float* px_occ, const float* py_occ, const float* scale,
                                    float* enc_grad, float* dec_grad, float* W_grad,
                                    float* bias_grad, float* logits_grad, void* workspace,

@@ -25,6 +25,7 @@ __all__ = [
     "pruned_joiner_workspace_size", "pruned_loss_workspace_size", "BAND_ALGORITHMS",
     "pruned_joiner_backward_workspace_size", "PrunedRnntLoss", "RNNT_F32", "RNNT_BF16",
     "rnnt_combine_losses", "rnnt_validate_inputs", "RNNT_FLAGS", "rnnt_pruned_loss_noalloc",
+    "backward_chunk_rows",
 ]
 
 
@@ -181,9 +182,17 @@ def rnnt_prune_ranges(batch: Batch, S: int, px_occ: torch.Tensor, py_occ: torch.
     return ranges
 
 
+def backward_chunk_rows(N, T, S, J, V, dtype, chunk_rows: int = 0) -> int:
+    """Rows of the joiner backward's chunk (the head's rows)."""
+    return int(lib().rnnt_pruned_joiner_backward_chunk_rows(N, T, S, J, V, dtype, chunk_rows))
+
+
 def rnnt_pruned_joiner(batch: Batch, S: int, enc: torch.Tensor, dec: torch.Tensor, W: torch.Tensor,
                        bias: Optional[torch.Tensor], ranges: torch.Tensor, px=None, py=None, lse=None,
-                       logits=None, workspace=None, stream=None, keep_logits: bool = False) -> dict:
+                       logits=None, workspace=None, stream=None, keep_logits: bool = False, head=None,
+                       head_rows: int = 0) -> dict:
+    """The pruned joiner; with ``head`` ([head_rows, ldl] fp32) it calls
+    rnnt_pruned_joiner_ex, which also keeps the first chunk's logits there."""
     N, T, U = batch.N, batch.T, batch.U
     J, V = int(W.shape[0]), int(W.shape[1])
     dt = _jdtype(W)
@@ -201,8 +210,14 @@ def rnnt_pruned_joiner(batch: Batch, S: int, enc: torch.Tensor, dec: torch.Tenso
     if logits is not None:
         _need(logits, "logits", torch.float32, (N, T, S, V))
     ws = _ws(pruned_joiner_workspace_size(N, T, S, J, V, dt), batch.device, workspace)
-    check(lib().rnnt_pruned_joiner(batch.c, S, J, V, dt, _p(enc), _p(dec), _p(W), _p(bias), _p(ranges),
-                                   _p(px), _p(py), _p(lse), _p(logits), _p(ws), ws.numel(), _stream(stream)))
+    if head is None:
+        check(lib().rnnt_pruned_joiner(batch.c, S, J, V, dt, _p(enc), _p(dec), _p(W), _p(bias), _p(ranges),
+                                       _p(px), _p(py), _p(lse), _p(logits), _p(ws), ws.numel(), _stream(stream)))
+    else:
+        _need(head, "head", torch.float32, (head_rows, (V + 7) // 8 * 8))
+        check(lib().rnnt_pruned_joiner_ex(batch.c, S, J, V, dt, _p(enc), _p(dec), _p(W), _p(bias), _p(ranges),
+                                          _p(px), _p(py), _p(lse), _p(logits), _p(head), int(head_rows), _p(ws),
+                                          ws.numel(), _stream(stream)))
     return {"px": px, "py": py, "lse": lse, "logits": logits}
 
 
@@ -252,9 +267,11 @@ def rnnt_pruned_loss_noalloc(batch: Batch, S: int, px: torch.Tensor, py: torch.T
 def rnnt_pruned_joiner_backward(batch: Batch, S: int, enc, dec, W, bias, ranges, lse, px_occ, py_occ,
                                 scale=None, enc_grad=None, dec_grad=None, W_grad=None, bias_grad=None,
                                 logits_grad=None, workspace=None, stream=None, want_param_grads=True,
-                                want_logits_grad=False, logits=None, chunk_rows: int = 0) -> dict:
-    """The joiner backward; chunk_rows != 0 (a multiple of 128) selects
-    rnnt_pruned_joiner_backward_ex with that chunk size."""
+                                want_logits_grad=False, logits=None, chunk_rows: int = 0, head=None,
+                                head_rows: int = 0) -> dict:
+    """The joiner backward; chunk_rows != 0 (a multiple of 128) or a head
+    (the first chunk's logits from rnnt_pruned_joiner with ``head``) selects
+    rnnt_pruned_joiner_backward_ex."""
     N, T, U = batch.N, batch.T, batch.U
     J, V = int(W.shape[0]), int(W.shape[1])
     dt = _jdtype(W)
@@ -276,10 +293,13 @@ def rnnt_pruned_joiner_backward(batch: Batch, S: int, enc, dec, W, bias, ranges,
     rest = (_p(enc), _p(dec), _p(W), _p(bias), _p(ranges), _p(lse), _p(logits), _p(px_occ), _p(py_occ), _p(scale),
             _p(enc_grad), _p(dec_grad), _p(W_grad), _p(bias_grad), _p(logits_grad), _p(ws), ws.numel(),
             _stream(stream))
-    if chunk_rows == 0:
+    if chunk_rows == 0 and head is None:
         check(lib().rnnt_pruned_joiner_backward(batch.c, S, J, V, dt, *rest))
     else:
-        check(lib().rnnt_pruned_joiner_backward_ex(batch.c, S, J, V, dt, int(chunk_rows), *rest))
+        if head is not None:
+            _need(head, "head", torch.float32, (head_rows, (V + 7) // 8 * 8))
+        check(lib().rnnt_pruned_joiner_backward_ex(batch.c, S, J, V, dt, int(chunk_rows), *rest[:7], _p(head),
+                                                   int(head_rows), *rest[7:]))
     return {"enc_grad": enc_grad, "dec_grad": dec_grad, "W_grad": W_grad, "bias_grad": bias_grad,
             "logits_grad": logits_grad}
 
@@ -386,7 +406,10 @@ class PrunedRnntLoss:
     ``keep_logits`` the pruned logits [N, T, S, V] are stored by the forward
     and streamed by the backward instead (one GEMM less, the logits' memory
     more). ``bwd_chunk_rows`` (a multiple of 128, 0 = the library's choice)
-    sets the backward's chunk.
+    sets the backward's chunk. With ``keep_head`` (default) the forward keeps
+    the logits of the backward's first chunk only (at most 16,384 rows, a
+    buffer whose size does not depend on N or T), so that the backward
+    streams that chunk instead of recomputing it.
 
     ``step`` also returns the training loss per utterance (``loss``) and its
     sum or mean (``total``), formed by the library (rnnt_combine_losses).
@@ -397,7 +420,7 @@ class PrunedRnntLoss:
 
     def __init__(self, S: int, simple_scale: float = 0.5, pruned_scale: float = 1.0,
                  keep_logits: bool = False, overlap: bool = True, lm_only_scale: float = 0.0,
-                 am_only_scale: float = 0.0, bwd_chunk_rows: int = 0):
+                 am_only_scale: float = 0.0, bwd_chunk_rows: int = 0, keep_head: bool = True):
         self.S = int(S)
         self.simple_scale = float(simple_scale)
         self.pruned_scale = float(pruned_scale)
@@ -406,6 +429,7 @@ class PrunedRnntLoss:
         self.keep_logits = bool(keep_logits)
         self.overlap = bool(overlap)
         self.bwd_chunk_rows = int(bwd_chunk_rows)
+        self.keep_head = bool(keep_head)
         self._cache = {}
         self._side = {}
 
@@ -483,8 +507,13 @@ class PrunedRnntLoss:
         ranges = rnnt_prune_ranges(batch, S, sim["px_occ"], sim["py_occ"], ranges=o("ranges", (N, T, S), torch.int32),
                                    stream=main)
         logits = o("logits", (N, T, S, V)) if self.keep_logits else None
+        head, head_rows = None, 0
+        if not self.keep_logits and self.keep_head:
+            head_rows = backward_chunk_rows(N, T, S, J, V, dt, self.bwd_chunk_rows)
+            head = self._buf("head", (head_rows, (V + 7) // 8 * 8), f32, dev)
         jo = rnnt_pruned_joiner(batch, S, enc, dec, W, bias, ranges, px=o("px", (N, T, S)), py=o("py", (N, T, S)),
-                                lse=o("lse", (N, T, S)), logits=logits, workspace=ws_p, stream=main)
+                                lse=o("lse", (N, T, S)), logits=logits, workspace=ws_p, stream=main, head=head,
+                                head_rows=head_rows)
         if self.overlap:
             side, fork, join = self._side_stream(dev)
             fork.record(main)
@@ -499,7 +528,7 @@ class PrunedRnntLoss:
         rnnt_pruned_joiner_backward(
             batch, S, enc, dec, W, bias, ranges, jo["lse"], pl["px_occ"], pl["py_occ"], scale=psc,
             enc_grad=enc_grad, dec_grad=dec_grad, W_grad=W_grad, bias_grad=bias_grad, workspace=ws_p,
-            stream=main, logits=logits, chunk_rows=self.bwd_chunk_rows)
+            stream=main, logits=logits, chunk_rows=self.bwd_chunk_rows, head=head, head_rows=head_rows)
         res.update(rnnt_combine_losses(sim["loss"], pl["loss"], self.simple_scale, self.pruned_scale, reduction,
                                        loss=o("loss", (N,)), total=o("total", ()), stream=main))
         if self.overlap:

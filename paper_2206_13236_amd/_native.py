@@ -77,9 +77,14 @@ SIGNATURES = {
     "rnnt_pruned_joiner_backward_ex_workspace_size": (c_size_t, [c_int32] * 8),
     "rnnt_pruned_joiner_backward_ex": (c_int32, [POINTER(RnntBatch), c_int32, c_int32, c_int32, c_int32, c_int32,
                                                  c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
+                                                 c_void_p, c_void_p, c_void_p, c_int32, c_void_p, c_void_p,
                                                  c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
-                                                 c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
-                                                 c_void_p, c_size_t, c_void_p]),
+                                                 c_void_p, c_void_p, c_size_t, c_void_p]),
+    "rnnt_pruned_joiner_backward_chunk_rows": (c_int32, [c_int32] * 7),
+    "rnnt_pruned_joiner_ex": (c_int32, [POINTER(RnntBatch), c_int32, c_int32, c_int32, c_int32,
+                                        c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
+                                        c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_int32,
+                                        c_void_p, c_size_t, c_void_p]),
     "rnnt_combine_losses": (c_int32, [c_int32, c_void_p, c_void_p, c_float, c_float, c_int32, c_void_p, c_void_p,
                                       c_void_p]),
     "rnnt_validate_inputs": (c_int32, [POINTER(RnntBatch), c_int32, c_int32, c_int32, c_int32, c_void_p, c_void_p,

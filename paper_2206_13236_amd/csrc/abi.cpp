@@ -320,6 +320,7 @@ JoinerArgs joiner_args(const rnnt_batch* batch, int S, int J, int V, int dtype, 
 }
 
 void set_joiner_fwd(JoinerArgs& a, const JoinerFwdWs& w, float* px, float* py, float* lse, float* logits) {
+  a.ldl = joiner_ldl(a.V);
   a.frame_off = w.frame_off;
   a.rowinfo = w.rowinfo;
   a.part = w.part;
@@ -454,7 +455,7 @@ int scratch_for(hipStream_t stream, void** out) {
 
 extern "C" {
 
-int rnnt_abi_version(void) { return 7; }
+int rnnt_abi_version(void) { return 8; }
 
 const char* rnnt_last_error(void) { return g_err.c_str(); }
 
@@ -543,26 +544,38 @@ size_t rnnt_pruned_joiner_workspace_size(int32_t N, int32_t T, int32_t S, int32_
   return joiner_fwd_layout(nullptr, N, T, S, J, V, dtype == RNNT_BF16).bytes;
 }
 
-int rnnt_pruned_joiner(const rnnt_batch* batch, int32_t S, int32_t J, int32_t V, int32_t dtype, const void* enc,
-                       const void* dec, const void* W, const void* bias, const int32_t* ranges, float* px, float* py,
-                       float* lse, float* logits, void* workspace, size_t workspace_bytes, void* stream) {
+int rnnt_pruned_joiner_ex(const rnnt_batch* batch, int32_t S, int32_t J, int32_t V, int32_t dtype, const void* enc,
+                          const void* dec, const void* W, const void* bias, const int32_t* ranges, float* px,
+                          float* py, float* lse, float* logits, float* head, int32_t head_rows, void* workspace,
+                          size_t workspace_bytes, void* stream) {
   int rc = check_batch(batch, true);
   if (rc) return rc;
   rc = check_joiner_sizes(batch, S, J, V, dtype);
   if (rc) return rc;
   if (!enc || !dec || !W || !ranges) return fail(RNNT_EINVAL, "enc, dec, W and ranges are required");
   if (!px || !py || !lse) return fail(RNNT_EINVAL, "px, py and lse are required");
-  if (!aligned16(logits)) return fail(RNNT_EINVAL, "logits must be 16-byte aligned");
+  if (!aligned16(logits) || !aligned16(head)) return fail(RNNT_EINVAL, "logits and head must be 16-byte aligned");
+  if (head && (head_rows < 128 || head_rows % 128 != 0 || head_rows > joiner_bwd_chunk_max_rows(J, V)))
+    return fail(RNNT_EINVAL, "head_rows = %d must be a positive multiple of 128 within the chunk limit", head_rows);
   const int bf = dtype == RNNT_BF16;
   rc = check_ws(workspace, workspace_bytes, joiner_fwd_layout(nullptr, batch->N, batch->T, S, J, V, bf).bytes);
   if (rc) return rc;
   const JoinerFwdWs w = joiner_fwd_layout(workspace, batch->N, batch->T, S, J, V, bf);
   JoinerArgs a = joiner_args(batch, S, J, V, dtype, enc, dec, W, bias, ranges);
   set_joiner_fwd(a, w, px, py, lse, logits);
+  a.head = head;
+  a.head_rows = head ? head_rows : 0;
   hipStream_t s = static_cast<hipStream_t>(stream);
   hipError_t e = launch_joiner_prep(a, s);
   if (e == hipSuccess) e = launch_joiner_fwd(a, s);
   return hip_status(e, "rnnt_pruned_joiner");
+}
+
+int rnnt_pruned_joiner(const rnnt_batch* batch, int32_t S, int32_t J, int32_t V, int32_t dtype, const void* enc,
+                       const void* dec, const void* W, const void* bias, const int32_t* ranges, float* px, float* py,
+                       float* lse, float* logits, void* workspace, size_t workspace_bytes, void* stream) {
+  return rnnt_pruned_joiner_ex(batch, S, J, V, dtype, enc, dec, W, bias, ranges, px, py, lse, logits, nullptr, 0,
+                               workspace, workspace_bytes, stream);
 }
 
 // Workspace of rnnt_pruned_loss: the band in a diagonal-major layout of
@@ -741,12 +754,20 @@ size_t rnnt_pruned_joiner_backward_workspace_size(int32_t N, int32_t T, int32_t 
   return rnnt_pruned_joiner_backward_ex_workspace_size(N, T, U, S, J, V, dtype, 0);
 }
 
+int32_t rnnt_pruned_joiner_backward_chunk_rows(int32_t N, int32_t T, int32_t S, int32_t J, int32_t V, int32_t dtype,
+                                               int32_t chunk_rows) {
+  if (N < 1 || T < 1 || S < 1 || J < 1 || V < 1 || chunk_rows < 0 || chunk_rows % 128 != 0) return 0;
+  if (chunk_rows > joiner_bwd_chunk_max_rows(J, V) || joiner_bwd_chunk_max_rows(J, V) < 128) return 0;
+  return joiner_bwd_chunk_rows(N, T, S, J, V, dtype == RNNT_BF16, chunk_rows);
+}
+
 int rnnt_pruned_joiner_backward_ex(const rnnt_batch* batch, int32_t S, int32_t J, int32_t V, int32_t dtype,
                                    int32_t chunk_rows, const void* enc, const void* dec, const void* W,
                                    const void* bias, const int32_t* ranges, const float* lse, const float* logits,
-                                   const float* px_occ, const float* py_occ, const float* scale, float* enc_grad,
-                                   float* dec_grad, float* W_grad, float* bias_grad, float* logits_grad,
-                                   void* workspace, size_t workspace_bytes, void* stream) {
+                                   const float* head, int32_t head_rows, const float* px_occ,
+                                   const float* py_occ, const float* scale, float* enc_grad, float* dec_grad,
+                                   float* W_grad, float* bias_grad, float* logits_grad, void* workspace,
+                                   size_t workspace_bytes, void* stream) {
   int rc = check_batch(batch, true);
   if (rc) return rc;
   rc = check_joiner_sizes(batch, S, J, V, dtype);
@@ -761,12 +782,20 @@ int rnnt_pruned_joiner_backward_ex(const rnnt_batch* batch, int32_t S, int32_t J
   if (logits_grad && (long long)batch->N * batch->T * S * (long long)V > (1ll << 40))
     return fail(RNNT_EUNSUPPORTED, "logits_grad is a debugging aid for small shapes");
   const int bf = dtype == RNNT_BF16;
+  if (head) {
+    if (!aligned16(head)) return fail(RNNT_EINVAL, "head must be 16-byte aligned");
+    const int C = joiner_bwd_chunk_rows(batch->N, batch->T, S, J, V, bf, chunk_rows);
+    if (head_rows != C)
+      return fail(RNNT_EINVAL, "head_rows = %d must equal the backward's chunk of %d rows", head_rows, C);
+  }
   rc = check_ws(workspace, workspace_bytes,
                 joiner_bwd_layout(nullptr, batch->N, batch->T, S, J, V, bf, chunk_rows).bytes);
   if (rc) return rc;
   const JoinerBwdWs w = joiner_bwd_layout(workspace, batch->N, batch->T, S, J, V, bf, chunk_rows);
   JoinerArgs a = joiner_args(batch, S, J, V, dtype, enc, dec, W, bias, ranges);
   set_joiner_bwd(a, w, lse, logits, px_occ, py_occ, scale, enc_grad, dec_grad, W_grad, bias_grad, logits_grad);
+  a.head = logits ? nullptr : const_cast<float*>(head);  // with all logits stored the head is not needed
+  a.head_rows = a.head ? head_rows : 0;
   hipStream_t s = static_cast<hipStream_t>(stream);
   hipError_t e = launch_joiner_prep(a, s);
   if (e == hipSuccess) e = launch_joiner_bwd(a, s);
@@ -779,9 +808,9 @@ int rnnt_pruned_joiner_backward(const rnnt_batch* batch, int32_t S, int32_t J, i
                                 const float* px_occ, const float* py_occ,
                                 const float* scale, float* enc_grad, float* dec_grad, float* W_grad, float* bias_grad,
                                 float* logits_grad, void* workspace, size_t workspace_bytes, void* stream) {
-  return rnnt_pruned_joiner_backward_ex(batch, S, J, V, dtype, 0, enc, dec, W, bias, ranges, lse, logits, px_occ,
-                                        py_occ, scale, enc_grad, dec_grad, W_grad, bias_grad, logits_grad, workspace,
-                                        workspace_bytes, stream);
+  return rnnt_pruned_joiner_backward_ex(batch, S, J, V, dtype, 0, enc, dec, W, bias, ranges, lse, logits, nullptr, 0,
+                                        px_occ, py_occ, scale, enc_grad, dec_grad, W_grad, bias_grad, logits_grad,
+                                        workspace, workspace_bytes, stream);
 }
 
 int rnnt_validate_inputs(const rnnt_batch* batch, int32_t V, int32_t S, int32_t J, int32_t dtype, const float* am,

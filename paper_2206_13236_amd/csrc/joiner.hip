@@ -518,6 +518,7 @@ __global__ __launch_bounds__(kGemmThreads, 4) void joiner_fwd_kernel(JoinerArgs 
             if (col == info.z) a.tgt[m] = lg[j];
             if (col == a.b.blank) a.blk[m] = lg[j];
             if (a.logits) a.logits[(size_t)info.w * V + col] = lg[j];
+            if (m < a.head_rows) a.head[(size_t)m * a.ldl + col] = lg[j];
           }
         }
       }
@@ -697,10 +698,11 @@ DEV void dlogits_tile(const JoinerArgs& a, int cm0, int cm1, int v, int nblocks,
 
 // ---------------------------------------------------------------------------
 // Backward 1, stored logits: the same d(logits) streamed from the logits the
-// forward kept. One block per kDlRows rows of the chunk, threads over groups
-// of 4 columns (padding columns up to ldl get zeros), several rows per thread
-// with their loads issued together; the block's column sums are one db_part
-// row.
+// forward kept, either all of them ([N, T, S, V], logits_in) or those of the
+// first chunk (head, rows in joiner-row order, for chunk 0 only). One block
+// per kDlRows rows of the chunk, threads over groups of 4 columns (padding
+// columns up to ldl get zeros), several rows per thread with their loads
+// issued together; the block's column sums are one db_part row.
 // ---------------------------------------------------------------------------
 constexpr int kDlRows = 32;
 constexpr int kDlThreads = 256;
@@ -729,12 +731,13 @@ __global__ __launch_bounds__(kDlThreads) void joiner_dl_kernel(JoinerArgs a, int
     rx[r] = x;
   }
   __syncthreads();
-  const float* __restrict__ lg = a.logits_in;
+  const bool from_head = a.logits_in == nullptr;  // chunk 0 from the head rows
+  const float* __restrict__ lg = from_head ? a.head : a.logits_in;
   typename In<BF>::Cfg::T* __restrict__ dl = reinterpret_cast<typename In<BF>::Cfg::T*>(a.dl);
   const int ng = ldl / 4;
   const int tpr = ng <= 64 ? 64 : (ng <= 128 ? 128 : (ng <= 256 ? 256 : kDlThreads));
   const int nrg = kDlThreads / tpr, rg = threadIdx.x / tpr, ct = threadIdx.x - rg * tpr;
-  const bool vec = (V & 3) == 0;
+  const bool vec = from_head || (V & 3) == 0;
   for (int g0 = 0; g0 < ng; g0 += tpr) {
     const int c = 4 * (g0 + ct);
     const bool gok = g0 + ct < ng;
@@ -747,7 +750,7 @@ __global__ __launch_bounds__(kDlThreads) void joiner_dl_kernel(JoinerArgs a, int
           const int r = r0 + k * nrg;
           const int4 info = ri[min(r, kDlRows - 1)];
           const bool ok = r < nrows && info.w >= 0 && c < V;
-          const float* src = lg + (ok ? (size_t)info.w * V + c : 0);
+          const float* src = lg + (ok ? (from_head ? (size_t)(m0 + r) * ldl : (size_t)info.w * V) + c : 0);
           if (ok && vec) {
             const float4 q = *reinterpret_cast<const float4*>(src);
             l[k][0] = q.x; l[k][1] = q.y; l[k][2] = q.z; l[k][3] = q.w;
@@ -1207,7 +1210,11 @@ DEV void tail_dbsum(const JoinerArgs& a, int b, float (*red)[kDbCols]) {
   constexpr int kParts = kTailThreads / kDbCols;
   const int v = b * kDbCols + c;
   const int M = min(a.frame_off[a.b.N] * a.S, a.chunk_rows);  // rows of the first (largest) chunk
-  const int rows = a.logits_in ? (M + kDlRows - 1) / kDlRows : CfgF::WGM * ((M + CfgF::BM - 1) / CfgF::BM);
+  // the rows the first chunk wrote: one per 32 rows streamed (stored logits
+  // or the head), one per wave row of each recomputed tile (the same 32-row
+  // groups, whole tiles); a later chunk only adds to a prefix of them
+  const bool streamed = a.logits_in || (a.head && a.head_rows == a.chunk_rows);
+  const int rows = streamed ? (M + kDlRows - 1) / kDlRows : CfgF::WGM * ((M + CfgF::BM - 1) / CfgF::BM);
   const int q = (rows + kParts - 1) / kParts, r0 = min(rows, part * q), r1 = min(rows, r0 + q);
   float s = 0.f;
   if (v < a.V) {
@@ -1736,7 +1743,7 @@ hipError_t launch_joiner_bwd(const JoinerArgs& a, hipStream_t s) {
   if (a.logits_in) return launch_joiner_bwd_stored(a, s);
   // Recomputed logits, software-pipelined over the chunks with two ring
   // slots of chunk buffers (h, d(logits) and their transposes):
-  //   tail{H(0), H(1)}; gemm{L(0)};
+  //   tail{H(0), H(1)}; gemm{L(0)} (or chunk 0 streamed from the head);
   //   for each chunk k: gemm{L(k+1), D(k), W(k)}; tail{dec(k), H(k+2)}
   // (H: h pass, L: recomputed logits and d(logits), D: dh and the d enc /
   // d dec pieces, W: dW, dec: the chunk's d dec pass; the last tail also sums
@@ -1751,7 +1758,26 @@ hipError_t launch_joiner_bwd(const JoinerArgs& a, hipStream_t s) {
     if (nch > 1) tr.h1 = h_pass(ring_slot(a, 1), lo(1), hi(1));
     e = launch_tail(a, tr, s, "joiner_h");
   }
-  if (e == hipSuccess) e = launch_bwd_gemms(ring_slot(a, 0), ring_slot(a, 0), lo(0), hi(0), 0, 0, false, false, false, s);
+  if (e == hipSuccess && a.head && a.head_rows == C) {
+    // chunk 0's logits were kept by the forward: stream them (and, for bf16,
+    // transpose d(logits) for dW) instead of the one recomputation launch
+    // the pipeline cannot fill
+    const dim3 gdl((hi(0) - lo(0) + kDlRows - 1) / kDlRows);
+    {
+      RNNT_PROF(s, "joiner_dl");
+      if (a.bf16) hipLaunchKernelGGL(joiner_dl_kernel<true>, gdl, dim3(kDlThreads), 0, s, a, lo(0), hi(0));
+      else hipLaunchKernelGGL(joiner_dl_kernel<false>, gdl, dim3(kDlThreads), 0, s, a, lo(0), hi(0));
+    }
+    e = hipGetLastError();
+    if (e == hipSuccess && a.bf16) {
+      RNNT_PROF(s, "joiner_dlt");
+      const dim3 gt((hi(0) - lo(0) + 63) / 64, (a.ldl + 63) / 64);
+      hipLaunchKernelGGL(joiner_dlt_kernel, gt, dim3(256), 0, s, a, lo(0), hi(0));
+      e = hipGetLastError();
+    }
+  } else if (e == hipSuccess) {
+    e = launch_bwd_gemms(ring_slot(a, 0), ring_slot(a, 0), lo(0), hi(0), 0, 0, false, false, false, s);
+  }
   for (int k = 0; k < nch && e == hipSuccess; ++k) {
     const JoinerArgs cur = ring_slot(a, k), nxt = ring_slot(a, k + 1);
     const bool more = k + 1 < nch;

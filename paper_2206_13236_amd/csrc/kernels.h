@@ -131,6 +131,8 @@ struct JoinerArgs {
   float* py;
   float* lse;
   float* logits;       // [N, T, S, V] or null: the forward also stores the logits
+  float* head;         // [head_rows, ldl] or null: the logits of the first head_rows rows (the backward's
+  int head_rows;       //   first chunk), stored by the forward and streamed by the backward
   // backward
   const float* lse_in;
   const float* logits_in;  // [N, T, S, V] or null: stored logits (else recomputed)

@@ -42,7 +42,7 @@ def test_library_exports_every_declared_symbol(L):
     missing = [n for n in _declared() if not hasattr(L, n)]
     assert not missing, f"not exported: {missing}"
     assert set(_declared()) == set(_native.SIGNATURES), "binding signatures out of sync with the header"
-    assert L.rnnt_abi_version() == 7
+    assert L.rnnt_abi_version() == 8
 
 
 def test_workspace_queries(L):
@@ -195,8 +195,8 @@ def test_sizes_beyond_32_bit_buffer_offsets_are_refused(L):
     assert L.rnnt_full_loss(pb, 8, V, N.RNNT_F32, fake, fake, fake, None, None, fake, fake, fake, None, None,
                             None, fake, 1 << 40, None) == N.RNNT_EUNSUPPORTED
     # V = 500, J = 512: at most (2^31 - 1) / (512 * 4) rows, rounded down to 1,024
-    args = (fake, fake, fake, None, fake, fake, None, fake, fake, None, fake, fake, None, None, None, fake, 1 << 40,
-            None)
+    args = (fake, fake, fake, None, fake, fake, None, None, 0, fake, fake, None, fake, fake, None, None, None, fake,
+            1 << 40, None)
     assert L.rnnt_pruned_joiner_backward_ex(pb, 2, 512, 500, N.RNNT_F32, 1 << 20, *args) == N.RNNT_EUNSUPPORTED
     assert L.rnnt_pruned_joiner_backward_ex(pb, 2, 512, 500, N.RNNT_F32, 100, *args) == N.RNNT_EINVAL
     # the unpruned loss at the largest workload's shape (8 x 1000 x 301 rows of
@@ -259,3 +259,22 @@ def test_noalloc_entry_refuses_batches_beyond_its_scratch(L):
     # the workloads' batches fit
     for n, t, u, s_ in ((16, 248, 58, 5), (32, 495, 100, 5), (8, 970, 298, 10)):
         assert 0 < L.rnnt_pruned_loss_workspace_size(n, t, u, s_) <= N.RNNT_SCRATCH_BYTES
+
+
+def test_head_rows_must_match_the_backward_chunk(L):
+    # the first chunk's logits kept by the forward are accepted by the
+    # backward only with the row count of its own first chunk
+    from paper_2206_13236_amd import _native as N
+    b = _batch(N=16, T=248, U=58)
+    pb = ctypes.byref(b)
+    fake = ctypes.c_void_p(0x4000)
+    C = L.rnnt_pruned_joiner_backward_chunk_rows(16, 248, 5, 512, 500, N.RNNT_F32, 0)
+    assert C % 128 == 0 and 8192 <= C <= 16384
+    assert L.rnnt_pruned_joiner_backward_chunk_rows(16, 248, 5, 512, 500, N.RNNT_F32, 1024) == 1024
+    assert L.rnnt_pruned_joiner_backward_chunk_rows(16, 248, 5, 512, 500, N.RNNT_F32, 100) == 0
+    args = lambda head_rows: (fake, fake, fake, None, fake, fake, None, fake, head_rows, fake, fake, None, fake,
+                              fake, None, None, None, fake, 1 << 40, None)
+    assert L.rnnt_pruned_joiner_backward_ex(pb, 5, 512, 500, N.RNNT_F32, 0, *args(C + 128)) == N.RNNT_EINVAL
+    assert "head_rows" in _err(L)
+    assert L.rnnt_pruned_joiner_ex(pb, 5, 512, 500, N.RNNT_F32, fake, fake, fake, None, fake, fake, fake, fake,
+                                   None, fake, 100, fake, 1 << 40, None) == N.RNNT_EINVAL

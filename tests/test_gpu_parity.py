@@ -181,11 +181,11 @@ def test_pruned_loss(name, alg, chunk):
     assert_close("py_occ", host(out["py_occ"]), gy_ref, atol=1e-4)
 
 
-def _joiner_backward(name, stored, chunk_rows=0):
+def _joiner_backward(name, stored, chunk_rows=0, head=False):
     o = _oracle(name)
     b = o["b"]
     bf = b.wl.joiner_dtype == "bf16"
-    say(f"[joiner-bwd] {name} bf16={bf} stored_logits={stored} chunk_rows={chunk_rows}")
+    say(f"[joiner-bwd] {name} bf16={bf} stored_logits={stored} chunk_rows={chunk_rows} head={head}")
     st = o["st"]
     lse32 = st["lse"].astype(np.float32)
     gx32, gy32 = st["gx"].astype(np.float32), st["gy"].astype(np.float32)
@@ -196,13 +196,20 @@ def _joiner_backward(name, stored, chunk_rows=0):
     args = (dev_joiner(b.enc, bf), dev_joiner(b.dec, bf), dev_joiner(b.W, bf), dev_joiner(b.bias, bf))
     rng = dev_i32(o["ranges"])
     logits, lse = None, dev_f32(lse32)
+    hd, C = None, 0
     if stored:
         # the backward streams the logits the forward kept, with the forward's own lse
         fw = P.rnnt_pruned_joiner(batch, o["S"], *args, rng, keep_logits=True)
         logits, lse = fw["logits"], fw["lse"]
+    elif head:
+        # the forward keeps the logits of the backward's first chunk only
+        C = P.backward_chunk_rows(b.N, b.T, o["S"], b.wl.J, b.V, P._jdtype(args[2]), chunk_rows)
+        hd = torch.empty(C, (b.V + 7) // 8 * 8, dtype=torch.float32, device=DEV)
+        fw = P.rnnt_pruned_joiner(batch, o["S"], *args, rng, head=hd, head_rows=C)
+        lse = fw["lse"]
     out = P.rnnt_pruned_joiner_backward(
         batch, o["S"], *args, rng, lse, dev_f32(gx32), dev_f32(gy32), scale=dev_f32(o["sc"]),
-        want_logits_grad=(name == "tiny"), logits=logits, chunk_rows=chunk_rows)
+        want_logits_grad=(name == "tiny"), logits=logits, chunk_rows=chunk_rows, head=hd, head_rows=C)
     torch.cuda.synchronize()
     for k in ("enc_grad", "dec_grad"):
         assert_close(k, host(out[k]), ref[k], atol=grad_atol(ref[k], bf))
@@ -222,6 +229,36 @@ def test_pruned_joiner_backward(name, stored):
 # chunks of rows that S does not divide (frames straddle chunk edges), three
 # or more chunks per batch
 CHUNKED = [("small_f32", 128), ("small_f32", 384), ("small_bf16", 128), ("small_bf16_oddv", 256), ("bpe_sub", 1024)]
+
+
+@pytest.mark.parametrize("name,chunk", [("tiny", 0), ("small_f32", 128), ("small_bf16", 256),
+                                        ("small_bf16_oddv", 128), ("bpe_sub", 0), ("long_sub", 1024)])
+def test_pruned_joiner_backward_with_head(name, chunk):
+    # the forward keeps the first chunk's logits, the backward streams that
+    # chunk and recomputes the others; d enc and d dec are bitwise those of
+    # the backward that recomputes every chunk
+    _joiner_backward(name, False, chunk_rows=chunk, head=True)  # against the oracle
+    # the same forward's lse for both backward calls, with and without the head
+    o = _oracle(name)
+    b = o["b"]
+    bf = b.wl.joiner_dtype == "bf16"
+    batch = make_dev_batch(b)
+    args = (dev_joiner(b.enc, bf), dev_joiner(b.dec, bf), dev_joiner(b.W, bf), dev_joiner(b.bias, bf))
+    rng = dev_i32(o["ranges"])
+    C = P.backward_chunk_rows(b.N, b.T, o["S"], b.wl.J, b.V, P._jdtype(args[2]), chunk)
+    hd = torch.empty(C, (b.V + 7) // 8 * 8, dtype=torch.float32, device=DEV)
+    fw = P.rnnt_pruned_joiner(batch, o["S"], *args, rng, head=hd, head_rows=C)
+    gx, gy = dev_f32(o["st"]["gx"].astype(np.float32)), dev_f32(o["st"]["gy"].astype(np.float32))
+    with_head = P.rnnt_pruned_joiner_backward(batch, o["S"], *args, rng, fw["lse"], gx, gy, scale=dev_f32(o["sc"]),
+                                              chunk_rows=chunk, head=hd, head_rows=C)
+    without = P.rnnt_pruned_joiner_backward(batch, o["S"], *args, rng, fw["lse"], gx, gy, scale=dev_f32(o["sc"]),
+                                            chunk_rows=chunk)
+    torch.cuda.synchronize()
+    for k in ("enc_grad", "dec_grad"):
+        assert torch.equal(with_head[k], without[k]), f"{k} differs with the head"
+    for k in ("W_grad", "bias_grad"):
+        ref = host(without[k])
+        assert_close(k, host(with_head[k]), ref, atol=1e-6 * max(1.0, np.abs(ref).max()))
 
 
 @pytest.mark.parametrize("stored", [False, True], ids=["recompute", "stored_logits"])
