@@ -1540,11 +1540,11 @@ int joiner_fwd_chunk_rows(int N, int T, int S, int J, int bf16) {
 
 bool joiner_fwd_uses_hbuf(int bf16) { return bf16 ? kFwdHbuf<true> : kFwdHbuf<false>; }
 
-// dW splits a chunk's rows into ranges of about 2 max(J, V) rows, so that a
-// dW tile does about twice the work of a dh or recomputed-logits tile of the
-// same launch (their K is V or J): long enough K loops, few partials.
+// dW splits a chunk's rows into ranges of about max(J, V) rows, so that a dW
+// tile does about the work of a dh or recomputed-logits tile of the same
+// launch (their K is V or J): no block kind outlasts the others.
 int joiner_bwd_splits(int J, int V, int chunk_rows) {
-  const int target = 2 * (J > V ? J : V);
+  const int target = J > V ? J : V;
   int s = (chunk_rows + target / 2) / target;
   if (s < 1) s = 1;
   if (s > 32) s = 32;
