@@ -404,8 +404,8 @@ class PrunedRnntLoss:
     By default no [N, T, S, V] array is kept: the backward recomputes the
     logits in chunks of rows whose size does not depend on N or T. With
     ``keep_logits`` the pruned logits [N, T, S, V] are stored by the forward
-    and streamed by the backward instead (one GEMM less, the logits' memory
-    more). ``bwd_chunk_rows`` (a multiple of 128, 0 = the library's choice)
+    and streamed by the backward instead, in one chunk of all rows (one GEMM
+    less, the logits' memory more). ``bwd_chunk_rows`` (a multiple of 128, 0 = the library's choice)
     sets the backward's chunk. With ``keep_head`` (default) the forward keeps
     the logits of the backward's first chunk only (at most 16,384 rows, a
     buffer whose size does not depend on N or T), so that the backward
@@ -463,11 +463,16 @@ class PrunedRnntLoss:
             t = out.get(key)
             return t if t is not None else self._buf(key, shape, dtype, dev)
 
+        chunk = self.bwd_chunk_rows
+        if self.keep_logits and chunk == 0:
+            # the caller keeps all the logits anyway: one chunk of every row
+            # (fewer, fuller launches) unless that breaks the 32-bit limit
+            whole = (N * T * S + 127) // 128 * 128
+            chunk = whole if backward_chunk_rows(N, T, S, J, V, dt, whole) else 0
         ws_s = self._buf("ws_simple", (simple_loss_workspace_size(N, T, U, V),), torch.uint8, dev)
         ws_p = self._buf("ws_pruned", (max(pruned_joiner_workspace_size(N, T, S, J, V, dt),
                                            pruned_loss_workspace_size(N, T, U, S),
-                                           pruned_joiner_backward_workspace_size(N, T, U, S, J, V, dt,
-                                                                                 self.bwd_chunk_rows)),),
+                                           pruned_joiner_backward_workspace_size(N, T, U, S, J, V, dt, chunk)),),
                          torch.uint8, dev)
         ssc = self._buf("ssc", (N,), f32, dev)
         psc = self._buf("psc", (N,), f32, dev)
@@ -509,7 +514,7 @@ class PrunedRnntLoss:
         logits = o("logits", (N, T, S, V)) if self.keep_logits else None
         head, head_rows = None, 0
         if not self.keep_logits and self.keep_head:
-            head_rows = backward_chunk_rows(N, T, S, J, V, dt, self.bwd_chunk_rows)
+            head_rows = backward_chunk_rows(N, T, S, J, V, dt, chunk)
             head = self._buf("head", (head_rows, (V + 7) // 8 * 8), f32, dev)
         jo = rnnt_pruned_joiner(batch, S, enc, dec, W, bias, ranges, px=o("px", (N, T, S)), py=o("py", (N, T, S)),
                                 lse=o("lse", (N, T, S)), logits=logits, workspace=ws_p, stream=main, head=head,
@@ -528,7 +533,7 @@ class PrunedRnntLoss:
         rnnt_pruned_joiner_backward(
             batch, S, enc, dec, W, bias, ranges, jo["lse"], pl["px_occ"], pl["py_occ"], scale=psc,
             enc_grad=enc_grad, dec_grad=dec_grad, W_grad=W_grad, bias_grad=bias_grad, workspace=ws_p,
-            stream=main, logits=logits, chunk_rows=self.bwd_chunk_rows, head=head, head_rows=head_rows)
+            stream=main, logits=logits, chunk_rows=chunk, head=head, head_rows=head_rows)
         res.update(rnnt_combine_losses(sim["loss"], pl["loss"], self.simple_scale, self.pruned_scale, reduction,
                                        loss=o("loss", (N,)), total=o("total", ()), stream=main))
         if self.overlap:

@@ -371,6 +371,16 @@ void set_joiner_bwd(JoinerArgs& a, const JoinerBwdWs& w, const float* lse, const
   a.logits_grad = logits_grad;
 }
 
+// The unpruned loss's backward chunk: about 256 MiB of d(logits) (within the
+// 32-bit limit), a comparison path that holds the [N, T, U+1, V] scale of
+// memory by design and runs fewest, fullest launches.
+int full_chunk_rows(int J, int V, int bf16) {
+  long long r = (256ll << 20) / ((long long)joiner_ldl(V) * (bf16 ? 2 : 4)) / 128 * 128;
+  const long long lim = joiner_bwd_chunk_max_rows(J, V);
+  if (r > lim) r = lim;
+  return (int)(r < 128 ? 128 : r);
+}
+
 // Workspace of rnnt_full_loss: the lattice-sized arrays, then one region
 // that the joiner's forward and backward use in turn.
 struct FullWs {
@@ -404,7 +414,7 @@ FullWs full_layout(void* base, int N, int T, int U, int J, int V, int bf16) {
   w.cpx = c.take<double>((size_t)N * lattice_colblocks(T) * S);
   w.cpy = c.take<double>((size_t)N * lattice_colblocks(T) * S);
   const size_t jf = joiner_fwd_layout(nullptr, N, T, S, J, V, bf16).bytes;
-  const size_t jb = joiner_bwd_layout(nullptr, N, T, S, J, V, bf16).bytes;
+  const size_t jb = joiner_bwd_layout(nullptr, N, T, S, J, V, bf16, full_chunk_rows(J, V, bf16)).bytes;
   w.joiner = c.take<unsigned char>(jf > jb ? jf : jb);
   w.bytes = c.off;
   return w;
@@ -917,7 +927,8 @@ int rnnt_full_loss(const rnnt_batch* batch, int32_t J, int32_t V, int32_t dtype,
   if (e == hipSuccess) e = launch_lattice(la, s);
   // the joiner's backward on every (t, u)
   JoinerArgs jb = joiner_args(batch, S, J, V, dtype, enc, dec, W, bias, w.ranges);
-  set_joiner_bwd(jb, joiner_bwd_layout(w.joiner, batch->N, batch->T, S, J, V, bf), w.lse, logits, w.gx, w.gy,
+  set_joiner_bwd(jb, joiner_bwd_layout(w.joiner, batch->N, batch->T, S, J, V, bf, full_chunk_rows(J, V, bf)), w.lse,
+                 logits, w.gx, w.gy,
                  scale, enc_grad, dec_grad, W_grad, bias_grad, nullptr);
   if (e == hipSuccess) e = launch_joiner_prep(jb, s);
   if (e == hipSuccess) e = launch_joiner_bwd(jb, s);
