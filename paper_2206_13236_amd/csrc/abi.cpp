@@ -196,6 +196,7 @@ struct JoinerFwdWs {
   float* tgt;
   float* blk;
   void* h;
+  void* wt;
   int chunk_rows;
   size_t bytes;
 };
@@ -212,6 +213,7 @@ JoinerFwdWs joiner_fwd_layout(void* base, int N, int T, int S, int J, int V, int
   w.blk = c.take<float>(M);
   const size_t h_elems = joiner_fwd_uses_hbuf(bf16) ? (size_t)w.chunk_rows * J : 0;
   w.h = h_elems == 0 ? nullptr : bf16 ? (void*)c.take<uint16_t>(h_elems) : (void*)c.take<float>(h_elems);
+  w.wt = bf16 ? (void*)c.take<uint16_t>((size_t)V * J) : nullptr;
   w.bytes = c.off;
   return w;
 }
@@ -224,6 +226,7 @@ struct JoinerBwdWs {
   void* dl[2];
   void* dlT[2];
   void* wpad;
+  void* wt;
   float* dpre;
   float* enc_part;
   void* hbuf[2];
@@ -239,7 +242,7 @@ JoinerBwdWs joiner_bwd_layout(void* base, int N, int T, int S, int J, int V, int
   JoinerBwdWs w;
   const size_t M = (size_t)N * T * S;
   w.chunk_rows = joiner_bwd_chunk_rows(N, T, S, J, V, bf16, chunk_request);
-  w.splits = joiner_bwd_splits(J, V, w.chunk_rows);
+  w.splits = joiner_bwd_splits(J, V, w.chunk_rows, bf16);
   w.n_db_rows = joiner_db_rows(w.chunk_rows);
   w.frame_off = c.take<int>((size_t)N + 1);
   w.frame_nt = c.take<int>((size_t)N * T);
@@ -255,6 +258,7 @@ JoinerBwdWs joiner_bwd_layout(void* base, int N, int T, int S, int J, int V, int
     w.hT[k] = bf16 ? (void*)c.take<uint16_t>(h_elems) : nullptr;
   }
   w.wpad = (bf16 && V % 8 != 0) ? (void*)c.take<uint16_t>((size_t)J * joiner_ldl(V)) : nullptr;
+  w.wt = bf16 ? (void*)c.take<uint16_t>((size_t)V * J) : nullptr;
   w.dpre = c.take<float>((size_t)w.chunk_rows * J);
   w.enc_part = c.take<float>((M + 127) / 128 * 2 * J);
   w.dw_part = c.take<float>((size_t)w.splits * J * V);
@@ -328,6 +332,7 @@ void set_joiner_fwd(JoinerArgs& a, const JoinerFwdWs& w, float* px, float* py, f
   a.tgt = w.tgt;
   a.blk = w.blk;
   a.hbuf = w.h;
+  a.wt = w.wt;
   a.chunk_rows = w.chunk_rows;
   a.px = px;
   a.py = py;
@@ -355,6 +360,7 @@ void set_joiner_bwd(JoinerArgs& a, const JoinerBwdWs& w, const float* lse, const
   a.ring1[2] = w.dl[1];
   a.ring1[3] = w.dlT[1];
   a.wpad = w.wpad;
+  a.wt = w.wt;
   a.ldl = joiner_ldl(a.V);
   a.chunk_rows = w.chunk_rows;
   a.dpre = w.dpre;

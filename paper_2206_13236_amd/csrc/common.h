@@ -110,6 +110,11 @@ DEV float fast_tanh(float x) {
   return 1.0f - 2.0f * __builtin_amdgcn_rcpf(e + 1.0f);
 }
 
+// Waits until every vector memory access this wave has issued is complete.
+// The compiler's wait tracking sees it, so registers loaded before it need no
+// wait of their own at their uses, in whatever branch those are.
+DEV void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70); }  // vmcnt(0), expcnt and lgkmcnt not waited
+
 DEV double shfl_up_d(double v, int delta) { return __shfl_up(v, delta, 64); }
 DEV double shfl_down_d(double v, int delta) { return __shfl_down(v, delta, 64); }
 

@@ -343,3 +343,144 @@ DEV int tile_col(int j) {
   const int lane = threadIdx.x & 63, wn = (threadIdx.x >> 6) % Cfg::WGN;
   return wn * Cfg::WN + j * 16 + (lane & 15);
 }
+
+// ---------------------------------------------------------------------------
+// Main loop with both operands loaded straight from global memory into LDS
+// (buffer_load_dwordx4 ... lds: the 16 bytes of lane i land at the
+// instruction's LDS base + 16 i). Nothing is staged through registers, so a
+// K-step's loads stay in flight at no register cost while the previous
+// K-step computes, and two workgroups share a CU (64 KiB of LDS each at
+// 128 x 128 and 128-byte rows, two stages).
+//
+// Both operands must be k-contiguous in global memory, in 16-byte chunks
+// (8 bf16 or 4 fp32) at 16-byte aligned offsets. An LDS row holds BK
+// elements unpadded; the chunks of row r are stored XOR-swizzled (chunk c at
+// position c ^ (r & 7)), so that the fragment reads of 8 consecutive rows fall
+// in distinct banks. MFMAs and accumulator layout are those of GemmCfg
+// (tile_row, tile_col).
+// ---------------------------------------------------------------------------
+template <int BM_, int BN_, int BK_, int WGM_, int WGN_, bool BF16_ = true>
+struct LdsCfg {
+  static constexpr int BM = BM_, BN = BN_, BK = BK_;
+  static constexpr bool BF16 = BF16_;
+  using T = typename std::conditional<BF16_, uint16_t, float>::type;
+  static constexpr int ESZ = (int)sizeof(T);
+  static constexpr int KV = 16 / ESZ;          // k values per 16-byte chunk
+  static constexpr int WGM = WGM_, WGN = WGN_;
+  static constexpr int NW = WGM * WGN, NT = 64 * NW;
+  static constexpr int WM = BM / WGM, WN = BN / WGN;
+  static constexpr int FM = WM / 16, FN = WN / 16;
+  static constexpr int CH = BK / KV;           // chunks per row
+  static constexpr int ROWB = BK * ESZ;        // bytes per LDS row
+  static constexpr int RPI = 64 / CH;          // rows filled by one wave-wide load
+  static constexpr int A_BYTES = BM * ROWB, B_BYTES = BN * ROWB;
+  static constexpr int STAGE_BYTES = A_BYTES + B_BYTES;
+  static constexpr int SMEM_BYTES = 2 * STAGE_BYTES;
+  static constexpr int A_IPW = BM / RPI / NW, B_IPW = BN / RPI / NW;  // loads per wave per stage
+  static_assert(CH >= 8 && CH % 4 == 0, "the swizzle needs at least 8 chunks per row");
+  static_assert((BM / RPI) % NW == 0 && (BN / RPI) % NW == 0, "whole loads per wave");
+  static_assert(FM >= 1 && FN >= 1, "tile too small");
+};
+
+// Operand rows [row0, row0 + nvalid) of a k-contiguous array of ESZ-byte
+// elements with row stride ld (elements); element (r, k) of the tile is
+// array[row0 + r][k - kofs] for k < kend, zero elsewhere (loads past the end
+// read through kOob).
+template <int ESZ>
+struct LdsSrc {
+  Rsrc rsrc;
+  int row0, nvalid, ld, kofs, kend;
+  DEV uint32_t off(int r, int k) const {
+    return (r < nvalid && k < kend) ? (uint32_t)((row0 + r) * ld + (k - kofs)) * (uint32_t)ESZ : kOob;
+  }
+};
+
+typedef __attribute__((address_space(3))) void* LdsPtr;
+
+// One operand tile for K-step k0 into `lds`: wave w issues loads
+// w*IPW .. w*IPW+IPW-1, load q filling tile rows [q*RPI, (q+1)*RPI).
+template <class Cfg, int IPW>
+DEV void lds_fetch(const LdsSrc<Cfg::ESZ>& s, int k0, unsigned char* lds) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int i = 0; i < IPW; ++i) {
+    const int q = wave * IPW + i;
+    const int r = q * Cfg::RPI + lane / Cfg::CH;
+    const int c = (lane % Cfg::CH) ^ (r & 7);  // the chunk stored at this lane's position
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(s.rsrc, (LdsPtr)(lds + q * 1024), 16, s.off(r, k0 + c * Cfg::KV), 0, 0, 0);
+  }
+}
+
+template <class Cfg>
+DEV void lds_compute_stage(const unsigned char* As, const unsigned char* Bs, floatx4 (&acc)[Cfg::FM][Cfg::FN]) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave / Cfg::WGN, wn = wave % Cfg::WGN;
+  const int lr = lane & 15, lq = lane >> 4;
+  // fragment rows are 16-aligned plus lr, so their swizzle key is lr & 7
+  const unsigned char* a_row = As + (wm * Cfg::WM + lr) * Cfg::ROWB;
+  const unsigned char* b_row = Bs + (wn * Cfg::WN + lr) * Cfg::ROWB;
+#pragma unroll
+  for (int kc = 0; kc < Cfg::CH; kc += 4) {
+    const int pos = ((kc + lq) ^ (lr & 7)) * 16;
+    if constexpr (Cfg::BF16) {
+      bf16x8 fa[Cfg::FM], fb[Cfg::FN];
+#pragma unroll
+      for (int i = 0; i < Cfg::FM; ++i) fa[i] = *reinterpret_cast<const bf16x8*>(a_row + i * 16 * Cfg::ROWB + pos);
+#pragma unroll
+      for (int j = 0; j < Cfg::FN; ++j) fb[j] = *reinterpret_cast<const bf16x8*>(b_row + j * 16 * Cfg::ROWB + pos);
+#pragma unroll
+      for (int i = 0; i < Cfg::FM; ++i)
+#pragma unroll
+        for (int j = 0; j < Cfg::FN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+    } else {
+      // a chunk holds 4 consecutive k; MFMA s takes element s of every lane's
+      // chunk (the same permutation of k for A and B)
+      floatx4 fa[Cfg::FM], fb[Cfg::FN];
+#pragma unroll
+      for (int i = 0; i < Cfg::FM; ++i) fa[i] = *reinterpret_cast<const floatx4*>(a_row + i * 16 * Cfg::ROWB + pos);
+#pragma unroll
+      for (int j = 0; j < Cfg::FN; ++j) fb[j] = *reinterpret_cast<const floatx4*>(b_row + j * 16 * Cfg::ROWB + pos);
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int i = 0; i < Cfg::FM; ++i)
+#pragma unroll
+          for (int j = 0; j < Cfg::FN; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[i][q], fb[j][q], acc[i][j], 0, 0, 0);
+    }
+  }
+}
+
+// Waits for this wave's outstanding loads, then meets the other waves. An
+// explicit s_waitcnt + s_barrier rather than __syncthreads(), whose release
+// fence the compiler would also place after the next stage's loads.
+DEV void lds_stage_barrier() { asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+// K loop over [k_begin, k_end) with two LDS stages: at step kt the loads of
+// step kt+1 run while step kt computes; one barrier per step. Leaves the
+// tile in `acc` and LDS free for the caller (it ends with a barrier). Must be
+// called by all NT threads of the workgroup.
+template <class Cfg>
+DEV void gemm_mainloop_lds(const LdsSrc<Cfg::ESZ>& sa, const LdsSrc<Cfg::ESZ>& sb, int k_begin, int k_end,
+                           unsigned char* smem, floatx4 (&acc)[Cfg::FM][Cfg::FN]) {
+#pragma unroll
+  for (int i = 0; i < Cfg::FM; ++i)
+#pragma unroll
+    for (int j = 0; j < Cfg::FN; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+  const int nk = (k_end - k_begin + Cfg::BK - 1) / Cfg::BK;
+  if (nk <= 0) return;
+  lds_fetch<Cfg, Cfg::A_IPW>(sa, k_begin, smem);
+  lds_fetch<Cfg, Cfg::B_IPW>(sb, k_begin, smem + Cfg::A_BYTES);
+  for (int kt = 0; kt < nk; ++kt) {
+    lds_stage_barrier();  // step kt landed everywhere; step kt-1's slot is free
+    if (kt + 1 < nk) {
+      unsigned char* st = smem + ((kt + 1) & 1) * Cfg::STAGE_BYTES;
+      lds_fetch<Cfg, Cfg::A_IPW>(sa, k_begin + (kt + 1) * Cfg::BK, st);
+      lds_fetch<Cfg, Cfg::B_IPW>(sb, k_begin + (kt + 1) * Cfg::BK, st + Cfg::A_BYTES);
+    }
+    const unsigned char* cs = smem + (kt & 1) * Cfg::STAGE_BYTES;
+    lds_compute_stage<Cfg>(cs, cs + Cfg::A_BYTES, acc);
+  }
+  __syncthreads();
+}

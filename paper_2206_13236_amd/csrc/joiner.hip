@@ -41,10 +41,13 @@ namespace {
 // 8 waves in a 4 x 2 grid (32 x 64 wave tiles): about 100 registers per
 // lane, so two workgroups (four waves per SIMD) share a CU.
 constexpr int kGemmThreads = 512;
+// fp32: operands staged through registers (the forward forms tanh(enc + dec)
+// while staging; dW transposes both operands in registers)
 using CfgF = GemmCfg<128, 128, 32, false, 4, 2>;
-using CfgB = GemmCfg<128, 128, 64, true, 4, 2, false>;
-// dW stages both operands through register transposes: one fetch set fits
-using CfgBw = GemmCfg<128, 128, 64, true, 4, 2, false>;
+// bf16: every operand is read k-contiguous (h, d(logits) and their
+// transposes, W and its transposed copy) straight into LDS
+using CfgB = LdsCfg<128, 128, 64, 4, 2>;
+using CfgBw = CfgB;
 static_assert(CfgF::NT == kGemmThreads && CfgB::NT == kGemmThreads, "joiner GEMM block size");
 static_assert(CfgF::WN == 64 && CfgB::WN == 64, "the forward's partial log-sum-exp slices are 64 columns");
 static_assert(CfgF::BM == CfgB::BM && CfgF::WGM == CfgB::WGM, "db partial rows per row tile");
@@ -63,9 +66,9 @@ struct In<true> {
 };
 
 // Whether the forward reads h from a buffer written by the h kernel (bf16:
-// its MFMA K-steps are too short to hide the tanh work of staging) or forms
-// it while staging the A tile (fp32: measured ~5 us faster per step at the
-// BPE size than a separate h pass).
+// its operands go straight into LDS, with no register stage where tanh could
+// be formed) or forms it while staging the A tile (fp32: measured ~5 us
+// faster per step at the BPE size than a separate h pass).
 template <bool BF>
 constexpr bool kFwdHbuf = BF;
 
@@ -271,25 +274,6 @@ struct WtSrcKC {
   DEV void kc_finish(const Raw& r, float (&v)[Cfg::KV]) const { raw_to_float(r, v); }
 };
 
-// bf16 dW operands from transposed chunk buffers (k = m contiguous):
-// A(j, m) = hT[j][m - cm0], B(v, m) = dlT[v][m - cm0]. Rows past mend hold
-// zeros up to the 128-row tile end, so a 16-byte segment that crosses mend
-// reads zeros there; split boundaries inside a chunk are K-step aligned.
-template <class Cfg>
-struct TrSrcKC {
-  static constexpr bool kDirect = true;
-  using T = typename Cfg::T;
-  using Raw = RawVec<T, Cfg::KV>;
-  Rsrc p;
-  int cm0, ke, r0, nrows, ld;
-  DEV void kc_load(int row, int k, Raw& r) const {
-    const int q = r0 + row;
-    const int n = (q < nrows && k < ke) ? Cfg::KV : 0;
-    raw_load(p, (uint32_t)(q * ld + (k - cm0)) * sizeof(T), n, kSegVector, r);
-  }
-  DEV void kc_finish(const Raw& r, float (&v)[Cfg::KV]) const { raw_to_float(r, v); }
-};
-
 // A(j, m) = h(m, j) from the chunk's hbuf [rows, J] (j-contiguous).
 template <class Cfg>
 struct HbufSrcMNC {
@@ -329,6 +313,25 @@ DEV float bias_at(const void* bias, int bf16, int v) {
   return bf16 ? bf2f(reinterpret_cast<const uint16_t*>(bias)[v]) : reinterpret_cast<const float*>(bias)[v];
 }
 
+// The bias of this lane's FN output columns v0 + tile_col(j) (0 past V or
+// without a bias), with branch-free buffer loads: issued ahead of the main
+// loop (bf16) or right after it (fp32, whose main loop has no registers to
+// spare), and waited for once with wait_vmem() before the epilogue. A load
+// inside a per-column branch would instead make the compiler wait again at
+// every later branch, and with it for every store issued in between.
+template <class Cfg, bool BF>
+DEV void bias_cols(const JoinerArgs& a, int v0, float (&bj)[Cfg::FN]) {
+  constexpr uint32_t esz = BF ? 2 : 4;
+  const Rsrc rb = make_rsrc(a.bias, a.bias ? (size_t)a.V * esz : 0);
+#pragma unroll
+  for (int j = 0; j < Cfg::FN; ++j) {
+    const int col = v0 + tile_col<Cfg>(j);
+    const uint32_t off = col < a.V ? (uint32_t)col * esz : kOob;
+    if constexpr (BF) bj[j] = bf2f(__builtin_amdgcn_raw_buffer_load_b16(rb, (int)off, 0, 0));
+    else bj[j] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rb, (int)off, 0, 0));
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Prep: per-utterance frame offsets and per-row info.
 // ---------------------------------------------------------------------------
@@ -352,11 +355,43 @@ DEV void prep_wpad(const JoinerArgs& a, int b) {
 
 int prep_wpad_blocks(const JoinerArgs& a) { return a.wpad ? (a.J * (a.ldl / 8) + 255) / 256 : 0; }
 
-__global__ __launch_bounds__(256) void joiner_prep_kernel(JoinerArgs a) {
+// W [J, V] bf16 transposed into wt [V, J], one 64 x 64 tile per block through
+// LDS: W read along v (consecutive threads, consecutive v), wt written in
+// 16-byte groups of 8 consecutive j (J is a multiple of 8).
+constexpr int kWtTile = 64;
+DEV void prep_wt(const JoinerArgs& a, int b) {
+  __shared__ uint16_t tile[kWtTile][kWtTile + 2];
+  const int nvt = (a.V + kWtTile - 1) / kWtTile;
+  const int j0 = (b / nvt) * kWtTile, v0 = (b % nvt) * kWtTile;
+  const uint16_t* W = reinterpret_cast<const uint16_t*>(a.W);
+  const int c = threadIdx.x % kWtTile;
+  for (int r = threadIdx.x / kWtTile; r < kWtTile; r += 256 / kWtTile) {
+    const int j = j0 + r, v = v0 + c;
+    tile[r][c] = (j < a.J && v < a.V) ? W[(size_t)j * a.V + v] : (uint16_t)0;
+  }
+  __syncthreads();
+  for (int q = threadIdx.x; q < kWtTile * (kWtTile / 8); q += 256) {
+    const int vr = q / (kWtTile / 8), jg = (q % (kWtTile / 8)) * 8;
+    const int v = v0 + vr, j = j0 + jg;
+    if (v >= a.V || j >= a.J) continue;
+    uint32_t w[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) w[k] = (uint32_t)tile[jg + 2 * k][vr] | ((uint32_t)tile[jg + 2 * k + 1][vr] << 16);
+    *reinterpret_cast<uint4*>(reinterpret_cast<uint16_t*>(a.wt) + (size_t)v * a.J + j) = make_uint4(w[0], w[1], w[2], w[3]);
+  }
+}
+
+int prep_wt_blocks(const JoinerArgs& a) {
+  return a.wt ? ((a.J + kWtTile - 1) / kWtTile) * ((a.V + kWtTile - 1) / kWtTile) : 0;
+}
+
+__global__ __launch_bounds__(256) void joiner_prep_kernel(JoinerArgs a, int wpad_blocks) {
   __shared__ int s_part[4];
   const int per = (a.b.T * a.S + 255) / 256;  // blocks per utterance: one (t, s) slot per thread
-  if ((int)blockIdx.x >= a.b.N * per) {  // blocks after the utterances' copy W for dh
-    prep_wpad(a, blockIdx.x - a.b.N * per);
+  if ((int)blockIdx.x >= a.b.N * per) {  // blocks after the utterances' copy W for dh, then transpose it
+    const int b = blockIdx.x - a.b.N * per;
+    if (b < wpad_blocks) prep_wpad(a, b);
+    else prep_wt(a, b - wpad_blocks);
     return;
   }
   const int n = blockIdx.x / per, i = (blockIdx.x - n * per) * 256 + threadIdx.x;
@@ -463,27 +498,28 @@ __global__ __launch_bounds__(kGemmThreads, 4) void joiner_fwd_kernel(JoinerArgs 
   for (int r = threadIdx.x; r < Cfg::BM; r += Cfg::NT)
     ri[r] = (m0 + r < mend) ? a.rowinfo[m0 + r] : make_int4(0, 0, -1, -1);
   __syncthreads();
-  WSrcMNC<Cfg, TIn, WM> sb(a, v0);
-  MNCLoader<Cfg, Cfg::BN, WSrcMNC<Cfg, TIn, WM>> lb(sb);
+  float bj[Cfg::FN];
+  if constexpr (BF) bias_cols<Cfg, BF>(a, v0, bj);
   floatx4 acc[Cfg::FM][Cfg::FN];
-  if constexpr (kFwdHbuf<BF>) {
-    HbufSrcKC<Cfg> sa{make_rsrc(a.hbuf, (size_t)a.chunk_rows * J * sizeof(typename Cfg::T)), m0, cm0, mend, J};
-    KCLoader<Cfg, Cfg::BM, HbufSrcKC<Cfg>> la(sa);
-    gemm_mainloop<Cfg>(la, lb, 0, J, smem, acc);
+  if constexpr (BF) {
+    static_assert(kFwdHbuf<BF>, "the bf16 forward reads h from the h pass");
+    // h of the chunk and W^T (the prep kernel's copy), both k = j contiguous
+    const LdsSrc<2> sa{make_rsrc(a.hbuf, (size_t)a.chunk_rows * J * 2), m0 - cm0, mend - m0, J, 0, J};
+    const LdsSrc<2> sb{make_rsrc(a.wt, (size_t)V * J * 2), v0, V - v0, J, 0, J};
+    gemm_mainloop_lds<Cfg>(sa, sb, 0, J, reinterpret_cast<unsigned char*>(smem), acc);
   } else {
+    static_assert(!kFwdHbuf<BF>, "the fp32 forward forms h while staging");
+    WSrcMNC<Cfg, TIn, WM> sb(a, v0);
+    MNCLoader<Cfg, Cfg::BN, WSrcMNC<Cfg, TIn, WM>> lb(sb);
     HSrcKC<Cfg, TIn> sa{EncDec<TIn>(a), ri, J};
     KCLoader<Cfg, Cfg::BM, HSrcKC<Cfg, TIn>> la(sa);
     gemm_mainloop<Cfg>(la, lb, 0, J, smem, acc);
   }
 
+  if constexpr (!BF) bias_cols<Cfg, BF>(a, v0, bj);
+  wait_vmem();
   const int lane = threadIdx.x & 63, wn = (threadIdx.x >> 6) % Cfg::WGN;
   const int slice = nt * Cfg::WGN + wn;
-  float bj[Cfg::FN];
-#pragma unroll
-  for (int j = 0; j < Cfg::FN; ++j) {
-    const int col = v0 + tile_col<Cfg>(j);
-    bj[j] = (col < V) ? bias_at(a.bias, a.bf16, col) : 0.f;
-  }
 #pragma unroll
   for (int i = 0; i < Cfg::FM; ++i)
 #pragma unroll
@@ -599,7 +635,6 @@ template <bool BF, int WM>
 DEV void dlogits_tile(const JoinerArgs& a, int cm0, int cm1, int v, int nblocks, int ncol, unsigned char* lds) {
   using TIn = typename In<BF>::T;
   using Cfg = typename In<BF>::Cfg;
-  typename Cfg::T* smem = lds_stages<Cfg>(lds);
   int4* ri = lds_rowinfo(lds);
   float4* rx = lds_rowx(lds);  // lse, gx, gy, scale
   const int M = a.frame_off[a.b.N] * a.S;
@@ -621,22 +656,41 @@ DEV void dlogits_tile(const JoinerArgs& a, int cm0, int cm1, int v, int nblocks,
     rx[r] = x;
   }
   __syncthreads();
-  HbufSrcKC<Cfg> sa{make_rsrc(a.hbuf, (size_t)a.chunk_rows * J * sizeof(typename Cfg::T)), m0, cm0, mend, J};
-  WSrcMNC<Cfg, TIn, WM> sb(a, v0);
-  KCLoader<Cfg, Cfg::BM, HbufSrcKC<Cfg>> la(sa);
-  MNCLoader<Cfg, Cfg::BN, WSrcMNC<Cfg, TIn, WM>> lb(sb);
-  floatx4 acc[Cfg::FM][Cfg::FN];
-  gemm_mainloop<Cfg>(la, lb, 0, J, smem, acc);
-
   const int lane = threadIdx.x & 63, wm = (threadIdx.x >> 6) / Cfg::WGN;
-  typename Cfg::T* dl = reinterpret_cast<typename Cfg::T*>(a.dl);
-  float bj[Cfg::FN], colsum[Cfg::FN];
+  // this lane's db_part entries (lanes < 16 of each wave row; a later chunk
+  // adds to what the earlier ones left) and bias values, loaded before the
+  // epilogue's stores: see bias_cols
+  const int mt = (m0 - cm0) / Cfg::BM;
+  float* dbq = a.db_part + ((size_t)mt * Cfg::WGM + wm) * V + v0;
+  float bj[Cfg::FN], dbold[Cfg::FN];
+  auto early_loads = [&]() {
+    bias_cols<Cfg, BF>(a, v0, bj);
 #pragma unroll
-  for (int j = 0; j < Cfg::FN; ++j) {
-    const int col = v0 + tile_col<Cfg>(j);
-    bj[j] = (col < V) ? bias_at(a.bias, a.bf16, col) : 0.f;
-    colsum[j] = 0.f;
+    for (int j = 0; j < Cfg::FN; ++j) {
+      const int c = tile_col<Cfg>(j);
+      dbold[j] = (cm0 != 0 && lane < 16 && v0 + c < V) ? dbq[c] : 0.f;
+    }
+  };
+  if constexpr (BF) early_loads();
+  floatx4 acc[Cfg::FM][Cfg::FN];
+  if constexpr (BF) {
+    const LdsSrc<2> sa{make_rsrc(a.hbuf, (size_t)a.chunk_rows * J * 2), m0 - cm0, mend - m0, J, 0, J};
+    const LdsSrc<2> sb{make_rsrc(a.wt, (size_t)V * J * 2), v0, V - v0, J, 0, J};
+    gemm_mainloop_lds<Cfg>(sa, sb, 0, J, lds, acc);
+  } else {
+    HbufSrcKC<Cfg> sa{make_rsrc(a.hbuf, (size_t)a.chunk_rows * J * sizeof(typename Cfg::T)), m0, cm0, mend, J};
+    WSrcMNC<Cfg, TIn, WM> sb(a, v0);
+    KCLoader<Cfg, Cfg::BM, HbufSrcKC<Cfg>> la(sa);
+    MNCLoader<Cfg, Cfg::BN, WSrcMNC<Cfg, TIn, WM>> lb(sb);
+    gemm_mainloop<Cfg>(la, lb, 0, J, lds_stages<Cfg>(lds), acc);
+    early_loads();
   }
+  wait_vmem();
+
+  typename Cfg::T* dl = reinterpret_cast<typename Cfg::T*>(a.dl);
+  float colsum[Cfg::FN];
+#pragma unroll
+  for (int j = 0; j < Cfg::FN; ++j) colsum[j] = 0.f;
 #pragma unroll
   for (int i = 0; i < Cfg::FM; ++i)
 #pragma unroll
@@ -682,17 +736,13 @@ DEV void dlogits_tile(const JoinerArgs& a, int cm0, int cm1, int v, int nblocks,
   }
   // db partial: sum over this wave's WM rows, one row of db_part per (m-tile
   // of the chunk, wave row); the first chunk writes it, later ones add to it.
-  const int mt = (m0 - cm0) / Cfg::BM;
 #pragma unroll
   for (int j = 0; j < Cfg::FN; ++j) {
     float s = colsum[j];
     s += __shfl_xor(s, 16, 64);
     s += __shfl_xor(s, 32, 64);
-    const int col = v0 + tile_col<Cfg>(j);
-    if (lane < 16 && col < V) {
-      float* q = a.db_part + ((size_t)mt * Cfg::WGM + wm) * V + col;
-      *q = cm0 == 0 ? s : *q + s;
-    }
+    const int c = tile_col<Cfg>(j);
+    if (lane < 16 && v0 + c < V) dbq[c] = dbold[j] + s;
   }
 }
 
@@ -927,7 +977,6 @@ DEV void dh_tile(const JoinerArgs& a, int cm0, int cm1, int v, int nblocks, int 
                  bool write_h) {
   using TIn = typename In<BF>::T;
   using Cfg = typename In<BF>::Cfg;
-  typename Cfg::T* smem = lds_stages<Cfg>(lds);
   int4* ri = lds_rowinfo(lds);
   const int M = a.frame_off[a.b.N] * a.S;
   const int mend = min(cm1, M);
@@ -940,21 +989,51 @@ DEV void dh_tile(const JoinerArgs& a, int cm0, int cm1, int v, int nblocks, int 
   for (int r = threadIdx.x; r < Cfg::BM; r += Cfg::NT)
     ri[r] = (m0 + r < mend) ? a.rowinfo[m0 + r] : make_int4(0, 0, -1, -1);
   __syncthreads();
-  DlSrcKC<Cfg> sa{make_rsrc(a.dl, (size_t)a.chunk_rows * a.ldl * sizeof(typename Cfg::T)), m0, cm0, mend, a.ldl};
-  WtSrcKC<Cfg, TIn, WM> sb(a, j0);
-  KCLoader<Cfg, Cfg::BM, DlSrcKC<Cfg>> la(sa);
-  KCLoader<Cfg, Cfg::BN, WtSrcKC<Cfg, TIn, WM>> lb(sb);
   const TileFrameRegs fr = tile_frames_fetch(a, m0, mend, Cfg::BM);
+  // enc and dec of this thread's 4-column groups of the tile (the epilogue's
+  // h = tanh(enc + dec)), all issued together: ahead of the main loop for
+  // bf16, right after it for fp32 (whose main loop has no registers to
+  // spare), then waited for once
+  constexpr int NIT = Cfg::BM * Cfg::BN / 4 / Cfg::NT;  // 4-column groups per thread
+  static_assert(Cfg::BM * Cfg::BN / 4 % Cfg::NT == 0, "whole groups per thread");
+  const EncDec<TIn> ed(a);
+  RawVec<TIn, 4> pe[NIT], pd[NIT];
+  auto fetch_enc_dec = [&]() {
+#pragma unroll
+    for (int q8 = 0; q8 < NIT; ++q8) {
+      const int it = threadIdx.x + q8 * Cfg::NT;
+      const int row = it / (Cfg::BN / 4), jj = j0 + (it - row * (Cfg::BN / 4)) * 4;
+      const int4 info = ri[row];  // absent (w < 0) for rows past mend
+      const int n = (info.w >= 0 && jj < J) ? 4 : 0;  // J is a multiple of 8: a group is all in or out
+      raw_load(ed.enc, (uint32_t)(info.x + jj) * sizeof(TIn), n, kSegVector, pe[q8]);
+      raw_load(ed.dec, (uint32_t)(info.y + jj) * sizeof(TIn), n, kSegVector, pd[q8]);
+    }
+  };
+  if constexpr (BF) fetch_enc_dec();
   floatx4 acc[Cfg::FM][Cfg::FN];
-  gemm_mainloop<Cfg>(la, lb, 0, a.V, smem, acc);
+  if constexpr (BF) {
+    // d(logits) of the chunk and W (or its zero-padded copy), both k = v contiguous
+    const int ldw = a.wpad ? a.ldl : a.V;
+    const LdsSrc<2> sa{make_rsrc(a.dl, (size_t)a.chunk_rows * a.ldl * 2), m0 - cm0, mend - m0, a.ldl, 0, a.ldl};
+    const LdsSrc<2> sb{make_rsrc(a.wpad ? a.wpad : a.W, (size_t)J * ldw * 2), j0, J - j0, ldw, 0, ldw};
+    gemm_mainloop_lds<Cfg>(sa, sb, 0, a.V, lds, acc);
+  } else {
+    DlSrcKC<Cfg> sa{make_rsrc(a.dl, (size_t)a.chunk_rows * a.ldl * sizeof(typename Cfg::T)), m0, cm0, mend, a.ldl};
+    WtSrcKC<Cfg, TIn, WM> sb(a, j0);
+    KCLoader<Cfg, Cfg::BM, DlSrcKC<Cfg>> la(sa);
+    KCLoader<Cfg, Cfg::BN, WtSrcKC<Cfg, TIn, WM>> lb(sb);
+    gemm_mainloop<Cfg>(la, lb, 0, a.V, lds_stages<Cfg>(lds), acc);
+    fetch_enc_dec();
+  }
+  wait_vmem();
 
   // Epilogue through LDS (the operand stages are free after the main loop's
   // last barrier): the tile goes to LDS in the MFMA layout and comes back row
   // by row, so that enc, dec, dpre and h are read and written with 16-byte
   // accesses per thread along J.
   constexpr int LDC = Cfg::BN + 4;
-  static_assert(Cfg::BM * LDC * 4 <= Cfg::SMEM_BYTES, "epilogue tile fits the operand stages");
-  float* C = reinterpret_cast<float*>(smem);
+  static_assert(Cfg::BM * LDC * 4 <= kBwdStageBytes, "epilogue tile fits the operand stages");
+  float* C = reinterpret_cast<float*>(lds);
 #pragma unroll
   for (int i = 0; i < Cfg::FM; ++i)
 #pragma unroll
@@ -962,9 +1041,6 @@ DEV void dh_tile(const JoinerArgs& a, int cm0, int cm1, int v, int nblocks, int 
 #pragma unroll
       for (int r = 0; r < 4; ++r) C[tile_row<Cfg>(i, r) * LDC + tile_col<Cfg>(j)] = acc[i][j][r];
   __syncthreads();
-  const EncDec<TIn> ed(a);
-  constexpr int NIT = Cfg::BM * Cfg::BN / 4 / Cfg::NT;  // 4-column groups per thread
-  static_assert(Cfg::BM * Cfg::BN / 4 % Cfg::NT == 0, "whole groups per thread");
   float4 hk[BF ? NIT : 1];  // bf16: h of this thread's groups, back to the tile after the d enc / d dec pieces
 #pragma unroll
   for (int q8 = 0; q8 < NIT; ++q8) {
@@ -974,14 +1050,10 @@ DEV void dh_tile(const JoinerArgs& a, int cm0, int cm1, int v, int nblocks, int 
     if constexpr (BF) hk[q8] = make_float4(0.f, 0.f, 0.f, 0.f);
     if (jj >= J) continue;  // J is a multiple of 8: the group is all in or all out
     float* cr = C + row * LDC + cg * 4;
-    const int4 info = ri[row];  // absent (w < 0) for rows past mend
-    const bool on = info.w >= 0;
-    RawVec<TIn, 4> e, d;
-    raw_load(ed.enc, (uint32_t)(info.x + jj) * sizeof(TIn), on ? 4 : 0, kSegVector, e);
-    raw_load(ed.dec, (uint32_t)(info.y + jj) * sizeof(TIn), on ? 4 : 0, kSegVector, d);
+    const bool on = ri[row].w >= 0;  // absent (w < 0) for rows past mend
     float fe[4], fd[4], h[4], dp[4];
-    raw_to_float(e, fe);
-    raw_to_float(d, fd);
+    raw_to_float(pe[q8], fe);
+    raw_to_float(pd[q8], fd);
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       h[q] = on ? fast_tanh(fe[q] + fd[q]) : 0.f;
@@ -1074,7 +1146,6 @@ __global__ __launch_bounds__(256) void joiner_dlt_kernel(JoinerArgs a, int cm0, 
 template <bool BF>
 DEV void dw_tile(const JoinerArgs& a, int cm0, int cm1, int first, int v, int nj, int nv, unsigned char* lds) {
   using Cfg = typename std::conditional<BF, CfgBw, CfgF>::type;
-  typename Cfg::T* smem = lds_stages<Cfg>(lds);
   const int M = a.frame_off[a.b.N] * a.S;
   const int mend = min(cm1, M);
   const int per_split = nj * nv;
@@ -1098,21 +1169,43 @@ DEV void dw_tile(const JoinerArgs& a, int cm0, int cm1, int first, int v, int nj
     }
     return;
   }
+  // the partials the earlier chunks left for this thread's elements, loaded
+  // together before any store (ahead of the main loop for bf16, after it for
+  // fp32) rather than one load-add-store round trip per element
+  float old[Cfg::FM][Cfg::FN][4];
+  auto fetch_old = [&]() {
+#pragma unroll
+    for (int i = 0; i < Cfg::FM; ++i)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int j = j0 + tile_row<Cfg>(i, r);
+#pragma unroll
+        for (int jj = 0; jj < Cfg::FN; ++jj) {
+          const int vv = v0 + tile_col<Cfg>(jj);
+          old[i][jj][r] = (!first && j < J && vv < V) ? part[(size_t)j * V + vv] : 0.f;
+        }
+      }
+  };
+  if constexpr (BF) fetch_old();
   floatx4 acc[Cfg::FM][Cfg::FN];
   if constexpr (BF) {
-    const size_t tb = (size_t)a.chunk_rows * sizeof(typename Cfg::T);
-    TrSrcKC<Cfg> sa{make_rsrc(a.hT, tb * J), cm0, ke, j0, J, a.chunk_rows};
-    TrSrcKC<Cfg> sb{make_rsrc(a.dlT, tb * a.ldl), cm0, ke, v0, V, a.chunk_rows};
-    KCLoader<Cfg, Cfg::BM, TrSrcKC<Cfg>> la(sa);
-    KCLoader<Cfg, Cfg::BN, TrSrcKC<Cfg>> lb(sb);
-    gemm_mainloop<Cfg>(la, lb, kb, ke, smem, acc);
+    // h^T and d(logits)^T of the chunk (k = m - cm0 contiguous). Rows past
+    // mend hold zeros up to the 128-row tile end, so a chunk of 8 rows that
+    // crosses ke reads zeros there; split boundaries inside a chunk are K-step
+    // aligned.
+    const size_t tb = (size_t)a.chunk_rows * 2;
+    const LdsSrc<2> sa{make_rsrc(a.hT, tb * J), j0, J - j0, a.chunk_rows, cm0, ke};
+    const LdsSrc<2> sb{make_rsrc(a.dlT, tb * a.ldl), v0, V - v0, a.chunk_rows, cm0, ke};
+    gemm_mainloop_lds<Cfg>(sa, sb, kb, ke, lds, acc);
   } else {
     HbufSrcMNC<Cfg> sa{make_rsrc(a.hbuf, (size_t)a.chunk_rows * J * sizeof(typename Cfg::T)), cm0, ke, j0, J};
     DlSrcMNC<Cfg> sb{make_rsrc(a.dl, (size_t)a.chunk_rows * a.ldl * sizeof(typename Cfg::T)), cm0, ke, v0, a.ldl};
     MNCLoader<Cfg, Cfg::BM, HbufSrcMNC<Cfg>> la(sa);
     MNCLoader<Cfg, Cfg::BN, DlSrcMNC<Cfg>, decltype(la)::NBLK> lb(sb);  // threads after A's blocks
-    gemm_mainloop<Cfg>(la, lb, kb, ke, smem, acc);
+    gemm_mainloop<Cfg>(la, lb, kb, ke, lds_stages<Cfg>(lds), acc);
+    fetch_old();
   }
+  wait_vmem();
 #pragma unroll
   for (int i = 0; i < Cfg::FM; ++i)
 #pragma unroll
@@ -1122,10 +1215,7 @@ DEV void dw_tile(const JoinerArgs& a, int cm0, int cm1, int first, int v, int nj
 #pragma unroll
       for (int jj = 0; jj < Cfg::FN; ++jj) {
         const int vv = v0 + tile_col<Cfg>(jj);
-        if (vv < V) {
-          float* q = part + (size_t)j * V + vv;
-          *q = first ? acc[i][jj][r] : *q + acc[i][jj][r];
-        }
+        if (vv < V) part[(size_t)j * V + vv] = first ? acc[i][jj][r] : old[i][jj][r] + acc[i][jj][r];
       }
     }
 }
@@ -1540,11 +1630,14 @@ int joiner_fwd_chunk_rows(int N, int T, int S, int J, int bf16) {
 
 bool joiner_fwd_uses_hbuf(int bf16) { return bf16 ? kFwdHbuf<true> : kFwdHbuf<false>; }
 
-// dW splits a chunk's rows into ranges of about max(J, V) rows, so that a dW
-// tile does about the work of a dh or recomputed-logits tile of the same
-// launch (their K is V or J): no block kind outlasts the others.
-int joiner_bwd_splits(int J, int V, int chunk_rows) {
-  const int target = J > V ? J : V;
+// dW splits a chunk's rows into ranges of about max(J, V) rows (fp32), so
+// that a dW tile does about the work of a dh or recomputed-logits tile of the
+// same launch (their K is V or J): no block kind outlasts the others. bf16
+// takes ranges twice as long: its dW tiles run at the rate of the others, the
+// launch still packs into the same number of tile rounds, and half as many
+// partials are written and re-read per chunk.
+int joiner_bwd_splits(int J, int V, int chunk_rows, int bf16) {
+  const int target = (J > V ? J : V) * (bf16 ? 2 : 1);
   int s = (chunk_rows + target / 2) / target;
   if (s < 1) s = 1;
   if (s > 32) s = 32;
@@ -1561,7 +1654,9 @@ int joiner_db_rows(int chunk_rows) {
 hipError_t launch_joiner_prep(const JoinerArgs& a, hipStream_t s) {
   {
     RNNT_PROF(s, "joiner_prep");
-    hipLaunchKernelGGL(joiner_prep_kernel, dim3(a.b.N * ((a.b.T * a.S + 255) / 256) + prep_wpad_blocks(a)), dim3(256), 0, s, a);
+    const int wpad_blocks = prep_wpad_blocks(a);
+    hipLaunchKernelGGL(joiner_prep_kernel, dim3(a.b.N * ((a.b.T * a.S + 255) / 256) + wpad_blocks + prep_wt_blocks(a)),
+                       dim3(256), 0, s, a, wpad_blocks);
   }
   return hipGetLastError();
 }
@@ -1591,12 +1686,11 @@ hipError_t launch_joiner_fwd(const JoinerArgs& a, hipStream_t s) {
     }
     const dim3 grid((cm1 - cm0 + 127) / 128, (a.V + 127) / 128);
     RNNT_PROF(s, "joiner_fwd");
-    // W rows (length V) are read in segments of 16 / KV elements
-    const int wm = host_seg_mode(a.V, a.bf16 ? 2 : 4, a.bf16);
+    // fp32 W rows (length V) are read in segments of 4 elements; bf16 reads
+    // the transposed copy, whose rows (length J) are whole 16-byte chunks
+    const int wm = host_seg_mode(a.V, 4, 0);
     if (a.bf16) {
-      if (wm == kSegVector) hipLaunchKernelGGL((joiner_fwd_kernel<true, kSegVector>), grid, dim3(kGemmThreads), 0, s, a, cm0, cm1);
-      else if (wm == kSegWords) hipLaunchKernelGGL((joiner_fwd_kernel<true, kSegWords>), grid, dim3(kGemmThreads), 0, s, a, cm0, cm1);
-      else hipLaunchKernelGGL((joiner_fwd_kernel<true, kSegElems>), grid, dim3(kGemmThreads), 0, s, a, cm0, cm1);
+      hipLaunchKernelGGL((joiner_fwd_kernel<true, kSegVector>), grid, dim3(kGemmThreads), 0, s, a, cm0, cm1);
     } else {
       if (wm == kSegVector) hipLaunchKernelGGL((joiner_fwd_kernel<false, kSegVector>), grid, dim3(kGemmThreads), 0, s, a, cm0, cm1);
       else hipLaunchKernelGGL((joiner_fwd_kernel<false, kSegWords>), grid, dim3(kGemmThreads), 0, s, a, cm0, cm1);
@@ -1685,19 +1779,15 @@ static hipError_t launch_bwd_gemms(const JoinerArgs& cur, const JoinerArgs& nxt,
   // and every launch of the recomputed path's pipeline as one kernel
   const char* name = (p.nD && !p.nL && !p.nW) ? "joiner_dh" : (p.nW && !p.nL && !p.nD) ? "joiner_dw" : "joiner_bwd";
   RNNT_PROF(s, name);
-  // segment modes of the W reads: the recomputed logits read W rows in
-  // segments of 16 / KV elements, dh reads them k-contiguous in KV (bf16 W
-  // with V not a multiple of 8: from its zero-padded copy, in 16-byte segments)
-  const int wm_f = host_seg_mode(V, cur.bf16 ? 2 : 4, cur.bf16);
-  const int wm_h = cur.wpad ? (int)kSegVector : host_seg_mode(V, cur.bf16 ? 8 : 4, cur.bf16);
   const dim3 g(blocks), t(kGemmThreads);
   if (cur.bf16) {
-    if (wm_h != kSegVector) return hipErrorInvalidValue;  // bf16 dh always reads W in 16-byte segments
-    if (wm_f == kSegVector) hipLaunchKernelGGL((joiner_bwd_gemm_kernel<true, kSegVector, kSegVector>), g, t, 0, s, cur, nxt, p);
-    else if (wm_f == kSegWords) hipLaunchKernelGGL((joiner_bwd_gemm_kernel<true, kSegWords, kSegVector>), g, t, 0, s, cur, nxt, p);
-    else hipLaunchKernelGGL((joiner_bwd_gemm_kernel<true, kSegElems, kSegVector>), g, t, 0, s, cur, nxt, p);
+    // every bf16 operand is read in 16-byte chunks (W through its transposed
+    // or zero-padded copies)
+    hipLaunchKernelGGL((joiner_bwd_gemm_kernel<true, kSegVector, kSegVector>), g, t, 0, s, cur, nxt, p);
   } else {
-    if (wm_f != wm_h) return hipErrorInvalidValue;  // both follow V % 4
+    // fp32 W rows are read in segments of 4 elements, by the recomputed
+    // logits across rows and by dh along them
+    const int wm_f = host_seg_mode(V, 4, 0);
     if (wm_f == kSegVector) hipLaunchKernelGGL((joiner_bwd_gemm_kernel<false, kSegVector, kSegVector>), g, t, 0, s, cur, nxt, p);
     else hipLaunchKernelGGL((joiner_bwd_gemm_kernel<false, kSegWords, kSegWords>), g, t, 0, s, cur, nxt, p);
   }

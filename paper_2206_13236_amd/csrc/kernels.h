@@ -144,6 +144,8 @@ struct JoinerArgs {
   void* dlT;           // ws chunk [ldl, chunk_rows] (bf16 only): d(logits) transposed for dW
   void* wpad;          // ws [J, ldl] bf16 or null: W with its rows padded by zeros to ldl elements, so
                        // that dh reads W in 16-byte segments when V is not a multiple of 8
+  void* wt;            // ws [V, J] bf16 or null: W transposed (k = j contiguous), the B operand of the
+                       // bf16 forward and recomputed logits, written by the prep kernel
   int chunk_rows;
   float* dpre;         // ws chunk [chunk_rows, J]: the chunk's d dec pieces, each in the row of its first row
   float* enc_part;     // ws [ceil(N*T*S/128), 2, J]: d enc pieces of frames cut by a 128-row tile
@@ -172,7 +174,7 @@ int joiner_bwd_chunk_rows(int N, int T, int S, int J, int V, int bf16, int reque
 int joiner_bwd_chunk_max_rows(int J, int V);
 int joiner_fwd_chunk_rows(int N, int T, int S, int J, int bf16);
 bool joiner_fwd_uses_hbuf(int bf16);
-int joiner_bwd_splits(int J, int V, int chunk_rows);
+int joiner_bwd_splits(int J, int V, int chunk_rows, int bf16);
 int joiner_db_rows(int chunk_rows);  // db partial rows of one chunk
 int joiner_nparts(int V);
 int joiner_ldl(int V);
