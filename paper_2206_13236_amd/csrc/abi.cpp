@@ -227,10 +227,10 @@ struct JoinerBwdWs {
   void* dlT[2];
   void* wpad;
   void* wt;
-  float* dpre;
+  float* dpre[2];
   float* enc_part;
-  void* hbuf[2];
-  void* hT[2];
+  void* hbuf[3];
+  void* hT[3];
   float* dw_part;
   float* db_part;
   int chunk_rows, splits, n_db_rows;
@@ -248,18 +248,21 @@ JoinerBwdWs joiner_bwd_layout(void* base, int N, int T, int S, int J, int V, int
   w.frame_nt = c.take<int>((size_t)N * T);
   w.frame_p = c.take<int>((size_t)N * T);
   w.rowinfo = c.take<int4>(M);
-  // two ring slots of chunk buffers: d(logits), its bf16 transpose, h, its bf16 transpose
+  // rings of chunk buffers: 2 slots of d(logits) and its bf16 transpose, 3
+  // of h and its bf16 transpose
   const size_t dl_elems = (size_t)w.chunk_rows * joiner_ldl(V);
   const size_t h_elems = (size_t)w.chunk_rows * J;
   for (int k = 0; k < 2; ++k) {
     w.dl[k] = bf16 ? (void*)c.take<uint16_t>(dl_elems) : (void*)c.take<float>(dl_elems);
     w.dlT[k] = bf16 ? (void*)c.take<uint16_t>(dl_elems) : nullptr;
+  }
+  for (int k = 0; k < 3; ++k) {
     w.hbuf[k] = bf16 ? (void*)c.take<uint16_t>(h_elems) : (void*)c.take<float>(h_elems);
     w.hT[k] = bf16 ? (void*)c.take<uint16_t>(h_elems) : nullptr;
   }
   w.wpad = (bf16 && V % 8 != 0) ? (void*)c.take<uint16_t>((size_t)J * joiner_ldl(V)) : nullptr;
   w.wt = bf16 ? (void*)c.take<uint16_t>((size_t)V * J) : nullptr;
-  w.dpre = c.take<float>((size_t)w.chunk_rows * J);
+  for (int k = 0; k < 2; ++k) w.dpre[k] = c.take<float>((size_t)w.chunk_rows * J);
   w.enc_part = c.take<float>((M + 127) / 128 * 2 * J);
   w.dw_part = c.take<float>((size_t)w.splits * J * V);
   w.db_part = c.take<float>((size_t)w.n_db_rows * V);
@@ -355,15 +358,20 @@ void set_joiner_bwd(JoinerArgs& a, const JoinerBwdWs& w, const float* lse, const
   a.dl = w.dl[0];
   a.dlT = w.dlT[0];
   a.hT = w.hT[0];
-  a.ring1[0] = w.hbuf[1];
-  a.ring1[1] = w.hT[1];
-  a.ring1[2] = w.dl[1];
-  a.ring1[3] = w.dlT[1];
+  for (int k = 0; k < 3; ++k) {
+    a.hring[k] = w.hbuf[k];
+    a.hTring[k] = w.hT[k];
+  }
+  for (int k = 0; k < 2; ++k) {
+    a.dlring[k] = w.dl[k];
+    a.dlTring[k] = w.dlT[k];
+    a.dpring[k] = w.dpre[k];
+  }
   a.wpad = w.wpad;
   a.wt = w.wt;
   a.ldl = joiner_ldl(a.V);
   a.chunk_rows = w.chunk_rows;
-  a.dpre = w.dpre;
+  a.dpre = w.dpre[0];
   a.enc_part = w.enc_part;
   a.hbuf = w.hbuf[0];
   a.dw_part = w.dw_part;

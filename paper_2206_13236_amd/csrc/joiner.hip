@@ -1220,36 +1220,6 @@ DEV void dw_tile(const JoinerArgs& a, int cm0, int cm1, int first, int v, int nj
     }
 }
 
-// The backward's GEMM kernel. Every tile kind runs in one kernel, each on
-// its own range of blocks, so that the recomputed logits of the next chunk
-// (L), dh of the current chunk (D) and its dW (W) share a launch: a chunk's
-// dh alone puts only one workgroup on each CU.
-struct BwdParts {
-  int nL, nLcol;   // blocks and column tiles of L (chunk [lm0, lm1) of `nxt`)
-  int nD, nDcol;   // blocks and column tiles of D (chunk [cm0, cm1) of `cur`)
-  int nW, nWj, nWv;  // blocks and (j, v) tiles per split of W (same chunk)
-  int lm0, lm1, cm0, cm1, first;
-  int write_h;     // D also leaves h for a later W (no h pass ran)
-};
-
-// Blocks in the order W, D, L: the dW tiles, the longest, start first.
-template <bool BF, int WMF, int WMH>
-__global__ __launch_bounds__(kGemmThreads, 4) void joiner_bwd_gemm_kernel(JoinerArgs cur, JoinerArgs nxt, BwdParts p) {
-  __shared__ __align__(16) unsigned char lds[kBwdLdsBytes];
-  int b = blockIdx.x;
-  if (b < p.nW) {
-    dw_tile<BF>(cur, p.cm0, p.cm1, p.first, b, p.nWj, p.nWv, lds);
-    return;
-  }
-  b -= p.nW;
-  if (b < p.nD) {
-    dh_tile<BF, WMH>(cur, p.cm0, p.cm1, b, p.nD, p.nDcol, lds, p.write_h != 0);
-    return;
-  }
-  b -= p.nD;
-  dlogits_tile<BF, WMF>(nxt, p.lm0, p.lm1, b, p.nL, p.nLcol, lds);
-}
-
 // The tail of the backward: dW and db summed from their partials, d enc and
 // d dec from their pieces. Four independent, latency-bound reductions, run as
 // one launch whose block ranges take one part each (d dec, d enc, dW, db), so
@@ -1372,18 +1342,23 @@ DEV void tail_enc_pieces(const JoinerArgs& a, int b) {
 // (0 in the chunk that holds the first row of u), so that the sum's order is
 // that of one pass over all tiles. The first chunk also writes the zero rows
 // (u > U_n, or u in no frame's band).
-DEV void tail_dec_pieces(const JoinerArgs& a, int b, int* sp, int cm0, int cm1) {
+DEV void tail_dec_pieces(const JoinerArgs& a, int b, int* sp, int cm0, int cm1, const float* dpre) {
+  const int nt = blockDim.x;
   const int T = a.b.T, U1 = a.b.U + 1, S = a.S, J = a.J, tpr = J / 4;
   const int n = b / U1, u = b - n * U1;
   int Tn, Un;
   utt_dims(a.b, n, Tn, Un);
   float4* out = reinterpret_cast<float4*>(a.dec_grad + ((size_t)n * U1 + u) * J);
-  if (u > Un) {
+  // No row of utterance n in the chunk (most blocks: an utterance spans one
+  // or two chunks): the first chunk zeroes the row, which the chunk holding
+  // the first row of u overwrites; later chunks have nothing to add.
+  const int off = a.frame_off[n];
+  if (u > Un || (size_t)a.frame_off[n + 1] * S <= (size_t)cm0 || (size_t)off * S >= (size_t)cm1) {
     if (cm0 == 0)
-      for (int g = threadIdx.x; g < tpr; g += kTailThreads) out[g] = make_float4(0.f, 0.f, 0.f, 0.f);
+      for (int g = threadIdx.x; g < tpr; g += nt) out[g] = make_float4(0.f, 0.f, 0.f, 0.f);
     return;
   }
-  for (int t = threadIdx.x; t < Tn; t += kTailThreads) sp[t] = a.ranges[((size_t)n * T + t) * S];
+  for (int t = threadIdx.x; t < Tn; t += nt) sp[t] = a.ranges[((size_t)n * T + t) * S];
   __syncthreads();
   // frames [t0, t1) whose band holds u
   int lo = 0, hi = Tn;
@@ -1400,7 +1375,6 @@ DEV void tail_dec_pieces(const JoinerArgs& a, int b, int* sp, int cm0, int cm1) 
     else lo = mid + 1;
   }
   const int t1 = lo;
-  const int off = a.frame_off[n];
   auto row_of = [&](int t) { return (off + t) * S + u - sp[t]; };
   // the first frame in [l, h] whose row of u is at least r (h + 1: none)
   auto first_at = [&](int l, int h, int r) {
@@ -1414,7 +1388,7 @@ DEV void tail_dec_pieces(const JoinerArgs& a, int b, int* sp, int cm0, int cm1) 
   };
   if (t1 <= t0) {
     if (cm0 == 0)
-      for (int g = threadIdx.x; g < tpr; g += kTailThreads) out[g] = make_float4(0.f, 0.f, 0.f, 0.f);
+      for (int g = threadIdx.x; g < tpr; g += nt) out[g] = make_float4(0.f, 0.f, 0.f, 0.f);
     return;
   }
   const int mend = min(cm1, a.frame_off[a.b.N] * S);
@@ -1422,9 +1396,9 @@ DEV void tail_dec_pieces(const JoinerArgs& a, int b, int* sp, int cm0, int cm1) 
   if (ta >= tb) return;
   const bool starts = row_of(t0) >= cm0;  // the chunk holds the first row of u
   const int rows = __builtin_amdgcn_readfirstlane(a.chunk_rows);  // keeps the resource scalar
-  const Rsrc dr = make_rsrc(a.dpre, (size_t)rows * J * sizeof(float));
+  const Rsrc dr = make_rsrc(dpre, (size_t)rows * J * sizeof(float));
   const int ia = row_of(ta) / kTileRows, ib = row_of(tb - 1) / kTileRows;
-  for (int g = threadIdx.x; g < tpr; g += kTailThreads) {
+  for (int g = threadIdx.x; g < tpr; g += nt) {
     float4 acc = starts ? make_float4(0.f, 0.f, 0.f, 0.f) : out[g];
     for (int i0 = ia; i0 <= ib; i0 += 8) {
       float4 v[8];
@@ -1458,7 +1432,7 @@ DEV void h_pass_f32(const JoinerArgs& a, const HPass& hp, int b) {
   const int M = a.frame_off[a.b.N] * a.S;
   const int mend = min(hp.cm1, M);
   const int cpr = a.J / 4;
-  const size_t i = (size_t)b * kTailThreads + threadIdx.x;
+  const size_t i = (size_t)b * blockDim.x + threadIdx.x;
   const int rr = (int)(i / cpr), c = (int)(i - (size_t)rr * cpr);
   const int m = hp.cm0 + rr;
   if (m >= mend) return;
@@ -1477,26 +1451,29 @@ DEV void h_pass_f32(const JoinerArgs& a, const HPass& hp, int b) {
   *reinterpret_cast<float4*>(reinterpret_cast<float*>(hp.h) + (size_t)rr * a.J + j) = make_float4(h[0], h[1], h[2], h[3]);
 }
 
-// bf16: a 64-row x 64-column tile per block through LDS, both layouts
-// written 16 bytes per thread.
+// bf16: a 64-row x 64-column tile per 256 threads (tid: the thread among
+// them; the two halves of a 512-thread block take two tiles) through LDS,
+// both layouts written 16 bytes per thread. Every thread of the block reaches
+// the barrier, with or without a tile (`active`).
 constexpr int kHTile = 64;
+constexpr int kHThreads = 256;
 static int h_pass_bf16_blocks(int rows, int J) {
   const int rt = (rows + CfgF::BM - 1) / CfgF::BM * (CfgF::BM / kHTile);  // to the 128-row tile end
   return rt * ((J + kHTile - 1) / kHTile);
 }
-DEV void h_pass_bf16(const JoinerArgs& a, const HPass& hp, int b, uint16_t (*tile)[kHTile + 8]) {
+DEV void h_pass_bf16(const JoinerArgs& a, const HPass& hp, int b, int tid, bool active, uint16_t (*tile)[kHTile + 8]) {
   const int M = a.frame_off[a.b.N] * a.S;
   const int mend = min(hp.cm1, M);
   const int ncj = (a.J + kHTile - 1) / kHTile;
   const int rt = b / ncj, jt = b - rt * ncj;
   const int r0 = rt * kHTile, j0 = jt * kHTile;  // rows (m - cm0), columns j
-  const int ty = threadIdx.x >> 3, tx = threadIdx.x & 7;
+  const int ty = tid >> 3, tx = tid & 7;
   const EncDec<uint16_t> ed(a);
 #pragma unroll
   for (int hh = 0; hh < 2; ++hh) {
     const int r = ty + 32 * hh, m = hp.cm0 + r0 + r, j = j0 + tx * 8;
     uint4 o = make_uint4(0, 0, 0, 0);
-    if (m < mend && j < a.J) {
+    if (active && m < mend && j < a.J) {
       const int4 info = a.rowinfo[m];
       if (info.w >= 0) {
         RawVec<uint16_t, 8> e, d;
@@ -1517,6 +1494,7 @@ DEV void h_pass_bf16(const JoinerArgs& a, const HPass& hp, int b, uint16_t (*til
     *reinterpret_cast<uint4*>(&tile[r][tx * 8]) = o;
   }
   __syncthreads();
+  if (!active) return;
 #pragma unroll
   for (int hh = 0; hh < 2; ++hh) {
     const int c = ty + 32 * hh;  // column within the tile: hT row
@@ -1544,7 +1522,7 @@ __global__ __launch_bounds__(kTailThreads) void joiner_tail_kernel(JoinerArgs a,
   __shared__ float red[kTailThreads / kDbCols][kDbCols];  // db blocks
   __shared__ uint16_t htile[BF ? kHTile : 1][kHTile + 8];  // bf16 h pass
   int b = blockIdx.x;
-  if (b < r.dec) { tail_dec_pieces(a, b, sp, r.cm0, r.cm1); return; }
+  if (b < r.dec) { tail_dec_pieces(a, b, sp, r.cm0, r.cm1, a.dpre); return; }
   b -= r.dec;
   if (b < r.enc) { tail_enc_pieces(a, b); return; }
   b -= r.enc;
@@ -1554,9 +1532,67 @@ __global__ __launch_bounds__(kTailThreads) void joiner_tail_kernel(JoinerArgs a,
   b -= r.dbsum;
   const HPass& hp = b < r.h0.blocks ? r.h0 : r.h1;
   if (b >= r.h0.blocks) b -= r.h0.blocks;
-  if constexpr (BF) h_pass_bf16(a, hp, b, htile);
+  if constexpr (BF) h_pass_bf16(a, hp, b, threadIdx.x, true, htile);
   else h_pass_f32(a, hp, b);
 }
+
+// The backward's GEMM kernel. Every block kind runs in one kernel, each on
+// its own range of blocks, so that the recomputed logits of the next chunk
+// (L), dh of the current chunk (D) and its dW (W) share a launch (a chunk's
+// dh alone puts only one workgroup on each CU), and so that the memory- and
+// latency-bound passes of the pipeline run in the slots the GEMM tiles leave
+// free at the end of the launch instead of as launches of their own: the h
+// pass of a later chunk (H) and the d dec pass of the previous chunk (E).
+struct BwdParts {
+  int nL, nLcol;   // blocks and column tiles of L (chunk [lm0, lm1) of `nxt`)
+  int nD, nDcol;   // blocks and column tiles of D (chunk [cm0, cm1) of `cur`)
+  int nW, nWj, nWv;  // blocks and (j, v) tiles per split of W (same chunk)
+  int lm0, lm1, cm0, cm1, first;
+  int write_h;     // D also leaves h for a later W (no h pass ran)
+  int nH;          // blocks of H (its HPass: chunk rows, target buffers; bf16: two 64 x 64 tiles a block)
+  HPass h;
+  int nE;          // blocks of E: one per (n, u) row of d dec, adding the pieces of chunk [ecm0, ecm1) in edpre
+  int ecm0, ecm1;
+  const float* edpre;
+};
+
+// Blocks in the order W, D, L, H, E: the dW tiles, the longest, start first.
+template <bool BF, int WMF, int WMH>
+__global__ __launch_bounds__(kGemmThreads, 4) void joiner_bwd_gemm_kernel(JoinerArgs cur, JoinerArgs nxt, BwdParts p) {
+  __shared__ __align__(16) unsigned char lds[kBwdLdsBytes];
+  int b = blockIdx.x;
+  if (b < p.nW) {
+    dw_tile<BF>(cur, p.cm0, p.cm1, p.first, b, p.nWj, p.nWv, lds);
+    return;
+  }
+  b -= p.nW;
+  if (b < p.nD) {
+    dh_tile<BF, WMH>(cur, p.cm0, p.cm1, b, p.nD, p.nDcol, lds, p.write_h != 0);
+    return;
+  }
+  b -= p.nD;
+  if (b < p.nL) {
+    dlogits_tile<BF, WMF>(nxt, p.lm0, p.lm1, b, p.nL, p.nLcol, lds);
+    return;
+  }
+  b -= p.nL;
+  if (b < p.nH) {
+    if constexpr (BF) {
+      static_assert(kGemmThreads == 2 * kHThreads, "two h tiles per block");
+      const int half = threadIdx.x / kHThreads, hb = 2 * b + half;
+      uint16_t (*tile)[kHTile + 8] = reinterpret_cast<uint16_t (*)[kHTile + 8]>(lds) + half * kHTile;
+      h_pass_bf16(cur, p.h, hb, threadIdx.x - half * kHThreads, hb < p.h.blocks, tile);
+    } else {
+      h_pass_f32(cur, p.h, b);
+    }
+    return;
+  }
+  b -= p.nH;
+  static_assert(kBwdLdsBytes >= 16384 * (int)sizeof(int), "p_t of one utterance (T <= 16384) in LDS");
+  tail_dec_pieces(cur, b, reinterpret_cast<int*>(lds), p.ecm0, p.ecm1, p.edpre);
+}
+
+
 
 // ranges[n,t,s] = s: every (t, u) of the lattice as a "band" of width U+1.
 __global__ __launch_bounds__(256) void full_ranges_kernel(int* ranges, size_t total, int S) {
@@ -1704,15 +1740,16 @@ hipError_t launch_joiner_fwd(const JoinerArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-// Joiner args for ring slot k % 2 of the recomputed path's chunk buffers.
+// Joiner args of chunk k's buffers in the recomputed path's rings: h (and
+// h^T) in slot k % 3, d(logits) (and its transpose) and the d dec pieces in
+// slot k % 2.
 static JoinerArgs ring_slot(const JoinerArgs& a, int k) {
   JoinerArgs c = a;
-  if (k & 1) {
-    c.hbuf = a.ring1[0];
-    c.hT = a.ring1[1];
-    c.dl = a.ring1[2];
-    c.dlT = a.ring1[3];
-  }
+  c.hbuf = a.hring[k % 3];
+  c.hT = a.hTring[k % 3];
+  c.dl = a.dlring[k % 2];
+  c.dlT = a.dlTring[k % 2];
+  c.dpre = a.dpring[k % 2];
   return c;
 }
 
@@ -1756,8 +1793,17 @@ static hipError_t launch_tail(const JoinerArgs& a, const TailRanges& tr, hipStre
 // A GEMM launch of the backward: L of chunk [lm0, lm1) (ring slot of
 // `nxt`), D and/or W of chunk [cm0, cm1) (slot of `cur`); an empty range or
 // a false flag skips its part.
+// The other block kinds a pipeline launch may carry: the h pass of a later
+// chunk (H) and the d dec pass of the previous one (E).
+struct BwdExtras {
+  const HPass* h = nullptr;
+  const JoinerArgs* dec = nullptr;  // the previous chunk's args (its d dec pieces, in its dpre)
+  int dcm0 = 0, dcm1 = 0;
+};
+
 static hipError_t launch_bwd_gemms(const JoinerArgs& cur, const JoinerArgs& nxt, int lm0, int lm1, int cm0,
-                                   int cm1, bool do_D, bool do_W, bool write_h, hipStream_t s) {
+                                   int cm1, bool do_D, bool do_W, bool write_h, hipStream_t s,
+                                   const BwdExtras& x = BwdExtras()) {
   const int V = cur.V, J = cur.J;
   BwdParts p{};
   p.lm0 = lm0;
@@ -1773,7 +1819,18 @@ static hipError_t launch_bwd_gemms(const JoinerArgs& cur, const JoinerArgs& nxt,
   p.nWj = (J + 127) / 128;
   p.nWv = (V + 127) / 128;
   p.nW = (do_W && cm1 > cm0) ? p.nWj * p.nWv * cur.splits : 0;
-  const int blocks = p.nL + p.nD + p.nW;
+  if (x.h && x.h->cm1 > x.h->cm0) {
+    p.h = *x.h;
+    p.nH = cur.bf16 ? (x.h->blocks + 1) / 2
+                    : (int)(((size_t)(x.h->cm1 - x.h->cm0) * (J / 4) + kGemmThreads - 1) / kGemmThreads);
+  }
+  if (x.dec && x.dcm1 > x.dcm0) {
+    p.nE = (cur.b.U + 1) * cur.b.N;
+    p.ecm0 = x.dcm0;
+    p.ecm1 = x.dcm1;
+    p.edpre = x.dec->dpre;
+  }
+  const int blocks = p.nL + p.nD + p.nW + p.nH + p.nE;
   if (blocks == 0) return hipSuccess;
   // profiling names: the stored-logits path's separate dh and dW launches,
   // and every launch of the recomputed path's pipeline as one kernel
@@ -1831,14 +1888,18 @@ hipError_t launch_joiner_bwd(const JoinerArgs& a, hipStream_t s) {
     if (e != hipSuccess) return e;
   }
   if (a.logits_in) return launch_joiner_bwd_stored(a, s);
-  // Recomputed logits, software-pipelined over the chunks with two ring
-  // slots of chunk buffers (h, d(logits) and their transposes):
+  // Recomputed logits, software-pipelined over the chunks with rings of
+  // chunk buffers (h and h^T: 3 slots; d(logits), its transpose and the d dec
+  // pieces: 2 slots):
   //   tail{H(0), H(1)}; gemm{L(0)} (or chunk 0 streamed from the head);
-  //   for each chunk k: gemm{L(k+1), D(k), W(k)}; tail{dec(k), H(k+2)}
+  //   for each chunk k: gemm{W(k), D(k), L(k+1), H(k+2), E(k-1)};
+  //   tail{E(last), d enc, dW and db sums}
   // (H: h pass, L: recomputed logits and d(logits), D: dh and the d enc /
-  // d dec pieces, W: dW, dec: the chunk's d dec pass; the last tail also sums
-  // d enc, dW and db). Every launch's reads were written by earlier launches
-  // on the stream, and a slot is rewritten only after its last reader.
+  // d dec pieces, W: dW, E: a chunk's d dec pass). Every launch's reads were
+  // written by earlier launches on the stream; within a launch, H writes the
+  // h slot of chunk k+2 while W and L read those of chunks k and k+1, L
+  // writes the d(logits) slot of chunk k+1 while D and W read chunk k's, and
+  // E reads chunk k-1's pieces while D writes chunk k's.
   const int nch = (mmax + C - 1) / C;
   auto lo = [&](int k) { return k * C; };
   auto hi = [&](int k) { return (k + 1) * C < mmax ? (k + 1) * C : mmax; };
@@ -1869,13 +1930,24 @@ hipError_t launch_joiner_bwd(const JoinerArgs& a, hipStream_t s) {
     e = launch_bwd_gemms(ring_slot(a, 0), ring_slot(a, 0), lo(0), hi(0), 0, 0, false, false, false, s);
   }
   for (int k = 0; k < nch && e == hipSuccess; ++k) {
-    const JoinerArgs cur = ring_slot(a, k), nxt = ring_slot(a, k + 1);
+    const JoinerArgs cur = ring_slot(a, k), nxt = ring_slot(a, k + 1), prev = ring_slot(a, k > 0 ? k - 1 : 0);
     const bool more = k + 1 < nch;
-    e = launch_bwd_gemms(cur, nxt, more ? lo(k + 1) : 0, more ? hi(k + 1) : 0, lo(k), hi(k), true, true, false, s);
-    if (e != hipSuccess) break;
-    TailRanges tr = tail_ranges(cur, lo(k), hi(k), k == nch - 1);
-    if (k + 2 < nch) tr.h0 = h_pass(ring_slot(a, k + 2), lo(k + 2), hi(k + 2));
-    e = launch_tail(cur, tr, s, k == nch - 1 ? "joiner_tail" : "joiner_dec");
+    BwdExtras x;
+    HPass hp{};
+    if (k + 2 < nch) {
+      hp = h_pass(ring_slot(a, k + 2), lo(k + 2), hi(k + 2));
+      x.h = &hp;
+    }
+    if (k >= 1) {
+      x.dec = &prev;
+      x.dcm0 = lo(k - 1);
+      x.dcm1 = hi(k - 1);
+    }
+    e = launch_bwd_gemms(cur, nxt, more ? lo(k + 1) : 0, more ? hi(k + 1) : 0, lo(k), hi(k), true, true, false, s, x);
+  }
+  if (e == hipSuccess) {
+    const JoinerArgs last = ring_slot(a, nch - 1);
+    e = launch_tail(last, tail_ranges(last, lo(nch - 1), hi(nch - 1), true), s, "joiner_tail");
   }
   return e;
 }

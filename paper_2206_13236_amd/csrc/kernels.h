@@ -152,7 +152,11 @@ struct JoinerArgs {
   void* hbuf;          // ws chunk [chunk_rows, J] (f32 or bf16): h = tanh(enc + dec) of the chunk's rows
                        // (written by an h pass, or by dh when the logits were stored)
   void* hT;            // ws chunk [J, chunk_rows] (bf16 only): h transposed, the dW operand
-  void* ring1[4];      // the second ring slot of the recomputed backward: hbuf, hT, dl, dlT
+  void* hring[3];      // the recomputed backward's rings of chunk buffers: hbuf and hT of 3 slots,
+  void* hTring[3];     //   dl and dlT of 2, dpre of 2 (the fields above are those of slot 0)
+  void* dlring[2];
+  void* dlTring[2];
+  float* dpring[2];
   float* dw_part;      // ws [splits, J, V]
   int splits;
   float* db_part;      // ws [n_db_rows, V]: column sums per row group of a chunk, summed over the chunks
