@@ -591,6 +591,47 @@ __global__ __launch_bounds__(256) void joiner_combine_kernel(JoinerArgs a) {
   a.lse[i] = l;
 }
 
+// The same for wide vocabularies (more than kCombineSerialParts slices of 64
+// columns): one wave per output, lanes over the slices (coalesced reads), the
+// max and the sum each by a lane-ordered pass and a fixed butterfly, so the
+// result does not depend on scheduling.
+constexpr int kCombineSerialParts = 16;
+__global__ __launch_bounds__(256) void joiner_combine_wide_kernel(JoinerArgs a) {
+  const int T = a.b.T, S = a.S, lane = threadIdx.x & 63;
+  const size_t total = (size_t)a.b.N * T * S;
+  const size_t i = (size_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (i >= total) return;
+  const int n = (int)(i / ((size_t)T * S));
+  const int rem = (int)(i - (size_t)n * T * S);
+  const int t = rem / S, s = rem - t * S;
+  int Tn, Un;
+  utt_dims(a.b, n, Tn, Un);
+  float px = kNegInfF, py = kNegInfF, l = 0.f;
+  if (t < Tn) {
+    const int m = (a.frame_off[n] + t) * S + s;
+    const int4 info = a.rowinfo[m];
+    if (info.w >= 0) {
+      const float2* pp = a.part + (size_t)m * a.nparts;
+      float M = kNegInfF;
+      for (int p = lane; p < a.nparts; p += 64) M = fmaxf(M, pp[p].x);
+#pragma unroll
+      for (int off = 32; off >= 1; off >>= 1) M = fmaxf(M, __shfl_xor(M, off, 64));
+      float sum = 0.f;
+      for (int p = lane; p < a.nparts; p += 64) sum += pp[p].y * __expf(pp[p].x - M);
+#pragma unroll
+      for (int off = 32; off >= 1; off >>= 1) sum += __shfl_xor(sum, off, 64);
+      l = M + __logf(sum);
+      py = a.blk[m] - l;
+      px = (info.z >= 0) ? a.tgt[m] - l : (info.z == -2 ? __builtin_nanf("") : kNegInfF);
+    }
+  }
+  if (lane == 0) {
+    a.px[i] = px;
+    a.py[i] = py;
+    a.lse[i] = l;
+  }
+}
+
 // ---------------------------------------------------------------------------
 // LDS of the backward's GEMM tiles: the operand stages (also the epilogue's
 // C tile), then per-row info and per-row scalars of the row tile. One size
@@ -758,6 +799,17 @@ constexpr int kDlRows = 32;
 constexpr int kDlThreads = 256;
 constexpr int kDlInFlight = 16;  // rows per thread whose loads are issued together
 
+// Threads per row of a block (over the ng 4-column groups of a row); a block
+// takes tpr groups of kDlRows rows, and grid.y the ceil(ng / tpr) column
+// ranges, so that wide rows spread over many blocks.
+__host__ __device__ inline int dl_threads_per_row(int ng) {
+  return ng <= 64 ? 64 : (ng <= 128 ? 128 : (ng <= 256 ? 256 : kDlThreads));
+}
+static dim3 dl_grid(int rows, int ldl) {
+  const int ng = ldl / 4;
+  return dim3((unsigned)((rows + kDlRows - 1) / kDlRows), (unsigned)((ng + dl_threads_per_row(ng) - 1) / dl_threads_per_row(ng)));
+}
+
 template <bool BF>
 __global__ __launch_bounds__(kDlThreads) void joiner_dl_kernel(JoinerArgs a, int cm0, int cm1) {
   __shared__ int4 ri[kDlRows];
@@ -785,10 +837,11 @@ __global__ __launch_bounds__(kDlThreads) void joiner_dl_kernel(JoinerArgs a, int
   const float* __restrict__ lg = from_head ? a.head : a.logits_in;
   typename In<BF>::Cfg::T* __restrict__ dl = reinterpret_cast<typename In<BF>::Cfg::T*>(a.dl);
   const int ng = ldl / 4;
-  const int tpr = ng <= 64 ? 64 : (ng <= 128 ? 128 : (ng <= 256 ? 256 : kDlThreads));
+  const int tpr = dl_threads_per_row(ng);
   const int nrg = kDlThreads / tpr, rg = threadIdx.x / tpr, ct = threadIdx.x - rg * tpr;
   const bool vec = from_head || (V & 3) == 0;
-  for (int g0 = 0; g0 < ng; g0 += tpr) {
+  {
+    const int g0 = blockIdx.y * tpr;  // this block's column groups
     const int c = 4 * (g0 + ct);
     const bool gok = g0 + ct < ng;
     float cs[4] = {0.f, 0.f, 0.f, 0.f};
@@ -1735,7 +1788,10 @@ hipError_t launch_joiner_fwd(const JoinerArgs& a, hipStream_t s) {
   const size_t total = (size_t)a.b.N * a.b.T * a.S;
   {
     RNNT_PROF(s, "joiner_combine");
-    hipLaunchKernelGGL(joiner_combine_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, a);
+    if (a.nparts > kCombineSerialParts)
+      hipLaunchKernelGGL(joiner_combine_wide_kernel, dim3((unsigned)((total + 3) / 4)), dim3(256), 0, s, a);
+    else
+      hipLaunchKernelGGL(joiner_combine_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, a);
   }
   return hipGetLastError();
 }
@@ -1859,7 +1915,7 @@ static hipError_t launch_joiner_bwd_stored(const JoinerArgs& a, hipStream_t s) {
   hipError_t e = hipSuccess;
   for (int cm0 = 0; cm0 < mmax && e == hipSuccess; cm0 += a.chunk_rows) {
     const int cm1 = (cm0 + a.chunk_rows < mmax) ? cm0 + a.chunk_rows : mmax;
-    const dim3 gdl((cm1 - cm0 + kDlRows - 1) / kDlRows);
+    const dim3 gdl = dl_grid(cm1 - cm0, a.ldl);
     {
       RNNT_PROF(s, "joiner_dl");
       if (a.bf16) hipLaunchKernelGGL(joiner_dl_kernel<true>, gdl, dim3(kDlThreads), 0, s, a, cm0, cm1);
@@ -1913,7 +1969,7 @@ hipError_t launch_joiner_bwd(const JoinerArgs& a, hipStream_t s) {
     // chunk 0's logits were kept by the forward: stream them (and, for bf16,
     // transpose d(logits) for dW) instead of the one recomputation launch
     // the pipeline cannot fill
-    const dim3 gdl((hi(0) - lo(0) + kDlRows - 1) / kDlRows);
+    const dim3 gdl = dl_grid(hi(0) - lo(0), a.ldl);
     {
       RNNT_PROF(s, "joiner_dl");
       if (a.bf16) hipLaunchKernelGGL(joiner_dl_kernel<true>, gdl, dim3(kDlThreads), 0, s, a, lo(0), hi(0));
