@@ -88,7 +88,7 @@ DEV void lattice_fill_outside(DiagT* pxd, DiagT* pyd, int blk, int tid, int bs, 
   const uint32_t W = 64u * (uint32_t)R, DW = (uint32_t)(T + U1 - 1) * W;
   const uint32_t c = (uint32_t)(blk - n * per) * (uint32_t)bs + (uint32_t)tid;
   if (c >= DW) return;
-  const int d = (int)(c / W), slot = (int)(c % W);  // W is a power of two
+  const int d = (int)(c / W), slot = (int)(c % W);
   const int u = (slot & 63) * R + (slot >> 6), t = d - u;
   if (u >= U1 || t < 0 || t >= T) {
     const size_t j = (size_t)n * DW + c;
@@ -96,9 +96,11 @@ DEV void lattice_fill_outside(DiagT* pxd, DiagT* pyd, int blk, int tid, int bs, 
     pyd[j] = (DiagT)kNegInfD;
   }
 }
+// Rows of the lattice per lane: the fewest that hold U + 1 rows up to 6
+// (every padding row costs a log-add per diagonal step), then 8, 12 or 16.
 DEV int lattice_rows_per_lane_dev(int U1) {
   const int need = (U1 + 63) / 64;
-  return need <= 1 ? 1 : need <= 2 ? 2 : need <= 4 ? 4 : need <= 8 ? 8 : 16;
+  return need <= 6 ? (need < 1 ? 1 : need) : need <= 8 ? 8 : need <= 12 ? 12 : 16;
 }
 hipError_t launch_smoothing_stats(const SimpleArgs& a, hipStream_t s);
 hipError_t launch_simple_grads(const SimpleArgs& a, hipStream_t s);

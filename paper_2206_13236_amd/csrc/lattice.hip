@@ -328,7 +328,7 @@ int lattice_colblocks(int T) { return (T + kOccFrames - 1) / kOccFrames; }
 
 int lattice_rows_per_lane(int U1) {
   const int need = (U1 + 63) / 64;
-  return need <= 1 ? 1 : need <= 2 ? 2 : need <= 4 ? 4 : need <= 8 ? 8 : 16;
+  return need <= 6 ? (need < 1 ? 1 : need) : need <= 8 ? 8 : need <= 12 ? 12 : 16;
 }
 
 hipError_t launch_lattice_diag_copy(const SimpleArgs& a, hipStream_t s) {
@@ -348,8 +348,12 @@ hipError_t launch_lattice_recursion(const SimpleArgs& a, hipStream_t s) {
   switch (lattice_rows_per_lane(a.b.U + 1)) {
     case 1: hipLaunchKernelGGL((lattice_fb_kernel<1, 8>), dim3(a.b.N), dim3(128), 0, s, a); break;
     case 2: hipLaunchKernelGGL((lattice_fb_kernel<2, 8>), dim3(a.b.N), dim3(128), 0, s, a); break;
+    case 3: hipLaunchKernelGGL((lattice_fb_kernel<3, 8>), dim3(a.b.N), dim3(128), 0, s, a); break;
     case 4: hipLaunchKernelGGL((lattice_fb_kernel<4, 8>), dim3(a.b.N), dim3(128), 0, s, a); break;
+    case 5: hipLaunchKernelGGL((lattice_fb_kernel<5, 6>), dim3(a.b.N), dim3(128), 0, s, a); break;
+    case 6: hipLaunchKernelGGL((lattice_fb_kernel<6, 5>), dim3(a.b.N), dim3(128), 0, s, a); break;
     case 8: hipLaunchKernelGGL((lattice_fb_kernel<8, 4>), dim3(a.b.N), dim3(128), 0, s, a); break;
+    case 12: hipLaunchKernelGGL((lattice_fb_kernel<12, 3>), dim3(a.b.N), dim3(128), 0, s, a); break;
     default: hipLaunchKernelGGL((lattice_fb_kernel<16, 2>), dim3(a.b.N), dim3(128), 0, s, a); break;
   }
   return hipGetLastError();
@@ -361,8 +365,12 @@ hipError_t launch_lattice(const SimpleArgs& a, hipStream_t s) {
   switch (lattice_rows_per_lane(U1)) {
     case 1: launch_lattice_r<1, 8>(a, s); break;
     case 2: launch_lattice_r<2, 8>(a, s); break;
+    case 3: launch_lattice_r<3, 8>(a, s); break;
     case 4: launch_lattice_r<4, 8>(a, s); break;
+    case 5: launch_lattice_r<5, 6>(a, s); break;
+    case 6: launch_lattice_r<6, 5>(a, s); break;
     case 8: launch_lattice_r<8, 4>(a, s); break;
+    case 12: launch_lattice_r<12, 3>(a, s); break;
     default: launch_lattice_r<16, 2>(a, s); break;
   }
   return hipGetLastError();

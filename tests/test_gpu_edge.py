@@ -170,6 +170,27 @@ def test_long_transcript_near_the_lattice_limit():
     assert_close("lm_grad", host(got["lm_grad"]), s1["lm_grad"], atol=1e-4)
 
 
+@pytest.mark.parametrize("U_range,R", [((140, 150), 3), ((260, 300), 5), ((330, 370), 6), ((450, 500), 8),
+                                       ((705, 760), 12)])
+def test_simple_stage_at_every_lattice_width(U_range, R):
+    # the recursion's wave holds R lattice rows per lane (the fewest that
+    # hold U + 1 rows up to 6, then 8, 12, 16); ragged U inside each range
+    b = _small(seed=13, N=3, T_range=(30, 40), U_range=U_range, V=11, J=16, S=8)
+    need = -(-(b.U + 1) // 64)
+    assert R == (need if need <= 6 else 8 if need <= 8 else 12 if need <= 12 else 16)
+    say(f"[edge] simple stage, U = {b.U} ({R} rows per lane)")
+    batch = make_dev_batch(b)
+    sc = np.full(b.N, 0.5, np.float32)
+    got = P.rnnt_simple_loss(batch, b.V, dev_f32(b.am), dev_f32(b.lm), dev_f32(sc), want_grads=True)
+    torch.cuda.synchronize()
+    s1 = O.simple_stage(b.am, b.lm, b.symbols, b.t_len, b.u_len, b.wl.blank, scale=sc)
+    assert_close("loss", host(got["loss"]), s1["loss"], rtol=1e-5)
+    assert_close("px_occ", host(got["px_occ"]), s1["gx"], atol=1e-4)
+    assert_close("py_occ", host(got["py_occ"]), s1["gy"], atol=1e-4)
+    assert_close("am_grad", host(got["am_grad"]), s1["am_grad"], atol=1e-4)
+    assert_close("lm_grad", host(got["lm_grad"]), s1["lm_grad"], atol=1e-4)
+
+
 @pytest.mark.parametrize("alg,chunk", [("wavefront", 0), ("scan", 0), ("scan", 1), ("scan", 2), ("scan", 7)])
 def test_band_algorithms_on_a_mixed_batch(alg, chunk):
     # T_n = 1, U_n = 0, an infeasible utterance and ragged lengths in one
