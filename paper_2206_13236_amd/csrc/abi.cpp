@@ -237,7 +237,11 @@ struct JoinerBwdWs {
   size_t bytes;
 };
 
-JoinerBwdWs joiner_bwd_layout(void* base, int N, int T, int S, int J, int V, int bf16, int chunk_request = 0) {
+// stored_only: the caller always passes the logits (the unpruned loss), so
+// the backward streams them chunk by chunk through slot 0 and the rings of
+// the recomputed path's pipeline shrink to that one slot.
+JoinerBwdWs joiner_bwd_layout(void* base, int N, int T, int S, int J, int V, int bf16, int chunk_request = 0,
+                              bool stored_only = false) {
   Carve c(base);
   JoinerBwdWs w;
   const size_t M = (size_t)N * T * S;
@@ -249,20 +253,30 @@ JoinerBwdWs joiner_bwd_layout(void* base, int N, int T, int S, int J, int V, int
   w.frame_p = c.take<int>((size_t)N * T);
   w.rowinfo = c.take<int4>(M);
   // rings of chunk buffers: 2 slots of d(logits) and its bf16 transpose, 3
-  // of h and its bf16 transpose
+  // of h and its bf16 transpose (1 of each when stored_only)
   const size_t dl_elems = (size_t)w.chunk_rows * joiner_ldl(V);
   const size_t h_elems = (size_t)w.chunk_rows * J;
   for (int k = 0; k < 2; ++k) {
+    if (stored_only && k > 0) {
+      w.dl[k] = w.dl[0];
+      w.dlT[k] = w.dlT[0];
+      continue;
+    }
     w.dl[k] = bf16 ? (void*)c.take<uint16_t>(dl_elems) : (void*)c.take<float>(dl_elems);
     w.dlT[k] = bf16 ? (void*)c.take<uint16_t>(dl_elems) : nullptr;
   }
   for (int k = 0; k < 3; ++k) {
+    if (stored_only && k > 0) {
+      w.hbuf[k] = w.hbuf[0];
+      w.hT[k] = w.hT[0];
+      continue;
+    }
     w.hbuf[k] = bf16 ? (void*)c.take<uint16_t>(h_elems) : (void*)c.take<float>(h_elems);
     w.hT[k] = bf16 ? (void*)c.take<uint16_t>(h_elems) : nullptr;
   }
   w.wpad = (bf16 && V % 8 != 0) ? (void*)c.take<uint16_t>((size_t)J * joiner_ldl(V)) : nullptr;
   w.wt = bf16 ? (void*)c.take<uint16_t>((size_t)V * J) : nullptr;
-  for (int k = 0; k < 2; ++k) w.dpre[k] = c.take<float>((size_t)w.chunk_rows * J);
+  for (int k = 0; k < 2; ++k) w.dpre[k] = (stored_only && k > 0) ? w.dpre[0] : c.take<float>((size_t)w.chunk_rows * J);
   w.enc_part = c.take<float>((M + 127) / 128 * 2 * J);
   w.dw_part = c.take<float>((size_t)w.splits * J * V);
   w.db_part = c.take<float>((size_t)w.n_db_rows * V);
@@ -428,7 +442,7 @@ FullWs full_layout(void* base, int N, int T, int U, int J, int V, int bf16) {
   w.cpx = c.take<double>((size_t)N * lattice_colblocks(T) * S);
   w.cpy = c.take<double>((size_t)N * lattice_colblocks(T) * S);
   const size_t jf = joiner_fwd_layout(nullptr, N, T, S, J, V, bf16).bytes;
-  const size_t jb = joiner_bwd_layout(nullptr, N, T, S, J, V, bf16, full_chunk_rows(J, V, bf16)).bytes;
+  const size_t jb = joiner_bwd_layout(nullptr, N, T, S, J, V, bf16, full_chunk_rows(J, V, bf16), true).bytes;
   w.joiner = c.take<unsigned char>(jf > jb ? jf : jb);
   w.bytes = c.off;
   return w;
@@ -941,7 +955,7 @@ int rnnt_full_loss(const rnnt_batch* batch, int32_t J, int32_t V, int32_t dtype,
   if (e == hipSuccess) e = launch_lattice(la, s);
   // the joiner's backward on every (t, u)
   JoinerArgs jb = joiner_args(batch, S, J, V, dtype, enc, dec, W, bias, w.ranges);
-  set_joiner_bwd(jb, joiner_bwd_layout(w.joiner, batch->N, batch->T, S, J, V, bf, full_chunk_rows(J, V, bf)), w.lse,
+  set_joiner_bwd(jb, joiner_bwd_layout(w.joiner, batch->N, batch->T, S, J, V, bf, full_chunk_rows(J, V, bf), true), w.lse,
                  logits, w.gx, w.gy,
                  scale, enc_grad, dec_grad, W_grad, bias_grad, nullptr);
   if (e == hipSuccess) e = launch_joiner_prep(jb, s);
