@@ -224,9 +224,13 @@ DEV void load_exp4(const float* x, const float* mx, int row, int k, int V, bool 
     for (int i = 0; i < 4; ++i) r.x[i] = (valid && k + i < V) ? rowp[k + i] : kNegInfF;
   }
 }
+// exp(x - max) of a staged operand (x <= max: the value lies in [0, 1]) with
+// the hardware exp2: a few ulp, far below the contractions' fp32 rounding,
+// and a fraction of the full-precision expf's instructions on the staging
+// path that runs between the MFMAs.
 DEV void finish_exp4(const RawExp<4>& r, float (&v)[4]) {
 #pragma unroll
-  for (int i = 0; i < 4; ++i) v[i] = expf(r.x[i] - r.m);
+  for (int i = 0; i < 4; ++i) v[i] = __expf(r.x[i] - r.m);
 }
 DEV void load_plain4(const float* p, bool valid, RawF<4>& r) {
   if (valid) {
@@ -248,6 +252,12 @@ DEV void finish_plain4(const RawF<4>& r, float (&v)[4]) {
 // Normaliser contraction, per utterance: C[t][u] = sum_v Ea[t][v] El[u][v].
 // ---------------------------------------------------------------------------
 using NormCfg = GemmCfg<64, 64, 32, false>;
+// From this vocabulary on, the three contractions of the simple loss (K or N
+// = V) take the joiner's 128 x 128 tiles of 8 waves: enough tiles remain to
+// fill the chip, and a 32 x 32 or 16 x 32 wave tile spends most of its time
+// staging operands.
+constexpr int kSimpleBigV = 2048;
+using BigCfg = GemmCfg<128, 128, 32, false, 4, 2>;
 
 struct ExpRowsKC {  // rows r0 + row of x[.][V], value exp(x - max[row]); rows < lim
   using Raw = RawExp<4>;
@@ -261,8 +271,8 @@ struct ExpRowsKC {  // rows r0 + row of x[.][V], value exp(x - max[row]); rows <
 // Split over v into nsplit K ranges (the contraction alone has too few tiles
 // per batch to fill the chip); each writes its partial sums, and the
 // epilogue kernel adds them in split order.
-__global__ __launch_bounds__(256) void normalizer_kernel(SimpleArgs a) {
-  using Cfg = NormCfg;
+template <class Cfg>
+__global__ __launch_bounds__(Cfg::NT) void normalizer_kernel(SimpleArgs a) {
   __shared__ __align__(16) float smem[Cfg::SMEM_BYTES / sizeof(float)];
   const int n = blockIdx.z / a.nsplit, sk = blockIdx.z - n * a.nsplit;
   const int t0 = blockIdx.x * Cfg::BM, u0 = blockIdx.y * Cfg::BN;
@@ -409,8 +419,8 @@ struct ExpSrcMNC {  // B(k, col) = exp(x[k][c0+col] - mx[k]) for rows k < klim, 
   DEV void mnc_finish(const Raw& r, float (&v)[4]) const { finish_exp4(r, v); }
 };
 
-__global__ __launch_bounds__(256) void dam_kernel(SimpleArgs a) {
-  using Cfg = DamCfg;
+template <class Cfg>
+__global__ __launch_bounds__(Cfg::NT) void dam_kernel(SimpleArgs a) {
   __shared__ __align__(16) float smem[Cfg::SMEM_BYTES / sizeof(float)];
   const int n = blockIdx.z;
   const int t0 = blockIdx.x * Cfg::BM, v0 = blockIdx.y * Cfg::BN;
@@ -465,9 +475,11 @@ __global__ __launch_bounds__(256) void dam_kernel(SimpleArgs a) {
     constexpr int kChunk = kDamSymChunk;
     int* mu = reinterpret_cast<int*>(smem);  // [kChunk] listed u
     int* my = mu + kChunk;                   // [kChunk] their symbols
-    int* wcnt = my + kChunk;                 // [4] per-wave counts
-    float* g = reinterpret_cast<float*>(wcnt + 4);  // [kChunk][BM] gathered gx
-    static_assert((2 * kChunk + 4) * 4 + kChunk * Cfg::BM * 4 <= Cfg::SMEM_BYTES, "sparse chunk fits");
+    constexpr int kWaves = Cfg::NT / 64;
+    int* wcnt = my + kChunk;                 // [kWaves] per-wave counts
+    float* g = reinterpret_cast<float*>(wcnt + kWaves);  // [kChunk][BM] gathered gx
+    static_assert((2 * kChunk + kWaves) * 4 + kChunk * Cfg::BM * 4 <= Cfg::SMEM_BYTES, "sparse chunk fits");
+    static_assert(Cfg::NT >= kChunk, "one thread per symbol of a chunk");
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
     for (int c0 = 0; c0 < Un; c0 += kChunk) {
       __syncthreads();  // the previous user of smem is done
@@ -558,8 +570,8 @@ struct WtSrcMNC {  // A(u, t) = Wt[t][u]: global is [t][u], u-contiguous
 
 // Split over frames into lsplit K ranges; partial sums C[u][v] per split,
 // finished by dlm_epi_kernel.
-__global__ __launch_bounds__(256) void dlm_kernel(SimpleArgs a) {
-  using Cfg = DlmCfg;
+template <class Cfg>
+__global__ __launch_bounds__(Cfg::NT) void dlm_kernel(SimpleArgs a) {
   __shared__ __align__(16) float smem[Cfg::SMEM_BYTES / sizeof(float)];
   const int n = blockIdx.z / a.lsplit, sk = blockIdx.z - n * a.lsplit;
   const int u0 = blockIdx.x * Cfg::BM, v0 = blockIdx.y * Cfg::BN;
@@ -666,22 +678,35 @@ static int split_count(long long tiles, int K, int bk) {
   return sk < 1 ? 1 : (int)sk;
 }
 
+template <class Cfg>
+static int normalizer_splits_cfg(int N, int T, int U, int V) {
+  const long long tiles = (long long)N * ((T + Cfg::BM - 1) / Cfg::BM) * ((U + 1 + Cfg::BN - 1) / Cfg::BN);
+  return split_count(tiles, V, Cfg::BK);
+}
 int normalizer_splits(int N, int T, int U, int V) {
-  const long long tiles = (long long)N * ((T + NormCfg::BM - 1) / NormCfg::BM) * ((U + 1 + NormCfg::BN - 1) / NormCfg::BN);
-  return split_count(tiles, V, NormCfg::BK);
+  return V >= kSimpleBigV ? normalizer_splits_cfg<BigCfg>(N, T, U, V) : normalizer_splits_cfg<NormCfg>(N, T, U, V);
 }
 
+template <class Cfg>
+static int dlm_splits_cfg(int N, int T, int U, int V) {
+  const long long tiles = (long long)N * ((U + 1 + Cfg::BM - 1) / Cfg::BM) * ((V + Cfg::BN - 1) / Cfg::BN);
+  return split_count(tiles, T, Cfg::BK);
+}
 int dlm_splits(int N, int T, int U, int V) {
-  const long long tiles = (long long)N * ((U + 1 + DlmCfg::BM - 1) / DlmCfg::BM) * ((V + DlmCfg::BN - 1) / DlmCfg::BN);
-  return split_count(tiles, T, DlmCfg::BK);
+  return V >= kSimpleBigV ? dlm_splits_cfg<BigCfg>(N, T, U, V) : dlm_splits_cfg<DlmCfg>(N, T, U, V);
 }
 
 hipError_t launch_normalizer(const SimpleArgs& a, hipStream_t s) {
   const int T = a.b.T, U1 = a.b.U + 1;
-  dim3 grid((T + NormCfg::BM - 1) / NormCfg::BM, (U1 + NormCfg::BN - 1) / NormCfg::BN, a.b.N * a.nsplit);
   {
     RNNT_PROF(s, "normalizer");
-    hipLaunchKernelGGL(normalizer_kernel, grid, dim3(256), 0, s, a);
+    if (a.V >= kSimpleBigV) {
+      const dim3 grid((T + BigCfg::BM - 1) / BigCfg::BM, (U1 + BigCfg::BN - 1) / BigCfg::BN, a.b.N * a.nsplit);
+      hipLaunchKernelGGL(normalizer_kernel<BigCfg>, grid, dim3(BigCfg::NT), 0, s, a);
+    } else {
+      const dim3 grid((T + NormCfg::BM - 1) / NormCfg::BM, (U1 + NormCfg::BN - 1) / NormCfg::BN, a.b.N * a.nsplit);
+      hipLaunchKernelGGL(normalizer_kernel<NormCfg>, grid, dim3(NormCfg::NT), 0, s, a);
+    }
   }
   // tiles of the rectangle's nodes, then the cells of the diagonal-major copies
   const int FT = epi_tile_frames(lattice_rows_per_lane(U1));
@@ -716,18 +741,27 @@ hipError_t launch_simple_grads(const SimpleArgs& a, hipStream_t s) {
     hipLaunchKernelGGL(ac_colsum_kernel, dim3((V + 255) / 256, a.b.N), dim3(256), 0, s, a);
     hipLaunchKernelGGL(lm_s_kernel, dim3((a.b.N * U1 + 3) / 4), dim3(256), 0, s, a);
   }
+  const bool big = V >= kSimpleBigV;
   if (a.am_grad) {
-    dim3 grid((T + DamCfg::BM - 1) / DamCfg::BM, (V + DamCfg::BN - 1) / DamCfg::BN, a.b.N);
-    {
-      RNNT_PROF(s, "simple_dam");
-      hipLaunchKernelGGL(dam_kernel, grid, dim3(256), 0, s, a);
+    RNNT_PROF(s, "simple_dam");
+    if (big) {
+      const dim3 grid((T + BigCfg::BM - 1) / BigCfg::BM, (V + BigCfg::BN - 1) / BigCfg::BN, a.b.N);
+      hipLaunchKernelGGL(dam_kernel<BigCfg>, grid, dim3(BigCfg::NT), 0, s, a);
+    } else {
+      const dim3 grid((T + DamCfg::BM - 1) / DamCfg::BM, (V + DamCfg::BN - 1) / DamCfg::BN, a.b.N);
+      hipLaunchKernelGGL(dam_kernel<DamCfg>, grid, dim3(DamCfg::NT), 0, s, a);
     }
   }
   if (a.lm_grad) {
-    dim3 grid((U1 + DlmCfg::BM - 1) / DlmCfg::BM, (V + DlmCfg::BN - 1) / DlmCfg::BN, a.b.N * a.lsplit);
     {
       RNNT_PROF(s, "simple_dlm");
-      hipLaunchKernelGGL(dlm_kernel, grid, dim3(256), 0, s, a);
+      if (big) {
+        const dim3 grid((U1 + BigCfg::BM - 1) / BigCfg::BM, (V + BigCfg::BN - 1) / BigCfg::BN, a.b.N * a.lsplit);
+        hipLaunchKernelGGL(dlm_kernel<BigCfg>, grid, dim3(BigCfg::NT), 0, s, a);
+      } else {
+        const dim3 grid((U1 + DlmCfg::BM - 1) / DlmCfg::BM, (V + DlmCfg::BN - 1) / DlmCfg::BN, a.b.N * a.lsplit);
+        hipLaunchKernelGGL(dlm_kernel<DlmCfg>, grid, dim3(DlmCfg::NT), 0, s, a);
+      }
     }
     const size_t groups = (size_t)a.b.N * U1 * ((V + 3) / 4);
     {

@@ -191,6 +191,23 @@ def test_simple_stage_at_every_lattice_width(U_range, R):
     assert_close("lm_grad", host(got["lm_grad"]), s1["lm_grad"], atol=1e-4)
 
 
+def test_simple_stage_with_the_large_vocabulary_tiles():
+    # V >= 2048: normaliser, d am and d lm take 128 x 128 tiles; ragged T, U
+    # and V (2100 = 16 x 128 + 52), two tiles along T and along U + 1
+    b = _small(seed=14, N=3, T_range=(130, 150), U_range=(128, 140), V=2100, J=16, S=8)
+    say(f"[edge] simple stage, V = {b.V}, T = {b.T}, U = {b.U}")
+    batch = make_dev_batch(b)
+    sc = np.array([0.5, 1.0, 2.0], np.float32)
+    got = P.rnnt_simple_loss(batch, b.V, dev_f32(b.am), dev_f32(b.lm), dev_f32(sc), want_grads=True)
+    torch.cuda.synchronize()
+    s1 = O.simple_stage(b.am, b.lm, b.symbols, b.t_len, b.u_len, b.wl.blank, scale=sc)
+    assert_close("loss", host(got["loss"]), s1["loss"], rtol=1e-5)
+    assert_close("px_occ", host(got["px_occ"]), s1["gx"], atol=1e-4)
+    assert_close("py_occ", host(got["py_occ"]), s1["gy"], atol=1e-4)
+    assert_close("am_grad", host(got["am_grad"]), s1["am_grad"], atol=1e-4)
+    assert_close("lm_grad", host(got["lm_grad"]), s1["lm_grad"], atol=1e-4)
+
+
 @pytest.mark.parametrize("alg,chunk", [("wavefront", 0), ("scan", 0), ("scan", 1), ("scan", 2), ("scan", 7)])
 def test_band_algorithms_on_a_mixed_batch(alg, chunk):
     # T_n = 1, U_n = 0, an infeasible utterance and ragged lengths in one

@@ -45,6 +45,27 @@ def test_smoothed_simple_loss(w):
     assert_close("lm_grad", host(got["lm_grad"]), ref["lm_grad"], atol=1e-4)
 
 
+def test_smoothed_simple_loss_large_vocabulary():
+    # V >= 2048: the contractions take 128 x 128 tiles (V = 2100: a ragged
+    # last column tile)
+    a, bw = 0.25, 0.1
+    b = make_batch("bpe", seed=14, N=2, T_range=(100, 140), U_range=(20, 40), V=2100, J=32, S=4)
+    say(f"[smoothed] V = {b.V}")
+    sc = np.array([0.5, 2.0])
+    ref = O.smoothed_simple_stage(b.am, b.lm, b.symbols, b.t_len, b.u_len, b.wl.blank, a, bw, scale=sc)
+    batch = make_dev_batch(b)
+    got = P.rnnt_simple_loss(batch, b.V, dev_f32(b.am), dev_f32(b.lm), dev_f32(sc), want_logprobs=True,
+                             want_grads=True, lm_only_scale=a, am_only_scale=bw)
+    torch.cuda.synchronize()
+    assert_close("px", host(got["px"]), ref["px"], atol=5e-5)
+    assert_close("py", host(got["py"]), ref["py"], atol=5e-5)
+    assert_close("loss", host(got["loss"]), ref["loss"], rtol=1e-5)
+    assert_close("px_occ", host(got["px_occ"]), ref["gx"], atol=1e-4)
+    assert_close("py_occ", host(got["py_occ"]), ref["gy"], atol=1e-4)
+    assert_close("am_grad", host(got["am_grad"]), ref["am_grad"], atol=1e-4)
+    assert_close("lm_grad", host(got["lm_grad"]), ref["lm_grad"], atol=1e-4)
+
+
 def test_smoothed_backward_entry_equals_the_direct_gradients():
     b = _batch(seed=12)
     say("[smoothed] split backward")
