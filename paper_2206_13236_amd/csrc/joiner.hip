@@ -1395,78 +1395,100 @@ DEV void tail_enc_pieces(const JoinerArgs& a, int b) {
 // (0 in the chunk that holds the first row of u), so that the sum's order is
 // that of one pass over all tiles. The first chunk also writes the zero rows
 // (u > U_n, or u in no frame's band).
+// u rows of one utterance per d dec block: the block loads the utterance's
+// band starts once and its row groups (J / 4 threads each) take the rows.
+// Four rows are one pass of the GEMM launch's 512-thread blocks at J = 512;
+// longer groups serialise the latency-bound searches of several passes in
+// one block and measured slower (16 rows: +5% per step at BPE, +7% long).
+constexpr int kDecGroup = 4;
+__host__ __device__ inline int dec_blocks(int N, int U1) { return N * ((U1 + kDecGroup - 1) / kDecGroup); }
+
 DEV void tail_dec_pieces(const JoinerArgs& a, int b, int* sp, int cm0, int cm1, const float* dpre) {
   const int nt = blockDim.x;
   const int T = a.b.T, U1 = a.b.U + 1, S = a.S, J = a.J, tpr = J / 4;
-  const int n = b / U1, u = b - n * U1;
+  const int ng = (U1 + kDecGroup - 1) / kDecGroup;
+  const int n = b / ng, u0 = (b - n * ng) * kDecGroup, u1 = min(U1, u0 + kDecGroup);
   int Tn, Un;
   utt_dims(a.b, n, Tn, Un);
-  float4* out = reinterpret_cast<float4*>(a.dec_grad + ((size_t)n * U1 + u) * J);
+  // row groups: tpr threads per u row (all threads, looping, when a row is wider)
+  const int rgw = tpr < nt ? tpr : nt, nrg = nt / rgw;
+  const int rg = threadIdx.x / rgw, ct = threadIdx.x - rg * rgw;
+  auto zero_row = [&](int u) {
+    float4* out = reinterpret_cast<float4*>(a.dec_grad + ((size_t)n * U1 + u) * J);
+    for (int g = ct; g < tpr; g += rgw) out[g] = make_float4(0.f, 0.f, 0.f, 0.f);
+  };
   // No row of utterance n in the chunk (most blocks: an utterance spans one
-  // or two chunks): the first chunk zeroes the row, which the chunk holding
-  // the first row of u overwrites; later chunks have nothing to add.
+  // or two chunks): the first chunk zeroes the rows, which the chunk holding
+  // the first row of each u overwrites; later chunks have nothing to add.
   const int off = a.frame_off[n];
-  if (u > Un || (size_t)a.frame_off[n + 1] * S <= (size_t)cm0 || (size_t)off * S >= (size_t)cm1) {
-    if (cm0 == 0)
-      for (int g = threadIdx.x; g < tpr; g += nt) out[g] = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (u0 > Un || (size_t)a.frame_off[n + 1] * S <= (size_t)cm0 || (size_t)off * S >= (size_t)cm1) {
+    if (cm0 == 0 && rg < nrg)
+      for (int u = u0 + rg; u < u1; u += nrg) zero_row(u);
     return;
   }
   for (int t = threadIdx.x; t < Tn; t += nt) sp[t] = a.ranges[((size_t)n * T + t) * S];
   __syncthreads();
-  // frames [t0, t1) whose band holds u
-  int lo = 0, hi = Tn;
-  while (lo < hi) {
-    const int mid = (lo + hi) >> 1;
-    if (sp[mid] > u - S) hi = mid;
-    else lo = mid + 1;
-  }
-  const int t0 = lo;
-  hi = Tn;
-  while (lo < hi) {
-    const int mid = (lo + hi) >> 1;
-    if (sp[mid] > u) hi = mid;
-    else lo = mid + 1;
-  }
-  const int t1 = lo;
-  auto row_of = [&](int t) { return (off + t) * S + u - sp[t]; };
-  // the first frame in [l, h] whose row of u is at least r (h + 1: none)
-  auto first_at = [&](int l, int h, int r) {
-    int e = h + 1;
-    while (l < e) {
-      const int mid = (l + e) >> 1;
-      if (row_of(mid) >= r) e = mid;
-      else l = mid + 1;
-    }
-    return l;
-  };
-  if (t1 <= t0) {
-    if (cm0 == 0)
-      for (int g = threadIdx.x; g < tpr; g += nt) out[g] = make_float4(0.f, 0.f, 0.f, 0.f);
-    return;
-  }
+  if (rg >= nrg) return;
   const int mend = min(cm1, a.frame_off[a.b.N] * S);
-  const int ta = first_at(t0, t1 - 1, cm0), tb = first_at(ta, t1 - 1, mend);  // frames of u in the chunk
-  if (ta >= tb) return;
-  const bool starts = row_of(t0) >= cm0;  // the chunk holds the first row of u
   const int rows = __builtin_amdgcn_readfirstlane(a.chunk_rows);  // keeps the resource scalar
   const Rsrc dr = make_rsrc(dpre, (size_t)rows * J * sizeof(float));
-  const int ia = row_of(ta) / kTileRows, ib = row_of(tb - 1) / kTileRows;
-  for (int g = threadIdx.x; g < tpr; g += nt) {
-    float4 acc = starts ? make_float4(0.f, 0.f, 0.f, 0.f) : out[g];
-    for (int i0 = ia; i0 <= ib; i0 += 8) {
-      float4 v[8];
-#pragma unroll
-      for (int k = 0; k < 8; ++k) {
-        const int i = i0 + k;
-        const int t = (i > ia && i <= ib) ? first_at(ta, tb - 1, i * kTileRows) : ta;  // first frame of u in tile i
-        const uint32_t o = (uint32_t)(((size_t)(row_of(t) - cm0) * J + 4 * g) * sizeof(float));
-        const u32x4 w = __builtin_amdgcn_raw_buffer_load_b128(dr, (int)(i <= ib ? o : kOob), 0, 0);
-        v[k] = make_float4(__uint_as_float(w.x), __uint_as_float(w.y), __uint_as_float(w.z), __uint_as_float(w.w));
-      }
-#pragma unroll
-      for (int k = 0; k < 8; ++k) acc = f4add(acc, v[k]);
+  for (int u = u0 + rg; u < u1; u += nrg) {
+    if (u > Un) {
+      if (cm0 == 0) zero_row(u);
+      continue;
     }
-    out[g] = acc;
+    // frames [t0, t1) whose band holds u
+    int lo = 0, hi = Tn;
+    while (lo < hi) {
+      const int mid = (lo + hi) >> 1;
+      if (sp[mid] > u - S) hi = mid;
+      else lo = mid + 1;
+    }
+    const int t0 = lo;
+    hi = Tn;
+    while (lo < hi) {
+      const int mid = (lo + hi) >> 1;
+      if (sp[mid] > u) hi = mid;
+      else lo = mid + 1;
+    }
+    const int t1 = lo;
+    auto row_of = [&](int t) { return (off + t) * S + u - sp[t]; };
+    // the first frame in [l, h] whose row of u is at least r (h + 1: none)
+    auto first_at = [&](int l, int h, int r) {
+      int e = h + 1;
+      while (l < e) {
+        const int mid = (l + e) >> 1;
+        if (row_of(mid) >= r) e = mid;
+        else l = mid + 1;
+      }
+      return l;
+    };
+    if (t1 <= t0) {
+      if (cm0 == 0) zero_row(u);
+      continue;
+    }
+    const int ta = first_at(t0, t1 - 1, cm0), tb = first_at(ta, t1 - 1, mend);  // frames of u in the chunk
+    if (ta >= tb) continue;
+    const bool starts = row_of(t0) >= cm0;  // the chunk holds the first row of u
+    const int ia = row_of(ta) / kTileRows, ib = row_of(tb - 1) / kTileRows;
+    float4* out = reinterpret_cast<float4*>(a.dec_grad + ((size_t)n * U1 + u) * J);
+    for (int g = ct; g < tpr; g += rgw) {
+      float4 acc = starts ? make_float4(0.f, 0.f, 0.f, 0.f) : out[g];
+      for (int i0 = ia; i0 <= ib; i0 += 8) {
+        float4 v[8];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+          const int i = i0 + k;
+          const int t = (i > ia && i <= ib) ? first_at(ta, tb - 1, i * kTileRows) : ta;  // first frame of u in tile i
+          const uint32_t o = (uint32_t)(((size_t)(row_of(t) - cm0) * J + 4 * g) * sizeof(float));
+          const u32x4 w = __builtin_amdgcn_raw_buffer_load_b128(dr, (int)(i <= ib ? o : kOob), 0, 0);
+          v[k] = make_float4(__uint_as_float(w.x), __uint_as_float(w.y), __uint_as_float(w.z), __uint_as_float(w.w));
+        }
+#pragma unroll
+        for (int k = 0; k < 8; ++k) acc = f4add(acc, v[k]);
+      }
+      out[g] = acc;
+    }
   }
 }
 
@@ -1815,7 +1837,7 @@ static TailRanges tail_ranges(const JoinerArgs& a, int cm0, int cm1, bool last) 
   TailRanges tr{};
   tr.cm0 = cm0;
   tr.cm1 = cm1;
-  tr.dec = (cm1 > cm0) ? (a.b.U + 1) * a.b.N : 0;
+  tr.dec = (cm1 > cm0) ? dec_blocks(a.b.N, a.b.U + 1) : 0;
   tr.enc = last ? (a.b.N * a.b.T + R - 1) / R : 0;
   const bool wvec = JV % kWsumVec == 0 && (reinterpret_cast<uintptr_t>(a.W_grad) & 15) == 0;
   const size_t wthreads = wvec ? JV / kWsumVec : JV;
@@ -1881,7 +1903,7 @@ static hipError_t launch_bwd_gemms(const JoinerArgs& cur, const JoinerArgs& nxt,
                     : (int)(((size_t)(x.h->cm1 - x.h->cm0) * (J / 4) + kGemmThreads - 1) / kGemmThreads);
   }
   if (x.dec && x.dcm1 > x.dcm0) {
-    p.nE = (cur.b.U + 1) * cur.b.N;
+    p.nE = dec_blocks(cur.b.N, cur.b.U + 1);
     p.ecm0 = x.dcm0;
     p.ecm1 = x.dcm1;
     p.edpre = x.dec->dpre;
