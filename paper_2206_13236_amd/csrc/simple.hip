@@ -304,27 +304,39 @@ __global__ __launch_bounds__(Cfg::NT) void normalizer_kernel(SimpleArgs a) {
 }
 
 // Z = m_a + m_l + log(sum of the partials), px and py (Eqs. (1)-(2), (5)).
-// A block takes a tile of kEpiCells nodes: FT = kEpiCells / (64 R) frames of
-// one utterance times the 64 R rows of a lane-row of the lattice layout. The
-// nodes are formed in row-major order (coalesced reads of the partials and
-// writes of Z, px, py), their diagonal-major copies go to LDS, and are then
-// written diagonal by diagonal, so that the cells of one diagonal in the
-// tile (consecutive slots) are written together. The blocks after the tiles
-// fill the cells of the copies that no node of the rectangle maps to.
-constexpr int kEpiCells = 512;                 // threads per block: one node per thread
-constexpr int kEpiMaxCells = 64 * 16;          // a tile holds at least one lane-row of 64 R slots
-static_assert(kEpiCells <= kEpiMaxCells, "tile buffer");
+// A block takes a tile of kEpiTileCells cells: FT = kEpiTileCells / (64 R)
+// frames of one utterance times the 64 R slots of a row of the lattice
+// layout, kEpiNodes per thread with all their loads issued together (the
+// kernel is a chain of two dependent load rounds: partial sums, offsets and
+// symbols, then the am / lm values at the symbols). The nodes are formed in
+// row-major order (coalesced reads of the partials and writes of Z, px,
+// py), their diagonal-major copies go to LDS, and are then written diagonal
+// by diagonal, so that the cells of one diagonal in the tile (consecutive
+// slots) are written together. The blocks after the tiles fill the cells of
+// the copies that no node of the rectangle maps to, kEpiNodes cells per
+// thread. Small lattices take one node per thread (enough blocks to fill the
+// chip), those of more than kEpiWideNodes nodes four.
+constexpr int kEpiThreads = 512;
+constexpr long long kEpiWideNodes = 1 << 20;
+__host__ __device__ inline int epi_tile_frames(int R, int nodes) {
+  const int f = kEpiThreads * nodes / (64 * R);
+  return f > 1 ? f : 1;
+}
+static int epi_nodes(int N, int T, int U1) { return (long long)N * T * U1 > kEpiWideNodes ? 4 : 1; }
 
-__host__ __device__ inline int epi_tile_frames(int R) { return kEpiCells / (64 * R) > 1 ? kEpiCells / (64 * R) : 1; }
-
-__global__ __launch_bounds__(kEpiCells) void normalizer_epi_kernel(SimpleArgs a) {
-  __shared__ double tx[kEpiMaxCells], ty[kEpiMaxCells];  // [frame of the tile][slot]
+template <int kEpiNodes>
+__global__ __launch_bounds__(kEpiThreads) void normalizer_epi_kernel(SimpleArgs a) {
+  constexpr int kEpiTileCells = kEpiThreads * kEpiNodes < 64 * 16 ? 64 * 16 : kEpiThreads * kEpiNodes;
+  __shared__ double tx[kEpiTileCells], ty[kEpiTileCells];  // [frame of the tile][slot]
   const int T = a.b.T, U1 = a.b.U + 1, V = a.V;
-  const int R = lattice_rows_per_lane_dev(U1), W = 64 * R, FT = epi_tile_frames(R);
+  const int R = lattice_rows_per_lane_dev(U1), W = 64 * R, FT = epi_tile_frames(R, kEpiNodes);
   const int tiles_per_utt = (T + FT - 1) / FT;
   const int tile_blocks = a.b.N * tiles_per_utt;
   if ((int)blockIdx.x >= tile_blocks) {
-    lattice_fill_outside(a.pxd, a.pyd, (int)blockIdx.x - tile_blocks, threadIdx.x, kEpiCells, T, U1, R);
+#pragma unroll
+    for (int k = 0; k < kEpiNodes; ++k)
+      lattice_fill_outside(a.pxd, a.pyd, (int)blockIdx.x - tile_blocks, threadIdx.x + k * kEpiThreads,
+                           kEpiThreads * kEpiNodes, T, U1, R);
     return;
   }
   const int n = blockIdx.x / tiles_per_utt, t0 = (blockIdx.x - n * tiles_per_utt) * FT;
@@ -332,49 +344,85 @@ __global__ __launch_bounds__(kEpiCells) void normalizer_epi_kernel(SimpleArgs a)
   int Tn, Un;
   utt_dims(a.b, n, Tn, Un);
   const int blank = a.b.blank;
-  for (int c = threadIdx.x; c < FT * W; c += blockDim.x) {
-    const int tl = c / W, u = c - tl * W, t = t0 + tl;
+  const bool smooth = a.lm_only != 0.f || a.am_only != 0.f;
+  // round 1: partial sums, row offsets and symbols of the thread's nodes
+  static_assert(kEpiNodes == 1 || kEpiThreads * kEpiNodes >= 64 * 16, "a tile holds at least one frame");
+  for (int c0 = 0; c0 < FT * W; c0 += kEpiThreads * kEpiNodes) {
+  int tl[kEpiNodes], uu[kEpiNodes], yy[kEpiNodes];
+  bool cell[kEpiNodes], node[kEpiNodes];
+  size_t idx[kEpiNodes];
+  float sm[kEpiNodes], ma[kEpiNodes], ml[kEpiNodes];
+#pragma unroll
+  for (int k = 0; k < kEpiNodes; ++k) {
+    const int c = c0 + threadIdx.x + k * kEpiThreads;
+    tl[k] = c / W;
+    uu[k] = c - tl[k] * W;
+    const int t = t0 + tl[k], u = uu[k];
+    cell[k] = tl[k] < FT && u < U1 && t < T;  // FT * W may fall short of the tile's cells
+    node[k] = cell[k] && t < Tn && u <= Un;
+    idx[k] = cell[k] ? ((size_t)n * T + t) * U1 + u : 0;
+    sm[k] = 0.f;
+    ma[k] = node[k] ? a.m_a[(size_t)n * T + t] : 0.f;
+    ml[k] = node[k] ? a.m_l[(size_t)n * U1 + u] : 0.f;
+    bool ok = true;
+    yy[k] = (node[k] && u < Un) ? symbol_at(a.b, n, u, V, ok) : 0;
+  }
+  for (int q0 = 0; q0 < a.nsplit; q0 += 4) {  // the split partials in order, loads of 4 per node issued together
+    float pv[kEpiNodes][4];
+#pragma unroll
+    for (int k = 0; k < kEpiNodes; ++k)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) pv[k][j] = (node[k] && q0 + j < a.nsplit) ? a.npart[(size_t)(q0 + j) * L + idx[k]] : 0.f;
+#pragma unroll
+    for (int k = 0; k < kEpiNodes; ++k)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) sm[k] += pv[k][j];
+  }
+  // round 2: the am and lm values at blank and at the symbol
+  float ab[kEpiNodes], lb[kEpiNodes], ay[kEpiNodes], ly[kEpiNodes];
+#pragma unroll
+  for (int k = 0; k < kEpiNodes; ++k) {
+    const float* amt = a.am + ((size_t)n * T + (node[k] ? t0 + tl[k] : 0)) * V;
+    const float* lmu = a.lm + ((size_t)n * U1 + (node[k] ? uu[k] : 0)) * V;
+    ab[k] = node[k] ? amt[blank] : 0.f;
+    lb[k] = node[k] ? lmu[blank] : 0.f;
+    ay[k] = node[k] ? amt[yy[k]] : 0.f;
+    ly[k] = node[k] ? lmu[yy[k]] : 0.f;
+  }
+#pragma unroll
+  for (int k = 0; k < kEpiNodes; ++k) {
+    const int t = t0 + tl[k], u = uu[k];
     double dx = kNegInfD, dy = kNegInfD;
-    if (u < U1 && t < T) {
-      const size_t idx = ((size_t)n * T + t) * U1 + u;
-      if (t >= Tn || u > Un) {
-        a.Z[idx] = 0.f;
-        a.px[idx] = kNegInfF;
-        a.py[idx] = kNegInfF;
+    if (cell[k]) {
+      if (!node[k]) {
+        a.Z[idx[k]] = 0.f;
+        a.px[idx[k]] = kNegInfF;
+        a.py[idx[k]] = kNegInfF;
       } else {
-        float sm = 0.f;  // the split partials in order, loads of 8 issued together
-        for (int q0 = 0; q0 < a.nsplit; q0 += 8) {
-          float pv[8];
-#pragma unroll
-          for (int k = 0; k < 8; ++k) pv[k] = (q0 + k < a.nsplit) ? a.npart[(size_t)(q0 + k) * L + idx] : 0.f;
-#pragma unroll
-          for (int k = 0; k < 8; ++k) sm += pv[k];
-        }
-        sm = (sm > FLT_MIN || sm != sm) ? sm : FLT_MIN;
-        const float z = a.m_a[(size_t)n * T + t] + a.m_l[(size_t)n * U1 + u] + logf(sm);
-        const float* amt = a.am + ((size_t)n * T + t) * V;
-        const float* lmu = a.lm + ((size_t)n * U1 + u) * V;
-        a.Z[idx] = z;
-        bool ok = true;
-        const int y = (u < Un) ? symbol_at(a.b, n, u, V, ok) : 0;
-        float py = amt[blank] + lmu[blank] - z;
-        float px = amt[y] + lmu[y] - z;
-        if (a.lm_only != 0.f || a.am_only != 0.f) {
+        const float s1 = (sm[k] > FLT_MIN || sm[k] != sm[k]) ? sm[k] : FLT_MIN;
+        const float z = ma[k] + ml[k] + logf(s1);
+        a.Z[idx[k]] = z;
+        float py = ab[k] + lb[k] - z;
+        float px = ay[k] + ly[k] - z;
+        if (smooth) {
           // smoothed joiner: c L_trivial + a L_lm + b L_acoustic (Sec. 3.3.1)
           const float cw = 1.f - a.lm_only - a.am_only;
           const float zl = a.Zlm[(size_t)n * U1 + u], za = a.Zac[(size_t)n * T + t];
           const float* la = a.lavg + (size_t)n * V;
-          py = cw * py + a.lm_only * (lmu[blank] - zl) + a.am_only * (amt[blank] + la[blank] - za);
-          px = cw * px + a.lm_only * (lmu[y] - zl) + a.am_only * (amt[y] + la[y] - za);
+          py = cw * py + a.lm_only * (lb[k] - zl) + a.am_only * (ab[k] + la[blank] - za);
+          px = cw * px + a.lm_only * (ly[k] - zl) + a.am_only * (ay[k] + la[yy[k]] - za);
         }
-        a.py[idx] = py;
-        a.px[idx] = (u < Un) ? px : kNegInfF;
+        a.py[idx[k]] = py;
+        a.px[idx[k]] = (u < Un) ? px : kNegInfF;
         dy = (double)py * kLog2e;
         dx = (u < Un) ? (double)px * kLog2e : kNegInfD;
       }
     }
-    tx[tl * W + lattice_slot(u, R)] = dx;
-    ty[tl * W + lattice_slot(u, R)] = dy;
+    if (tl[k] < FT) {
+      tx[tl[k] * W + lattice_slot(u, R)] = dx;
+      ty[tl[k] * W + lattice_slot(u, R)] = dy;
+    }
+  }
   }
   __syncthreads();
   // diagonal d = t0 + k holds the tile's nodes (t0 + FT-1-j', u = d - t) for
@@ -709,11 +757,14 @@ hipError_t launch_normalizer(const SimpleArgs& a, hipStream_t s) {
     }
   }
   // tiles of the rectangle's nodes, then the cells of the diagonal-major copies
-  const int FT = epi_tile_frames(lattice_rows_per_lane(U1));
-  const size_t blocks = (size_t)a.b.N * ((T + FT - 1) / FT) + (size_t)a.b.N * lattice_fill_blocks(T, a.b.U, kEpiCells);
+  const int nodes = epi_nodes(a.b.N, T, U1);
+  const int FT = epi_tile_frames(lattice_rows_per_lane(U1), nodes);
+  const size_t blocks =
+      (size_t)a.b.N * ((T + FT - 1) / FT) + (size_t)a.b.N * lattice_fill_blocks(T, a.b.U, kEpiThreads * nodes);
   {
     RNNT_PROF(s, "normalizer_epi");
-    hipLaunchKernelGGL(normalizer_epi_kernel, dim3((unsigned)blocks), dim3(kEpiCells), 0, s, a);
+    if (nodes == 4) hipLaunchKernelGGL(normalizer_epi_kernel<4>, dim3((unsigned)blocks), dim3(kEpiThreads), 0, s, a);
+    else hipLaunchKernelGGL(normalizer_epi_kernel<1>, dim3((unsigned)blocks), dim3(kEpiThreads), 0, s, a);
   }
   return hipGetLastError();
 }
