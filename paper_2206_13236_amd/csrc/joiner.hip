@@ -1631,11 +1631,19 @@ struct BwdParts {
   const float* edpre;
 };
 
-// Blocks in the order W, D, L, H, E: the dW tiles, the longest, start first.
+// Blocks in the order E, W, D, L, H: the d dec blocks first (short and
+// latency-bound; dispatched last they would run after the GEMM tiles and
+// lengthen the launch's tail), then the dW tiles, the longest.
 template <bool BF, int WMF, int WMH>
 __global__ __launch_bounds__(kGemmThreads, 4) void joiner_bwd_gemm_kernel(JoinerArgs cur, JoinerArgs nxt, BwdParts p) {
   __shared__ __align__(16) unsigned char lds[kBwdLdsBytes];
   int b = blockIdx.x;
+  if (b < p.nE) {
+    static_assert(kBwdLdsBytes >= 16384 * (int)sizeof(int), "p_t of one utterance (T <= 16384) in LDS");
+    tail_dec_pieces(cur, b, reinterpret_cast<int*>(lds), p.ecm0, p.ecm1, p.edpre);
+    return;
+  }
+  b -= p.nE;
   if (b < p.nW) {
     dw_tile<BF>(cur, p.cm0, p.cm1, p.first, b, p.nWj, p.nWv, lds);
     return;
@@ -1662,9 +1670,6 @@ __global__ __launch_bounds__(kGemmThreads, 4) void joiner_bwd_gemm_kernel(Joiner
     }
     return;
   }
-  b -= p.nH;
-  static_assert(kBwdLdsBytes >= 16384 * (int)sizeof(int), "p_t of one utterance (T <= 16384) in LDS");
-  tail_dec_pieces(cur, b, reinterpret_cast<int*>(lds), p.ecm0, p.ecm1, p.edpre);
 }
 
 
