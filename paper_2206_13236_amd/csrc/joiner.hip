@@ -48,6 +48,14 @@ using CfgF = GemmCfg<128, 128, 32, false, 4, 2>;
 // transposes, W and its transposed copy) straight into LDS
 using CfgB = LdsCfg<128, 128, 64, 4, 2>;
 using CfgBw = CfgB;
+// bf16 forward at wide vocabularies: 256 x 256 tiles of 16 waves (64 x 64
+// wave tiles, one workgroup per CU) read a third fewer operand bytes from
+// LDS per MFMA than the 32 x 64 wave tiles; measured 1015 against 831
+// TFLOP/s on the main loop at 6941 x 8000 x 768, slower where V gives few
+// column tiles (608 against 832 at 16384 x 512 x 512)
+using CfgBWide = LdsCfg<256, 256, 64, 4, 4>;
+constexpr int kFwdWideV = 2048;
+static_assert(CfgBWide::WN == 64, "the forward's partial log-sum-exp slices are 64 columns");
 static_assert(CfgF::NT == kGemmThreads && CfgB::NT == kGemmThreads, "joiner GEMM block size");
 static_assert(CfgF::WN == 64 && CfgB::WN == 64, "the forward's partial log-sum-exp slices are 64 columns");
 static_assert(CfgF::BM == CfgB::BM && CfgF::WGM == CfgB::WGM, "db partial rows per row tile");
@@ -439,51 +447,68 @@ __global__ __launch_bounds__(256) void joiner_prep_kernel(JoinerArgs a, int wpad
 
 // ---------------------------------------------------------------------------
 // h = tanh(enc + dec) of the rows [cm0, min(cm1, M)) into the chunk buffer
-// hbuf [rows, J] in the GEMM operand type (zero rows for absent slots): one
-// 16-byte group of J per thread.
+// hbuf [rows, J] in the GEMM operand type (zero rows for absent slots):
+// kHItems 16-byte groups of J per thread (consecutive threads, consecutive
+// groups), whose row info, then enc and dec loads, are issued together; the
+// batch's row count M is loaded beside the row info (rows past it hold no
+// row info and are skipped).
 // ---------------------------------------------------------------------------
+constexpr int kHItems = 4;
 template <bool BF>
 __global__ __launch_bounds__(256) void joiner_h_kernel(JoinerArgs a, int cm0, int cm1) {
   using TIn = typename In<BF>::T;
   constexpr int KV = 16 / (int)sizeof(TIn);
+  const int cpr = a.J / KV;
+  const size_t base = (size_t)blockIdx.x * (256 * kHItems) + threadIdx.x;
+  int rr[kHItems], jj[kHItems];
+  int4 info[kHItems];
+#pragma unroll
+  for (int k = 0; k < kHItems; ++k) {
+    const size_t i = base + (size_t)k * 256;
+    rr[k] = (int)(i / cpr);
+    jj[k] = (int)(i - (size_t)rr[k] * cpr) * KV;
+    // within the row info array (cm1 <= N*T*S); rows past M are masked below
+    info[k] = cm0 + rr[k] < cm1 ? a.rowinfo[cm0 + rr[k]] : make_int4(0, 0, -1, -1);
+  }
   const int M = a.frame_off[a.b.N] * a.S;
   const int mend = min(cm1, M);
-  const int cpr = a.J / KV;
-  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int rr = (int)(i / cpr), c = (int)(i - (size_t)rr * cpr);
-  const int m = cm0 + rr;
-  if (m >= mend) return;
-  const int4 info = a.rowinfo[m];
-  const int j = c * KV;
   const EncDec<TIn> ed(a);
-  RawVec<TIn, KV> e, d;
-  const int n = info.w >= 0 ? KV : 0;
-  raw_load(ed.enc, (uint32_t)(info.x + j) * sizeof(TIn), n, kSegVector, e);
-  raw_load(ed.dec, (uint32_t)(info.y + j) * sizeof(TIn), n, kSegVector, d);
-  float fe[KV], fd[KV], h[KV];
-  raw_to_float(e, fe);
-  raw_to_float(d, fd);
+  RawVec<TIn, KV> e[kHItems], d[kHItems];
 #pragma unroll
-  for (int q = 0; q < KV; ++q) h[q] = info.w >= 0 ? fast_tanh(fe[q] + fd[q]) : 0.f;
-  uint4 o;
-  if constexpr (BF) {
-    uint32_t w[4];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) w[q] = (uint32_t)f2bf(h[2 * q]) | ((uint32_t)f2bf(h[2 * q + 1]) << 16);
-    o = make_uint4(w[0], w[1], w[2], w[3]);
-  } else {
-    o = make_uint4(__float_as_uint(h[0]), __float_as_uint(h[1]), __float_as_uint(h[2]), __float_as_uint(h[3]));
+  for (int k = 0; k < kHItems; ++k) {
+    const int n = (cm0 + rr[k] < mend && info[k].w >= 0) ? KV : 0;
+    raw_load(ed.enc, (uint32_t)(info[k].x + jj[k]) * sizeof(TIn), n, kSegVector, e[k]);
+    raw_load(ed.dec, (uint32_t)(info[k].y + jj[k]) * sizeof(TIn), n, kSegVector, d[k]);
   }
-  *reinterpret_cast<uint4*>(reinterpret_cast<TIn*>(a.hbuf) + (size_t)rr * a.J + j) = o;
+#pragma unroll
+  for (int k = 0; k < kHItems; ++k) {
+    if (cm0 + rr[k] >= mend) continue;
+    float fe[KV], fd[KV], h[KV];
+    raw_to_float(e[k], fe);
+    raw_to_float(d[k], fd);
+#pragma unroll
+    for (int q = 0; q < KV; ++q) h[q] = info[k].w >= 0 ? fast_tanh(fe[q] + fd[q]) : 0.f;
+    uint4 o;
+    if constexpr (BF) {
+      uint32_t w[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) w[q] = (uint32_t)f2bf(h[2 * q]) | ((uint32_t)f2bf(h[2 * q + 1]) << 16);
+      o = make_uint4(w[0], w[1], w[2], w[3]);
+    } else {
+      o = make_uint4(__float_as_uint(h[0]), __float_as_uint(h[1]), __float_as_uint(h[2]), __float_as_uint(h[3]));
+    }
+    *reinterpret_cast<uint4*>(reinterpret_cast<TIn*>(a.hbuf) + (size_t)rr[k] * a.J + jj[k]) = o;
+  }
 }
 
 // ---------------------------------------------------------------------------
 // Forward GEMM + partial log-sum-exp over the rows [cm0, cm1) (h in hbuf)
 // ---------------------------------------------------------------------------
-template <bool BF, int WM>
-__global__ __launch_bounds__(kGemmThreads, 4) void joiner_fwd_kernel(JoinerArgs a, int cm0, int cm1) {
+template <bool BF, int WM, bool WIDE = false>
+__global__ __launch_bounds__(WIDE ? CfgBWide::NT : kGemmThreads, 4) void joiner_fwd_kernel(JoinerArgs a, int cm0, int cm1) {
   using TIn = typename In<BF>::T;
-  using Cfg = typename In<BF>::Cfg;
+  using Cfg = typename std::conditional<WIDE, CfgBWide, typename In<BF>::Cfg>::type;
+  static_assert(!WIDE || BF, "wide tiles for bf16");
   __shared__ __align__(16) typename Cfg::T smem[Cfg::SMEM_BYTES / sizeof(typename Cfg::T)];
   __shared__ int4 ri[Cfg::BM];
   const int M = a.frame_off[a.b.N] * a.S;
@@ -1785,7 +1810,7 @@ static int host_seg_mode(int row_len, int seg, int bf16) {
 
 hipError_t launch_joiner_h(const JoinerArgs& a, int cm0, int cm1, hipStream_t s) {
   const size_t groups = (size_t)(cm1 - cm0) * (a.J / (a.bf16 ? 8 : 4));
-  const dim3 grid((unsigned)((groups + 255) / 256));
+  const dim3 grid((unsigned)((groups + 256 * kHItems - 1) / (256 * kHItems)));
   RNNT_PROF(s, "joiner_h");
   if (a.bf16) hipLaunchKernelGGL(joiner_h_kernel<true>, grid, dim3(256), 0, s, a, cm0, cm1);
   else hipLaunchKernelGGL(joiner_h_kernel<false>, grid, dim3(256), 0, s, a, cm0, cm1);
@@ -1805,7 +1830,10 @@ hipError_t launch_joiner_fwd(const JoinerArgs& a, hipStream_t s) {
     // fp32 W rows (length V) are read in segments of 4 elements; bf16 reads
     // the transposed copy, whose rows (length J) are whole 16-byte chunks
     const int wm = host_seg_mode(a.V, 4, 0);
-    if (a.bf16) {
+    if (a.bf16 && a.V >= kFwdWideV) {
+      const dim3 gw((cm1 - cm0 + CfgBWide::BM - 1) / CfgBWide::BM, (a.V + CfgBWide::BN - 1) / CfgBWide::BN);
+      hipLaunchKernelGGL((joiner_fwd_kernel<true, kSegVector, true>), gw, dim3(CfgBWide::NT), 0, s, a, cm0, cm1);
+    } else if (a.bf16) {
       hipLaunchKernelGGL((joiner_fwd_kernel<true, kSegVector>), grid, dim3(kGemmThreads), 0, s, a, cm0, cm1);
     } else {
       if (wm == kSegVector) hipLaunchKernelGGL((joiner_fwd_kernel<false, kSegVector>), grid, dim3(kGemmThreads), 0, s, a, cm0, cm1);
