@@ -1648,6 +1648,7 @@ struct BwdParts {
   int nD, nDcol;   // blocks and column tiles of D (chunk [cm0, cm1) of `cur`)
   int nW, nWj, nWv;  // blocks and (j, v) tiles per split of W (same chunk)
   int lm0, lm1, cm0, cm1, first;
+  int d_first;     // D's tiles (K = V) are longer than W's (K = a split's rows): dispatched before them
   int write_h;     // D also leaves h for a later W (no h pass ran)
   int nH;          // blocks of H (its HPass: chunk rows, target buffers; bf16: two 64 x 64 tiles a block)
   HPass h;
@@ -1656,9 +1657,10 @@ struct BwdParts {
   const float* edpre;
 };
 
-// Blocks in the order E, W, D, L, H: the d dec blocks first (short and
-// latency-bound; dispatched last they would run after the GEMM tiles and
-// lengthen the launch's tail), then the dW tiles, the longest.
+// Blocks in the order E, then W and D (the kind with the longer K loop
+// first), L, H: the d dec blocks first (short and latency-bound; dispatched
+// last they would run after the GEMM tiles and lengthen the launch's tail),
+// then the longest GEMM tiles, so that the shorter ones fill in around them.
 template <bool BF, int WMF, int WMH>
 __global__ __launch_bounds__(kGemmThreads, 4) void joiner_bwd_gemm_kernel(JoinerArgs cur, JoinerArgs nxt, BwdParts p) {
   __shared__ __align__(16) unsigned char lds[kBwdLdsBytes];
@@ -1669,16 +1671,13 @@ __global__ __launch_bounds__(kGemmThreads, 4) void joiner_bwd_gemm_kernel(Joiner
     return;
   }
   b -= p.nE;
-  if (b < p.nW) {
-    dw_tile<BF>(cur, p.cm0, p.cm1, p.first, b, p.nWj, p.nWv, lds);
+  if (b < p.nW + p.nD) {
+    const int bd = p.d_first ? b : b - p.nW;  // index among the D blocks (negative: a W block)
+    if (bd >= 0 && bd < p.nD) dh_tile<BF, WMH>(cur, p.cm0, p.cm1, bd, p.nD, p.nDcol, lds, p.write_h != 0);
+    else dw_tile<BF>(cur, p.cm0, p.cm1, p.first, p.d_first ? b - p.nD : b, p.nWj, p.nWv, lds);
     return;
   }
-  b -= p.nW;
-  if (b < p.nD) {
-    dh_tile<BF, WMH>(cur, p.cm0, p.cm1, b, p.nD, p.nDcol, lds, p.write_h != 0);
-    return;
-  }
-  b -= p.nD;
+  b -= p.nW + p.nD;
   if (b < p.nL) {
     dlogits_tile<BF, WMF>(nxt, p.lm0, p.lm1, b, p.nL, p.nLcol, lds);
     return;
@@ -1774,11 +1773,12 @@ bool joiner_fwd_uses_hbuf(int bf16) { return bf16 ? kFwdHbuf<true> : kFwdHbuf<fa
 // dW splits a chunk's rows into ranges of about max(J, V) rows (fp32), so
 // that a dW tile does about the work of a dh or recomputed-logits tile of the
 // same launch (their K is V or J): no block kind outlasts the others. bf16
-// takes ranges twice as long: its dW tiles run at the rate of the others, the
-// launch still packs into the same number of tile rounds, and half as many
-// partials are written and re-read per chunk.
+// takes ranges four times as long: its dW tiles run at the rate of the
+// others, start first (the longest tiles of a launch do), and a quarter as
+// many partials are written and re-read per chunk (measured: long step
+// 0.818 -> 0.807 ms against twice as long; no change at the stress size).
 int joiner_bwd_splits(int J, int V, int chunk_rows, int bf16) {
-  const int target = (J > V ? J : V) * (bf16 ? 2 : 1);
+  const int target = (J > V ? J : V) * (bf16 ? 4 : 1);
   int s = (chunk_rows + target / 2) / target;
   if (s < 1) s = 1;
   if (s > 32) s = 32;
@@ -1930,6 +1930,11 @@ static hipError_t launch_bwd_gemms(const JoinerArgs& cur, const JoinerArgs& nxt,
   p.nWj = (J + 127) / 128;
   p.nWv = (V + 127) / 128;
   p.nW = (do_W && cm1 > cm0) ? p.nWj * p.nWv * cur.splits : 0;
+  {
+    const int bk = cur.bf16 ? CfgBw::BK : CfgF::BK;
+    const int per = ((cm1 - cm0 + cur.splits - 1) / cur.splits + bk - 1) / bk * bk;  // a split's rows (dw_tile)
+    p.d_first = cur.ldl > per;
+  }
   if (x.h && x.h->cm1 > x.h->cm0) {
     p.h = *x.h;
     p.nH = cur.bf16 ? (x.h->blocks + 1) / 2
