@@ -208,6 +208,16 @@ def test_simple_stage_with_the_large_vocabulary_tiles():
     assert_close("lm_grad", host(got["lm_grad"]), s1["lm_grad"], atol=1e-4)
 
 
+def test_step_with_the_wide_forward_tiles():
+    # bf16 at V >= 2048: the joiner forward takes 256 x 256 tiles of 16
+    # waves; ragged rows (M = S sum T_n is no multiple of 256) and columns
+    # (2100 = 8 x 256 + 52); every output of the step against the oracle
+    b = _small(seed=15, N=3, T_range=(40, 60), U_range=(10, 20), V=2100, J=64, S=5, joiner_dtype="bf16")
+    say(f"[edge] step with the wide forward tiles, V = {b.V}, M = {5 * int(b.t_len.sum())}")
+    out = run_step(b, 5)
+    check_step(out, oracle_step(b, 5), b, 5)
+
+
 @pytest.mark.parametrize("alg,chunk", [("wavefront", 0), ("scan", 0), ("scan", 1), ("scan", 2), ("scan", 7)])
 def test_band_algorithms_on_a_mixed_batch(alg, chunk):
     # T_n = 1, U_n = 0, an infeasible utterance and ragged lengths in one
