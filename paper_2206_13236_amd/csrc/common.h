@@ -132,6 +132,29 @@ DEV double dpp_move_d(double v, double old) {
   return __hiloint2double(hi, lo);
 }
 
+// Max and sum over the 16 lanes of a DPP row (lanes 16 k .. 16 k + 15, the
+// lanes that share an MFMA output row), the result in every lane of the row:
+// the row rotated by 8, 4, 2 and 1 lanes (DPP row_ror) and folded in, one
+// VALU instruction per step instead of a permute through LDS. Each pairing
+// is commutative, so every lane of the row ends with the same bits.
+template <int N>
+DEV float dpp_row_ror(float v) {
+  static_assert(N >= 1 && N <= 15, "row rotation");
+  return __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(v), __float_as_int(v), 0x120 + N, 0xf, 0xf, false));
+}
+DEV float row16_max(float v) {
+  v = fmaxf(v, dpp_row_ror<8>(v));
+  v = fmaxf(v, dpp_row_ror<4>(v));
+  v = fmaxf(v, dpp_row_ror<2>(v));
+  return fmaxf(v, dpp_row_ror<1>(v));
+}
+DEV float row16_sum(float v) {
+  v += dpp_row_ror<8>(v);
+  v += dpp_row_ror<4>(v);
+  v += dpp_row_ror<2>(v);
+  return v + dpp_row_ror<1>(v);
+}
+
 // Wave-wide max and sum of doubles (fixed butterfly order: deterministic).
 DEV double wave_max_d(double v) {
 #pragma unroll

@@ -559,16 +559,14 @@ __global__ __launch_bounds__(WIDE ? CfgBWide::NT : kGemmThreads, 4) void joiner_
         lg[j] = (col < V) ? acc[i][j][r] + bj[j] : kNegInfF;
         mx = fmaxf(mx, lg[j]);
       }
-#pragma unroll
-      for (int off = 8; off >= 1; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off, 64));
+      mx = row16_max(mx);
       float se = 0.f;
 #pragma unroll
       for (int j = 0; j < Cfg::FN; ++j) {
         const int col = v0 + tile_col<Cfg>(j);
         se += (col < V) ? __expf(lg[j] - mx) : 0.f;
       }
-#pragma unroll
-      for (int off = 8; off >= 1; off >>= 1) se += __shfl_xor(se, off, 64);
+      se = row16_sum(se);
       if (info.w >= 0) {
         const int m = m0 + row;
         if ((lane & 15) == 0 && slice < a.nparts) a.part[(size_t)m * a.nparts + slice] = make_float2(mx, se);
