@@ -155,18 +155,44 @@ DEV float row16_sum(float v) {
   return v + dpp_row_ror<1>(v);
 }
 
-// Wave-wide max and sum of doubles (fixed butterfly order: deterministic).
+// The same for doubles (two VGPRs moved per step).
+template <int N>
+DEV double dpp_row_ror_d(double v) {
+  static_assert(N >= 1 && N <= 15, "row rotation");
+  return dpp_move_d<0x120 + N>(v, v);
+}
+DEV double row16_max_d(double v) {
+  double o = dpp_row_ror_d<8>(v);
+  v = o > v ? o : v;
+  o = dpp_row_ror_d<4>(v);
+  v = o > v ? o : v;
+  o = dpp_row_ror_d<2>(v);
+  v = o > v ? o : v;
+  o = dpp_row_ror_d<1>(v);
+  return o > v ? o : v;
+}
+DEV double row16_sum_d(double v) {
+  v += dpp_row_ror_d<8>(v);
+  v += dpp_row_ror_d<4>(v);
+  v += dpp_row_ror_d<2>(v);
+  return v + dpp_row_ror_d<1>(v);
+}
+
+// Wave-wide max and sum of doubles in a fixed order (deterministic): within
+// each 16-lane row by DPP, then across the rows.
 DEV double wave_max_d(double v) {
+  v = row16_max_d(v);
 #pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) {
+  for (int off = 16; off <= 32; off <<= 1) {
     const double o = __shfl_xor(v, off, 64);
     v = o > v ? o : v;
   }
   return v;
 }
 DEV double wave_sum_d(double v) {
+  v = row16_sum_d(v);
 #pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
+  for (int off = 16; off <= 32; off <<= 1) v += __shfl_xor(v, off, 64);
   return v;
 }
 

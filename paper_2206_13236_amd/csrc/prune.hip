@@ -82,8 +82,15 @@ __global__ __launch_bounds__(256) void prune_score_kernel(BatchDev b, int S, con
       better(bs, bp, (acc != acc) ? kNegInfF : acc, q);
     }
   }
+  // the best (score, p) of the wave: within each 16-lane row by DPP
+  // rotations, then across the rows (a total order: any order of the
+  // comparisons selects the same pair)
+  better(bs, bp, dpp_row_ror<8>(bs), __float_as_int(dpp_row_ror<8>(__int_as_float(bp))));
+  better(bs, bp, dpp_row_ror<4>(bs), __float_as_int(dpp_row_ror<4>(__int_as_float(bp))));
+  better(bs, bp, dpp_row_ror<2>(bs), __float_as_int(dpp_row_ror<2>(__int_as_float(bp))));
+  better(bs, bp, dpp_row_ror<1>(bs), __float_as_int(dpp_row_ror<1>(__int_as_float(bp))));
 #pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) {
+  for (int off = 16; off <= 32; off <<= 1) {
     const float os = __shfl_xor(bs, off, 64);
     const int op = __shfl_xor(bp, off, 64);
     better(bs, bp, os, op);

@@ -437,16 +437,9 @@ __global__ __launch_bounds__(128) void scan_replay_kernel(BandArgs a) {
       ey = al + s_ey[o];
       ex = al + s_ex[o];
     }
-    // frame total over the row (butterfly within 16 lanes)
-    double mx = ey;
-#pragma unroll
-    for (int off = 8; off >= 1; off >>= 1) {
-      const double o = __shfl_xor(mx, off, 16);
-      mx = o > mx ? o : mx;
-    }
-    double sm = (ey != kNegInfD) ? (double)__builtin_amdgcn_exp2f((float)(ey - mx)) : 0.0;
-#pragma unroll
-    for (int off = 8; off >= 1; off >>= 1) sm += __shfl_xor(sm, off, 16);
+    // frame total over the row (the chunk's 16 lanes)
+    const double mx = row16_max_d(ey);
+    const double sm = row16_sum_d((ey != kNegInfD) ? (double)__builtin_amdgcn_exp2f((float)(ey - mx)) : 0.0);
     const double Lt = mx + log2(sm);
     if (s < S) {
       float gxv = 0.f, gyv = 0.f;
