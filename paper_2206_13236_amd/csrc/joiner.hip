@@ -616,8 +616,8 @@ __global__ __launch_bounds__(256) void joiner_combine_kernel(JoinerArgs a) {
 
 // The same for wide vocabularies (more than kCombineSerialParts slices of 64
 // columns): one wave per output, lanes over the slices (coalesced reads), the
-// max and the sum each by a lane-ordered pass and a fixed butterfly, so the
-// result does not depend on scheduling.
+// max and the sum each by a lane-ordered pass and a fixed reduction across
+// the lanes, so the result does not depend on scheduling.
 constexpr int kCombineSerialParts = 16;
 __global__ __launch_bounds__(256) void joiner_combine_wide_kernel(JoinerArgs a) {
   const int T = a.b.T, S = a.S, lane = threadIdx.x & 63;
@@ -637,12 +637,14 @@ __global__ __launch_bounds__(256) void joiner_combine_wide_kernel(JoinerArgs a) 
       const float2* pp = a.part + (size_t)m * a.nparts;
       float M = kNegInfF;
       for (int p = lane; p < a.nparts; p += 64) M = fmaxf(M, pp[p].x);
-#pragma unroll
-      for (int off = 32; off >= 1; off >>= 1) M = fmaxf(M, __shfl_xor(M, off, 64));
+      M = row16_max(M);  // within each 16-lane row, then across the rows
+      M = fmaxf(M, __shfl_xor(M, 16, 64));
+      M = fmaxf(M, __shfl_xor(M, 32, 64));
       float sum = 0.f;
       for (int p = lane; p < a.nparts; p += 64) sum += pp[p].y * __expf(pp[p].x - M);
-#pragma unroll
-      for (int off = 32; off >= 1; off >>= 1) sum += __shfl_xor(sum, off, 64);
+      sum = row16_sum(sum);
+      sum += __shfl_xor(sum, 16, 64);
+      sum += __shfl_xor(sum, 32, 64);
       l = M + __logf(sum);
       py = a.blk[m] - l;
       px = (info.z >= 0) ? a.tgt[m] - l : (info.z == -2 ? __builtin_nanf("") : kNegInfF);

@@ -80,8 +80,13 @@ __global__ __launch_bounds__(256) void rowmax_kernel(const float* __restrict__ a
   } else {
     for (int v = lane; v < V; v += 64) m = keep_nan_max(m, r[v]);
   }
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) m = keep_nan_max(m, __shfl_xor(m, off, 64));
+  // within each 16-lane row by DPP rotations, then across the rows
+  m = keep_nan_max(m, dpp_row_ror<8>(m));
+  m = keep_nan_max(m, dpp_row_ror<4>(m));
+  m = keep_nan_max(m, dpp_row_ror<2>(m));
+  m = keep_nan_max(m, dpp_row_ror<1>(m));
+  m = keep_nan_max(m, __shfl_xor(m, 16, 64));
+  m = keep_nan_max(m, __shfl_xor(m, 32, 64));
   if (lane == 0) out[row] = m;
 }
 
