@@ -132,7 +132,8 @@ SimpleWs simple_layout(void* base, int N, int T, int U, int V) {
   w.nsplit = normalizer_splits(N, T, U, V);
   w.npart = c.take<float>((size_t)w.nsplit * L);
   w.lsplit = dlm_splits(N, T, U, V);
-  w.lpart = c.take<float>((size_t)w.lsplit * NU * V);
+  const int gsplit = simple_grad_splits(N, T, U, V);
+  w.lpart = c.take<float>((size_t)(gsplit > w.lsplit ? gsplit : w.lsplit) * NU * V);
   w.rx = c.take<double>(NT);
   w.Gx = c.take<double>(NU);
   w.Gy = c.take<double>(NU);

@@ -147,6 +147,9 @@ DEV void band_alpha(const BandDiag& v, int lane) {
   uint32_t mr[kBandPrefetch];
 #pragma unroll
   for (int k = 0; k < kBandPrefetch; ++k) band_load(v, k, lane, live, xr[k], yr[k], mr[k]);
+  // drained once, so that the loop's wait counts cover only its own loads,
+  // a whole ring old
+  __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
   for (int d0 = 0; d0 < v.Dn; d0 += kBandPrefetch) {
 #pragma unroll
     for (int k = 0; k < kBandPrefetch; ++k) {
@@ -175,6 +178,7 @@ DEV void band_beta(const BandDiag& v, int lane) {
   uint32_t mr[kBandPrefetch];
 #pragma unroll
   for (int k = 0; k < kBandPrefetch; ++k) band_load(v, v.Dn - 1 - k, lane, live, xr[k], yr[k], mr[k]);
+  __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
   for (int d0 = v.Dn - 1; d0 >= 0; d0 -= kBandPrefetch) {
 #pragma unroll
     for (int k = 0; k < kBandPrefetch; ++k) {

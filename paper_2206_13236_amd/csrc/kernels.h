@@ -60,6 +60,8 @@ hipError_t launch_rowmax(const SimpleArgs& a, hipStream_t s);
 hipError_t launch_normalizer(const SimpleArgs& a, hipStream_t s);
 int normalizer_splits(int N, int T, int U, int V);
 int dlm_splits(int N, int T, int U, int V);
+// frame ranges of the fused d am / d lm kernel (0: it does not apply to these sizes)
+int simple_grad_splits(int N, int T, int U, int V);
 hipError_t launch_lattice(const SimpleArgs& a, hipStream_t s);
 hipError_t launch_lattice_diag_copy(const SimpleArgs& a, hipStream_t s);
 // the recursion alone (no occupations) on a.pxd / a.pyd; a.V = 0 skips the symbol check

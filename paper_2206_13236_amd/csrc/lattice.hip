@@ -23,7 +23,7 @@
 // the row sums of gx and gy and per-16-frame partial column sums of gx and gy.
 //
 // Precision: log2 domain with fp64 accumulators; only the bounded correction
-// term of LogAdd goes through fp32 exp2/log2 (see log2add). alpha and beta are
+// term of LogAdd goes through fp32 exp2/log2 (see lse2). alpha and beta are
 // stored in fp64.
 // A NaN px or py at a node of the lattice is flagged on the side and makes
 // the utterance's loss NaN, like an out-of-range length or symbol.
@@ -75,6 +75,17 @@ DEV void lattice_check(const DiagT (&x)[R], const DiagT (&y)[R], bool& bad) {
   for (int r = 0; r < R; ++r) bad |= __builtin_isunordered(x[r], y[r]);
 }
 
+// log2(2^a + 2^b) for the recursions: the bounded correction
+// log2(1 + 2^-|a-b|) through the fp32 hardware exp2/log2. The difference is
+// formed directly, so that only the sum's own max waits for both inputs
+// beside it; a NaN difference (two -inf inputs, or a NaN input, which is
+// flagged on the side) is clamped to 0, so that two -inf give -inf + 1.
+DEV double lse2(double a, double b) {
+  const double mx = __builtin_fmax(a, b);
+  const float d = __builtin_fminf((float)(-__builtin_fabs(a - b)), 0.0f);
+  return mx + (double)__builtin_amdgcn_logf(1.0f + __builtin_amdgcn_exp2f(d));
+}
+
 // Returns whether this lane saw a NaN input.
 template <int R, int P>
 DEV bool alpha_pass(const LatView& v, int lane) {
@@ -86,21 +97,28 @@ DEV bool alpha_pass(const LatView& v, int lane) {
     hout[r] = (lane * R + r == 0) ? 0.0 : kNegInfD;
     vout[r] = kNegInfD;
   }
+  // The symbol term into row 0 comes from the lane below by one DPP wave
+  // shift whose destination is carried from step to step: lane 0 receives
+  // nothing and keeps the -inf it starts with, so that no step resets it.
+  double vsh = kNegInfD;
   bool bad = false;
   DiagT xr[P][R], yr[P][R];  // converted at use, not at load
 #pragma unroll
   for (int k = 0; k < P; ++k) lattice_load<R>(v, k, lane, xr[k], yr[k]);
+  // The loop's wait counts then cover only the loads of its own steps, a
+  // whole ring old, rather than the order the loads above were issued in.
+  __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
   for (int d0 = 0; d0 < D; d0 += P) {
 #pragma unroll
     for (int k = 0; k < P; ++k) {
       const int d = d0 + k;
       const int dW = d * v.W + lane;
-      const double vfirst = dpp_move_d<kDppWaveShr1>(vout[R - 1], kNegInfD);
+      vsh = dpp_move_d<kDppWaveShr1>(vout[R - 1], vsh);
       double nh[R], nv[R];
 #pragma unroll
       for (int r = 0; r < R; ++r) {
-        const double vin = (r == 0) ? vfirst : vout[r - 1];
-        const double al = log2add_nonan(hout[r], vin);
+        const double vin = (r == 0) ? vsh : vout[r - 1];
+        const double al = lse2(hout[r], vin);
         nh[r] = al + (double)yr[k][r];
         nv[r] = al + (double)xr[k][r];
         buf_store_f64(v.out, (uint32_t)(dW + r * 64) * 8u, al);
@@ -128,21 +146,23 @@ DEV bool beta_pass(const LatView& v, int lane) {
   double bprev[R];
 #pragma unroll
   for (int r = 0; r < R; ++r) bprev[r] = (lane * R + r == v.Un) ? 0.0 : kNegInfD;
+  double vsh = kNegInfD;  // lane 63 receives nothing from the shift and keeps -inf
   bool bad = false;
   DiagT xr[P][R], yr[P][R];  // converted at use, not at load
 #pragma unroll
   for (int k = 0; k < P; ++k) lattice_load<R>(v, D - 1 - k, lane, xr[k], yr[k]);
+  __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0), as in the forward pass
   for (int d0 = D - 1; d0 >= 0; d0 -= P) {
 #pragma unroll
     for (int k = 0; k < P; ++k) {
       const int d = d0 - k;
       const int dW = d * v.W + lane;
-      const double vlast = dpp_move_d<kDppWaveShl1>(bprev[0], kNegInfD);
+      vsh = dpp_move_d<kDppWaveShl1>(bprev[0], vsh);
       double nb[R];
 #pragma unroll
       for (int r = 0; r < R; ++r) {
-        const double vin = (r == R - 1) ? vlast : bprev[r + 1];
-        nb[r] = log2add_nonan((double)yr[k][r] + bprev[r], (double)xr[k][r] + vin);
+        const double vin = (r == R - 1) ? vsh : bprev[r + 1];
+        nb[r] = lse2((double)yr[k][r] + bprev[r], (double)xr[k][r] + vin);
         buf_store_f64(v.out, (uint32_t)(dW + r * 64) * 8u, nb[r]);
       }
 #pragma unroll

@@ -70,6 +70,7 @@ __global__ __launch_bounds__(256) void rowmax_kernel(const float* __restrict__ a
   float m = kNegInfF;
   if ((V & 3) == 0) {
     const float4* r4 = reinterpret_cast<const float4*>(r);
+#pragma unroll 4
     for (int v = lane; v < V / 4; v += 64) {
       float4 q = r4[v];
       m = keep_nan_max(m, q.x);
@@ -78,6 +79,7 @@ __global__ __launch_bounds__(256) void rowmax_kernel(const float* __restrict__ a
       m = keep_nan_max(m, q.w);
     }
   } else {
+#pragma unroll 4
     for (int v = lane; v < V; v += 64) m = keep_nan_max(m, r[v]);
   }
   // within each 16-lane row by DPP rotations, then across the rows
@@ -163,6 +165,9 @@ __global__ __launch_bounds__(256) void colsum_kernel(SimpleArgs a) {
   const double* px_ = a.cpx + (size_t)n * a.ncolblk * U1 + u;
   const double* py_ = a.cpy + (size_t)n * a.ncolblk * U1 + u;
   double cx = 0.0, cy = 0.0;
+  // unrolled so that eight blocks' loads are in flight before the first add
+  // (the adds keep their order)
+#pragma unroll 8
   for (int q = 0; q < a.ncolblk; ++q) {
     cx += px_[(size_t)q * U1];
     cy += py_[(size_t)q * U1];
@@ -703,6 +708,331 @@ __global__ __launch_bounds__(256) void dlm_epi_kernel(SimpleArgs a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// d am and d lm in one pass (U + 1 <= 128, plain trivial joiner).
+//
+// One workgroup per (utterance, 64 columns of v, range of frames). The
+// columns' e^{lm - m_l} (every u) is formed once into LDS; per step of 32
+// frames the workgroup stages W(t, u) and e^{am - m_a} through LDS and runs
+// both contractions on them:
+//   d am [32 x 64] = W [32 x U+1] . e^{lm - m_l} [U+1 x 64], finished at once
+//     (times e^{am - m_a}, minus the target and blank terms) and stored;
+//   d lm [U+1 x 64] += W^T [U+1 x 32] . e^{am - m_a} [32 x 64], kept in
+//     registers over the range's frames and finished at the end (a single
+//     range) or stored as the range's partial sums for dlm_epi_kernel.
+// am is read once for both, every exponential is formed once, and the next
+// step's global loads are in flight during the current step's MFMAs. Eight
+// waves (two per SIMD, so that one's LDS waits overlap the other's MFMAs):
+// wave w computes the d am block of rows 16 (w & 1) .. +15, columns
+// 16 (w >> 1) .. +15 of a step, and the d lm blocks of columns 16 (w & 3) ..
+// +15 whose u block has the parity w >> 2.
+// ---------------------------------------------------------------------------
+constexpr int kSgT = 32;        // frames per step
+constexpr int kSgV = 64;        // columns per workgroup
+constexpr int kSgMaxU1 = 128;   // the fused kernel takes U + 1 up to this
+constexpr int kSgThreads = 512;
+constexpr int kSgWaves = kSgThreads / 64;
+constexpr int kSgDam = 8 / kSgWaves;  // d am blocks of a step per wave (along v)
+constexpr int kSgUg = kSgWaves / 4;   // wave groups sharing the d lm u blocks of a column block
+constexpr int kSgList = 32;     // listed targets whose gx one gather round stages
+constexpr int kSgTS = kSgT + 4; // row stride of eaT (16-byte rows, conflict-free fragment reads)
+
+// A workgroup barrier after this thread's LDS writes have completed. Unlike
+// __syncthreads() it does not wait for outstanding global loads, so that the
+// next step's loads stay in flight across it.
+DEV void sg_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+template <int KP>  // u extent staged: U + 1 <= KP (a multiple of 16)
+struct alignas(16) SgSmem {
+  static constexpr int K = KP + 4;  // row stride of wt and elT
+  float wt[kSgT * K];               // W(t, u) of the step's frames, [t][u] (zero past ldw)
+  float eaT[kSgV * kSgTS];          // e^{am - m_a}, [v][t] (zero past T_n or V)
+  float elT[kSgV * K];              // e^{lm - m_l}, [v][u] (zero past U_n or V)
+  float g[kSgList * kSgT];          // gx(t, u_k) of listed targets, [k][t]
+  double ry[kSgT];                  // row sums of gy
+  int lu[kSgMaxU1], ly[kSgMaxU1];   // targets in the columns (ascending u) and their symbols
+  int sym[kSgMaxU1];                // y_{u+1}
+  int cnt[kSgWaves];
+};
+
+struct SgPrefetch {  // one step's global loads, held until the step's LDS writes
+  float4 w[kSgMaxU1 * 8 / kSgThreads];  // W: 32 ldw floats
+  float4 x[512 / kSgThreads];           // am: 32 x 64 values
+  float ma[512 / kSgThreads];
+  float gx[kSgT * kSgList / kSgThreads];
+  double ry;
+};
+
+// The utterance's arrays as buffer resources: every step load is issued
+// unconditionally (kOob where there is nothing to load), so that the step's
+// code is straight-line and the wait counts stay exact.
+struct SgSrc {
+  Rsrc wt, am, ma, gx, ry;
+  int ldw, V, U1, Tn;
+};
+
+DEV float4 buf_load_f4(Rsrc r, uint32_t off) {
+  return __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0));
+}
+
+template <int KP, bool V4>  // V4: V is a multiple of 4 (16-byte loads of am)
+DEV void sg_load(const SgSrc& c, int t0, int v0, int nml, const int* lu, SgPrefetch& f) {
+  const int tid = threadIdx.x, q4 = c.ldw / 4;
+#pragma unroll
+  for (int i = 0; i < KP * 8 / kSgThreads; ++i) {  // the step's rows of W are one contiguous block; rows past T fall outside
+    const int q = tid + i * kSgThreads;
+    f.w[i] = buf_load_f4(c.wt, q < kSgT * q4 ? (uint32_t)(t0 * c.ldw + 4 * q) * 4u : kOob);
+  }
+#pragma unroll
+  for (int i = 0; i < 512 / kSgThreads; ++i) {
+    const int q = tid + i * kSgThreads, t = t0 + q / 16, v = v0 + 4 * (q % 16);
+    const bool in = t < c.Tn && v < c.V;
+    const uint32_t o = (uint32_t)(t * c.V + v) * 4u;
+    f.ma[i] = buf_load_f32(c.ma, t < c.Tn ? (uint32_t)t * 4u : kOob);
+    if (V4) {
+      f.x[i] = buf_load_f4(c.am, in ? o : kOob);
+    } else {
+      f.x[i].x = buf_load_f32(c.am, in ? o : kOob);
+      f.x[i].y = buf_load_f32(c.am, in && v + 1 < c.V ? o + 4u : kOob);
+      f.x[i].z = buf_load_f32(c.am, in && v + 2 < c.V ? o + 8u : kOob);
+      f.x[i].w = buf_load_f32(c.am, in && v + 3 < c.V ? o + 12u : kOob);
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < kSgT * kSgList / kSgThreads; ++i) {
+    const int q = tid + i * kSgThreads, k = q / kSgT, t = t0 + q % kSgT;
+    f.gx[i] = buf_load_f32(c.gx, (k < nml && t < c.Tn) ? (uint32_t)(t * c.U1 + lu[k]) * 4u : kOob);
+  }
+  f.ry = buf_load_f64(c.ry, (tid < kSgT && t0 + tid < c.Tn) ? (uint32_t)(t0 + tid) * 8u : kOob);
+}
+
+template <int KP>
+DEV void sg_store(SgSmem<KP>& sm, const SgPrefetch& f, int t0, int v0, int Tn, int V, int ldw) {
+  constexpr int K = SgSmem<KP>::K;
+  const int tid = threadIdx.x, q4 = ldw / 4;
+#pragma unroll
+  for (int i = 0; i < KP * 8 / kSgThreads; ++i) {
+    const int q = tid + i * kSgThreads;
+    if (q < kSgT * q4) *reinterpret_cast<float4*>(&sm.wt[(q / q4) * K + 4 * (q % q4)]) = f.w[i];
+  }
+#pragma unroll
+  for (int i = 0; i < 512 / kSgThreads; ++i) {
+    const int q = tid + i * kSgThreads, t = q / 16, c = 4 * (q % 16);
+    const bool row = t0 + t < Tn;
+    const float xv[4] = {f.x[i].x, f.x[i].y, f.x[i].z, f.x[i].w};
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      sm.eaT[(c + j) * kSgTS + t] = (row && v0 + c + j < V) ? __expf(xv[j] - f.ma[i]) : 0.f;
+  }
+#pragma unroll
+  for (int i = 0; i < kSgT * kSgList / kSgThreads; ++i) sm.g[tid + i * kSgThreads] = f.gx[i];
+  if (tid < kSgT) sm.ry[tid] = f.ry;
+}
+
+template <int KP, bool V4>
+__global__ __launch_bounds__(kSgThreads) void simple_grad_kernel(SimpleArgs a, int splits) {
+  constexpr int K = SgSmem<KP>::K;
+  __shared__ SgSmem<KP> sm;
+  const int v0 = blockIdx.x * kSgV, sk = blockIdx.y, n = blockIdx.z;
+  const int T = a.b.T, U1 = a.b.U + 1, V = a.V, blank = a.b.blank;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, l16 = lane & 15, g4 = lane >> 4;
+  int Tn, Un;
+  utt_dims(a.b, n, Tn, Un);
+  const int kn = (Un + 1 + 15) / 16 * 16;  // contraction length of d am; u blocks of d lm = kn / 16
+  const float sc = a.scale ? a.scale[n] : 1.f;
+  // setup: zeroed W tile (columns past ldw stay zero), symbols, e^{lm - m_l}
+  for (int i = tid; i < kSgT * K; i += kSgThreads) sm.wt[i] = 0.f;
+  for (int u = tid; u < kSgMaxU1; u += kSgThreads) {
+    bool ok = true;
+    sm.sym[u] = (u < Un) ? symbol_at(a.b, n, u, V, ok) : -1;
+  }
+  for (int q = tid; q < KP * 16; q += kSgThreads) {
+    const int u = q / 16, c = 4 * (q % 16), v = v0 + c;
+    const bool row = u <= Un;
+    const float* lr = a.lm + ((size_t)n * U1 + (row ? u : 0)) * V;
+    const float ml = row ? a.m_l[(size_t)n * U1 + u] : 0.f;
+    float x[4];
+    if (row && (V & 3) == 0 && v + 4 <= V) {
+      const float4 q4 = *reinterpret_cast<const float4*>(lr + v);
+      x[0] = q4.x; x[1] = q4.y; x[2] = q4.z; x[3] = q4.w;
+    } else {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) x[j] = (row && v + j < V) ? lr[v + j] : 0.f;
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) sm.elT[(c + j) * K + u] = (row && v + j < V) ? __expf(x[j] - ml) : 0.f;
+  }
+  __syncthreads();
+  // the targets that fall in the columns, ascending u (ballot compaction)
+  {
+    const int y = (tid < Un) ? sm.sym[tid] : -1;
+    const bool hit = y >= v0 && y < v0 + kSgV;
+    const uint64_t bal = __ballot(hit);
+    if (lane == 0) sm.cnt[wave] = __popcll(bal);
+    __syncthreads();
+    int base = 0;
+    for (int w = 0; w < wave; ++w) base += sm.cnt[w];
+    if (hit) {
+      const int k = base + __popcll(bal & ((1ull << lane) - 1));
+      sm.lu[k] = tid;
+      sm.ly[k] = y;
+    }
+    __syncthreads();
+  }
+  int nm = 0;
+#pragma unroll
+  for (int w = 0; w < kSgWaves; ++w) nm += sm.cnt[w];
+  const int nml = min(nm, kSgList);
+  const int tb = wave & 1, vb0 = (wave >> 1) * kSgDam;  // d am blocks
+  const int lvb = wave & 3, ug = wave >> 2;              // d lm column block and u-block group
+  // the list entries whose symbol is the lane's d am column j (bit k of 128)
+  uint64_t mk[kSgDam][2];
+#pragma unroll
+  for (int j = 0; j < kSgDam; ++j) mk[j][0] = mk[j][1] = 0;
+  for (int k = 0; k < nm; ++k) {
+    const int y = sm.ly[k];
+#pragma unroll
+    for (int j = 0; j < kSgDam; ++j)
+      if (y == v0 + 16 * (vb0 + j) + l16) mk[j][k >> 6] |= 1ull << (k & 63);
+  }
+  // frame steps of this range (rows up to T: those past T_n get zeros)
+  SgSrc src;
+  src.wt = make_rsrc(a.Wt + (size_t)n * T * a.ldw, (size_t)T * a.ldw * 4);
+  src.am = make_rsrc(a.am + (size_t)n * T * V, (size_t)T * V * 4);
+  src.ma = make_rsrc(a.m_a + (size_t)n * T, (size_t)T * 4);
+  src.gx = make_rsrc(a.gx + (size_t)n * T * U1, (size_t)T * U1 * 4);
+  src.ry = make_rsrc(a.ry + (size_t)n * T, (size_t)T * 8);
+  src.ldw = a.ldw;
+  src.V = V;
+  src.U1 = U1;
+  src.Tn = Tn;
+  const Rsrc gout = make_rsrc(a.am_grad + (size_t)n * T * V, (size_t)T * V * 4);
+  const int nsteps = (T + kSgT - 1) / kSgT, per = (nsteps + splits - 1) / splits;
+  const int s0 = sk * per, s1 = min(nsteps, s0 + per);
+  constexpr int NUB = KP / 16 / kSgUg;  // d lm u blocks per wave (u block ug + kSgUg i)
+  floatx4 accl[NUB];
+#pragma unroll
+  for (int i = 0; i < NUB; ++i) accl[i] = floatx4{0.f, 0.f, 0.f, 0.f};
+  SgPrefetch f;
+  if (s0 < s1) sg_load<KP, V4>(src, s0 * kSgT, v0, nml, sm.lu, f);
+  for (int st = s0; st < s1; ++st) {
+    const int t0 = st * kSgT;
+    sg_barrier();  // the previous step's LDS reads are done
+    sg_store<KP>(sm, f, t0, v0, Tn, V, a.ldw);
+    sg_barrier();
+    // the next step's loads, in flight during this step's MFMAs and stores
+    if (st + 1 < s1) sg_load<KP, V4>(src, t0 + kSgT, v0, nml, sm.lu, f);
+    const bool live = t0 < Tn;
+    floatx4 accd[kSgDam];
+#pragma unroll
+    for (int j = 0; j < kSgDam; ++j) accd[j] = floatx4{0.f, 0.f, 0.f, 0.f};
+    if (live) {
+      // d am: W rows of the wave's 16 frames against e^{lm - m_l} columns
+#pragma unroll
+      for (int kk = 0; kk < KP; kk += 16) {
+        if (kk >= kn) break;
+        const floatx4 fa = *reinterpret_cast<const floatx4*>(&sm.wt[(16 * tb + l16) * K + kk + 4 * g4]);
+#pragma unroll
+        for (int j = 0; j < kSgDam; ++j) {
+          const floatx4 fb = *reinterpret_cast<const floatx4*>(&sm.elT[(16 * (vb0 + j) + l16) * K + kk + 4 * g4]);
+#pragma unroll
+          for (int q = 0; q < 4; ++q) accd[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[q], fb[q], accd[j], 0, 0, 0);
+        }
+      }
+      // d lm: W^T (u rows) against e^{am - m_a} of the wave's 16 columns; the
+      // A fragment's 4 frames are one per row of wt (k-permuted like B)
+#pragma unroll
+      for (int kk = 0; kk < kSgT; kk += 16) {
+        const floatx4 fb = *reinterpret_cast<const floatx4*>(&sm.eaT[(16 * lvb + l16) * kSgTS + kk + 4 * g4]);
+#pragma unroll
+        for (int i = 0; i < NUB; ++i) {
+          const int ub = ug + kSgUg * i;
+          if (16 * ub >= kn) break;
+          floatx4 fa;
+#pragma unroll
+          for (int q = 0; q < 4; ++q) fa[q] = sm.wt[(kk + 4 * g4 + q) * K + 16 * ub + l16];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) accl[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[q], fb[q], accl[i], 0, 0, 0);
+        }
+      }
+    }
+    // d am epilogue: e^{am - m_a} * acc, minus gx at the targets (ascending
+    // u) and the blank column's row sum of gy
+    float res[kSgDam][4];
+#pragma unroll
+    for (int j = 0; j < kSgDam; ++j) {
+      const floatx4 ea = *reinterpret_cast<const floatx4*>(&sm.eaT[(16 * (vb0 + j) + l16) * kSgTS + 16 * tb + 4 * g4]);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) res[j][r] = ea[r] * accd[j][r];
+    }
+    if (live) {
+      for (int k0 = 0; k0 < nm; k0 += kSgList) {
+        if (k0 > 0) {  // more targets than one gather round holds: the next ones, synchronously
+          sg_barrier();
+          for (int q = tid; q < kSgT * kSgList; q += kSgThreads) {
+            const int k = k0 + q / kSgT, t = t0 + q % kSgT;
+            sm.g[q] = (k < nm && t < Tn) ? a.gx[((size_t)n * T + t) * U1 + sm.lu[k]] : 0.f;
+          }
+          sg_barrier();
+        }
+#pragma unroll
+        for (int j = 0; j < kSgDam; ++j) {
+          uint32_t bits = (uint32_t)(mk[j][k0 >> 6] >> (k0 & 63));
+          while (bits) {  // the lane's targets in ascending u
+            const int k = __builtin_ctz(bits);
+            bits &= bits - 1;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) res[j][r] -= sm.g[k * kSgT + 16 * tb + 4 * g4 + r];
+          }
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < kSgDam; ++j)
+        if (v0 + 16 * (vb0 + j) + l16 == blank)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int tl = 16 * tb + 4 * g4 + r;
+            if (t0 + tl < Tn) res[j][r] = (float)((double)res[j][r] - sm.ry[tl]);
+          }
+    }
+#pragma unroll
+    for (int j = 0; j < kSgDam; ++j) {
+      const int v = v0 + 16 * (vb0 + j) + l16;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {  // rows past T fall outside the resource
+        const int t = t0 + 16 * tb + 4 * g4 + r;
+        __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint((t < Tn) ? sc * res[j][r] : 0.f), gout,
+                                              (int)(v < V ? (uint32_t)(t * V + v) * 4u : kOob), 0, 0);
+      }
+    }
+  }
+  // d lm: the range's partial sums, or (one range) the finished gradient
+  const int v = v0 + 16 * lvb + l16;
+  if (v >= V) return;
+#pragma unroll
+  for (int i = 0; i < NUB; ++i) {
+    const int ub = ug + kSgUg * i;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int u = 16 * ub + 4 * g4 + r;
+      if (u >= U1) continue;
+      if (splits > 1) {
+        if (u <= Un) a.lpart[(((size_t)sk * a.b.N + n) * U1 + u) * V + v] = accl[i][r];
+        continue;
+      }
+      float out = 0.f;
+      if (u <= Un) {
+        const float d = sm.elT[(16 * lvb + l16) * K + u] * accl[i][r];
+        double gd = (double)d;
+        if (v == sm.sym[u]) gd -= a.Gx[(size_t)n * U1 + u];
+        if (v == blank) gd -= a.Gy[(size_t)n * U1 + u];
+        out = (float)(sc * gd);
+      }
+      a.lm_grad[((size_t)n * U1 + u) * V + v] = out;
+    }
+  }
+}
+
 __global__ void fill_f32_kernel(float* p, size_t n, float v) {
   size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
   size_t stride = (size_t)gridDim.x * blockDim.x;
@@ -747,6 +1077,21 @@ static int dlm_splits_cfg(int N, int T, int U, int V) {
 }
 int dlm_splits(int N, int T, int U, int V) {
   return V >= kSimpleBigV ? dlm_splits_cfg<BigCfg>(N, T, U, V) : dlm_splits_cfg<DlmCfg>(N, T, U, V);
+}
+
+// Frame ranges of the fused d am / d lm kernel: enough for about
+// kSgBlocks workgroups (one per CU: the kernel runs beside the pruned stage
+// on a second stream, and more workgroups measured no faster per step);
+// 0 where the kernel does not apply.
+constexpr int kSgBlocks = 256;
+int simple_grad_splits(int N, int T, int U, int V) {
+  // one utterance's am must stay below 2^31 bytes (32-bit buffer offsets)
+  if (U + 1 > kSgMaxU1 || (long long)T * V * 4 >= (1ll << 31)) return 0;
+  const long long base = (long long)N * ((V + kSgV - 1) / kSgV);
+  const int steps = (T + kSgT - 1) / kSgT;
+  long long s = (kSgBlocks + base - 1) / base;
+  if (s > steps) s = steps;
+  return s < 1 ? 1 : (int)s;
 }
 
 hipError_t launch_normalizer(const SimpleArgs& a, hipStream_t s) {
@@ -798,6 +1143,29 @@ hipError_t launch_simple_grads(const SimpleArgs& a, hipStream_t s) {
     hipLaunchKernelGGL(lm_s_kernel, dim3((a.b.N * U1 + 3) / 4), dim3(256), 0, s, a);
   }
   const bool big = V >= kSimpleBigV;
+  const int gs = simple_grad_splits(a.b.N, T, a.b.U, V);
+  if (gs > 0 && a.am_grad && a.lm_grad && a.lm_only == 0.f && a.am_only == 0.f) {
+    {
+      RNNT_PROF(s, "simple_grad");
+      const dim3 grid((V + kSgV - 1) / kSgV, gs, a.b.N);
+      const bool v4 = (V & 3) == 0;
+      if (U1 <= 64) {
+        if (v4) hipLaunchKernelGGL((simple_grad_kernel<64, true>), grid, dim3(kSgThreads), 0, s, a, gs);
+        else hipLaunchKernelGGL((simple_grad_kernel<64, false>), grid, dim3(kSgThreads), 0, s, a, gs);
+      } else {
+        if (v4) hipLaunchKernelGGL((simple_grad_kernel<kSgMaxU1, true>), grid, dim3(kSgThreads), 0, s, a, gs);
+        else hipLaunchKernelGGL((simple_grad_kernel<kSgMaxU1, false>), grid, dim3(kSgThreads), 0, s, a, gs);
+      }
+    }
+    if (gs > 1) {
+      SimpleArgs e = a;
+      e.lsplit = gs;  // the workspace holds max(dlm_splits, simple_grad_splits) partial sets
+      const size_t groups = (size_t)a.b.N * U1 * ((V + 3) / 4);
+      RNNT_PROF(s, "simple_dlm_epi");
+      hipLaunchKernelGGL(dlm_epi_kernel, dim3((unsigned)((groups + 255) / 256)), dim3(256), 0, s, e);
+    }
+    return hipGetLastError();
+  }
   if (a.am_grad) {
     RNNT_PROF(s, "simple_dam");
     if (big) {

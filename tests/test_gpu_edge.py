@@ -208,6 +208,34 @@ def test_simple_stage_with_the_large_vocabulary_tiles():
     assert_close("lm_grad", host(got["lm_grad"]), s1["lm_grad"], atol=1e-4)
 
 
+@pytest.mark.parametrize("cfg", [
+    # T <= 32: one frame range, d lm finished in the kernel; V = 11: every
+    # target in one column tile (more than one gather round of 32), scalar loads
+    dict(seed=16, N=3, T_range=(20, 32), U_range=(90, 110), V=11),
+    # 64 utterances x 8 column tiles: one frame range over several steps
+    dict(seed=17, N=64, T_range=(40, 70), U_range=(20, 60), V=500),
+    # a few workgroups: several frame ranges, partial sums finished by dlm_epi
+    dict(seed=18, N=2, T_range=(90, 130), U_range=(40, 63), V=130),
+    # U + 1 = 128, the largest the fused kernel takes; and 129, past it
+    dict(seed=19, N=3, T_range=(30, 50), U_range=(127, 127), V=70),
+    dict(seed=20, N=3, T_range=(30, 50), U_range=(128, 128), V=70),
+])
+def test_simple_grads_fused_kernel_paths(cfg):
+    # d am and d lm of the plain trivial joiner come from one kernel for
+    # U + 1 <= 128; every branch of its launch and of its target lists
+    c = dict(cfg)
+    b = _small(seed=c.pop("seed"), J=16, S=4, **c)
+    say(f"[edge] simple grads, N = {b.N}, T = {b.T}, U = {b.U}, V = {b.V}")
+    batch = make_dev_batch(b)
+    sc = (0.5 + np.random.default_rng(3).random(b.N)).astype(np.float32)
+    got = P.rnnt_simple_loss(batch, b.V, dev_f32(b.am), dev_f32(b.lm), dev_f32(sc), want_grads=True)
+    torch.cuda.synchronize()
+    s1 = O.simple_stage(b.am, b.lm, b.symbols, b.t_len, b.u_len, b.wl.blank, scale=sc)
+    assert_close("loss", host(got["loss"]), s1["loss"], rtol=1e-5)
+    assert_close("am_grad", host(got["am_grad"]), s1["am_grad"], atol=1e-4)
+    assert_close("lm_grad", host(got["lm_grad"]), s1["lm_grad"], atol=1e-4)
+
+
 def test_step_with_the_wide_forward_tiles():
     # bf16 at V >= 2048: the joiner forward takes 256 x 256 tiles of 16
     # waves; ragged rows (M = S sum T_n is no multiple of 256) and columns
