@@ -709,7 +709,7 @@ __global__ __launch_bounds__(256) void dlm_epi_kernel(SimpleArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// d am and d lm in one pass (U + 1 <= 128, plain trivial joiner).
+// d am and d lm in one pass (U + 1 <= 320, plain trivial joiner).
 //
 // One workgroup per (utterance, 64 columns of v, range of frames). The
 // columns' e^{lm - m_l} (every u) is formed once into LDS; per step of 32
@@ -729,7 +729,7 @@ __global__ __launch_bounds__(256) void dlm_epi_kernel(SimpleArgs a) {
 // ---------------------------------------------------------------------------
 constexpr int kSgT = 32;        // frames per step
 constexpr int kSgV = 64;        // columns per workgroup
-constexpr int kSgMaxU1 = 128;   // the fused kernel takes U + 1 up to this
+constexpr int kSgMaxU1 = 320;   // the fused kernel takes U + 1 up to this
 constexpr int kSgThreads = 512;
 constexpr int kSgWaves = kSgThreads / 64;
 constexpr int kSgDam = 8 / kSgWaves;  // d am blocks of a step per wave (along v)
@@ -750,8 +750,8 @@ struct alignas(16) SgSmem {
   float elT[kSgV * K];              // e^{lm - m_l}, [v][u] (zero past U_n or V)
   float g[kSgList * kSgT];          // gx(t, u_k) of listed targets, [k][t]
   double ry[kSgT];                  // row sums of gy
-  int lu[kSgMaxU1], ly[kSgMaxU1];   // targets in the columns (ascending u) and their symbols
-  int sym[kSgMaxU1];                // y_{u+1}
+  int lu[KP], ly[KP];               // targets in the columns (ascending u) and their symbols
+  int sym[KP];                      // y_{u+1}
   int cnt[kSgWaves];
 };
 
@@ -842,7 +842,7 @@ __global__ __launch_bounds__(kSgThreads) void simple_grad_kernel(SimpleArgs a, i
   const float sc = a.scale ? a.scale[n] : 1.f;
   // setup: zeroed W tile (columns past ldw stay zero), symbols, e^{lm - m_l}
   for (int i = tid; i < kSgT * K; i += kSgThreads) sm.wt[i] = 0.f;
-  for (int u = tid; u < kSgMaxU1; u += kSgThreads) {
+  for (int u = tid; u < KP; u += kSgThreads) {
     bool ok = true;
     sm.sym[u] = (u < Un) ? symbol_at(a.b, n, u, V, ok) : -1;
   }
@@ -865,7 +865,7 @@ __global__ __launch_bounds__(kSgThreads) void simple_grad_kernel(SimpleArgs a, i
   __syncthreads();
   // the targets that fall in the columns, ascending u (ballot compaction)
   {
-    const int y = (tid < Un) ? sm.sym[tid] : -1;
+    const int y = (tid < Un) ? sm.sym[tid] : -1;  // U_n < KP <= kSgThreads
     const bool hit = y >= v0 && y < v0 + kSgV;
     const uint64_t bal = __ballot(hit);
     if (lane == 0) sm.cnt[wave] = __popcll(bal);
@@ -885,15 +885,20 @@ __global__ __launch_bounds__(kSgThreads) void simple_grad_kernel(SimpleArgs a, i
   const int nml = min(nm, kSgList);
   const int tb = wave & 1, vb0 = (wave >> 1) * kSgDam;  // d am blocks
   const int lvb = wave & 3, ug = wave >> 2;              // d lm column block and u-block group
-  // the list entries whose symbol is the lane's d am column j (bit k of 128)
-  uint64_t mk[kSgDam][2];
+  // the list entries whose symbol is the lane's d am column j (bit k of KP)
+  constexpr int MW = (KP + 63) / 64;
+  uint64_t mk[kSgDam][MW];
 #pragma unroll
-  for (int j = 0; j < kSgDam; ++j) mk[j][0] = mk[j][1] = 0;
-  for (int k = 0; k < nm; ++k) {
+  for (int j = 0; j < kSgDam; ++j)
+#pragma unroll
+    for (int w = 0; w < MW; ++w) mk[j][w] = 0;
+  for (int k = 0; k < nm; ++k) {  // (words picked by compares: no indexing of the register array)
     const int y = sm.ly[k];
 #pragma unroll
     for (int j = 0; j < kSgDam; ++j)
-      if (y == v0 + 16 * (vb0 + j) + l16) mk[j][k >> 6] |= 1ull << (k & 63);
+#pragma unroll
+      for (int w = 0; w < MW; ++w)
+        if (y == v0 + 16 * (vb0 + j) + l16 && (k >> 6) == w) mk[j][w] |= 1ull << (k & 63);
   }
   // frame steps of this range (rows up to T: those past T_n get zeros)
   SgSrc src;
@@ -930,13 +935,14 @@ __global__ __launch_bounds__(kSgThreads) void simple_grad_kernel(SimpleArgs a, i
       // d am: W rows of the wave's 16 frames against e^{lm - m_l} columns
 #pragma unroll
       for (int kk = 0; kk < KP; kk += 16) {
-        if (kk >= kn) break;
-        const floatx4 fa = *reinterpret_cast<const floatx4*>(&sm.wt[(16 * tb + l16) * K + kk + 4 * g4]);
+        if (kk < kn) {
+          const floatx4 fa = *reinterpret_cast<const floatx4*>(&sm.wt[(16 * tb + l16) * K + kk + 4 * g4]);
 #pragma unroll
-        for (int j = 0; j < kSgDam; ++j) {
-          const floatx4 fb = *reinterpret_cast<const floatx4*>(&sm.elT[(16 * (vb0 + j) + l16) * K + kk + 4 * g4]);
+          for (int j = 0; j < kSgDam; ++j) {
+            const floatx4 fb = *reinterpret_cast<const floatx4*>(&sm.elT[(16 * (vb0 + j) + l16) * K + kk + 4 * g4]);
 #pragma unroll
-          for (int q = 0; q < 4; ++q) accd[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[q], fb[q], accd[j], 0, 0, 0);
+            for (int q = 0; q < 4; ++q) accd[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[q], fb[q], accd[j], 0, 0, 0);
+          }
         }
       }
       // d lm: W^T (u rows) against e^{am - m_a} of the wave's 16 columns; the
@@ -947,12 +953,13 @@ __global__ __launch_bounds__(kSgThreads) void simple_grad_kernel(SimpleArgs a, i
 #pragma unroll
         for (int i = 0; i < NUB; ++i) {
           const int ub = ug + kSgUg * i;
-          if (16 * ub >= kn) break;
-          floatx4 fa;
+          if (16 * ub < kn) {  // (a guard, not an exit: the loop stays fully unrolled)
+            floatx4 fa;
 #pragma unroll
-          for (int q = 0; q < 4; ++q) fa[q] = sm.wt[(kk + 4 * g4 + q) * K + 16 * ub + l16];
+            for (int q = 0; q < 4; ++q) fa[q] = sm.wt[(kk + 4 * g4 + q) * K + 16 * ub + l16];
 #pragma unroll
-          for (int q = 0; q < 4; ++q) accl[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[q], fb[q], accl[i], 0, 0, 0);
+            for (int q = 0; q < 4; ++q) accl[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[q], fb[q], accl[i], 0, 0, 0);
+          }
         }
       }
     }
@@ -977,7 +984,10 @@ __global__ __launch_bounds__(kSgThreads) void simple_grad_kernel(SimpleArgs a, i
         }
 #pragma unroll
         for (int j = 0; j < kSgDam; ++j) {
-          uint32_t bits = (uint32_t)(mk[j][k0 >> 6] >> (k0 & 63));
+          uint64_t word = 0;
+#pragma unroll
+          for (int w = 0; w < MW; ++w) word = (w == (k0 >> 6)) ? mk[j][w] : word;
+          uint32_t bits = (uint32_t)(word >> (k0 & 63));
           while (bits) {  // the lane's targets in ascending u
             const int k = __builtin_ctz(bits);
             bits &= bits - 1;
@@ -1131,6 +1141,14 @@ hipError_t launch_smoothing_stats(const SimpleArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
+// u extent KP: the smallest of 64, 128, 192, 320 that holds U + 1 (LDS and
+// the d lm accumulators scale with it)
+template <int KP>
+static void launch_simple_grad(const SimpleArgs& a, int gs, bool v4, dim3 grid, hipStream_t s) {
+  if (v4) hipLaunchKernelGGL((simple_grad_kernel<KP, true>), grid, dim3(kSgThreads), 0, s, a, gs);
+  else hipLaunchKernelGGL((simple_grad_kernel<KP, false>), grid, dim3(kSgThreads), 0, s, a, gs);
+}
+
 hipError_t launch_simple_grads(const SimpleArgs& a, hipStream_t s) {
   const int T = a.b.T, U1 = a.b.U + 1, V = a.V;
   {
@@ -1149,13 +1167,10 @@ hipError_t launch_simple_grads(const SimpleArgs& a, hipStream_t s) {
       RNNT_PROF(s, "simple_grad");
       const dim3 grid((V + kSgV - 1) / kSgV, gs, a.b.N);
       const bool v4 = (V & 3) == 0;
-      if (U1 <= 64) {
-        if (v4) hipLaunchKernelGGL((simple_grad_kernel<64, true>), grid, dim3(kSgThreads), 0, s, a, gs);
-        else hipLaunchKernelGGL((simple_grad_kernel<64, false>), grid, dim3(kSgThreads), 0, s, a, gs);
-      } else {
-        if (v4) hipLaunchKernelGGL((simple_grad_kernel<kSgMaxU1, true>), grid, dim3(kSgThreads), 0, s, a, gs);
-        else hipLaunchKernelGGL((simple_grad_kernel<kSgMaxU1, false>), grid, dim3(kSgThreads), 0, s, a, gs);
-      }
+      if (U1 <= 64) launch_simple_grad<64>(a, gs, v4, grid, s);
+      else if (U1 <= 128) launch_simple_grad<128>(a, gs, v4, grid, s);
+      else if (U1 <= 192) launch_simple_grad<192>(a, gs, v4, grid, s);
+      else launch_simple_grad<kSgMaxU1>(a, gs, v4, grid, s);
     }
     if (gs > 1) {
       SimpleArgs e = a;

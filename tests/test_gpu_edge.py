@@ -216,13 +216,17 @@ def test_simple_stage_with_the_large_vocabulary_tiles():
     dict(seed=17, N=64, T_range=(40, 70), U_range=(20, 60), V=500),
     # a few workgroups: several frame ranges, partial sums finished by dlm_epi
     dict(seed=18, N=2, T_range=(90, 130), U_range=(40, 63), V=130),
-    # U + 1 = 128, the largest the fused kernel takes; and 129, past it
+    # the u extents the kernel is built for (64, 128, 192, 320) at and just
+    # past each boundary; U + 1 = 321 takes the separate d am and d lm kernels
     dict(seed=19, N=3, T_range=(30, 50), U_range=(127, 127), V=70),
     dict(seed=20, N=3, T_range=(30, 50), U_range=(128, 128), V=70),
+    dict(seed=21, N=2, T_range=(30, 40), U_range=(191, 192), V=70),
+    dict(seed=22, N=2, T_range=(30, 40), U_range=(319, 319), V=70),
+    dict(seed=23, N=2, T_range=(30, 40), U_range=(320, 320), V=70),
 ])
 def test_simple_grads_fused_kernel_paths(cfg):
     # d am and d lm of the plain trivial joiner come from one kernel for
-    # U + 1 <= 128; every branch of its launch and of its target lists
+    # U + 1 <= 320; every branch of its launch and of its target lists
     c = dict(cfg)
     b = _small(seed=c.pop("seed"), J=16, S=4, **c)
     say(f"[edge] simple grads, N = {b.N}, T = {b.T}, U = {b.U}, V = {b.V}")
