@@ -40,6 +40,16 @@ namespace {
 
 DEV float keep_nan_max(float m, float x) { return (x > m || x != x) ? x : m; }
 
+// A workgroup barrier after this thread's LDS writes have completed. Unlike
+// __syncthreads() it does not wait for outstanding global loads, so that the
+// next step's loads stay in flight across it.
+DEV void sg_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+DEV float4 buf_load_f4(Rsrc r, uint32_t off) {
+  return __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0));
+}
+
+
 // Length of each of `splits` contiguous K ranges over [0, K), a multiple of bk.
 DEV int split_chunk(int K, int splits, int bk) { return ((K + splits - 1) / splits + bk - 1) / bk * bk; }
 
@@ -452,6 +462,245 @@ __global__ __launch_bounds__(kEpiThreads) void normalizer_epi_kernel(SimpleArgs 
 }
 
 // ---------------------------------------------------------------------------
+// Normaliser and its epilogue in one kernel (U + 1 <= 320). One workgroup
+// of 8 waves per (utterance, 32 frames) holds C[t][u] for every u of its
+// frames: C = sum over chunks of 64 v of e^{am - m_a} [32 x 64] .
+// e^{lm - m_l}^T [64 x U+1], both exponentials staged through LDS and the
+// next chunk's loads in flight during the current chunk's MFMAs; then Z, px
+// and py of its nodes (Eqs. (1)-(2), (5)) go to the rectangle, and through
+// LDS (the staging buffer reused) to the diagonal-major copies, diagonal by
+// diagonal. No split over v: no partial sums and no second launch. Wave w
+// holds the C blocks of rows 16 (w & 1) .. +15 whose u block is (w >> 1) +
+// 4 i. The blocks after the tiles fill the cells of the copies that no node
+// of the rectangle maps to.
+// ---------------------------------------------------------------------------
+constexpr int kNfT = 32;         // frames per workgroup
+constexpr int kNfV = 64;         // v per chunk
+constexpr int kNfThreads = 512;
+constexpr int kNfS = kNfV + 4;   // row stride of the staged chunks (conflict-free fragment reads)
+constexpr int kNfMaxU1 = 320;
+constexpr int kNfFill = 4;       // cells per thread of a fill block
+
+template <int KP>
+struct alignas(16) NfSmem {
+  union {
+    struct {
+      float ea[kNfT * kNfS];  // e^{am - m_a}, [t][v]
+      float el[KP * kNfS];    // e^{lm - m_l}, [u][v]
+    } g;
+    struct {
+      float px[kNfT * KP];    // px, py of the tile's cells, [frame][slot of the lattice row]
+      float py[kNfT * KP];
+    } d;
+  };
+  float ma[kNfT], ab[kNfT], za[kNfT];  // per frame: m_a, am[t, blank], Zac
+  float ml[KP], lb[KP], lyv[KP], zl[KP], lay[KP];  // per u: m_l, lm[u, blank], lm[u, y], Zlm, lavg[y]
+  int yy[KP];                          // y_{u+1}
+};
+
+struct NfPrefetch {
+  float4 x;                        // am: 32 x 64 values over 512 threads
+  float4 l[kNfMaxU1 * 16 / kNfThreads];  // lm: KP x 64 values
+};
+
+template <int KP, bool V4>
+DEV void nf_load(Rsrc am, Rsrc lm, int t0, int v0, int Tn, int Un, int V, NfPrefetch& f) {
+  const int tid = threadIdx.x;
+  {
+    const int t = t0 + tid / 16, v = v0 + 4 * (tid % 16);
+    const bool in = t < Tn && v < V;
+    const uint32_t o = (uint32_t)(t * V + v) * 4u;
+    if (V4) {
+      f.x = buf_load_f4(am, in ? o : kOob);
+    } else {
+      f.x.x = buf_load_f32(am, in ? o : kOob);
+      f.x.y = buf_load_f32(am, in && v + 1 < V ? o + 4u : kOob);
+      f.x.z = buf_load_f32(am, in && v + 2 < V ? o + 8u : kOob);
+      f.x.w = buf_load_f32(am, in && v + 3 < V ? o + 12u : kOob);
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < KP * 16 / kNfThreads; ++i) {
+    const int q = tid + i * kNfThreads, u = q / 16, v = v0 + 4 * (q % 16);
+    const bool in = u <= Un && v < V;
+    const uint32_t o = (uint32_t)(u * V + v) * 4u;
+    if (V4) {
+      f.l[i] = buf_load_f4(lm, in ? o : kOob);
+    } else {
+      f.l[i].x = buf_load_f32(lm, in ? o : kOob);
+      f.l[i].y = buf_load_f32(lm, in && v + 1 < V ? o + 4u : kOob);
+      f.l[i].z = buf_load_f32(lm, in && v + 2 < V ? o + 8u : kOob);
+      f.l[i].w = buf_load_f32(lm, in && v + 3 < V ? o + 12u : kOob);
+    }
+  }
+}
+
+template <int KP>
+DEV void nf_store(NfSmem<KP>& sm, const NfPrefetch& f, int t0, int v0, int Tn, int Un, int V) {
+  const int tid = threadIdx.x;
+  {
+    const int t = tid / 16, c = 4 * (tid % 16);
+    const bool row = t0 + t < Tn;
+    const float m = sm.ma[t];
+    const float xv[4] = {f.x.x, f.x.y, f.x.z, f.x.w};
+    float e[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) e[j] = (row && v0 + c + j < V) ? __expf(xv[j] - m) : 0.f;
+    *reinterpret_cast<float4*>(&sm.g.ea[t * kNfS + c]) = make_float4(e[0], e[1], e[2], e[3]);
+  }
+#pragma unroll
+  for (int i = 0; i < KP * 16 / kNfThreads; ++i) {
+    const int q = tid + i * kNfThreads, u = q / 16, c = 4 * (q % 16);
+    const bool row = u <= Un;
+    const float m = sm.ml[u];
+    const float xv[4] = {f.l[i].x, f.l[i].y, f.l[i].z, f.l[i].w};
+    float e[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) e[j] = (row && v0 + c + j < V) ? __expf(xv[j] - m) : 0.f;
+    *reinterpret_cast<float4*>(&sm.g.el[u * kNfS + c]) = make_float4(e[0], e[1], e[2], e[3]);
+  }
+}
+
+template <int KP, bool V4>
+__global__ __launch_bounds__(kNfThreads) void normalizer_fused_kernel(SimpleArgs a) {
+  __shared__ NfSmem<KP> sm;
+  const int T = a.b.T, U1 = a.b.U + 1, V = a.V, blank = a.b.blank;
+  const int ntt = (T + kNfT - 1) / kNfT;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, l16 = lane & 15, g4 = lane >> 4;
+  const int R = lattice_rows_per_lane_dev(U1), W = 64 * R;  // W <= KP
+  if ((int)blockIdx.x >= a.b.N * ntt) {
+#pragma unroll
+    for (int k = 0; k < kNfFill; ++k)
+      lattice_fill_outside(a.pxd, a.pyd, (int)blockIdx.x - a.b.N * ntt, tid + k * kNfThreads, kNfFill * kNfThreads, T,
+                           U1, R);
+    return;
+  }
+  const int n = blockIdx.x / ntt, t0 = (blockIdx.x - n * ntt) * kNfT;
+  int Tn, Un;
+  utt_dims(a.b, n, Tn, Un);
+  const bool smooth = a.lm_only != 0.f || a.am_only != 0.f;
+  const float* amn = a.am + (size_t)n * T * V;
+  const float* lmn = a.lm + (size_t)n * U1 * V;
+  // per-frame and per-u values of the epilogue (and the offsets of the staging)
+  if (tid < kNfT) {
+    const int t = t0 + tid;
+    const bool node = t < Tn;
+    sm.ma[tid] = node ? a.m_a[(size_t)n * T + t] : 0.f;
+    sm.ab[tid] = node ? amn[(size_t)t * V + blank] : 0.f;
+    sm.za[tid] = (node && smooth) ? a.Zac[(size_t)n * T + t] : 0.f;
+  }
+  for (int u = tid; u < KP; u += kNfThreads) {
+    const bool row = u <= Un;
+    bool ok = true;
+    const int y = (u < Un) ? symbol_at(a.b, n, u, V, ok) : 0;
+    sm.yy[u] = y;
+    sm.ml[u] = row ? a.m_l[(size_t)n * U1 + u] : 0.f;
+    sm.lb[u] = row ? lmn[(size_t)u * V + blank] : 0.f;
+    sm.lyv[u] = row ? lmn[(size_t)u * V + y] : 0.f;
+    sm.zl[u] = (row && smooth) ? a.Zlm[(size_t)n * U1 + u] : 0.f;
+    sm.lay[u] = (row && smooth) ? a.lavg[(size_t)n * V + y] : 0.f;
+  }
+  __syncthreads();
+  const int kn = (Un + 1 + 15) / 16 * 16;
+  const int tb = wave & 1;
+  constexpr int NB = KP / 64;  // C blocks per wave: u block (w >> 1) + 4 i
+  floatx4 acc[NB];
+#pragma unroll
+  for (int i = 0; i < NB; ++i) acc[i] = floatx4{0.f, 0.f, 0.f, 0.f};
+  if (t0 < Tn) {
+    const Rsrc amr = make_rsrc(amn, (size_t)T * V * 4), lmr = make_rsrc(lmn, (size_t)U1 * V * 4);
+    const int nc = (V + kNfV - 1) / kNfV;
+    NfPrefetch f;
+    nf_load<KP, V4>(amr, lmr, t0, 0, Tn, Un, V, f);
+    for (int c = 0; c < nc; ++c) {
+      sg_barrier();  // the previous chunk's LDS reads are done
+      nf_store<KP>(sm, f, t0, c * kNfV, Tn, Un, V);
+      sg_barrier();
+      if (c + 1 < nc) nf_load<KP, V4>(amr, lmr, t0, (c + 1) * kNfV, Tn, Un, V, f);
+#pragma unroll
+      for (int kk = 0; kk < kNfV; kk += 16) {
+        const floatx4 fa = *reinterpret_cast<const floatx4*>(&sm.g.ea[(16 * tb + l16) * kNfS + kk + 4 * g4]);
+#pragma unroll
+        for (int i = 0; i < NB; ++i) {
+          const int ub = (wave >> 1) + 4 * i;
+          if (16 * ub < kn) {
+            const floatx4 fb = *reinterpret_cast<const floatx4*>(&sm.g.el[(16 * ub + l16) * kNfS + kk + 4 * g4]);
+#pragma unroll
+            for (int q = 0; q < 4; ++q) acc[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[q], fb[q], acc[i], 0, 0, 0);
+          }
+        }
+      }
+    }
+  }
+  // epilogue: the target logits am[t, y_u] of the lane's nodes first (one gather round)
+  const Rsrc amr = make_rsrc(amn, (size_t)T * V * 4);
+  float ay[NB][4];
+#pragma unroll
+  for (int i = 0; i < NB; ++i) {
+    const int u = 16 * ((wave >> 1) + 4 * i) + l16;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int t = t0 + 16 * tb + 4 * g4 + r;
+      const bool node = t < Tn && u < Un;
+      ay[i][r] = buf_load_f32(amr, node ? (uint32_t)(t * V + sm.yy[u]) * 4u : kOob);
+    }
+  }
+  sg_barrier();  // every wave's MFMAs are done with the staging buffer
+  const float cw = 1.f - a.lm_only - a.am_only;
+  const float* la = a.lavg + (size_t)n * V;
+  const float lab = smooth ? la[blank] : 0.f;
+  const size_t L0 = ((size_t)n * T) * U1;
+#pragma unroll
+  for (int i = 0; i < NB; ++i) {
+    const int u = 16 * ((wave >> 1) + 4 * i) + l16;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int tl = 16 * tb + 4 * g4 + r, t = t0 + tl;
+      const bool cell = t < T && u < U1, node = t < Tn && u <= Un;
+      float z = 0.f, px = kNegInfF, py = kNegInfF;
+      if (node) {
+        const float sv = acc[i][r];
+        const float s1 = (sv > FLT_MIN || sv != sv) ? sv : FLT_MIN;
+        z = sm.ma[tl] + sm.ml[u] + logf(s1);
+        py = sm.ab[tl] + sm.lb[u] - z;
+        float pxv = ay[i][r] + sm.lyv[u] - z;
+        if (smooth) {
+          // smoothed joiner: c L_trivial + a L_lm + b L_acoustic (Sec. 3.3.1)
+          py = cw * py + a.lm_only * (sm.lb[u] - sm.zl[u]) + a.am_only * (sm.ab[tl] + lab - sm.za[tl]);
+          pxv = cw * pxv + a.lm_only * (sm.lyv[u] - sm.zl[u]) + a.am_only * (ay[i][r] + sm.lay[u] - sm.za[tl]);
+        }
+        px = (u < Un) ? pxv : kNegInfF;
+      }
+      if (cell) {
+        const size_t idx = L0 + (size_t)t * U1 + u;
+        a.Z[idx] = z;
+        a.px[idx] = px;
+        a.py[idx] = py;
+      }
+      if (u < U1) {
+        sm.d.px[tl * KP + lattice_slot(u, R)] = px;
+        sm.d.py[tl * KP + lattice_slot(u, R)] = py;
+      }
+    }
+  }
+  __syncthreads();
+  // diagonal d = t0 + k holds the tile's nodes (t0 + tl, u = k - tl); item
+  // (k, j): u = k - (kNfT - 1) + j, so that consecutive j are consecutive u
+  // on one diagonal
+  const int ft = min(kNfT, T - t0), nd = kNfT - 1 + U1;
+  const size_t base = (size_t)n * (T + U1 - 1) * W;
+  for (int it = tid; it < nd * kNfT; it += kNfThreads) {
+    const int k = it / kNfT, j = it - k * kNfT;
+    const int u = k - (kNfT - 1) + j, tl = k - u;
+    if (u < 0 || u >= U1 || tl < 0 || tl >= ft) continue;
+    const int sl = lattice_slot(u, R);
+    const size_t o = base + (size_t)(t0 + k) * W + sl;
+    a.pxd[o] = (DiagT)((double)sm.d.px[tl * KP + sl] * kLog2e);
+    a.pyd[o] = (DiagT)((double)sm.d.py[tl * KP + sl] * kLog2e);
+  }
+}
+
+// ---------------------------------------------------------------------------
 // d am: per utterance C[t][v] = sum_u Wt[t][u] El[u][v]  (K = U_n + 1)
 // ---------------------------------------------------------------------------
 using DamCfg = GemmCfg<32, 64, 32, false>;
@@ -737,11 +986,6 @@ constexpr int kSgUg = kSgWaves / 4;   // wave groups sharing the d lm u blocks o
 constexpr int kSgList = 32;     // listed targets whose gx one gather round stages
 constexpr int kSgTS = kSgT + 4; // row stride of eaT (16-byte rows, conflict-free fragment reads)
 
-// A workgroup barrier after this thread's LDS writes have completed. Unlike
-// __syncthreads() it does not wait for outstanding global loads, so that the
-// next step's loads stay in flight across it.
-DEV void sg_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
-
 template <int KP>  // u extent staged: U + 1 <= KP (a multiple of 16)
 struct alignas(16) SgSmem {
   static constexpr int K = KP + 4;  // row stride of wt and elT
@@ -770,10 +1014,6 @@ struct SgSrc {
   Rsrc wt, am, ma, gx, ry;
   int ldw, V, U1, Tn;
 };
-
-DEV float4 buf_load_f4(Rsrc r, uint32_t off) {
-  return __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0));
-}
 
 template <int KP, bool V4>  // V4: V is a multiple of 4 (16-byte loads of am)
 DEV void sg_load(const SgSrc& c, int t0, int v0, int nml, const int* lu, SgPrefetch& f) {
@@ -1104,8 +1344,32 @@ int simple_grad_splits(int N, int T, int U, int V) {
   return s < 1 ? 1 : (int)s;
 }
 
+template <int KP>
+static void launch_normalizer_fused(const SimpleArgs& a, bool v4, unsigned blocks, hipStream_t s) {
+  if (v4) hipLaunchKernelGGL((normalizer_fused_kernel<KP, true>), dim3(blocks), dim3(kNfThreads), 0, s, a);
+  else hipLaunchKernelGGL((normalizer_fused_kernel<KP, false>), dim3(blocks), dim3(kNfThreads), 0, s, a);
+}
+
 hipError_t launch_normalizer(const SimpleArgs& a, hipStream_t s) {
   const int T = a.b.T, U1 = a.b.U + 1;
+  const long long tiles = (long long)a.b.N * ((T + kNfT - 1) / kNfT);
+  const int chunks = (a.V + kNfV - 1) / kNfV;
+  if (U1 <= kNfMaxU1 && (long long)T * a.V * 4 < (1ll << 31) && (long long)U1 * a.V * 4 < (1ll << 31) &&
+      (tiles >= 256 || chunks <= 16)) {
+    // every u of 32 frames per workgroup, the epilogue in the same kernel;
+    // u extent as in the fused gradient kernel. Its workgroups run the whole
+    // of V in sequence: with fewer tiles than CUs and a long V (largev: 160
+    // tiles, 79 chunks, 137 against 123 us) the split kernels below are faster.
+    const size_t blocks = (size_t)a.b.N * ((T + kNfT - 1) / kNfT) +
+                          (size_t)a.b.N * lattice_fill_blocks(T, a.b.U, kNfFill * kNfThreads);
+    const bool v4 = (a.V & 3) == 0;
+    RNNT_PROF(s, "normalizer");
+    if (U1 <= 64) launch_normalizer_fused<64>(a, v4, (unsigned)blocks, s);
+    else if (U1 <= 128) launch_normalizer_fused<128>(a, v4, (unsigned)blocks, s);
+    else if (U1 <= 192) launch_normalizer_fused<192>(a, v4, (unsigned)blocks, s);
+    else launch_normalizer_fused<kNfMaxU1>(a, v4, (unsigned)blocks, s);
+    return hipGetLastError();
+  }
   {
     RNNT_PROF(s, "normalizer");
     if (a.V >= kSimpleBigV) {
