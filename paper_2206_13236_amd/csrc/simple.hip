@@ -1069,11 +1069,10 @@ DEV void sg_store(SgSmem<KP>& sm, const SgPrefetch& f, int t0, int v0, int Tn, i
   if (tid < kSgT) sm.ry[tid] = f.ry;
 }
 
+// One work item: utterance n, the 64 columns from v0, frame range sk.
 template <int KP, bool V4>
-__global__ __launch_bounds__(kSgThreads) void simple_grad_kernel(SimpleArgs a, int splits) {
+DEV void sg_item(const SimpleArgs& a, int splits, SgSmem<KP>& sm, int v0, int sk, int n) {
   constexpr int K = SgSmem<KP>::K;
-  __shared__ SgSmem<KP> sm;
-  const int v0 = blockIdx.x * kSgV, sk = blockIdx.y, n = blockIdx.z;
   const int T = a.b.T, U1 = a.b.U + 1, V = a.V, blank = a.b.blank;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, l16 = lane & 15, g4 = lane >> 4;
   int Tn, Un;
@@ -1283,6 +1282,19 @@ __global__ __launch_bounds__(kSgThreads) void simple_grad_kernel(SimpleArgs a, i
   }
 }
 
+// Work items in order (column tiles of an utterance's frame range next to
+// each other); a grid smaller than the item count loops over them.
+template <int KP, bool V4>
+__global__ __launch_bounds__(kSgThreads) void simple_grad_kernel(SimpleArgs a, int splits, int items) {
+  __shared__ SgSmem<KP> sm;
+  const int nvt = (a.V + kSgV - 1) / kSgV;
+  for (int it = blockIdx.x; it < items; it += gridDim.x) {
+    const int vt = it % nvt, rest = it / nvt;
+    sg_item<KP, V4>(a, splits, sm, vt * kSgV, rest % splits, rest / splits);
+    __syncthreads();  // the next item rewrites the LDS
+  }
+}
+
 __global__ void fill_f32_kernel(float* p, size_t n, float v) {
   size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
   size_t stride = (size_t)gridDim.x * blockDim.x;
@@ -1355,11 +1367,13 @@ hipError_t launch_normalizer(const SimpleArgs& a, hipStream_t s) {
   const long long tiles = (long long)a.b.N * ((T + kNfT - 1) / kNfT);
   const int chunks = (a.V + kNfV - 1) / kNfV;
   if (U1 <= kNfMaxU1 && (long long)T * a.V * 4 < (1ll << 31) && (long long)U1 * a.V * 4 < (1ll << 31) &&
-      (tiles >= 256 || chunks <= 16)) {
+      (tiles >= 192 || chunks <= 16)) {
     // every u of 32 frames per workgroup, the epilogue in the same kernel;
     // u extent as in the fused gradient kernel. Its workgroups run the whole
-    // of V in sequence: with fewer tiles than CUs and a long V (largev: 160
-    // tiles, 79 chunks, 137 against 123 us) the split kernels below are faster.
+    // of V in sequence: with far fewer tiles than CUs and a long V (largev:
+    // 160 tiles, 79 chunks, 137 against 123 us) the split kernels below are
+    // faster; at the stress shape (248 tiles, 125 chunks) this one is (661
+    // against 756 us).
     const size_t blocks = (size_t)a.b.N * ((T + kNfT - 1) / kNfT) +
                           (size_t)a.b.N * lattice_fill_blocks(T, a.b.U, kNfFill * kNfThreads);
     const bool v4 = (a.V & 3) == 0;
@@ -1408,9 +1422,13 @@ hipError_t launch_smoothing_stats(const SimpleArgs& a, hipStream_t s) {
 // u extent KP: the smallest of 64, 128, 192, 320 that holds U + 1 (LDS and
 // the d lm accumulators scale with it)
 template <int KP>
-static void launch_simple_grad(const SimpleArgs& a, int gs, bool v4, dim3 grid, hipStream_t s) {
-  if (v4) hipLaunchKernelGGL((simple_grad_kernel<KP, true>), grid, dim3(kSgThreads), 0, s, a, gs);
-  else hipLaunchKernelGGL((simple_grad_kernel<KP, false>), grid, dim3(kSgThreads), 0, s, a, gs);
+static void launch_simple_grad(const SimpleArgs& a, int gs, bool v4, hipStream_t s) {
+  // one workgroup per item (grids capped at 128-256 workgroups, leaving CUs
+  // to the pruned stage, measured no faster at the stress and long shapes)
+  const int items = a.b.N * gs * ((a.V + kSgV - 1) / kSgV);
+  const dim3 grid(items);
+  if (v4) hipLaunchKernelGGL((simple_grad_kernel<KP, true>), grid, dim3(kSgThreads), 0, s, a, gs, items);
+  else hipLaunchKernelGGL((simple_grad_kernel<KP, false>), grid, dim3(kSgThreads), 0, s, a, gs, items);
 }
 
 hipError_t launch_simple_grads(const SimpleArgs& a, hipStream_t s) {
@@ -1429,12 +1447,11 @@ hipError_t launch_simple_grads(const SimpleArgs& a, hipStream_t s) {
   if (gs > 0 && a.am_grad && a.lm_grad && a.lm_only == 0.f && a.am_only == 0.f) {
     {
       RNNT_PROF(s, "simple_grad");
-      const dim3 grid((V + kSgV - 1) / kSgV, gs, a.b.N);
       const bool v4 = (V & 3) == 0;
-      if (U1 <= 64) launch_simple_grad<64>(a, gs, v4, grid, s);
-      else if (U1 <= 128) launch_simple_grad<128>(a, gs, v4, grid, s);
-      else if (U1 <= 192) launch_simple_grad<192>(a, gs, v4, grid, s);
-      else launch_simple_grad<kSgMaxU1>(a, gs, v4, grid, s);
+      if (U1 <= 64) launch_simple_grad<64>(a, gs, v4, s);
+      else if (U1 <= 128) launch_simple_grad<128>(a, gs, v4, s);
+      else if (U1 <= 192) launch_simple_grad<192>(a, gs, v4, s);
+      else launch_simple_grad<kSgMaxU1>(a, gs, v4, s);
     }
     if (gs > 1) {
       SimpleArgs e = a;
