@@ -835,14 +835,21 @@ static dim3 dl_grid(int rows, int ldl) {
   return dim3((unsigned)((rows + kDlRows - 1) / kDlRows), (unsigned)((ng + dl_threads_per_row(ng) - 1) / dl_threads_per_row(ng)));
 }
 
+struct DlSmem {
+  int4 ri[kDlRows];
+  float4 rx[kDlRows];  // lse, gx, gy, scale
+  float4 red[kDlThreads];
+};
+
+// Block (bx, by) of the d(logits) stream: rows cm0 + 32 bx .., column groups of by.
 template <bool BF>
-__global__ __launch_bounds__(kDlThreads) void joiner_dl_kernel(JoinerArgs a, int cm0, int cm1) {
-  __shared__ int4 ri[kDlRows];
-  __shared__ float4 rx[kDlRows];  // lse, gx, gy, scale
-  __shared__ float4 red[kDlThreads];
+DEV void dl_block(const JoinerArgs& a, int cm0, int cm1, int bx, int by, DlSmem& sm) {
+  int4* ri = sm.ri;
+  float4* rx = sm.rx;
+  float4* red = sm.red;
   const int M = a.frame_off[a.b.N] * a.S;
   const int mend = min(cm1, M);
-  const int m0 = cm0 + blockIdx.x * kDlRows;
+  const int m0 = cm0 + bx * kDlRows;
   if (m0 >= mend) return;
   const int V = a.V, TS = a.b.T * a.S, ldl = a.ldl, blank = a.b.blank;
   const int nrows = min(kDlRows, mend - m0);
@@ -866,7 +873,7 @@ __global__ __launch_bounds__(kDlThreads) void joiner_dl_kernel(JoinerArgs a, int
   const int nrg = kDlThreads / tpr, rg = threadIdx.x / tpr, ct = threadIdx.x - rg * tpr;
   const bool vec = from_head || (V & 3) == 0;
   {
-    const int g0 = blockIdx.y * tpr;  // this block's column groups
+    const int g0 = by * tpr;  // this block's column groups
     const int c = 4 * (g0 + ct);
     const bool gok = g0 + ct < ng;
     float cs[4] = {0.f, 0.f, 0.f, 0.f};
@@ -936,6 +943,12 @@ __global__ __launch_bounds__(kDlThreads) void joiner_dl_kernel(JoinerArgs a, int
         if (c + q < V) db[c + q] = cm0 == 0 ? cs[q] : db[c + q] + cs[q];
     }
   }
+}
+
+template <bool BF>
+__global__ __launch_bounds__(kDlThreads) void joiner_dl_kernel(JoinerArgs a, int cm0, int cm1) {
+  __shared__ DlSmem sm;
+  dl_block<BF>(a, cm0, cm1, blockIdx.x, blockIdx.y, sm);
 }
 
 // ---------------------------------------------------------------------------
@@ -1636,6 +1649,29 @@ __global__ __launch_bounds__(kTailThreads) void joiner_tail_kernel(JoinerArgs a,
   else h_pass_f32(a, hp, b);
 }
 
+// The backward's first launch when chunk 0's logits come from the head: the
+// d(logits) stream of chunk 0 (the first dlx * dly blocks) and the h passes
+// of the first chunks (the rest) as block kinds of one launch. Both are
+// memory-bound and independent, so that they run side by side instead of one
+// after the other.
+template <bool BF>
+__global__ __launch_bounds__(kTailThreads) void joiner_head_kernel(JoinerArgs a, TailRanges r, int cm0, int cm1,
+                                                                   int dlx, int dly) {
+  __shared__ DlSmem dsm;
+  __shared__ uint16_t htile[BF ? kHTile : 1][kHTile + 8];  // bf16 h pass
+  static_assert(kTailThreads == kDlThreads, "one block size for both kinds");
+  int b = blockIdx.x;
+  if (b < dlx * dly) {
+    dl_block<BF>(a, cm0, cm1, b % dlx, b / dlx, dsm);
+    return;
+  }
+  b -= dlx * dly;
+  const HPass& hp = b < r.h0.blocks ? r.h0 : r.h1;
+  if (b >= r.h0.blocks) b -= r.h0.blocks;
+  if constexpr (BF) h_pass_bf16(a, hp, b, threadIdx.x, true, htile);
+  else h_pass_f32(a, hp, b);
+}
+
 // The backward's GEMM kernel. Every block kind runs in one kernel, each on
 // its own range of blocks, so that the recomputed logits of the next chunk
 // (L), dh of the current chunk (D) and its dW (W) share a launch (a chunk's
@@ -2024,21 +2060,24 @@ hipError_t launch_joiner_bwd(const JoinerArgs& a, hipStream_t s) {
   const int nch = (mmax + C - 1) / C;
   auto lo = [&](int k) { return k * C; };
   auto hi = [&](int k) { return (k + 1) * C < mmax ? (k + 1) * C : mmax; };
-  {
-    TailRanges tr{};
-    tr.h0 = h_pass(ring_slot(a, 0), lo(0), hi(0));
-    if (nch > 1) tr.h1 = h_pass(ring_slot(a, 1), lo(1), hi(1));
-    e = launch_tail(a, tr, s, "joiner_h");
-  }
-  if (e == hipSuccess && a.head && a.head_rows == C) {
+  TailRanges tr{};
+  tr.h0 = h_pass(ring_slot(a, 0), lo(0), hi(0));
+  if (nch > 1) tr.h1 = h_pass(ring_slot(a, 1), lo(1), hi(1));
+  if (a.head && a.head_rows == C) {
     // chunk 0's logits were kept by the forward: stream them (and, for bf16,
     // transpose d(logits) for dW) instead of the one recomputation launch
-    // the pipeline cannot fill
+    // the pipeline cannot fill; the stream shares its launch with the first
+    // h passes
     const dim3 gdl = dl_grid(hi(0) - lo(0), a.ldl);
     {
       RNNT_PROF(s, "joiner_dl");
-      if (a.bf16) hipLaunchKernelGGL(joiner_dl_kernel<true>, gdl, dim3(kDlThreads), 0, s, a, lo(0), hi(0));
-      else hipLaunchKernelGGL(joiner_dl_kernel<false>, gdl, dim3(kDlThreads), 0, s, a, lo(0), hi(0));
+      const unsigned blocks = gdl.x * gdl.y + tr.h0.blocks + tr.h1.blocks;
+      if (a.bf16)
+        hipLaunchKernelGGL(joiner_head_kernel<true>, dim3(blocks), dim3(kTailThreads), 0, s, a, tr, lo(0), hi(0),
+                           (int)gdl.x, (int)gdl.y);
+      else
+        hipLaunchKernelGGL(joiner_head_kernel<false>, dim3(blocks), dim3(kTailThreads), 0, s, a, tr, lo(0), hi(0),
+                           (int)gdl.x, (int)gdl.y);
     }
     e = hipGetLastError();
     if (e == hipSuccess && a.bf16) {
@@ -2047,8 +2086,9 @@ hipError_t launch_joiner_bwd(const JoinerArgs& a, hipStream_t s) {
       hipLaunchKernelGGL(joiner_dlt_kernel, gt, dim3(256), 0, s, a, lo(0), hi(0));
       e = hipGetLastError();
     }
-  } else if (e == hipSuccess) {
-    e = launch_bwd_gemms(ring_slot(a, 0), ring_slot(a, 0), lo(0), hi(0), 0, 0, false, false, false, s);
+  } else {
+    e = launch_tail(a, tr, s, "joiner_h");
+    if (e == hipSuccess) e = launch_bwd_gemms(ring_slot(a, 0), ring_slot(a, 0), lo(0), hi(0), 0, 0, false, false, false, s);
   }
   for (int k = 0; k < nch && e == hipSuccess; ++k) {
     const JoinerArgs cur = ring_slot(a, k), nxt = ring_slot(a, k + 1), prev = ring_slot(a, k > 0 ? k - 1 : 0);
