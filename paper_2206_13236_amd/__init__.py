@@ -394,8 +394,10 @@ class PrunedRnntLoss:
     and the joiner backward. The simple loss's own gradients (two
     contractions that only the caller needs) run on a second stream at the
     default priority, forked after the joiner forward so that they overlap
-    the pruned recursion, which occupies a few workgroups per utterance, and
-    joined back before ``step`` returns (in stream order).
+    the pruned recursion, which occupies a few workgroups per utterance; the
+    combined loss follows them there once the pruned loss is final (beside
+    the joiner backward), and the stream is joined back before ``step``
+    returns (in stream order).
 
     With ``pruned_scale == 0`` (the warm-up of Sec. 4: the pruned part is
     disabled until the simple loss gives useful bounds) the pruned stages are
@@ -443,7 +445,8 @@ class PrunedRnntLoss:
     def _side_stream(self, device):
         key = device.index if device.index is not None else torch.cuda.current_device()
         if key not in self._side:
-            self._side[key] = (torch.cuda.Stream(device=device), torch.cuda.Event(), torch.cuda.Event())
+            self._side[key] = (torch.cuda.Stream(device=device), torch.cuda.Event(), torch.cuda.Event(),
+                               torch.cuda.Event())
         return self._side[key]
 
     def step(self, batch: Batch, am, lm, enc, dec, W, bias=None, stream=None, out=None,
@@ -520,23 +523,30 @@ class PrunedRnntLoss:
                                 lse=o("lse", (N, T, S)), logits=logits, workspace=ws_p, stream=main, head=head,
                                 head_rows=head_rows)
         if self.overlap:
-            side, fork, join = self._side_stream(dev)
+            side, fork, join, lossev = self._side_stream(dev)
             fork.record(main)
             side.wait_event(fork)
             simple_backward(side)
-            join.record(side)
         else:
             simple_backward(main)
         pl = rnnt_pruned_loss(batch, S, jo["px"], jo["py"], ranges, loss=o("pruned_loss", (N,)),
                               px_occ=o("pruned_px_occ", (N, T, S)), py_occ=o("pruned_py_occ", (N, T, S)),
                               workspace=ws_p, stream=main)
+        if self.overlap:
+            lossev.record(main)  # both losses are final here
         rnnt_pruned_joiner_backward(
             batch, S, enc, dec, W, bias, ranges, jo["lse"], pl["px_occ"], pl["py_occ"], scale=psc,
             enc_grad=enc_grad, dec_grad=dec_grad, W_grad=W_grad, bias_grad=bias_grad, workspace=ws_p,
             stream=main, logits=logits, chunk_rows=chunk, head=head, head_rows=head_rows)
-        res.update(rnnt_combine_losses(sim["loss"], pl["loss"], self.simple_scale, self.pruned_scale, reduction,
-                                       loss=o("loss", (N,)), total=o("total", ()), stream=main))
+        # the combined loss needs only the two losses: with the second stream
+        # it runs there, beside the joiner backward, instead of after it
         if self.overlap:
+            side.wait_event(lossev)
+        res.update(rnnt_combine_losses(sim["loss"], pl["loss"], self.simple_scale, self.pruned_scale, reduction,
+                                       loss=o("loss", (N,)), total=o("total", ()),
+                                       stream=side if self.overlap else main))
+        if self.overlap:
+            join.record(side)
             main.wait_event(join)
         res.update(pruned_loss=pl["loss"], ranges=ranges, px=jo["px"], py=jo["py"], lse=jo["lse"],
                    pruned_px_occ=pl["px_occ"], pruned_py_occ=pl["py_occ"])
