@@ -297,7 +297,7 @@ size_t rnnt_pruned_joiner_backward_workspace_size(int32_t N, int32_t T, int32_t 
  * every valid frame, frames in batch order): d(logits), h and the d dec
  * pieces are held for one chunk at a time. The chunk's size depends on J, V
  * and the dtype only, never on N or T (8,192 to 16,384 rows: d(logits) of
- * about 32 MiB at V = 500), so without the forward's logits no [N, T, S, V]
+ * about 16 MiB at V = 500), so without the forward's logits no [N, T, S, V]
  * array exists at any time.
  *
  * lse, px_occ, py_occ [N, T, S]: from rnnt_pruned_joiner / rnnt_pruned_loss.

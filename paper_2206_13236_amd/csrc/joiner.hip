@@ -1774,14 +1774,12 @@ static long long even_chunk(long long mmax, long long cap) {
   return ((mmax + n - 1) / n + 127) / 128 * 128;
 }
 
-// The backward's chunk: d(logits) of about 32 MiB, but 8,192 to 16,384 rows
+// The backward's chunk: d(logits) of about 16 MiB, but 8,192 to 16,384 rows
 // (64 to 128 row tiles, so that each launch of the pipelined backward puts
 // one or two workgroups of every kind on each CU), within the 32-bit limit.
-// fp32 at V ~ 500 takes 16,384 rows: a batch of up to that many rows runs
-// as one chunk whose logits the forward keeps as the head, so that nothing
-// is recomputed (BPE: 0.465 -> 0.415 ms per step against 16 MiB chunks of
-// 8,320 rows, 227 -> 375 MB peak); 32,768-row chunks measured slower at the
-// long shape (bf16 rows are already at 16,384).
+// The head the forward keeps is one chunk: the bound keeps it well below the
+// whole [N, T, S, V] logits at the benchmark shapes (a 32 MiB bound would
+// hold every row of the BPE batch in it).
 // The bound depends on J, V and the dtype only, not on N or T. Chunks are
 // taken whole from the start of the padded rows: rows past the last frame of
 // the batch (padding frames take none) are absent, so a trailing chunk that
@@ -1793,7 +1791,7 @@ int joiner_bwd_chunk_rows(int N, int T, int S, int J, int V, int bf16, int reque
   const long long all = (mmax + 127) / 128 * 128;
   if (request > 0) return (int)(request < all ? request : all);
   const long long bytes_per_row = (long long)joiner_ldl(V) * (bf16 ? 2 : 4);
-  long long cap = ((32ll << 20) / bytes_per_row) / 128 * 128;
+  long long cap = ((16ll << 20) / bytes_per_row) / 128 * 128;
   cap = cap < 8192 ? 8192 : cap > 16384 ? 16384 : cap;
   const long long lim = joiner_bwd_chunk_max_rows(J, V);
   if (cap > lim) cap = lim;
