@@ -464,29 +464,32 @@ __global__ __launch_bounds__(kEpiThreads) void normalizer_epi_kernel(SimpleArgs 
 // ---------------------------------------------------------------------------
 // Normaliser and its epilogue in one kernel (U + 1 <= 320). One workgroup
 // of 8 waves per (utterance, 32 frames) holds C[t][u] for every u of its
-// frames: C = sum over chunks of 64 v of e^{am - m_a} [32 x 64] .
-// e^{lm - m_l}^T [64 x U+1], both exponentials staged through LDS and the
-// next chunk's loads in flight during the current chunk's MFMAs; then Z, px
-// and py of its nodes (Eqs. (1)-(2), (5)) go to the rectangle, and through
-// LDS (the staging buffer reused) to the diagonal-major copies, diagonal by
-// diagonal. No split over v: no partial sums and no second launch. Wave w
-// holds the C blocks of rows 16 (w & 1) .. +15 whose u block is (w >> 1) +
-// 4 i. The blocks after the tiles fill the cells of the copies that no node
-// of the rectangle maps to.
+// frames: C = sum over chunks of v of e^{am - m_a} [32 x CV] .
+// e^{lm - m_l}^T [CV x U+1], both exponentials staged through two LDS
+// stages: the MFMAs of chunk c read one stage, then the exponentials of
+// chunk c+1 (loaded two chunks before) go to the other and chunk c+3's loads
+// are issued; one barrier per chunk. Then Z, px and py of its nodes (Eqs.
+// (1)-(2), (5)) go to the rectangle, and through LDS (the stages reused) to
+// the diagonal-major copies, diagonal by diagonal. No split over v: no
+// partial sums and no second launch. Wave w holds the C blocks of rows
+// 16 (w & 1) .. +15 whose u block is (w >> 1) + 4 i. The blocks after the
+// tiles fill the cells of the copies that no node of the rectangle maps to.
 // ---------------------------------------------------------------------------
 constexpr int kNfT = 32;         // frames per workgroup
-constexpr int kNfV = 64;         // v per chunk
+constexpr int kNfV = 64;         // v per chunk at U + 1 <= 64 (32 above: two stages of 64 would halve the workgroups per CU)
 constexpr int kNfThreads = 512;
-constexpr int kNfS = kNfV + 4;   // row stride of the staged chunks (conflict-free fragment reads)
 constexpr int kNfMaxU1 = 320;
 constexpr int kNfFill = 4;       // cells per thread of a fill block
+constexpr float kLog2eF = 1.44269504f;
 
 template <int KP>
 struct alignas(16) NfSmem {
+  static constexpr int CV = KP > 64 ? 32 : kNfV;  // v per chunk
+  static constexpr int S = CV + 4;                // row stride of a stage (conflict-free fragment reads)
   union {
     struct {
-      float ea[kNfT * kNfS];  // e^{am - m_a}, [t][v]
-      float el[KP * kNfS];    // e^{lm - m_l}, [u][v]
+      float ea[2][kNfT * S];  // e^{am - m_a}, [stage][t][v]
+      float el[2][KP * S];    // e^{lm - m_l}, [stage][u][v]
     } g;
     struct {
       float px[kNfT * KP];    // px, py of the tile's cells, [frame][slot of the lattice row]
@@ -498,17 +501,26 @@ struct alignas(16) NfSmem {
   int yy[KP];                          // y_{u+1}
 };
 
+// One chunk's loads in registers: a thread takes float4 number tid of the
+// am rows (if any) and tid + 512 i of the lm rows, the same rows in every
+// chunk (their maxima stay in registers).
+template <int KP>
 struct NfPrefetch {
-  float4 x;                        // am: 32 x 64 values over 512 threads
-  float4 l[kNfMaxU1 * 16 / kNfThreads];  // lm: KP x 64 values
+  static constexpr int Q = NfSmem<KP>::CV / 4;   // float4 per staged row
+  static constexpr int AQ = kNfT * Q;            // float4 of the am rows
+  static constexpr int NL = KP * Q / kNfThreads; // float4 of the lm rows per thread
+  static_assert(AQ <= kNfThreads && NL * kNfThreads == KP * Q, "staging split");
+  float4 x;
+  float4 l[NL];
 };
 
 template <int KP, bool V4>
-DEV void nf_load(Rsrc am, Rsrc lm, int t0, int v0, int Tn, int Un, int V, NfPrefetch& f) {
+DEV void nf_load(Rsrc am, Rsrc lm, int t0, int v0, int Tn, int Un, int V, NfPrefetch<KP>& f) {
+  using P = NfPrefetch<KP>;
   const int tid = threadIdx.x;
   {
-    const int t = t0 + tid / 16, v = v0 + 4 * (tid % 16);
-    const bool in = t < Tn && v < V;
+    const int t = t0 + tid / P::Q, v = v0 + 4 * (tid % P::Q);
+    const bool in = tid < P::AQ && t < Tn && v < V;
     const uint32_t o = (uint32_t)(t * V + v) * 4u;
     if (V4) {
       f.x = buf_load_f4(am, in ? o : kOob);
@@ -520,8 +532,8 @@ DEV void nf_load(Rsrc am, Rsrc lm, int t0, int v0, int Tn, int Un, int V, NfPref
     }
   }
 #pragma unroll
-  for (int i = 0; i < KP * 16 / kNfThreads; ++i) {
-    const int q = tid + i * kNfThreads, u = q / 16, v = v0 + 4 * (q % 16);
+  for (int i = 0; i < P::NL; ++i) {
+    const int q = tid + i * kNfThreads, u = q / P::Q, v = v0 + 4 * (q % P::Q);
     const bool in = u <= Un && v < V;
     const uint32_t o = (uint32_t)(u * V + v) * 4u;
     if (V4) {
@@ -535,43 +547,57 @@ DEV void nf_load(Rsrc am, Rsrc lm, int t0, int v0, int Tn, int Un, int V, NfPref
   }
 }
 
-template <int KP>
-DEV void nf_store(NfSmem<KP>& sm, const NfPrefetch& f, int t0, int v0, int Tn, int Un, int V) {
+// e^{x - m} = 2^{x log2(e) - m log2(e)} of one chunk into stage st (m2 =
+// m log2(e) per staged row). Rows past the utterance (loaded as zeros) only
+// feed C entries of absent nodes, which nothing reads; the columns past V
+// (the last chunk only, TAIL) are zeroed.
+template <int KP, bool TAIL>
+DEV void nf_store(NfSmem<KP>& sm, int st, const NfPrefetch<KP>& f, float ma2, const float (&ml2)[NfPrefetch<KP>::NL],
+                  int v0, int V) {
+  using P = NfPrefetch<KP>;
+  constexpr int S = NfSmem<KP>::S;
   const int tid = threadIdx.x;
-  {
-    const int t = tid / 16, c = 4 * (tid % 16);
-    const bool row = t0 + t < Tn;
-    const float m = sm.ma[t];
-    const float xv[4] = {f.x.x, f.x.y, f.x.z, f.x.w};
+  auto ex = [&](float4 x, float m2, int c) {
+    const float xv[4] = {x.x, x.y, x.z, x.w};
     float e[4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) e[j] = (row && v0 + c + j < V) ? __expf(xv[j] - m) : 0.f;
-    *reinterpret_cast<float4*>(&sm.g.ea[t * kNfS + c]) = make_float4(e[0], e[1], e[2], e[3]);
+    for (int j = 0; j < 4; ++j) {
+      e[j] = __builtin_amdgcn_exp2f(fmaf(xv[j], kLog2eF, -m2));
+      if (TAIL && v0 + c + j >= V) e[j] = 0.f;
+    }
+    return make_float4(e[0], e[1], e[2], e[3]);
+  };
+  if (tid < P::AQ) {
+    const int t = tid / P::Q, c = 4 * (tid % P::Q);
+    *reinterpret_cast<float4*>(&sm.g.ea[st][t * S + c]) = ex(f.x, ma2, c);
   }
 #pragma unroll
-  for (int i = 0; i < KP * 16 / kNfThreads; ++i) {
-    const int q = tid + i * kNfThreads, u = q / 16, c = 4 * (q % 16);
-    const bool row = u <= Un;
-    const float m = sm.ml[u];
-    const float xv[4] = {f.l[i].x, f.l[i].y, f.l[i].z, f.l[i].w};
-    float e[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) e[j] = (row && v0 + c + j < V) ? __expf(xv[j] - m) : 0.f;
-    *reinterpret_cast<float4*>(&sm.g.el[u * kNfS + c]) = make_float4(e[0], e[1], e[2], e[3]);
+  for (int i = 0; i < P::NL; ++i) {
+    const int q = tid + i * kNfThreads, u = q / P::Q, c = 4 * (q % P::Q);
+    *reinterpret_cast<float4*>(&sm.g.el[st][u * S + c]) = ex(f.l[i], ml2[i], c);
   }
+}
+
+template <int KP>
+DEV void nf_store_chunk(NfSmem<KP>& sm, int st, const NfPrefetch<KP>& f, float ma2,
+                        const float (&ml2)[NfPrefetch<KP>::NL], int v0, int V) {
+  if (v0 + NfSmem<KP>::CV <= V) nf_store<KP, false>(sm, st, f, ma2, ml2, v0, V);
+  else nf_store<KP, true>(sm, st, f, ma2, ml2, v0, V);
 }
 
 template <int KP, bool V4>
 __global__ __launch_bounds__(kNfThreads) void normalizer_fused_kernel(SimpleArgs a) {
   __shared__ NfSmem<KP> sm;
+  using P = NfPrefetch<KP>;
+  constexpr int CV = NfSmem<KP>::CV, S = NfSmem<KP>::S;
   const int T = a.b.T, U1 = a.b.U + 1, V = a.V, blank = a.b.blank;
-  const int ntt = (T + kNfT - 1) / kNfT;
+  const int ntt = (T + kNfT - 1) / kNfT, tiles = a.b.N * ntt;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, l16 = lane & 15, g4 = lane >> 4;
   const int R = lattice_rows_per_lane_dev(U1), W = 64 * R;  // W <= KP
-  if ((int)blockIdx.x >= a.b.N * ntt) {
+  if ((int)blockIdx.x >= tiles) {
 #pragma unroll
     for (int k = 0; k < kNfFill; ++k)
-      lattice_fill_outside(a.pxd, a.pyd, (int)blockIdx.x - a.b.N * ntt, tid + k * kNfThreads, kNfFill * kNfThreads, T,
+      lattice_fill_outside(a.pxd, a.pyd, (int)blockIdx.x - tiles, tid + k * kNfThreads, kNfFill * kNfThreads, T,
                            U1, R);
     return;
   }
@@ -581,7 +607,7 @@ __global__ __launch_bounds__(kNfThreads) void normalizer_fused_kernel(SimpleArgs
   const bool smooth = a.lm_only != 0.f || a.am_only != 0.f;
   const float* amn = a.am + (size_t)n * T * V;
   const float* lmn = a.lm + (size_t)n * U1 * V;
-  // per-frame and per-u values of the epilogue (and the offsets of the staging)
+  // per-frame and per-u values of the epilogue (and the maxima of the staging)
   if (tid < kNfT) {
     const int t = t0 + tid;
     const bool node = t < Tn;
@@ -602,34 +628,57 @@ __global__ __launch_bounds__(kNfThreads) void normalizer_fused_kernel(SimpleArgs
   }
   __syncthreads();
   const int kn = (Un + 1 + 15) / 16 * 16;
-  const int tb = wave & 1;
+  const int tb = wave & 1, ubw = __builtin_amdgcn_readfirstlane(wave >> 1);
   constexpr int NB = KP / 64;  // C blocks per wave: u block (w >> 1) + 4 i
   floatx4 acc[NB];
 #pragma unroll
   for (int i = 0; i < NB; ++i) acc[i] = floatx4{0.f, 0.f, 0.f, 0.f};
   if (t0 < Tn) {
     const Rsrc amr = make_rsrc(amn, (size_t)T * V * 4), lmr = make_rsrc(lmn, (size_t)U1 * V * 4);
-    const int nc = (V + kNfV - 1) / kNfV;
-    NfPrefetch f;
-    nf_load<KP, V4>(amr, lmr, t0, 0, Tn, Un, V, f);
-    for (int c = 0; c < nc; ++c) {
-      sg_barrier();  // the previous chunk's LDS reads are done
-      nf_store<KP>(sm, f, t0, c * kNfV, Tn, Un, V);
-      sg_barrier();
-      if (c + 1 < nc) nf_load<KP, V4>(amr, lmr, t0, (c + 1) * kNfV, Tn, Un, V, f);
+    const float ma2 = tid < P::AQ ? sm.ma[tid / P::Q] * kLog2eF : 0.f;
+    float ml2[P::NL];
 #pragma unroll
-      for (int kk = 0; kk < kNfV; kk += 16) {
-        const floatx4 fa = *reinterpret_cast<const floatx4*>(&sm.g.ea[(16 * tb + l16) * kNfS + kk + 4 * g4]);
+    for (int i = 0; i < P::NL; ++i) ml2[i] = sm.ml[(tid + i * kNfThreads) / P::Q] * kLog2eF;
+    const int nc = (V + CV - 1) / CV;
+    // chunk c (> 0) in f[c % 2]; chunks past V load zeros (kOob): the loads
+    // stay unconditional, so that each store waits only for its own chunk
+    P f[2];
+    nf_load<KP, V4>(amr, lmr, t0, 0, Tn, Un, V, f[0]);
+    nf_store_chunk<KP>(sm, 0, f[0], ma2, ml2, 0, V);
+    nf_load<KP, V4>(amr, lmr, t0, CV, Tn, Un, V, f[1]);
+    nf_load<KP, V4>(amr, lmr, t0, 2 * CV, Tn, Un, V, f[0]);
+    sg_barrier();
+    auto step = [&](int c, P& fn) {
+      const int st = c & 1;
+      // chunk c: every fragment of the stage first, then the MFMAs of the
+      // wave's u blocks that hold rows of the utterance
+      floatx4 fa[CV / 16], fb[CV / 16][NB];
 #pragma unroll
-        for (int i = 0; i < NB; ++i) {
-          const int ub = (wave >> 1) + 4 * i;
-          if (16 * ub < kn) {
-            const floatx4 fb = *reinterpret_cast<const floatx4*>(&sm.g.el[(16 * ub + l16) * kNfS + kk + 4 * g4]);
+      for (int k = 0; k < CV / 16; ++k) {
+        fa[k] = *reinterpret_cast<const floatx4*>(&sm.g.ea[st][(16 * tb + l16) * S + 16 * k + 4 * g4]);
 #pragma unroll
-            for (int q = 0; q < 4; ++q) acc[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[q], fb[q], acc[i], 0, 0, 0);
-          }
-        }
+        for (int i = 0; i < NB; ++i)
+          fb[k][i] = *reinterpret_cast<const floatx4*>(&sm.g.el[st][(16 * (ubw + 4 * i) + l16) * S + 16 * k + 4 * g4]);
       }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int k = 0; k < CV / 16; ++k)
+#pragma unroll
+        for (int i = 0; i < NB; ++i)
+          if (16 * (ubw + 4 * i) < kn) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+              acc[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[k][q], fb[k][i][q], acc[i], 0, 0, 0);
+          }
+      // chunk c+1 into the other stage (last read by chunk c-1, before the
+      // previous barrier), then chunk c+3's loads
+      if (c + 1 < nc) nf_store_chunk<KP>(sm, st ^ 1, fn, ma2, ml2, (c + 1) * CV, V);
+      nf_load<KP, V4>(amr, lmr, t0, (c + 3) * CV, Tn, Un, V, fn);
+      sg_barrier();
+    };
+    for (int c = 0; c < nc; c += 2) {
+      step(c, f[1]);
+      if (c + 1 < nc) step(c + 1, f[0]);
     }
   }
   // epilogue: the target logits am[t, y_u] of the lane's nodes first (one gather round)
@@ -637,7 +686,7 @@ __global__ __launch_bounds__(kNfThreads) void normalizer_fused_kernel(SimpleArgs
   float ay[NB][4];
 #pragma unroll
   for (int i = 0; i < NB; ++i) {
-    const int u = 16 * ((wave >> 1) + 4 * i) + l16;
+    const int u = 16 * (ubw + 4 * i) + l16;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int t = t0 + 16 * tb + 4 * g4 + r;
@@ -645,14 +694,14 @@ __global__ __launch_bounds__(kNfThreads) void normalizer_fused_kernel(SimpleArgs
       ay[i][r] = buf_load_f32(amr, node ? (uint32_t)(t * V + sm.yy[u]) * 4u : kOob);
     }
   }
-  sg_barrier();  // every wave's MFMAs are done with the staging buffer
+  sg_barrier();  // every wave's MFMAs are done with the stages
   const float cw = 1.f - a.lm_only - a.am_only;
   const float* la = a.lavg + (size_t)n * V;
   const float lab = smooth ? la[blank] : 0.f;
   const size_t L0 = ((size_t)n * T) * U1;
 #pragma unroll
   for (int i = 0; i < NB; ++i) {
-    const int u = 16 * ((wave >> 1) + 4 * i) + l16;
+    const int u = 16 * (ubw + 4 * i) + l16;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int tl = 16 * tb + 4 * g4 + r, t = t0 + tl;
@@ -1370,10 +1419,10 @@ hipError_t launch_normalizer(const SimpleArgs& a, hipStream_t s) {
       (tiles >= 192 || chunks <= 16)) {
     // every u of 32 frames per workgroup, the epilogue in the same kernel;
     // u extent as in the fused gradient kernel. Its workgroups run the whole
-    // of V in sequence: with far fewer tiles than CUs and a long V (largev:
-    // 160 tiles, 79 chunks, 137 against 123 us) the split kernels below are
-    // faster; at the stress shape (248 tiles, 125 chunks) this one is (661
-    // against 756 us).
+    // of V in sequence: with far fewer tiles than CUs and a long V (160
+    // tiles, 79 chunks of 64 at V = 5000: 112 against 108 us) the split
+    // kernels below are faster; with 248 tiles and 125 chunks (V = 8000,
+    // U + 1 <= 301) this one is (550 against 756 us).
     const size_t blocks = (size_t)a.b.N * ((T + kNfT - 1) / kNfT) +
                           (size_t)a.b.N * lattice_fill_blocks(T, a.b.U, kNfFill * kNfThreads);
     const bool v4 = (a.V & 3) == 0;
