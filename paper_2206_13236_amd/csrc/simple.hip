@@ -1123,7 +1123,8 @@ template <int KP, bool V4>
 DEV void sg_item(const SimpleArgs& a, int splits, SgSmem<KP>& sm, int v0, int sk, int n) {
   constexpr int K = SgSmem<KP>::K;
   const int T = a.b.T, U1 = a.b.U + 1, V = a.V, blank = a.b.blank;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, l16 = lane & 15, g4 = lane >> 4;
+  const int tid = threadIdx.x, lane = tid & 63, l16 = lane & 15, g4 = lane >> 4;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // (uniform: the block guards below are scalar)
   int Tn, Un;
   utt_dims(a.b, n, Tn, Un);
   const int kn = (Un + 1 + 15) / 16 * 16;  // contraction length of d am; u blocks of d lm = kn / 16
@@ -1203,6 +1204,7 @@ DEV void sg_item(const SimpleArgs& a, int splits, SgSmem<KP>& sm, int v0, int sk
   const int nsteps = (T + kSgT - 1) / kSgT, per = (nsteps + splits - 1) / splits;
   const int s0 = sk * per, s1 = min(nsteps, s0 + per);
   constexpr int NUB = KP / 16 / kSgUg;  // d lm u blocks per wave (u block ug + kSgUg i)
+  static_assert(KP % 64 == 0, "d am reads its fragments in batches of 64 rows");
   floatx4 accl[NUB];
 #pragma unroll
   for (int i = 0; i < NUB; ++i) accl[i] = floatx4{0.f, 0.f, 0.f, 0.f};
@@ -1220,35 +1222,50 @@ DEV void sg_item(const SimpleArgs& a, int splits, SgSmem<KP>& sm, int v0, int sk
 #pragma unroll
     for (int j = 0; j < kSgDam; ++j) accd[j] = floatx4{0.f, 0.f, 0.f, 0.f};
     if (live) {
-      // d am: W rows of the wave's 16 frames against e^{lm - m_l} columns
+      // d am: W rows of the wave's 16 frames against e^{lm - m_l} columns,
+      // over the utterance's kn rows in batches of 64 (the batch's fragments
+      // read first; KP is a multiple of 64, so they are inside the rows)
 #pragma unroll
-      for (int kk = 0; kk < KP; kk += 16) {
-        if (kk < kn) {
-          const floatx4 fa = *reinterpret_cast<const floatx4*>(&sm.wt[(16 * tb + l16) * K + kk + 4 * g4]);
+      for (int kb = 0; kb < KP; kb += 64) {
+        if (kb < kn) {
+          floatx4 fa[4], fb[4][kSgDam];
 #pragma unroll
-          for (int j = 0; j < kSgDam; ++j) {
-            const floatx4 fb = *reinterpret_cast<const floatx4*>(&sm.elT[(16 * (vb0 + j) + l16) * K + kk + 4 * g4]);
+          for (int s4 = 0; s4 < 4; ++s4) {
+            const int kk = kb + 16 * s4;
+            fa[s4] = *reinterpret_cast<const floatx4*>(&sm.wt[(16 * tb + l16) * K + kk + 4 * g4]);
 #pragma unroll
-            for (int q = 0; q < 4; ++q) accd[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[q], fb[q], accd[j], 0, 0, 0);
+            for (int j = 0; j < kSgDam; ++j)
+              fb[s4][j] = *reinterpret_cast<const floatx4*>(&sm.elT[(16 * (vb0 + j) + l16) * K + kk + 4 * g4]);
           }
+#pragma unroll
+          for (int s4 = 0; s4 < 4; ++s4)
+            if (kb + 16 * s4 < kn) {
+#pragma unroll
+              for (int j = 0; j < kSgDam; ++j)
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+                  accd[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[s4][q], fb[s4][j][q], accd[j], 0, 0, 0);
+            }
         }
       }
       // d lm: W^T (u rows) against e^{am - m_a} of the wave's 16 columns; the
-      // A fragment's 4 frames are one per row of wt (k-permuted like B)
+      // A fragment's 4 frames are one per row of wt (k-permuted like B). All
+      // fragments of a 16-frame half are read first (rows past kn too: they
+      // are inside wt), then the MFMAs of the u blocks that hold rows.
 #pragma unroll
       for (int kk = 0; kk < kSgT; kk += 16) {
         const floatx4 fb = *reinterpret_cast<const floatx4*>(&sm.eaT[(16 * lvb + l16) * kSgTS + kk + 4 * g4]);
+        float fa[NUB][4];
 #pragma unroll
-        for (int i = 0; i < NUB; ++i) {
-          const int ub = ug + kSgUg * i;
-          if (16 * ub < kn) {  // (a guard, not an exit: the loop stays fully unrolled)
-            floatx4 fa;
+        for (int i = 0; i < NUB; ++i)
 #pragma unroll
-            for (int q = 0; q < 4; ++q) fa[q] = sm.wt[(kk + 4 * g4 + q) * K + 16 * ub + l16];
+          for (int q = 0; q < 4; ++q) fa[i][q] = sm.wt[(kk + 4 * g4 + q) * K + 16 * (ug + kSgUg * i) + l16];
 #pragma unroll
-            for (int q = 0; q < 4; ++q) accl[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[q], fb[q], accl[i], 0, 0, 0);
+        for (int i = 0; i < NUB; ++i)
+          if (16 * (ug + kSgUg * i) < kn) {  // (a guard, not an exit: the loop stays fully unrolled)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) accl[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[i][q], fb[q], accl[i], 0, 0, 0);
           }
-        }
       }
     }
     // d am epilogue: e^{am - m_a} * acc, minus gx at the targets (ascending
