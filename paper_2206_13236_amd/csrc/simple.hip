@@ -547,42 +547,43 @@ DEV void nf_load(Rsrc am, Rsrc lm, int t0, int v0, int Tn, int Un, int V, NfPref
   }
 }
 
-// e^{x - m} = 2^{x log2(e) - m log2(e)} of one chunk into stage st (m2 =
-// m log2(e) per staged row). Rows past the utterance (loaded as zeros) only
-// feed C entries of absent nodes, which nothing reads; the columns past V
-// (the last chunk only, TAIL) are zeroed.
+// e^{x - m} = 2^{(x - m) log2(e)} of one chunk into stage st (m per staged
+// row; x - m first, so that a row's maximum gives exactly 1 and no rounding
+// of m log2(e) biases a whole row). Rows past the utterance (loaded as
+// zeros) only feed C entries of absent nodes, which nothing reads; the
+// columns past V (the last chunk only, TAIL) are zeroed.
 template <int KP, bool TAIL>
-DEV void nf_store(NfSmem<KP>& sm, int st, const NfPrefetch<KP>& f, float ma2, const float (&ml2)[NfPrefetch<KP>::NL],
+DEV void nf_store(NfSmem<KP>& sm, int st, const NfPrefetch<KP>& f, float mA, const float (&mL)[NfPrefetch<KP>::NL],
                   int v0, int V) {
   using P = NfPrefetch<KP>;
   constexpr int S = NfSmem<KP>::S;
   const int tid = threadIdx.x;
-  auto ex = [&](float4 x, float m2, int c) {
+  auto ex = [&](float4 x, float m, int c) {
     const float xv[4] = {x.x, x.y, x.z, x.w};
     float e[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      e[j] = __builtin_amdgcn_exp2f(fmaf(xv[j], kLog2eF, -m2));
+      e[j] = __builtin_amdgcn_exp2f((xv[j] - m) * kLog2eF);
       if (TAIL && v0 + c + j >= V) e[j] = 0.f;
     }
     return make_float4(e[0], e[1], e[2], e[3]);
   };
   if (tid < P::AQ) {
     const int t = tid / P::Q, c = 4 * (tid % P::Q);
-    *reinterpret_cast<float4*>(&sm.g.ea[st][t * S + c]) = ex(f.x, ma2, c);
+    *reinterpret_cast<float4*>(&sm.g.ea[st][t * S + c]) = ex(f.x, mA, c);
   }
 #pragma unroll
   for (int i = 0; i < P::NL; ++i) {
     const int q = tid + i * kNfThreads, u = q / P::Q, c = 4 * (q % P::Q);
-    *reinterpret_cast<float4*>(&sm.g.el[st][u * S + c]) = ex(f.l[i], ml2[i], c);
+    *reinterpret_cast<float4*>(&sm.g.el[st][u * S + c]) = ex(f.l[i], mL[i], c);
   }
 }
 
 template <int KP>
-DEV void nf_store_chunk(NfSmem<KP>& sm, int st, const NfPrefetch<KP>& f, float ma2,
-                        const float (&ml2)[NfPrefetch<KP>::NL], int v0, int V) {
-  if (v0 + NfSmem<KP>::CV <= V) nf_store<KP, false>(sm, st, f, ma2, ml2, v0, V);
-  else nf_store<KP, true>(sm, st, f, ma2, ml2, v0, V);
+DEV void nf_store_chunk(NfSmem<KP>& sm, int st, const NfPrefetch<KP>& f, float mA,
+                        const float (&mL)[NfPrefetch<KP>::NL], int v0, int V) {
+  if (v0 + NfSmem<KP>::CV <= V) nf_store<KP, false>(sm, st, f, mA, mL, v0, V);
+  else nf_store<KP, true>(sm, st, f, mA, mL, v0, V);
 }
 
 template <int KP, bool V4>
@@ -635,16 +636,16 @@ __global__ __launch_bounds__(kNfThreads) void normalizer_fused_kernel(SimpleArgs
   for (int i = 0; i < NB; ++i) acc[i] = floatx4{0.f, 0.f, 0.f, 0.f};
   if (t0 < Tn) {
     const Rsrc amr = make_rsrc(amn, (size_t)T * V * 4), lmr = make_rsrc(lmn, (size_t)U1 * V * 4);
-    const float ma2 = tid < P::AQ ? sm.ma[tid / P::Q] * kLog2eF : 0.f;
-    float ml2[P::NL];
+    const float mA = tid < P::AQ ? sm.ma[tid / P::Q] : 0.f;
+    float mL[P::NL];
 #pragma unroll
-    for (int i = 0; i < P::NL; ++i) ml2[i] = sm.ml[(tid + i * kNfThreads) / P::Q] * kLog2eF;
+    for (int i = 0; i < P::NL; ++i) mL[i] = sm.ml[(tid + i * kNfThreads) / P::Q];
     const int nc = (V + CV - 1) / CV;
     // chunk c (> 0) in f[c % 2]; chunks past V load zeros (kOob): the loads
     // stay unconditional, so that each store waits only for its own chunk
     P f[2];
     nf_load<KP, V4>(amr, lmr, t0, 0, Tn, Un, V, f[0]);
-    nf_store_chunk<KP>(sm, 0, f[0], ma2, ml2, 0, V);
+    nf_store_chunk<KP>(sm, 0, f[0], mA, mL, 0, V);
     nf_load<KP, V4>(amr, lmr, t0, CV, Tn, Un, V, f[1]);
     nf_load<KP, V4>(amr, lmr, t0, 2 * CV, Tn, Un, V, f[0]);
     sg_barrier();
@@ -672,7 +673,7 @@ __global__ __launch_bounds__(kNfThreads) void normalizer_fused_kernel(SimpleArgs
           }
       // chunk c+1 into the other stage (last read by chunk c-1, before the
       // previous barrier), then chunk c+3's loads
-      if (c + 1 < nc) nf_store_chunk<KP>(sm, st ^ 1, fn, ma2, ml2, (c + 1) * CV, V);
+      if (c + 1 < nc) nf_store_chunk<KP>(sm, st ^ 1, fn, mA, mL, (c + 1) * CV, V);
       nf_load<KP, V4>(amr, lmr, t0, (c + 3) * CV, Tn, Un, V, fn);
       sg_barrier();
     };
