@@ -199,6 +199,13 @@ DEV void beta_frame(double& bt, const FrameIn& f, const ScanSrc& v, int s, int r
   bt = act ? be : bt;
 }
 
+// The scan's kernels are the step's critical path while the simple loss's
+// gradients run beside them on another stream: their waves take the highest
+// issue priority, so that a SIMD shared with those contractions issues the
+// recursion's dependent instructions first. Priority only orders issue; it
+// changes no result.
+DEV void raise_wave_priority() { __builtin_amdgcn_s_setprio(3); }
+
 // Wave w of the grid: chains 4g .. 4g+3 (one per 16-lane row) of chunk c of
 // utterance n. Each chain starts from a unit arrival at slot i of the
 // chunk's first frame and runs the chunk's frames; the arrivals at the next
@@ -206,6 +213,7 @@ DEV void beta_frame(double& bt, const FrameIn& f, const ScanSrc& v, int s, int r
 // is E[i].
 template <int K>
 __global__ __launch_bounds__(256) void scan_chunk_kernel(BandArgs a) {
+  raise_wave_priority();
   const int lane = threadIdx.x & 63, row = lane >> 4, s = lane & 15;
   const int S = a.S, nc = a.nchunk, G = (S + 3) >> 2;
   const int w = blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // uniform: scalar resources
@@ -286,6 +294,7 @@ DEV double readlane_d(double v, int l) {
 // (straight-line buffer loads, so the wait counts stay exact).
 template <int NS>  // slots carried: S <= NS (NS = S up to 8, so that no step works on padding slots)
 __global__ __launch_bounds__(128) void scan_sweep_kernel(BandArgs a) {
+  raise_wave_priority();
   const int n = blockIdx.x;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -363,6 +372,7 @@ __global__ __launch_bounds__(128) void scan_sweep_kernel(BandArgs a) {
 // occupations frame by frame.
 template <int K>
 __global__ __launch_bounds__(128) void scan_replay_kernel(BandArgs a) {
+  raise_wave_priority();
   // one spare frame row takes the stores of steps past a chunk's end
   // [4 rows][C + 1 frames][16 slots] each, sized by C at launch; frame C is
   // the spare row that takes the stores of steps past a chunk's end
