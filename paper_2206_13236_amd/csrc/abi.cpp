@@ -196,7 +196,7 @@ struct JoinerFwdWs {
   float2* part;
   float* tgt;
   float* blk;
-  void* h;
+  void* h[2];
   void* wt;
   int chunk_rows;
   size_t bytes;
@@ -212,8 +212,10 @@ JoinerFwdWs joiner_fwd_layout(void* base, int N, int T, int S, int J, int V, int
   w.part = c.take<float2>(M * joiner_nparts(V));
   w.tgt = c.take<float>(M);
   w.blk = c.take<float>(M);
+  // two h slots: a chunk's GEMM launch writes the next chunk's h beside it
   const size_t h_elems = joiner_fwd_uses_hbuf(bf16) ? (size_t)w.chunk_rows * J : 0;
-  w.h = h_elems == 0 ? nullptr : bf16 ? (void*)c.take<uint16_t>(h_elems) : (void*)c.take<float>(h_elems);
+  for (int k = 0; k < 2; ++k)
+    w.h[k] = h_elems == 0 ? nullptr : bf16 ? (void*)c.take<uint16_t>(h_elems) : (void*)c.take<float>(h_elems);
   w.wt = bf16 ? (void*)c.take<uint16_t>((size_t)V * J) : nullptr;
   w.bytes = c.off;
   return w;
@@ -349,7 +351,9 @@ void set_joiner_fwd(JoinerArgs& a, const JoinerFwdWs& w, float* px, float* py, f
   a.nparts = joiner_nparts(a.V);
   a.tgt = w.tgt;
   a.blk = w.blk;
-  a.hbuf = w.h;
+  a.hbuf = w.h[0];
+  a.hring[0] = w.h[0];
+  a.hring[1] = w.h[1];
   a.wt = w.wt;
   a.chunk_rows = w.chunk_rows;
   a.px = px;

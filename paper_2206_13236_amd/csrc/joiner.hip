@@ -454,17 +454,18 @@ __global__ __launch_bounds__(256) void joiner_prep_kernel(JoinerArgs a, int wpad
 // row info and are skipped).
 // ---------------------------------------------------------------------------
 constexpr int kHItems = 4;
-template <bool BF>
-__global__ __launch_bounds__(256) void joiner_h_kernel(JoinerArgs a, int cm0, int cm1) {
+// Block blk of NT threads of an h pass into hdst (the chunk's rows from cm0).
+template <bool BF, int NT>
+DEV void h_rows_block(const JoinerArgs& a, void* hdst, int cm0, int cm1, int blk) {
   using TIn = typename In<BF>::T;
   constexpr int KV = 16 / (int)sizeof(TIn);
   const int cpr = a.J / KV;
-  const size_t base = (size_t)blockIdx.x * (256 * kHItems) + threadIdx.x;
+  const size_t base = (size_t)blk * (NT * kHItems) + threadIdx.x;
   int rr[kHItems], jj[kHItems];
   int4 info[kHItems];
 #pragma unroll
   for (int k = 0; k < kHItems; ++k) {
-    const size_t i = base + (size_t)k * 256;
+    const size_t i = base + (size_t)k * NT;
     rr[k] = (int)(i / cpr);
     jj[k] = (int)(i - (size_t)rr[k] * cpr) * KV;
     // within the row info array (cm1 <= N*T*S); rows past M are masked below
@@ -497,26 +498,45 @@ __global__ __launch_bounds__(256) void joiner_h_kernel(JoinerArgs a, int cm0, in
     } else {
       o = make_uint4(__float_as_uint(h[0]), __float_as_uint(h[1]), __float_as_uint(h[2]), __float_as_uint(h[3]));
     }
-    *reinterpret_cast<uint4*>(reinterpret_cast<TIn*>(a.hbuf) + (size_t)rr[k] * a.J + jj[k]) = o;
+    *reinterpret_cast<uint4*>(reinterpret_cast<TIn*>(hdst) + (size_t)rr[k] * a.J + jj[k]) = o;
   }
 }
+
+template <bool BF>
+__global__ __launch_bounds__(256) void joiner_h_kernel(JoinerArgs a, int cm0, int cm1) {
+  h_rows_block<BF, 256>(a, a.hbuf, cm0, cm1, blockIdx.x);
+}
+
+// The h pass of the next forward chunk, run by the trailing blocks of the
+// current chunk's GEMM launch (bf16): rows [cm0, cm1) into h.
+struct HNext {
+  void* h;
+  int cm0, cm1, blocks;
+};
 
 // ---------------------------------------------------------------------------
 // Forward GEMM + partial log-sum-exp over the rows [cm0, cm1) (h in hbuf)
 // ---------------------------------------------------------------------------
 template <bool BF, int WM, bool WIDE = false>
-__global__ __launch_bounds__(WIDE ? CfgBWide::NT : kGemmThreads, 4) void joiner_fwd_kernel(JoinerArgs a, int cm0, int cm1) {
+__global__ __launch_bounds__(WIDE ? CfgBWide::NT : kGemmThreads, 4) void joiner_fwd_kernel(JoinerArgs a, int cm0, int cm1,
+                                                                                            int ncol, int ngemm,
+                                                                                            HNext hn) {
   using TIn = typename In<BF>::T;
   using Cfg = typename std::conditional<WIDE, CfgBWide, typename In<BF>::Cfg>::type;
   static_assert(!WIDE || BF, "wide tiles for bf16");
   __shared__ __align__(16) typename Cfg::T smem[Cfg::SMEM_BYTES / sizeof(typename Cfg::T)];
   __shared__ int4 ri[Cfg::BM];
+  // blocks past the ngemm tile blocks: the next chunk's h pass (its own slot)
+  if ((int)blockIdx.x >= ngemm) {
+    if constexpr (BF) h_rows_block<BF, Cfg::NT>(a, hn.h, hn.cm0, hn.cm1, blockIdx.x - ngemm);
+    return;
+  }
   const int M = a.frame_off[a.b.N] * a.S;
   const int mend = min(cm1, M);
   // the column tiles of one row tile are consecutive tile ids (one XCD, shared A panel)
-  const int tile = xcd_tile_id(mend > cm0 ? (mend - cm0 + Cfg::BM - 1) / Cfg::BM * gridDim.y : 0);
+  const int tile = xcd_tile_id(mend > cm0 ? (mend - cm0 + Cfg::BM - 1) / Cfg::BM * ncol : 0);
   if (tile < 0) return;
-  const int mt = tile / gridDim.y, nt = tile - mt * gridDim.y;
+  const int mt = tile / ncol, nt = tile - mt * ncol;
   const int m0 = cm0 + mt * Cfg::BM;
   const int v0 = nt * Cfg::BN;
   const int V = a.V, J = a.J;
@@ -1858,26 +1878,53 @@ hipError_t launch_joiner_h(const JoinerArgs& a, int cm0, int cm1, hipStream_t s)
 
 hipError_t launch_joiner_fwd(const JoinerArgs& a, hipStream_t s) {
   const int mmax = a.b.N * a.b.T * a.S;
-  for (int cm0 = 0; cm0 < mmax; cm0 += a.chunk_rows) {
-    const int cm1 = (cm0 + a.chunk_rows < mmax) ? cm0 + a.chunk_rows : mmax;
-    if (a.bf16 ? kFwdHbuf<true> : kFwdHbuf<false>) {
-      const hipError_t e = launch_joiner_h(a, cm0, cm1, s);
-      if (e != hipSuccess) return e;
+  const int C = a.chunk_rows;
+  const int nch = (mmax + C - 1) / C;
+  auto lo = [&](int k) { return k * C; };
+  auto hi = [&](int k) { return (k + 1) * C < mmax ? (k + 1) * C : mmax; };
+  const bool hbuf = a.bf16 ? kFwdHbuf<true> : kFwdHbuf<false>;
+  // bf16: h of chunk k in slot k % 2; chunk 0's h pass runs alone, that of
+  // chunk k + 1 as the trailing blocks of chunk k's GEMM launch (they write
+  // the slot chunk k - 1's launch read)
+  auto slot = [&](int k) { return a.hring[k % 2]; };
+  if (hbuf) {
+    JoinerArgs c = a;
+    c.hbuf = slot(0);
+    const hipError_t e = launch_joiner_h(c, lo(0), hi(0), s);
+    if (e != hipSuccess) return e;
+  }
+  for (int k = 0; k < nch; ++k) {
+    const int cm0 = lo(k), cm1 = hi(k);
+    JoinerArgs c = a;
+    HNext hn{};
+    if (hbuf) c.hbuf = slot(k);
+    const bool wide = a.bf16 && a.V >= kFwdWideV;
+    const int bm = wide ? CfgBWide::BM : 128, bn = wide ? CfgBWide::BN : 128;
+    const int nt = wide ? CfgBWide::NT : kGemmThreads;
+    if (hbuf && k + 1 < nch) {
+      const size_t groups = (size_t)(hi(k + 1) - lo(k + 1)) * (a.J / (a.bf16 ? 8 : 4));
+      hn = HNext{slot(k + 1), lo(k + 1), hi(k + 1), (int)((groups + nt * kHItems - 1) / (nt * kHItems))};
     }
-    const dim3 grid((cm1 - cm0 + 127) / 128, (a.V + 127) / 128);
+    const int ncol = (a.V + bn - 1) / bn;
+    const int ngemm = (cm1 - cm0 + bm - 1) / bm * ncol;
+    const dim3 grid((unsigned)(ngemm + hn.blocks));
     RNNT_PROF(s, "joiner_fwd");
     // fp32 W rows (length V) are read in segments of 4 elements; bf16 reads
     // the transposed copy, whose rows (length J) are whole 16-byte chunks
     const int wm = host_seg_mode(a.V, 4, 0);
-    if (a.bf16 && a.V >= kFwdWideV) {
-      const dim3 gw((cm1 - cm0 + CfgBWide::BM - 1) / CfgBWide::BM, (a.V + CfgBWide::BN - 1) / CfgBWide::BN);
-      hipLaunchKernelGGL((joiner_fwd_kernel<true, kSegVector, true>), gw, dim3(CfgBWide::NT), 0, s, a, cm0, cm1);
+    if (wide) {
+      hipLaunchKernelGGL((joiner_fwd_kernel<true, kSegVector, true>), grid, dim3(nt), 0, s, c, cm0, cm1, ncol, ngemm,
+                         hn);
     } else if (a.bf16) {
-      hipLaunchKernelGGL((joiner_fwd_kernel<true, kSegVector>), grid, dim3(kGemmThreads), 0, s, a, cm0, cm1);
+      hipLaunchKernelGGL((joiner_fwd_kernel<true, kSegVector>), grid, dim3(nt), 0, s, c, cm0, cm1, ncol, ngemm, hn);
     } else {
-      if (wm == kSegVector) hipLaunchKernelGGL((joiner_fwd_kernel<false, kSegVector>), grid, dim3(kGemmThreads), 0, s, a, cm0, cm1);
-      else hipLaunchKernelGGL((joiner_fwd_kernel<false, kSegWords>), grid, dim3(kGemmThreads), 0, s, a, cm0, cm1);
+      if (wm == kSegVector)
+        hipLaunchKernelGGL((joiner_fwd_kernel<false, kSegVector>), grid, dim3(nt), 0, s, c, cm0, cm1, ncol, ngemm, hn);
+      else
+        hipLaunchKernelGGL((joiner_fwd_kernel<false, kSegWords>), grid, dim3(nt), 0, s, c, cm0, cm1, ncol, ngemm, hn);
     }
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
   }
   const size_t total = (size_t)a.b.N * a.b.T * a.S;
   {
