@@ -891,6 +891,11 @@ DEV void dl_block(const JoinerArgs& a, int cm0, int cm1, int bx, int by, DlSmem&
   const int ng = ldl / 4;
   const int tpr = dl_threads_per_row(ng);
   const int nrg = kDlThreads / tpr, rg = threadIdx.x / tpr, ct = threadIdx.x - rg * tpr;
+  // a thread's rows are contiguous (rpt of them from rb), so that bf16 can
+  // also write d(logits) transposed for dW straight from registers: per
+  // column, 8 or 16 consecutive rows in one or two 16-byte stores (rows past
+  // the chunk's last row as zeros: dW's 16-byte loads may reach them)
+  const int rpt = kDlRows / nrg, rb = rg * rpt;
   const bool vec = from_head || (V & 3) == 0;
   {
     const int g0 = by * tpr;  // this block's column groups
@@ -898,13 +903,19 @@ DEV void dl_block(const JoinerArgs& a, int cm0, int cm1, int bx, int by, DlSmem&
     const bool gok = g0 + ct < ng;
     float cs[4] = {0.f, 0.f, 0.f, 0.f};
     if (gok) {
-      for (int r0 = rg; r0 < nrows; r0 += kDlInFlight * nrg) {
+      for (int p0 = 0; p0 < rpt; p0 += kDlInFlight) {
+        const int r0 = rb + p0, nk = min(kDlInFlight, rpt - p0);
         float l[kDlInFlight][4];
+        uint32_t tw[4][kDlInFlight / 2];  // bf16 pairs of d, rows r0 .. r0 + nk - 1, per column
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+#pragma unroll
+          for (int k = 0; k < kDlInFlight / 2; ++k) tw[q][k] = 0u;
 #pragma unroll
         for (int k = 0; k < kDlInFlight; ++k) {
-          const int r = r0 + k * nrg;
+          const int r = r0 + k;
           const int4 info = ri[min(r, kDlRows - 1)];
-          const bool ok = r < nrows && info.w >= 0 && c < V;
+          const bool ok = k < nk && r < nrows && info.w >= 0 && c < V;
           const float* src = lg + (ok ? (from_head ? (size_t)(m0 + r) * ldl : (size_t)info.w * V) + c : 0);
           if (ok && vec) {
             const float4 q = *reinterpret_cast<const float4*>(src);
@@ -916,8 +927,8 @@ DEV void dl_block(const JoinerArgs& a, int cm0, int cm1, int bx, int by, DlSmem&
         }
 #pragma unroll
         for (int k = 0; k < kDlInFlight; ++k) {
-          const int r = r0 + k * nrg;
-          if (r >= nrows) break;
+          const int r = r0 + k;
+          if (k >= nk || r >= nrows) break;
           const int4 info = ri[r];
           const float4 x = rx[r];
           const float g = x.y + x.z;
@@ -940,8 +951,19 @@ DEV void dl_block(const JoinerArgs& a, int cm0, int cm1, int bx, int by, DlSmem&
             *reinterpret_cast<uint2*>(dl + o) =
                 make_uint2((uint32_t)f2bf(d[0]) | ((uint32_t)f2bf(d[1]) << 16),
                            (uint32_t)f2bf(d[2]) | ((uint32_t)f2bf(d[3]) << 16));
+#pragma unroll
+            for (int q = 0; q < 4; ++q) tw[q][k >> 1] |= (uint32_t)f2bf(d[q]) << (16 * (k & 1));
           } else {
             *reinterpret_cast<float4*>(dl + o) = make_float4(d[0], d[1], d[2], d[3]);
+          }
+        }
+        if constexpr (BF) {
+          uint16_t* dlT = reinterpret_cast<uint16_t*>(a.dlT) + (size_t)c * a.chunk_rows + (m0 - cm0 + r0);
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            uint4* dst = reinterpret_cast<uint4*>(dlT + (size_t)q * a.chunk_rows);
+            dst[0] = make_uint4(tw[q][0], tw[q][1], tw[q][2], tw[q][3]);
+            if (nk > 8) dst[1] = make_uint4(tw[q][4], tw[q][5], tw[q][6], tw[q][7]);
           }
         }
       }
@@ -1211,40 +1233,6 @@ DEV void dh_tile(const JoinerArgs& a, int cm0, int cm1, int v, int nblocks, int 
             make_uint2((uint32_t)f2bf(hv[0]) | ((uint32_t)f2bf(hv[1]) << 16),
                        (uint32_t)f2bf(hv[2]) | ((uint32_t)f2bf(hv[3]) << 16));
       }
-  }
-}
-
-// ---------------------------------------------------------------------------
-// bf16 d(logits) transposed for the dW contraction: dlT[v][m - cm0] for the
-// chunk's rows, zero for rows past mend up to the 128-row tile end. 64 x 64
-// tiles through LDS; every global access is 16 bytes per thread.
-// ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void joiner_dlt_kernel(JoinerArgs a, int cm0, int cm1) {
-  __shared__ uint16_t tile[64][64 + 8];
-  const int M = a.frame_off[a.b.N] * a.S;
-  const int mend = min(cm1, M);
-  const int r0 = blockIdx.x * 64, c0 = blockIdx.y * 64;  // rows (m - cm0), columns v
-  const uint16_t* dl = reinterpret_cast<const uint16_t*>(a.dl);
-  uint16_t* dlT = reinterpret_cast<uint16_t*>(a.dlT);
-  const int ty = threadIdx.x >> 3, tx = threadIdx.x & 7;
-#pragma unroll
-  for (int h = 0; h < 2; ++h) {
-    const int r = ty + 32 * h;
-    const int c = c0 + tx * 8;
-    uint4 v = make_uint4(0, 0, 0, 0);
-    if (cm0 + r0 + r < mend && c < a.ldl) v = *reinterpret_cast<const uint4*>(dl + (size_t)(r0 + r) * a.ldl + c);
-    *reinterpret_cast<uint4*>(&tile[r][tx * 8]) = v;
-  }
-  __syncthreads();
-#pragma unroll
-  for (int h = 0; h < 2; ++h) {
-    const int c = ty + 32 * h;  // column within the tile: dlT row
-    if (c0 + c >= a.ldl) continue;
-    uint32_t w[4];
-#pragma unroll
-    for (int q = 0; q < 4; ++q)
-      w[q] = (uint32_t)tile[tx * 8 + 2 * q][c] | ((uint32_t)tile[tx * 8 + 2 * q + 1][c] << 16);
-    *reinterpret_cast<uint4*>(dlT + (size_t)(c0 + c) * a.chunk_rows + r0 + tx * 8) = make_uint4(w[0], w[1], w[2], w[3]);
   }
 }
 
@@ -2053,8 +2041,8 @@ static hipError_t launch_bwd_gemms(const JoinerArgs& cur, const JoinerArgs& nxt,
   return hipGetLastError();
 }
 
-// Stored logits: per chunk, d(logits) streamed from them, then dh (which
-// also leaves h for dW), for bf16 the transpose of d(logits), dW, and the
+// Stored logits: per chunk, d(logits) streamed from them (for bf16 also
+// transposed for dW), then dh (which also leaves h for dW), dW, and the
 // chunk's d dec pass (one ring slot).
 static hipError_t launch_joiner_bwd_stored(const JoinerArgs& a, hipStream_t s) {
   const int mmax = a.b.N * a.b.T * a.S;
@@ -2069,12 +2057,6 @@ static hipError_t launch_joiner_bwd_stored(const JoinerArgs& a, hipStream_t s) {
     }
     e = hipGetLastError();
     if (e == hipSuccess) e = launch_bwd_gemms(a, a, 0, 0, cm0, cm1, true, false, true, s);  // dh, leaves h
-    if (e == hipSuccess && a.bf16) {
-      RNNT_PROF(s, "joiner_dlt");
-      const dim3 gt((cm1 - cm0 + 63) / 64, (a.ldl + 63) / 64);
-      hipLaunchKernelGGL(joiner_dlt_kernel, gt, dim3(256), 0, s, a, cm0, cm1);
-      e = hipGetLastError();
-    }
     if (e == hipSuccess) e = launch_bwd_gemms(a, a, 0, 0, cm0, cm1, false, true, false, s);  // dW
     if (e == hipSuccess) e = launch_tail(a, tail_ranges(a, cm0, cm1, cm1 >= mmax), s, cm1 >= mmax ? "joiner_tail" : "joiner_dec");
   }
@@ -2109,8 +2091,9 @@ hipError_t launch_joiner_bwd(const JoinerArgs& a, hipStream_t s) {
   tr.h0 = h_pass(ring_slot(a, 0), lo(0), hi(0));
   if (nch > 1) tr.h1 = h_pass(ring_slot(a, 1), lo(1), hi(1));
   if (a.head && a.head_rows == C) {
-    // chunk 0's logits were kept by the forward: stream them (and, for bf16,
-    // transpose d(logits) for dW) instead of the one recomputation launch
+    // chunk 0's logits were kept by the forward: stream them (for bf16 the
+    // stream also writes d(logits) transposed for dW) instead of the one
+    // recomputation launch
     // the pipeline cannot fill; the stream shares its launch with the first
     // h passes
     const dim3 gdl = dl_grid(hi(0) - lo(0), a.ldl);
@@ -2125,12 +2108,6 @@ hipError_t launch_joiner_bwd(const JoinerArgs& a, hipStream_t s) {
                            (int)gdl.x, (int)gdl.y);
     }
     e = hipGetLastError();
-    if (e == hipSuccess && a.bf16) {
-      RNNT_PROF(s, "joiner_dlt");
-      const dim3 gt((hi(0) - lo(0) + 63) / 64, (a.ldl + 63) / 64);
-      hipLaunchKernelGGL(joiner_dlt_kernel, gt, dim3(256), 0, s, a, lo(0), hi(0));
-      e = hipGetLastError();
-    }
   } else {
     e = launch_tail(a, tr, s, "joiner_h");
     if (e == hipSuccess) e = launch_bwd_gemms(ring_slot(a, 0), ring_slot(a, 0), lo(0), hi(0), 0, 0, false, false, false, s);
