@@ -197,3 +197,8 @@ DEV double wave_sum_d(double v) {
 }
 
 DEV size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// This wave's instruction-issue priority raised to the highest level, for
+// kernels on a step's critical path that share CUs with work on another
+// stream. It orders issue between waves only and changes no result.
+DEV void raise_wave_priority() { __builtin_amdgcn_s_setprio(3); }

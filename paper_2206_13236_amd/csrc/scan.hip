@@ -201,10 +201,8 @@ DEV void beta_frame(double& bt, const FrameIn& f, const ScanSrc& v, int s, int r
 
 // The scan's kernels are the step's critical path while the simple loss's
 // gradients run beside them on another stream: their waves take the highest
-// issue priority, so that a SIMD shared with those contractions issues the
-// recursion's dependent instructions first. Priority only orders issue; it
-// changes no result.
-DEV void raise_wave_priority() { __builtin_amdgcn_s_setprio(3); }
+// issue priority (raise_wave_priority), so that a SIMD shared with those
+// contractions issues the recursion's dependent instructions first.
 
 // Wave w of the grid: chains 4g .. 4g+3 (one per 16-lane row) of chunk c of
 // utterance n. Each chain starts from a unit arrival at slot i of the
